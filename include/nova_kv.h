@@ -1,0 +1,188 @@
+/*
+ * nova_kv.h -- C ABI of the NOVA-KV hot path on MI355X (gfx950).
+ *
+ * NOVA-KV ("Spend Bits Where Queries Look: KV Cache Vector Quantization with
+ * Attention-Preserving Transforms") stores every cached key and value as one
+ * 8-bit codebook index per group of g = 4 transform coefficients, i.e. 2 bits
+ * per element.  This library implements the two calls a serving engine makes
+ * on that cache:
+ *
+ *   nova_kv_encode       append-time write path: transform the new keys and
+ *                        values, pick the nearest codeword of every group, and
+ *                        store the code bytes (paper: Algorithm 1, "Write";
+ *                        Theorem 1 and Corollary 1 for the transforms; Sec.
+ *                        "Calibration": exact Euclidean nearest-neighbour
+ *                        search in the transform domain).
+ *   nova_kv_decode_attn  single-token decode attention read straight from the
+ *                        codes (paper: Algorithm 1, "Attention"; Sec. "Decoding
+ *                        kernel and read path"; Appendix "Attention sinks in the
+ *                        quantized serving path").
+ *
+ * Conventions for every call
+ *   - All tensor pointers are DEVICE pointers owned by the caller; the library
+ *     never allocates, frees or synchronizes inside these calls.  All work is
+ *     enqueued on `hip_stream` (a hipStream_t passed as void*; NULL = default
+ *     stream) and completes asynchronously.
+ *   - Structs are passed by host pointer and read only during the call.
+ *   - Arguments are validated on the host before anything is launched; on any
+ *     error nothing is launched and a status != NOVA_KV_OK is returned, with a
+ *     human-readable detail in nova_kv_last_error() (thread-local).
+ *   - Device-resident values (seq_lens, start_pos, block_table entries) cannot
+ *     be checked without a synchronisation; their preconditions are stated
+ *     per call and are the caller's responsibility.
+ *   - All arrays are dense and row-major in the index order written.
+ */
+#ifndef NOVA_KV_H
+#define NOVA_KV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    NOVA_KV_OK = 0,
+    NOVA_KV_ERR_INVALID_ARG = 1,   /* NULL required pointer, bad shape or count   */
+    NOVA_KV_ERR_UNSUPPORTED = 2,   /* valid but not implemented (g != 4, D, flags) */
+    NOVA_KV_ERR_WORKSPACE = 3,     /* workspace missing or too small               */
+    NOVA_KV_ERR_HIP = 4            /* a HIP runtime call or kernel launch failed   */
+} nova_kv_status;
+
+typedef enum {
+    NOVA_KV_F32 = 0,               /* IEEE fp32                                    */
+    NOVA_KV_BF16 = 1               /* bfloat16, stored as uint16 bit patterns      */
+} nova_kv_dtype;
+
+/*
+ * Per-layer calibration outputs (paper: Algorithm 2 and 3; Sec. "Reported
+ * quantities" lists what is stored per (layer, KV head)).  Hkv = num_kv_heads,
+ * D = head_dim, L = D / group_dim, K = codebook_size.
+ *
+ *   kbar      [Hkv][D]      fp32  key mean k_bar
+ *   t_k       [Hkv][D][D]   fp32  key transform R_K with the grouping folded
+ *                                 into its columns:  r = (k - k_bar) @ t_k
+ *   t_k_inv_t [Hkv][D][D]   fp32  R_K^{-T} (same column order): q' = q @ t_k_inv_t
+ *   t_v       [Hkv][D][D]   fp32  value transform R_V (orthogonal, columns
+ *                                 grouped):  s = v @ t_v,  v_hat = s_hat @ t_v^T
+ *   cb_k      [Hkv][L][K][g] fp16 bit patterns: key codebook of each group
+ *   cb_v      [Hkv][L][K][g] fp16 bit patterns: value codebook of each group
+ *
+ * Group l covers transform coordinates [l*g, (l+1)*g).  Supported: g = 4,
+ * K = 256, D in {64, 128}; flags must be 0 (reserved).
+ */
+typedef struct {
+    int32_t num_kv_heads;
+    int32_t head_dim;
+    int32_t group_dim;
+    int32_t codebook_size;
+    uint32_t flags;
+    const float *kbar;
+    const float *t_k;
+    const float *t_k_inv_t;
+    const float *t_v;
+    const uint16_t *cb_k;
+    const uint16_t *cb_v;
+} nova_kv_params;
+
+/*
+ * Code pool layout (paper: the codes go into a fixed-width paged cache,
+ * Fig. 2b).  One pool for key codes and one for value codes, each
+ *
+ *   uint8 codes[num_blocks][Hkv][block_size][L]
+ *
+ * Token t of sequence b lives in logical block i = t / block_size at row
+ * t % block_size of physical block
+ *   p = block_table ? block_table[b * blocks_per_seq + i] : b * blocks_per_seq + i.
+ *
+ * A contiguous cache is block_table = NULL, blocks_per_seq = 1 and
+ * block_size = the per-sequence capacity (codes[B][Hkv][capacity][L]).
+ * block_table is a DEVICE int32 array [B][blocks_per_seq]; every entry used
+ * must index a physical block of both pools (caller's precondition).
+ */
+typedef struct {
+    int32_t block_size;
+    int32_t blocks_per_seq;
+    const int32_t *block_table;
+} nova_kv_layout;
+
+/*
+ * nova_kv_encode -- append n_new tokens per sequence to the code pools.
+ *
+ * Paper: Algorithm 1 ("Write": cache Q+((k_j - k_bar) R_K)); Theorem 1
+ * (r = (k - k_bar) R_K); Corollary 1 (s = v R_V); Sec. "Calibration"
+ * (nearest codeword, Euclidean metric, transform domain).
+ *
+ *   k, v       [B][n_new][Hkv][D] device, dtype in_dtype (F32 or BF16)
+ *   start_pos  [B] int32 device: position of the first new token of each
+ *              sequence; precondition start_pos[b] + n_new <= block_size *
+ *              blocks_per_seq.
+ *   k_codes, v_codes  code pools (see nova_kv_layout), written at positions
+ *              start_pos[b] .. start_pos[b] + n_new - 1; nothing else is touched.
+ *
+ * For every (b, token, KV head, group l) the stored byte is the smallest index
+ * c minimising sum_i (u_i - cb[l][c][i])^2, u the group's coefficients; the
+ * transform and the distances are evaluated in fp64.
+ * batch == 0 or n_new == 0 is a valid no-op.
+ */
+nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *layout,
+                              const void *k, const void *v, nova_kv_dtype in_dtype,
+                              int32_t batch, int32_t n_new, const int32_t *start_pos,
+                              uint8_t *k_codes, uint8_t *v_codes, void *hip_stream);
+
+/*
+ * Bytes of device workspace nova_kv_decode_attn needs for this shape (split
+ * partials, pre-transformed queries, counters).  Returns 0 on invalid input.
+ */
+size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch,
+                                      int32_t num_q_heads, int32_t max_seq_len);
+
+/*
+ * nova_kv_decode_attn -- one decode step of attention over the code pools.
+ *
+ * Paper: Algorithm 1 ("Attention": softmax(Q R_K^{-T} Q-(K_hat)^T / sqrt(d)));
+ * Sec. "Decoding kernel and read path" (q R_K^{-T} formed once per step, one
+ * codeword lookup per group, k_bar dropped by Lemma S1, two-stage split-KV
+ * decode); Corollary 1 (v_hat = s_hat R_V^T); Appendix "Attention sinks"
+ * (sink added once after the split combine, shifted by -(q . k_bar) * scale).
+ *
+ *   q          [B][Hq][D] device, dtype q_dtype (F32 or BF16); query head h
+ *              reads KV head h / (Hq / Hkv).
+ *   seq_lens   [B] int32 device: cached tokens of each sequence (the current
+ *              token already appended); precondition 0 <= seq_lens[b] <= max_seq_len.
+ *   max_seq_len  host upper bound of seq_lens; must not exceed the layout's
+ *              per-sequence capacity block_size * blocks_per_seq.
+ *   window     0 = attend to all seq_lens[b] tokens; W > 0 = the last W only.
+ *   sinks      [Hq] fp32 device learned sink logits (scaled-logit units, no
+ *              value vector), or NULL.
+ *   softmax_scale  logit scale; 0 selects 1/sqrt(D).
+ *   out        [B][Hq][D] fp32 device:
+ *                out = sum_t p_t v_hat_t,  p = softmax({z_t} U {sink}),
+ *                z_t = q . k_hat_t * scale,  k_hat_t = r_hat_t t_k_inv_t^T + k_bar,
+ *                v_hat_t = s_hat_t t_v^T.
+ *              A row with no attended token and no sink is written as zeros.
+ *   workspace  device scratch of at least nova_kv_decode_workspace_bytes(...)
+ *              bytes, 256-byte aligned; contents need no initialisation.
+ * batch == 0 is a valid no-op.
+ */
+nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
+                                   const void *q, nova_kv_dtype q_dtype,
+                                   int32_t batch, int32_t num_q_heads,
+                                   const uint8_t *k_codes, const uint8_t *v_codes,
+                                   const int32_t *seq_lens, int32_t max_seq_len,
+                                   int32_t window, const float *sinks, float softmax_scale,
+                                   float *out, void *workspace, size_t workspace_bytes,
+                                   void *hip_stream);
+
+/* Static description of a status code. */
+const char *nova_kv_status_string(nova_kv_status s);
+
+/* Detail of the last failing call on this thread ("" if none). */
+const char *nova_kv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NOVA_KV_H */

@@ -1,0 +1,9 @@
+"""NOVA-KV hot path for MI355X (gfx950): 2-bit VQ KV-cache encode and decode attention.
+
+The compute lives in ``libnovakv.so`` (hand-written HIP, C ABI in
+``include/nova_kv.h``); this package is its Python binding.
+"""
+
+from .api import (CacheLayout, NovaKVParams, code_pool_shape, decode_attn,  # noqa: F401
+                  decode_workspace_bytes, encode)
+from ._native import NovaKVError  # noqa: F401

@@ -1,0 +1,99 @@
+"""ctypes view of libnovakv.so (the C ABI declared in include/nova_kv.h).
+
+Loading fails loudly when the library has not been built: there is no
+fallback implementation of any call.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libnovakv.so")
+
+NOVA_KV_OK = 0
+NOVA_KV_ERR_INVALID_ARG = 1
+NOVA_KV_ERR_UNSUPPORTED = 2
+NOVA_KV_ERR_WORKSPACE = 3
+NOVA_KV_ERR_HIP = 4
+
+NOVA_KV_F32 = 0
+NOVA_KV_BF16 = 1
+
+EXPORTED = (
+    "nova_kv_encode",
+    "nova_kv_decode_workspace_bytes",
+    "nova_kv_decode_attn",
+    "nova_kv_status_string",
+    "nova_kv_last_error",
+)
+
+
+class Params(ctypes.Structure):
+    _fields_ = [
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("group_dim", ctypes.c_int32),
+        ("codebook_size", ctypes.c_int32),
+        ("flags", ctypes.c_uint32),
+        ("kbar", ctypes.c_void_p),
+        ("t_k", ctypes.c_void_p),
+        ("t_k_inv_t", ctypes.c_void_p),
+        ("t_v", ctypes.c_void_p),
+        ("cb_k", ctypes.c_void_p),
+        ("cb_v", ctypes.c_void_p),
+    ]
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [
+        ("block_size", ctypes.c_int32),
+        ("blocks_per_seq", ctypes.c_int32),
+        ("block_table", ctypes.c_void_p),
+    ]
+
+
+class NovaKVError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        super().__init__(f"nova_kv status {status}: {detail}")
+        self.status = status
+        self.detail = detail
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m "
+                               "paper_2608_04074_amd.build` (or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.nova_kv_encode.restype = ctypes.c_int
+        L.nova_kv_encode.argtypes = [P(Params), P(Layout), ctypes.c_void_p, ctypes.c_void_p,
+                                     ctypes.c_int, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        L.nova_kv_decode_workspace_bytes.restype = ctypes.c_size_t
+        L.nova_kv_decode_workspace_bytes.argtypes = [P(Params), ctypes.c_int32, ctypes.c_int32,
+                                                     ctypes.c_int32]
+        L.nova_kv_decode_attn.restype = ctypes.c_int
+        L.nova_kv_decode_attn.argtypes = [P(Params), P(Layout), ctypes.c_void_p, ctypes.c_int,
+                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                          ctypes.c_int32, ctypes.c_void_p, ctypes.c_float,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                          ctypes.c_void_p]
+        L.nova_kv_status_string.restype = ctypes.c_char_p
+        L.nova_kv_status_string.argtypes = [ctypes.c_int]
+        L.nova_kv_last_error.restype = ctypes.c_char_p
+        L.nova_kv_last_error.argtypes = []
+        _lib = L
+    return _lib
+
+
+def check(status: int) -> None:
+    if status != NOVA_KV_OK:
+        raise NovaKVError(status, lib().nova_kv_last_error().decode())

@@ -1,0 +1,169 @@
+"""Python binding of the NOVA-KV C ABI: marshals torch device tensors into the calls.
+
+Every step of the hot path runs in the HIP kernels of libnovakv.so; this module
+only checks dtypes/shapes/devices, hands over raw device pointers and the
+current HIP stream, and raises on a non-OK status.
+"""
+
+from __future__ import annotations
+
+import ctypes
+from typing import Optional
+
+import torch
+
+from . import _native as nat
+
+__all__ = ["NovaKVParams", "CacheLayout", "encode", "decode_attn", "decode_workspace_bytes",
+           "code_pool_shape"]
+
+
+def _stream_ptr(stream: Optional[torch.cuda.Stream]) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def _require(t: torch.Tensor, name: str, dtypes, numel: Optional[int] = None) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {numel}")
+
+
+class NovaKVParams:
+    """Per-layer calibration outputs resident on the device (see nova_kv_params)."""
+
+    def __init__(self, kbar, t_k, t_k_inv_t, t_v, cb_k, cb_v, group_dim: int = 4,
+                 codebook_size: int = 256):
+        hkv, d = kbar.shape
+        L = d // group_dim
+        _require(kbar, "kbar", (torch.float32,), hkv * d)
+        for name, t in (("t_k", t_k), ("t_k_inv_t", t_k_inv_t), ("t_v", t_v)):
+            _require(t, name, (torch.float32,), hkv * d * d)
+        for name, t in (("cb_k", cb_k), ("cb_v", cb_v)):
+            _require(t, name, (torch.float16,), hkv * L * codebook_size * group_dim)
+        self.num_kv_heads, self.head_dim = hkv, d
+        self.group_dim, self.codebook_size = group_dim, codebook_size
+        self.kbar, self.t_k, self.t_k_inv_t, self.t_v = kbar, t_k, t_k_inv_t, t_v
+        self.cb_k, self.cb_v = cb_k, cb_v
+        self._c = nat.Params(hkv, d, group_dim, codebook_size, 0, kbar.data_ptr(), t_k.data_ptr(),
+                             t_k_inv_t.data_ptr(), t_v.data_ptr(), cb_k.data_ptr(),
+                             cb_v.data_ptr())
+
+    @property
+    def groups(self) -> int:
+        return self.head_dim // self.group_dim
+
+    @classmethod
+    def from_arrays(cls, arrays: dict, device="cuda") -> "NovaKVParams":
+        """From host arrays: kbar/t_k/t_k_inv_t/t_v float32, cb_k/cb_v float16 ([Hkv][...])."""
+        f32 = {k: torch.as_tensor(arrays[k]).to(torch.float32).contiguous().to(device)
+               for k in ("kbar", "t_k", "t_k_inv_t", "t_v")}
+        f16 = {k: torch.as_tensor(arrays[k]).to(torch.float16).contiguous().to(device)
+               for k in ("cb_k", "cb_v")}
+        return cls(**f32, **f16)
+
+    @property
+    def c(self) -> nat.Params:
+        return self._c
+
+
+class CacheLayout:
+    """Code-pool layout (see nova_kv_layout); ``block_table`` is a device int32 [B][blocks_per_seq]."""
+
+    def __init__(self, block_size: int, blocks_per_seq: int = 1,
+                 block_table: Optional[torch.Tensor] = None):
+        if block_table is not None:
+            _require(block_table, "block_table", (torch.int32,))
+        self.block_size, self.blocks_per_seq, self.block_table = block_size, blocks_per_seq, block_table
+        self._c = nat.Layout(block_size, blocks_per_seq,
+                             block_table.data_ptr() if block_table is not None else None)
+
+    @classmethod
+    def contiguous(cls, capacity: int) -> "CacheLayout":
+        return cls(capacity, 1, None)
+
+    @property
+    def capacity(self) -> int:
+        return self.block_size * self.blocks_per_seq
+
+    @property
+    def c(self) -> nat.Layout:
+        return self._c
+
+
+def code_pool_shape(params: NovaKVParams, layout: CacheLayout, batch: int, num_blocks=None):
+    """Shape of one code pool: [num_blocks][Hkv][block_size][L]."""
+    nb = batch * layout.blocks_per_seq if num_blocks is None else num_blocks
+    return (nb, params.num_kv_heads, layout.block_size, params.groups)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return nat.NOVA_KV_F32
+    if t.dtype == torch.bfloat16:
+        return nat.NOVA_KV_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v: torch.Tensor,
+           start_pos: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
+           stream: Optional[torch.cuda.Stream] = None) -> None:
+    """nova_kv_encode: k, v [B][n_new][Hkv][D] (fp32 or bf16), start_pos int32 [B]."""
+    if k.dim() != 4:
+        raise ValueError("k must be [B][n_new][Hkv][D]")
+    b, n_new, hkv, d = k.shape
+    if hkv != params.num_kv_heads or d != params.head_dim:
+        raise ValueError("k does not match the parameters' head count / head_dim")
+    _require(k, "k", (torch.float32, torch.bfloat16))
+    _require(v, "v", (k.dtype,), k.numel())
+    _require(start_pos, "start_pos", (torch.int32,), b)
+    _require(k_codes, "k_codes", (torch.uint8,))
+    _require(v_codes, "v_codes", (torch.uint8,), k_codes.numel())
+    nat.check(nat.lib().nova_kv_encode(
+        ctypes.byref(params.c), ctypes.byref(layout.c), k.data_ptr(), v.data_ptr(), _dtype_code(k),
+        b, n_new, start_pos.data_ptr(), k_codes.data_ptr(), v_codes.data_ptr(),
+        _stream_ptr(stream)))
+
+
+def decode_workspace_bytes(params: NovaKVParams, batch: int, num_q_heads: int,
+                           max_seq_len: int) -> int:
+    return int(nat.lib().nova_kv_decode_workspace_bytes(ctypes.byref(params.c), batch,
+                                                        num_q_heads, max_seq_len))
+
+
+def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
+                k_codes: torch.Tensor, v_codes: torch.Tensor, seq_lens: torch.Tensor,
+                max_seq_len: int, window: int = 0, sinks: Optional[torch.Tensor] = None,
+                softmax_scale: float = 0.0, out: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None,
+                stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """nova_kv_decode_attn: q [B][Hq][D] (fp32 or bf16) -> out [B][Hq][D] fp32."""
+    if q.dim() != 3 or q.shape[2] != params.head_dim:
+        raise ValueError("q must be [B][Hq][D]")
+    b, hq, d = q.shape
+    _require(q, "q", (torch.float32, torch.bfloat16))
+    _require(k_codes, "k_codes", (torch.uint8,))
+    _require(v_codes, "v_codes", (torch.uint8,), k_codes.numel())
+    _require(seq_lens, "seq_lens", (torch.int32,), b)
+    if sinks is not None:
+        _require(sinks, "sinks", (torch.float32,), hq)
+    if out is None:
+        out = torch.empty((b, hq, d), dtype=torch.float32, device=q.device)
+    _require(out, "out", (torch.float32,), b * hq * d)
+    need = decode_workspace_bytes(params, b, hq, max_seq_len) if b > 0 else 0
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    _require(workspace, "workspace", (torch.uint8,))
+    nat.check(nat.lib().nova_kv_decode_attn(
+        ctypes.byref(params.c), ctypes.byref(layout.c), q.data_ptr(), _dtype_code(q), b, hq,
+        k_codes.data_ptr(), v_codes.data_ptr(), seq_lens.data_ptr(), max_seq_len, window,
+        sinks.data_ptr() if sinks is not None else None, float(softmax_scale), out.data_ptr(),
+        workspace.data_ptr(), workspace.numel(), _stream_ptr(stream)))
+    return out

@@ -1,0 +1,206 @@
+// C ABI of libnovakv: host-side validation, workspace planning and dispatch.
+// Every check runs before any HIP call, so an invalid call launches nothing.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+
+#include "../../include/nova_kv.h"
+#include "nova_kv_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+nova_kv_status fail(nova_kv_status s, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+
+nova_kv_status fail(nova_kv_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+nova_kv_status ok() {
+  g_last_error.clear();
+  return NOVA_KV_OK;
+}
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+nova_kv_status check_params(const nova_kv_params *p, bool need_encode, bool need_decode) {
+  if (!p) return fail(NOVA_KV_ERR_INVALID_ARG, "params is NULL");
+  if (p->num_kv_heads <= 0) return fail(NOVA_KV_ERR_INVALID_ARG, "num_kv_heads must be > 0");
+  if (p->group_dim <= 0 || p->head_dim <= 0 || p->head_dim % p->group_dim != 0)
+    return fail(NOVA_KV_ERR_INVALID_ARG, "head_dim (%d) must be a positive multiple of group_dim (%d)",
+                p->head_dim, p->group_dim);
+  if (p->codebook_size <= 0) return fail(NOVA_KV_ERR_INVALID_ARG, "codebook_size must be > 0");
+  if (p->group_dim != novakv::kGroupDim)
+    return fail(NOVA_KV_ERR_UNSUPPORTED, "group_dim %d unsupported (only 4)", p->group_dim);
+  if (p->codebook_size != novakv::kCodebookSize)
+    return fail(NOVA_KV_ERR_UNSUPPORTED, "codebook_size %d unsupported (only 256)", p->codebook_size);
+  if (p->head_dim != 64 && p->head_dim != 128)
+    return fail(NOVA_KV_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", p->head_dim);
+  if (p->flags != 0) return fail(NOVA_KV_ERR_UNSUPPORTED, "flags 0x%x unsupported (must be 0)", p->flags);
+  if (!p->kbar || !p->cb_k || !p->cb_v) return fail(NOVA_KV_ERR_INVALID_ARG, "kbar/cb_k/cb_v is NULL");
+  if (!aligned(p->cb_k, 16) || !aligned(p->cb_v, 16))
+    return fail(NOVA_KV_ERR_INVALID_ARG, "codebooks must be 16-byte aligned");
+  if (need_encode && (!p->t_k || !p->t_v)) return fail(NOVA_KV_ERR_INVALID_ARG, "t_k/t_v is NULL");
+  if (need_decode && (!p->t_k_inv_t || !p->t_v))
+    return fail(NOVA_KV_ERR_INVALID_ARG, "t_k_inv_t/t_v is NULL");
+  return NOVA_KV_OK;
+}
+
+nova_kv_status check_layout(const nova_kv_layout *lay) {
+  if (!lay) return fail(NOVA_KV_ERR_INVALID_ARG, "layout is NULL");
+  if (lay->block_size <= 0 || lay->blocks_per_seq <= 0)
+    return fail(NOVA_KV_ERR_INVALID_ARG, "block_size and blocks_per_seq must be > 0");
+  if (static_cast<long long>(lay->block_size) * lay->blocks_per_seq > (1LL << 30))
+    return fail(NOVA_KV_ERR_INVALID_ARG, "per-sequence capacity too large");
+  return NOVA_KV_OK;
+}
+
+novakv::CacheLayout to_layout(const nova_kv_layout *lay) {
+  return novakv::CacheLayout{lay->block_size, lay->blocks_per_seq, lay->block_table};
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *nova_kv_status_string(nova_kv_status s) {
+  switch (s) {
+    case NOVA_KV_OK: return "ok";
+    case NOVA_KV_ERR_INVALID_ARG: return "invalid argument";
+    case NOVA_KV_ERR_UNSUPPORTED: return "unsupported configuration";
+    case NOVA_KV_ERR_WORKSPACE: return "workspace missing or too small";
+    case NOVA_KV_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char *nova_kv_last_error(void) { return g_last_error.c_str(); }
+
+nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *layout,
+                              const void *k, const void *v, nova_kv_dtype in_dtype,
+                              int32_t batch, int32_t n_new, const int32_t *start_pos,
+                              uint8_t *k_codes, uint8_t *v_codes, void *hip_stream) {
+  nova_kv_status st = check_params(p, true, false);
+  if (st != NOVA_KV_OK) return st;
+  if ((st = check_layout(layout)) != NOVA_KV_OK) return st;
+  if (batch < 0 || n_new < 0) return fail(NOVA_KV_ERR_INVALID_ARG, "batch and n_new must be >= 0");
+  if (in_dtype != NOVA_KV_F32 && in_dtype != NOVA_KV_BF16)
+    return fail(NOVA_KV_ERR_INVALID_ARG, "in_dtype must be NOVA_KV_F32 or NOVA_KV_BF16");
+  if (batch > 65535) return fail(NOVA_KV_ERR_INVALID_ARG, "batch > 65535");
+  if (static_cast<long long>(n_new) > static_cast<long long>(layout->block_size) * layout->blocks_per_seq)
+    return fail(NOVA_KV_ERR_INVALID_ARG, "n_new exceeds the per-sequence capacity");
+  if (batch == 0 || n_new == 0) return ok();
+  if (!k || !v || !start_pos || !k_codes || !v_codes)
+    return fail(NOVA_KV_ERR_INVALID_ARG, "k, v, start_pos, k_codes or v_codes is NULL");
+
+  novakv::EncodeArgs a{};
+  a.batch = batch;
+  a.n_new = n_new;
+  a.num_kv_heads = p->num_kv_heads;
+  a.head_dim = p->head_dim;
+  a.kbar = p->kbar;
+  a.t_k = p->t_k;
+  a.t_v = p->t_v;
+  a.cb_k = p->cb_k;
+  a.cb_v = p->cb_v;
+  a.layout = to_layout(layout);
+  a.k = k;
+  a.v = v;
+  a.in_bf16 = in_dtype == NOVA_KV_BF16;
+  a.start_pos = start_pos;
+  a.k_codes = k_codes;
+  a.v_codes = v_codes;
+  hipError_t e = novakv::launch_encode(a, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "encode launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch, int32_t num_q_heads,
+                                      int32_t max_seq_len) {
+  if (!p || batch <= 0 || num_q_heads <= 0 || max_seq_len <= 0 || p->num_kv_heads <= 0 ||
+      p->head_dim <= 0)
+    return 0;
+  return novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len).total;
+}
+
+nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
+                                   const void *q, nova_kv_dtype q_dtype, int32_t batch,
+                                   int32_t num_q_heads, const uint8_t *k_codes,
+                                   const uint8_t *v_codes, const int32_t *seq_lens,
+                                   int32_t max_seq_len, int32_t window, const float *sinks,
+                                   float softmax_scale, float *out, void *workspace,
+                                   size_t workspace_bytes, void *hip_stream) {
+  nova_kv_status st = check_params(p, false, true);
+  if (st != NOVA_KV_OK) return st;
+  if ((st = check_layout(layout)) != NOVA_KV_OK) return st;
+  if (batch < 0) return fail(NOVA_KV_ERR_INVALID_ARG, "batch must be >= 0");
+  if (batch > 65535) return fail(NOVA_KV_ERR_INVALID_ARG, "batch > 65535");
+  if (num_q_heads <= 0 || num_q_heads % p->num_kv_heads != 0)
+    return fail(NOVA_KV_ERR_INVALID_ARG, "num_q_heads (%d) must be a positive multiple of num_kv_heads (%d)",
+                num_q_heads, p->num_kv_heads);
+  if (num_q_heads / p->num_kv_heads > novakv::kMaxGqa)
+    return fail(NOVA_KV_ERR_UNSUPPORTED, "more than %d query heads per KV head", novakv::kMaxGqa);
+  if (max_seq_len <= 0) return fail(NOVA_KV_ERR_INVALID_ARG, "max_seq_len must be > 0");
+  if (static_cast<long long>(max_seq_len) > static_cast<long long>(layout->block_size) * layout->blocks_per_seq)
+    return fail(NOVA_KV_ERR_INVALID_ARG, "max_seq_len exceeds the per-sequence capacity");
+  if (window < 0) return fail(NOVA_KV_ERR_INVALID_ARG, "window must be >= 0");
+  if (q_dtype != NOVA_KV_F32 && q_dtype != NOVA_KV_BF16)
+    return fail(NOVA_KV_ERR_INVALID_ARG, "q_dtype must be NOVA_KV_F32 or NOVA_KV_BF16");
+  if (!(softmax_scale >= 0.f)) return fail(NOVA_KV_ERR_INVALID_ARG, "softmax_scale must be >= 0");
+  if (batch == 0) return ok();
+  if (!q || !k_codes || !v_codes || !seq_lens || !out)
+    return fail(NOVA_KV_ERR_INVALID_ARG, "q, k_codes, v_codes, seq_lens or out is NULL");
+  if (!aligned(k_codes, 16) || !aligned(v_codes, 16))
+    return fail(NOVA_KV_ERR_INVALID_ARG, "code pools must be 16-byte aligned");
+  const novakv::DecodePlan plan =
+      novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len);
+  if (!workspace || workspace_bytes < plan.total)
+    return fail(NOVA_KV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
+                workspace ? workspace_bytes : static_cast<size_t>(0));
+  if (!aligned(workspace, 256)) return fail(NOVA_KV_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+
+  novakv::DecodeArgs a{};
+  a.batch = batch;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = p->num_kv_heads;
+  a.head_dim = p->head_dim;
+  a.gqa = num_q_heads / p->num_kv_heads;
+  a.kbar = p->kbar;
+  a.t_k_inv_t = p->t_k_inv_t;
+  a.t_v = p->t_v;
+  a.cb_k = p->cb_k;
+  a.cb_v = p->cb_v;
+  a.layout = to_layout(layout);
+  a.q = q;
+  a.q_bf16 = q_dtype == NOVA_KV_BF16;
+  a.k_codes = k_codes;
+  a.v_codes = v_codes;
+  a.seq_lens = seq_lens;
+  a.max_seq_len = max_seq_len;
+  a.window = window;
+  a.sinks = sinks;
+  a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf(static_cast<float>(p->head_dim));
+  a.out = out;
+  char *ws = static_cast<char *>(workspace);
+  a.qp = reinterpret_cast<float *>(ws + plan.off_qp);
+  a.sinkp = reinterpret_cast<float *>(ws + plan.off_sinkp);
+  a.part_ml = reinterpret_cast<float *>(ws + plan.off_ml);
+  a.part_acc = reinterpret_cast<float *>(ws + plan.off_acc);
+  a.n_split = plan.n_split;
+  a.chunk = plan.chunk;
+  hipError_t e = novakv::launch_decode(a, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

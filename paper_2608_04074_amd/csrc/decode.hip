@@ -1,0 +1,275 @@
+// Decode attention over the 2-bit VQ cache: query pre-transform, split-context
+// stage 1 (codebook gather, online softmax, transform-domain value
+// accumulation) and split combine with one inverse value transform per head.
+//
+// Paper: Algorithm 1 (attention step), Sec. "Decoding kernel and read path"
+// (q R_K^{-T} once per step, per-group codeword lookup, k_bar dropped by
+// Lemma S1, two-stage split-KV decode), Corollary 1 (v_hat = s_hat R_V^T) and
+// the sinks appendix (sink added once after the combine, shifted by
+// -(q . k_bar) * scale).
+#include <math.h>
+
+#include "nova_kv_internal.h"
+
+namespace novakv {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+// q'[b][h] = (q[b][h] @ t_k_inv_t[kv]) * scale and the shifted sink logit.
+template <int D>
+__global__ void __launch_bounds__(D) decode_prologue(DecodeArgs a) {
+  const int bh = blockIdx.x;
+  const int h = bh % a.num_q_heads;
+  const int kv = h / a.gqa;
+  const int tid = threadIdx.x;
+  __shared__ float qsh[D];
+  __shared__ float red[D / 64];
+  float qv;
+  if (a.q_bf16)
+    qv = bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[static_cast<size_t>(bh) * D + tid]);
+  else
+    qv = static_cast<const float *>(a.q)[static_cast<size_t>(bh) * D + tid];
+  qsh[tid] = qv;
+  float dotk = wave_sum(qv * a.kbar[kv * D + tid]);
+  if ((tid & 63) == 0) red[tid >> 6] = dotk;
+  __syncthreads();
+  const float *tk = a.t_k_inv_t + static_cast<size_t>(kv) * D * D;
+  float acc = 0.f;
+  for (int d = 0; d < D; ++d) acc = fmaf(qsh[d], tk[d * D + tid], acc);
+  a.qp[static_cast<size_t>(bh) * D + tid] = acc * a.scale;
+  if (tid == 0) {
+    float s = 0.f;
+    for (int w = 0; w < D / 64; ++w) s += red[w];
+    a.sinkp[bh] = a.sinks ? a.sinks[h] - s * a.scale : -INFINITY;
+  }
+}
+
+// Stage 1: one workgroup per (split, KV head, sequence); one token per thread
+// for the scores, one transform-domain coordinate per thread for the values.
+template <int D>
+__global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
+  constexpr int L = D / kGroupDim;
+  constexpr int CB = L * kCodebookSize * kGroupDim;  // halves per side
+  __shared__ __attribute__((aligned(16))) uint16_t cbk[CB];
+  __shared__ __attribute__((aligned(16))) uint16_t cbv[CB];
+  __shared__ float qs[kMaxGqa][D];
+  __shared__ float ps[kThreads][kMaxGqa];
+  __shared__ __attribute__((aligned(16))) uint8_t vcodes[kThreads][L];
+  __shared__ float red[kWaves][kMaxGqa];
+
+  const int split = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int G = a.gqa;
+
+  {
+    const uint4 *sk = reinterpret_cast<const uint4 *>(a.cb_k + static_cast<size_t>(kv) * CB);
+    const uint4 *sv = reinterpret_cast<const uint4 *>(a.cb_v + static_cast<size_t>(kv) * CB);
+    uint4 *dk = reinterpret_cast<uint4 *>(cbk);
+    uint4 *dv = reinterpret_cast<uint4 *>(cbv);
+    for (int i = tid; i < CB * 2 / 16; i += kThreads) {
+      dk[i] = sk[i];
+      dv[i] = sv[i];
+    }
+    for (int i = tid; i < G * D; i += kThreads)
+      qs[i / D][i % D] =
+          a.qp[(static_cast<size_t>(b) * a.num_q_heads + kv * G + i / D) * D + (i % D)];
+  }
+
+  const int S = a.seq_lens[b];
+  const int lo = a.window > 0 ? max(0, S - a.window) : 0;
+  const int t0 = max(lo, split * a.chunk);
+  const int t1 = min(S, (split + 1) * a.chunk);
+
+  float m[kMaxGqa], l[kMaxGqa], acc[kMaxGqa];
+#pragma unroll
+  for (int h = 0; h < kMaxGqa; ++h) {
+    m[h] = -INFINITY;
+    l[h] = 0.f;
+    acc[h] = 0.f;
+  }
+  __syncthreads();
+
+  const int wave = tid >> 6, lane = tid & 63;
+  for (int ts = t0; ts < t1; ts += kThreads) {
+    const int t = ts + tid;
+    const bool valid = t < t1;
+    float z[kMaxGqa];
+#pragma unroll
+    for (int h = 0; h < kMaxGqa; ++h) z[h] = valid ? 0.f : -INFINITY;
+    if (valid) {
+      const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, t);
+      const uint8_t *kc = a.k_codes + off;
+      const uint8_t *vc = a.v_codes + off;
+      for (int g0 = 0; g0 < L; g0 += 16) {
+        uint4 w = *reinterpret_cast<const uint4 *>(kc + g0);
+        *reinterpret_cast<uint4 *>(&vcodes[tid][g0]) = *reinterpret_cast<const uint4 *>(vc + g0);
+        const uint32_t words[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int ell = g0 + j;
+          const int c = (words[j >> 2] >> (8 * (j & 3))) & 0xff;
+          const uint16_t *cw = &cbk[(ell * kCodebookSize + c) * kGroupDim];
+          const float f0 = half_bits_to_float(cw[0]);
+          const float f1 = half_bits_to_float(cw[1]);
+          const float f2 = half_bits_to_float(cw[2]);
+          const float f3 = half_bits_to_float(cw[3]);
+#pragma unroll
+          for (int h = 0; h < kMaxGqa; ++h) {
+            if (h < G) {
+              const float *qh = &qs[h][ell * kGroupDim];
+              z[h] = fmaf(qh[0], f0, fmaf(qh[1], f1, fmaf(qh[2], f2, fmaf(qh[3], f3, z[h]))));
+            }
+          }
+        }
+      }
+    }
+    // tile max per head
+#pragma unroll
+    for (int h = 0; h < kMaxGqa; ++h) {
+      if (h < G) {
+        const float wm = wave_max(z[h]);
+        if (lane == 0) red[wave][h] = wm;
+      }
+    }
+    __syncthreads();
+    float mnew[kMaxGqa], alpha[kMaxGqa];
+#pragma unroll
+    for (int h = 0; h < kMaxGqa; ++h) {
+      if (h < G) {
+        float tm = red[0][h];
+        for (int w = 1; w < kWaves; ++w) tm = fmaxf(tm, red[w][h]);
+        mnew[h] = fmaxf(m[h], tm);
+        alpha[h] = (m[h] == -INFINITY) ? 0.f : __expf(m[h] - mnew[h]);
+        ps[tid][h] = valid ? __expf(z[h] - mnew[h]) : 0.f;
+      }
+    }
+    __syncthreads();  // red reused below; ps and vcodes complete
+#pragma unroll
+    for (int h = 0; h < kMaxGqa; ++h) {
+      if (h < G) {
+        const float ws = wave_sum(ps[tid][h]);
+        if (lane == 0) red[wave][h] = ws;
+      }
+    }
+    if (tid < D) {
+      const int ell = tid >> 2, i = tid & 3;
+      const int n = min(kThreads, t1 - ts);
+#pragma unroll
+      for (int h = 0; h < kMaxGqa; ++h) acc[h] *= (h < G) ? alpha[h] : 0.f;
+      for (int j = 0; j < n; ++j) {
+        const int c = vcodes[j][ell];
+        const float f = half_bits_to_float(cbv[(ell * kCodebookSize + c) * kGroupDim + i]);
+#pragma unroll
+        for (int h = 0; h < kMaxGqa; ++h)
+          if (h < G) acc[h] = fmaf(ps[j][h], f, acc[h]);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < kMaxGqa; ++h) {
+      if (h < G) {
+        float tsum = 0.f;
+        for (int w = 0; w < kWaves; ++w) tsum += red[w][h];
+        l[h] = l[h] * alpha[h] + tsum;
+        m[h] = mnew[h];
+      }
+    }
+    __syncthreads();  // red and ps free for the next tile
+  }
+
+  const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
+  for (int h = 0; h < G; ++h) {
+    const size_t r = (row0 + h) * a.n_split + split;
+    if (tid < D) a.part_acc[r * D + tid] = acc[h];
+    if (tid == 0) {
+      a.part_ml[2 * r] = m[h];
+      a.part_ml[2 * r + 1] = l[h];
+    }
+  }
+}
+
+// Stage 2: log-sum-exp merge of the splits, sink once, divide, then v = s t_v^T.
+template <int D>
+__global__ void __launch_bounds__(D) decode_combine(DecodeArgs a) {
+  const int bh = blockIdx.x;
+  const int h = bh % a.num_q_heads;
+  const int kv = h / a.gqa;
+  const int tid = threadIdx.x;
+  __shared__ float sh[D];
+  const float *ml = a.part_ml + static_cast<size_t>(bh) * a.n_split * 2;
+  const float *pa = a.part_acc + static_cast<size_t>(bh) * a.n_split * D;
+  const float sink = a.sinkp[bh];
+  float big = sink;
+  for (int s = 0; s < a.n_split; ++s) big = fmaxf(big, ml[2 * s]);
+  float den = 0.f, num = 0.f;
+  if (big != -INFINITY) {
+    for (int s = 0; s < a.n_split; ++s) {
+      const float ms = ml[2 * s];
+      const float w = (ms == -INFINITY) ? 0.f : __expf(ms - big);
+      den = fmaf(w, ml[2 * s + 1], den);
+      num = fmaf(w, pa[static_cast<size_t>(s) * D + tid], num);
+    }
+    if (sink != -INFINITY) den += __expf(sink - big);
+  }
+  sh[tid] = (den > 0.f) ? num / den : 0.f;
+  __syncthreads();
+  const float *tv = a.t_v + static_cast<size_t>(kv) * D * D + static_cast<size_t>(tid) * D;
+  float o = 0.f;
+  for (int j = 0; j < D; ++j) o = fmaf(sh[j], tv[j], o);
+  a.out[static_cast<size_t>(bh) * D + tid] = o;
+}
+
+template <int D>
+hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
+  const int rows = a.batch * a.num_q_heads;
+  decode_prologue<D><<<dim3(rows), dim3(D), 0, stream>>>(a);
+  decode_stage1_v0<D><<<dim3(a.n_split, a.num_kv_heads, a.batch), dim3(kThreads), 0, stream>>>(a);
+  decode_combine<D><<<dim3(rows), dim3(D), 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_dim,
+                       int max_seq_len) {
+  DecodePlan p{};
+  int chunk = 1024;
+  auto splits = [&](int c) { return (max_seq_len + c - 1) / c; };
+  while (chunk > 64 && static_cast<long long>(batch) * num_kv_heads * splits(chunk) < 2048)
+    chunk /= 2;
+  p.chunk = chunk;
+  p.n_split = splits(chunk);
+  auto align = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
+  const size_t rows = static_cast<size_t>(batch) * num_q_heads;
+  p.off_qp = 0;
+  p.off_sinkp = align(p.off_qp + rows * head_dim * sizeof(float));
+  p.off_ml = align(p.off_sinkp + rows * sizeof(float));
+  p.off_acc = align(p.off_ml + rows * p.n_split * 2 * sizeof(float));
+  p.total = align(p.off_acc + rows * p.n_split * head_dim * sizeof(float));
+  return p;
+}
+
+hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream) {
+  switch (a.head_dim) {
+    case 64: return launch_decode_d<64>(a, stream);
+    case 128: return launch_decode_d<128>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace novakv

@@ -1,0 +1,115 @@
+// Append-time encoder: transform new keys/values and store the nearest
+// codeword index of every group.
+//
+// Paper: Algorithm 1 (write step, Q+((k - k_bar) R_K)), Theorem 1 (key
+// transform), Corollary 1 (s = v R_V), Sec. "Calibration" (exact
+// nearest-neighbour search in the Euclidean metric of the transform domain).
+// The transform and the distances are evaluated in fp64 so that the stored
+// index is the exact argmin (smallest index among equal distances).
+#include <math.h>
+
+#include "nova_kv_internal.h"
+
+namespace novakv {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTokens = 16;  // tokens per workgroup
+
+template <int D>
+__global__ void __launch_bounds__(kThreads) encode_v0(EncodeArgs a) {
+  constexpr int L = D / kGroupDim;
+  constexpr int CB = L * kCodebookSize * kGroupDim;
+  __shared__ double xs[kTokens][D];
+  __shared__ double us[kTokens][D];
+  __shared__ __attribute__((aligned(16))) uint16_t cb[CB];
+
+  const int tile = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  const int n0 = tile * kTokens;
+  const int nt = min(kTokens, a.n_new - n0);
+  const int pos0 = a.start_pos[b] + n0;
+
+  for (int side = 0; side < 2; ++side) {
+    const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D;
+    const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * CB;
+    const void *src = side == 0 ? a.k : a.v;
+    uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
+
+    {
+      const uint4 *s4 = reinterpret_cast<const uint4 *>(cbg);
+      uint4 *d4 = reinterpret_cast<uint4 *>(cb);
+      for (int i = tid; i < CB * 2 / 16; i += kThreads) d4[i] = s4[i];
+    }
+    for (int i = tid; i < nt * D; i += kThreads) {
+      const int t = i / D, d = i % D;
+      const size_t idx =
+          ((static_cast<size_t>(b) * a.n_new + n0 + t) * a.num_kv_heads + kv) * D + d;
+      double x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
+                           : static_cast<double>(static_cast<const float *>(src)[idx]);
+      if (side == 0) x -= static_cast<double>(a.kbar[kv * D + d]);
+      xs[t][d] = x;
+    }
+    __syncthreads();
+
+    if (tid < D) {
+      double acc[kTokens];
+#pragma unroll
+      for (int t = 0; t < kTokens; ++t) acc[t] = 0.0;
+      for (int d = 0; d < D; ++d) {
+        const double w = static_cast<double>(tm[d * D + tid]);
+#pragma unroll
+        for (int t = 0; t < kTokens; ++t) acc[t] = fma(xs[t][d], w, acc[t]);
+      }
+      for (int t = 0; t < nt; ++t) us[t][tid] = acc[t];
+    }
+    __syncthreads();
+
+    for (int p = tid; p < nt * L; p += kThreads) {
+      const int t = p / L, ell = p % L;
+      const double u0 = us[t][ell * 4 + 0], u1 = us[t][ell * 4 + 1];
+      const double u2 = us[t][ell * 4 + 2], u3 = us[t][ell * 4 + 3];
+      const uint16_t *row = &cb[ell * kCodebookSize * kGroupDim];
+      double best = INFINITY;
+      int arg = 0;
+      for (int c = 0; c < kCodebookSize; ++c) {
+#pragma clang fp contract(off)
+        const double e0 = u0 - static_cast<double>(half_bits_to_float(row[c * 4 + 0]));
+        const double e1 = u1 - static_cast<double>(half_bits_to_float(row[c * 4 + 1]));
+        const double e2 = u2 - static_cast<double>(half_bits_to_float(row[c * 4 + 2]));
+        const double e3 = u3 - static_cast<double>(half_bits_to_float(row[c * 4 + 3]));
+        double dist = e0 * e0;
+        dist = dist + e1 * e1;
+        dist = dist + e2 * e2;
+        dist = dist + e3 * e3;
+        if (dist < best) {
+          best = dist;
+          arg = c;
+        }
+      }
+      const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos0 + t);
+      pool[off + ell] = static_cast<uint8_t>(arg);
+    }
+    __syncthreads();
+  }
+}
+
+template <int D>
+hipError_t launch_encode_d(const EncodeArgs &a, hipStream_t stream) {
+  const dim3 grid((a.n_new + kTokens - 1) / kTokens, a.num_kv_heads, a.batch);
+  encode_v0<D><<<grid, dim3(kThreads), 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_encode(const EncodeArgs &a, hipStream_t stream) {
+  switch (a.head_dim) {
+    case 64: return launch_encode_d<64>(a, stream);
+    case 128: return launch_encode_d<128>(a, stream);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace novakv

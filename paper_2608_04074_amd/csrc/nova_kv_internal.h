@@ -1,0 +1,84 @@
+// Internal declarations shared by the HIP translation units of libnovakv.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace novakv {
+
+constexpr int kGroupDim = 4;        // g: coefficients per codebook group
+constexpr int kCodebookSize = 256;  // K: codewords per group (8-bit codes)
+constexpr int kMaxGqa = 8;          // query heads per KV head handled by the kernels
+
+struct CacheLayout {
+  int block_size;
+  int blocks_per_seq;
+  const int32_t *block_table;  // device [B][blocks_per_seq] or nullptr
+};
+
+// Byte offset of the L code bytes of (sequence b, KV head kv, token t).
+__device__ __forceinline__ size_t code_row_offset(const CacheLayout &lay, int num_kv_heads,
+                                                  int groups, int b, int kv, int t) {
+  const int blk = t / lay.block_size;
+  const int row = t - blk * lay.block_size;
+  const int logical = b * lay.blocks_per_seq + blk;
+  const int phys = lay.block_table ? lay.block_table[logical] : logical;
+  return ((static_cast<size_t>(phys) * num_kv_heads + kv) * lay.block_size + row) *
+         static_cast<size_t>(groups);
+}
+
+struct DecodeArgs {
+  int batch, num_q_heads, num_kv_heads, head_dim, gqa;
+  const float *kbar, *t_k_inv_t, *t_v;
+  const uint16_t *cb_k, *cb_v;
+  CacheLayout layout;
+  const void *q;
+  int q_bf16;
+  const uint8_t *k_codes, *v_codes;
+  const int32_t *seq_lens;
+  int max_seq_len, window;
+  const float *sinks;
+  float scale;
+  float *out;
+  // workspace carve-out
+  float *qp;        // [B][Hq][D]     pre-transformed, pre-scaled queries
+  float *sinkp;     // [B][Hq]        shifted sink logits (-inf when no sink)
+  float *part_ml;   // [B][Hq][n_split][2]  running max, denominator
+  float *part_acc;  // [B][Hq][n_split][D]  transform-domain value accumulator
+  int n_split;      // context splits per sequence
+  int chunk;        // tokens per split
+};
+
+struct EncodeArgs {
+  int batch, n_new, num_kv_heads, head_dim;
+  const float *kbar, *t_k, *t_v;
+  const uint16_t *cb_k, *cb_v;
+  CacheLayout layout;
+  const void *k, *v;
+  int in_bf16;
+  const int32_t *start_pos;
+  uint8_t *k_codes, *v_codes;
+};
+
+// Split plan and workspace carve-out of the decode path.
+struct DecodePlan {
+  int n_split;
+  int chunk;
+  size_t off_qp, off_sinkp, off_ml, off_acc, total;
+};
+DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_dim,
+                       int max_seq_len);
+
+hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream);
+hipError_t launch_encode(const EncodeArgs &a, hipStream_t stream);
+
+__device__ __forceinline__ float half_bits_to_float(uint16_t h) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, h));
+}
+
+__device__ __forceinline__ float bf16_bits_to_float(uint16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+}  // namespace novakv

@@ -1,0 +1,145 @@
+"""C-ABI checks that need no GPU: exports, status strings, host-side argument validation.
+
+Every call here is rejected by the host-side checks before any HIP call or
+launch, so nothing touches a device.
+"""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_04074_amd import _native as nat
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "nova_kv.h")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(nova_kv_\w+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    lib = nat.lib()
+    declared = _declared_functions()
+    assert set(declared) == set(nat.EXPORTED)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    lib = nat.lib()
+    for s in range(5):
+        assert lib.nova_kv_status_string(s)
+    assert lib.nova_kv_status_string(99) == b"unknown status"
+
+
+def _params(**kw):
+    base = dict(num_kv_heads=8, head_dim=128, group_dim=4, codebook_size=256, flags=0,
+                kbar=0x1000, t_k=0x2000, t_k_inv_t=0x3000, t_v=0x4000, cb_k=0x5000, cb_v=0x6000)
+    base.update(kw)
+    return nat.Params(**base)
+
+
+def _layout(**kw):
+    base = dict(block_size=4096, blocks_per_seq=1, block_table=None)
+    base.update(kw)
+    return nat.Layout(**base)
+
+
+def _decode(p, lay, **kw):
+    a = dict(q=0x7000, q_dtype=nat.NOVA_KV_BF16, batch=2, hq=32, k=0x8000, v=0x9000, seq=0xA000,
+             max_seq=4096, window=0, sinks=None, scale=0.0, out=0xB000, ws=None, ws_bytes=0)
+    a.update(kw)
+    return nat.lib().nova_kv_decode_attn(
+        ctypes.byref(p) if p is not None else None, ctypes.byref(lay) if lay is not None else None,
+        a["q"], a["q_dtype"], a["batch"], a["hq"], a["k"], a["v"], a["seq"], a["max_seq"],
+        a["window"], a["sinks"], a["scale"], a["out"], a["ws"], a["ws_bytes"], None)
+
+
+def _encode(p, lay, **kw):
+    a = dict(k=0x7000, v=0x7800, dtype=nat.NOVA_KV_BF16, batch=2, n_new=16, start=0xA000,
+             kc=0x8000, vc=0x9000)
+    a.update(kw)
+    return nat.lib().nova_kv_encode(ctypes.byref(p) if p is not None else None,
+                                    ctypes.byref(lay) if lay is not None else None,
+                                    a["k"], a["v"], a["dtype"], a["batch"], a["n_new"], a["start"],
+                                    a["kc"], a["vc"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(group_dim=8), nat.NOVA_KV_ERR_UNSUPPORTED),
+    (dict(codebook_size=16), nat.NOVA_KV_ERR_UNSUPPORTED),
+    (dict(head_dim=96), nat.NOVA_KV_ERR_UNSUPPORTED),
+    (dict(head_dim=130), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(flags=1), nat.NOVA_KV_ERR_UNSUPPORTED),
+    (dict(num_kv_heads=0), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(cb_k=None), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(cb_v=0x6001), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(t_k_inv_t=None), nat.NOVA_KV_ERR_INVALID_ARG),
+])
+def test_decode_rejects_bad_params(kw, status):
+    assert _decode(_params(**kw), _layout()) == status
+    assert nat.lib().nova_kv_last_error()
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(hq=12), nat.NOVA_KV_ERR_INVALID_ARG),          # not a multiple of Hkv
+    (dict(hq=128), nat.NOVA_KV_ERR_UNSUPPORTED),         # 16 query heads per KV head
+    (dict(batch=-1), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(max_seq=0), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(max_seq=5000), nat.NOVA_KV_ERR_INVALID_ARG),   # above capacity 4096
+    (dict(window=-3), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(q_dtype=7), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(scale=-1.0), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(q=None), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(out=None), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(k=0x8001), nat.NOVA_KV_ERR_INVALID_ARG),       # misaligned pool
+    (dict(ws=None), nat.NOVA_KV_ERR_WORKSPACE),
+    (dict(ws=0x10000, ws_bytes=16), nat.NOVA_KV_ERR_WORKSPACE),
+    (dict(ws=0x10010, ws_bytes=1 << 30), nat.NOVA_KV_ERR_WORKSPACE),   # misaligned workspace
+])
+def test_decode_rejects_bad_arguments(kw, status):
+    assert _decode(_params(), _layout(), **kw) == status
+
+
+def test_decode_rejects_null_structs_and_bad_layout():
+    assert _decode(None, _layout()) == nat.NOVA_KV_ERR_INVALID_ARG
+    assert _decode(_params(), None) == nat.NOVA_KV_ERR_INVALID_ARG
+    assert _decode(_params(), _layout(block_size=0)) == nat.NOVA_KV_ERR_INVALID_ARG
+
+
+def test_decode_batch_zero_is_a_noop():
+    assert _decode(_params(), _layout(), batch=0, q=None, out=None) == nat.NOVA_KV_OK
+
+
+def test_workspace_query():
+    lib = nat.lib()
+    p = _params()
+    n = lib.nova_kv_decode_workspace_bytes(ctypes.byref(p), 8, 32, 16384)
+    assert n > 8 * 32 * 128 * 4 and n % 256 == 0
+    assert lib.nova_kv_decode_workspace_bytes(ctypes.byref(p), 0, 32, 16384) == 0
+    assert lib.nova_kv_decode_workspace_bytes(None, 8, 32, 16384) == 0
+    # monotone in the context length
+    assert lib.nova_kv_decode_workspace_bytes(ctypes.byref(p), 8, 32, 32768) >= n
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(batch=-1), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(n_new=-1), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(n_new=5000), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(dtype=5), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(k=None), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(start=None), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(kc=None), nat.NOVA_KV_ERR_INVALID_ARG),
+])
+def test_encode_rejects_bad_arguments(kw, status):
+    assert _encode(_params(), _layout(), **kw) == status
+
+
+def test_encode_needs_forward_transforms_and_noops():
+    assert _encode(_params(t_k=None), _layout()) == nat.NOVA_KV_ERR_INVALID_ARG
+    assert _encode(_params(), _layout(), n_new=0, k=None) == nat.NOVA_KV_OK
+    assert _encode(_params(), _layout(), batch=0, k=None) == nat.NOVA_KV_OK

@@ -1,0 +1,342 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 CPU oracle.
+
+Inputs are seeded synthetic workloads from ``synth``; transforms and codebooks
+come from the oracle's calibration.  Codes must match bit-exactly except where
+the oracle's top-2 distance gap is a near-tie (< 1e-6); decode outputs must
+be within 2e-3 of the oracle's, max-abs relative to each row's L2 norm.
+At full sizes the oracle checks sampled (sequence, KV head) units.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from helpers import assert_outputs_close, compare_codes, read_rows, write_rows
+from oracle import attention as oatt
+from oracle import codec as ocodec
+from oracle_cache import calibrated_params
+
+pytestmark = pytest.mark.gpu
+
+
+def say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+
+
+@pytest.fixture(scope="module")
+def nk():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2608_04074_amd as nk
+    nk._native.lib()          # fail loudly if the HIP library is missing
+    return nk
+
+
+def dev(x, dtype):
+    return torch.as_tensor(np.ascontiguousarray(x)).to(dtype).cuda()
+
+
+def qdtype(wl):
+    return torch.float32 if wl.dtype == "f32" else torch.bfloat16
+
+
+def upload_params(nk, params):
+    return nk.NovaKVParams.from_arrays(params)
+
+
+def lay_kwargs(wl_hkv, block_size, blocks_per_seq, table=None):
+    return dict(hkv=wl_hkv, block_size=block_size, blocks_per_seq=blocks_per_seq, table=table)
+
+
+def oracle_rows(q, pool_k, pool_v, params, b, kv, n, scale, lay, window=0, sinks=None, gqa=1):
+    L = params["cb_k"].shape[1]
+    ck = read_rows(pool_k, b, kv, 0, n, groups=L, **lay)
+    cv = read_rows(pool_v, b, kv, 0, n, groups=L, **lay)
+    hp = oatt.head_params(params, kv)
+    heads = slice(kv * gqa, (kv + 1) * gqa)
+    return oatt.decode_rows(q[b, heads], ck, cv, hp, scale, window,
+                            None if sinks is None else sinks[heads])
+
+
+# ----------------------------------------------------------------- config 1
+
+def test_single_head_encode_and_decode(nk):
+    """Single head, batch 1, D=128, S=2048, fp32: codes bit-exact, output within tolerance."""
+    wl = synth.get_workload("single_head")
+    params = calibrated_params(wl, 0)
+    hp = oatt.head_params(params, 0)
+    S, L = wl.seq_len, wl.groups
+    kc, vc = synth.cache_tokens(wl, 0, 0, 0, S)
+    P = upload_params(nk, params)
+    lay = nk.CacheLayout.contiguous(S)
+    pk = torch.zeros((1, 1, S, L), dtype=torch.uint8, device="cuda")
+    pv = torch.zeros_like(pk)
+    say("single_head encode")
+    nk.encode(P, lay, dev(kc[None, :, None, :], torch.float32), dev(vc[None, :, None, :], torch.float32),
+              dev([0], torch.int32), pk, pv)
+    torch.cuda.synchronize()
+    ck, gk, cv, gv = ocodec.encode_tokens(kc, vc, hp)
+    compare_codes(pk.cpu().numpy()[0, 0], ck, gk, "single_head K")
+    compare_codes(pv.cpu().numpy()[0, 0], cv, gv, "single_head V")
+
+    q = synth.decode_queries(wl, 0)
+    scale = 1 / np.sqrt(wl.head_dim)
+    ref = oatt.decode_rows(q[0], ck, cv, hp, scale)
+    # identical inputs: the oracle's codes
+    pk.copy_(dev(ck[None, None], torch.uint8))
+    pv.copy_(dev(cv[None, None], torch.uint8))
+    say("single_head decode")
+    out = nk.decode_attn(P, lay, dev(q, torch.float32), pk, pv, dev([S], torch.int32), S)
+    assert_outputs_close(out.cpu().numpy()[0], ref, what="single_head decode")
+
+
+# ------------------------------------------------ qwen-shaped, moderate size
+
+@pytest.fixture(scope="module")
+def qwen_small(nk):
+    wl = synth.get_workload("qwen3_8b")
+    params = calibrated_params(wl, 0)
+    return wl, params, upload_params(nk, params)
+
+
+@pytest.mark.parametrize("paged", [False, True])
+def test_qwen_shape_encode_ragged(nk, qwen_small, paged):
+    """32q/8kv, D=128, bf16: GPU encode of 3 sequences x 1100 tokens (ragged tile tail)."""
+    wl, params, P = qwen_small
+    B, n_new, start = 3, 1100, 37
+    cap = 1280
+    L, H = wl.groups, wl.num_kv_heads
+    if paged:
+        bs, bps = 16, cap // 16
+        table = np.random.default_rng(7).permutation(B * bps).astype(np.int32).reshape(B, bps)
+        lay = nk.CacheLayout(bs, bps, dev(table, torch.int32))
+    else:
+        bs, bps, table = cap, 1, None
+        lay = nk.CacheLayout.contiguous(cap)
+    kk = np.empty((B, n_new, H, wl.head_dim))
+    vv = np.empty_like(kk)
+    for b in range(B):
+        for kv in range(H):
+            kk[b, :, kv], vv[b, :, kv] = synth.cache_tokens(wl, 0, kv, b, n_new)
+    nblocks = B * bps
+    pk = torch.zeros((nblocks, H, bs, L), dtype=torch.uint8, device="cuda")
+    pv = torch.zeros_like(pk)
+    say(f"qwen encode paged={paged}")
+    nk.encode(P, lay, dev(kk, torch.bfloat16), dev(vv, torch.bfloat16),
+              dev([start] * B, torch.int32), pk, pv)
+    torch.cuda.synchronize()
+    hk = pk.cpu().numpy().reshape(-1)
+    hv = pv.cpu().numpy().reshape(-1)
+    lk = lay_kwargs(H, bs, bps, table)
+    for b in range(B):
+        for kv in range(H):
+            ck, gk, cv, gv = ocodec.encode_tokens(kk[b, :, kv], vv[b, :, kv], oatt.head_params(params, kv))
+            compare_codes(read_rows(hk, b, kv, start, n_new, groups=L, **lk), ck, gk, f"b{b} kv{kv} K")
+            compare_codes(read_rows(hv, b, kv, start, n_new, groups=L, **lk), cv, gv, f"b{b} kv{kv} V")
+    # nothing outside the written range was touched
+    before = read_rows(hk, 0, 0, 0, start, groups=L, **lk)
+    assert not before.any()
+
+
+def _random_pools(wl, layer, B, cap, H, L):
+    ck = synth.random_codes(wl, layer, "k", (B, H, cap, L))
+    cv = synth.random_codes(wl, layer, "v", (B, H, cap, L))
+    return ck, cv
+
+
+@pytest.mark.parametrize("window,use_sink", [(0, False), (0, True), (300, True), (1, False)])
+def test_qwen_shape_decode_ragged(nk, qwen_small, window, use_sink):
+    """Ragged lengths incl. 0 and 1, windows, sinks; every row checked."""
+    wl, params, P = qwen_small
+    B, cap = 6, 2304
+    H, L, G = wl.num_kv_heads, wl.groups, wl.gqa
+    lens = np.array([0, 1, 255, 1023, 2000, 2304], dtype=np.int32)
+    ck, cv = _random_pools(wl, 0, B, cap, H, L)
+    q = synth.decode_queries(wl, 0, batch=B)
+    sinks = np.random.default_rng(3).standard_normal(wl.num_q_heads).astype(np.float32) if use_sink else None
+    lay = nk.CacheLayout.contiguous(cap)
+    say(f"qwen decode window={window} sink={use_sink}")
+    out = nk.decode_attn(P, lay, dev(q, torch.bfloat16), dev(ck, torch.uint8), dev(cv, torch.uint8),
+                         dev(lens, torch.int32), cap, window=window,
+                         sinks=dev(sinks, torch.float32) if use_sink else None).cpu().numpy()
+    scale = 1 / np.sqrt(wl.head_dim)
+    lk = lay_kwargs(H, cap, 1)
+    hk, hv = ck.reshape(-1), cv.reshape(-1)
+    ref = np.zeros_like(out, dtype=np.float64)
+    for b in range(B):
+        for kv in range(H):
+            ref[b, kv * G:(kv + 1) * G] = oracle_rows(q, hk, hv, params, b, kv, int(lens[b]), scale, lk,
+                                                       window, sinks, G)
+    if not use_sink:
+        assert np.all(out[0] == 0)            # empty sequence, no sink: zeros
+    assert_outputs_close(out.reshape(-1, wl.head_dim), ref.reshape(-1, wl.head_dim),
+                         what=f"qwen ragged window={window} sink={use_sink}")
+
+
+def test_paged_equals_contiguous_and_split_invariance(nk, qwen_small):
+    wl, params, P = qwen_small
+    B, cap = 2, 4096
+    H, L = wl.num_kv_heads, wl.groups
+    ck, cv = _random_pools(wl, 0, B, cap, H, L)
+    q = dev(synth.decode_queries(wl, 0, batch=B), torch.bfloat16)
+    lens = dev([4096, 3001], torch.int32)
+    say("contiguous vs paged")
+    out_c = nk.decode_attn(P, nk.CacheLayout.contiguous(cap), q, dev(ck, torch.uint8),
+                           dev(cv, torch.uint8), lens, cap)
+    bs, bps = 16, cap // 16
+    table = np.random.default_rng(11).permutation(B * bps).astype(np.int32).reshape(B, bps)
+    flat_k = np.zeros(B * bps * H * bs * L, dtype=np.uint8)
+    flat_v = np.zeros_like(flat_k)
+    lk = lay_kwargs(H, bs, bps, table)
+    for b in range(B):
+        for kv in range(H):
+            write_rows(flat_k, ck[b, kv], b, kv, 0, **lk)
+            write_rows(flat_v, cv[b, kv], b, kv, 0, **lk)
+    out_p = nk.decode_attn(P, nk.CacheLayout(bs, bps, dev(table, torch.int32)), q,
+                           dev(flat_k, torch.uint8), dev(flat_v, torch.uint8), lens, cap)
+    assert torch.equal(out_c, out_p)
+    # a larger max_seq_len changes the split plan, not the result (beyond rounding)
+    big = torch.zeros((B, H, 8192, L), dtype=torch.uint8, device="cuda")
+    big[:, :, :cap] = dev(ck, torch.uint8)
+    bigv = torch.zeros_like(big)
+    bigv[:, :, :cap] = dev(cv, torch.uint8)
+    out_b = nk.decode_attn(P, nk.CacheLayout.contiguous(8192), q, big, bigv, lens, 8192)
+    torch.testing.assert_close(out_b, out_c, rtol=1e-5, atol=1e-6)
+
+
+# ------------------------------------------------- full-size configurations
+
+def _full_decode(nk, wl, layer, params, units, window=0, batch=None, cap=None):
+    B = wl.batch if batch is None else batch
+    cap = wl.seq_len if cap is None else cap
+    H, L, G, D = wl.num_kv_heads, wl.groups, wl.gqa, wl.head_dim
+    P = upload_params(nk, params)
+    ck, cv = _random_pools(wl, layer, B, cap, H, L)
+    q = synth.decode_queries(wl, layer, batch=B)
+    sinks = synth.sink_logits(wl, layer)
+    lens = np.full(B, cap, dtype=np.int32)
+    say(f"{wl.name} layer {layer} full decode B={B} S={cap} window={window}")
+    out = nk.decode_attn(P, nk.CacheLayout.contiguous(cap), dev(q, qdtype(wl)), dev(ck, torch.uint8),
+                         dev(cv, torch.uint8), dev(lens, torch.int32), cap, window=window,
+                         sinks=dev(sinks, torch.float32) if sinks is not None else None)
+    torch.cuda.synchronize()
+    out = out.cpu().numpy()
+    scale = 1 / np.sqrt(D)
+    lk = lay_kwargs(H, cap, 1)
+    hk, hv = ck.reshape(-1), cv.reshape(-1)
+    gots, refs = [], []
+    for b, kv in units:
+        refs.append(oracle_rows(q, hk, hv, params, b, kv, cap, scale, lk, window, sinks, G))
+        gots.append(out[b, kv * G:(kv + 1) * G])
+    assert_outputs_close(np.concatenate(gots), np.concatenate(refs), what=f"{wl.name} L{layer}")
+    assert np.isfinite(out).all()
+
+
+def test_qwen3_8b_full_decode(nk):
+    wl = synth.get_workload("qwen3_8b")
+    _full_decode(nk, wl, 0, calibrated_params(wl, 0), [(0, 0), (3, 5), (7, 7)])
+
+
+def test_sweep_b64_s32k_decode(nk):
+    wl = synth.get_workload("sweep_b64_s32k")
+    _full_decode(nk, wl, 0, calibrated_params(synth.get_workload("qwen3_8b"), 0),
+                 [(0, 1), (40, 3), (63, 6)])
+
+
+def test_sweep_b1_s128k_decode(nk):
+    wl = synth.get_workload("sweep_b1_s128k")
+    _full_decode(nk, wl, 0, calibrated_params(synth.get_workload("qwen3_8b"), 0), [(0, 0), (0, 4)])
+
+
+@pytest.mark.parametrize("layer", [0, 1])
+def test_gptoss_pair_decode(nk, layer):
+    wl = synth.get_workload("gptoss_pair")
+    _full_decode(nk, wl, layer, calibrated_params(wl, layer), [(0, 0), (9, 2), (15, 7)],
+                 window=wl.windows[layer])
+
+
+def test_qwen3_8b_full_encode_sampled(nk):
+    """Full-size GPU encode of B=8 x 8 KV heads x 16384 tokens; oracle re-encodes sampled units."""
+    wl = synth.get_workload("qwen3_8b")
+    params = calibrated_params(wl, 0)
+    P = upload_params(nk, params)
+    B, S, H, L, D = wl.batch, wl.seq_len, wl.num_kv_heads, wl.groups, wl.head_dim
+    pk = torch.zeros((B, H, S, L), dtype=torch.uint8, device="cuda")
+    pv = torch.zeros_like(pk)
+    sample = [(0, 0), (5, 3), (7, 7)]
+    kept = {}
+    for b in range(B):
+        kk = np.empty((S, H, D))
+        vv = np.empty_like(kk)
+        for kv in range(H):
+            kk[:, kv], vv[:, kv] = synth.cache_tokens(wl, 0, kv, b, S)
+            if (b, kv) in sample:
+                kept[(b, kv)] = (kk[:, kv].copy(), vv[:, kv].copy())
+        # one sequence at a time: start_pos is per sequence, so encode the row's slice of the pool
+        say(f"qwen3_8b encode sequence {b}")
+        nk.encode(P, nk.CacheLayout.contiguous(S), dev(kk[None], torch.bfloat16),
+                  dev(vv[None], torch.bfloat16), dev([0], torch.int32), pk[b:b + 1], pv[b:b + 1])
+    torch.cuda.synchronize()
+    for (b, kv), (kk, vv) in kept.items():
+        ck, gk, cv, gv = ocodec.encode_tokens(kk, vv, oatt.head_params(params, kv))
+        compare_codes(pk[b, kv].cpu().numpy(), ck, gk, f"qwen3_8b b{b} kv{kv} K")
+        compare_codes(pv[b, kv].cpu().numpy(), cv, gv, f"qwen3_8b b{b} kv{kv} V")
+
+
+def test_append_paged_then_decode(nk):
+    """32 sequences append 4096 tokens into a shuffled 16-token-block pool, then decode at 32768."""
+    wl = synth.get_workload("append_paged")
+    params = calibrated_params(synth.get_workload("qwen3_8b"), 0)
+    P = upload_params(nk, params)
+    B, S, H, L, D, G = wl.batch, wl.seq_len, wl.num_kv_heads, wl.groups, wl.head_dim, wl.gqa
+    bs = wl.block_size
+    bps = S // bs
+    start = S - wl.n_new
+    table = synth.shuffled_block_table(wl)
+    lk = lay_kwargs(H, bs, bps, table)
+    # history: stand-in codes written through the block table
+    hist_k, hist_v = _random_pools(wl, 0, B, start, H, L)
+    flat_k = np.zeros(B * bps * H * bs * L, dtype=np.uint8)
+    flat_v = np.zeros_like(flat_k)
+    for b in range(B):
+        for kv in range(H):
+            write_rows(flat_k, hist_k[b, kv], b, kv, 0, **lk)
+            write_rows(flat_v, hist_v[b, kv], b, kv, 0, **lk)
+    pk = dev(flat_k, torch.uint8)
+    pv = dev(flat_v, torch.uint8)
+    lay = nk.CacheLayout(bs, bps, dev(table, torch.int32))
+    kk = np.empty((B, wl.n_new, H, D))
+    vv = np.empty_like(kk)
+    for b in range(B):
+        for kv in range(H):
+            kk[b, :, kv], vv[b, :, kv] = synth.cache_tokens(wl, 0, kv, b, wl.n_new, start=start)
+    say("append_paged encode")
+    nk.encode(P, lay, dev(kk, torch.bfloat16), dev(vv, torch.bfloat16), dev([start] * B, torch.int32),
+              pk, pv)
+    torch.cuda.synchronize()
+    gk_pool = pk.cpu().numpy()
+    gv_pool = pv.cpu().numpy()
+    # history untouched
+    assert np.array_equal(read_rows(gk_pool, 3, 2, 0, start, groups=L, **lk), hist_k[3, 2])
+    units = [(0, 0), (13, 4), (31, 7)]
+    oracle_codes = {}
+    for b, kv in units:
+        ck, gk, cv, gv = ocodec.encode_tokens(kk[b, :, kv], vv[b, :, kv], oatt.head_params(params, kv))
+        compare_codes(read_rows(gk_pool, b, kv, start, wl.n_new, groups=L, **lk), ck, gk,
+                      f"append b{b} kv{kv} K")
+        compare_codes(read_rows(gv_pool, b, kv, start, wl.n_new, groups=L, **lk), cv, gv,
+                      f"append b{b} kv{kv} V")
+        oracle_codes[(b, kv)] = (ck, cv)
+    # decode over the paged pool; the oracle uses its own codes for the appended tokens
+    q = synth.decode_queries(wl, 0)
+    say("append_paged decode")
+    out = nk.decode_attn(P, lay, dev(q, torch.bfloat16), pk, pv, dev([S] * B, torch.int32), S)
+    out = out.cpu().numpy()
+    scale = 1 / np.sqrt(D)
+    gots, refs = [], []
+    for b, kv in units:
+        ck = np.concatenate([hist_k[b, kv], oracle_codes[(b, kv)][0]])
+        cv = np.concatenate([hist_v[b, kv], oracle_codes[(b, kv)][1]])
+        refs.append(oatt.decode_rows(q[b, kv * G:(kv + 1) * G], ck, cv, oatt.head_params(params, kv), scale))
+        gots.append(out[b, kv * G:(kv + 1) * G])
+    assert_outputs_close(np.concatenate(gots), np.concatenate(refs), what="append_paged decode")
