@@ -130,7 +130,7 @@ size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch, in
   if (!p || batch <= 0 || num_q_heads <= 0 || max_seq_len <= 0 || p->num_kv_heads <= 0 ||
       p->head_dim <= 0)
     return 0;
-  return novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len).total;
+  return novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len, 0).total;
 }
 
 nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
@@ -162,8 +162,8 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
     return fail(NOVA_KV_ERR_INVALID_ARG, "q, k_codes, v_codes, seq_lens or out is NULL");
   if (!aligned(k_codes, 16) || !aligned(v_codes, 16))
     return fail(NOVA_KV_ERR_INVALID_ARG, "code pools must be 16-byte aligned");
-  const novakv::DecodePlan plan =
-      novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len);
+  const novakv::DecodePlan plan = novakv::plan_decode(batch, num_q_heads, p->num_kv_heads,
+                                                      p->head_dim, max_seq_len, layout->block_size);
   if (!workspace || workspace_bytes < plan.total)
     return fail(NOVA_KV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
                 workspace ? workspace_bytes : static_cast<size_t>(0));
@@ -190,6 +190,7 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
   a.window = window;
   a.sinks = sinks;
   a.scale = softmax_scale > 0.f ? softmax_scale : 1.0f / sqrtf(static_cast<float>(p->head_dim));
+  a.qscale = plan.use_lut ? a.scale * 1.44269504088896341f : a.scale;
   a.out = out;
   char *ws = static_cast<char *>(workspace);
   a.qp = reinterpret_cast<float *>(ws + plan.off_qp);
@@ -198,7 +199,7 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
   a.part_acc = reinterpret_cast<float *>(ws + plan.off_acc);
   a.n_split = plan.n_split;
   a.chunk = plan.chunk;
-  hipError_t e = novakv::launch_decode(a, static_cast<hipStream_t>(hip_stream));
+  hipError_t e = novakv::launch_decode(a, plan.use_lut, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
   return ok();
 }

@@ -51,7 +51,7 @@ __global__ void __launch_bounds__(D) decode_prologue(DecodeArgs a) {
   const float *tk = a.t_k_inv_t + static_cast<size_t>(kv) * D * D;
   float acc = 0.f;
   for (int d = 0; d < D; ++d) acc = fmaf(qsh[d], tk[d * D + tid], acc);
-  a.qp[static_cast<size_t>(bh) * D + tid] = acc * a.scale;
+  a.qp[static_cast<size_t>(bh) * D + tid] = acc * a.qscale;
   if (tid == 0) {
     float s = 0.f;
     for (int w = 0; w < D / 64; ++w) s += red[w];
@@ -235,39 +235,66 @@ __global__ void __launch_bounds__(D) decode_combine(DecodeArgs a) {
 }
 
 template <int D>
-hipError_t launch_decode_d(const DecodeArgs &a, hipStream_t stream) {
+hipError_t launch_decode_d(const DecodeArgs &a, int use_lut, hipStream_t stream) {
   const int rows = a.batch * a.num_q_heads;
   decode_prologue<D><<<dim3(rows), dim3(D), 0, stream>>>(a);
-  decode_stage1_v0<D><<<dim3(a.n_split, a.num_kv_heads, a.batch), dim3(kThreads), 0, stream>>>(a);
+  if (use_lut) {
+    const hipError_t e = launch_decode_lut(a, stream);
+    if (e != hipSuccess) return e;
+  } else {
+    decode_stage1_v0<D><<<dim3(a.n_split, a.num_kv_heads, a.batch), dim3(kThreads), 0, stream>>>(a);
+  }
   decode_combine<D><<<dim3(rows), dim3(D), 0, stream>>>(a);
   return hipGetLastError();
 }
 
 }  // namespace
 
+namespace {
+
+void plan_generic(int batch, int num_kv_heads, int max_seq_len, int *n_split, int *chunk) {
+  int c = 1024;
+  auto splits = [&](int cc) { return (max_seq_len + cc - 1) / cc; };
+  while (c > 64 && static_cast<long long>(batch) * num_kv_heads * splits(c) < 2048) c /= 2;
+  *chunk = c;
+  *n_split = splits(c);
+}
+
+}  // namespace
+
 DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_dim,
-                       int max_seq_len) {
+                       int max_seq_len, int block_size) {
   DecodePlan p{};
-  int chunk = 1024;
-  auto splits = [&](int c) { return (max_seq_len + c - 1) / c; };
-  while (chunk > 64 && static_cast<long long>(batch) * num_kv_heads * splits(chunk) < 2048)
-    chunk /= 2;
-  p.chunk = chunk;
-  p.n_split = splits(chunk);
+  const int gqa = num_q_heads / num_kv_heads;
+  int ns_g, ch_g, ns_l, ch_l;
+  plan_generic(batch, num_kv_heads, max_seq_len, &ns_g, &ch_g);
+  plan_lut(batch, num_kv_heads, max_seq_len, &ns_l, &ch_l);
+  int max_split;
+  if (block_size > 0) {
+    p.use_lut = lut_path_eligible(head_dim, gqa, block_size) ? 1 : 0;
+    p.n_split = p.use_lut ? ns_l : ns_g;
+    p.chunk = p.use_lut ? ch_l : ch_g;
+    max_split = p.n_split;
+  } else {
+    p.use_lut = 0;
+    p.n_split = ns_g;
+    p.chunk = ch_g;
+    max_split = ns_g > ns_l ? ns_g : ns_l;
+  }
   auto align = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
   const size_t rows = static_cast<size_t>(batch) * num_q_heads;
   p.off_qp = 0;
   p.off_sinkp = align(p.off_qp + rows * head_dim * sizeof(float));
   p.off_ml = align(p.off_sinkp + rows * sizeof(float));
-  p.off_acc = align(p.off_ml + rows * p.n_split * 2 * sizeof(float));
-  p.total = align(p.off_acc + rows * p.n_split * head_dim * sizeof(float));
+  p.off_acc = align(p.off_ml + rows * max_split * 2 * sizeof(float));
+  p.total = align(p.off_acc + rows * max_split * head_dim * sizeof(float));
   return p;
 }
 
-hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream) {
+hipError_t launch_decode(const DecodeArgs &a, int use_lut, hipStream_t stream) {
   switch (a.head_dim) {
-    case 64: return launch_decode_d<64>(a, stream);
-    case 128: return launch_decode_d<128>(a, stream);
+    case 64: return launch_decode_d<64>(a, 0, stream);
+    case 128: return launch_decode_d<128>(a, use_lut, stream);
     default: return hipErrorInvalidValue;
   }
 }

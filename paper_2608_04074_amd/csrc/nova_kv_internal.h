@@ -39,7 +39,8 @@ struct DecodeArgs {
   const int32_t *seq_lens;
   int max_seq_len, window;
   const float *sinks;
-  float scale;
+  float scale;      // softmax scale (natural-log units)
+  float qscale;     // factor folded into q' (scale, or scale * log2(e) for the table path)
   float *out;
   // workspace carve-out
   float *qp;        // [B][Hq][D]     pre-transformed, pre-scaled queries
@@ -63,14 +64,21 @@ struct EncodeArgs {
 
 // Split plan and workspace carve-out of the decode path.
 struct DecodePlan {
+  int use_lut;      // 1: table-based stage 1 (decode_lut.hip), 0: generic stage 1
   int n_split;
   int chunk;
   size_t off_qp, off_sinkp, off_ml, off_acc, total;
 };
+// block_size <= 0 plans for the worst case over both stage-1 kernels.
 DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_dim,
-                       int max_seq_len);
+                       int max_seq_len, int block_size);
 
-hipError_t launch_decode(const DecodeArgs &a, hipStream_t stream);
+hipError_t launch_decode(const DecodeArgs &a, int use_lut, hipStream_t stream);
+
+// Table-based stage 1 (head_dim 128, <= 4 query heads per KV head, 16-token-aligned blocks).
+bool lut_path_eligible(int head_dim, int gqa, int block_size);
+void plan_lut(int batch, int num_kv_heads, int max_seq_len, int *n_split, int *chunk);
+hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream);
 hipError_t launch_encode(const EncodeArgs &a, hipStream_t stream);
 
 __device__ __forceinline__ float half_bits_to_float(uint16_t h) {
