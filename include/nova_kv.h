@@ -70,7 +70,8 @@ typedef enum {
  *   cb_v      [Hkv][L][K][g] fp16 bit patterns: value codebook of each group
  *
  * Group l covers transform coordinates [l*g, (l+1)*g).  Supported: g = 4,
- * K = 256, D in {64, 128}; flags must be 0 (reserved).
+ * K = 256, D in {64, 128}; flags must be 0 (reserved).  Every array must be
+ * 16-byte aligned (NOVA_KV_ERR_INVALID_ARG otherwise).
  */
 typedef struct {
     int32_t num_kv_heads;
@@ -99,7 +100,8 @@ typedef struct {
  * A contiguous cache is block_table = NULL, blocks_per_seq = 1 and
  * block_size = the per-sequence capacity (codes[B][Hkv][capacity][L]).
  * block_table is a DEVICE int32 array [B][blocks_per_seq]; every entry used
- * must index a physical block of both pools (caller's precondition).
+ * must index a physical block of both pools (caller's precondition).  Both
+ * pools must be 16-byte aligned.
  */
 typedef struct {
     int32_t block_size;

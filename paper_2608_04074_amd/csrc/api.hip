@@ -53,6 +53,9 @@ nova_kv_status check_params(const nova_kv_params *p, bool need_encode, bool need
   if (need_encode && (!p->t_k || !p->t_v)) return fail(NOVA_KV_ERR_INVALID_ARG, "t_k/t_v is NULL");
   if (need_decode && (!p->t_k_inv_t || !p->t_v))
     return fail(NOVA_KV_ERR_INVALID_ARG, "t_k_inv_t/t_v is NULL");
+  if (!aligned(p->kbar, 16) || !aligned(p->t_v, 16) || (need_encode && !aligned(p->t_k, 16)) ||
+      (need_decode && !aligned(p->t_k_inv_t, 16)))
+    return fail(NOVA_KV_ERR_INVALID_ARG, "kbar and transforms must be 16-byte aligned");
   return NOVA_KV_OK;
 }
 

@@ -50,6 +50,7 @@ __global__ void __launch_bounds__(D) decode_prologue(DecodeArgs a) {
   __syncthreads();
   const float *tk = a.t_k_inv_t + static_cast<size_t>(kv) * D * D;
   float acc = 0.f;
+#pragma unroll 16
   for (int d = 0; d < D; ++d) acc = fmaf(qsh[d], tk[d * D + tid], acc);
   a.qp[static_cast<size_t>(bh) * D + tid] = acc * a.qscale;
   if (tid == 0) {
@@ -203,35 +204,62 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
   }
 }
 
-// Stage 2: log-sum-exp merge of the splits, sink once, divide, then v = s t_v^T.
+// Stage 2, one workgroup per (sequence, KV head): log-sum-exp merge of the
+// splits, sink once, divide, then v = s t_v^T for the KV head's query heads
+// (t_v read once per workgroup, rows as 16-byte vectors).
 template <int D>
-__global__ void __launch_bounds__(D) decode_combine(DecodeArgs a) {
-  const int bh = blockIdx.x;
-  const int h = bh % a.num_q_heads;
-  const int kv = h / a.gqa;
+__global__ void __launch_bounds__(256) decode_combine(DecodeArgs a) {
+  const int b = blockIdx.x / a.num_kv_heads;
+  const int kv = blockIdx.x - b * a.num_kv_heads;
+  const int G = a.gqa;
   const int tid = threadIdx.x;
-  __shared__ float sh[D];
-  const float *ml = a.part_ml + static_cast<size_t>(bh) * a.n_split * 2;
-  const float *pa = a.part_acc + static_cast<size_t>(bh) * a.n_split * D;
-  const float sink = a.sinkp[bh];
-  float big = sink;
-  for (int s = 0; s < a.n_split; ++s) big = fmaxf(big, ml[2 * s]);
-  float den = 0.f, num = 0.f;
-  if (big != -INFINITY) {
-    for (int s = 0; s < a.n_split; ++s) {
-      const float ms = ml[2 * s];
-      const float w = (ms == -INFINITY) ? 0.f : __expf(ms - big);
-      den = fmaf(w, ml[2 * s + 1], den);
-      num = fmaf(w, pa[static_cast<size_t>(s) * D + tid], num);
+  __shared__ float sh[kMaxGqa][D];
+  for (int i = tid; i < G * D; i += 256) {
+    const int h = i / D, d = i - h * D;
+    const size_t bh = static_cast<size_t>(b) * a.num_q_heads + kv * G + h;
+    const float *ml = a.part_ml + bh * a.n_split * 2;
+    const float *pa = a.part_acc + bh * a.n_split * D;
+    const float sink = a.sinkp[bh];
+    float big = sink;
+    for (int s = 0; s < a.n_split; ++s) big = fmaxf(big, ml[2 * s]);
+    float den = 0.f, num = 0.f;
+    if (big != -INFINITY) {
+      for (int s = 0; s < a.n_split; ++s) {
+        const float ms = ml[2 * s];
+        const float w = (ms == -INFINITY) ? 0.f : __expf(ms - big);
+        den = fmaf(w, ml[2 * s + 1], den);
+        num = fmaf(w, pa[static_cast<size_t>(s) * D + d], num);
+      }
+      if (sink != -INFINITY) den += __expf(sink - big);
     }
-    if (sink != -INFINITY) den += __expf(sink - big);
+    sh[h][d] = (den > 0.f) ? num / den : 0.f;
   }
-  sh[tid] = (den > 0.f) ? num / den : 0.f;
   __syncthreads();
-  const float *tv = a.t_v + static_cast<size_t>(kv) * D * D + static_cast<size_t>(tid) * D;
-  float o = 0.f;
-  for (int j = 0; j < D; ++j) o = fmaf(sh[j], tv[j], o);
-  a.out[static_cast<size_t>(bh) * D + tid] = o;
+  // thread -> (output coordinate d, half of the heads)
+  constexpr int HALVES = 256 / D;
+  const int d = tid % D, part = tid / D;
+  const float4 *tv = reinterpret_cast<const float4 *>(a.t_v + static_cast<size_t>(kv) * D * D +
+                                                      static_cast<size_t>(d) * D);
+  float o[kMaxGqa];
+#pragma unroll
+  for (int h = 0; h < kMaxGqa; ++h) o[h] = 0.f;
+#pragma unroll 8
+  for (int j4 = 0; j4 < D / 4; ++j4) {
+    const float4 w = tv[j4];
+#pragma unroll
+    for (int h = 0; h < kMaxGqa; ++h) {
+      if (h % HALVES == part && h < G) {
+        o[h] = fmaf(sh[h][4 * j4 + 0], w.x, o[h]);
+        o[h] = fmaf(sh[h][4 * j4 + 1], w.y, o[h]);
+        o[h] = fmaf(sh[h][4 * j4 + 2], w.z, o[h]);
+        o[h] = fmaf(sh[h][4 * j4 + 3], w.w, o[h]);
+      }
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < kMaxGqa; ++h)
+    if (h % HALVES == part && h < G)
+      a.out[(static_cast<size_t>(b) * a.num_q_heads + kv * G + h) * D + d] = o[h];
 }
 
 template <int D>
@@ -244,7 +272,7 @@ hipError_t launch_decode_d(const DecodeArgs &a, int use_lut, hipStream_t stream)
   } else {
     decode_stage1_v0<D><<<dim3(a.n_split, a.num_kv_heads, a.batch), dim3(kThreads), 0, stream>>>(a);
   }
-  decode_combine<D><<<dim3(rows), dim3(D), 0, stream>>>(a);
+  decode_combine<D><<<dim3(a.batch * a.num_kv_heads), dim3(256), 0, stream>>>(a);
   return hipGetLastError();
 }
 

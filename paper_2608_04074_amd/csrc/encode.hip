@@ -95,10 +95,85 @@ __global__ void __launch_bounds__(kThreads) encode_v0(EncodeArgs a) {
   }
 }
 
+// Few new tokens per sequence (a decode step): one workgroup per (token,
+// sequence, KV head, side).  The codebook is read straight from the cache
+// hierarchy; eight lanes share a group and keep the best (distance, index)
+// pair, smallest index on equal distance, before a lane reduction.
+template <int D>
+__global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
+  constexpr int L = D / kGroupDim;
+  constexpr int LANES = 256 / L;  // lanes per group (8 at D=128, 16 at D=64)
+  __shared__ double xs[D];
+  __shared__ double us[D];
+  const int side = blockIdx.x & 1;
+  const int t = blockIdx.x >> 1;
+  const int kv = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x;
+  const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D;
+  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * L * kCodebookSize * kGroupDim;
+  const void *src = side == 0 ? a.k : a.v;
+  uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
+  if (tid < D) {
+    const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + tid;
+    double x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
+                         : static_cast<double>(static_cast<const float *>(src)[idx]);
+    if (side == 0) x -= static_cast<double>(a.kbar[kv * D + tid]);
+    xs[tid] = x;
+  }
+  __syncthreads();
+  if (tid < D) {
+    double acc = 0.0;
+#pragma unroll 16
+    for (int d = 0; d < D; ++d) acc = fma(xs[d], static_cast<double>(tm[d * D + tid]), acc);
+    us[tid] = acc;
+  }
+  __syncthreads();
+  const int ell = tid / LANES, r = tid % LANES;
+  const double u0 = us[ell * 4 + 0], u1 = us[ell * 4 + 1], u2 = us[ell * 4 + 2], u3 = us[ell * 4 + 3];
+  const uint2 *row = reinterpret_cast<const uint2 *>(cbg + static_cast<size_t>(ell) * kCodebookSize * kGroupDim);
+  double best = INFINITY;
+  int arg = 0;
+  for (int k = 0; k < kCodebookSize / LANES; ++k) {
+#pragma clang fp contract(off)
+    const int c = r + LANES * k;
+    const uint2 w = row[c];
+    const double e0 = u0 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.x & 0xffff)));
+    const double e1 = u1 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.x >> 16)));
+    const double e2 = u2 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.y & 0xffff)));
+    const double e3 = u3 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.y >> 16)));
+    double dist = e0 * e0;
+    dist = dist + e1 * e1;
+    dist = dist + e2 * e2;
+    dist = dist + e3 * e3;
+    if (dist < best) {
+      best = dist;
+      arg = c;
+    }
+  }
+#pragma unroll
+  for (int o = LANES / 2; o > 0; o >>= 1) {
+    const double ob = __shfl_xor(best, o, 64);
+    const int oa = __shfl_xor(arg, o, 64);
+    if (ob < best || (ob == best && oa < arg)) {
+      best = ob;
+      arg = oa;
+    }
+  }
+  if (r == 0) {
+    const int pos = a.start_pos[b] + t;
+    pool[code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos) + ell] = static_cast<uint8_t>(arg);
+  }
+}
+
 template <int D>
 hipError_t launch_encode_d(const EncodeArgs &a, hipStream_t stream) {
-  const dim3 grid((a.n_new + kTokens - 1) / kTokens, a.num_kv_heads, a.batch);
-  encode_v0<D><<<grid, dim3(kThreads), 0, stream>>>(a);
+  if (a.n_new <= 4) {
+    const dim3 grid(2 * a.n_new, a.num_kv_heads, a.batch);
+    encode_small<D><<<grid, dim3(256), 0, stream>>>(a);
+  } else {
+    const dim3 grid((a.n_new + kTokens - 1) / kTokens, a.num_kv_heads, a.batch);
+    encode_v0<D><<<grid, dim3(kThreads), 0, stream>>>(a);
+  }
   return hipGetLastError();
 }
 

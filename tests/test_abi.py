@@ -79,6 +79,8 @@ def _encode(p, lay, **kw):
     (dict(cb_k=None), nat.NOVA_KV_ERR_INVALID_ARG),
     (dict(cb_v=0x6001), nat.NOVA_KV_ERR_INVALID_ARG),
     (dict(t_k_inv_t=None), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(t_v=0x4004), nat.NOVA_KV_ERR_INVALID_ARG),
+    (dict(kbar=0x1008), nat.NOVA_KV_ERR_INVALID_ARG),
 ])
 def test_decode_rejects_bad_params(kw, status):
     assert _decode(_params(**kw), _layout()) == status
