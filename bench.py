@@ -129,7 +129,7 @@ def main():
     start_pos = torch.full((B,), S - 1, dtype=torch.int32, device=dev)
     seq_lens = torch.full((B,), S, dtype=torch.int32, device=dev)
     out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
-    ws = torch.empty(nk.decode_workspace_bytes(P, B, Hq, S), dtype=torch.uint8, device=dev)
+    ws = torch.zeros(nk.decode_workspace_bytes(P, B, Hq, S), dtype=torch.uint8, device=dev)
 
     def step(i, ev=None):
         pk, pv = pools[i % COPIES]

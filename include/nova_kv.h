@@ -135,7 +135,8 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
 
 /*
  * Bytes of device workspace nova_kv_decode_attn needs for this shape (split
- * partials, pre-transformed queries, counters).  Returns 0 on invalid input.
+ * arrival counters, split partials, pre-transformed queries).  Returns 0 on
+ * invalid input.
  */
 size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch,
                                       int32_t num_q_heads, int32_t max_seq_len);
@@ -165,7 +166,10 @@ size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch,
  *                v_hat_t = s_hat_t t_v^T.
  *              A row with no attended token and no sink is written as zeros.
  *   workspace  device scratch of at least nova_kv_decode_workspace_bytes(...)
- *              bytes, 256-byte aligned; contents need no initialisation.
+ *              bytes, 256-byte aligned.  It must be zero-filled before its
+ *              first use (e.g. hipMemset once after allocation); every call
+ *              leaves it ready for the next one, so it is never cleared again.
+ *              Calls that share a workspace must be ordered on one stream.
  * batch == 0 is a valid no-op.
  */
 nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,

@@ -144,7 +144,11 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
                 softmax_scale: float = 0.0, out: Optional[torch.Tensor] = None,
                 workspace: Optional[torch.Tensor] = None,
                 stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
-    """nova_kv_decode_attn: q [B][Hq][D] (fp32 or bf16) -> out [B][Hq][D] fp32."""
+    """nova_kv_decode_attn: q [B][Hq][D] (fp32 or bf16) -> out [B][Hq][D] fp32.
+
+    A caller-provided workspace must be zero-filled before its first use; each
+    call leaves it ready for the next.  When omitted, a zeroed one is allocated.
+    """
     if q.dim() != 3 or q.shape[2] != params.head_dim:
         raise ValueError("q must be [B][Hq][D]")
     b, hq, d = q.shape
@@ -159,7 +163,7 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
     _require(out, "out", (torch.float32,), b * hq * d)
     need = decode_workspace_bytes(params, b, hq, max_seq_len) if b > 0 else 0
     if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+        workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=q.device)
     _require(workspace, "workspace", (torch.uint8,))
     nat.check(nat.lib().nova_kv_decode_attn(
         ctypes.byref(params.c), ctypes.byref(layout.c), q.data_ptr(), _dtype_code(q), b, hq,

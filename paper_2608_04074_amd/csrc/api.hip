@@ -196,6 +196,7 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
   a.qscale = plan.use_lut ? a.scale * 1.44269504088896341f : a.scale;
   a.out = out;
   char *ws = static_cast<char *>(workspace);
+  a.counters = reinterpret_cast<int *>(ws + plan.off_cnt);
   a.qp = reinterpret_cast<float *>(ws + plan.off_qp);
   a.sinkp = reinterpret_cast<float *>(ws + plan.off_sinkp);
   a.part_ml = reinterpret_cast<float *>(ws + plan.off_ml);

@@ -264,14 +264,10 @@ __global__ void __launch_bounds__(256) decode_combine(DecodeArgs a) {
 
 template <int D>
 hipError_t launch_decode_d(const DecodeArgs &a, int use_lut, hipStream_t stream) {
+  if (use_lut) return launch_decode_lut(a, stream);
   const int rows = a.batch * a.num_q_heads;
   decode_prologue<D><<<dim3(rows), dim3(D), 0, stream>>>(a);
-  if (use_lut) {
-    const hipError_t e = launch_decode_lut(a, stream);
-    if (e != hipSuccess) return e;
-  } else {
-    decode_stage1_v0<D><<<dim3(a.n_split, a.num_kv_heads, a.batch), dim3(kThreads), 0, stream>>>(a);
-  }
+  decode_stage1_v0<D><<<dim3(a.n_split, a.num_kv_heads, a.batch), dim3(kThreads), 0, stream>>>(a);
   decode_combine<D><<<dim3(a.batch * a.num_kv_heads), dim3(256), 0, stream>>>(a);
   return hipGetLastError();
 }
@@ -311,7 +307,8 @@ DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_di
   }
   auto align = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
   const size_t rows = static_cast<size_t>(batch) * num_q_heads;
-  p.off_qp = 0;
+  p.off_cnt = 0;
+  p.off_qp = align(static_cast<size_t>(batch) * num_kv_heads * sizeof(int));
   p.off_sinkp = align(p.off_qp + rows * head_dim * sizeof(float));
   p.off_ml = align(p.off_sinkp + rows * sizeof(float));
   p.off_acc = align(p.off_ml + rows * max_split * 2 * sizeof(float));

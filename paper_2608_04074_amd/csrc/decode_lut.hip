@@ -31,6 +31,7 @@ namespace novakv {
 namespace {
 
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 typedef short short4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
@@ -43,12 +44,19 @@ constexpr uint32_t kLutBytes = 65536;       // [256 codes][32 groups][4 heads] f
 constexpr uint32_t kVBase = kLutBytes;      // value codebook, 64 KB
 constexpr uint32_t kMergeBase = 0;          // per-wave merge scratch, reuses the table once done
 constexpr int kMergeFloats = 4 * kD + 8;
+// Auxiliary region: query staging and the partial sums of q', later the
+// combine's merged accumulator and partial outputs, and a few control words.
+constexpr uint32_t kAuxQ = 2 * 65536;               // [4][128] f32
+constexpr uint32_t kAuxPart = kAuxQ + 4 * kD * 4;   // [8 parts][4 heads][128] f32
+constexpr uint32_t kAuxCtl = kAuxPart + 32 * kD * 4;
+constexpr uint32_t kLdsBytes = kAuxCtl + 64;
 
 template <int WAVES>
 constexpr uint32_t lds_bytes() {
   static_assert(WAVES * kMergeFloats * 4 <= kLutBytes, "merge scratch must fit in the table region");
   static_assert(WAVES >= kL / 4, "one wave per group block builds the table");
-  return 2 * 65536;
+  static_assert(WAVES * 64 >= 512, "512 threads form q' and apply t_v");
+  return kLdsBytes;
 }
 
 __device__ __forceinline__ half4_t tr16_read(uint32_t addr) {
@@ -93,6 +101,27 @@ template <int N>
 __device__ __forceinline__ float row_ror(float x) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x120 + N, 0xf, 0xf, false));
 }
+// Split partials and arrival counters are exchanged between workgroups that
+// may sit on different XCDs, each with its own L2.  Every access to them is a
+// relaxed agent-scope atomic (a load or store with device coherence that
+// bypasses the non-coherent caches); ordering comes from waiting for these
+// stores to complete before the arrival is counted, and from issuing the
+// loads only after the last arrival has been observed.  This avoids the L2
+// write-back and invalidation that a device-wide fence costs on this part.
+__device__ __forceinline__ void store_dev(float *p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_dev(const float *p) {
+  return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+  x += row_ror<8>(x);
+  x += row_ror<4>(x);
+  x += row_ror<2>(x);
+  x += row_ror<1>(x);
+  return add_rows32(add_rows16(x));
+}
 
 // Byte offset of the code row of token `t_start` (16-aligned) in the pools,
 // for a 16-token sub-tile that lies inside one cache block.
@@ -107,34 +136,30 @@ __device__ __forceinline__ size_t subtile_offset(const DecodeArgs &a, int b, int
   return ((static_cast<size_t>(phys) * a.num_kv_heads + kv) * bs + row) * kL;
 }
 
+// Work of one (sequence, KV head, split) unit that attends to at least one
+// token: q' of the unit's query heads, the two LDS tables, the token loop, and
+// the split's partials (max in natural-log units, denominator, accumulator).
+// Thread t < 512 of a workgroup holds row (t mod 128) of t_v, columns
+// 32 * (t / 128) .. +31, for the inverse value transform of the combine.
+__device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, float4 (&tv)[8]) {
+  const int tid = threadIdx.x;
+  if (tid < 512) {
+    const float4 *row = reinterpret_cast<const float4 *>(a.t_v + (static_cast<size_t>(kv) * kD + (tid & (kD - 1))) * kD) +
+                        8 * (tid >> 7);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) tv[i] = row[i];
+  }
+}
+
 template <int WAVES>
-__global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
+__device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
+                                           const int split, const int t0, const int t1, const size_t row0,
+                                           float4 (&tv)[8]) {
   const uint32_t sbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8_ptr)smem));
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int split = blockIdx.x % a.n_split;
-  const int bk = blockIdx.x / a.n_split;
-  const int b = bk / a.num_kv_heads;
-  const int kv = bk - b * a.num_kv_heads;
   const int G = a.gqa;
-
-  const int S = a.seq_lens[b];
-  const int lo = a.window > 0 ? max(0, S - a.window) : 0;
-  const int t0 = max(lo, split * a.chunk);
-  const int t1 = min(S, (split + 1) * a.chunk);
-  const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
-
-  if (t0 >= t1) {  // nothing attended in this split
-    for (int i = tid; i < G * kD; i += WAVES * 64)
-      a.part_acc[((row0 + i / kD) * a.n_split + split) * kD + (i % kD)] = 0.f;
-    if (tid < G) {
-      a.part_ml[2 * ((row0 + tid) * a.n_split + split)] = -INFINITY;
-      a.part_ml[2 * ((row0 + tid) * a.n_split + split) + 1] = 0.f;
-    }
-    return;
-  }
 
   // ---- lane roles
   const int beta = lane >> 4, u = (lane >> 2) & 3, v = lane & 3;
@@ -161,7 +186,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   const uint8_t *vpool = a.v_codes;
 
   // Code bytes of one round: K windows (bytes 8u..8u+7 of tokens R+16r+4beta+v) and
-  // V windows (bytes 8v..8v+7 of tokens R+16u+4beta+s).
+  // V windows (bytes 8v..8v+7 of tokens R+16beta+4u+s).
   auto load_round = [&](int R, uint2 *kw, uint2 *vw) {
     size_t sub[4];
 #pragma unroll
@@ -169,10 +194,10 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
 #pragma unroll
     for (int r = 0; r < 4; ++r)
       kw[r] = *reinterpret_cast<const uint2 *>(kpool + sub[r] + (4 * beta + v) * kL + 8 * u);
-    const size_t subu = u == 0 ? sub[0] : (u == 1 ? sub[1] : (u == 2 ? sub[2] : sub[3]));
+    const size_t subb = beta == 0 ? sub[0] : (beta == 1 ? sub[1] : (beta == 2 ? sub[2] : sub[3]));
 #pragma unroll
     for (int s = 0; s < 4; ++s)
-      vw[s] = *reinterpret_cast<const uint2 *>(vpool + subu + (4 * beta + s) * kL + 8 * v);
+      vw[s] = *reinterpret_cast<const uint2 *>(vpool + subb + (4 * u + s) * kL + 8 * v);
   };
   // Two named buffers of code bytes alternate through the token loop (unrolled
   // by two), so no in-flight load destination is ever copied: round rd+W is in
@@ -182,45 +207,110 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
 
   // ---- setup: value codebook into LDS, table of partial logits via MFMA.
   // All global loads of the setup are issued before any of them is used.
-  // Value entry (g, c) goes to kVBase + (g&7)*8192 + 32c + 8(g>>3).
-  // Table tile (gb, cb) = groups 4gb..4gb+3 x codes 16cb..16cb+15:
-  //   C[(gq,h)][code] = sum_i q'_h[4(4gb+gq)+i] * C_K[4gb+gq][code][i].
+  // Value entry (g, c) goes to kVBase + (g&7)*8192 + 32c + 8(g>>3); element e
+  // of the staging pass maps to (g, c) so that the 32 lanes of a half-wave
+  // write 32 distinct bank pairs.
+  // Table: the 16-block 4x4x4 MFMA gives every 4-lane block its own group, so
+  // one instruction produces 16 groups x 4 codes x 4 heads:
+  //   LUT[c][g][h] = sum_i q'_h[4g+i] * C_K[g][c][i].
   {
     constexpr int NT = WAVES * 64;
+    // q' = q t_k_inv_t (Theorem 1: the query side of the key transform),
+    // formed here for the unit's query heads.  Thread (jq, e4) < 512 holds
+    // rows 8*jq .. 8*jq+7 of columns 4*e4 .. 4*e4+3.
+    const int e4 = tid & 31, jq = tid >> 5;
+    float qval = 0.f;
+    float4 trow[8];
+    if (tid < 512) {
+      const int qh = tid >> 7;
+      if (qh < G) {
+        const size_t qi = (row0 + qh) * kD + (tid & (kD - 1));
+        qval = a.q_bf16 ? bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi])
+                        : static_cast<const float *>(a.q)[qi];
+      }
+      const float4 *tk = reinterpret_cast<const float4 *>(a.t_k_inv_t + (static_cast<size_t>(kv) * kD + 8 * jq) * kD) + e4;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) trow[r] = tk[r * (kD / 4)];
+    }
     constexpr int VPER = (kL * 256 + NT - 1) / NT;
     const uint2 *vsrc = reinterpret_cast<const uint2 *>(a.cb_v + static_cast<size_t>(kv) * kL * 256 * 4);
+    auto vmap = [](int e, int &g, int &c) {
+      const int r = e >> 5;
+      g = 8 * ((e >> 3) & 3) + (r & 7);
+      c = 8 * (r >> 3) + (e & 7);
+    };
     uint2 vst[VPER];
 #pragma unroll
     for (int k = 0; k < VPER; ++k) {
       const int e = tid + k * NT;
-      if (e < kL * 256) vst[k] = vsrc[e];
-    }
-    const int m = lane & 15, kq = lane >> 4;
-    const int gq = m >> 2, h = m & 3;
-    const uint16_t *cbk = a.cb_k + static_cast<size_t>(kv) * kL * 256 * 4;
-    const bool lut_wave = wave < kL / 4;        // one group block per wave
-    const int gb = wave;
-    uint2 kst[16];
-    float qv[4] = {0.f, 0.f, 0.f, 0.f};
-    if (lut_wave) {
-#pragma unroll
-      for (int cb = 0; cb < 16; ++cb)
-        kst[cb] = *reinterpret_cast<const uint2 *>(
-            cbk + (static_cast<size_t>(4 * gb + kq) * 256 + 16 * cb + m) * 4);
-      if (kq == gq && h < G) {
-        const float4 q4 = *reinterpret_cast<const float4 *>(a.qp + (row0 + h) * kD + 4 * (4 * gb + kq));
-        qv[0] = q4.x; qv[1] = q4.y; qv[2] = q4.z; qv[3] = q4.w;
+      if (e < kL * 256) {
+        int g, c;
+        vmap(e, g, c);
+        vst[k] = vsrc[g * 256 + c];
       }
     }
+    // table waves: group set (wave & 1) of 16 groups, code range 64*(wave >> 1) .. +63
+    const bool lut_wave = wave < 8;
+    const int lg = 16 * (wave & 1) + (lane >> 2);  // this lane's group
+    const int lj = lane & 3;                       // head (A operand) / code in a quad (B, D)
+    const int cbase = 64 * (wave >> 1);
+    const uint2 *cbk = reinterpret_cast<const uint2 *>(a.cb_k + static_cast<size_t>(kv) * kL * 256 * 4);
+    uint2 kst[16];
+    if (lut_wave) {
+#pragma unroll
+      for (int t = 0; t < 16; ++t) kst[t] = cbk[lg * 256 + cbase + 4 * t + lj];
+    }
+    float *qs = reinterpret_cast<float *>(smem + kAuxQ);       // [4][128] query
+    float *qsum = reinterpret_cast<float *>(smem + kAuxPart);  // [8 parts][4 heads][128] partial q'
+    if (tid < 512) qs[tid] = qval;
 #pragma unroll
     for (int k = 0; k < VPER; ++k) {
       const int e = tid + k * NT;
       if (e < kL * 256) {
-        const int g = e >> 8, c = e & 255;
+        int g, c;
+        vmap(e, g, c);
         *reinterpret_cast<uint2 *>(smem + kVBase + (g & 7) * 8192 + (c << 5) + 8 * (g >> 3)) = vst[k];
       }
     }
+    __syncthreads();
+    if (tid < 512) {
+      float4 acc[4];
+#pragma unroll
+      for (int hh = 0; hh < 4; ++hh) {
+        acc[hh] = make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 q0 = *reinterpret_cast<const float4 *>(qs + hh * kD + 8 * jq);
+        const float4 q1 = *reinterpret_cast<const float4 *>(qs + hh * kD + 8 * jq + 4);
+        const float qq[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          acc[hh].x = fmaf(qq[r], trow[r].x, acc[hh].x);
+          acc[hh].y = fmaf(qq[r], trow[r].y, acc[hh].y);
+          acc[hh].z = fmaf(qq[r], trow[r].z, acc[hh].z);
+          acc[hh].w = fmaf(qq[r], trow[r].w, acc[hh].w);
+        }
+      }
+      // lanes l and l + 32 hold rows of the same columns: fold them, one part per wave
+#pragma unroll
+      for (int hh = 0; hh < 4; ++hh) {
+        acc[hh].x = add_rows32(acc[hh].x);
+        acc[hh].y = add_rows32(acc[hh].y);
+        acc[hh].z = add_rows32(acc[hh].z);
+        acc[hh].w = add_rows32(acc[hh].w);
+        if (lane < 32) *reinterpret_cast<float4 *>(qsum + (wave * 4 + hh) * kD + 4 * e4) = acc[hh];
+      }
+    }
+    __syncthreads();
     if (lut_wave) {
+      float qv[4] = {0.f, 0.f, 0.f, 0.f};
+      if (lj < G) {
+#pragma unroll
+        for (int pp = 0; pp < 8; ++pp) {
+          const float4 x4 = *reinterpret_cast<const float4 *>(qsum + (pp * 4 + lj) * kD + 4 * lg);
+          qv[0] += x4.x; qv[1] += x4.y; qv[2] += x4.z; qv[3] += x4.w;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) qv[i] *= a.qscale;
+      }
       half4_t a_hi, a_lo;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -229,49 +319,66 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
         a_lo[i] = static_cast<_Float16>(qv[i] - static_cast<float>(hi));
       }
 #pragma unroll
-      for (int cb = 0; cb < 16; ++cb) {
-        const half4_t bv = __builtin_bit_cast(half4_t, kst[cb]);
+      for (int t = 0; t < 16; ++t) {
+        const half4_t bv = __builtin_bit_cast(half4_t, kst[t]);
         float4_t c = {0.f, 0.f, 0.f, 0.f};
-        c = __builtin_amdgcn_mfma_f32_16x16x16f16(a_hi, bv, c, 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_16x16x16f16(a_lo, bv, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_hi, bv, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_lo, bv, c, 0, 0, 0);
         half4_t o;
         o[0] = static_cast<_Float16>(c[0]);
         o[1] = static_cast<_Float16>(c[1]);
         o[2] = static_cast<_Float16>(c[2]);
         o[3] = static_cast<_Float16>(c[3]);
-        // lane (code 16cb+m, group 4gb+kq) holds the 4 heads
-        *reinterpret_cast<half4_t *>(smem + (16 * cb + m) * 256 + (4 * gb + kq) * 8) = o;
+        // lane (group lg, code cbase + 4t + lj) holds the 4 heads
+        *reinterpret_cast<half4_t *>(smem + (cbase + 4 * t + lj) * 256 + lg * 8) = o;
       }
     }
   }
   __syncthreads();
 
+  // Selector of the key-side MFMA: row block r of the accumulator receives the
+  // table partials of sub-tile r (A[m][k] = 1 where m = 4r + k-row).
+  half8_t asel[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const _Float16 one = ((lane & 15) == 4 * r + beta) ? static_cast<_Float16>(1.f) : static_cast<_Float16>(0.f);
+    asel[r] = half8_t{one, one, one, one, one, one, one, one};
+  }
+
   auto process_round = [&](const int R, const uint2 *kw, const uint2 *vw) {
-    // K: logits of tokens R + 16r + 4beta + u for head v (log2 units); the four
-    // sub-tiles are independent chains, interleaved step by step.
+    // K: partial logits gathered from the table by transposing reads; each
+    // read hands lane (beta,u,v) four partials of (token R+16r+4beta+u, head v)
+    // and serves as the B operand of a 16x16x32 MFMA (two steps per MFMA)
+    // whose selector A sums them into accumulator row 4r+beta, column (u,v).
+    // Lane (tau,u,v) then holds in register i the logit of token
+    // R + 16 tau + 4 i + u for head v (log2 units), tau = lane >> 4.
     uint32_t w0[4], w1[4];
-    float zs[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       w0[r] = __builtin_amdgcn_perm(kw[r].y, kw[r].x, rsel0);
       w1[r] = __builtin_amdgcn_perm(kw[r].y, kw[r].x, rsel1);
-      zs[r] = 0.f;
     }
+    float4_t kacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      const uint32_t sel = 0x0C0C0000u | ((4u + (t & 3)) << 8) | (t & 3);
-      half4_t e[4];
+    for (int tp = 0; tp < 4; ++tp) {
+      half8_t e[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        e[r] = tr16_read(sbase + __builtin_amdgcn_perm(t < 4 ? w0[r] : w1[r], t < 4 ? kc0 : kc1, sel));
+      for (int r = 0; r < 4; ++r) {
+        const uint32_t w = tp < 2 ? w0[r] : w1[r];
+        const uint32_t kc = tp < 2 ? kc0 : kc1;
+        const uint32_t ta = (2 * tp) & 3, tb = (2 * tp + 1) & 3;
+        const half4_t lo = tr16_read(sbase + __builtin_amdgcn_perm(w, kc, 0x0C0C0000u | ((4u + ta) << 8) | ta));
+        const half4_t hi = tr16_read(sbase + __builtin_amdgcn_perm(w, kc, 0x0C0C0000u | ((4u + tb) << 8) | tb));
+        e[r] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) zs[r] = sum4(e[r], zs[r]);
+      for (int r = 0; r < 4; ++r) kacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(asel[r], e[r], kacc, 0, 0, 0);
     }
     float z[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int tok = R + 16 * r + 4 * beta + u;
-      z[r] = (tok >= t0 && tok < t1) ? zs[r] : -INFINITY;
+    for (int i = 0; i < 4; ++i) {
+      const int tok = R + 16 * beta + 4 * i + u;
+      z[i] = (tok >= t0 && tok < t1) ? kacc[i] : -INFINITY;
     }
 
     // online softmax over the round.  Accumulator column (u, v) of the value
@@ -288,7 +395,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
     float p[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) p[r] = __builtin_amdgcn_exp2f(z[r] - m_ref);
+    for (int i = 0; i < 4; ++i) p[i] = __builtin_amdgcn_exp2f(z[i] - m_ref);
     l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
     m_run = m_new;
     if (__any(alpha != 1.f)) {
@@ -299,29 +406,27 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
                         static_cast<_Float16>(p[2]), static_cast<_Float16>(p[3])};
     const half4_t zero4 = {0, 0, 0, 0};
 
-    // V: for token set s (tokens R + 16k + 4beta + s), coordinates of groups 8*(0..3) + X.
-    // The eight reads of a set are issued one set ahead of its MFMAs.
-    auto v_reads = [&](int s, half4_t *av) {
+    // V: token sets s (tokens R + 16 beta + 4 i + s) in pairs; the A operand of
+    // tile X holds coordinates of groups 8*(0..3) + X for the pair's 8 tokens
+    // of each lane row, the B operand the matching probabilities of column
+    // (set, head) = (u, v), zero where u is not the set.
+#pragma unroll
+    for (int sp = 0; sp < 2; ++sp) {
+      const int s0 = 2 * sp, s1 = 2 * sp + 1;
+      const half8_t bpair = __builtin_shufflevector(u == s0 ? pb : zero4, u == s1 ? pb : zero4, 0, 1, 2, 3, 4, 5, 6, 7);
+      half8_t av[8];
 #pragma unroll
       for (int X = 0; X < 8; ++X) {
-        const uint32_t word = X < 4 ? vw[s].x : vw[s].y;
-        const uint32_t c = (word >> (8 * (X & 3))) & 0xffu;
-        av[X] = tr16_read(vbase + (c << 5) + X * 8192);
+        const uint32_t wa = X < 4 ? vw[s0].x : vw[s0].y;
+        const uint32_t wb = X < 4 ? vw[s1].x : vw[s1].y;
+        const uint32_t ca = (wa >> (8 * (X & 3))) & 0xffu;
+        const uint32_t cb = (wb >> (8 * (X & 3))) & 0xffu;
+        const half4_t lo = tr16_read(vbase + (ca << 5) + X * 8192);
+        const half4_t hi = tr16_read(vbase + (cb << 5) + X * 8192);
+        av[X] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
       }
-    };
-    half4_t avA[8], avB[8];
-    v_reads(0, avA);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      half4_t *cur = (s & 1) ? avB : avA;
-      half4_t *nxt = (s & 1) ? avA : avB;
-      if (s < 3) v_reads(s + 1, nxt);
-      __builtin_amdgcn_sched_barrier(0);
-      const half4_t bset = (u == s) ? pb : zero4;
-#pragma unroll
-      for (int X = 0; X < 8; ++X)
-        acc[X] = __builtin_amdgcn_mfma_f32_16x16x16f16(cur[X], bset, acc[X], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
+      for (int X = 0; X < 8; ++X) acc[X] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av[X], bpair, acc[X], 0, 0, 0);
     }
   };
 
@@ -332,6 +437,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
     if (rd + 2 * WAVES < nrounds) load_round(R0 + 64 * (rd + 2 * WAVES), kwA, vwA);
     process_round(R0 + 64 * (rd + WAVES), kwB, vwB);
   }
+  load_tv_rows(a, kv, tv);
 
   // ---- per-wave reduction.  l over the rows of a column; then the four
   // columns u of head v are rescaled to their common max and summed (lanes
@@ -387,12 +493,160 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
       }
     }
     const size_t r = (row0 + h) * a.n_split + split;
-    a.part_acc[r * kD + d] = num;
+    store_dev(a.part_acc + r * kD + d, num);
     if (d == 0) {
-      a.part_ml[2 * r] = big == -INFINITY ? -INFINITY : big * kLn2;
-      a.part_ml[2 * r + 1] = den;
+      store_dev(a.part_ml + 2 * r, big == -INFINITY ? -INFINITY : big * kLn2);
+      store_dev(a.part_ml + 2 * r + 1, den);
     }
   }
+}
+
+// Last arriving split of a (sequence, KV head): log-sum-exp merge of the
+// splits' partials, the sink added once with its shift -(q . k_bar) * scale
+// (Lemma S1; appendix on attention sinks), division by the denominator, and
+// the inverse value transform out = s_hat t_v^T (Corollary 1).
+template <int WAVES>
+__device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int kv, const size_t row0,
+                                             const float4 (&tv)[8]) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int G = a.gqa;
+  float *shat = reinterpret_cast<float *>(smem + kAuxQ);     // [4][128]
+  float *outp = reinterpret_cast<float *>(smem + kAuxPart);  // [part][head][128]
+  float *sinkp = reinterpret_cast<float *>(smem + kAuxCtl + 16);
+  const int d = tid & (kD - 1), jp = tid >> 7;  // tv holds row d of t_v, columns 32*jp .. 32*jp+31
+  if (wave < G) {
+    const size_t qi = (row0 + wave) * kD + 2 * lane;
+    float q0, q1;
+    if (a.q_bf16) {
+      q0 = bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi]);
+      q1 = bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi + 1]);
+    } else {
+      q0 = static_cast<const float *>(a.q)[qi];
+      q1 = static_cast<const float *>(a.q)[qi + 1];
+    }
+    const float *kb = a.kbar + static_cast<size_t>(kv) * kD + 2 * lane;
+    const float dot = wave_sum(fmaf(q0, kb[0], q1 * kb[1]));
+    if (lane == 0) sinkp[wave] = a.sinks ? a.sinks[kv * G + wave] - a.scale * dot : -INFINITY;
+  }
+  __syncthreads();
+  if (tid < G * kD) {
+    const int h = tid >> 7;
+    const size_t r = (row0 + h) * a.n_split;
+    const float sk = sinkp[h];
+    // online log-sum-exp over the splits, the sink counted once; the loads of
+    // up to 8 splits are issued together
+    float big = sk, num = 0.f, den = sk == -INFINITY ? 0.f : 1.f;
+    for (int s0 = 0; s0 < a.n_split; s0 += 8) {
+      float ms[8], ls[8], as[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        ms[i] = -INFINITY;
+        ls[i] = 0.f;
+        as[i] = 0.f;
+        if (s0 + i < a.n_split) {
+          ms[i] = load_dev(a.part_ml + 2 * (r + s0 + i));
+          ls[i] = load_dev(a.part_ml + 2 * (r + s0 + i) + 1);
+          as[i] = load_dev(a.part_acc + (r + s0 + i) * kD + d);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if (ms[i] == -INFINITY) continue;
+        if (ms[i] > big) {
+          const float f = big == -INFINITY ? 0.f : __expf(big - ms[i]);
+          num *= f;
+          den *= f;
+          big = ms[i];
+        }
+        const float w = __expf(ms[i] - big);
+        den = fmaf(w, ls[i], den);
+        num = fmaf(w, as[i], num);
+      }
+    }
+    shat[tid] = den > 0.f ? num / den : 0.f;
+  } else if (tid < 4 * kD) {
+    shat[tid] = 0.f;
+  }
+  __syncthreads();
+  if (tid < 512) {
+    float o[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const float4 sv = *reinterpret_cast<const float4 *>(shat + h * kD + 32 * jp + 4 * i);
+        o[h] = fmaf(sv.x, tv[i].x, o[h]);
+        o[h] = fmaf(sv.y, tv[i].y, o[h]);
+        o[h] = fmaf(sv.z, tv[i].z, o[h]);
+        o[h] = fmaf(sv.w, tv[i].w, o[h]);
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < 4; ++h) outp[(jp * 4 + h) * kD + d] = o[h];
+  }
+  __syncthreads();
+  if (tid < G * kD) {
+    const int h = tid >> 7;
+    a.out[(row0 + h) * kD + d] =
+        (outp[h * kD + d] + outp[(4 + h) * kD + d]) + (outp[(8 + h) * kD + d] + outp[(12 + h) * kD + d]);
+  }
+}
+
+// One workgroup per (sequence, KV head, split).  Every split publishes its
+// partials and counts its arrival; the last one of a (sequence, KV head)
+// combines them, so a decode step is a single launch.  The arrival counters
+// live in the workspace; the last arrival resets its counter to zero.
+template <int WAVES>
+__global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
+  const int tid = threadIdx.x;
+  // Workgroups are dealt to the XCDs round-robin; with the KV head varying
+  // fastest, all workgroups of a KV head (its parameters, its splits) land on
+  // one XCD when the KV head count divides or is a multiple of 8.
+  const int kv = blockIdx.x % a.num_kv_heads;
+  const int rest = blockIdx.x / a.num_kv_heads;
+  const int split = rest % a.n_split;
+  const int b = rest / a.n_split;
+  const int bk = b * a.num_kv_heads + kv;
+  const int G = a.gqa;
+
+  const int S = a.seq_lens[b];
+  const int lo = a.window > 0 ? max(0, S - a.window) : 0;
+  const int t0 = max(lo, split * a.chunk);
+  const int t1 = min(S, (split + 1) * a.chunk);
+  const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
+
+  // Rows of t_v for the combine are requested as soon as the split's token
+  // loop ends, before the arrival is known, so that the last arrival finds
+  // them in flight or in the cache.
+  float4 tv[8];
+  if (t0 < t1) {
+    split_pass<WAVES>(a, smem, b, kv, split, t0, t1, row0, tv);
+  } else {
+    load_tv_rows(a, kv, tv);
+  }
+  if (t0 >= t1 && tid < G) {  // nothing attended in this split
+    store_dev(a.part_ml + 2 * ((row0 + tid) * a.n_split + split), -INFINITY);
+    store_dev(a.part_ml + 2 * ((row0 + tid) * a.n_split + split) + 1, 0.f);
+  }
+
+  __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
+  __syncthreads();
+  int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
+  if (tid == 0) {
+    int last = 1;
+    if (a.n_split > 1) {
+      last = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+             a.n_split - 1;
+      if (last) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    ctl[0] = last;
+  }
+  __syncthreads();
+  if (ctl[0] == 0) return;
+  combine_unit<WAVES>(a, smem, kv, row0, tv);
 }
 
 }  // namespace

@@ -43,6 +43,7 @@ struct DecodeArgs {
   float qscale;     // factor folded into q' (scale, or scale * log2(e) for the table path)
   float *out;
   // workspace carve-out
+  int *counters;    // [B][Hkv]       split arrival counters (zero between calls)
   float *qp;        // [B][Hq][D]     pre-transformed, pre-scaled queries
   float *sinkp;     // [B][Hq]        shifted sink logits (-inf when no sink)
   float *part_ml;   // [B][Hq][n_split][2]  running max, denominator
@@ -67,7 +68,7 @@ struct DecodePlan {
   int use_lut;      // 1: table-based stage 1 (decode_lut.hip), 0: generic stage 1
   int n_split;
   int chunk;
-  size_t off_qp, off_sinkp, off_ml, off_acc, total;
+  size_t off_cnt, off_qp, off_sinkp, off_ml, off_acc, total;
 };
 // block_size <= 0 plans for the worst case over both stage-1 kernels.
 DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_dim,
@@ -75,7 +76,8 @@ DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_di
 
 hipError_t launch_decode(const DecodeArgs &a, int use_lut, hipStream_t stream);
 
-// Table-based stage 1 (head_dim 128, <= 4 query heads per KV head, 16-token-aligned blocks).
+// Table-based decode (head_dim 128, <= 4 query heads per KV head, 16-token-aligned
+// blocks): query transform, split pass and combine in one launch.
 bool lut_path_eligible(int head_dim, int gqa, int block_size);
 void plan_lut(int batch, int num_kv_heads, int max_seq_len, int *n_split, int *chunk);
 hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream);
