@@ -44,11 +44,17 @@ constexpr uint32_t kLutBytes = 65536;       // [256 codes][32 groups][4 heads] f
 constexpr uint32_t kVBase = kLutBytes;      // value codebook, 64 KB
 constexpr uint32_t kMergeBase = 0;          // per-wave merge scratch, reuses the table once done
 constexpr int kMergeFloats = 4 * kD + 8;
+constexpr float kLazyLog2 = 8.f;  // reference lag allowed in the online softmax (log2 units)
 // Auxiliary region: query staging and the partial sums of q', later the
 // combine's merged accumulator and partial outputs, and a few control words.
 constexpr uint32_t kAuxQ = 2 * 65536;               // [4][128] f32
 constexpr uint32_t kAuxPart = kAuxQ + 4 * kD * 4;   // [8 parts][4 heads][128] f32
 constexpr uint32_t kAuxCtl = kAuxPart + 32 * kD * 4;
+// After the setup the partial-sum area holds the split's own merged partial
+// ([4][128] accumulator at kAuxOwn) and the combine's partial outputs.
+constexpr uint32_t kAuxOwn = kAuxPart;
+constexpr uint32_t kAuxOut = kAuxPart + 4 * kD * 4;
+// control words: [0] arrival state, [4..8) shifted sink logits, [8..16) own (m, l) per head
 constexpr uint32_t kLdsBytes = kAuxCtl + 64;
 
 template <int WAVES>
@@ -56,6 +62,7 @@ constexpr uint32_t lds_bytes() {
   static_assert(WAVES * kMergeFloats * 4 <= kLutBytes, "merge scratch must fit in the table region");
   static_assert(WAVES >= kL / 4, "one wave per group block builds the table");
   static_assert(WAVES * 64 >= 512, "512 threads form q' and apply t_v");
+  static_assert(WAVES >= 12, "waves 8..11 form the shifted sink logits");
   return kLdsBytes;
 }
 
@@ -125,11 +132,12 @@ __device__ __forceinline__ float wave_sum(float x) {
 
 // Byte offset of the code row of token `t_start` (16-aligned) in the pools,
 // for a 16-token sub-tile that lies inside one cache block.
-__device__ __forceinline__ size_t subtile_offset(const DecodeArgs &a, int b, int kv, int t_start) {
+// bs_shift = log2(block_size) when it is a power of two, else -1.
+__device__ __forceinline__ size_t subtile_offset(const DecodeArgs &a, int b, int kv, int t_start, int bs_shift) {
   const int bs = a.layout.block_size;
   if (a.layout.block_table == nullptr && a.layout.blocks_per_seq == 1)
     return ((static_cast<size_t>(b) * a.num_kv_heads + kv) * bs + t_start) * kL;
-  const int blk = t_start / bs;
+  const int blk = bs_shift >= 0 ? (t_start >> bs_shift) : t_start / bs;
   const int row = t_start - blk * bs;
   const int logical = b * a.layout.blocks_per_seq + blk;
   const int phys = a.layout.block_table ? a.layout.block_table[logical] : logical;
@@ -187,17 +195,23 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 
   // Code bytes of one round: K windows (bytes 8u..8u+7 of tokens R+16r+4beta+v) and
   // V windows (bytes 8v..8v+7 of tokens R+16beta+4u+s).
+  const int bsz = a.layout.block_size;
+  const int bs_shift = (bsz & (bsz - 1)) == 0 ? __builtin_ctz(bsz) : -1;
+  const uint32_t koff = (4 * beta + v) * kL + 8 * u;  // lane offsets inside a 16-token sub-tile
+  const uint32_t voff = 4 * u * kL + 8 * v;
   auto load_round = [&](int R, uint2 *kw, uint2 *vw) {
-    size_t sub[4];
+    size_t sub[4];  // uniform: byte offsets of the round's four sub-tiles
 #pragma unroll
-    for (int r = 0; r < 4; ++r) sub[r] = subtile_offset(a, b, kv, min(R + 16 * r, last16));
+    for (int r = 0; r < 4; ++r) sub[r] = subtile_offset(a, b, kv, min(R + 16 * r, last16), bs_shift);
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
-      kw[r] = *reinterpret_cast<const uint2 *>(kpool + sub[r] + (4 * beta + v) * kL + 8 * u);
+    for (int r = 0; r < 4; ++r) {
+      const uint8_t *kb = kpool + sub[r];
+      kw[r] = *reinterpret_cast<const uint2 *>(kb + koff);
+    }
     const size_t subb = beta == 0 ? sub[0] : (beta == 1 ? sub[1] : (beta == 2 ? sub[2] : sub[3]));
+    const uint8_t *vb = vpool + subb;
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-      vw[s] = *reinterpret_cast<const uint2 *>(vpool + subb + (4 * u + s) * kL + 8 * v);
+    for (int s = 0; s < 4; ++s) vw[s] = *reinterpret_cast<const uint2 *>(vb + voff + s * kL);
   };
   // Two named buffers of code bytes alternate through the token loop (unrolled
   // by two), so no in-flight load destination is ever copied: round rd+W is in
@@ -260,6 +274,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
       for (int t = 0; t < 16; ++t) kst[t] = cbk[lg * 256 + cbase + 4 * t + lj];
     }
+    // waves 8 .. 8+G-1 form the shifted sink logit of head wave-8 (Lemma S1)
+    const int sh = wave - 8;
+    float2 kb2 = make_float2(0.f, 0.f);
+    if (sh >= 0 && sh < G) kb2 = *reinterpret_cast<const float2 *>(a.kbar + static_cast<size_t>(kv) * kD + 2 * lane);
     float *qs = reinterpret_cast<float *>(smem + kAuxQ);       // [4][128] query
     float *qsum = reinterpret_cast<float *>(smem + kAuxPart);  // [8 parts][4 heads][128] partial q'
     if (tid < 512) qs[tid] = qval;
@@ -273,6 +291,11 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       }
     }
     __syncthreads();
+    if (sh >= 0 && sh < G) {
+      const float dot = wave_sum(fmaf(qs[sh * kD + 2 * lane], kb2.x, qs[sh * kD + 2 * lane + 1] * kb2.y));
+      if (lane == 0)
+        reinterpret_cast<float *>(smem + kAuxCtl)[4 + sh] = a.sinks ? a.sinks[kv * G + sh] - a.scale * dot : -INFINITY;
+    }
     if (tid < 512) {
       float4 acc[4];
 #pragma unroll
@@ -374,11 +397,13 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
       for (int r = 0; r < 4; ++r) kacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(asel[r], e[r], kacc, 0, 0, 0);
     }
-    float z[4];
+    float z[4] = {kacc[0], kacc[1], kacc[2], kacc[3]};
+    if (R < t0 || R + 64 > t1) {  // ragged first or last round of the split
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int tok = R + 16 * beta + 4 * i + u;
-      z[i] = (tok >= t0 && tok < t1) ? kacc[i] : -INFINITY;
+      for (int i = 0; i < 4; ++i) {
+        const int tok = R + 16 * beta + 4 * i + u;
+        if (tok < t0 || tok >= t1) z[i] = -INFINITY;
+      }
     }
 
     // online softmax over the round.  Accumulator column (u, v) of the value
@@ -388,20 +413,24 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     float zmax = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
     zmax = max_rows16(zmax);
     zmax = max_rows32(zmax);
-    // A column may have no attended token yet (ragged first or last round):
-    // then its reference stays -inf and the exponent base is taken as 0.
+    // The reference of a column moves only when its max exceeds it by more
+    // than kLazyLog2, so the accumulator is rescaled rarely; probabilities
+    // relative to a lagging reference stay below 2^kLazyLog2.  A column with
+    // no attended token yet keeps reference -inf (exponent base taken as 0).
     const float m_new = fmaxf(m_run, zmax);
-    const float m_ref = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_ref);
+    const bool bump = m_new > m_run + kLazyLog2;
+    const float ref = bump ? m_new : m_run;
+    const float alpha = bump ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
+    const float base = ref == -INFINITY ? 0.f : ref;
     float p[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) p[i] = __builtin_amdgcn_exp2f(z[i] - m_ref);
+    for (int i = 0; i < 4; ++i) p[i] = __builtin_amdgcn_exp2f(z[i] - base);
     l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
-    m_run = m_new;
-    if (__any(alpha != 1.f)) {
+    if (__any(bump && m_run != -INFINITY)) {  // accumulators of -inf columns are zero
 #pragma unroll
       for (int X = 0; X < 8; ++X) acc[X] *= alpha;
     }
+    m_run = ref;
     const half4_t pb = {static_cast<_Float16>(p[0]), static_cast<_Float16>(p[1]),
                         static_cast<_Float16>(p[2]), static_cast<_Float16>(p[3])};
     const half4_t zero4 = {0, 0, 0, 0};
@@ -477,8 +506,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   }
   __syncthreads();
 
-  // ---- merge the waves and write this split's partials (natural-log max)
+  // ---- merge the waves into this split's partial (natural-log max), kept in LDS
   constexpr float kLn2 = 0.693147180559945309f;
+  float *own = reinterpret_cast<float *>(smem + kAuxOwn);
+  float *ownml = reinterpret_cast<float *>(smem + kAuxCtl) + 8;
   for (int i = tid; i < G * kD; i += WAVES * 64) {
     const int h = i / kD, d = i % kD;
     float big = -INFINITY;
@@ -492,11 +523,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
         den = fmaf(wt, merge[w * kMergeFloats + 4 + h], den);
       }
     }
-    const size_t r = (row0 + h) * a.n_split + split;
-    store_dev(a.part_acc + r * kD + d, num);
+    own[i] = num;
     if (d == 0) {
-      store_dev(a.part_ml + 2 * r, big == -INFINITY ? -INFINITY : big * kLn2);
-      store_dev(a.part_ml + 2 * r + 1, den);
+      ownml[2 * h] = big == -INFINITY ? -INFINITY : big * kLn2;
+      ownml[2 * h + 1] = den;
     }
   }
 }
@@ -504,66 +534,82 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 // Last arriving split of a (sequence, KV head): log-sum-exp merge of the
 // splits' partials, the sink added once with its shift -(q . k_bar) * scale
 // (Lemma S1; appendix on attention sinks), division by the denominator, and
-// the inverse value transform out = s_hat t_v^T (Corollary 1).
+// the inverse value transform out = s_hat t_v^T (Corollary 1).  The split's
+// own partial is read from LDS, the other non-empty splits' from the
+// workspace; splits that attend to no token published nothing and are skipped.
 template <int WAVES>
 __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int kv, const size_t row0,
+                                             const int own_split, const bool own_active, const int S, const int lo,
                                              const float4 (&tv)[8]) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = a.gqa;
-  float *shat = reinterpret_cast<float *>(smem + kAuxQ);     // [4][128]
-  float *outp = reinterpret_cast<float *>(smem + kAuxPart);  // [part][head][128]
-  float *sinkp = reinterpret_cast<float *>(smem + kAuxCtl + 16);
+  float *shat = reinterpret_cast<float *>(smem + kAuxQ);    // [4][128]
+  float *outp = reinterpret_cast<float *>(smem + kAuxOut);  // [part][head][128]
+  float *ctlf = reinterpret_cast<float *>(smem + kAuxCtl);
+  const float *own = reinterpret_cast<const float *>(smem + kAuxOwn);
   const int d = tid & (kD - 1), jp = tid >> 7;  // tv holds row d of t_v, columns 32*jp .. 32*jp+31
-  if (wave < G) {
-    const size_t qi = (row0 + wave) * kD + 2 * lane;
-    float q0, q1;
-    if (a.q_bf16) {
-      q0 = bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi]);
-      q1 = bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi + 1]);
-    } else {
-      q0 = static_cast<const float *>(a.q)[qi];
-      q1 = static_cast<const float *>(a.q)[qi + 1];
+  if (!own_active) {  // the setup did not run: form the shifted sink logits here
+    if (wave < G) {
+      const size_t qi = (row0 + wave) * kD + 2 * lane;
+      float q0, q1;
+      if (a.q_bf16) {
+        q0 = bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi]);
+        q1 = bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi + 1]);
+      } else {
+        q0 = static_cast<const float *>(a.q)[qi];
+        q1 = static_cast<const float *>(a.q)[qi + 1];
+      }
+      const float *kb = a.kbar + static_cast<size_t>(kv) * kD + 2 * lane;
+      const float dot = wave_sum(fmaf(q0, kb[0], q1 * kb[1]));
+      if (lane == 0) ctlf[4 + wave] = a.sinks ? a.sinks[kv * G + wave] - a.scale * dot : -INFINITY;
     }
-    const float *kb = a.kbar + static_cast<size_t>(kv) * kD + 2 * lane;
-    const float dot = wave_sum(fmaf(q0, kb[0], q1 * kb[1]));
-    if (lane == 0) sinkp[wave] = a.sinks ? a.sinks[kv * G + wave] - a.scale * dot : -INFINITY;
+    __syncthreads();
   }
-  __syncthreads();
   if (tid < G * kD) {
     const int h = tid >> 7;
     const size_t r = (row0 + h) * a.n_split;
-    const float sk = sinkp[h];
-    // online log-sum-exp over the splits, the sink counted once; the loads of
-    // up to 8 splits are issued together
+    const float sk = ctlf[4 + h];
+    // online log-sum-exp over the splits, the sink counted once
     float big = sk, num = 0.f, den = sk == -INFINITY ? 0.f : 1.f;
+    auto take = [&](float ms, float ls, float as) {
+      if (ms == -INFINITY) return;
+      if (ms > big) {
+        const float f = big == -INFINITY ? 0.f : __expf(big - ms);
+        num *= f;
+        den *= f;
+        big = ms;
+      }
+      const float w = __expf(ms - big);
+      den = fmaf(w, ls, den);
+      num = fmaf(w, as, num);
+    };
+    // splits in index order whichever split combines, so the result does not
+    // depend on the arrival order; the loads of up to 8 splits are issued together
     for (int s0 = 0; s0 < a.n_split; s0 += 8) {
       float ms[8], ls[8], as[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
+        const int sp = s0 + i;
         ms[i] = -INFINITY;
         ls[i] = 0.f;
         as[i] = 0.f;
-        if (s0 + i < a.n_split) {
-          ms[i] = load_dev(a.part_ml + 2 * (r + s0 + i));
-          ls[i] = load_dev(a.part_ml + 2 * (r + s0 + i) + 1);
-          as[i] = load_dev(a.part_acc + (r + s0 + i) * kD + d);
+        const bool nonempty = max(lo, sp * a.chunk) < min(S, (sp + 1) * a.chunk);
+        if (sp == own_split) {
+          if (own_active) {
+            ms[i] = ctlf[8 + 2 * h];
+            ls[i] = ctlf[8 + 2 * h + 1];
+            as[i] = own[tid];
+          }
+        } else if (sp < a.n_split && nonempty) {
+          ms[i] = load_dev(a.part_ml + 2 * (r + sp));
+          ls[i] = load_dev(a.part_ml + 2 * (r + sp) + 1);
+          as[i] = load_dev(a.part_acc + (r + sp) * kD + d);
         }
       }
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        if (ms[i] == -INFINITY) continue;
-        if (ms[i] > big) {
-          const float f = big == -INFINITY ? 0.f : __expf(big - ms[i]);
-          num *= f;
-          den *= f;
-          big = ms[i];
-        }
-        const float w = __expf(ms[i] - big);
-        den = fmaf(w, ls[i], den);
-        num = fmaf(w, as[i], num);
-      }
+      for (int i = 0; i < 8; ++i) take(ms[i], ls[i], as[i]);
     }
     shat[tid] = den > 0.f ? num / den : 0.f;
   } else if (tid < 4 * kD) {
@@ -594,10 +640,12 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
   }
 }
 
-// One workgroup per (sequence, KV head, split).  Every split publishes its
-// partials and counts its arrival; the last one of a (sequence, KV head)
-// combines them, so a decode step is a single launch.  The arrival counters
-// live in the workspace; the last arrival resets its counter to zero.
+// One workgroup per (sequence, KV head, split).  A split that is not the last
+// of its (sequence, KV head) publishes its partial to the workspace and
+// counts its arrival; the last one combines.  A split that finds every other
+// split already arrived is the last without publishing.  The arrival
+// counters live in the workspace and the last split resets its counter to 0,
+// so a decode step is a single launch.
 template <int WAVES>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
@@ -617,36 +665,54 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   const int t0 = max(lo, split * a.chunk);
   const int t1 = min(S, (split + 1) * a.chunk);
   const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
+  const bool active = t0 < t1;
 
   // Rows of t_v for the combine are requested as soon as the split's token
   // loop ends, before the arrival is known, so that the last arrival finds
   // them in flight or in the cache.
   float4 tv[8];
-  if (t0 < t1) {
+  if (active) {
     split_pass<WAVES>(a, smem, b, kv, split, t0, t1, row0, tv);
   } else {
     load_tv_rows(a, kv, tv);
   }
-  if (t0 >= t1 && tid < G) {  // nothing attended in this split
-    store_dev(a.part_ml + 2 * ((row0 + tid) * a.n_split + split), -INFINITY);
-    store_dev(a.part_ml + 2 * ((row0 + tid) * a.n_split + split) + 1, 0.f);
-  }
-
-  __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
-  __syncthreads();
   int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
+  __syncthreads();
   if (tid == 0) {
-    int last = 1;
+    int st = 1;  // 1: last without publishing
     if (a.n_split > 1) {
-      last = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-             a.n_split - 1;
-      if (last) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      st = __hip_atomic_load(a.counters + bk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.n_split - 1 ? 1 : 0;
+      if (st) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    ctl[0] = last;
+    ctl[0] = st;
   }
   __syncthreads();
-  if (ctl[0] == 0) return;
-  combine_unit<WAVES>(a, smem, kv, row0, tv);
+  if (ctl[0] == 0) {
+    if (active) {
+      const float *own = reinterpret_cast<const float *>(smem + kAuxOwn);
+      const float *ownml = reinterpret_cast<const float *>(smem + kAuxCtl) + 8;
+      for (int i = tid; i < G * kD; i += WAVES * 64) {
+        const int h = i / kD, d = i % kD;
+        const size_t r = (row0 + h) * a.n_split + split;
+        store_dev(a.part_acc + r * kD + d, own[i]);
+        if (d == 0) {
+          store_dev(a.part_ml + 2 * r, ownml[2 * h]);
+          store_dev(a.part_ml + 2 * r + 1, ownml[2 * h + 1]);
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
+    __syncthreads();
+    if (tid == 0) {
+      const int last = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                       a.n_split - 1;
+      if (last) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      ctl[0] = last;
+    }
+    __syncthreads();
+    if (ctl[0] == 0) return;
+  }
+  combine_unit<WAVES>(a, smem, kv, row0, split, active, S, lo, tv);
 }
 
 }  // namespace
