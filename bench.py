@@ -18,8 +18,10 @@ bounded sample of the same workload) is reported next to it.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -31,6 +33,10 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 WORKLOAD = "qwen3_8b"
 COPIES = 6
+DECODE_KERNEL = "decode_lut_d128"
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_04074_amd", "csrc", "decode_lut.hip")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_lut_d128_qwen3_8b_traffic.md")
+COPY_CALIB_BYTES = 256 << 20
 
 
 def parse():
@@ -42,7 +48,29 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--skip-append", action="store_true")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help=f"finish with one plain device copy of {COPY_CALIB_BYTES >> 20} MiB, the known-size "
+                         "reference for scaling FETCH_SIZE / WRITE_SIZE counter runs")
     return ap.parse_args()
+
+
+def kernel_source_sha256() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per decode launch from the committed counter summary, or None
+    when the summary is missing or was taken on a different kernel source."""
+    try:
+        text = open(TRAFFIC_SUMMARY).read()
+    except OSError:
+        return None
+    sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    val = re.search(r"traffic_bytes_per_launch:\s*([0-9]+)", text)
+    if not sha or not val or sha.group(1) != kernel_source_sha256():
+        return None
+    return int(val.group(1))
 
 
 def cpu_baseline(wl, budget_s: float):
@@ -131,34 +159,40 @@ def main():
     out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
     ws = torch.zeros(nk.decode_workspace_bytes(P, B, Hq, S), dtype=torch.uint8, device=dev)
 
-    def step(i, ev=None):
-        pk, pv = pools[i % COPIES]
-        nk.encode(P, layout, k_new, v_new, start_pos, pk, pv)
-        if ev is not None:
-            ev[0].record()
-        nk.decode_attn(P, layout, q, pk, pv, seq_lens, S, out=out, workspace=ws)
-        if ev is not None:
-            ev[1].record()
+    # prepared calls: arguments marshalled once, so the host keeps ahead of the GPU
+    enc_calls = [nk.prepare_encode(P, layout, k_new, v_new, start_pos, pk, pv) for pk, pv in pools]
+    dec_calls = [nk.prepare_decode(P, layout, q, pk, pv, seq_lens, S, out, ws) for pk, pv in pools]
+
+    def step(i):
+        enc_calls[i % COPIES]()
+        dec_calls[i % COPIES]()
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
 
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps)]
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    for i in range(args.steps):
-        step(i, evs[i])
-    end.record()
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(end)
-    ms_step = total_ms / args.steps
-    dec_ms = np.array([a.elapsed_time(b) for a, b in evs])
-    dec_med_us = float(np.median(dec_ms) * 1e3)
-    dec_mean_us = float(np.mean(dec_ms) * 1e3)
+    def timed(fn, n):
+        """Mean GPU time per call of n back-to-back calls, events on the current
+        stream (the stream the calls launch on)."""
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(n):
+            fn(i)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
+    # whole step (append the new token, then decode attention): the headline
+    ms_step = timed(step, args.steps) * 1e-3
+    # each kernel alone, back to back, for the roofline of the dominant kernel
+    n_runs = 5
+    dec_runs = [timed(lambda i: dec_calls[i % COPIES](), args.steps) for _ in range(n_runs)]
+    enc_runs = [timed(lambda i: enc_calls[i % COPIES](), args.steps) for _ in range(n_runs)]
+    dec_mean_us = float(np.mean(dec_runs))
+    dec_med_us = float(np.median(dec_runs))
+    enc_us = np.array(enc_runs)
 
     value = code_bytes / (ms_step * 1e-3) / 1e9
     achieved = code_bytes / (dec_mean_us * 1e-6) / 1e9
@@ -190,9 +224,18 @@ def main():
         append = {"workload": "append 4096 tokens x 32 sequences, 8 KV heads, D=128, paged 16-token blocks",
                   "ms": round(a_ms, 3), "token_heads_per_s": round(th / (a_ms * 1e-3), 1)}
 
+    if args.copy_calib:  # plain copy of known size, last dispatch of the run
+        src = torch.empty(COPY_CALIB_BYTES, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(wl, args.cpu_seconds)
+    traffic = measured_traffic()
 
     rec = {
         "metric": "VQ-KV decode attention effective compressed-KV bandwidth (K+V code bytes / step time), S=16K",
@@ -216,15 +259,21 @@ def main():
             "code_bytes_per_step": code_bytes, "pool_copies": COPIES,
             "params": "random orthogonal transforms, fp16 N(0,1) codebooks, uniform random codes",
         },
-        "decode_call_us": {"median": round(dec_med_us, 2), "mean": round(dec_mean_us, 2)},
+        "decode_kernel_us": {"mean": round(dec_mean_us, 2), "median_of_runs": round(dec_med_us, 2),
+                             "min_of_runs": round(float(np.min(dec_runs)), 2),
+                             "max_of_runs": round(float(np.max(dec_runs)), 2),
+                             "runs": n_runs, "calls_per_run": args.steps},
+        "append_kernel_us": {"mean": round(float(np.mean(enc_us)), 2),
+                             "median_of_runs": round(float(np.median(enc_us)), 2)},
         "roofline": {
-            "kernel": "decode call (prologue + stage 1 + combine)",
+            "kernel": f"{DECODE_KERNEL} (one launch: query transform, split pass, combine)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": code_bytes,
         },
         "append_encode": append,
         "cpu_baseline": cpu,

@@ -5,5 +5,5 @@ The compute lives in ``libnovakv.so`` (hand-written HIP, C ABI in
 """
 
 from .api import (CacheLayout, NovaKVParams, code_pool_shape, decode_attn,  # noqa: F401
-                  decode_workspace_bytes, encode)
+                  decode_workspace_bytes, encode, prepare_decode, prepare_encode)
 from ._native import NovaKVError  # noqa: F401

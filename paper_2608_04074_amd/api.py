@@ -15,7 +15,7 @@ import torch
 from . import _native as nat
 
 __all__ = ["NovaKVParams", "CacheLayout", "encode", "decode_attn", "decode_workspace_bytes",
-           "code_pool_shape"]
+           "code_pool_shape", "prepare_encode", "prepare_decode"]
 
 
 def _stream_ptr(stream: Optional[torch.cuda.Stream]) -> int:
@@ -171,3 +171,66 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
         sinks.data_ptr() if sinks is not None else None, float(softmax_scale), out.data_ptr(),
         workspace.data_ptr(), workspace.numel(), _stream_ptr(stream)))
     return out
+
+
+class PreparedCall:
+    """One C call with every argument already marshalled: calling it costs a
+    single foreign call, for loops that issue the same call many times (the
+    tensors it was prepared from must stay alive and unchanged in place)."""
+
+    def __init__(self, fn, args, keep):
+        self._fn, self._args, self._keep = fn, args, keep
+
+    def __call__(self) -> None:
+        nat.check(self._fn(*self._args))
+
+
+def prepare_encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v: torch.Tensor,
+                   start_pos: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
+                   stream: Optional[torch.cuda.Stream] = None) -> PreparedCall:
+    """nova_kv_encode with the arguments of encode(), marshalled once."""
+    if k.dim() != 4:
+        raise ValueError("k must be [B][n_new][Hkv][D]")
+    b, n_new, hkv, d = k.shape
+    if hkv != params.num_kv_heads or d != params.head_dim:
+        raise ValueError("k does not match the parameters' head count / head_dim")
+    _require(k, "k", (torch.float32, torch.bfloat16))
+    _require(v, "v", (k.dtype,), k.numel())
+    _require(start_pos, "start_pos", (torch.int32,), b)
+    _require(k_codes, "k_codes", (torch.uint8,))
+    _require(v_codes, "v_codes", (torch.uint8,), k_codes.numel())
+    vp = ctypes.c_void_p
+    args = (ctypes.byref(params.c), ctypes.byref(layout.c), vp(k.data_ptr()), vp(v.data_ptr()),
+            ctypes.c_int(_dtype_code(k)), ctypes.c_int32(b), ctypes.c_int32(n_new),
+            vp(start_pos.data_ptr()), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()),
+            vp(_stream_ptr(stream)))
+    return PreparedCall(nat.lib().nova_kv_encode, args, (params, layout, k, v, start_pos, k_codes, v_codes))
+
+
+def prepare_decode(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
+                   k_codes: torch.Tensor, v_codes: torch.Tensor, seq_lens: torch.Tensor,
+                   max_seq_len: int, out: torch.Tensor, workspace: torch.Tensor, window: int = 0,
+                   sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
+                   stream: Optional[torch.cuda.Stream] = None) -> PreparedCall:
+    """nova_kv_decode_attn with the arguments of decode_attn(), marshalled once
+    (out and a zero-filled workspace are required here)."""
+    if q.dim() != 3 or q.shape[2] != params.head_dim:
+        raise ValueError("q must be [B][Hq][D]")
+    b, hq, d = q.shape
+    _require(q, "q", (torch.float32, torch.bfloat16))
+    _require(k_codes, "k_codes", (torch.uint8,))
+    _require(v_codes, "v_codes", (torch.uint8,), k_codes.numel())
+    _require(seq_lens, "seq_lens", (torch.int32,), b)
+    if sinks is not None:
+        _require(sinks, "sinks", (torch.float32,), hq)
+    _require(out, "out", (torch.float32,), b * hq * d)
+    _require(workspace, "workspace", (torch.uint8,))
+    vp = ctypes.c_void_p
+    args = (ctypes.byref(params.c), ctypes.byref(layout.c), vp(q.data_ptr()), ctypes.c_int(_dtype_code(q)),
+            ctypes.c_int32(b), ctypes.c_int32(hq), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()),
+            vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len), ctypes.c_int32(window),
+            vp(sinks.data_ptr() if sinks is not None else None), ctypes.c_float(softmax_scale),
+            vp(out.data_ptr()), vp(workspace.data_ptr()), ctypes.c_size_t(workspace.numel()),
+            vp(_stream_ptr(stream)))
+    return PreparedCall(nat.lib().nova_kv_decode_attn, args,
+                        (params, layout, q, k_codes, v_codes, seq_lens, sinks, out, workspace))

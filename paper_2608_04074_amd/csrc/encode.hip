@@ -96,14 +96,21 @@ __global__ void __launch_bounds__(kThreads) encode_v0(EncodeArgs a) {
 }
 
 // Few new tokens per sequence (a decode step): one workgroup per (token,
-// sequence, KV head, side).  The codebook is read straight from the cache
-// hierarchy; eight lanes share a group and keep the best (distance, index)
-// pair, smallest index on equal distance, before a lane reduction.
+// sequence, KV head, side).  Every global load (a slice of the transform, the
+// lane's codewords) is issued before the first use, so the launch costs about
+// one memory latency.  Thread (part, e) forms the part's share of coefficient
+// e in fp64; eight lanes (sixteen at D=64) share a group and keep the best
+// (distance, index) pair, smallest index on equal distance, before a lane
+// reduction.
 template <int D>
 __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   constexpr int L = D / kGroupDim;
-  constexpr int LANES = 256 / L;  // lanes per group (8 at D=128, 16 at D=64)
+  constexpr int LANES = 256 / L;      // lanes per group (8 at D=128, 16 at D=64)
+  constexpr int PER = kCodebookSize / LANES;
+  constexpr int PARTS = 256 / D;      // row parts of the transform (2 at D=128, 4 at D=64)
+  constexpr int ROWS = D / PARTS;
   __shared__ double xs[D];
+  __shared__ double up[PARTS][D];
   __shared__ double us[D];
   const int side = blockIdx.x & 1;
   const int t = blockIdx.x >> 1;
@@ -113,6 +120,16 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * L * kCodebookSize * kGroupDim;
   const void *src = side == 0 ? a.k : a.v;
   uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
+  const int e = tid % D, part = tid / D;
+  const int ell = tid / LANES, r = tid % LANES;
+
+  float tcol[ROWS];
+#pragma unroll
+  for (int j = 0; j < ROWS; ++j) tcol[j] = tm[(part * ROWS + j) * D + e];
+  const uint2 *row = reinterpret_cast<const uint2 *>(cbg + static_cast<size_t>(ell) * kCodebookSize * kGroupDim);
+  uint2 cw[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) cw[k] = row[r + LANES * k];
   if (tid < D) {
     const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + tid;
     double x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
@@ -121,22 +138,28 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
     xs[tid] = x;
   }
   __syncthreads();
-  if (tid < D) {
+  {
     double acc = 0.0;
-#pragma unroll 16
-    for (int d = 0; d < D; ++d) acc = fma(xs[d], static_cast<double>(tm[d * D + tid]), acc);
-    us[tid] = acc;
+#pragma unroll
+    for (int j = 0; j < ROWS; ++j) acc = fma(xs[part * ROWS + j], static_cast<double>(tcol[j]), acc);
+    up[part][e] = acc;
   }
   __syncthreads();
-  const int ell = tid / LANES, r = tid % LANES;
+  if (tid < D) {
+    double u = up[0][tid];
+#pragma unroll
+    for (int p = 1; p < PARTS; ++p) u += up[p][tid];
+    us[tid] = u;
+  }
+  __syncthreads();
   const double u0 = us[ell * 4 + 0], u1 = us[ell * 4 + 1], u2 = us[ell * 4 + 2], u3 = us[ell * 4 + 3];
-  const uint2 *row = reinterpret_cast<const uint2 *>(cbg + static_cast<size_t>(ell) * kCodebookSize * kGroupDim);
   double best = INFINITY;
   int arg = 0;
-  for (int k = 0; k < kCodebookSize / LANES; ++k) {
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
 #pragma clang fp contract(off)
     const int c = r + LANES * k;
-    const uint2 w = row[c];
+    const uint2 w = cw[k];
     const double e0 = u0 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.x & 0xffff)));
     const double e1 = u1 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.x >> 16)));
     const double e2 = u2 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.y & 0xffff)));
