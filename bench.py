@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline sample")
     ap.add_argument("--skip-append", action="store_true")
+    ap.add_argument("--skip-others", action="store_true",
+                    help="do not time the decode of the other workload shapes")
     ap.add_argument("--copy-calib", action="store_true",
                     help=f"finish with one plain device copy of {COPY_CALIB_BYTES >> 20} MiB, the known-size "
                          "reference for scaling FETCH_SIZE / WRITE_SIZE counter runs")
@@ -119,6 +121,63 @@ def cpu_baseline(wl, budget_s: float):
                   f"{len(units)}",
         "wall_s": round(time.perf_counter() - t0, 2),
     }
+
+
+def other_workloads(nk, torch, dev, calls: int):
+    """Decode-kernel time of every other workload shape (one line each).
+
+    Pools hold uniformly random codes; shapes too small to exceed the 256 MB
+    last-level cache are measured as they would run (cache-resident)."""
+    import synth
+    res = []
+    cases = [("single_head", 0), ("sweep_b64_s32k", 0), ("sweep_b1_s128k", 0),
+             ("gptoss_pair", 0), ("gptoss_pair", 1), ("append_paged", 0)]
+    for name, layer in cases:
+        wl = synth.get_workload(name)
+        B, S, H, Hq, D, L = wl.batch, wl.seq_len, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.groups
+        P = nk.NovaKVParams.from_arrays(synth.bench_params(wl, layer), device=dev)
+        gen = torch.Generator(device=dev)
+        gen.manual_seed(7)
+        if wl.block_size:
+            bps = S // wl.block_size
+            layout = nk.CacheLayout(wl.block_size, bps, torch.as_tensor(synth.shuffled_block_table(wl)).to(dev))
+            shape = (B * bps, H, wl.block_size, L)
+        else:
+            layout = nk.CacheLayout.contiguous(S)
+            shape = (B, H, S, L)
+        pool_bytes = 2 * int(np.prod(shape))
+        copies = int(min(6, max(1, -(-(600 << 20) // pool_bytes)))) if pool_bytes > (64 << 20) else 1
+        pools = [(torch.randint(0, 256, shape, dtype=torch.uint8, device=dev, generator=gen),
+                  torch.randint(0, 256, shape, dtype=torch.uint8, device=dev, generator=gen))
+                 for _ in range(copies)]
+        q = torch.randn((B, Hq, D), generator=gen, device=dev).to(torch.bfloat16)
+        seq = torch.full((B,), S, dtype=torch.int32, device=dev)
+        sinks = torch.as_tensor(synth.sink_logits(wl, layer), dtype=torch.float32).to(dev) if wl.sinks else None
+        out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+        ws = torch.zeros(nk.decode_workspace_bytes(P, B, Hq, S), dtype=torch.uint8, device=dev)
+        window = wl.windows[layer]
+        calls_ = [nk.prepare_decode(P, layout, q, pk, pv, seq, S, out, ws, window=window, sinks=sinks)
+                  for pk, pv in pools]
+        for i in range(5):
+            calls_[i % copies]()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(calls):
+            calls_[i % copies]()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / calls
+        cb = wl.code_bytes_per_step(layer)
+        res.append({"workload": f"{name}" + (f" layer {layer} (window {window})" if wl.num_layers > 1 else ""),
+                    "batch": B, "seq_len": S, "q_heads": Hq, "kv_heads": H, "head_dim": D,
+                    "paged_block": wl.block_size or None, "code_bytes": cb, "pool_copies": copies,
+                    "decode_us": round(us, 2), "GB_per_s": round(cb / (us * 1e-6) / 1e9, 1),
+                    "frac_of_hbm_peak": round(cb / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
+        del pools, calls_, ws
+        torch.cuda.empty_cache()
+    return res
 
 
 def main():
@@ -224,6 +283,8 @@ def main():
         append = {"workload": "append 4096 tokens x 32 sequences, 8 KV heads, D=128, paged 16-token blocks",
                   "ms": round(a_ms, 3), "token_heads_per_s": round(th / (a_ms * 1e-3), 1)}
 
+    others = None if args.skip_others else other_workloads(nk, torch, dev, 50)
+
     if args.copy_calib:  # plain copy of known size, last dispatch of the run
         src = torch.empty(COPY_CALIB_BYTES, dtype=torch.uint8, device=dev)
         dst = torch.empty_like(src)
@@ -276,6 +337,7 @@ def main():
             "algorithmic_bytes_per_launch": code_bytes,
         },
         "append_encode": append,
+        "other_workloads_decode": others,
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)

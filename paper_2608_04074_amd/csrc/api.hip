@@ -133,7 +133,7 @@ size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch, in
   if (!p || batch <= 0 || num_q_heads <= 0 || max_seq_len <= 0 || p->num_kv_heads <= 0 ||
       p->head_dim <= 0)
     return 0;
-  return novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len, 0).total;
+  return novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len, 0, 0).total;
 }
 
 nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
@@ -166,7 +166,7 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
   if (!aligned(k_codes, 16) || !aligned(v_codes, 16))
     return fail(NOVA_KV_ERR_INVALID_ARG, "code pools must be 16-byte aligned");
   const novakv::DecodePlan plan = novakv::plan_decode(batch, num_q_heads, p->num_kv_heads,
-                                                      p->head_dim, max_seq_len, layout->block_size);
+                                                      p->head_dim, max_seq_len, layout->block_size, window);
   if (!workspace || workspace_bytes < plan.total)
     return fail(NOVA_KV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
                 workspace ? workspace_bytes : static_cast<size_t>(0));

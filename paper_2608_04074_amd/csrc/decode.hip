@@ -77,6 +77,23 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
   const int tid = threadIdx.x;
   const int G = a.gqa;
 
+  {  // a split beyond the attended span publishes an empty partial and stops
+    const int S = a.seq_lens[b];
+    const int lo = a.window > 0 ? max(0, S - a.window) : 0;
+    if (lo + split * a.chunk >= S) {
+      const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
+      for (int i = tid; i < G * D; i += kThreads) {
+        const size_t r = (row0 + i / D) * a.n_split + split;
+        a.part_acc[r * D + i % D] = 0.f;
+        if (i % D == 0) {
+          a.part_ml[2 * r] = -INFINITY;
+          a.part_ml[2 * r + 1] = 0.f;
+        }
+      }
+      return;
+    }
+  }
+
   {
     const uint4 *sk = reinterpret_cast<const uint4 *>(a.cb_k + static_cast<size_t>(kv) * CB);
     const uint4 *sv = reinterpret_cast<const uint4 *>(a.cb_v + static_cast<size_t>(kv) * CB);
@@ -93,8 +110,8 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
 
   const int S = a.seq_lens[b];
   const int lo = a.window > 0 ? max(0, S - a.window) : 0;
-  const int t0 = max(lo, split * a.chunk);
-  const int t1 = min(S, (split + 1) * a.chunk);
+  const int t0 = lo + split * a.chunk;  // splits tile the attended span [lo, S)
+  const int t1 = min(S, lo + (split + 1) * a.chunk);
 
   float m[kMaxGqa], l[kMaxGqa], acc[kMaxGqa];
 #pragma unroll
@@ -287,24 +304,32 @@ void plan_generic(int batch, int num_kv_heads, int max_seq_len, int *n_split, in
 }  // namespace
 
 DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_dim,
-                       int max_seq_len, int block_size) {
+                       int max_seq_len, int block_size, int window) {
   DecodePlan p{};
   const int gqa = num_q_heads / num_kv_heads;
+  // Splits tile the attended span: the last `window` tokens, or all of them.
+  const int span = window > 0 && window < max_seq_len ? window : max_seq_len;
   int ns_g, ch_g, ns_l, ch_l;
   plan_generic(batch, num_kv_heads, max_seq_len, &ns_g, &ch_g);
-  plan_lut(batch, num_kv_heads, max_seq_len, &ns_l, &ch_l);
-  int max_split;
+  ns_g = (span + ch_g - 1) / ch_g;  // the full-context chunk, so a window never adds splits
+  plan_lut(batch, num_kv_heads, span, &ns_l, &ch_l);
+  // Workspace bound over every window: the full-context generic plan, and the
+  // table plan's split target (its split count never exceeds it).
+  int ns_full, ch_full;
+  plan_generic(batch, num_kv_heads, max_seq_len, &ns_full, &ch_full);
+  const long long units = static_cast<long long>(batch) * num_kv_heads;
+  const int lut_bound = static_cast<int>((256 + units - 1) / units);
+  int max_split = ns_full > lut_bound ? ns_full : lut_bound;
   if (block_size > 0) {
     p.use_lut = lut_path_eligible(head_dim, gqa, block_size) ? 1 : 0;
     p.n_split = p.use_lut ? ns_l : ns_g;
     p.chunk = p.use_lut ? ch_l : ch_g;
-    max_split = p.n_split;
   } else {
     p.use_lut = 0;
     p.n_split = ns_g;
     p.chunk = ch_g;
-    max_split = ns_g > ns_l ? ns_g : ns_l;
   }
+  if (p.n_split > max_split) max_split = p.n_split;
   auto align = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
   const size_t rows = static_cast<size_t>(batch) * num_q_heads;
   p.off_cnt = 0;

@@ -595,7 +595,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
         ms[i] = -INFINITY;
         ls[i] = 0.f;
         as[i] = 0.f;
-        const bool nonempty = max(lo, sp * a.chunk) < min(S, (sp + 1) * a.chunk);
+        const bool nonempty = lo + sp * a.chunk < S;
         if (sp == own_split) {
           if (own_active) {
             ms[i] = ctlf[8 + 2 * h];
@@ -662,8 +662,8 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
 
   const int S = a.seq_lens[b];
   const int lo = a.window > 0 ? max(0, S - a.window) : 0;
-  const int t0 = max(lo, split * a.chunk);
-  const int t1 = min(S, (split + 1) * a.chunk);
+  const int t0 = lo + split * a.chunk;  // splits tile the attended span [lo, S)
+  const int t1 = min(S, lo + (split + 1) * a.chunk);
   const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
   const bool active = t0 < t1;
 

@@ -70,9 +70,12 @@ struct DecodePlan {
   int chunk;
   size_t off_cnt, off_qp, off_sinkp, off_ml, off_acc, total;
 };
-// block_size <= 0 plans for the worst case over both stage-1 kernels.
+// Splits tile each sequence's attended span (the last `window` tokens, or all).
+// The workspace (off_*, total) is sized for every window and both decode
+// paths, so it depends only on (batch, heads, head_dim, max_seq_len);
+// block_size <= 0 asks for that size alone.
 DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_dim,
-                       int max_seq_len, int block_size);
+                       int max_seq_len, int block_size, int window);
 
 hipError_t launch_decode(const DecodeArgs &a, int use_lut, hipStream_t stream);
 
