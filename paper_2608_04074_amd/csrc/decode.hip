@@ -281,7 +281,7 @@ __global__ void __launch_bounds__(256) decode_combine(DecodeArgs a) {
 
 template <int D>
 hipError_t launch_decode_d(const DecodeArgs &a, int use_lut, hipStream_t stream) {
-  if (use_lut) return launch_decode_lut(a, stream);
+  if (use_lut) return D == 128 ? launch_decode_lut(a, stream) : launch_decode_lut64(a, stream);
   const int rows = a.batch * a.num_q_heads;
   decode_prologue<D><<<dim3(rows), dim3(D), 0, stream>>>(a);
   decode_stage1_v0<D><<<dim3(a.n_split, a.num_kv_heads, a.batch), dim3(kThreads), 0, stream>>>(a);
@@ -343,7 +343,7 @@ DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_di
 
 hipError_t launch_decode(const DecodeArgs &a, int use_lut, hipStream_t stream) {
   switch (a.head_dim) {
-    case 64: return launch_decode_d<64>(a, 0, stream);
+    case 64: return launch_decode_d<64>(a, use_lut, stream);
     case 128: return launch_decode_d<128>(a, use_lut, stream);
     default: return hipErrorInvalidValue;
   }

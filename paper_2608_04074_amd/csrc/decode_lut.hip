@@ -24,19 +24,14 @@
 // combine kernel applies t_v^T once per head.
 #include <math.h>
 
+#include "lut_common.h"
 #include "nova_kv_internal.h"
 
 namespace novakv {
 
 namespace {
 
-typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
-typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
-typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
-typedef short short4_t __attribute__((ext_vector_type(4)));
-typedef float float4_t __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) short4_t *lds_short4_ptr;
-typedef __attribute__((address_space(3))) uint8_t *lds_u8_ptr;
+using namespace lut;
 
 constexpr int kD = 128;
 constexpr int kL = kD / kGroupDim;          // 32 groups
@@ -66,69 +61,6 @@ constexpr uint32_t lds_bytes() {
   return kLdsBytes;
 }
 
-__device__ __forceinline__ half4_t tr16_read(uint32_t addr) {
-  const short4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_ptr)(uintptr_t)(addr));
-  return __builtin_bit_cast(half4_t, v);
-}
-
-__device__ __forceinline__ float sum4(half4_t v, float acc) {
-  const half2_t ones = {(_Float16)1.0f, (_Float16)1.0f};
-  const half2_t lo = {v[0], v[1]};
-  const half2_t hi = {v[2], v[3]};
-  acc = __builtin_amdgcn_fdot2(lo, ones, acc, false);
-  return __builtin_amdgcn_fdot2(hi, ones, acc, false);
-}
-
-// Cross-row reductions (lane ^ 16, lane ^ 32) with v_permlane{16,32}_swap:
-// swapping x with a copy of itself yields (rows 0,2 | rows 1,3), or (low half |
-// high half), in the two results, whose elementwise combination is the
-// reduction.  The two results are copied out of the returned vector before any
-// bit cast (a bit cast of a vector element reads element 0 with this compiler).
-struct SwapPair {
-  float a, b;
-};
-__device__ __forceinline__ SwapPair swap_rows16(float x) {
-  const unsigned xu = __builtin_bit_cast(unsigned, x);
-  const auto s = __builtin_amdgcn_permlane16_swap(xu, xu, false, false);
-  const unsigned s0 = s[0], s1 = s[1];
-  return {__builtin_bit_cast(float, s0), __builtin_bit_cast(float, s1)};
-}
-__device__ __forceinline__ SwapPair swap_rows32(float x) {
-  const unsigned xu = __builtin_bit_cast(unsigned, x);
-  const auto s = __builtin_amdgcn_permlane32_swap(xu, xu, false, false);
-  const unsigned s0 = s[0], s1 = s[1];
-  return {__builtin_bit_cast(float, s0), __builtin_bit_cast(float, s1)};
-}
-__device__ __forceinline__ float max_rows16(float x) { const SwapPair p = swap_rows16(x); return fmaxf(p.a, p.b); }
-__device__ __forceinline__ float max_rows32(float x) { const SwapPair p = swap_rows32(x); return fmaxf(p.a, p.b); }
-__device__ __forceinline__ float add_rows16(float x) { const SwapPair p = swap_rows16(x); return p.a + p.b; }
-__device__ __forceinline__ float add_rows32(float x) { const SwapPair p = swap_rows32(x); return p.a + p.b; }
-// Within a 16-lane row: value of lane (l - n) mod 16 (DPP row_ror:n).
-template <int N>
-__device__ __forceinline__ float row_ror(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), 0x120 + N, 0xf, 0xf, false));
-}
-// Split partials and arrival counters are exchanged between workgroups that
-// may sit on different XCDs, each with its own L2.  Every access to them is a
-// relaxed agent-scope atomic (a load or store with device coherence that
-// bypasses the non-coherent caches); ordering comes from waiting for these
-// stores to complete before the arrival is counted, and from issuing the
-// loads only after the last arrival has been observed.  This avoids the L2
-// write-back and invalidation that a device-wide fence costs on this part.
-__device__ __forceinline__ void store_dev(float *p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float load_dev(const float *p) {
-  return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-__device__ __forceinline__ float wave_sum(float x) {
-  x += row_ror<8>(x);
-  x += row_ror<4>(x);
-  x += row_ror<2>(x);
-  x += row_ror<1>(x);
-  return add_rows32(add_rows16(x));
-}
 
 // Byte offset of the code row of token `t_start` (16-aligned) in the pools,
 // for a 16-token sub-tile that lies inside one cache block.
@@ -718,7 +650,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
 }  // namespace
 
 bool lut_path_eligible(int head_dim, int gqa, int block_size) {
-  return head_dim == kD && gqa <= 4 && block_size % 16 == 0;
+  return block_size % 16 == 0 && ((head_dim == 128 && gqa <= 4) || (head_dim == 64 && gqa <= 8));
 }
 
 void plan_lut(int batch, int num_kv_heads, int max_seq_len, int *n_split, int *chunk) {

@@ -1,0 +1,594 @@
+// Decode attention for head_dim 64 and up to 8 query heads per KV head (the
+// GPT-OSS-20B shape), in one launch.  Same method as the head_dim-128 table
+// kernel: per-query table of partial logits, transposing LDS gathers summed on
+// the matrix cores, per-column online softmax, values accumulated in the
+// transform domain, and the split combine by the last arriving split.
+//
+// Paper: Algorithm 1 (attention step); Theorem 1 (q' = q R_K^{-T}); Sec.
+// "Decoding kernel and read path" (query transformed once per step, one
+// codebook lookup per group, k_bar dropped by Lemma S1, split-KV decode);
+// Corollary 1 (v_hat = s_hat R_V^T); appendix on attention sinks.
+//
+// Differences from the head_dim-128 kernel:
+//  * 16 groups, 8 heads per table entry: LUT[c][g][h] (fp16, 16 B) at
+//    c*256 + g*16 + 8*(h/4); a transposing read fetches one half (4 heads).
+//  * A round is 32 tokens.  Read lane (rho, j, tq, hh) = 16 rho + 4 j + 2 tq + hh
+//    gathers half hh of group 4j + ((2(rho&1) + tq) ^ t) of token
+//    8r + 2 rho + tq at step t: a half-wave touches 16 groups x 2 halves, i.e.
+//    32 distinct bank pairs.  The selector MFMA leaves lane (tau, set, head)
+//    = 16 tau + 8 set + head with the logits of tokens 8 tau + 2 i + set.
+//  * Values: two token sets per round, 4 coordinate tiles of 16.
+#include <math.h>
+
+#include "lut_common.h"
+#include "nova_kv_internal.h"
+
+namespace novakv {
+
+namespace {
+
+using namespace lut;
+
+constexpr int kD = 64;
+constexpr int kL = kD / kGroupDim;     // 16 groups
+constexpr int kH = 8;                  // heads per table entry
+constexpr int kRound = 32;             // tokens per round
+constexpr int kBuf = 4;                // rounds of code bytes in flight per wave
+constexpr uint32_t kLutBytes = 65536;  // [256 codes][16 groups][8 heads] fp16
+constexpr uint32_t kVBase = kLutBytes; // value codebook, 32 KB
+constexpr uint32_t kMergeBase = 0;     // per-wave merge scratch, reuses the table once done
+constexpr int kMergeFloats = kH * kD + 2 * kH;
+constexpr float kLazyLog2 = 8.f;       // reference lag allowed in the online softmax (log2 units)
+// Auxiliary region: query staging, partial sums of q' (4 parts), later the
+// split's own partial ([8][64]) and the combine's partial outputs ([4][8][64]).
+constexpr uint32_t kAuxQ = kVBase + 32768;          // [8][64] f32
+constexpr uint32_t kAuxPart = kAuxQ + kH * kD * 4;  // 10 KB
+constexpr uint32_t kAuxOwn = kAuxPart;
+constexpr uint32_t kAuxOut = kAuxPart + kH * kD * 4;
+constexpr uint32_t kAuxCtl = kAuxPart + 10240;
+// control words (32-bit): [0] arrival state, [8..16) shifted sink logits, [16..32) own (m, l)
+constexpr uint32_t kLdsBytes = kAuxCtl + 128;
+
+template <int WAVES>
+constexpr uint32_t lds_bytes() {
+  static_assert(WAVES * kMergeFloats * 4 <= kLutBytes, "merge scratch must fit in the table region");
+  static_assert(WAVES >= 12, "8 table waves and 4 sink waves");
+  static_assert(4 * kH * kD * 4 <= 10240 - kH * kD * 4, "combine outputs fit the part area");
+  return kLdsBytes;
+}
+
+__device__ __forceinline__ size_t subtile_offset(const DecodeArgs &a, int b, int kv, int t_start, int bs_shift) {
+  const int bs = a.layout.block_size;
+  if (a.layout.block_table == nullptr && a.layout.blocks_per_seq == 1)
+    return ((static_cast<size_t>(b) * a.num_kv_heads + kv) * bs + t_start) * kL;
+  const int blk = bs_shift >= 0 ? (t_start >> bs_shift) : t_start / bs;
+  const int row = t_start - blk * bs;
+  const int logical = b * a.layout.blocks_per_seq + blk;
+  const int phys = a.layout.block_table ? a.layout.block_table[logical] : logical;
+  return ((static_cast<size_t>(phys) * a.num_kv_heads + kv) * bs + row) * kL;
+}
+
+// Thread t < 256 holds row (t mod 64) of t_v, columns 16 * (t / 64) .. +15.
+__device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, float4 (&tv)[4]) {
+  const int tid = threadIdx.x;
+  if (tid < 256) {
+    const float4 *row = reinterpret_cast<const float4 *>(a.t_v + (static_cast<size_t>(kv) * kD + (tid & (kD - 1))) * kD) +
+                        4 * (tid >> 6);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) tv[i] = row[i];
+  }
+}
+
+template <int WAVES>
+__device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
+                                           const int t0, const int t1, const size_t row0, float4 (&tv)[4]) {
+  const uint32_t sbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8_ptr)smem));
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int G = a.gqa;
+
+  // ---- read-lane roles: rho = lane row, jj = group quad, tq = token of a pair, hh = head half
+  const int rho = lane >> 4, jj = (lane >> 2) & 3, tq = (lane >> 1) & 1, hh = lane & 1;
+  const int a2 = lane & 3;
+  // ---- accumulator-lane roles: tau = lane row, column (set, head)
+  const int set = (lane >> 3) & 1;
+
+  uint32_t rselw = 0, kcw = 0;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const uint32_t x = static_cast<uint32_t>((2 * (rho & 1) + tq) ^ t);  // byte of the group quad at step t
+    rselw |= x << (8 * t);
+    kcw |= static_cast<uint32_t>(16 * (4 * jj + x) + 8 * hh) << (8 * t);
+  }
+  const uint32_t vbase = sbase + kVBase + 8 * a2;
+
+  float m_run = -INFINITY, l_run = 0.f;
+  float4_t acc[4];
+#pragma unroll
+  for (int X = 0; X < 4; ++X) acc[X] = float4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int R0 = t0 & ~(kRound - 1);
+  int nrounds = (t1 - R0 + kRound - 1) / kRound;
+  const int last16 = (t1 - 1) & ~15;
+  const uint8_t *kpool = a.k_codes;
+  const uint8_t *vpool = a.v_codes;
+  const int bsz = a.layout.block_size;
+  const int bs_shift = (bsz & (bsz - 1)) == 0 ? __builtin_ctz(bsz) : -1;
+  const uint32_t koff = (2 * rho + tq) * kL + 4 * jj;        // + 128 for odd r
+  const uint32_t voff = (8 * (rho & 1) + 2 * jj) * kL + 4 * a2;  // + 16 for set 1
+
+  // Code bytes of one round: K dwords (bytes 4jj..4jj+3 of tokens R + 8r + 2rho + tq)
+  // and V dwords (bytes 4a2..4a2+3 of tokens R + 8rho + 2jj + s).
+  auto load_round = [&](int R, uint32_t *kw, uint32_t *vw) {
+    const size_t s0 = subtile_offset(a, b, kv, min(R, last16), bs_shift);
+    const size_t s1 = subtile_offset(a, b, kv, min(R + 16, last16), bs_shift);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint8_t *kb = kpool + (r < 2 ? s0 : s1);
+      kw[r] = *reinterpret_cast<const uint32_t *>(kb + koff + 128 * (r & 1));
+    }
+    const uint8_t *vb = vpool + ((rho >> 1) ? s1 : s0);
+#pragma unroll
+    for (int s = 0; s < 2; ++s) vw[s] = *reinterpret_cast<const uint32_t *>(vb + voff + 16 * s);
+  };
+  uint32_t kwb[kBuf][4], vwb[kBuf][2];
+#pragma unroll
+  for (int k = 0; k < kBuf - 1; ++k)
+    if (wave + k * WAVES < nrounds) load_round(R0 + kRound * (wave + k * WAVES), kwb[k], vwb[k]);
+
+  // ---- setup: query transform, sink shifts, value codebook into LDS, table via MFMA
+  {
+    constexpr int NT = WAVES * 64;
+    // thread (jq, e4) < 256 holds rows 4jq .. 4jq+3, columns 4e4 .. 4e4+3 of t_k_inv_t
+    const int e4 = tid & 15, jq = tid >> 4;
+    float qval = 0.f;
+    float4 trow[4];
+    if (tid < kH * kD) {
+      const int qh = tid >> 6;
+      if (qh < G) {
+        const size_t qi = (row0 + qh) * kD + (tid & (kD - 1));
+        qval = a.q_bf16 ? bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi])
+                        : static_cast<const float *>(a.q)[qi];
+      }
+    }
+    if (tid < 256) {
+      const float4 *tk = reinterpret_cast<const float4 *>(a.t_k_inv_t + (static_cast<size_t>(kv) * kD + 4 * jq) * kD) + e4;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) trow[r] = tk[r * (kD / 4)];
+    }
+    constexpr int VPER = (kL * 256 + NT - 1) / NT;
+    const uint2 *vsrc = reinterpret_cast<const uint2 *>(a.cb_v + static_cast<size_t>(kv) * kL * 256 * 4);
+    // element e -> (g, c) so that each half-wave writes 32 distinct bank pairs
+    auto vmap = [](int e, int &g, int &c) {
+      const int r = e >> 5;
+      g = 4 * ((e >> 3) & 3) + (r & 3);
+      c = 8 * (r >> 2) + (e & 7);
+    };
+    uint2 vst[VPER];
+#pragma unroll
+    for (int k = 0; k < VPER; ++k) {
+      const int e = tid + k * NT;
+      if (e < kL * 256) {
+        int g, c;
+        vmap(e, g, c);
+        vst[k] = vsrc[g * 256 + c];
+      }
+    }
+    // table waves: groups 8*(wave & 1) .. +7, codes 64*(wave >> 1) .. +63; 4-lane
+    // block b = (group 8*(wave&1) + b/2, head half b&1)
+    const bool lut_wave = wave < 8;
+    const int blk = lane >> 2;
+    const int lg = 8 * (wave & 1) + (blk >> 1);
+    const int lh = blk & 1;
+    const int lj = lane & 3;
+    const int cbase = 64 * (wave >> 1);
+    const uint2 *cbk = reinterpret_cast<const uint2 *>(a.cb_k + static_cast<size_t>(kv) * kL * 256 * 4);
+    uint2 kst[16];
+    if (lut_wave) {
+#pragma unroll
+      for (int t = 0; t < 16; ++t) kst[t] = cbk[lg * 256 + cbase + 4 * t + lj];
+    }
+    // waves 8..11 form the shifted sink logits of heads 2(wave-8), 2(wave-8)+1
+    const int sh = 2 * (wave - 8);
+    float kbv = 0.f;
+    if (wave >= 8) kbv = a.kbar[static_cast<size_t>(kv) * kD + lane];
+    float *qs = reinterpret_cast<float *>(smem + kAuxQ);       // [8][64] query
+    float *qsum = reinterpret_cast<float *>(smem + kAuxPart);  // [4 parts][8 heads][64] partial q'
+    if (tid < kH * kD) qs[tid] = qval;
+#pragma unroll
+    for (int k = 0; k < VPER; ++k) {
+      const int e = tid + k * NT;
+      if (e < kL * 256) {
+        int g, c;
+        vmap(e, g, c);
+        *reinterpret_cast<uint2 *>(smem + kVBase + (g & 3) * 8192 + (c << 5) + 8 * (g >> 2)) = vst[k];
+      }
+    }
+    __syncthreads();
+    if (wave >= 8) {
+      float *ctlf = reinterpret_cast<float *>(smem + kAuxCtl);
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        if (sh + k < G) {
+          const float dot = wave_sum(qs[(sh + k) * kD + lane] * kbv);
+          if (lane == 0) ctlf[8 + sh + k] = a.sinks ? a.sinks[kv * G + sh + k] - a.scale * dot : -INFINITY;
+        }
+      }
+    }
+    if (tid < 256) {
+      float4 acc4[kH];
+#pragma unroll
+      for (int hq = 0; hq < kH; ++hq) {
+        const float4 q4 = *reinterpret_cast<const float4 *>(qs + hq * kD + 4 * jq);
+        const float qq[4] = {q4.x, q4.y, q4.z, q4.w};
+        acc4[hq] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          acc4[hq].x = fmaf(qq[r], trow[r].x, acc4[hq].x);
+          acc4[hq].y = fmaf(qq[r], trow[r].y, acc4[hq].y);
+          acc4[hq].z = fmaf(qq[r], trow[r].z, acc4[hq].z);
+          acc4[hq].w = fmaf(qq[r], trow[r].w, acc4[hq].w);
+        }
+      }
+      // the 4 lane rows of a wave hold rows of the same columns: fold them, one part per wave
+#pragma unroll
+      for (int hq = 0; hq < kH; ++hq) {
+        acc4[hq].x = add_rows32(add_rows16(acc4[hq].x));
+        acc4[hq].y = add_rows32(add_rows16(acc4[hq].y));
+        acc4[hq].z = add_rows32(add_rows16(acc4[hq].z));
+        acc4[hq].w = add_rows32(add_rows16(acc4[hq].w));
+        if (lane < 16) *reinterpret_cast<float4 *>(qsum + (wave * kH + hq) * kD + 4 * e4) = acc4[hq];
+      }
+    }
+    __syncthreads();
+    if (lut_wave) {
+      float qv[4] = {0.f, 0.f, 0.f, 0.f};
+      const int head = 4 * lh + lj;
+      if (head < G) {
+#pragma unroll
+        for (int pp = 0; pp < 4; ++pp) {
+          const float4 x4 = *reinterpret_cast<const float4 *>(qsum + (pp * kH + head) * kD + 4 * lg);
+          qv[0] += x4.x; qv[1] += x4.y; qv[2] += x4.z; qv[3] += x4.w;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) qv[i] *= a.qscale;
+      }
+      half4_t a_hi, a_lo;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const _Float16 hi = static_cast<_Float16>(qv[i]);
+        a_hi[i] = hi;
+        a_lo[i] = static_cast<_Float16>(qv[i] - static_cast<float>(hi));
+      }
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        const half4_t bv = __builtin_bit_cast(half4_t, kst[t]);
+        float4_t c = {0.f, 0.f, 0.f, 0.f};
+        c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_hi, bv, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_lo, bv, c, 0, 0, 0);
+        half4_t o;
+        o[0] = static_cast<_Float16>(c[0]);
+        o[1] = static_cast<_Float16>(c[1]);
+        o[2] = static_cast<_Float16>(c[2]);
+        o[3] = static_cast<_Float16>(c[3]);
+        // lane (group lg, half lh, code cbase + 4t + lj) holds heads 4lh .. 4lh+3
+        *reinterpret_cast<half4_t *>(smem + (cbase + 4 * t + lj) * 256 + lg * 16 + 8 * lh) = o;
+      }
+    }
+  }
+  __syncthreads();
+
+  // Selector of the key-side MFMA: row block r of the accumulator receives the
+  // partials of tokens 8r + 2 rho + tq (A[m][k] = 1 where m = 4r + k-row).
+  half8_t asel[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const _Float16 one = ((lane & 15) == 4 * r + rho) ? static_cast<_Float16>(1.f) : static_cast<_Float16>(0.f);
+    asel[r] = half8_t{one, one, one, one, one, one, one, one};
+  }
+
+  auto process_round = [&](const int R, const uint32_t *kw, const uint32_t *vw) {
+    // K: four steps per token, pairs of steps per 16x16x32 MFMA
+    uint32_t wr[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) wr[r] = __builtin_amdgcn_perm(kw[r], kw[r], rselw);
+    float4_t kacc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int tp = 0; tp < 2; ++tp) {
+      half8_t e[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint32_t ta = 2 * tp, tb = 2 * tp + 1;
+        const half4_t lo = tr16_read(sbase + __builtin_amdgcn_perm(wr[r], kcw, 0x0C0C0000u | ((4u + ta) << 8) | ta));
+        const half4_t hi = tr16_read(sbase + __builtin_amdgcn_perm(wr[r], kcw, 0x0C0C0000u | ((4u + tb) << 8) | tb));
+        e[r] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) kacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(asel[r], e[r], kacc, 0, 0, 0);
+    }
+    // lane (tau, set, head): register i = token R + 8 tau + 2 i + set
+    float z[4] = {kacc[0], kacc[1], kacc[2], kacc[3]};
+    if (R < t0 || R + kRound > t1) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int tok = R + 8 * rho + 2 * i + set;
+        if (tok < t0 || tok >= t1) z[i] = -INFINITY;
+      }
+    }
+    float zmax = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+    zmax = max_rows16(zmax);
+    zmax = max_rows32(zmax);
+    const float m_new = fmaxf(m_run, zmax);
+    const bool bump = m_new > m_run + kLazyLog2;
+    const float ref = bump ? m_new : m_run;
+    const float alpha = bump ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
+    const float base = ref == -INFINITY ? 0.f : ref;
+    float p[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p[i] = __builtin_amdgcn_exp2f(z[i] - base);
+    l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+    if (__any(bump && m_run != -INFINITY)) {
+#pragma unroll
+      for (int X = 0; X < 4; ++X) acc[X] *= alpha;
+    }
+    m_run = ref;
+    const half4_t pb = {static_cast<_Float16>(p[0]), static_cast<_Float16>(p[1]),
+                        static_cast<_Float16>(p[2]), static_cast<_Float16>(p[3])};
+    const half4_t zero4 = {0, 0, 0, 0};
+    const half8_t bpair = __builtin_shufflevector(set == 0 ? pb : zero4, set == 1 ? pb : zero4, 0, 1, 2, 3, 4, 5, 6, 7);
+    // V: tile X = coordinates of groups 4*(0..3) + X; sets 0 and 1 in one MFMA
+#pragma unroll
+    for (int X = 0; X < 4; ++X) {
+      const uint32_t ca = (vw[0] >> (8 * X)) & 0xffu;
+      const uint32_t cb = (vw[1] >> (8 * X)) & 0xffu;
+      const half4_t lo = tr16_read(vbase + (ca << 5) + X * 8192);
+      const half4_t hi = tr16_read(vbase + (cb << 5) + X * 8192);
+      const half8_t av = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      acc[X] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bpair, acc[X], 0, 0, 0);
+    }
+  };
+
+  for (int rd = wave; rd < nrounds; rd += kBuf * WAVES) {
+#pragma unroll
+    for (int k = 0; k < kBuf; ++k) {
+      const int cur = rd + k * WAVES;
+      if (cur >= nrounds) break;
+      const int nxt = cur + (kBuf - 1) * WAVES;
+      if (nxt < nrounds) load_round(R0 + kRound * nxt, kwb[(k + kBuf - 1) % kBuf], vwb[(k + kBuf - 1) % kBuf]);
+      process_round(R0 + kRound * cur, kwb[k], vwb[k]);
+    }
+  }
+  load_tv_rows(a, kv, tv);
+
+  // ---- per-wave reduction: l over the rows of a column; the two set columns
+  // of a head (lanes n and n + 8 of a row) are rescaled to a common max and summed
+  float l_tot = add_rows32(add_rows16(l_run));
+  const float m_head = fmaxf(m_run, row_ror<8>(m_run));
+  const float wcol = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_head);
+  l_tot *= wcol;
+  l_tot += row_ror<8>(l_tot);
+#pragma unroll
+  for (int X = 0; X < 4; ++X) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float y = acc[X][i] * wcol;
+      y += row_ror<8>(y);
+      acc[X][i] = y;
+    }
+  }
+
+  __syncthreads();  // every wave is done with the table before it becomes merge scratch
+  float *merge = reinterpret_cast<float *>(smem + kMergeBase);
+  float *mw = merge + wave * kMergeFloats;  // [0..8) m, [8..16) l, [16 + h*64 + d) acc
+  const int head = lane & 7;
+  if (lane < 8) {
+    mw[head] = m_head;
+    mw[kH + head] = l_tot;
+  }
+  if (set == 0) {
+#pragma unroll
+    for (int X = 0; X < 4; ++X)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) mw[2 * kH + head * kD + 4 * (4 * rho + X) + i] = acc[X][i];
+  }
+  __syncthreads();
+
+  // ---- merge the waves into this split's partial (natural-log max), kept in LDS
+  constexpr float kLn2 = 0.693147180559945309f;
+  float *own = reinterpret_cast<float *>(smem + kAuxOwn);
+  float *ownml = reinterpret_cast<float *>(smem + kAuxCtl) + 16;
+  for (int i = tid; i < G * kD; i += WAVES * 64) {
+    const int h = i / kD, d = i % kD;
+    float big = -INFINITY;
+    for (int w = 0; w < WAVES; ++w) big = fmaxf(big, merge[w * kMergeFloats + h]);
+    float num = 0.f, den = 0.f;
+    if (big != -INFINITY) {
+      for (int w = 0; w < WAVES; ++w) {
+        const float mwv = merge[w * kMergeFloats + h];
+        const float wt = (mwv == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mwv - big);
+        num = fmaf(wt, merge[w * kMergeFloats + 2 * kH + h * kD + d], num);
+        den = fmaf(wt, merge[w * kMergeFloats + kH + h], den);
+      }
+    }
+    own[i] = num;
+    if (d == 0) {
+      ownml[2 * h] = big == -INFINITY ? -INFINITY : big * kLn2;
+      ownml[2 * h + 1] = den;
+    }
+  }
+}
+
+// Last split of a (sequence, KV head): log-sum-exp merge of the splits in
+// index order, the sink once (shifted, Lemma S1), division, and out = s_hat t_v^T.
+template <int WAVES>
+__device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int kv, const size_t row0,
+                                             const int own_split, const bool own_active, const int S, const int lo,
+                                             const float4 (&tv)[4]) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int G = a.gqa;
+  float *shat = reinterpret_cast<float *>(smem + kAuxQ);    // [8][64]
+  float *outp = reinterpret_cast<float *>(smem + kAuxOut);  // [4 parts][8 heads][64]
+  float *ctlf = reinterpret_cast<float *>(smem + kAuxCtl);
+  const float *own = reinterpret_cast<const float *>(smem + kAuxOwn);
+  const int d = tid & (kD - 1), jp = tid >> 6;  // tv holds row d of t_v, columns 16*jp .. 16*jp+15
+  if (!own_active) {  // the setup did not run: form the shifted sink logits here
+    if (wave < G) {
+      const size_t qi = (row0 + wave) * kD + lane;
+      const float q0 = a.q_bf16 ? bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi])
+                                : static_cast<const float *>(a.q)[qi];
+      const float dot = wave_sum(q0 * a.kbar[static_cast<size_t>(kv) * kD + lane]);
+      if (lane == 0) ctlf[8 + wave] = a.sinks ? a.sinks[kv * G + wave] - a.scale * dot : -INFINITY;
+    }
+    __syncthreads();
+  }
+  if (tid < G * kD) {
+    const int h = tid >> 6;
+    const size_t r = (row0 + h) * a.n_split;
+    const float sk = ctlf[8 + h];
+    float big = sk, num = 0.f, den = sk == -INFINITY ? 0.f : 1.f;
+    auto take = [&](float ms, float ls, float as) {
+      if (ms == -INFINITY) return;
+      if (ms > big) {
+        const float f = big == -INFINITY ? 0.f : __expf(big - ms);
+        num *= f;
+        den *= f;
+        big = ms;
+      }
+      const float w = __expf(ms - big);
+      den = fmaf(w, ls, den);
+      num = fmaf(w, as, num);
+    };
+    for (int s0 = 0; s0 < a.n_split; s0 += 8) {
+      float ms[8], ls[8], as[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int sp = s0 + i;
+        ms[i] = -INFINITY;
+        ls[i] = 0.f;
+        as[i] = 0.f;
+        const bool nonempty = lo + sp * a.chunk < S;
+        if (sp == own_split) {
+          if (own_active) {
+            ms[i] = ctlf[16 + 2 * h];
+            ls[i] = ctlf[16 + 2 * h + 1];
+            as[i] = own[tid];
+          }
+        } else if (sp < a.n_split && nonempty) {
+          ms[i] = load_dev(a.part_ml + 2 * (r + sp));
+          ls[i] = load_dev(a.part_ml + 2 * (r + sp) + 1);
+          as[i] = load_dev(a.part_acc + (r + sp) * kD + d);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) take(ms[i], ls[i], as[i]);
+    }
+    shat[tid] = den > 0.f ? num / den : 0.f;
+  } else if (tid < kH * kD) {
+    shat[tid] = 0.f;
+  }
+  __syncthreads();
+  if (tid < 256) {
+    float o[kH];
+#pragma unroll
+    for (int h = 0; h < kH; ++h) o[h] = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+      for (int h = 0; h < kH; ++h) {
+        const float4 sv = *reinterpret_cast<const float4 *>(shat + h * kD + 16 * jp + 4 * i);
+        o[h] = fmaf(sv.x, tv[i].x, o[h]);
+        o[h] = fmaf(sv.y, tv[i].y, o[h]);
+        o[h] = fmaf(sv.z, tv[i].z, o[h]);
+        o[h] = fmaf(sv.w, tv[i].w, o[h]);
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < kH; ++h) outp[(jp * kH + h) * kD + d] = o[h];
+  }
+  __syncthreads();
+  if (tid < G * kD) {
+    const int h = tid >> 6;
+    a.out[(row0 + h) * kD + d] = (outp[h * kD + d] + outp[(kH + h) * kD + d]) +
+                                 (outp[(2 * kH + h) * kD + d] + outp[(3 * kH + h) * kD + d]);
+  }
+}
+
+// One workgroup per (sequence, KV head, split); the arrival protocol is the
+// one of the head_dim-128 kernel (relaxed agent-scope partials and counters,
+// the last split combines, a split finding all others arrived does not publish).
+template <int WAVES>
+__global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
+  const int tid = threadIdx.x;
+  const int kv = blockIdx.x % a.num_kv_heads;  // KV head fastest: one XCD per KV head
+  const int rest = blockIdx.x / a.num_kv_heads;
+  const int split = rest % a.n_split;
+  const int b = rest / a.n_split;
+  const int bk = b * a.num_kv_heads + kv;
+  const int G = a.gqa;
+
+  const int S = a.seq_lens[b];
+  const int lo = a.window > 0 ? max(0, S - a.window) : 0;
+  const int t0 = lo + split * a.chunk;  // splits tile the attended span [lo, S)
+  const int t1 = min(S, lo + (split + 1) * a.chunk);
+  const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
+  const bool active = t0 < t1;
+
+  float4 tv[4];
+  if (active) {
+    split_pass<WAVES>(a, smem, b, kv, t0, t1, row0, tv);
+  } else {
+    load_tv_rows(a, kv, tv);
+  }
+  int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
+  __syncthreads();
+  if (tid == 0) {
+    int st = 1;
+    if (a.n_split > 1) {
+      st = __hip_atomic_load(a.counters + bk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.n_split - 1 ? 1 : 0;
+      if (st) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    ctl[0] = st;
+  }
+  __syncthreads();
+  if (ctl[0] == 0) {
+    if (active) {
+      const float *own = reinterpret_cast<const float *>(smem + kAuxOwn);
+      const float *ownml = reinterpret_cast<const float *>(smem + kAuxCtl) + 16;
+      for (int i = tid; i < G * kD; i += WAVES * 64) {
+        const int h = i / kD, d = i % kD;
+        const size_t r = (row0 + h) * a.n_split + split;
+        store_dev(a.part_acc + r * kD + d, own[i]);
+        if (d == 0) {
+          store_dev(a.part_ml + 2 * r, ownml[2 * h]);
+          store_dev(a.part_ml + 2 * r + 1, ownml[2 * h + 1]);
+        }
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
+    __syncthreads();
+    if (tid == 0) {
+      const int last = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                       a.n_split - 1;
+      if (last) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      ctl[0] = last;
+    }
+    __syncthreads();
+    if (ctl[0] == 0) return;
+  }
+  combine_unit<WAVES>(a, smem, kv, row0, split, active, S, lo, tv);
+}
+
+}  // namespace
+
+hipError_t launch_decode_lut64(const DecodeArgs &a, hipStream_t stream) {
+  constexpr int W = 12;
+  const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
+  decode_lut_d64<W><<<grid, dim3(W * 64), 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace novakv

@@ -79,11 +79,13 @@ DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_di
 
 hipError_t launch_decode(const DecodeArgs &a, int use_lut, hipStream_t stream);
 
-// Table-based decode (head_dim 128, <= 4 query heads per KV head, 16-token-aligned
-// blocks): query transform, split pass and combine in one launch.
+// Table-based decode (head_dim 128 with <= 4, or head_dim 64 with <= 8 query
+// heads per KV head; 16-token-aligned blocks): query transform, split pass and
+// combine in one launch.
 bool lut_path_eligible(int head_dim, int gqa, int block_size);
 void plan_lut(int batch, int num_kv_heads, int max_seq_len, int *n_split, int *chunk);
-hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream);
+hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream);    // head_dim 128
+hipError_t launch_decode_lut64(const DecodeArgs &a, hipStream_t stream);  // head_dim 64
 hipError_t launch_encode(const EncodeArgs &a, hipStream_t stream);
 
 __device__ __forceinline__ float half_bits_to_float(uint16_t h) {

@@ -204,6 +204,69 @@ def test_paged_equals_contiguous_and_split_invariance(nk, qwen_small):
     torch.testing.assert_close(out_b, out_c, rtol=1e-5, atol=1e-6)
 
 
+# ------------------------------------------ GPT-OSS-shaped (D=64, 8 heads/KV)
+
+@pytest.fixture(scope="module")
+def gptoss_small(nk):
+    wl = synth.get_workload("gptoss_pair")
+    params = calibrated_params(wl, 0)
+    return wl, params, upload_params(nk, params)
+
+
+@pytest.mark.parametrize("window,use_sink", [(0, True), (128, True), (1, False), (0, False)])
+def test_gptoss_shape_decode_ragged(nk, gptoss_small, window, use_sink):
+    """64q/8kv, D=64: ragged lengths incl. 0, 1 and a partial round; windows, sinks; every row."""
+    wl, params, P = gptoss_small
+    B, cap = 5, 1536
+    H, L, G = wl.num_kv_heads, wl.groups, wl.gqa
+    lens = np.array([0, 1, 130, 1001, 1536], dtype=np.int32)
+    ck, cv = _random_pools(wl, 0, B, cap, H, L)
+    q = synth.decode_queries(wl, 0, batch=B)
+    sinks = synth.sink_logits(wl, 0) if use_sink else None
+    lay = nk.CacheLayout.contiguous(cap)
+    say(f"gptoss decode window={window} sink={use_sink}")
+    out = nk.decode_attn(P, lay, dev(q, torch.bfloat16), dev(ck, torch.uint8), dev(cv, torch.uint8),
+                         dev(lens, torch.int32), cap, window=window,
+                         sinks=dev(sinks, torch.float32) if use_sink else None).cpu().numpy()
+    scale = 1 / np.sqrt(wl.head_dim)
+    lk = lay_kwargs(H, cap, 1)
+    hk, hv = ck.reshape(-1), cv.reshape(-1)
+    ref = np.zeros_like(out, dtype=np.float64)
+    for b in range(B):
+        for kv in range(H):
+            ref[b, kv * G:(kv + 1) * G] = oracle_rows(q, hk, hv, params, b, kv, int(lens[b]), scale, lk,
+                                                       window, sinks, G)
+    if not use_sink:
+        assert np.all(out[0] == 0)
+    assert_outputs_close(out.reshape(-1, wl.head_dim), ref.reshape(-1, wl.head_dim),
+                         what=f"gptoss ragged window={window} sink={use_sink}")
+
+
+def test_gptoss_shape_paged_equals_contiguous(nk, gptoss_small):
+    wl, params, P = gptoss_small
+    B, cap = 2, 2048
+    H, L = wl.num_kv_heads, wl.groups
+    ck, cv = _random_pools(wl, 0, B, cap, H, L)
+    q = dev(synth.decode_queries(wl, 0, batch=B), torch.bfloat16)
+    lens = dev([2048, 1203], torch.int32)
+    sinks = dev(synth.sink_logits(wl, 0), torch.float32)
+    say("gptoss contiguous vs paged")
+    out_c = nk.decode_attn(P, nk.CacheLayout.contiguous(cap), q, dev(ck, torch.uint8),
+                           dev(cv, torch.uint8), lens, cap, sinks=sinks)
+    bs, bps = 16, cap // 16
+    table = np.random.default_rng(5).permutation(B * bps).astype(np.int32).reshape(B, bps)
+    flat_k = np.zeros(B * bps * H * bs * L, dtype=np.uint8)
+    flat_v = np.zeros_like(flat_k)
+    lk = lay_kwargs(H, bs, bps, table)
+    for b in range(B):
+        for kv in range(H):
+            write_rows(flat_k, ck[b, kv], b, kv, 0, **lk)
+            write_rows(flat_v, cv[b, kv], b, kv, 0, **lk)
+    out_p = nk.decode_attn(P, nk.CacheLayout(bs, bps, dev(table, torch.int32)), q,
+                           dev(flat_k, torch.uint8), dev(flat_v, torch.uint8), lens, cap, sinks=sinks)
+    assert torch.equal(out_c, out_p)
+
+
 # ------------------------------------------------- full-size configurations
 
 def _full_decode(nk, wl, layer, params, units, window=0, batch=None, cap=None):
