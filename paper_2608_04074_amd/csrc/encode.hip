@@ -14,87 +14,6 @@ namespace novakv {
 
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kTokens = 16;  // tokens per workgroup
-
-template <int D>
-__global__ void __launch_bounds__(kThreads) encode_v0(EncodeArgs a) {
-  constexpr int L = D / kGroupDim;
-  constexpr int CB = L * kCodebookSize * kGroupDim;
-  __shared__ double xs[kTokens][D];
-  __shared__ double us[kTokens][D];
-  __shared__ __attribute__((aligned(16))) uint16_t cb[CB];
-
-  const int tile = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x;
-  const int n0 = tile * kTokens;
-  const int nt = min(kTokens, a.n_new - n0);
-  const int pos0 = a.start_pos[b] + n0;
-
-  for (int side = 0; side < 2; ++side) {
-    const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D;
-    const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * CB;
-    const void *src = side == 0 ? a.k : a.v;
-    uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
-
-    {
-      const uint4 *s4 = reinterpret_cast<const uint4 *>(cbg);
-      uint4 *d4 = reinterpret_cast<uint4 *>(cb);
-      for (int i = tid; i < CB * 2 / 16; i += kThreads) d4[i] = s4[i];
-    }
-    for (int i = tid; i < nt * D; i += kThreads) {
-      const int t = i / D, d = i % D;
-      const size_t idx =
-          ((static_cast<size_t>(b) * a.n_new + n0 + t) * a.num_kv_heads + kv) * D + d;
-      double x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
-                           : static_cast<double>(static_cast<const float *>(src)[idx]);
-      if (side == 0) x -= static_cast<double>(a.kbar[kv * D + d]);
-      xs[t][d] = x;
-    }
-    __syncthreads();
-
-    if (tid < D) {
-      double acc[kTokens];
-#pragma unroll
-      for (int t = 0; t < kTokens; ++t) acc[t] = 0.0;
-      for (int d = 0; d < D; ++d) {
-        const double w = static_cast<double>(tm[d * D + tid]);
-#pragma unroll
-        for (int t = 0; t < kTokens; ++t) acc[t] = fma(xs[t][d], w, acc[t]);
-      }
-      for (int t = 0; t < nt; ++t) us[t][tid] = acc[t];
-    }
-    __syncthreads();
-
-    for (int p = tid; p < nt * L; p += kThreads) {
-      const int t = p / L, ell = p % L;
-      const double u0 = us[t][ell * 4 + 0], u1 = us[t][ell * 4 + 1];
-      const double u2 = us[t][ell * 4 + 2], u3 = us[t][ell * 4 + 3];
-      const uint16_t *row = &cb[ell * kCodebookSize * kGroupDim];
-      double best = INFINITY;
-      int arg = 0;
-      for (int c = 0; c < kCodebookSize; ++c) {
-#pragma clang fp contract(off)
-        const double e0 = u0 - static_cast<double>(half_bits_to_float(row[c * 4 + 0]));
-        const double e1 = u1 - static_cast<double>(half_bits_to_float(row[c * 4 + 1]));
-        const double e2 = u2 - static_cast<double>(half_bits_to_float(row[c * 4 + 2]));
-        const double e3 = u3 - static_cast<double>(half_bits_to_float(row[c * 4 + 3]));
-        double dist = e0 * e0;
-        dist = dist + e1 * e1;
-        dist = dist + e2 * e2;
-        dist = dist + e3 * e3;
-        if (dist < best) {
-          best = dist;
-          arg = c;
-        }
-      }
-      const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos0 + t);
-      pool[off + ell] = static_cast<uint8_t>(arg);
-    }
-    __syncthreads();
-  }
-}
-
 // Few new tokens per sequence (a decode step): one workgroup per (token,
 // sequence, KV head, side).  Every global load (a slice of the transform, the
 // lane's codewords) is issued before the first use, so the launch costs about
@@ -188,14 +107,163 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   }
 }
 
+// Bulk append: one workgroup (4 waves) per (32-token tile, KV head, sequence,
+// side), everything on the fp64 matrix cores.
+//  * transform: U = (X - k_bar) T with v_mfma_f64_16x16x4f64 (A = 16 tokens x 4
+//    input coordinates from LDS, B = 4 input x 16 output coordinates of T);
+//  * distances: per group, rows = codewords, columns = tokens; the accumulator
+//    starts at |c|^2 + off_g (off_g >= every |u_g|^2 of the tile, so the value
+//    |u - c|^2 + (off_g - |u_g|^2) is >= 0 and ordered like the distance) and
+//    the MFMA adds -2 c . u;
+//  * argmin: the codeword index replaces the low 8 mantissa bits of the
+//    (clamped, non-negative) fp64 value, so one min per score keeps the nearest
+//    codeword and, on equal values, the smallest index.  The truncation is
+//    2^-44 relative, far below the spacing of distinct distances.
+// LDS rows are padded by two doubles so the operand reads hit distinct banks.
+// Operand layout of v_mfma_f64_16x16x4f64 (measured): A[m][k] in lane 16k + m,
+// B[k][n] in lane 16k + n, D[m][n] in lane 16 (m mod 4) + n, register m / 4.
+template <int D>
+__global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
+  constexpr int L = D / kGroupDim;
+  constexpr int TT = 32;                 // tokens per workgroup
+  constexpr int RS = D + 2;              // LDS row stride (doubles)
+  constexpr int OT = D / 16;             // output tiles of the transform
+  constexpr int KS = D / 4;              // k-steps of the transform
+  typedef double double4_t __attribute__((ext_vector_type(4)));
+  __shared__ double xs[TT * RS];         // inputs, then coefficients
+  __shared__ __attribute__((aligned(32))) double cn[4][kCodebookSize];
+  __shared__ uint8_t codes[TT][L];
+
+  const int tile = blockIdx.x, kv = blockIdx.y;
+  const int b = blockIdx.z >> 1, side = blockIdx.z & 1;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n0 = tile * TT;
+  const int nt = min(TT, a.n_new - n0);
+  const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D;
+  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * L * kCodebookSize * kGroupDim;
+  const void *src = side == 0 ? a.k : a.v;
+  uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
+
+  for (int i = tid; i < TT * D; i += 256) {
+    const int t = i / D, d = i % D;
+    double x = 0.0;
+    if (t < nt) {
+      const size_t idx = ((static_cast<size_t>(b) * a.n_new + n0 + t) * a.num_kv_heads + kv) * D + d;
+      x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
+                    : static_cast<double>(static_cast<const float *>(src)[idx]);
+      if (side == 0) x -= static_cast<double>(a.kbar[kv * D + d]);
+    }
+    xs[t * RS + d] = x;
+  }
+  __syncthreads();
+
+  // ---- transform: wave w computes output tiles w*OT/4 .. of both token tiles
+  const int m = lane & 15, q = lane >> 4;
+  constexpr int OPW = OT / 4;
+  double4_t acc[2][OPW];
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+    for (int j = 0; j < OPW; ++j) acc[tt][j] = double4_t{0.0, 0.0, 0.0, 0.0};
+#pragma unroll 4
+  for (int ks = 0; ks < KS; ++ks) {
+    double bt[OPW];
+#pragma unroll
+    for (int j = 0; j < OPW; ++j) bt[j] = static_cast<double>(tm[(4 * ks + q) * D + 16 * (wave * OPW + j) + m]);
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      const double ax = xs[(16 * tt + m) * RS + 4 * ks + q];
+#pragma unroll
+      for (int j = 0; j < OPW; ++j) acc[tt][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ax, bt[j], acc[tt][j], 0, 0, 0);
+    }
+  }
+  __syncthreads();  // every wave has read its inputs; the coefficients overwrite them
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+    for (int j = 0; j < OPW; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xs[(16 * tt + 4 * i + q) * RS + 16 * (wave * OPW + j) + m] = acc[tt][j][i];
+  __syncthreads();
+
+  // ---- nearest codeword: wave w takes groups w, w+4, ...
+  for (int g = wave; g < L; g += 4) {
+    const uint2 *cw = reinterpret_cast<const uint2 *>(cbg) + static_cast<size_t>(g) * kCodebookSize;
+    // A operands: coordinate q of codewords 16t + m
+    double ac[16];
+#pragma unroll
+    for (int t = 0; t < 16; ++t)
+      ac[t] = static_cast<double>(half_bits_to_float(cbg[(static_cast<size_t>(g) * kCodebookSize + 16 * t + m) * 4 + q]));
+    // offset: the largest |u_g|^2 of the tile (uniform)
+    double un = 0.0;
+    if (lane < TT) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const double u = xs[lane * RS + 4 * g + i];
+        un = fma(u, u, un);
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) un = fmax(un, __shfl_xor(un, o, 64));
+    // |c|^2 + offset for the group's codewords, 4 per lane, stored so that the
+    // accumulator rows 4i + q of tile t (codewords 16t + 4i + q) are contiguous
+    // for each lane row q: codeword c at 16 (c / 16) + 4 (c mod 4) + (c / 4) mod 4
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c = 4 * lane + j;
+      const uint2 w = cw[c];
+      const double c0 = half_bits_to_float(static_cast<uint16_t>(w.x & 0xffff));
+      const double c1 = half_bits_to_float(static_cast<uint16_t>(w.x >> 16));
+      const double c2 = half_bits_to_float(static_cast<uint16_t>(w.y & 0xffff));
+      const double c3 = half_bits_to_float(static_cast<uint16_t>(w.y >> 16));
+      cn[wave][16 * (c >> 4) + 4 * (c & 3) + ((c >> 2) & 3)] = ((c0 * c0 + c1 * c1) + (c2 * c2 + c3 * c3)) + un;
+    }
+#pragma unroll
+    for (int t = 0; t < 16; ++t) ac[t] *= -2.0;
+    // LDS writes of this wave's norms are read only by this wave: a wave-level wait suffices
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      const double bu = xs[(16 * tt + m) * RS + 4 * g + q];  // B[k = q][n = token m]
+      double best = __builtin_huge_val();
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        const double4_t cin = *reinterpret_cast<const double4_t *>(&cn[wave][16 * t + 4 * q]);
+        const double4_t dd = __builtin_amdgcn_mfma_f64_16x16x4f64(ac[t], bu, cin, 0, 0, 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {  // register i = codeword 16t + 4i + q
+          unsigned long long bits = static_cast<unsigned long long>(__double_as_longlong(fmax(dd[i], 0.0)));
+          bits = (bits & ~0xffull) | static_cast<unsigned long long>(16 * t + 4 * i);
+          best = fmin(best, __longlong_as_double(static_cast<long long>(bits)));
+        }
+      }
+      // full codeword index 16t + 4i + q into the low byte, then the minimum over q
+      unsigned long long bits = static_cast<unsigned long long>(__double_as_longlong(best));
+      bits = (bits & ~0xffull) | ((bits & 0xffull) + static_cast<unsigned long long>(q));
+      best = __longlong_as_double(static_cast<long long>(bits));
+      best = fmin(best, __shfl_xor(best, 16, 64));
+      best = fmin(best, __shfl_xor(best, 32, 64));
+      if (lane < 16) codes[16 * tt + lane][g] = static_cast<uint8_t>(__double_as_longlong(best) & 0xff);
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i < nt * L; i += 256) {
+    const int t = i / L, ell = i % L;
+    const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, a.start_pos[b] + n0 + t);
+    pool[off + ell] = codes[t][ell];
+  }
+}
+
 template <int D>
 hipError_t launch_encode_d(const EncodeArgs &a, hipStream_t stream) {
   if (a.n_new <= 4) {
     const dim3 grid(2 * a.n_new, a.num_kv_heads, a.batch);
     encode_small<D><<<grid, dim3(256), 0, stream>>>(a);
   } else {
-    const dim3 grid((a.n_new + kTokens - 1) / kTokens, a.num_kv_heads, a.batch);
-    encode_v0<D><<<grid, dim3(kThreads), 0, stream>>>(a);
+    const dim3 grid((a.n_new + 31) / 32, a.num_kv_heads, 2 * a.batch);
+    encode_bulk<D><<<grid, dim3(256), 0, stream>>>(a);
   }
   return hipGetLastError();
 }
