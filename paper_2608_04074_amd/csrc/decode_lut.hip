@@ -49,7 +49,8 @@ constexpr uint32_t kAuxCtl = kAuxPart + 32 * kD * 4;
 // ([4][128] accumulator at kAuxOwn) and the combine's partial outputs.
 constexpr uint32_t kAuxOwn = kAuxPart;
 constexpr uint32_t kAuxOut = kAuxPart + 4 * kD * 4;
-// control words: [0] arrival state, [4..8) shifted sink logits, [8..16) own (m, l) per head
+// control words: [0] arrival state, [1] next unclaimed round, [4..8) shifted
+// sink logits, [8..16) own (m, l) per head
 constexpr uint32_t kLdsBytes = kAuxCtl + 64;
 
 template <int WAVES>
@@ -94,7 +95,7 @@ __device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, 
 template <int WAVES>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int split, const int t0, const int t1, const size_t row0,
-                                           float4 (&tv)[8]) {
+                                           const int rot, float4 (&tv)[8]) {
   const uint32_t sbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8_ptr)smem));
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -148,8 +149,14 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   // Two named buffers of code bytes alternate through the token loop (unrolled
   // by two), so no in-flight load destination is ever copied: round rd+W is in
   // flight while round rd is processed.
-  uint2 kwA[4], vwA[4], kwB[4], vwB[4];
-  if (wave < nrounds) load_round(R0 + 64 * wave, kwA, vwA);
+  // Two round buffers: wave w requests round w before the setup; afterwards
+  // each wave claims its next round from a workgroup counter when it starts
+  // processing the current one, so waves that the issue arbiter serves less
+  // often simply take fewer rounds and all waves end together.
+  uint2 kwb[2][4], vwb[2][4];
+  if (wave < nrounds) load_round(R0 + 64 * wave, kwb[0], vwb[0]);
+  int *rctr = reinterpret_cast<int *>(smem + kAuxCtl) + 1;
+  if (tid == 0) *rctr = WAVES;  // rounds 0 .. WAVES-1 are taken; visible after the setup's barriers
 
   // ---- setup: value codebook into LDS, table of partial logits via MFMA.
   // All global loads of the setup are issued before any of them is used.
@@ -185,13 +192,16 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       g = 8 * ((e >> 3) & 3) + (r & 7);
       c = 8 * (r >> 3) + (e & 7);
     };
+    // the workgroups that share a KV head start at different offsets, so their
+    // simultaneous requests for the same parameters spread over the L2 channels
+    const int vrot = 256 * (rot & 31);
     uint2 vst[VPER];
 #pragma unroll
     for (int k = 0; k < VPER; ++k) {
       const int e = tid + k * NT;
       if (e < kL * 256) {
         int g, c;
-        vmap(e, g, c);
+        vmap((e + vrot) & (kL * 256 - 1), g, c);
         vst[k] = vsrc[g * 256 + c];
       }
     }
@@ -204,7 +214,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     uint2 kst[16];
     if (lut_wave) {
 #pragma unroll
-      for (int t = 0; t < 16; ++t) kst[t] = cbk[lg * 256 + cbase + 4 * t + lj];
+      for (int t = 0; t < 16; ++t) kst[t] = cbk[lg * 256 + cbase + 4 * ((t + rot) & 15) + lj];
     }
     // waves 8 .. 8+G-1 form the shifted sink logit of head wave-8 (Lemma S1)
     const int sh = wave - 8;
@@ -218,7 +228,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       const int e = tid + k * NT;
       if (e < kL * 256) {
         int g, c;
-        vmap(e, g, c);
+        vmap((e + vrot) & (kL * 256 - 1), g, c);
         *reinterpret_cast<uint2 *>(smem + kVBase + (g & 7) * 8192 + (c << 5) + 8 * (g >> 3)) = vst[k];
       }
     }
@@ -284,8 +294,8 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
         o[1] = static_cast<_Float16>(c[1]);
         o[2] = static_cast<_Float16>(c[2]);
         o[3] = static_cast<_Float16>(c[3]);
-        // lane (group lg, code cbase + 4t + lj) holds the 4 heads
-        *reinterpret_cast<half4_t *>(smem + (cbase + 4 * t + lj) * 256 + lg * 8) = o;
+        // lane (group lg, code cbase + 4t' + lj) holds the 4 heads
+        *reinterpret_cast<half4_t *>(smem + (cbase + 4 * ((t + rot) & 15) + lj) * 256 + lg * 8) = o;
       }
     }
   }
@@ -391,14 +401,22 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     }
   };
 
-  for (int rd = wave; rd < nrounds; rd += 2 * WAVES) {
-    if (rd + WAVES < nrounds) load_round(R0 + 64 * (rd + WAVES), kwB, vwB);
-    process_round(R0 + 64 * rd, kwA, vwA);
-    if (rd + WAVES >= nrounds) break;
-    if (rd + 2 * WAVES < nrounds) load_round(R0 + 64 * (rd + 2 * WAVES), kwA, vwA);
-    process_round(R0 + 64 * (rd + WAVES), kwB, vwB);
+  auto claim = [&]() -> int {
+    int v = 0;
+    if (lane == 0) v = __hip_atomic_fetch_add(rctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    return __builtin_amdgcn_readfirstlane(v);
+  };
+  int cur = wave;
+  while (cur < nrounds) {
+    const int nxt = claim();
+    if (nxt < nrounds) load_round(R0 + 64 * nxt, kwb[1], vwb[1]);
+    process_round(R0 + 64 * cur, kwb[0], vwb[0]);
+    if (nxt >= nrounds) break;
+    const int nxt2 = claim();
+    if (nxt2 < nrounds) load_round(R0 + 64 * nxt2, kwb[0], vwb[0]);
+    process_round(R0 + 64 * nxt, kwb[1], vwb[1]);
+    cur = nxt2;
   }
-  load_tv_rows(a, kv, tv);
 
   // ---- per-wave reduction.  l over the rows of a column; then the four
   // columns u of head v are rescaled to their common max and summed (lanes
@@ -424,6 +442,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   m_run = m_head;
 
   __syncthreads();  // every wave is done with the table before it becomes merge scratch
+  // Rows of t_v for the combine are requested now, before the arrival is
+  // known: their latency hides behind the wave merge, and the last arrival
+  // finds them in registers.
+  load_tv_rows(a, kv, tv);
   float *merge = reinterpret_cast<float *>(smem + kMergeBase);
   float *mw = merge + wave * kMergeFloats;  // [0..4) m, [4..8) l, [8 + h*128 + d) acc
   if (lane < 4) {
@@ -444,15 +466,24 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   float *ownml = reinterpret_cast<float *>(smem + kAuxCtl) + 8;
   for (int i = tid; i < G * kD; i += WAVES * 64) {
     const int h = i / kD, d = i % kD;
+    // all of this thread's reads first, then the arithmetic
+    float mv[WAVES], lv[WAVES], av[WAVES];
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) {
+      mv[w] = merge[w * kMergeFloats + h];
+      lv[w] = merge[w * kMergeFloats + 4 + h];
+      av[w] = merge[w * kMergeFloats + 8 + h * kD + d];
+    }
     float big = -INFINITY;
-    for (int w = 0; w < WAVES; ++w) big = fmaxf(big, merge[w * kMergeFloats + h]);
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) big = fmaxf(big, mv[w]);
     float num = 0.f, den = 0.f;
     if (big != -INFINITY) {
+#pragma unroll
       for (int w = 0; w < WAVES; ++w) {
-        const float mwv = merge[w * kMergeFloats + h];
-        const float wt = (mwv == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mwv - big);
-        num = fmaf(wt, merge[w * kMergeFloats + 8 + h * kD + d], num);
-        den = fmaf(wt, merge[w * kMergeFloats + 4 + h], den);
+        const float wt = (mv[w] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mv[w] - big);
+        num = fmaf(wt, av[w], num);
+        den = fmaf(wt, lv[w], den);
       }
     }
     own[i] = num;
@@ -600,11 +631,11 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   const bool active = t0 < t1;
 
   // Rows of t_v for the combine are requested as soon as the split's token
-  // loop ends, before the arrival is known, so that the last arrival finds
-  // them in flight or in the cache.
+  // loop ends, before the arrival is known: their latency hides behind the
+  // wave merge, and the last arrival finds them in registers.
   float4 tv[8];
   if (active) {
-    split_pass<WAVES>(a, smem, b, kv, split, t0, t1, row0, tv);
+    split_pass<WAVES>(a, smem, b, kv, split, t0, t1, row0, rest, tv);
   } else {
     load_tv_rows(a, kv, tv);
   }

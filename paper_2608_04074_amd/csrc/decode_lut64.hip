@@ -12,12 +12,14 @@
 // Differences from the head_dim-128 kernel:
 //  * 16 groups, 8 heads per table entry: LUT[c][g][h] (fp16, 16 B) at
 //    c*256 + g*16 + 8*(h/4); a transposing read fetches one half (4 heads).
-//  * A round is 32 tokens.  Read lane (rho, j, tq, hh) = 16 rho + 4 j + 2 tq + hh
-//    gathers half hh of group 4j + ((2(rho&1) + tq) ^ t) of token
-//    8r + 2 rho + tq at step t: a half-wave touches 16 groups x 2 halves, i.e.
-//    32 distinct bank pairs.  The selector MFMA leaves lane (tau, set, head)
-//    = 16 tau + 8 set + head with the logits of tokens 8 tau + 2 i + set.
-//  * Values: two token sets per round, 4 coordinate tiles of 16.
+//  * A round is 64 tokens in two halves of 32, whose key work, then softmax,
+//    then value work are issued together.  Within a half, read lane
+//    (rho, j, tq, hh) = 16 rho + 4 j + 2 tq + hh gathers half hh of group
+//    4j + ((2(rho&1) + tq) ^ t) of token 8r + 2 rho + tq at step t: a half-wave
+//    touches 16 groups x 2 halves, i.e. 32 distinct bank pairs.  The selector
+//    MFMA leaves lane (tau, set, head) = 16 tau + 8 set + head with the logits
+//    of tokens 8 tau + 2 i + set of the half.
+//  * Values: two token sets per half, 4 coordinate tiles of 16.
 #include <math.h>
 
 #include "lut_common.h"
@@ -32,8 +34,8 @@ using namespace lut;
 constexpr int kD = 64;
 constexpr int kL = kD / kGroupDim;     // 16 groups
 constexpr int kH = 8;                  // heads per table entry
-constexpr int kRound = 32;             // tokens per round
-constexpr int kBuf = 4;                // rounds of code bytes in flight per wave
+constexpr int kRound = 64;             // tokens per round: two halves of 32
+constexpr int kBuf = 3;                // rounds of code bytes in flight per wave
 constexpr uint32_t kLutBytes = 65536;  // [256 codes][16 groups][8 heads] fp16
 constexpr uint32_t kVBase = kLutBytes; // value codebook, 32 KB
 constexpr uint32_t kMergeBase = 0;     // per-wave merge scratch, reuses the table once done
@@ -118,21 +120,25 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   const uint32_t koff = (2 * rho + tq) * kL + 4 * jj;        // + 128 for odd r
   const uint32_t voff = (8 * (rho & 1) + 2 * jj) * kL + 4 * a2;  // + 16 for set 1
 
-  // Code bytes of one round: K dwords (bytes 4jj..4jj+3 of tokens R + 8r + 2rho + tq)
-  // and V dwords (bytes 4a2..4a2+3 of tokens R + 8rho + 2jj + s).
+  // Code bytes of one round, per half h: K dwords kw[4h + r] (bytes 4jj..4jj+3
+  // of tokens R + 32h + 8r + 2rho + tq) and V dwords vw[2h + s] (bytes
+  // 4a2..4a2+3 of tokens R + 32h + 8rho + 2jj + s).
   auto load_round = [&](int R, uint32_t *kw, uint32_t *vw) {
-    const size_t s0 = subtile_offset(a, b, kv, min(R, last16), bs_shift);
-    const size_t s1 = subtile_offset(a, b, kv, min(R + 16, last16), bs_shift);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const uint8_t *kb = kpool + (r < 2 ? s0 : s1);
-      kw[r] = *reinterpret_cast<const uint32_t *>(kb + koff + 128 * (r & 1));
+    for (int h = 0; h < 2; ++h) {
+      const size_t s0 = subtile_offset(a, b, kv, min(R + 32 * h, last16), bs_shift);
+      const size_t s1 = subtile_offset(a, b, kv, min(R + 32 * h + 16, last16), bs_shift);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint8_t *kb = kpool + (r < 2 ? s0 : s1);
+        kw[4 * h + r] = *reinterpret_cast<const uint32_t *>(kb + koff + 128 * (r & 1));
+      }
+      const uint8_t *vb = vpool + ((rho >> 1) ? s1 : s0);
+#pragma unroll
+      for (int s = 0; s < 2; ++s) vw[2 * h + s] = *reinterpret_cast<const uint32_t *>(vb + voff + 16 * s);
     }
-    const uint8_t *vb = vpool + ((rho >> 1) ? s1 : s0);
-#pragma unroll
-    for (int s = 0; s < 2; ++s) vw[s] = *reinterpret_cast<const uint32_t *>(vb + voff + 16 * s);
   };
-  uint32_t kwb[kBuf][4], vwb[kBuf][2];
+  uint32_t kwb[kBuf][8], vwb[kBuf][4];
 #pragma unroll
   for (int k = 0; k < kBuf - 1; ++k)
     if (wave + k * WAVES < nrounds) load_round(R0 + kRound * (wave + k * WAVES), kwb[k], vwb[k]);
@@ -289,34 +295,38 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   }
 
   auto process_round = [&](const int R, const uint32_t *kw, const uint32_t *vw) {
-    // K: four steps per token, pairs of steps per 16x16x32 MFMA
-    uint32_t wr[4];
+    // K: both halves, four steps per token, pairs of steps per 16x16x32 MFMA
+    uint32_t wr[8];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) wr[r] = __builtin_amdgcn_perm(kw[r], kw[r], rselw);
-    float4_t kacc = {0.f, 0.f, 0.f, 0.f};
+    for (int r = 0; r < 8; ++r) wr[r] = __builtin_amdgcn_perm(kw[r], kw[r], rselw);
+    float4_t kacc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
     for (int tp = 0; tp < 2; ++tp) {
-      half8_t e[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const uint32_t ta = 2 * tp, tb = 2 * tp + 1;
-        const half4_t lo = tr16_read(sbase + __builtin_amdgcn_perm(wr[r], kcw, 0x0C0C0000u | ((4u + ta) << 8) | ta));
-        const half4_t hi = tr16_read(sbase + __builtin_amdgcn_perm(wr[r], kcw, 0x0C0C0000u | ((4u + tb) << 8) | tb));
-        e[r] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      for (int h = 0; h < 2; ++h) {
+        half8_t e[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const uint32_t ta = 2 * tp, tb = 2 * tp + 1;
+          const uint32_t w = wr[4 * h + r];
+          const half4_t lo = tr16_read(sbase + __builtin_amdgcn_perm(w, kcw, 0x0C0C0000u | ((4u + ta) << 8) | ta));
+          const half4_t hi = tr16_read(sbase + __builtin_amdgcn_perm(w, kcw, 0x0C0C0000u | ((4u + tb) << 8) | tb));
+          e[r] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) kacc[h] = __builtin_amdgcn_mfma_f32_16x16x32_f16(asel[r], e[r], kacc[h], 0, 0, 0);
       }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) kacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(asel[r], e[r], kacc, 0, 0, 0);
     }
-    // lane (tau, set, head): register i = token R + 8 tau + 2 i + set
-    float z[4] = {kacc[0], kacc[1], kacc[2], kacc[3]};
+    // lane (tau, set, head): half h register i = token R + 32h + 8 tau + 2 i + set
+    float z[8] = {kacc[0][0], kacc[0][1], kacc[0][2], kacc[0][3], kacc[1][0], kacc[1][1], kacc[1][2], kacc[1][3]};
     if (R < t0 || R + kRound > t1) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int tok = R + 8 * rho + 2 * i + set;
+      for (int i = 0; i < 8; ++i) {
+        const int tok = R + 32 * (i >> 2) + 8 * rho + 2 * (i & 3) + set;
         if (tok < t0 || tok >= t1) z[i] = -INFINITY;
       }
     }
-    float zmax = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
+    float zmax = fmaxf(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])), fmaxf(fmaxf(z[4], z[5]), fmaxf(z[6], z[7])));
     zmax = max_rows16(zmax);
     zmax = max_rows32(zmax);
     const float m_new = fmaxf(m_run, zmax);
@@ -324,28 +334,31 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     const float ref = bump ? m_new : m_run;
     const float alpha = bump ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
     const float base = ref == -INFINITY ? 0.f : ref;
-    float p[4];
+    float p[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) p[i] = __builtin_amdgcn_exp2f(z[i] - base);
-    l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+    for (int i = 0; i < 8; ++i) p[i] = __builtin_amdgcn_exp2f(z[i] - base);
+    l_run = l_run * alpha + (((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7])));
     if (__any(bump && m_run != -INFINITY)) {
 #pragma unroll
       for (int X = 0; X < 4; ++X) acc[X] *= alpha;
     }
     m_run = ref;
-    const half4_t pb = {static_cast<_Float16>(p[0]), static_cast<_Float16>(p[1]),
-                        static_cast<_Float16>(p[2]), static_cast<_Float16>(p[3])};
     const half4_t zero4 = {0, 0, 0, 0};
-    const half8_t bpair = __builtin_shufflevector(set == 0 ? pb : zero4, set == 1 ? pb : zero4, 0, 1, 2, 3, 4, 5, 6, 7);
-    // V: tile X = coordinates of groups 4*(0..3) + X; sets 0 and 1 in one MFMA
+    // V: per half, tile X = coordinates of groups 4*(0..3) + X; sets 0 and 1 in one MFMA
 #pragma unroll
-    for (int X = 0; X < 4; ++X) {
-      const uint32_t ca = (vw[0] >> (8 * X)) & 0xffu;
-      const uint32_t cb = (vw[1] >> (8 * X)) & 0xffu;
-      const half4_t lo = tr16_read(vbase + (ca << 5) + X * 8192);
-      const half4_t hi = tr16_read(vbase + (cb << 5) + X * 8192);
-      const half8_t av = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      acc[X] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bpair, acc[X], 0, 0, 0);
+    for (int h = 0; h < 2; ++h) {
+      const half4_t pb = {static_cast<_Float16>(p[4 * h]), static_cast<_Float16>(p[4 * h + 1]),
+                          static_cast<_Float16>(p[4 * h + 2]), static_cast<_Float16>(p[4 * h + 3])};
+      const half8_t bpair = __builtin_shufflevector(set == 0 ? pb : zero4, set == 1 ? pb : zero4, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+      for (int X = 0; X < 4; ++X) {
+        const uint32_t ca = (vw[2 * h] >> (8 * X)) & 0xffu;
+        const uint32_t cb = (vw[2 * h + 1] >> (8 * X)) & 0xffu;
+        const half4_t lo = tr16_read(vbase + (ca << 5) + X * 8192);
+        const half4_t hi = tr16_read(vbase + (cb << 5) + X * 8192);
+        const half8_t av = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        acc[X] = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bpair, acc[X], 0, 0, 0);
+      }
     }
   };
 
