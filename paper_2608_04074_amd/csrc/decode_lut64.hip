@@ -35,7 +35,7 @@ constexpr int kD = 64;
 constexpr int kL = kD / kGroupDim;     // 16 groups
 constexpr int kH = 8;                  // heads per table entry
 constexpr int kRound = 64;             // tokens per round: two halves of 32
-constexpr int kBuf = 3;                // rounds of code bytes in flight per wave
+constexpr int kBuf = 2;                // rounds of code bytes in flight per wave
 constexpr uint32_t kLutBytes = 65536;  // [256 codes][16 groups][8 heads] fp16
 constexpr uint32_t kVBase = kLutBytes; // value codebook, 32 KB
 constexpr uint32_t kMergeBase = 0;     // per-wave merge scratch, reuses the table once done
@@ -598,7 +598,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
 }  // namespace
 
 hipError_t launch_decode_lut64(const DecodeArgs &a, hipStream_t stream) {
-  constexpr int W = 12;
+  constexpr int W = 16;  // 4 waves per SIMD: the kernel fits in 128 VGPRs
   const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
   decode_lut_d64<W><<<grid, dim3(W * 64), 0, stream>>>(a);
   return hipGetLastError();
