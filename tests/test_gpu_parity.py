@@ -267,6 +267,108 @@ def test_gptoss_shape_paged_equals_contiguous(nk, gptoss_small):
     assert torch.equal(out_c, out_p)
 
 
+# ------------------------------------------- D=64 encoder, head subsets, generic path
+
+@pytest.mark.parametrize("n_new", [1, 3, 101])
+def test_gptoss_shape_encode(nk, gptoss_small, n_new):
+    """D=64 encode: 1 and 3 tokens (per-token kernel) and 101 tokens (tiled kernel, ragged tail)."""
+    wl, params, P = gptoss_small
+    B, cap, H, L, D = 3, 256, wl.num_kv_heads, wl.groups, wl.head_dim
+    starts = [0, 17, cap - n_new]
+    kk = np.empty((B, n_new, H, D))
+    vv = np.empty_like(kk)
+    for b in range(B):
+        for kv in range(H):
+            kk[b, :, kv], vv[b, :, kv] = synth.cache_tokens(wl, 0, kv, b, n_new, start=starts[b])
+    pk = torch.zeros((B, H, cap, L), dtype=torch.uint8, device="cuda")
+    pv = torch.zeros_like(pk)
+    say(f"gptoss encode n_new={n_new}")
+    nk.encode(P, nk.CacheLayout.contiguous(cap), dev(kk, torch.bfloat16), dev(vv, torch.bfloat16),
+              dev(starts, torch.int32), pk, pv)
+    torch.cuda.synchronize()
+    hk, hv = pk.cpu().numpy(), pv.cpu().numpy()
+    for b in range(B):
+        s0 = starts[b]
+        for kv in range(H):
+            ck, gk, cv, gv = ocodec.encode_tokens(kk[b, :, kv], vv[b, :, kv], oatt.head_params(params, kv))
+            compare_codes(hk[b, kv, s0:s0 + n_new], ck, gk, f"gptoss b{b} kv{kv} K")
+            compare_codes(hv[b, kv, s0:s0 + n_new], cv, gv, f"gptoss b{b} kv{kv} V")
+        # rows outside [start, start + n_new) stay untouched
+        assert not hk[b, :, :s0].any() and not hk[b, :, s0 + n_new:].any()
+        assert not hv[b, :, :s0].any() and not hv[b, :, s0 + n_new:].any()
+
+
+def _head_subset(x, hkv, gqa_full, gqa):
+    """Keep the first ``gqa`` query heads of each KV head: [B][Hkv*gqa_full][...] -> [B][Hkv*gqa][...]."""
+    shp = x.shape
+    y = x.reshape(shp[0], hkv, gqa_full, *shp[2:])[:, :, :gqa]
+    return np.ascontiguousarray(y.reshape(shp[0], hkv * gqa, *shp[2:]))
+
+
+@pytest.mark.parametrize("shape,gqa", [("gptoss_pair", 1), ("gptoss_pair", 4), ("qwen3_8b", 1),
+                                       ("qwen3_8b", 2)])
+def test_fewer_query_heads_per_kv_head(nk, shape, gqa):
+    """Table kernels with fewer query heads per KV head than their head slots (D=64 and D=128)."""
+    wl = synth.get_workload(shape)
+    params = calibrated_params(wl, 0)
+    P = upload_params(nk, params)
+    B, cap = 3, 1200
+    H, L, D = wl.num_kv_heads, wl.groups, wl.head_dim
+    lens = np.array([1200, 77, 640], dtype=np.int32)
+    ck, cv = _random_pools(wl, 0, B, cap, H, L)
+    q = _head_subset(synth.decode_queries(wl, 0, batch=B), H, wl.gqa, gqa)
+    rng = np.random.default_rng(29)
+    sinks = rng.standard_normal(H * gqa).astype(np.float32)
+    say(f"{shape} decode with {gqa} query heads per KV head")
+    out = nk.decode_attn(P, nk.CacheLayout.contiguous(cap), dev(q, torch.bfloat16), dev(ck, torch.uint8),
+                         dev(cv, torch.uint8), dev(lens, torch.int32), cap,
+                         sinks=dev(sinks, torch.float32)).cpu().numpy()
+    scale = 1 / np.sqrt(D)
+    lk = lay_kwargs(H, cap, 1)
+    hk, hv = ck.reshape(-1), cv.reshape(-1)
+    ref = np.zeros_like(out, dtype=np.float64)
+    for b in range(B):
+        for kv in range(H):
+            ref[b, kv * gqa:(kv + 1) * gqa] = oracle_rows(q, hk, hv, params, b, kv, int(lens[b]), scale,
+                                                           lk, 0, sinks, gqa)
+    assert_outputs_close(out.reshape(-1, D), ref.reshape(-1, D), what=f"{shape} gqa={gqa}")
+
+
+@pytest.mark.parametrize("window,use_sink", [(0, False), (200, True)])
+def test_generic_path_paged_block8(nk, qwen_small, window, use_sink):
+    """Pages of 8 tokens are outside the table kernels' layout: the split-K kernels take them."""
+    wl, params, P = qwen_small
+    B, cap, bs = 4, 1000, 8
+    bps = cap // bs
+    H, L, G, D = wl.num_kv_heads, wl.groups, wl.gqa, wl.head_dim
+    lens = np.array([0, 9, 517, 1000], dtype=np.int32)
+    ck, cv = _random_pools(wl, 0, B, cap, H, L)
+    table = np.random.default_rng(13).permutation(B * bps).astype(np.int32).reshape(B, bps)
+    lk = lay_kwargs(H, bs, bps, table)
+    flat_k = np.zeros(B * bps * H * bs * L, dtype=np.uint8)
+    flat_v = np.zeros_like(flat_k)
+    for b in range(B):
+        for kv in range(H):
+            write_rows(flat_k, ck[b, kv], b, kv, 0, **lk)
+            write_rows(flat_v, cv[b, kv], b, kv, 0, **lk)
+    q = synth.decode_queries(wl, 0, batch=B)
+    sinks = np.random.default_rng(31).standard_normal(wl.num_q_heads).astype(np.float32) if use_sink else None
+    say(f"generic path block_size=8 window={window} sink={use_sink}")
+    out = nk.decode_attn(P, nk.CacheLayout(bs, bps, dev(table, torch.int32)), dev(q, torch.bfloat16),
+                         dev(flat_k, torch.uint8), dev(flat_v, torch.uint8), dev(lens, torch.int32), cap,
+                         window=window, sinks=dev(sinks, torch.float32) if use_sink else None).cpu().numpy()
+    scale = 1 / np.sqrt(D)
+    ref = np.zeros_like(out, dtype=np.float64)
+    for b in range(B):
+        for kv in range(H):
+            ref[b, kv * G:(kv + 1) * G] = oracle_rows(q, flat_k, flat_v, params, b, kv, int(lens[b]), scale,
+                                                       lk, window, sinks, G)
+    if not use_sink:
+        assert np.all(out[0] == 0)
+    assert_outputs_close(out.reshape(-1, D), ref.reshape(-1, D),
+                         what=f"generic block8 window={window} sink={use_sink}")
+
+
 # ------------------------------------------------- full-size configurations
 
 def _full_decode(nk, wl, layer, params, units, window=0, batch=None, cap=None):
