@@ -536,8 +536,11 @@ template <int WAVES>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
   const int tid = threadIdx.x;
-  const int kv = blockIdx.x % a.num_kv_heads;  // KV head fastest: one XCD per KV head
-  const int rest = blockIdx.x / a.num_kv_heads;
+  // logical order: KV head fastest, then split, then sequence; each XCD takes
+  // a contiguous range of it
+  const int wg = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int kv = wg % a.num_kv_heads;
+  const int rest = wg / a.num_kv_heads;
   const int split = rest % a.n_split;
   const int b = rest / a.n_split;
   const int bk = b * a.num_kv_heads + kv;

@@ -16,6 +16,19 @@ typedef __attribute__((address_space(3))) short4_t *lds_short4_ptr;
 typedef __attribute__((address_space(3))) uint8_t *lds_u8_ptr;
 
 
+// Workgroup i of a launch runs on XCD i mod 8.  This maps the launch order to
+// a logical order in which each XCD owns one contiguous range: XCD x holds
+// logical workgroups [start_x, start_x + count_x), the first n mod 8 XCDs one
+// more than the rest.  Consecutive logical workgroups (e.g. the KV heads and
+// splits of one sequence) then share an XCD and its L2, and the workgroups
+// that read one KV head's parameters spread over all XCDs, so no single L2
+// serves every request for the same lines.
+__device__ __forceinline__ int xcd_contiguous(const int i, const int n) {
+  const int x = i & 7, p = i >> 3;
+  const int q = n >> 3, r = n & 7;
+  return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + p;
+}
+
 __device__ __forceinline__ half4_t tr16_read(uint32_t addr) {
   const short4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_ptr)(uintptr_t)(addr));
   return __builtin_bit_cast(half4_t, v);
