@@ -603,12 +603,10 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
   }
 }
 
-// One workgroup per (sequence, KV head, split).  A split that is not the last
-// of its (sequence, KV head) publishes its partial to the workspace and
-// counts its arrival; the last one combines.  A split that finds every other
-// split already arrived is the last without publishing.  The arrival
-// counters live in the workspace and the last split resets its counter to 0,
-// so a decode step is a single launch.
+// One workgroup per (sequence, KV head, split).  Every split publishes its
+// partial to the workspace and counts its arrival; the last one combines.
+// The arrival counters live in the workspace and the last split resets its
+// counter to 0, so a decode step is a single launch.
 template <int WAVES>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
@@ -639,34 +637,33 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   } else {
     load_tv_rows(a, kv, tv);
   }
+  // Arrival: every split publishes its partial (when it has one) and counts
+  // itself in; the split that brings the count to n_split combines.  The
+  // protocol runs in waves 8.. (thread kCtl and the publishing threads), which
+  // hold no loads of t_v: a wave's memory operations complete in issue order,
+  // so a wait there would also wait for t_v.
+  constexpr int kCtl = 512;
   int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
   __syncthreads();
-  if (tid == 0) {
-    int st = 1;  // 1: last without publishing
-    if (a.n_split > 1) {
-      st = __hip_atomic_load(a.counters + bk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.n_split - 1 ? 1 : 0;
-      if (st) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    ctl[0] = st;
-  }
-  __syncthreads();
-  if (ctl[0] == 0) {
-    if (active) {
-      const float *own = reinterpret_cast<const float *>(smem + kAuxOwn);
-      const float *ownml = reinterpret_cast<const float *>(smem + kAuxCtl) + 8;
-      for (int i = tid; i < G * kD; i += WAVES * 64) {
-        const int h = i / kD, d = i % kD;
-        const size_t r = (row0 + h) * a.n_split + split;
-        store_dev(a.part_acc + r * kD + d, own[i]);
-        if (d == 0) {
-          store_dev(a.part_ml + 2 * r, ownml[2 * h]);
-          store_dev(a.part_ml + 2 * r + 1, ownml[2 * h + 1]);
+  if (a.n_split > 1) {
+    if (tid >= kCtl) {
+      if (active) {
+        const float *own = reinterpret_cast<const float *>(smem + kAuxOwn);
+        const float *ownml = reinterpret_cast<const float *>(smem + kAuxCtl) + 8;
+        for (int i = tid - kCtl; i < G * kD; i += WAVES * 64 - kCtl) {
+          const int h = i / kD, d = i % kD;
+          const size_t r = (row0 + h) * a.n_split + split;
+          store_dev(a.part_acc + r * kD + d, own[i]);
+          if (d == 0) {
+            store_dev(a.part_ml + 2 * r, ownml[2 * h]);
+            store_dev(a.part_ml + 2 * r + 1, ownml[2 * h + 1]);
+          }
         }
       }
+      __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
     }
-    __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
     __syncthreads();
-    if (tid == 0) {
+    if (tid == kCtl) {
       const int last = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
                        a.n_split - 1;
       if (last) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
