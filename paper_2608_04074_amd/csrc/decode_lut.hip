@@ -149,17 +149,22 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   // Two named buffers of code bytes alternate through the token loop (unrolled
   // by two), so no in-flight load destination is ever copied: round rd+W is in
   // flight while round rd is processed.
-  // Two round buffers: wave w requests round w before the setup; afterwards
+  // Two round buffers: wave w requests round w during the setup; afterwards
   // each wave claims its next round from a workgroup counter when it starts
   // processing the current one, so waves that the issue arbiter serves less
   // often simply take fewer rounds and all waves end together.
   uint2 kwb[2][4], vwb[2][4];
-  if (wave < nrounds) load_round(R0 + 64 * wave, kwb[0], vwb[0]);
   int *rctr = reinterpret_cast<int *>(smem + kAuxCtl) + 1;
   if (tid == 0) *rctr = WAVES;  // rounds 0 .. WAVES-1 are taken; visible after the setup's barriers
 
   // ---- setup: value codebook into LDS, table of partial logits via MFMA.
-  // All global loads of the setup are issued before any of them is used.
+  // All global loads of the setup are issued before any of them is used, in
+  // the order query, t_k_inv_t rows, key codebook, value codebook, k_bar,
+  // first round of codes.  A wave's loads complete in issue order and the
+  // compiler's waits assume the fewest loads any path issued, so everything
+  // younger than the value codebook is issued by every wave: the staging then
+  // waits for nothing past the codebook, and the first round's HBM reads stay
+  // in flight through the setup.
   // Value entry (g, c) goes to kVBase + (g&7)*8192 + 32c + 8(g>>3); element e
   // of the staging pass maps to (g, c) so that the 32 lanes of a half-wave
   // write 32 distinct bank pairs.
@@ -172,38 +177,17 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     // formed here for the unit's query heads.  Thread (jq, e4) < 512 holds
     // rows 8*jq .. 8*jq+7 of columns 4*e4 .. 4*e4+3.
     const int e4 = tid & 31, jq = tid >> 5;
-    float qval = 0.f;
+    // thread t < 512 stages element t & 127 of head t >> 7 (heads past G repeat
+    // head G-1 and are never used): one 32-bit load of the word holding it,
+    // converted only when it is stored
+    const size_t qi = (row0 + min(tid >> 7, G - 1)) * kD + (tid & (kD - 1));
+    uint32_t qword = 0;
     float4 trow[8];
     if (tid < 512) {
-      const int qh = tid >> 7;
-      if (qh < G) {
-        const size_t qi = (row0 + qh) * kD + (tid & (kD - 1));
-        qval = a.q_bf16 ? bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi])
-                        : static_cast<const float *>(a.q)[qi];
-      }
+      qword = a.q_bf16 ? reinterpret_cast<const uint32_t *>(a.q)[qi >> 1] : reinterpret_cast<const uint32_t *>(a.q)[qi];
       const float4 *tk = reinterpret_cast<const float4 *>(a.t_k_inv_t + (static_cast<size_t>(kv) * kD + 8 * jq) * kD) + e4;
 #pragma unroll
       for (int r = 0; r < 8; ++r) trow[r] = tk[r * (kD / 4)];
-    }
-    constexpr int VPER = (kL * 256 + NT - 1) / NT;
-    const uint2 *vsrc = reinterpret_cast<const uint2 *>(a.cb_v + static_cast<size_t>(kv) * kL * 256 * 4);
-    auto vmap = [](int e, int &g, int &c) {
-      const int r = e >> 5;
-      g = 8 * ((e >> 3) & 3) + (r & 7);
-      c = 8 * (r >> 3) + (e & 7);
-    };
-    // the workgroups that share a KV head start at different offsets, so their
-    // simultaneous requests for the same parameters spread over the L2 channels
-    const int vrot = 256 * (rot & 31);
-    uint2 vst[VPER];
-#pragma unroll
-    for (int k = 0; k < VPER; ++k) {
-      const int e = tid + k * NT;
-      if (e < kL * 256) {
-        int g, c;
-        vmap((e + vrot) & (kL * 256 - 1), g, c);
-        vst[k] = vsrc[g * 256 + c];
-      }
     }
     // table waves: group set (wave & 1) of 16 groups, code range 64*(wave >> 1) .. +63
     const bool lut_wave = wave < 8;
@@ -216,21 +200,44 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
       for (int t = 0; t < 16; ++t) kst[t] = cbk[lg * 256 + cbase + 4 * ((t + rot) & 15) + lj];
     }
-    // waves 8 .. 8+G-1 form the shifted sink logit of head wave-8 (Lemma S1)
-    const int sh = wave - 8;
-    float2 kb2 = make_float2(0.f, 0.f);
-    if (sh >= 0 && sh < G) kb2 = *reinterpret_cast<const float2 *>(a.kbar + static_cast<size_t>(kv) * kD + 2 * lane);
-    float *qs = reinterpret_cast<float *>(smem + kAuxQ);       // [4][128] query
-    float *qsum = reinterpret_cast<float *>(smem + kAuxPart);  // [8 parts][4 heads][128] partial q'
-    if (tid < 512) qs[tid] = qval;
+    constexpr int VPER = (kL * 256 + NT - 1) / NT;
+    const uint2 *vsrc = reinterpret_cast<const uint2 *>(a.cb_v + static_cast<size_t>(kv) * kL * 256 * 4);
+    auto vmap = [](int e, int &g, int &c) {
+      const int r = e >> 5;
+      g = 8 * ((e >> 3) & 3) + (r & 7);
+      c = 8 * (r >> 3) + (e & 7);
+    };
+    // the workgroups that share a KV head start at different offsets, so their
+    // simultaneous requests for the same parameters spread over the L2 channels
+    const int vrot = 256 * (rot & 31);
+    // elements past the codebook wrap onto entries that other threads also
+    // stage: the same value is written twice
+    uint2 vst[VPER];
 #pragma unroll
     for (int k = 0; k < VPER; ++k) {
-      const int e = tid + k * NT;
-      if (e < kL * 256) {
-        int g, c;
-        vmap((e + vrot) & (kL * 256 - 1), g, c);
-        *reinterpret_cast<uint2 *>(smem + kVBase + (g & 7) * 8192 + (c << 5) + 8 * (g >> 3)) = vst[k];
-      }
+      int g, c;
+      vmap((tid + k * NT + vrot) & (kL * 256 - 1), g, c);
+      vst[k] = vsrc[g * 256 + c];
+    }
+    // waves 8 .. 8+G-1 form the shifted sink logit of head wave-8 (Lemma S1)
+    const int sh = wave - 8;
+    const float2 kb2 = *reinterpret_cast<const float2 *>(a.kbar + static_cast<size_t>(kv) * kD + 2 * lane);
+    // a wave without a round of its own (nrounds >= 1 in an active split)
+    // re-reads the last round and never processes it
+    load_round(R0 + 64 * min(wave, nrounds - 1), kwb[0], vwb[0]);
+    float *qs = reinterpret_cast<float *>(smem + kAuxQ);       // [4][128] query
+    // partial q': [8 parts][32 groups][4 heads][4 coordinates], so that a table
+    // lane's float4 (its group, its head) sits next to its neighbours'
+    float *qsum = reinterpret_cast<float *>(smem + kAuxPart);
+    if (tid < 512) {
+      const uint32_t qb = a.q_bf16 ? ((qi & 1) ? (qword & 0xffff0000u) : (qword << 16)) : qword;
+      qs[tid] = __uint_as_float(qb);
+    }
+#pragma unroll
+    for (int k = 0; k < VPER; ++k) {
+      int g, c;
+      vmap((tid + k * NT + vrot) & (kL * 256 - 1), g, c);
+      *reinterpret_cast<uint2 *>(smem + kVBase + (g & 7) * 8192 + (c << 5) + 8 * (g >> 3)) = vst[k];
     }
     __syncthreads();
     if (sh >= 0 && sh < G) {
@@ -261,7 +268,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
         acc[hh].y = add_rows32(acc[hh].y);
         acc[hh].z = add_rows32(acc[hh].z);
         acc[hh].w = add_rows32(acc[hh].w);
-        if (lane < 32) *reinterpret_cast<float4 *>(qsum + (wave * 4 + hh) * kD + 4 * e4) = acc[hh];
+        if (lane < 32) *reinterpret_cast<float4 *>(qsum + wave * 512 + e4 * 16 + hh * 4) = acc[hh];
       }
     }
     __syncthreads();
@@ -270,7 +277,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       if (lj < G) {
 #pragma unroll
         for (int pp = 0; pp < 8; ++pp) {
-          const float4 x4 = *reinterpret_cast<const float4 *>(qsum + (pp * 4 + lj) * kD + 4 * lg);
+          const float4 x4 = *reinterpret_cast<const float4 *>(qsum + pp * 512 + lg * 16 + lj * 4);
           qv[0] += x4.x; qv[1] += x4.y; qv[2] += x4.z; qv[3] += x4.w;
         }
 #pragma unroll
@@ -283,19 +290,40 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
         a_hi[i] = hi;
         a_lo[i] = static_cast<_Float16>(qv[i] - static_cast<float>(hi));
       }
+      // After the MFMA of step t, lane 4b + j holds the 4 heads of (group
+      // 16*(wave&1) + b, code cbase + 4*((t + rot) & 15) + j); all 4 lanes of a
+      // block hit the bank pair of their group.  Two steps are exchanged across
+      // the wave halves first, so that each half-wave writes 16 groups x 2
+      // codes (2 lanes per bank pair instead of 4): lanes j < 2 keep groups
+      // b (< 8) in the first write and b + 8 in the second, lanes j >= 2 the
+      // reverse; the low half of the wave writes step t, the high half t + 1.
+      const int gA = 16 * (wave & 1) + ((lane >> 2) & 7), gB = gA + 8;
+      const bool lowj = lj < 2;
+      const int g1 = lowj ? gA : gB, g2 = lowj ? gB : gA;
 #pragma unroll
-      for (int t = 0; t < 16; ++t) {
-        const half4_t bv = __builtin_bit_cast(half4_t, kst[t]);
-        float4_t c = {0.f, 0.f, 0.f, 0.f};
-        c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_hi, bv, c, 0, 0, 0);
-        c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_lo, bv, c, 0, 0, 0);
-        half4_t o;
-        o[0] = static_cast<_Float16>(c[0]);
-        o[1] = static_cast<_Float16>(c[1]);
-        o[2] = static_cast<_Float16>(c[2]);
-        o[3] = static_cast<_Float16>(c[3]);
-        // lane (group lg, code cbase + 4t' + lj) holds the 4 heads
-        *reinterpret_cast<half4_t *>(smem + (cbase + 4 * ((t + rot) & 15) + lj) * 256 + lg * 8) = o;
+      for (int t = 0; t < 16; t += 2) {
+        uint2 o[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const half4_t bv = __builtin_bit_cast(half4_t, kst[t + u]);
+          float4_t c = {0.f, 0.f, 0.f, 0.f};
+          c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_hi, bv, c, 0, 0, 0);
+          c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_lo, bv, c, 0, 0, 0);
+          half4_t h;
+          h[0] = static_cast<_Float16>(c[0]);
+          h[1] = static_cast<_Float16>(c[1]);
+          h[2] = static_cast<_Float16>(c[2]);
+          h[3] = static_cast<_Float16>(c[3]);
+          o[u] = __builtin_bit_cast(uint2, h);
+        }
+        // x: group gA of this lane's step, y: group gB of it
+        const auto sx = __builtin_amdgcn_permlane32_swap(o[0].x, o[1].x, false, false);
+        const auto sy = __builtin_amdgcn_permlane32_swap(o[0].y, o[1].y, false, false);
+        const unsigned ax = sx[0], bx = sx[1], ay = sy[0], by = sy[1];
+        const uint2 wa = make_uint2(ax, ay), wb = make_uint2(bx, by);
+        const int code = cbase + 4 * ((t + (lane >> 5) + rot) & 15) + lj;
+        *reinterpret_cast<uint2 *>(smem + code * 256 + g1 * 8) = lowj ? wa : wb;
+        *reinterpret_cast<uint2 *>(smem + code * 256 + g2 * 8) = lowj ? wb : wa;
       }
     }
   }
