@@ -203,6 +203,7 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
   a.part_acc = reinterpret_cast<float *>(ws + plan.off_acc);
   a.n_split = plan.n_split;
   a.chunk = plan.chunk;
+  a.b_chunk = novakv::plan_b_chunk(batch, p->num_kv_heads, plan.n_split);
   hipError_t e = novakv::launch_decode(a, plan.use_lut, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
   return ok();

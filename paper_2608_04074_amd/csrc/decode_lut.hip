@@ -639,13 +639,10 @@ template <int WAVES>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
   const int tid = threadIdx.x;
-  // logical order: KV head fastest, then split, then sequence; each XCD takes
-  // a contiguous range of it
-  const int wg = xcd_contiguous(blockIdx.x, gridDim.x);
-  const int kv = wg % a.num_kv_heads;
-  const int rest = wg / a.num_kv_heads;
-  const int split = rest % a.n_split;
-  const int b = rest / a.n_split;
+  // each XCD takes a contiguous range of the logical workgroup order
+  int kv, b, split;
+  unit_of_workgroup(xcd_contiguous(blockIdx.x, gridDim.x), a.n_split, a.b_chunk, a.num_kv_heads, kv, b, split);
+  const int rest = b * a.n_split + split;  // distinct among the workgroups of a KV head
   const int bk = b * a.num_kv_heads + kv;
   const int G = a.gqa;
 
@@ -718,6 +715,23 @@ void plan_lut(int batch, int num_kv_heads, int max_seq_len, int *n_split, int *c
   if (ch < 64) ch = 64;
   *chunk = ch;
   *n_split = (max_seq_len + ch - 1) / ch;
+}
+
+// Sequences per block of the table kernels' workgroup order: the largest
+// divisor of batch that leaves about two KV heads (all their splits) in each
+// XCD's eighth of the grid.  Same-box timing at B=8, 8 KV heads, 4 splits:
+// two KV heads per XCD beat both one (32 CUs of one L2 request the same
+// parameter lines at once) and eight (every L2 fetches every KV head's
+// parameters).
+int plan_b_chunk(int batch, int num_kv_heads, int n_split) {
+  const long long grid = static_cast<long long>(batch) * num_kv_heads * n_split;
+  const long long per_xcd = grid / 8 > 0 ? grid / 8 : 1;
+  long long target = per_xcd / (2LL * n_split);
+  if (target < 1) target = 1;
+  int bc = 1;
+  for (int d = 1; d <= batch && d <= target; ++d)
+    if (batch % d == 0) bc = d;
+  return bc;
 }
 
 hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream) {

@@ -536,13 +536,10 @@ template <int WAVES>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
   const int tid = threadIdx.x;
-  // logical order: KV head fastest, then split, then sequence; each XCD takes
-  // a contiguous range of it
-  const int wg = xcd_contiguous(blockIdx.x, gridDim.x);
-  const int kv = wg % a.num_kv_heads;
-  const int rest = wg / a.num_kv_heads;
-  const int split = rest % a.n_split;
-  const int b = rest / a.n_split;
+  // each XCD takes a contiguous range of the logical workgroup order
+  int kv, b, split;
+  unit_of_workgroup(xcd_contiguous(blockIdx.x, gridDim.x), a.n_split, a.b_chunk, a.num_kv_heads, kv, b, split);
+  const int rest = b * a.n_split + split;  // distinct among the workgroups of a KV head
   const int bk = b * a.num_kv_heads + kv;
   const int G = a.gqa;
 

@@ -29,6 +29,22 @@ __device__ __forceinline__ int xcd_contiguous(const int i, const int n) {
   return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + p;
 }
 
+// Unit of workgroup number wg in the logical order (split fastest, then
+// sequence within a block of b_chunk sequences, then KV head, then sequence
+// block).  With the XCD-contiguous remap, an XCD's share of the grid then
+// holds all splits of b_chunk sequences for a few KV heads: each KV head's
+// parameters are requested by a moderate number of CUs of one L2, and the
+// splits of a unit meet in that L2.
+__device__ __forceinline__ void unit_of_workgroup(const int wg, const int n_split, const int b_chunk, const int hkv,
+                                                  int &kv, int &b, int &split) {
+  split = wg % n_split;
+  int r = wg / n_split;
+  const int bl = r % b_chunk;
+  r /= b_chunk;
+  kv = r % hkv;
+  b = (r / hkv) * b_chunk + bl;
+}
+
 __device__ __forceinline__ half4_t tr16_read(uint32_t addr) {
   const short4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_ptr)(uintptr_t)(addr));
   return __builtin_bit_cast(half4_t, v);

@@ -50,6 +50,7 @@ struct DecodeArgs {
   float *part_acc;  // [B][Hq][n_split][D]  transform-domain value accumulator
   int n_split;      // context splits per sequence
   int chunk;        // tokens per split
+  int b_chunk;      // table kernels: sequences per block of the workgroup order (divides batch)
 };
 
 struct EncodeArgs {
@@ -78,6 +79,7 @@ DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_di
                        int max_seq_len, int block_size, int window);
 
 hipError_t launch_decode(const DecodeArgs &a, int use_lut, hipStream_t stream);
+int plan_b_chunk(int batch, int num_kv_heads, int n_split);
 
 // Table-based decode (head_dim 128 with <= 4, or head_dim 64 with <= 8 query
 // heads per KV head; 16-token-aligned blocks): query transform, split pass and
