@@ -15,40 +15,47 @@ namespace novakv {
 namespace {
 
 // Few new tokens per sequence (a decode step): one workgroup per (token,
-// sequence, KV head, side).  Every global load (a slice of the transform, the
-// lane's codewords) is issued before the first use, so the launch costs about
-// one memory latency.  Thread (part, e) forms the part's share of coefficient
-// e in fp64; eight lanes (sixteen at D=64) share a group and keep the best
-// (distance, index) pair, smallest index on equal distance, before a lane
-// reduction.
+// sequence, KV head, side, block of 8 groups).  A block needs 32 transform
+// columns (D x 32 fp32) and its 8 codebooks (16 KB), so each workgroup
+// fetches a quarter (D=128) or half (D=64) of the parameters, all loads
+// coalesced and issued before the first use; the launch costs about one
+// memory latency.
+//  * transform: thread (rg, c4) forms, in fp64, the partial coefficients of
+//    columns 4*c4 .. 4*c4+3 over its D/32 rows; 32 row-group partials per
+//    column are summed through LDS;
+//  * search: 32 lanes per group, 8 codewords each, keep the best (distance,
+//    index) pair, smallest index on equal distance, then a lane reduction.
 template <int D>
 __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   constexpr int L = D / kGroupDim;
-  constexpr int LANES = 256 / L;      // lanes per group (8 at D=128, 16 at D=64)
-  constexpr int PER = kCodebookSize / LANES;
-  constexpr int PARTS = 256 / D;      // row parts of the transform (2 at D=128, 4 at D=64)
-  constexpr int ROWS = D / PARTS;
+  constexpr int GB = 8;                    // groups per workgroup
+  constexpr int NB = L / GB;               // group blocks per token
+  constexpr int COLS = GB * kGroupDim;     // 32 transform columns
+  constexpr int RPT = D / 32;              // rows per thread in the transform
+  constexpr int PER = kCodebookSize / 32;  // codewords per lane
   __shared__ double xs[D];
-  __shared__ double up[PARTS][D];
-  __shared__ double us[D];
-  const int side = blockIdx.x & 1;
-  const int t = blockIdx.x >> 1;
+  __shared__ double part[32][COLS + 1];
+  __shared__ double us[COLS];
+  const int blk = blockIdx.x % NB;
+  const int side = (blockIdx.x / NB) & 1;
+  const int t = blockIdx.x / (2 * NB);
   const int kv = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
-  const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D;
-  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * L * kCodebookSize * kGroupDim;
+  const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D + COLS * blk;
+  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) +
+                        (static_cast<size_t>(kv) * L + GB * blk) * kCodebookSize * kGroupDim;
   const void *src = side == 0 ? a.k : a.v;
   uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
-  const int e = tid % D, part = tid / D;
-  const int ell = tid / LANES, r = tid % LANES;
+  const int c4 = tid & 7, rg = tid >> 3;   // transform: columns 4*c4.., rows RPT*rg..
+  const int gl = tid >> 5, r = tid & 31;   // search: group gl of the block, lane r
 
-  float tcol[ROWS];
+  float4 trow[RPT];
 #pragma unroll
-  for (int j = 0; j < ROWS; ++j) tcol[j] = tm[(part * ROWS + j) * D + e];
-  const uint2 *row = reinterpret_cast<const uint2 *>(cbg + static_cast<size_t>(ell) * kCodebookSize * kGroupDim);
+  for (int j = 0; j < RPT; ++j) trow[j] = *reinterpret_cast<const float4 *>(tm + (RPT * rg + j) * D + 4 * c4);
+  const uint2 *row = reinterpret_cast<const uint2 *>(cbg) + gl * kCodebookSize;
   uint2 cw[PER];
 #pragma unroll
-  for (int k = 0; k < PER; ++k) cw[k] = row[r + LANES * k];
+  for (int k = 0; k < PER; ++k) cw[k] = row[r + 32 * k];
   if (tid < D) {
     const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + tid;
     double x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
@@ -58,26 +65,33 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   }
   __syncthreads();
   {
-    double acc = 0.0;
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int j = 0; j < ROWS; ++j) acc = fma(xs[part * ROWS + j], static_cast<double>(tcol[j]), acc);
-    up[part][e] = acc;
+    for (int j = 0; j < RPT; ++j) {
+      const double x = xs[RPT * rg + j];
+      acc[0] = fma(x, static_cast<double>(trow[j].x), acc[0]);
+      acc[1] = fma(x, static_cast<double>(trow[j].y), acc[1]);
+      acc[2] = fma(x, static_cast<double>(trow[j].z), acc[2]);
+      acc[3] = fma(x, static_cast<double>(trow[j].w), acc[3]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) part[rg][4 * c4 + i] = acc[i];
   }
   __syncthreads();
-  if (tid < D) {
-    double u = up[0][tid];
+  if (tid < COLS) {
+    double u = part[0][tid];
 #pragma unroll
-    for (int p = 1; p < PARTS; ++p) u += up[p][tid];
+    for (int p = 1; p < 32; ++p) u += part[p][tid];
     us[tid] = u;
   }
   __syncthreads();
-  const double u0 = us[ell * 4 + 0], u1 = us[ell * 4 + 1], u2 = us[ell * 4 + 2], u3 = us[ell * 4 + 3];
+  const double u0 = us[gl * 4 + 0], u1 = us[gl * 4 + 1], u2 = us[gl * 4 + 2], u3 = us[gl * 4 + 3];
   double best = INFINITY;
   int arg = 0;
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
 #pragma clang fp contract(off)
-    const int c = r + LANES * k;
+    const int c = r + 32 * k;
     const uint2 w = cw[k];
     const double e0 = u0 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.x & 0xffff)));
     const double e1 = u1 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.x >> 16)));
@@ -93,7 +107,7 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
     }
   }
 #pragma unroll
-  for (int o = LANES / 2; o > 0; o >>= 1) {
+  for (int o = 16; o > 0; o >>= 1) {
     const double ob = __shfl_xor(best, o, 64);
     const int oa = __shfl_xor(arg, o, 64);
     if (ob < best || (ob == best && oa < arg)) {
@@ -103,7 +117,7 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   }
   if (r == 0) {
     const int pos = a.start_pos[b] + t;
-    pool[code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos) + ell] = static_cast<uint8_t>(arg);
+    pool[code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos) + GB * blk + gl] = static_cast<uint8_t>(arg);
   }
 }
 
@@ -259,7 +273,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
 template <int D>
 hipError_t launch_encode_d(const EncodeArgs &a, hipStream_t stream) {
   if (a.n_new <= 4) {
-    const dim3 grid(2 * a.n_new, a.num_kv_heads, a.batch);
+    const dim3 grid(2 * a.n_new * (D / kGroupDim / 8), a.num_kv_heads, a.batch);
     encode_small<D><<<grid, dim3(256), 0, stream>>>(a);
   } else {
     const dim3 grid((a.n_new + 31) / 32, a.num_kv_heads, 2 * a.batch);
