@@ -4,8 +4,8 @@
  * NOVA-KV ("Spend Bits Where Queries Look: KV Cache Vector Quantization with
  * Attention-Preserving Transforms") stores every cached key and value as one
  * 8-bit codebook index per group of g = 4 transform coefficients, i.e. 2 bits
- * per element.  This library implements the two calls a serving engine makes
- * on that cache:
+ * per element.  This library implements the calls a serving engine makes on
+ * that cache:
  *
  *   nova_kv_encode       append-time write path: transform the new keys and
  *                        values, pick the nearest codeword of every group, and
@@ -17,6 +17,9 @@
  *                        codes (paper: Algorithm 1, "Attention"; Sec. "Decoding
  *                        kernel and read path"; Appendix "Attention sinks in the
  *                        quantized serving path").
+ *   nova_kv_append_decode_attn  both for one decode step (append the step's
+ *                        token, then attend), in a single launch where the
+ *                        shape allows.
  *
  * Conventions for every call
  *   - All tensor pointers are DEVICE pointers owned by the caller; the library
@@ -180,6 +183,41 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
                                    int32_t window, const float *sinks, float softmax_scale,
                                    float *out, void *workspace, size_t workspace_bytes,
                                    void *hip_stream);
+
+/*
+ * nova_kv_append_decode_attn -- one decode step in one call: append the step's
+ * key and value of every sequence to the code pools, then attend over the
+ * cache including them.
+ *
+ * Paper: Algorithm 1 (the "Write" of the new token, then "Attention"; Fig. 2:
+ * write, then read), with the references of nova_kv_encode and
+ * nova_kv_decode_attn.
+ *
+ *   k_new, v_new  [B][Hkv][D] device, dtype new_dtype (F32 or BF16): the token
+ *              at position seq_lens[b] - 1 of each sequence (the newest cached
+ *              token); precondition seq_lens[b] >= 1.
+ *   k_codes, v_codes  the code pools, written at position seq_lens[b] - 1
+ *              exactly as nova_kv_encode(n_new = 1, start_pos = seq_lens - 1)
+ *              writes them (same bytes); nothing else is touched.
+ *   all other arguments as in nova_kv_decode_attn (params also need t_k).
+ *
+ * out equals the output of nova_kv_decode_attn over the pools after that
+ * append, up to fp32 rounding (the new token's term is added after the
+ * split combine instead of inside a split).  With head_dim 128 on 16-aligned
+ * blocks the step is a single kernel launch, in which the workgroups that
+ * read the pools also encode the new token; other shapes run the one-token
+ * encode and the decode one after the other on the stream.
+ * batch == 0 is a valid no-op.
+ */
+nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
+                                          const void *k_new, const void *v_new, nova_kv_dtype new_dtype,
+                                          const void *q, nova_kv_dtype q_dtype,
+                                          int32_t batch, int32_t num_q_heads,
+                                          uint8_t *k_codes, uint8_t *v_codes,
+                                          const int32_t *seq_lens, int32_t max_seq_len,
+                                          int32_t window, const float *sinks, float softmax_scale,
+                                          float *out, void *workspace, size_t workspace_bytes,
+                                          void *hip_stream);
 
 /* Static description of a status code. */
 const char *nova_kv_status_string(nova_kv_status s);

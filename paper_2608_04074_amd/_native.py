@@ -25,6 +25,7 @@ EXPORTED = (
     "nova_kv_encode",
     "nova_kv_decode_workspace_bytes",
     "nova_kv_decode_attn",
+    "nova_kv_append_decode_attn",
     "nova_kv_status_string",
     "nova_kv_last_error",
 )
@@ -86,6 +87,14 @@ def lib() -> ctypes.CDLL:
                                           ctypes.c_int32, ctypes.c_void_p, ctypes.c_float,
                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                           ctypes.c_void_p]
+        L.nova_kv_append_decode_attn.restype = ctypes.c_int
+        L.nova_kv_append_decode_attn.argtypes = [P(Params), P(Layout), ctypes.c_void_p, ctypes.c_void_p,
+                                                 ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                                                 ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                                 ctypes.c_int32, ctypes.c_void_p, ctypes.c_float,
+                                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                                 ctypes.c_void_p]
         L.nova_kv_status_string.restype = ctypes.c_char_p
         L.nova_kv_status_string.argtypes = [ctypes.c_int]
         L.nova_kv_last_error.restype = ctypes.c_char_p

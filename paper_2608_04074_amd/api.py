@@ -173,6 +173,54 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
     return out
 
 
+def _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
+                        workspace, window, sinks, softmax_scale, stream):
+    if q.dim() != 3 or q.shape[2] != params.head_dim:
+        raise ValueError("q must be [B][Hq][D]")
+    b, hq, d = q.shape
+    if tuple(k_new.shape) != (b, params.num_kv_heads, d):
+        raise ValueError("k_new must be [B][Hkv][D]")
+    _require(k_new, "k_new", (torch.float32, torch.bfloat16))
+    _require(v_new, "v_new", (k_new.dtype,), k_new.numel())
+    _require(q, "q", (torch.float32, torch.bfloat16))
+    _require(k_codes, "k_codes", (torch.uint8,))
+    _require(v_codes, "v_codes", (torch.uint8,), k_codes.numel())
+    _require(seq_lens, "seq_lens", (torch.int32,), b)
+    if sinks is not None:
+        _require(sinks, "sinks", (torch.float32,), hq)
+    _require(out, "out", (torch.float32,), b * hq * d)
+    _require(workspace, "workspace", (torch.uint8,))
+    vp = ctypes.c_void_p
+    return (ctypes.byref(params.c), ctypes.byref(layout.c), vp(k_new.data_ptr()), vp(v_new.data_ptr()),
+            ctypes.c_int(_dtype_code(k_new)), vp(q.data_ptr()), ctypes.c_int(_dtype_code(q)),
+            ctypes.c_int32(b), ctypes.c_int32(hq), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()),
+            vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len), ctypes.c_int32(window),
+            vp(sinks.data_ptr() if sinks is not None else None), ctypes.c_float(softmax_scale),
+            vp(out.data_ptr()), vp(workspace.data_ptr()), ctypes.c_size_t(workspace.numel()),
+            vp(_stream_ptr(stream)))
+
+
+def append_decode_attn(params: NovaKVParams, layout: CacheLayout, k_new: torch.Tensor, v_new: torch.Tensor,
+                       q: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
+                       seq_lens: torch.Tensor, max_seq_len: int, window: int = 0,
+                       sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
+                       out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                       stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """nova_kv_append_decode_attn: store the step's k_new, v_new [B][Hkv][D] at
+    position seq_lens[b] - 1 of the pools, then decode q [B][Hq][D] over the
+    cache including them -> out [B][Hq][D] fp32.  Workspace as in decode_attn."""
+    b, hq, d = q.shape
+    if out is None:
+        out = torch.empty((b, hq, d), dtype=torch.float32, device=q.device)
+    need = decode_workspace_bytes(params, b, hq, max_seq_len) if b > 0 else 0
+    if workspace is None:
+        workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=q.device)
+    args = _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
+                               workspace, window, sinks, softmax_scale, stream)
+    nat.check(nat.lib().nova_kv_append_decode_attn(*args))
+    return out
+
+
 class PreparedCall:
     """One C call with every argument already marshalled: calling it costs a
     single foreign call, for loops that issue the same call many times (the
@@ -234,3 +282,16 @@ def prepare_decode(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
             vp(_stream_ptr(stream)))
     return PreparedCall(nat.lib().nova_kv_decode_attn, args,
                         (params, layout, q, k_codes, v_codes, seq_lens, sinks, out, workspace))
+
+
+def prepare_append_decode(params: NovaKVParams, layout: CacheLayout, k_new: torch.Tensor, v_new: torch.Tensor,
+                          q: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
+                          seq_lens: torch.Tensor, max_seq_len: int, out: torch.Tensor, workspace: torch.Tensor,
+                          window: int = 0, sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
+                          stream: Optional[torch.cuda.Stream] = None) -> PreparedCall:
+    """nova_kv_append_decode_attn with the arguments of append_decode_attn(),
+    marshalled once (out and a zero-filled workspace are required here)."""
+    args = _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
+                               workspace, window, sinks, softmax_scale, stream)
+    return PreparedCall(nat.lib().nova_kv_append_decode_attn, args,
+                        (params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, sinks, out, workspace))

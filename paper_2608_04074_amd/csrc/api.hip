@@ -136,14 +136,16 @@ size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch, in
   return novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len, 0, 0).total;
 }
 
-nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
-                                   const void *q, nova_kv_dtype q_dtype, int32_t batch,
-                                   int32_t num_q_heads, const uint8_t *k_codes,
-                                   const uint8_t *v_codes, const int32_t *seq_lens,
-                                   int32_t max_seq_len, int32_t window, const float *sinks,
-                                   float softmax_scale, float *out, void *workspace,
-                                   size_t workspace_bytes, void *hip_stream) {
-  nova_kv_status st = check_params(p, false, true);
+namespace {
+
+// Host checks and argument set-up shared by the decode entry points.
+nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *layout, const void *q,
+                              nova_kv_dtype q_dtype, int32_t batch, int32_t num_q_heads, const uint8_t *k_codes,
+                              const uint8_t *v_codes, const int32_t *seq_lens, int32_t max_seq_len,
+                              int32_t window, const float *sinks, float softmax_scale, float *out,
+                              void *workspace, size_t workspace_bytes, bool need_encode,
+                              novakv::DecodeArgs &a, novakv::DecodePlan &plan) {
+  nova_kv_status st = check_params(p, need_encode, true);
   if (st != NOVA_KV_OK) return st;
   if ((st = check_layout(layout)) != NOVA_KV_OK) return st;
   if (batch < 0) return fail(NOVA_KV_ERR_INVALID_ARG, "batch must be >= 0");
@@ -160,19 +162,19 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
   if (q_dtype != NOVA_KV_F32 && q_dtype != NOVA_KV_BF16)
     return fail(NOVA_KV_ERR_INVALID_ARG, "q_dtype must be NOVA_KV_F32 or NOVA_KV_BF16");
   if (!(softmax_scale >= 0.f)) return fail(NOVA_KV_ERR_INVALID_ARG, "softmax_scale must be >= 0");
-  if (batch == 0) return ok();
+  if (batch == 0) return NOVA_KV_OK;
   if (!q || !k_codes || !v_codes || !seq_lens || !out)
     return fail(NOVA_KV_ERR_INVALID_ARG, "q, k_codes, v_codes, seq_lens or out is NULL");
   if (!aligned(k_codes, 16) || !aligned(v_codes, 16))
     return fail(NOVA_KV_ERR_INVALID_ARG, "code pools must be 16-byte aligned");
-  const novakv::DecodePlan plan = novakv::plan_decode(batch, num_q_heads, p->num_kv_heads,
-                                                      p->head_dim, max_seq_len, layout->block_size, window);
+  plan = novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len, layout->block_size,
+                             window);
   if (!workspace || workspace_bytes < plan.total)
     return fail(NOVA_KV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
                 workspace ? workspace_bytes : static_cast<size_t>(0));
   if (!aligned(workspace, 256)) return fail(NOVA_KV_ERR_WORKSPACE, "workspace must be 256-byte aligned");
 
-  novakv::DecodeArgs a{};
+  a = novakv::DecodeArgs{};
   a.batch = batch;
   a.num_q_heads = num_q_heads;
   a.num_kv_heads = p->num_kv_heads;
@@ -201,11 +203,85 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
   a.sinkp = reinterpret_cast<float *>(ws + plan.off_sinkp);
   a.part_ml = reinterpret_cast<float *>(ws + plan.off_ml);
   a.part_acc = reinterpret_cast<float *>(ws + plan.off_acc);
+  a.newp = reinterpret_cast<float *>(ws + plan.off_new);
   a.n_split = plan.n_split;
   a.chunk = plan.chunk;
   a.b_chunk = novakv::plan_b_chunk(batch, p->num_kv_heads, plan.n_split);
+  return NOVA_KV_OK;
+}
+
+}  // namespace
+
+nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
+                                   const void *q, nova_kv_dtype q_dtype, int32_t batch,
+                                   int32_t num_q_heads, const uint8_t *k_codes,
+                                   const uint8_t *v_codes, const int32_t *seq_lens,
+                                   int32_t max_seq_len, int32_t window, const float *sinks,
+                                   float softmax_scale, float *out, void *workspace,
+                                   size_t workspace_bytes, void *hip_stream) {
+  novakv::DecodeArgs a;
+  novakv::DecodePlan plan;
+  nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, seq_lens,
+                                     max_seq_len, window, sinks, softmax_scale, out, workspace, workspace_bytes,
+                                     false, a, plan);
+  if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
   hipError_t e = novakv::launch_decode(a, plan.use_lut, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "decode launch: %s", hipGetErrorString(e));
+  return ok();
+}
+
+nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
+                                          const void *k_new, const void *v_new, nova_kv_dtype new_dtype,
+                                          const void *q, nova_kv_dtype q_dtype, int32_t batch,
+                                          int32_t num_q_heads, uint8_t *k_codes, uint8_t *v_codes,
+                                          const int32_t *seq_lens, int32_t max_seq_len, int32_t window,
+                                          const float *sinks, float softmax_scale, float *out,
+                                          void *workspace, size_t workspace_bytes, void *hip_stream) {
+  if (new_dtype != NOVA_KV_F32 && new_dtype != NOVA_KV_BF16)
+    return fail(NOVA_KV_ERR_INVALID_ARG, "new_dtype must be NOVA_KV_F32 or NOVA_KV_BF16");
+  novakv::DecodeArgs a;
+  novakv::DecodePlan plan;
+  nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, seq_lens,
+                                     max_seq_len, window, sinks, softmax_scale, out, workspace, workspace_bytes,
+                                     true, a, plan);
+  if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
+  if (!k_new || !v_new) return fail(NOVA_KV_ERR_INVALID_ARG, "k_new or v_new is NULL");
+  const hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  hipError_t e;
+  if (plan.use_lut && p->head_dim == 128) {
+    // one launch: the table kernel encodes the new token and attends to it
+    a.append = 1;
+    a.k_new = k_new;
+    a.v_new = v_new;
+    a.new_bf16 = new_dtype == NOVA_KV_BF16;
+    a.t_k = p->t_k;
+    a.k_codes_w = k_codes;
+    a.v_codes_w = v_codes;
+    e = novakv::launch_decode(a, plan.use_lut, stream);
+  } else {
+    // the one-token encode at position seq_lens[b] - 1, then the decode
+    novakv::EncodeArgs ea{};
+    ea.batch = batch;
+    ea.n_new = 1;
+    ea.num_kv_heads = p->num_kv_heads;
+    ea.head_dim = p->head_dim;
+    ea.kbar = p->kbar;
+    ea.t_k = p->t_k;
+    ea.t_v = p->t_v;
+    ea.cb_k = p->cb_k;
+    ea.cb_v = p->cb_v;
+    ea.layout = to_layout(layout);
+    ea.k = k_new;
+    ea.v = v_new;
+    ea.in_bf16 = new_dtype == NOVA_KV_BF16;
+    ea.start_pos = seq_lens;
+    ea.start_offset = -1;
+    ea.k_codes = k_codes;
+    ea.v_codes = v_codes;
+    e = novakv::launch_encode(ea, stream);
+    if (e == hipSuccess) e = novakv::launch_decode(a, plan.use_lut, stream);
+  }
+  if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "append-decode launch: %s", hipGetErrorString(e));
   return ok();
 }
 

@@ -24,6 +24,7 @@
 // combine kernel applies t_v^T once per head.
 #include <math.h>
 
+#include "encode_block.h"
 #include "lut_common.h"
 #include "nova_kv_internal.h"
 
@@ -52,14 +53,21 @@ constexpr uint32_t kAuxOut = kAuxPart + 4 * kD * 4;
 // control words: [0] arrival state, [1] next unclaimed round, [4..8) shifted
 // sink logits, [8..16) own (m, l) per head
 constexpr uint32_t kLdsBytes = kAuxCtl + 64;
+// Fused step only, after the decode's own LDS: three encoder teams' scratch
+// and the new token's per-block results [8 items][32] f32.
+constexpr uint32_t kAppendScratch = kLdsBytes;
+constexpr uint32_t kItemRes = kAppendScratch + 3 * sizeof(encblk::Scratch<kD>);
+constexpr uint32_t kLdsBytesAppend = kItemRes + 8 * 32 * 4;
+static_assert(kLdsBytes % 16 == 0 && kLdsBytesAppend <= 160 * 1024, "LDS budget of a workgroup");
+constexpr float kLn2 = 0.693147180559945309f;
 
-template <int WAVES>
+template <int WAVES, bool APPEND>
 constexpr uint32_t lds_bytes() {
   static_assert(WAVES * kMergeFloats * 4 <= kLutBytes, "merge scratch must fit in the table region");
   static_assert(WAVES >= kL / 4, "one wave per group block builds the table");
   static_assert(WAVES * 64 >= 512, "512 threads form q' and apply t_v");
   static_assert(WAVES >= 12, "waves 8..11 form the shifted sink logits");
-  return kLdsBytes;
+  return APPEND ? kLdsBytesAppend : kLdsBytes;
 }
 
 
@@ -92,10 +100,82 @@ __device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, 
   }
 }
 
+// Fused step: this split's share of the new token's encode.  Item i =
+// side * 4 + block (blocks of 8 groups) is done by split i mod n_eff.  Teams
+// of 256 threads (waves 4s .. 4s+3) take up to three items at a time with the
+// shared block encoder (encode_block.h), store the codes at position p of the
+// pools and leave each item's contribution in LDS: a key block the partial
+// logits of its 8 groups for each head (table entries of the stored codes,
+// added in group order), a value block its 32 coordinates of the decoded value
+// (transform domain).  Runs after the table and the value codebook are built;
+// every thread of the workgroup calls it.
 template <int WAVES>
+__device__ __forceinline__ void append_items(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
+                                             const int split, const int n_eff, const int p, const int bs_shift) {
+  static_assert(WAVES * 64 == 3 * encblk::kTeam, "three encoder teams");
+  const int tid = threadIdx.x;
+  const int slot = __builtin_amdgcn_readfirstlane(tid >> 8);
+  const int t = tid & (encblk::kTeam - 1);
+  encblk::Scratch<kD> *sc = reinterpret_cast<encblk::Scratch<kD> *>(smem + kAppendScratch) + slot;
+  float *res = reinterpret_cast<float *>(smem + kItemRes);
+  const int G = a.gqa;
+  const int nmine = (8 - split + n_eff - 1) / n_eff;  // items split, split + n_eff, ... below 8
+  const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
+  for (int base = 0; base < nmine; base += 3) {
+    const int k = base + slot;
+    const bool live = k < nmine;
+    const int item = split + k * n_eff;
+    const int side = item >> 2, blk = item & 3;
+    float4 trow[kD / 32];
+    uint2 cw[encblk::kPer];
+    if (live) {
+      const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * kD * kD;
+      const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * kL * 256 * 4;
+      encblk::load_block<kD>(t, tm, cbg, blk, trow, cw);
+      if (t < kD) {
+        const void *src = side == 0 ? a.k_new : a.v_new;
+        const size_t idx = (static_cast<size_t>(b) * a.num_kv_heads + kv) * kD + t;
+        double x = a.new_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
+                              : static_cast<double>(static_cast<const float *>(src)[idx]);
+        if (side == 0) x -= static_cast<double>(a.kbar[kv * kD + t]);
+        sc->xs[t] = x;
+      }
+    }
+    __syncthreads();
+    if (live) encblk::partial_block<kD>(t, *sc, trow);
+    __syncthreads();
+    if (live) encblk::sum_block<kD>(t, *sc);
+    __syncthreads();
+    if (live) {
+      const int code = encblk::search_block<kD>(t, *sc, cw);
+      if ((t & 31) == 0)
+        (side == 0 ? a.k_codes_w : a.v_codes_w)[tokoff + encblk::kGroups * blk + (t >> 5)] = static_cast<uint8_t>(code);
+    }
+    __syncthreads();
+    if (live && t < 32) {
+      float r = 0.f;
+      if (side == 0) {
+        if (t < G) {
+#pragma unroll
+          for (int gg = 0; gg < encblk::kGroups; ++gg) {
+            const int g = encblk::kGroups * blk + gg, c = sc->codes[gg];
+            r += static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + c * 256 + g * 8 + 2 * t));
+          }
+        }
+      } else {
+        const int g = encblk::kGroups * blk + (t >> 2), c = sc->codes[t >> 2];
+        r = static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + kVBase + (g & 7) * 8192 + 32 * c +
+                                                                   8 * (g >> 3) + 2 * (t & 3)));
+      }
+      res[item * 32 + t] = r;
+    }
+  }
+}
+
+template <int WAVES, bool APPEND>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int split, const int t0, const int t1, const size_t row0,
-                                           const int rot, float4 (&tv)[8]) {
+                                           const int rot, const int n_eff, const int S, float4 (&tv)[8]) {
   const uint32_t sbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8_ptr)smem));
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -122,7 +202,8 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 
   const int R0 = t0 & ~63;
   const int nrounds = (t1 - R0 + 63) >> 6;
-  const int last16 = (t1 - 1) & ~15;
+  // (a fused step's split that only encodes has t1 = t0: its position clamps stay in the sequence)
+  const int last16 = APPEND ? max(0, (t1 - 1) & ~15) : (t1 - 1) & ~15;
   const uint8_t *kpool = a.k_codes;
   const uint8_t *vpool = a.v_codes;
 
@@ -224,7 +305,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     const float2 kb2 = *reinterpret_cast<const float2 *>(a.kbar + static_cast<size_t>(kv) * kD + 2 * lane);
     // a wave without a round of its own (nrounds >= 1 in an active split)
     // re-reads the last round and never processes it
-    load_round(R0 + 64 * min(wave, nrounds - 1), kwb[0], vwb[0]);
+    load_round(max(0, R0 + 64 * min(wave, nrounds - 1)), kwb[0], vwb[0]);
     float *qs = reinterpret_cast<float *>(smem + kAuxQ);       // [4][128] query
     // partial q': [8 parts][32 groups][4 heads][4 coordinates], so that a table
     // lane's float4 (its group, its head) sits next to its neighbours'
@@ -328,6 +409,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     }
   }
   __syncthreads();
+  if constexpr (APPEND) {
+    if (n_eff > 0) append_items<WAVES>(a, smem, b, kv, split, n_eff, S - 1, bs_shift);
+  }
 
   // Selector of the key-side MFMA: row block r of the accumulator receives the
   // table partials of sub-tile r (A[m][k] = 1 where m = 4r + k-row).
@@ -489,7 +573,6 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   __syncthreads();
 
   // ---- merge the waves into this split's partial (natural-log max), kept in LDS
-  constexpr float kLn2 = 0.693147180559945309f;
   float *own = reinterpret_cast<float *>(smem + kAuxOwn);
   float *ownml = reinterpret_cast<float *>(smem + kAuxCtl) + 8;
   for (int i = tid; i < G * kD; i += WAVES * 64) {
@@ -528,10 +611,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 // the inverse value transform out = s_hat t_v^T (Corollary 1).  The split's
 // own partial is read from LDS, the other non-empty splits' from the
 // workspace; splits that attend to no token published nothing and are skipped.
-template <int WAVES>
-__device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int kv, const size_t row0,
-                                             const int own_split, const bool own_active, const int S, const int lo,
-                                             const float4 (&tv)[8]) {
+template <int WAVES, bool APPEND>
+__device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int kv, const int bk,
+                                             const size_t row0, const int own_split, const bool own_active,
+                                             const int S, const int lo, const int tend, const float4 (&tv)[8]) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -586,7 +669,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
         ms[i] = -INFINITY;
         ls[i] = 0.f;
         as[i] = 0.f;
-        const bool nonempty = lo + sp * a.chunk < S;
+        const bool nonempty = lo + sp * a.chunk < tend;
         if (sp == own_split) {
           if (own_active) {
             ms[i] = ctlf[8 + 2 * h];
@@ -601,6 +684,15 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
       }
 #pragma unroll
       for (int i = 0; i < 8; ++i) take(ms[i], ls[i], as[i]);
+    }
+    if constexpr (APPEND) {
+      if (S > 0) {  // the new token, after the splits: logit from the key blocks, value from the value blocks
+        const float *np = a.newp + static_cast<size_t>(bk) * 8 * 32;
+        float z = 0.f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) z += load_dev(np + k * 32 + h);
+        take(z * kLn2, 1.f, load_dev(np + (4 + (d >> 5)) * 32 + (d & 31)));
+      }
     }
     shat[tid] = den > 0.f ? num / den : 0.f;
   } else if (tid < 4 * kD) {
@@ -635,9 +727,9 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
 // partial to the workspace and counts its arrival; the last one combines.
 // The arrival counters live in the workspace and the last split resets its
 // counter to 0, so a decode step is a single launch.
-template <int WAVES>
+template <int WAVES, bool APPEND>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
+  __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES, APPEND>()];
   const int tid = threadIdx.x;
   // each XCD takes a contiguous range of the logical workgroup order
   int kv, b, split;
@@ -648,17 +740,30 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
 
   const int S = a.seq_lens[b];
   const int lo = a.window > 0 ? max(0, S - a.window) : 0;
-  const int t0 = lo + split * a.chunk;  // splits tile the attended span [lo, S)
-  const int t1 = min(S, lo + (split + 1) * a.chunk);
+  // A fused step reads the pools for [lo, S - 1); its newest token comes from
+  // the step's own key and value.
+  const int tend = APPEND ? max(S - 1, lo) : S;
+  const int t0 = lo + split * a.chunk;  // splits tile the attended span
+  const int t1 = min(tend, lo + (split + 1) * a.chunk);
   const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
   const bool active = t0 < t1;
+  // Fused step: the splits with pool tokens (at least split 0) share the encode
+  // of the new token; such a split runs the setup even with no token of its own.
+  int n_eff = 0;
+  bool items = false;
+  if (APPEND && S > 0) {
+    const int n_act = tend > lo ? (tend - lo + a.chunk - 1) / a.chunk : 0;
+    n_eff = max(n_act, 1);
+    items = split < n_eff;
+  }
+  const bool run = active || items;
 
   // Rows of t_v for the combine are requested as soon as the split's token
   // loop ends, before the arrival is known: their latency hides behind the
   // wave merge, and the last arrival finds them in registers.
   float4 tv[8];
-  if (active) {
-    split_pass<WAVES>(a, smem, b, kv, split, t0, t1, row0, rest, tv);
+  if (run) {
+    split_pass<WAVES, APPEND>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
   } else {
     load_tv_rows(a, kv, tv);
   }
@@ -670,9 +775,20 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   constexpr int kCtl = 512;
   int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
   __syncthreads();
+  if constexpr (APPEND) {  // this split's blocks of the new token, before its arrival
+    if (items && tid >= kCtl) {
+      const float *res = reinterpret_cast<const float *>(smem + kItemRes);
+      for (int j = tid - kCtl; j < 8 * 32; j += WAVES * 64 - kCtl)
+        if ((j >> 5) % n_eff == split) store_dev(a.newp + static_cast<size_t>(bk) * 8 * 32 + j, res[j]);
+    }
+    if (a.n_split == 1) {
+      if (tid >= kCtl) __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+    }
+  }
   if (a.n_split > 1) {
     if (tid >= kCtl) {
-      if (active) {
+      if (run) {
         const float *own = reinterpret_cast<const float *>(smem + kAuxOwn);
         const float *ownml = reinterpret_cast<const float *>(smem + kAuxCtl) + 8;
         for (int i = tid - kCtl; i < G * kD; i += WAVES * 64 - kCtl) {
@@ -697,7 +813,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
     __syncthreads();
     if (ctl[0] == 0) return;
   }
-  combine_unit<WAVES>(a, smem, kv, row0, split, active, S, lo, tv);
+  combine_unit<WAVES, APPEND>(a, smem, kv, bk, row0, split, run, S, lo, tend, tv);
 }
 
 }  // namespace
@@ -737,7 +853,10 @@ int plan_b_chunk(int batch, int num_kv_heads, int n_split) {
 hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream) {
   constexpr int W = 12;
   const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
-  decode_lut_d128<W><<<grid, dim3(W * 64), 0, stream>>>(a);
+  if (a.append)
+    decode_lut_d128<W, true><<<grid, dim3(W * 64), 0, stream>>>(a);
+  else
+    decode_lut_d128<W, false><<<grid, dim3(W * 64), 0, stream>>>(a);
   return hipGetLastError();
 }
 

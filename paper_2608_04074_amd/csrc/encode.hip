@@ -8,6 +8,7 @@
 // index is the exact argmin (smallest index among equal distances).
 #include <math.h>
 
+#include "encode_block.h"
 #include "nova_kv_internal.h"
 
 namespace novakv {
@@ -19,105 +20,42 @@ namespace {
 // columns (D x 32 fp32) and its 8 codebooks (16 KB), so each workgroup
 // fetches a quarter (D=128) or half (D=64) of the parameters, all loads
 // coalesced and issued before the first use; the launch costs about one
-// memory latency.
-//  * transform: thread (rg, c4) forms, in fp64, the partial coefficients of
-//    columns 4*c4 .. 4*c4+3 over its D/32 rows; 32 row-group partials per
-//    column are summed through LDS;
-//  * search: 32 lanes per group, 8 codewords each, keep the best (distance,
-//    index) pair, smallest index on equal distance, then a lane reduction.
+// memory latency.  The block itself is encode_block.h's team computation.
 template <int D>
 __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   constexpr int L = D / kGroupDim;
-  constexpr int GB = 8;                    // groups per workgroup
-  constexpr int NB = L / GB;               // group blocks per token
-  constexpr int COLS = GB * kGroupDim;     // 32 transform columns
-  constexpr int RPT = D / 32;              // rows per thread in the transform
-  constexpr int PER = kCodebookSize / 32;  // codewords per lane
-  __shared__ double xs[D];
-  __shared__ double part[32][COLS + 1];
-  __shared__ double us[COLS];
+  constexpr int NB = L / encblk::kGroups;  // group blocks per token
+  __shared__ encblk::Scratch<D> sc;
   const int blk = blockIdx.x % NB;
   const int side = (blockIdx.x / NB) & 1;
   const int t = blockIdx.x / (2 * NB);
   const int kv = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
-  const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D + COLS * blk;
-  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) +
-                        (static_cast<size_t>(kv) * L + GB * blk) * kCodebookSize * kGroupDim;
+  const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D;
+  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * L * kCodebookSize * kGroupDim;
   const void *src = side == 0 ? a.k : a.v;
   uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
-  const int c4 = tid & 7, rg = tid >> 3;   // transform: columns 4*c4.., rows RPT*rg..
-  const int gl = tid >> 5, r = tid & 31;   // search: group gl of the block, lane r
 
-  float4 trow[RPT];
-#pragma unroll
-  for (int j = 0; j < RPT; ++j) trow[j] = *reinterpret_cast<const float4 *>(tm + (RPT * rg + j) * D + 4 * c4);
-  const uint2 *row = reinterpret_cast<const uint2 *>(cbg) + gl * kCodebookSize;
-  uint2 cw[PER];
-#pragma unroll
-  for (int k = 0; k < PER; ++k) cw[k] = row[r + 32 * k];
+  float4 trow[D / 32];
+  uint2 cw[encblk::kPer];
+  encblk::load_block<D>(tid, tm, cbg, blk, trow, cw);
   if (tid < D) {
     const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + tid;
     double x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
                          : static_cast<double>(static_cast<const float *>(src)[idx]);
     if (side == 0) x -= static_cast<double>(a.kbar[kv * D + tid]);
-    xs[tid] = x;
+    sc.xs[tid] = x;
   }
   __syncthreads();
-  {
-    double acc[4] = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      const double x = xs[RPT * rg + j];
-      acc[0] = fma(x, static_cast<double>(trow[j].x), acc[0]);
-      acc[1] = fma(x, static_cast<double>(trow[j].y), acc[1]);
-      acc[2] = fma(x, static_cast<double>(trow[j].z), acc[2]);
-      acc[3] = fma(x, static_cast<double>(trow[j].w), acc[3]);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) part[rg][4 * c4 + i] = acc[i];
-  }
+  encblk::partial_block<D>(tid, sc, trow);
   __syncthreads();
-  if (tid < COLS) {
-    double u = part[0][tid];
-#pragma unroll
-    for (int p = 1; p < 32; ++p) u += part[p][tid];
-    us[tid] = u;
-  }
+  encblk::sum_block<D>(tid, sc);
   __syncthreads();
-  const double u0 = us[gl * 4 + 0], u1 = us[gl * 4 + 1], u2 = us[gl * 4 + 2], u3 = us[gl * 4 + 3];
-  double best = INFINITY;
-  int arg = 0;
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-#pragma clang fp contract(off)
-    const int c = r + 32 * k;
-    const uint2 w = cw[k];
-    const double e0 = u0 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.x & 0xffff)));
-    const double e1 = u1 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.x >> 16)));
-    const double e2 = u2 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.y & 0xffff)));
-    const double e3 = u3 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.y >> 16)));
-    double dist = e0 * e0;
-    dist = dist + e1 * e1;
-    dist = dist + e2 * e2;
-    dist = dist + e3 * e3;
-    if (dist < best) {
-      best = dist;
-      arg = c;
-    }
-  }
-#pragma unroll
-  for (int o = 16; o > 0; o >>= 1) {
-    const double ob = __shfl_xor(best, o, 64);
-    const int oa = __shfl_xor(arg, o, 64);
-    if (ob < best || (ob == best && oa < arg)) {
-      best = ob;
-      arg = oa;
-    }
-  }
-  if (r == 0) {
-    const int pos = a.start_pos[b] + t;
-    pool[code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos) + GB * blk + gl] = static_cast<uint8_t>(arg);
+  const int code = encblk::search_block<D>(tid, sc, cw);
+  if ((tid & 31) == 0) {
+    const int pos = a.start_pos[b] + a.start_offset + t;
+    pool[code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos) + encblk::kGroups * blk + (tid >> 5)] =
+        static_cast<uint8_t>(code);
   }
 }
 
@@ -265,7 +203,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   __syncthreads();
   for (int i = tid; i < nt * L; i += 256) {
     const int t = i / L, ell = i % L;
-    const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, a.start_pos[b] + n0 + t);
+    const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, a.start_pos[b] + a.start_offset + n0 + t);
     pool[off + ell] = codes[t][ell];
   }
 }

@@ -51,6 +51,15 @@ struct DecodeArgs {
   int n_split;      // context splits per sequence
   int chunk;        // tokens per split
   int b_chunk;      // table kernels: sequences per block of the workgroup order (divides batch)
+  // Fused step (nova_kv_append_decode_attn): the step's key and value of every
+  // sequence are encoded in the launch, stored at position seq_lens[b] - 1 and
+  // attended from their codes; the pool tokens read are [lo, seq_lens[b] - 1).
+  int append;
+  const void *k_new, *v_new;  // [B][Hkv][D]
+  int new_bf16;
+  const float *t_k;
+  uint8_t *k_codes_w, *v_codes_w;  // the pools k_codes / v_codes, written at the new position
+  float *newp;      // [B][Hkv][8 items][32] per-block results for the new token
 };
 
 struct EncodeArgs {
@@ -61,6 +70,7 @@ struct EncodeArgs {
   const void *k, *v;
   int in_bf16;
   const int32_t *start_pos;
+  int start_offset;  // the first new token of sequence b goes to start_pos[b] + start_offset
   uint8_t *k_codes, *v_codes;
 };
 
@@ -69,7 +79,7 @@ struct DecodePlan {
   int use_lut;      // 1: table-based stage 1 (decode_lut.hip), 0: generic stage 1
   int n_split;
   int chunk;
-  size_t off_cnt, off_qp, off_sinkp, off_ml, off_acc, total;
+  size_t off_cnt, off_qp, off_sinkp, off_ml, off_acc, off_new, total;
 };
 // Splits tile each sequence's attended span (the last `window` tokens, or all).
 // The workspace (off_*, total) is sized for every window and both decode

@@ -369,6 +369,106 @@ def test_generic_path_paged_block8(nk, qwen_small, window, use_sink):
                          what=f"generic block8 window={window} sink={use_sink}")
 
 
+# ----------------------------------------- fused step: append the token, then decode
+
+def _step_inputs(wl, B, cap, lens, seed_layer=0):
+    """History codes for positions < lens[b] - 1 and the step's token at lens[b] - 1."""
+    H, L, D = wl.num_kv_heads, wl.groups, wl.head_dim
+    ck, cv = _random_pools(wl, seed_layer, B, cap, H, L)
+    kn = np.empty((B, H, D))
+    vn = np.empty_like(kn)
+    for b in range(B):
+        for kv in range(H):
+            kn[b, kv], vn[b, kv] = (x[0] for x in synth.cache_tokens(wl, seed_layer, kv, b, 1,
+                                                                       start=max(int(lens[b]) - 1, 0)))
+    return ck, cv, kn, vn
+
+
+@pytest.mark.parametrize("paged,window,use_sink", [(False, 0, True), (False, 300, True), (True, 0, False),
+                                                   (False, 1, False)])
+def test_append_decode_matches_oracle(nk, qwen_small, paged, window, use_sink):
+    """One-launch step at the Qwen shape: the token's codes bit-exact, the output within tolerance."""
+    wl, params, P = qwen_small
+    B, cap = 6, 2304
+    H, L, G, D = wl.num_kv_heads, wl.groups, wl.gqa, wl.head_dim
+    lens = np.array([1, 2, 65, 1024, 2000, 2304], dtype=np.int32)
+    ck, cv, kn, vn = _step_inputs(wl, B, cap, lens)
+    if paged:
+        bs, bps = 16, cap // 16
+        table = np.random.default_rng(17).permutation(B * bps).astype(np.int32).reshape(B, bps)
+        lay = nk.CacheLayout(bs, bps, dev(table, torch.int32))
+    else:
+        bs, bps, table = cap, 1, None
+        lay = nk.CacheLayout.contiguous(cap)
+    lk = lay_kwargs(H, bs, bps, table)
+    flat_k = np.zeros(B * bps * H * bs * L, dtype=np.uint8)
+    flat_v = np.zeros_like(flat_k)
+    for b in range(B):
+        for kv in range(H):
+            write_rows(flat_k, ck[b, kv], b, kv, 0, **lk)
+            write_rows(flat_v, cv[b, kv], b, kv, 0, **lk)
+    pk, pv = dev(flat_k, torch.uint8), dev(flat_v, torch.uint8)
+    q = synth.decode_queries(wl, 0, batch=B)
+    sinks = np.random.default_rng(5).standard_normal(wl.num_q_heads).astype(np.float32) if use_sink else None
+    say(f"append+decode paged={paged} window={window} sink={use_sink}")
+    out = nk.append_decode_attn(P, lay, dev(kn, torch.bfloat16), dev(vn, torch.bfloat16), dev(q, torch.bfloat16),
+                                pk, pv, dev(lens, torch.int32), cap, window=window,
+                                sinks=dev(sinks, torch.float32) if use_sink else None).cpu().numpy()
+    hk, hv = pk.cpu().numpy(), pv.cpu().numpy()
+    ref_k, ref_v = flat_k.copy(), flat_v.copy()
+    for b in range(B):
+        p = int(lens[b]) - 1
+        for kv in range(H):
+            okk, ogk, ovv, ogv = ocodec.encode_tokens(kn[b, kv][None], vn[b, kv][None], oatt.head_params(params, kv))
+            compare_codes(read_rows(hk, b, kv, p, 1, groups=L, **lk), okk, ogk, f"step b{b} kv{kv} K")
+            compare_codes(read_rows(hv, b, kv, p, 1, groups=L, **lk), ovv, ogv, f"step b{b} kv{kv} V")
+            write_rows(ref_k, okk, b, kv, p, **lk)
+            write_rows(ref_v, ovv, b, kv, p, **lk)
+            # every other row untouched
+        before = read_rows(hk, b, 0, 0, p, groups=L, **lk)
+        assert np.array_equal(before, read_rows(flat_k, b, 0, 0, p, groups=L, **lk))
+    scale = 1 / np.sqrt(D)
+    ref = np.zeros_like(out, dtype=np.float64)
+    for b in range(B):
+        for kv in range(H):
+            ref[b, kv * G:(kv + 1) * G] = oracle_rows(q, ref_k, ref_v, params, b, kv, int(lens[b]), scale, lk,
+                                                       window, sinks, G)
+    assert_outputs_close(out.reshape(-1, D), ref.reshape(-1, D),
+                         what=f"append+decode paged={paged} window={window} sink={use_sink}")
+
+
+@pytest.mark.parametrize("shape", ["qwen3_8b", "gptoss_pair"])
+def test_append_decode_equals_encode_then_decode(nk, shape):
+    """The step in one call stores the same bytes as the one-token encode and gives the decode's output."""
+    wl = synth.get_workload(shape)
+    params = calibrated_params(wl, 0)
+    P = upload_params(nk, params)
+    B, cap = 4, 4096
+    H, L, D = wl.num_kv_heads, wl.groups, wl.head_dim
+    lens = np.array([4096, 3001, 64, 1], dtype=np.int32)
+    ck, cv, kn, vn = _step_inputs(wl, B, cap, lens)
+    q = dev(synth.decode_queries(wl, 0, batch=B), torch.bfloat16)
+    sinks = dev(synth.sink_logits(wl, 0), torch.float32) if wl.sinks else None
+    lay = nk.CacheLayout.contiguous(cap)
+    lens_d = dev(lens, torch.int32)
+    kn_d, vn_d = dev(kn, torch.bfloat16), dev(vn, torch.bfloat16)
+    say(f"{shape}: two calls")
+    pk1, pv1 = dev(ck, torch.uint8), dev(cv, torch.uint8)
+    nk.encode(P, lay, kn_d[:, None], vn_d[:, None], lens_d - 1, pk1, pv1)
+    out1 = nk.decode_attn(P, lay, q, pk1, pv1, lens_d, cap, sinks=sinks)
+    say(f"{shape}: one call")
+    pk2, pv2 = dev(ck, torch.uint8), dev(cv, torch.uint8)
+    out2 = nk.append_decode_attn(P, lay, kn_d, vn_d, q, pk2, pv2, lens_d, cap, sinks=sinks)
+    torch.cuda.synchronize()
+    assert torch.equal(pk1, pk2) and torch.equal(pv1, pv2)
+    # Inside a split the new token's probability passes through the fp16 value
+    # operand (relative rounding 2^-12 of its weight); the one-call step adds
+    # its term in fp32 after the combine.  The two differ by that rounding.
+    err = (out2 - out1).abs().amax(dim=-1) / out1.norm(dim=-1).clamp_min(1e-30)
+    print(f"[parity] {shape} one-call vs two-call worst_rel_diff={float(err.max()):.3e}", flush=True)
+    assert float(err.max()) <= 1e-4
+
+
 # ------------------------------------------------- full-size configurations
 
 def _full_decode(nk, wl, layer, params, units, window=0, batch=None, cap=None):
