@@ -57,7 +57,8 @@ constexpr uint32_t kLdsBytes = kAuxCtl + 64;
 // and the new token's per-block results [8 items][32] f32.
 constexpr uint32_t kAppendScratch = kLdsBytes;
 constexpr uint32_t kItemRes = kAppendScratch + 3 * sizeof(encblk::Scratch<kD>);
-constexpr uint32_t kLdsBytesAppend = kItemRes + 8 * 32 * 4;
+constexpr uint32_t kTeamCtr = kItemRes + 8 * 32 * 4;  // arrivals of the encoder team's waves
+constexpr uint32_t kLdsBytesAppend = kTeamCtr + 16;
 static_assert(kLdsBytes % 16 == 0 && kLdsBytesAppend <= 160 * 1024, "LDS budget of a workgroup");
 constexpr float kLn2 = 0.693147180559945309f;
 
@@ -101,74 +102,94 @@ __device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, 
 }
 
 // Fused step: this split's share of the new token's encode.  Item i =
-// side * 4 + block (blocks of 8 groups) is done by split i mod n_eff.  Teams
-// of 256 threads (waves 4s .. 4s+3) take up to three items at a time with the
-// shared block encoder (encode_block.h), store the codes at position p of the
-// pools and leave each item's contribution in LDS: a key block the partial
-// logits of its 8 groups for each head (table entries of the stored codes,
-// added in group order), a value block its 32 coordinates of the decoded value
-// (transform domain).  Runs after the table and the value codebook are built;
-// every thread of the workgroup calls it.
-template <int WAVES>
-__device__ __forceinline__ void append_items(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
-                                             const int split, const int n_eff, const int p, const int bs_shift) {
-  static_assert(WAVES * 64 == 3 * encblk::kTeam, "three encoder teams");
-  const int tid = threadIdx.x;
-  const int slot = __builtin_amdgcn_readfirstlane(tid >> 8);
-  const int t = tid & (encblk::kTeam - 1);
-  encblk::Scratch<kD> *sc = reinterpret_cast<encblk::Scratch<kD> *>(smem + kAppendScratch) + slot;
+// side * 4 + block (blocks of 8 groups) is done by split i mod n_eff.  Waves
+// 8..11 (the encoder team, 256 threads) take this split's items one after the
+// other with the shared block encoder (encode_block.h), right after the
+// table is built, while waves 0..7 start the token loop (rounds are claimed
+// dynamically, so the team's waves simply take fewer).  The team synchronises
+// through an LDS arrival counter instead of workgroup barriers.  Each item
+// stores its codes at position p of the pools and leaves its contribution in
+// LDS: a key block the partial logits of its 8 groups for each head (table
+// entries of the stored codes, added in group order), a value block its 32
+// coordinates of the decoded value (transform domain).
+__device__ __forceinline__ int items_of_split(const int split, const int n_eff) {
+  return (8 - split + n_eff - 1) / n_eff;  // items split, split + n_eff, ... below 8
+}
+
+// All four waves of the team arrive, then each continues once the counter
+// has reached 4 * phase: LDS writes before the call are visible after it.
+__device__ __forceinline__ void team_sync(uint8_t *smem, const int phase) {
+  int *ctr = reinterpret_cast<int *>(smem + kTeamCtr);
+  if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+  while (__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 4 * phase)
+    __builtin_amdgcn_s_sleep(1);
+}
+
+// The loads of the team's k-th item (thread t = tid - 512 of the team).
+struct ItemRegs {
+  float4 trow[kD / 32];
+  uint2 cw[encblk::kPer];
+  double x;  // thread t < D: element t of the token minus k_bar (keys) or of the token (values)
+};
+
+__device__ __forceinline__ void load_item(const DecodeArgs &a, const int b, const int kv, const int split,
+                                          const int n_eff, const int k, const int t, ItemRegs &r) {
+  const int item = split + k * n_eff;
+  const int side = item >> 2, blk = item & 3;
+  const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * kD * kD;
+  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * kL * 256 * 4;
+  encblk::load_block<kD>(t, tm, cbg, blk, r.trow, r.cw);
+  if (t < kD) {
+    const void *src = side == 0 ? a.k_new : a.v_new;
+    const size_t idx = (static_cast<size_t>(b) * a.num_kv_heads + kv) * kD + t;
+    double x = a.new_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
+                          : static_cast<double>(static_cast<const float *>(src)[idx]);
+    if (side == 0) x -= static_cast<double>(a.kbar[kv * kD + t]);
+    r.x = x;
+  }
+}
+
+// Called by the team's threads only (t = tid - 512); r holds item 0's loads.
+__device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
+                                             const int split, const int n_eff, const size_t tokoff, const int t,
+                                             ItemRegs &r) {
+  encblk::Scratch<kD> *sc = reinterpret_cast<encblk::Scratch<kD> *>(smem + kAppendScratch);
   float *res = reinterpret_cast<float *>(smem + kItemRes);
   const int G = a.gqa;
-  const int nmine = (8 - split + n_eff - 1) / n_eff;  // items split, split + n_eff, ... below 8
-  const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
-  for (int base = 0; base < nmine; base += 3) {
-    const int k = base + slot;
-    const bool live = k < nmine;
+  const int nmine = items_of_split(split, n_eff);
+  int phase = 0;
+  for (int k = 0; k < nmine; ++k) {
     const int item = split + k * n_eff;
     const int side = item >> 2, blk = item & 3;
-    float4 trow[kD / 32];
-    uint2 cw[encblk::kPer];
-    if (live) {
-      const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * kD * kD;
-      const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * kL * 256 * 4;
-      encblk::load_block<kD>(t, tm, cbg, blk, trow, cw);
-      if (t < kD) {
-        const void *src = side == 0 ? a.k_new : a.v_new;
-        const size_t idx = (static_cast<size_t>(b) * a.num_kv_heads + kv) * kD + t;
-        double x = a.new_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
-                              : static_cast<double>(static_cast<const float *>(src)[idx]);
-        if (side == 0) x -= static_cast<double>(a.kbar[kv * kD + t]);
-        sc->xs[t] = x;
-      }
-    }
-    __syncthreads();
-    if (live) encblk::partial_block<kD>(t, *sc, trow);
-    __syncthreads();
-    if (live) encblk::sum_block<kD>(t, *sc);
-    __syncthreads();
-    if (live) {
-      const int code = encblk::search_block<kD>(t, *sc, cw);
-      if ((t & 31) == 0)
-        (side == 0 ? a.k_codes_w : a.v_codes_w)[tokoff + encblk::kGroups * blk + (t >> 5)] = static_cast<uint8_t>(code);
-    }
-    __syncthreads();
-    if (live && t < 32) {
-      float r = 0.f;
+    if (k > 0) load_item(a, b, kv, split, n_eff, k, t, r);
+    if (t < kD) sc->xs[t] = r.x;
+    team_sync(smem, ++phase);
+    encblk::partial_block<kD>(t, *sc, r.trow);
+    team_sync(smem, ++phase);
+    encblk::sum_block<kD>(t, *sc);
+    team_sync(smem, ++phase);
+    const int code = encblk::search_block<kD>(t, *sc, r.cw);
+    if ((t & 31) == 0)
+      (side == 0 ? a.k_codes_w : a.v_codes_w)[tokoff + encblk::kGroups * blk + (t >> 5)] = static_cast<uint8_t>(code);
+    team_sync(smem, ++phase);
+    if (t < 32) {
+      float v = 0.f;
       if (side == 0) {
         if (t < G) {
 #pragma unroll
           for (int gg = 0; gg < encblk::kGroups; ++gg) {
             const int g = encblk::kGroups * blk + gg, c = sc->codes[gg];
-            r += static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + c * 256 + g * 8 + 2 * t));
+            v += static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + c * 256 + g * 8 + 2 * t));
           }
         }
       } else {
         const int g = encblk::kGroups * blk + (t >> 2), c = sc->codes[t >> 2];
-        r = static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + kVBase + (g & 7) * 8192 + 32 * c +
+        v = static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + kVBase + (g & 7) * 8192 + 32 * c +
                                                                    8 * (g >> 3) + 2 * (t & 3)));
       }
-      res[item * 32 + t] = r;
+      res[item * 32 + t] = v;
     }
+    team_sync(smem, ++phase);  // the scratch is reused by the next item
   }
 }
 
@@ -237,7 +258,11 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   uint2 kwb[2][4], vwb[2][4];
   int *rctr = reinterpret_cast<int *>(smem + kAuxCtl) + 1;
   if (tid == 0) *rctr = WAVES;  // rounds 0 .. WAVES-1 are taken; visible after the setup's barriers
+  if constexpr (APPEND) {
+    if (tid == 0) *reinterpret_cast<int *>(smem + kTeamCtr) = 0;
+  }
 
+  ItemRegs ir;  // fused step: the encoder team's first item, loaded during the setup
   // ---- setup: value codebook into LDS, table of partial logits via MFMA.
   // All global loads of the setup are issued before any of them is used, in
   // the order query, t_k_inv_t rows, key codebook, value codebook, k_bar,
@@ -351,6 +376,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
         acc[hh].w = add_rows32(acc[hh].w);
         if (lane < 32) *reinterpret_cast<float4 *>(qsum + wave * 512 + e4 * 16 + hh * 4) = acc[hh];
       }
+    } else if constexpr (APPEND) {
+      // the encoder team requests its first item; the table build covers the latency
+      if (n_eff > 0) load_item(a, b, kv, split, n_eff, 0, tid - 512, ir);
     }
     __syncthreads();
     if (lut_wave) {
@@ -410,7 +438,12 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   }
   __syncthreads();
   if constexpr (APPEND) {
-    if (n_eff > 0) append_items<WAVES>(a, smem, b, kv, split, n_eff, S - 1, bs_shift);
+    static_assert(WAVES == 12, "the encoder team is waves 8..11");
+    if (n_eff > 0 && wave >= 8) {
+      const int p = S - 1;
+      const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
+      encode_items(a, smem, b, kv, split, n_eff, tokoff, tid - 512, ir);
+    }
   }
 
   // Selector of the key-side MFMA: row block r of the accumulator receives the
@@ -645,6 +678,16 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
     const int h = tid >> 7;
     const size_t r = (row0 + h) * a.n_split;
     const float sk = ctlf[4 + h];
+    // fused step: the new token's block results, requested with the splits' partials
+    float zp[4] = {0.f, 0.f, 0.f, 0.f}, vp = 0.f;
+    if constexpr (APPEND) {
+      if (S > 0) {
+        const float *np = a.newp + static_cast<size_t>(bk) * 8 * 32;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) zp[k] = load_dev(np + k * 32 + h);
+        vp = load_dev(np + (4 + (d >> 5)) * 32 + (d & 31));
+      }
+    }
     // online log-sum-exp over the splits, the sink counted once
     float big = sk, num = 0.f, den = sk == -INFINITY ? 0.f : 1.f;
     auto take = [&](float ms, float ls, float as) {
@@ -686,13 +729,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
       for (int i = 0; i < 8; ++i) take(ms[i], ls[i], as[i]);
     }
     if constexpr (APPEND) {
-      if (S > 0) {  // the new token, after the splits: logit from the key blocks, value from the value blocks
-        const float *np = a.newp + static_cast<size_t>(bk) * 8 * 32;
-        float z = 0.f;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) z += load_dev(np + k * 32 + h);
-        take(z * kLn2, 1.f, load_dev(np + (4 + (d >> 5)) * 32 + (d & 31)));
-      }
+      if (S > 0) take((((zp[0] + zp[1]) + zp[2]) + zp[3]) * kLn2, 1.f, vp);  // the new token, after the splits
     }
     shat[tid] = den > 0.f ? num / den : 0.f;
   } else if (tid < 4 * kD) {
