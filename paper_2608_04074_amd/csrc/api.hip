@@ -204,6 +204,8 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   a.part_ml = reinterpret_cast<float *>(ws + plan.off_ml);
   a.part_acc = reinterpret_cast<float *>(ws + plan.off_acc);
   a.newp = reinterpret_cast<float *>(ws + plan.off_new);
+  a.xch = reinterpret_cast<uint64_t *>(ws + plan.off_xch);
+  a.xnew = reinterpret_cast<uint64_t *>(ws + plan.off_xnew);
   a.n_split = plan.n_split;
   a.chunk = plan.chunk;
   a.b_chunk = novakv::plan_b_chunk(batch, p->num_kv_heads, plan.n_split);

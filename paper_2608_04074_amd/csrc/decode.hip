@@ -338,7 +338,9 @@ DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_di
   p.off_ml = align(p.off_sinkp + rows * sizeof(float));
   p.off_acc = align(p.off_ml + rows * max_split * 2 * sizeof(float));
   p.off_new = align(p.off_acc + rows * max_split * head_dim * sizeof(float));
-  p.total = align(p.off_new + static_cast<size_t>(batch) * num_kv_heads * 8 * 32 * sizeof(float));
+  p.off_xch = align(p.off_new + static_cast<size_t>(batch) * num_kv_heads * 8 * 32 * sizeof(float));
+  p.off_xnew = align(p.off_xch + units * max_split * kXchSlotWords * sizeof(uint64_t));
+  p.total = align(p.off_xnew + static_cast<size_t>(units) * 8 * 32 * sizeof(uint64_t));
   return p;
 }
 

@@ -1,27 +1,29 @@
-// Decode stage 1 for head_dim 128 and up to 4 query heads per KV head.
+// Decode attention for head_dim 128 and up to 4 query heads per KV head, in
+// one launch: query transform, split pass, and the combine of the splits.
 //
 // One workgroup owns one (sequence, KV head, context split) unit.  It stages
 // the KV head's value codebook in LDS and builds a per-query table of partial
 // logits LUT[c][g] = (q'_h[4g..4g+3] . C_K[g][c])_{h<4} (fp16, 64 KB) with
-// MFMA, so that a key's logit is the sum of its 32 table entries.  This is
-// the paper's read path (q' = q R_K^{-T} folded in once per step, one
+// the 4x4x4 MFMA, so that a key's logit is the sum of its 32 table entries.
+// This is the paper's read path (q' = q R_K^{-T} folded in once per step, one
 // codebook lookup per group; Sec. "Decoding kernel and read path") with the
 // q'-codeword dot products hoisted out of the token loop.
 //
-// Token loop, per wave, per round of 64 tokens:
-//  * K: ds_read_b64_tr_b16 gathers from the table.  Lane (beta,u,v) =
-//    16*beta + 4*u + v reads, at step t, group 8u + ((t + 2v + (beta&1)) & 7)
-//    of token 16r + 4*beta + v: the 32 lanes of each half-wave touch 32
-//    distinct groups, i.e. 32 distinct bank pairs of the entry-major table.
-//    The transposing read hands lane (beta,u,v) the four partials of
-//    (token 16r + 4*beta + u, head v), summed with v_dot2_f32_f16.
-//  * online softmax in log2 units (q' carries the log2(e) factor);
-//  * V: transposing reads of the staged codebook give the token-major MFMA
-//    operand (4 tokens of one transform coordinate per lane); the
-//    probabilities already sit in the matching layout.  One
-//    v_mfma_f32_16x16x16_f16 per (token set, 16 coordinates).
-// The value accumulator stays in the transform domain (Corollary 1); the
-// combine kernel applies t_v^T once per head.
+// Token loop: waves claim rounds of 64 tokens from an LDS counter and
+// prefetch the next round's codes while processing the current one.
+//  * K: ds_read_b64_tr_b16 gathers from the table; a 16x16x32 MFMA with a
+//    0/1 selector operand sums each token's 32 partials per head.
+//  * online softmax in log2 units (q' carries the log2(e) factor), with a
+//    lagging reference so the accumulator is rescaled rarely;
+//  * V: transposing reads of the staged codebook give the MFMA operand of 8
+//    tokens' coordinates; the probabilities (fp16) are the other operand.
+// The value accumulator stays in the transform domain (Corollary 1).  Every
+// split publishes its partial and counts its arrival; the last one merges
+// the partials, adds the sink and applies t_v^T once per head.
+//
+// The APPEND variant is a whole decode step: it also encodes the step's key
+// and value (position seq_len - 1) and merges that token's term after the
+// splits, so the cache read covers positions before it only.
 #include <math.h>
 
 #include "encode_block.h"
@@ -39,7 +41,12 @@ constexpr int kL = kD / kGroupDim;          // 32 groups
 constexpr uint32_t kLutBytes = 65536;       // [256 codes][32 groups][4 heads] fp16
 constexpr uint32_t kVBase = kLutBytes;      // value codebook, 64 KB
 constexpr uint32_t kMergeBase = 0;          // per-wave merge scratch, reuses the table once done
-constexpr int kMergeFloats = 4 * kD + 8;
+// Per-wave merge scratch: [0..4) m, [4..8) l, then coordinate d of head h at
+// 8 + h * kMergeHead + (d / 32) * kMergeBlk + d % 32.  With this padding the 16
+// lanes that store a wave's accumulators (one 16-byte store per lane) hit 16
+// distinct groups of four banks.
+constexpr int kMergeHead = 144, kMergeBlk = 36;
+constexpr int kMergeFloats = 8 + 3 * kMergeHead + 3 * kMergeBlk + 32 + 4;
 constexpr float kLazyLog2 = 8.f;  // reference lag allowed in the online softmax (log2 units)
 // Auxiliary region: query staging and the partial sums of q', later the
 // combine's merged accumulator and partial outputs, and a few control words.
@@ -586,13 +593,14 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   }
   m_run = m_head;
 
-  __syncthreads();  // every wave is done with the table before it becomes merge scratch
-  // Rows of t_v for the combine are requested now, before the arrival is
-  // known: their latency hides behind the wave merge, and the last arrival
-  // finds them in registers.
+  // Rows of t_v for the combine are requested as soon as this wave's loop
+  // ends, before the arrival is known: their latency hides behind the waves
+  // still in the loop and the merge, and the last arrival finds them in
+  // registers.
   load_tv_rows(a, kv, tv);
+  __syncthreads();  // every wave is done with the table before it becomes merge scratch
   float *merge = reinterpret_cast<float *>(smem + kMergeBase);
-  float *mw = merge + wave * kMergeFloats;  // [0..4) m, [4..8) l, [8 + h*128 + d) acc
+  float *mw = merge + wave * kMergeFloats;
   if (lane < 4) {
     mw[lane] = m_run;
     mw[4 + lane] = l_tot;
@@ -601,7 +609,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
     for (int X = 0; X < 8; ++X)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) mw[8 + v * kD + 32 * beta + 4 * X + i] = acc[X][i];
+      for (int i = 0; i < 4; ++i) mw[8 + v * kMergeHead + kMergeBlk * beta + 4 * X + i] = acc[X][i];
   }
   __syncthreads();
 
@@ -616,7 +624,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     for (int w = 0; w < WAVES; ++w) {
       mv[w] = merge[w * kMergeFloats + h];
       lv[w] = merge[w * kMergeFloats + 4 + h];
-      av[w] = merge[w * kMergeFloats + 8 + h * kD + d];
+      av[w] = merge[w * kMergeFloats + 8 + h * kMergeHead + (d >> 5) * kMergeBlk + (d & 31)];
     }
     float big = -INFINITY;
 #pragma unroll
@@ -638,16 +646,70 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   }
 }
 
-// Last arriving split of a (sequence, KV head): log-sum-exp merge of the
+// Exchange between the splits of a (sequence, KV head).  Thread kCtl, alone
+// in its wave so that no other memory operation of that wave delays its reply
+// (a wave's memory operations complete in issue order), counts the split in;
+// waves kPub.. publish the split's partial and its blocks of the new token as
+// tagged words and do not wait for them to land.  The split that brings the
+// count to n_split combines: it checks the tag of every word it reads, so no
+// order between the stores and the count is needed.
+constexpr int kCtl = 512;
+constexpr int kPub = 576;
+constexpr int kPubThreads = 12 * 64 - kPub;
+// Bound of the wait for a word whose writer has already counted itself in:
+// it only has to complete a store, so the bound is never reached in practice.
+constexpr int kSpinLimit = 1 << 20;
+
+// Slot words: (m, l) of head h at 2h, 2h+1; coordinate d of head h at
+// 2G + h*128 + d.  New token: item k (side * 4 + block) lane j at 32k + j,
+// key blocks for lanes j < G (the heads), value blocks for all 32 lanes.
+// With clear set, the same threads empty the same words, in the same order.
+template <bool APPEND>
+__device__ __forceinline__ void publish(const DecodeArgs &a, uint8_t *smem, const int bk, const int split,
+                                        const bool partial, const bool items, const int n_eff, const int t,
+                                        const bool clear) {
+  const int G = a.gqa;
+  if (partial) {
+    uint64_t *slot = a.xch + (static_cast<size_t>(bk) * a.n_split + split) * kXchSlotWords;
+    const float *own = reinterpret_cast<const float *>(smem + kAuxOwn);
+    const float *ownml = reinterpret_cast<const float *>(smem + kAuxCtl) + 8;
+    for (int j = t; j < 2 * G + G * kD; j += kPubThreads) {
+      if (clear)
+        clear_word(slot + j);
+      else
+        put_word(slot + j, j < 2 * G ? ownml[j] : own[j - 2 * G]);
+    }
+  }
+  if constexpr (APPEND) {
+    if (items) {
+      const float *res = reinterpret_cast<const float *>(smem + kItemRes);
+      uint64_t *xn = a.xnew + static_cast<size_t>(bk) * 8 * 32;
+      for (int j = t; j < 8 * 32; j += kPubThreads) {
+        const int item = j >> 5;
+        if (item % n_eff == split && (item >= 4 || (j & 31) < G)) {
+          if (clear)
+            clear_word(xn + j);
+          else
+            put_word(xn + j, res[j]);
+        }
+      }
+    }
+  }
+}
+
+// The combining split of a (sequence, KV head): log-sum-exp merge of the
 // splits' partials, the sink added once with its shift -(q . k_bar) * scale
-// (Lemma S1; appendix on attention sinks), division by the denominator, and
-// the inverse value transform out = s_hat t_v^T (Corollary 1).  The split's
-// own partial is read from LDS, the other non-empty splits' from the
-// workspace; splits that attend to no token published nothing and are skipped.
+// (Lemma S1; appendix on attention sinks), the new token of a fused step,
+// division by the denominator, and the inverse value transform
+// out = s_hat t_v^T (Corollary 1).  The split's own partial and blocks of the
+// new token are read from LDS, the other splits' from the exchange (every
+// word's tag checked, the words emptied once read); splits that attend to no
+// token published no partial and are skipped.
 template <int WAVES, bool APPEND>
 __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int kv, const int bk,
                                              const size_t row0, const int own_split, const bool own_active,
-                                             const int S, const int lo, const int tend, const float4 (&tv)[8]) {
+                                             const int S, const int lo, const int tend, const int n_eff,
+                                             const float4 (&tv)[8]) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -676,17 +738,19 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
   }
   if (tid < G * kD) {
     const int h = tid >> 7;
-    const size_t r = (row0 + h) * a.n_split;
     const float sk = ctlf[4 + h];
-    // fused step: the new token's block results, requested with the splits' partials
+    bool ok = true;
+    // fused step: the new token's block results, requested with the splits'
+    // partials (blocks of this split from LDS)
     float zp[4] = {0.f, 0.f, 0.f, 0.f}, vp = 0.f;
+    const float *res = reinterpret_cast<const float *>(smem + kItemRes);
+    uint64_t *xn = a.xnew + static_cast<size_t>(bk) * 8 * 32;
+    const int vj = (4 + (d >> 5)) * 32 + (d & 31);
+    uint64_t wz[4], wv;
     if constexpr (APPEND) {
-      if (S > 0) {
-        const float *np = a.newp + static_cast<size_t>(bk) * 8 * 32;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) zp[k] = load_dev(np + k * 32 + h);
-        vp = load_dev(np + (4 + (d >> 5)) * 32 + (d & 31));
-      }
+      for (int k = 0; k < 4; ++k) wz[k] = get_word(xn + k * 32 + h);
+      wv = get_word(xn + vj);
     }
     // online log-sum-exp over the splits, the sink counted once
     float big = sk, num = 0.f, den = sk == -INFINITY ? 0.f : 1.f;
@@ -703,51 +767,112 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
       num = fmaf(w, as, num);
     };
     // splits in index order whichever split combines, so the result does not
-    // depend on the arrival order; the loads of up to 8 splits are issued together
-    for (int s0 = 0; s0 < a.n_split; s0 += 8) {
-      float ms[8], ls[8], as[8];
+    // depend on the arrival order.  The other splits' words are requested four
+    // splits at a time; past the last split the requests repeat its words, so
+    // every request is unconditional and one wait covers the four.
+    uint64_t *xs = a.xch + static_cast<size_t>(bk) * a.n_split * kXchSlotWords;
+    const int n_oth = a.n_split - 1;
+    bool own_done = false;
+    auto take_own = [&]() {
+      if (own_active) take(ctlf[8 + 2 * h], ctlf[8 + 2 * h + 1], own[tid]);
+      own_done = true;
+    };
+    for (int k0 = 0; k0 < n_oth; k0 += 4) {
+      uint64_t wm[4], wl[4], wa[4];
+      int spk[4];
+      bool want[4];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int sp = s0 + i;
-        ms[i] = -INFINITY;
-        ls[i] = 0.f;
-        as[i] = 0.f;
-        const bool nonempty = lo + sp * a.chunk < tend;
-        if (sp == own_split) {
-          if (own_active) {
-            ms[i] = ctlf[8 + 2 * h];
-            ls[i] = ctlf[8 + 2 * h + 1];
-            as[i] = own[tid];
+      for (int i = 0; i < 4; ++i) {
+        const int k = min(k0 + i, n_oth - 1);
+        spk[i] = k + (k >= own_split ? 1 : 0);
+        want[i] = k0 + i < n_oth && lo + spk[i] * a.chunk < tend;
+        const uint64_t *slot = xs + static_cast<size_t>(spk[i]) * kXchSlotWords;
+        wm[i] = get_word(slot + 2 * h);
+        wl[i] = get_word(slot + 2 * h + 1);
+        wa[i] = get_word(slot + 2 * G + tid);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (want[i]) {
+          const uint64_t *slot = xs + static_cast<size_t>(spk[i]) * kXchSlotWords;
+          for (int n = 0; !(word_ready(wm[i]) && word_ready(wl[i]) && word_ready(wa[i])); ++n) {
+            if (n == kSpinLimit) {
+              ok = false;
+              break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+            wm[i] = get_word(slot + 2 * h);
+            wl[i] = get_word(slot + 2 * h + 1);
+            wa[i] = get_word(slot + 2 * G + tid);
           }
-        } else if (sp < a.n_split && nonempty) {
-          ms[i] = load_dev(a.part_ml + 2 * (r + sp));
-          ls[i] = load_dev(a.part_ml + 2 * (r + sp) + 1);
-          as[i] = load_dev(a.part_acc + (r + sp) * kD + d);
         }
       }
 #pragma unroll
-      for (int i = 0; i < 8; ++i) take(ms[i], ls[i], as[i]);
+      for (int i = 0; i < 4; ++i) {
+        if (k0 + i < n_oth) {
+          if (!own_done && spk[i] > own_split) take_own();
+          if (want[i]) take(word_value(wm[i]), word_value(wl[i]), word_value(wa[i]));
+        }
+      }
     }
+    if (!own_done) take_own();
     if constexpr (APPEND) {
-      if (S > 0) take((((zp[0] + zp[1]) + zp[2]) + zp[3]) * kLn2, 1.f, vp);  // the new token, after the splits
+      if (S > 0) {  // the new token, after the splits
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if (k % n_eff == own_split) {
+            zp[k] = res[k * 32 + h];
+          } else {
+            for (int n = 0; !word_ready(wz[k]); ++n) {
+              if (n == kSpinLimit) {
+                ok = false;
+                break;
+              }
+              __builtin_amdgcn_s_sleep(2);
+              wz[k] = get_word(xn + k * 32 + h);
+            }
+            zp[k] = word_value(wz[k]);
+          }
+        }
+        if ((4 + (d >> 5)) % n_eff == own_split) {
+          vp = res[vj];
+        } else {
+          for (int n = 0; !word_ready(wv); ++n) {
+            if (n == kSpinLimit) {
+              ok = false;
+              break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+            wv = get_word(xn + vj);
+          }
+          vp = word_value(wv);
+        }
+        take((((zp[0] + zp[1]) + zp[2]) + zp[3]) * kLn2, 1.f, vp);
+      }
     }
-    shat[tid] = den > 0.f ? num / den : 0.f;
+    // a word that never arrived (not expected) leaves this row NaN
+    shat[tid] = !ok ? __builtin_nanf("") : (den > 0.f ? num / den : 0.f);
   } else if (tid < 4 * kD) {
     shat[tid] = 0.f;
   }
   __syncthreads();
   if (tid < 512) {
-    float o[4] = {0.f, 0.f, 0.f, 0.f};
+    // all eight values of a head are requested before they are used
+    float o[4];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int h = 0; h < 4; ++h) {
+      float4 sv[8];
 #pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        const float4 sv = *reinterpret_cast<const float4 *>(shat + h * kD + 32 * jp + 4 * i);
-        o[h] = fmaf(sv.x, tv[i].x, o[h]);
-        o[h] = fmaf(sv.y, tv[i].y, o[h]);
-        o[h] = fmaf(sv.z, tv[i].z, o[h]);
-        o[h] = fmaf(sv.w, tv[i].w, o[h]);
+      for (int i = 0; i < 8; ++i) sv[i] = *reinterpret_cast<const float4 *>(shat + h * kD + 32 * jp + 4 * i);
+      float x = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        x = fmaf(sv[i].x, tv[i].x, x);
+        x = fmaf(sv[i].y, tv[i].y, x);
+        x = fmaf(sv[i].z, tv[i].z, x);
+        x = fmaf(sv[i].w, tv[i].w, x);
       }
+      o[h] = x;
     }
 #pragma unroll
     for (int h = 0; h < 4; ++h) outp[(jp * 4 + h) * kD + d] = o[h];
@@ -758,14 +883,44 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
     a.out[(row0 + h) * kD + d] =
         (outp[h * kD + d] + outp[(4 + h) * kD + d]) + (outp[(8 + h) * kD + d] + outp[(12 + h) * kD + d]);
   }
+  // Every word read above has been seen with its tag by every thread that
+  // reads it (there were barriers since): empty the other splits' words for
+  // the next call, a word read by several threads by one of them.  These
+  // stores go out last, behind the output's.
+  if (tid < G * kD) {
+    const int h = tid >> 7;
+    uint64_t *xs = a.xch + static_cast<size_t>(bk) * a.n_split * kXchSlotWords;
+    for (int sp = 0; sp < a.n_split; ++sp) {
+      if (sp != own_split && lo + sp * a.chunk < tend) {
+        uint64_t *slot = xs + static_cast<size_t>(sp) * kXchSlotWords;
+        clear_word(slot + 2 * G + tid);
+        if (d == 0) {
+          clear_word(slot + 2 * h);
+          clear_word(slot + 2 * h + 1);
+        }
+      }
+    }
+    if constexpr (APPEND) {
+      if (S > 0) {
+        uint64_t *xn = a.xnew + static_cast<size_t>(bk) * 8 * 32;
+        if (d == 0) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k)
+            if (k % n_eff != own_split) clear_word(xn + k * 32 + h);
+        }
+        if (h == 0 && (4 + (d >> 5)) % n_eff != own_split) clear_word(xn + (4 + (d >> 5)) * 32 + (d & 31));
+      }
+    }
+  }
 }
 
 // One workgroup per (sequence, KV head, split).  Every split publishes its
-// partial to the workspace and counts its arrival; the last one combines.
+// partial to the exchange and counts its arrival; the last one combines.
 // The arrival counters live in the workspace and the last split resets its
 // counter to 0, so a decode step is a single launch.
 template <int WAVES, bool APPEND>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
+  static_assert(WAVES == 12, "the exchange roles assume 12 waves");
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES, APPEND>()];
   const int tid = threadIdx.x;
   // each XCD takes a contiguous range of the logical workgroup order
@@ -786,7 +941,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   const bool active = t0 < t1;
   // Fused step: the splits with pool tokens (at least split 0) share the encode
   // of the new token; such a split runs the setup even with no token of its own.
-  int n_eff = 0;
+  int n_eff = 1;
   bool items = false;
   if (APPEND && S > 0) {
     const int n_act = tend > lo ? (tend - lo + a.chunk - 1) / a.chunk : 0;
@@ -795,62 +950,29 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   }
   const bool run = active || items;
 
-  // Rows of t_v for the combine are requested as soon as the split's token
-  // loop ends, before the arrival is known: their latency hides behind the
-  // wave merge, and the last arrival finds them in registers.
   float4 tv[8];
   if (run) {
     split_pass<WAVES, APPEND>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
   } else {
     load_tv_rows(a, kv, tv);
   }
-  // Arrival: every split publishes its partial (when it has one) and counts
-  // itself in; the split that brings the count to n_split combines.  The
-  // protocol runs in waves 8.. (thread kCtl and the publishing threads), which
-  // hold no loads of t_v: a wave's memory operations complete in issue order,
-  // so a wait there would also wait for t_v.
-  constexpr int kCtl = 512;
   int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
-  __syncthreads();
-  if constexpr (APPEND) {  // this split's blocks of the new token, before its arrival
-    if (items && tid >= kCtl) {
-      const float *res = reinterpret_cast<const float *>(smem + kItemRes);
-      for (int j = tid - kCtl; j < 8 * 32; j += WAVES * 64 - kCtl)
-        if ((j >> 5) % n_eff == split) store_dev(a.newp + static_cast<size_t>(bk) * 8 * 32 + j, res[j]);
-    }
-    if (a.n_split == 1) {
-      if (tid >= kCtl) __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-    }
-  }
+  __syncthreads();  // the split's partial and its blocks of the new token are in LDS
   if (a.n_split > 1) {
-    if (tid >= kCtl) {
-      if (run) {
-        const float *own = reinterpret_cast<const float *>(smem + kAuxOwn);
-        const float *ownml = reinterpret_cast<const float *>(smem + kAuxCtl) + 8;
-        for (int i = tid - kCtl; i < G * kD; i += WAVES * 64 - kCtl) {
-          const int h = i / kD, d = i % kD;
-          const size_t r = (row0 + h) * a.n_split + split;
-          store_dev(a.part_acc + r * kD + d, own[i]);
-          if (d == 0) {
-            store_dev(a.part_ml + 2 * r, ownml[2 * h]);
-            store_dev(a.part_ml + 2 * r + 1, ownml[2 * h + 1]);
-          }
-        }
-      }
-      __builtin_amdgcn_s_waitcnt(0);  // this thread's partial stores have completed
-    }
-    __syncthreads();
     if (tid == kCtl) {
       const int last = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
                        a.n_split - 1;
       if (last) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       ctl[0] = last;
+    } else if (tid >= kPub) {
+      publish<APPEND>(a, smem, bk, split, active, items, n_eff, tid - kPub, false);
     }
     __syncthreads();
     if (ctl[0] == 0) return;
+    // the combining split's own words are emptied by the threads that wrote them
+    if (tid >= kPub) publish<APPEND>(a, smem, bk, split, active, items, n_eff, tid - kPub, true);
   }
-  combine_unit<WAVES, APPEND>(a, smem, kv, bk, row0, split, run, S, lo, tend, tv);
+  combine_unit<WAVES, APPEND>(a, smem, kv, bk, row0, split, run, S, lo, tend, n_eff, tv);
 }
 
 }  // namespace

@@ -60,7 +60,16 @@ struct DecodeArgs {
   const float *t_k;
   uint8_t *k_codes_w, *v_codes_w;  // the pools k_codes / v_codes, written at the new position
   float *newp;      // [B][Hkv][8 items][32] per-block results for the new token
+  // Tagged exchange of the head_dim-128 table kernel (64-bit words, 0 = empty):
+  // split partials [B*Hkv][n_split][kXchSlotWords] and the new token's
+  // per-block results [B*Hkv][8 items][32].
+  uint64_t *xch;
+  uint64_t *xnew;
 };
+
+// Words of one split's slot in the tagged exchange: (m, l) of up to 8 query
+// heads, then their accumulators (8 x 64 or 4 x 128 coordinates).
+constexpr int kXchSlotWords = 16 + 512;
 
 struct EncodeArgs {
   int batch, n_new, num_kv_heads, head_dim;
@@ -79,7 +88,7 @@ struct DecodePlan {
   int use_lut;      // 1: table-based stage 1 (decode_lut.hip), 0: generic stage 1
   int n_split;
   int chunk;
-  size_t off_cnt, off_qp, off_sinkp, off_ml, off_acc, off_new, total;
+  size_t off_cnt, off_qp, off_sinkp, off_ml, off_acc, off_new, off_xch, off_xnew, total;
 };
 // Splits tile each sequence's attended span (the last `window` tokens, or all).
 // The workspace (off_*, total) is sized for every window and both decode

@@ -469,6 +469,45 @@ def test_append_decode_equals_encode_then_decode(nk, shape):
     assert float(err.max()) <= 1e-4
 
 
+def test_shared_workspace_across_shapes(nk, qwen_small):
+    """One workspace serves calls of different shapes and split counts in turn.
+
+    The splits of a (sequence, KV head) exchange tagged words in the workspace
+    and the combining split empties what it read; a word left behind by an
+    earlier call of another shape must never be taken for a partial.  Each
+    call is compared with the same call on a fresh workspace."""
+    wl, params, P = qwen_small
+    H, L, D = wl.num_kv_heads, wl.groups, wl.head_dim
+    cases = [(4, 4096, [4096, 3001, 64, 1], 0), (2, 8192, [8192, 5000], 0), (4, 4096, [4096, 3001, 64, 1], 300),
+             (1, 16384, [16000], 0), (8, 2048, [2048, 2047, 1000, 64, 63, 1, 2, 1500], 0)]
+    inputs = []
+    for B, cap, lens, window in cases:
+        lens = np.array(lens, dtype=np.int32)
+        ck, cv, kn, vn = _step_inputs(wl, B, cap, lens)
+        q = dev(synth.decode_queries(wl, 0, batch=B), torch.bfloat16)
+        inputs.append((B, cap, lens, window, ck, cv, dev(kn, torch.bfloat16), dev(vn, torch.bfloat16), q))
+    need = max(nk.decode_workspace_bytes(P, B, wl.num_q_heads, cap) for B, cap, *_ in inputs)
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    for rep in range(2):
+        for i, (B, cap, lens, window, ck, cv, kn, vn, q) in enumerate(inputs):
+            lay = nk.CacheLayout.contiguous(cap)
+            lens_d = dev(lens, torch.int32)
+            for fused in (False, True):
+                say(f"shared workspace rep={rep} case={i} fused={fused}")
+                outs = []
+                for w in (ws, None):
+                    pk, pv = dev(ck, torch.uint8), dev(cv, torch.uint8)
+                    if fused:
+                        outs.append(nk.append_decode_attn(P, lay, kn, vn, q, pk, pv, lens_d, cap, window=window,
+                                                          workspace=w))
+                    else:
+                        outs.append(nk.decode_attn(P, lay, q, pk, pv, lens_d, cap, window=window, workspace=w))
+                torch.cuda.synchronize()
+                err = (outs[0] - outs[1]).abs().amax(dim=-1) / outs[1].norm(dim=-1).clamp_min(1e-30)
+                assert torch.isfinite(outs[0]).all()
+                assert float(err.max()) <= 1e-4, (rep, i, fused, float(err.max()))
+
+
 # ------------------------------------------------- full-size configurations
 
 def _full_decode(nk, wl, layer, params, units, window=0, batch=None, cap=None):
