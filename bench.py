@@ -35,7 +35,10 @@ HBM_PEAK_GBS = 8000.0
 WORKLOAD = "qwen3_8b"
 COPIES = 6
 DECODE_KERNEL = "decode_lut_d128"
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_04074_amd", "csrc", "decode_lut.hip")
+# The step kernel's source and the headers it includes: a change to any of
+# them invalidates the committed counter summary.
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_04074_amd", "csrc", f)
+                  for f in ("decode_lut.hip", "encode_block.h", "lut_common.h", "nova_kv_internal.h")]
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_lut_d128_qwen3_8b_traffic.md")
 COPY_CALIB_BYTES = 256 << 20
 
@@ -58,8 +61,11 @@ def parse():
 
 
 def kernel_source_sha256() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        with open(path, "rb") as f:
+            h.update(os.path.basename(path).encode() + b"\0" + f.read())
+    return h.hexdigest()
 
 
 def measured_traffic():

@@ -108,6 +108,24 @@ __device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, 
   }
 }
 
+// Exchange between the splits of a (sequence, KV head).  Each split's merge
+// threads publish its partial as tagged words as they form it, and the
+// encoder team publishes the new token's blocks as it computes them, without
+// waiting for the stores to land; thread kCtl, alone in its wave so that no
+// other memory operation of that wave delays its reply (a wave's memory
+// operations complete in issue order), counts the split in while the waves
+// merge.  The split that brings the count to n_split combines: it checks the
+// tag of every word it reads, so no order between the stores and the count
+// is needed.
+//   split slot: (m, l) of head h at words 2h, 2h+1, coordinate d of head h
+//               at 2G + h*128 + d;
+//   new token:  item k (side * 4 + block), lane j at word 32k + j, key
+//               blocks for lanes j < G (the heads), value blocks for all 32.
+constexpr int kCtl = 512;
+// Bound of the wait for a word whose writer has already counted itself in:
+// it only has to complete a store, so the bound is never reached in practice.
+constexpr int kSpinLimit = 1 << 20;
+
 // Fused step: this split's share of the new token's encode.  Item i =
 // side * 4 + block (blocks of 8 groups) is done by split i mod n_eff.  Waves
 // 8..11 (the encoder team, 256 threads) take this split's items one after the
@@ -195,6 +213,7 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
                                                                    8 * (g >> 3) + 2 * (t & 3)));
       }
       res[item * 32 + t] = v;
+      if (a.n_split > 1 && (side == 1 || t < G)) put_word(a.xnew + static_cast<size_t>(b * a.num_kv_heads + kv) * 8 * 32 + item * 32 + t, v);
     }
     team_sync(smem, ++phase);  // the scratch is reused by the next item
   }
@@ -228,10 +247,13 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
   for (int X = 0; X < 8; ++X) acc[X] = float4_t{0.f, 0.f, 0.f, 0.f};
 
+  // A split with no token of its own (t1 == t0) runs the setup and an empty
+  // loop: its round requests read row 0 of physical block 0, which every
+  // pool has, instead of positions of its sequence.
+  const bool act = t1 > t0;
   const int R0 = t0 & ~63;
-  const int nrounds = (t1 - R0 + 63) >> 6;
-  // (a fused step's split that only encodes has t1 = t0: its position clamps stay in the sequence)
-  const int last16 = APPEND ? max(0, (t1 - 1) & ~15) : (t1 - 1) & ~15;
+  const int nrounds = act ? (t1 - R0 + 63) >> 6 : 0;
+  const int last16 = max(0, (t1 - 1) & ~15);
   const uint8_t *kpool = a.k_codes;
   const uint8_t *vpool = a.v_codes;
 
@@ -244,7 +266,8 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   auto load_round = [&](int R, uint2 *kw, uint2 *vw) {
     size_t sub[4];  // uniform: byte offsets of the round's four sub-tiles
 #pragma unroll
-    for (int r = 0; r < 4; ++r) sub[r] = subtile_offset(a, b, kv, min(R + 16 * r, last16), bs_shift);
+    for (int r = 0; r < 4; ++r)
+      sub[r] = act ? subtile_offset(a, b, kv, min(R + 16 * r, last16), bs_shift) : static_cast<size_t>(kv) * bsz * kL;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const uint8_t *kb = kpool + sub[r];
@@ -613,9 +636,22 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   }
   __syncthreads();
 
-  // ---- merge the waves into this split's partial (natural-log max), kept in LDS
+  // ---- arrival (see the exchange below): counted now, while the waves merge
+  const int bk = b * a.num_kv_heads + kv;
+  if (a.n_split > 1 && tid == kCtl) {
+    int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
+    const int last = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                     a.n_split - 1;
+    if (last) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    ctl[0] = last;
+  }
+
+  // ---- merge the waves into this split's partial (natural-log max), kept in
+  // LDS and published to the exchange by the threads that form it
   float *own = reinterpret_cast<float *>(smem + kAuxOwn);
   float *ownml = reinterpret_cast<float *>(smem + kAuxCtl) + 8;
+  const bool pub = a.n_split > 1 && act;
+  uint64_t *slot = a.xch + (static_cast<size_t>(bk) * a.n_split + split) * kXchSlotWords;
   for (int i = tid; i < G * kD; i += WAVES * 64) {
     const int h = i / kD, d = i % kD;
     // all of this thread's reads first, then the arithmetic
@@ -639,59 +675,16 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       }
     }
     own[i] = num;
+    const float mlog = big == -INFINITY ? -INFINITY : big * kLn2;
     if (d == 0) {
-      ownml[2 * h] = big == -INFINITY ? -INFINITY : big * kLn2;
+      ownml[2 * h] = mlog;
       ownml[2 * h + 1] = den;
     }
-  }
-}
-
-// Exchange between the splits of a (sequence, KV head).  Thread kCtl, alone
-// in its wave so that no other memory operation of that wave delays its reply
-// (a wave's memory operations complete in issue order), counts the split in;
-// waves kPub.. publish the split's partial and its blocks of the new token as
-// tagged words and do not wait for them to land.  The split that brings the
-// count to n_split combines: it checks the tag of every word it reads, so no
-// order between the stores and the count is needed.
-constexpr int kCtl = 512;
-constexpr int kPub = 576;
-constexpr int kPubThreads = 12 * 64 - kPub;
-// Bound of the wait for a word whose writer has already counted itself in:
-// it only has to complete a store, so the bound is never reached in practice.
-constexpr int kSpinLimit = 1 << 20;
-
-// Slot words: (m, l) of head h at 2h, 2h+1; coordinate d of head h at
-// 2G + h*128 + d.  New token: item k (side * 4 + block) lane j at 32k + j,
-// key blocks for lanes j < G (the heads), value blocks for all 32 lanes.
-// With clear set, the same threads empty the same words, in the same order.
-template <bool APPEND>
-__device__ __forceinline__ void publish(const DecodeArgs &a, uint8_t *smem, const int bk, const int split,
-                                        const bool partial, const bool items, const int n_eff, const int t,
-                                        const bool clear) {
-  const int G = a.gqa;
-  if (partial) {
-    uint64_t *slot = a.xch + (static_cast<size_t>(bk) * a.n_split + split) * kXchSlotWords;
-    const float *own = reinterpret_cast<const float *>(smem + kAuxOwn);
-    const float *ownml = reinterpret_cast<const float *>(smem + kAuxCtl) + 8;
-    for (int j = t; j < 2 * G + G * kD; j += kPubThreads) {
-      if (clear)
-        clear_word(slot + j);
-      else
-        put_word(slot + j, j < 2 * G ? ownml[j] : own[j - 2 * G]);
-    }
-  }
-  if constexpr (APPEND) {
-    if (items) {
-      const float *res = reinterpret_cast<const float *>(smem + kItemRes);
-      uint64_t *xn = a.xnew + static_cast<size_t>(bk) * 8 * 32;
-      for (int j = t; j < 8 * 32; j += kPubThreads) {
-        const int item = j >> 5;
-        if (item % n_eff == split && (item >= 4 || (j & 31) < G)) {
-          if (clear)
-            clear_word(xn + j);
-          else
-            put_word(xn + j, res[j]);
-        }
+    if (pub) {
+      put_word(slot + 2 * G + i, num);
+      if (d == 0) {
+        put_word(slot + 2 * h, mlog);
+        put_word(slot + 2 * h + 1, den);
       }
     }
   }
@@ -707,35 +700,15 @@ __device__ __forceinline__ void publish(const DecodeArgs &a, uint8_t *smem, cons
 // token published no partial and are skipped.
 template <int WAVES, bool APPEND>
 __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int kv, const int bk,
-                                             const size_t row0, const int own_split, const bool own_active,
-                                             const int S, const int lo, const int tend, const int n_eff,
-                                             const float4 (&tv)[8]) {
+                                             const size_t row0, const int own_split, const int S, const int lo,
+                                             const int tend, const int n_eff, const float4 (&tv)[8]) {
   const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = a.gqa;
   float *shat = reinterpret_cast<float *>(smem + kAuxQ);    // [4][128]
   float *outp = reinterpret_cast<float *>(smem + kAuxOut);  // [part][head][128]
   float *ctlf = reinterpret_cast<float *>(smem + kAuxCtl);
   const float *own = reinterpret_cast<const float *>(smem + kAuxOwn);
   const int d = tid & (kD - 1), jp = tid >> 7;  // tv holds row d of t_v, columns 32*jp .. 32*jp+31
-  if (!own_active) {  // the setup did not run: form the shifted sink logits here
-    if (wave < G) {
-      const size_t qi = (row0 + wave) * kD + 2 * lane;
-      float q0, q1;
-      if (a.q_bf16) {
-        q0 = bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi]);
-        q1 = bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi + 1]);
-      } else {
-        q0 = static_cast<const float *>(a.q)[qi];
-        q1 = static_cast<const float *>(a.q)[qi + 1];
-      }
-      const float *kb = a.kbar + static_cast<size_t>(kv) * kD + 2 * lane;
-      const float dot = wave_sum(fmaf(q0, kb[0], q1 * kb[1]));
-      if (lane == 0) ctlf[4 + wave] = a.sinks ? a.sinks[kv * G + wave] - a.scale * dot : -INFINITY;
-    }
-    __syncthreads();
-  }
   if (tid < G * kD) {
     const int h = tid >> 7;
     const float sk = ctlf[4 + h];
@@ -774,7 +747,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
     const int n_oth = a.n_split - 1;
     bool own_done = false;
     auto take_own = [&]() {
-      if (own_active) take(ctlf[8 + 2 * h], ctlf[8 + 2 * h + 1], own[tid]);
+      take(ctlf[8 + 2 * h], ctlf[8 + 2 * h + 1], own[tid]);
       own_done = true;
     };
     for (int k0 = 0; k0 < n_oth; k0 += 4) {
@@ -948,31 +921,31 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
     n_eff = max(n_act, 1);
     items = split < n_eff;
   }
-  const bool run = active || items;
 
   float4 tv[8];
-  if (run) {
-    split_pass<WAVES, APPEND>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
-  } else {
-    load_tv_rows(a, kv, tv);
-  }
+  split_pass<WAVES, APPEND>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
   int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
-  __syncthreads();  // the split's partial and its blocks of the new token are in LDS
+  __syncthreads();  // the split's partial and its blocks of the new token are in LDS; the count is known
   if (a.n_split > 1) {
-    if (tid == kCtl) {
-      const int last = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-                       a.n_split - 1;
-      if (last) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      ctl[0] = last;
-    } else if (tid >= kPub) {
-      publish<APPEND>(a, smem, bk, split, active, items, n_eff, tid - kPub, false);
-    }
-    __syncthreads();
     if (ctl[0] == 0) return;
     // the combining split's own words are emptied by the threads that wrote them
-    if (tid >= kPub) publish<APPEND>(a, smem, bk, split, active, items, n_eff, tid - kPub, true);
+    if (active && tid < G * kD) {
+      uint64_t *slot = a.xch + (static_cast<size_t>(bk) * a.n_split + split) * kXchSlotWords;
+      clear_word(slot + 2 * G + tid);
+      if ((tid & (kD - 1)) == 0) {
+        clear_word(slot + 2 * (tid >> 7));
+        clear_word(slot + 2 * (tid >> 7) + 1);
+      }
+    }
+    if constexpr (APPEND) {
+      const int t = tid - 512;
+      if (items && t >= 0 && t < 32) {
+        for (int item = split; item < 8; item += n_eff)
+          if (item >= 4 || t < G) clear_word(a.xnew + static_cast<size_t>(bk) * 8 * 32 + item * 32 + t);
+      }
+    }
   }
-  combine_unit<WAVES, APPEND>(a, smem, kv, bk, row0, split, run, S, lo, tend, n_eff, tv);
+  combine_unit<WAVES, APPEND>(a, smem, kv, bk, row0, split, S, lo, tend, n_eff, tv);
 }
 
 }  // namespace

@@ -539,7 +539,6 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
   // each XCD takes a contiguous range of the logical workgroup order
   int kv, b, split;
   unit_of_workgroup(xcd_contiguous(blockIdx.x, gridDim.x), a.n_split, a.b_chunk, a.num_kv_heads, kv, b, split);
-  const int rest = b * a.n_split + split;  // distinct among the workgroups of a KV head
   const int bk = b * a.num_kv_heads + kv;
   const int G = a.gqa;
 
