@@ -40,7 +40,6 @@ constexpr int kD = 128;
 constexpr int kL = kD / kGroupDim;          // 32 groups
 constexpr uint32_t kLutBytes = 65536;       // [256 codes][32 groups][4 heads] fp16
 constexpr uint32_t kVBase = kLutBytes;      // value codebook, 64 KB
-constexpr uint32_t kMergeBase = 0;          // per-wave merge scratch, reuses the table once done
 // Per-wave merge scratch: [0..4) m, [4..8) l, then coordinate d of head h at
 // 8 + h * kMergeHead + (d / 32) * kMergeBlk + d % 32.  With this padding the 16
 // lanes that store a wave's accumulators (one 16-byte store per lane) hit 16
@@ -48,34 +47,36 @@ constexpr uint32_t kMergeBase = 0;          // per-wave merge scratch, reuses th
 constexpr int kMergeHead = 144, kMergeBlk = 36;
 constexpr int kMergeFloats = 8 + 3 * kMergeHead + 3 * kMergeBlk + 32 + 4;
 constexpr float kLazyLog2 = 8.f;  // reference lag allowed in the online softmax (log2 units)
-// Auxiliary region: query staging and the partial sums of q', later the
-// combine's merged accumulator and partial outputs, and a few control words.
-constexpr uint32_t kAuxQ = 2 * 65536;               // [4][128] f32
-constexpr uint32_t kAuxPart = kAuxQ + 4 * kD * 4;   // [8 parts][4 heads][128] f32
-constexpr uint32_t kAuxCtl = kAuxPart + 32 * kD * 4;
-// After the setup the partial-sum area holds the split's own merged partial
-// ([4][128] accumulator at kAuxOwn) and the combine's partial outputs.
-constexpr uint32_t kAuxOwn = kAuxPart;
-constexpr uint32_t kAuxOut = kAuxPart + 4 * kD * 4;
+// Auxiliary region: query staging (later the combine's s_hat), control words,
+// and the fused step's encoder-team counter and per-block results.
+constexpr uint32_t kAuxQ = 2 * 65536;              // [4][128] f32
+constexpr uint32_t kAuxCtl = kAuxQ + 4 * kD * 4;
 // control words: [0] arrival state, [1] next unclaimed round, [4..8) shifted
 // sink logits, [8..16) own (m, l) per head
-constexpr uint32_t kLdsBytes = kAuxCtl + 64;
-// Fused step only, after the decode's own LDS: three encoder teams' scratch
-// and the new token's per-block results [8 items][32] f32.
-constexpr uint32_t kAppendScratch = kLdsBytes;
-constexpr uint32_t kItemRes = kAppendScratch + 3 * sizeof(encblk::Scratch<kD>);
-constexpr uint32_t kTeamCtr = kItemRes + 8 * 32 * 4;  // arrivals of the encoder team's waves
-constexpr uint32_t kLdsBytesAppend = kTeamCtr + 16;
-static_assert(kLdsBytes % 16 == 0 && kLdsBytesAppend <= 160 * 1024, "LDS budget of a workgroup");
+constexpr uint32_t kTeamCtr = kAuxCtl + 64;        // arrivals of the encoder team's waves
+constexpr uint32_t kItemRes = kTeamCtr + 16;       // [8 items][32] f32
+// A region used in turn by the partial sums of q' (setup, [8 parts][4 heads]
+// [128] f32), the encoder team's scratch (fused step, early in the loop) and
+// the per-wave merge scratch (written by each wave as its loop ends, while
+// other waves still read both tables).
+constexpr uint32_t kMergeBase = (kItemRes + 8 * 32 * 4 + 255) & ~255u;
+constexpr uint32_t kAuxPart = kMergeBase;
+constexpr uint32_t kAppendScratch = kMergeBase;
+constexpr uint32_t kLdsBytes = kMergeBase + 12 * kMergeFloats * 4;
+// Once every wave has left the loop, the value-codebook region holds the
+// split's own merged partial ([4][128] at kAuxOwn) and the combine's partial
+// outputs.
+constexpr uint32_t kAuxOwn = kVBase;
+constexpr uint32_t kAuxOut = kVBase + 4 * kD * 4;
+static_assert(32 * kD * 4 <= 12 * kMergeFloats * 4 && sizeof(encblk::Scratch<kD>) <= 12 * kMergeFloats * 4,
+              "the q' partial sums and the encoder scratch fit in the merge region");
+static_assert(kLdsBytes <= 160 * 1024, "LDS budget of a workgroup");
 constexpr float kLn2 = 0.693147180559945309f;
 
 template <int WAVES, bool APPEND>
 constexpr uint32_t lds_bytes() {
-  static_assert(WAVES * kMergeFloats * 4 <= kLutBytes, "merge scratch must fit in the table region");
-  static_assert(WAVES >= kL / 4, "one wave per group block builds the table");
-  static_assert(WAVES * 64 >= 512, "512 threads form q' and apply t_v");
-  static_assert(WAVES >= 12, "waves 8..11 form the shifted sink logits");
-  return APPEND ? kLdsBytesAppend : kLdsBytes;
+  static_assert(WAVES == 12, "the merge region holds 12 waves' scratch; waves 8..11 form the sink logits");
+  return kLdsBytes;
 }
 
 
@@ -621,7 +622,15 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   // still in the loop and the merge, and the last arrival finds them in
   // registers.
   load_tv_rows(a, kv, tv);
-  __syncthreads();  // every wave is done with the table before it becomes merge scratch
+  if constexpr (APPEND) {
+    // the merge region holds the encoder team's scratch until its last item
+    if (n_eff > 0 && wave < 8) {
+      const int done = 4 * 5 * items_of_split(split, n_eff);  // five team_sync phases per item
+      int *ctr = reinterpret_cast<int *>(smem + kTeamCtr);
+      while (__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < done)
+        __builtin_amdgcn_s_sleep(1);
+    }
+  }
   float *merge = reinterpret_cast<float *>(smem + kMergeBase);
   float *mw = merge + wave * kMergeFloats;
   if (lane < 4) {
