@@ -68,7 +68,7 @@ constexpr uint32_t kLdsBytes = kMergeBase + 12 * kMergeFloats * 4;
 // outputs.
 constexpr uint32_t kAuxOwn = kVBase;
 constexpr uint32_t kAuxOut = kVBase + 4 * kD * 4;
-static_assert(32 * kD * 4 <= 12 * kMergeFloats * 4 && sizeof(encblk::Scratch<kD>) <= 12 * kMergeFloats * 4,
+static_assert(32 * kD * 4 <= 12 * kMergeFloats * 4 && 2 * sizeof(encblk::Scratch<kD>) <= 12 * kMergeFloats * 4,
               "the q' partial sums and the encoder scratch fit in the merge region");
 static_assert(kLdsBytes <= 160 * 1024, "LDS budget of a workgroup");
 constexpr float kLn2 = 0.693147180559945309f;
@@ -158,13 +158,13 @@ struct ItemRegs {
   double x;  // thread t < D: element t of the token minus k_bar (keys) or of the token (values)
 };
 
-__device__ __forceinline__ void load_item(const DecodeArgs &a, const int b, const int kv, const int split,
-                                          const int n_eff, const int k, const int t, ItemRegs &r) {
+// The transform columns and the token element of the item (its rows).
+__device__ __forceinline__ void load_item_rows(const DecodeArgs &a, const int b, const int kv, const int split,
+                                               const int n_eff, const int k, const int t, ItemRegs &r) {
   const int item = split + k * n_eff;
   const int side = item >> 2, blk = item & 3;
   const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * kD * kD;
-  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * kL * 256 * 4;
-  encblk::load_block<kD>(t, tm, cbg, blk, r.trow, r.cw);
+  encblk::load_rows<kD>(t, tm, blk, r.trow);
   if (t < kD) {
     const void *src = side == 0 ? a.k_new : a.v_new;
     const size_t idx = (static_cast<size_t>(b) * a.num_kv_heads + kv) * kD + t;
@@ -175,48 +175,95 @@ __device__ __forceinline__ void load_item(const DecodeArgs &a, const int b, cons
   }
 }
 
+// The codewords of the item's 8 groups.
+__device__ __forceinline__ void load_item_cw(const DecodeArgs &a, const int kv, const int split, const int n_eff,
+                                             const int k, const int t, ItemRegs &r) {
+  const int item = split + k * n_eff;
+  const int side = item >> 2, blk = item & 3;
+  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * kL * 256 * 4;
+  encblk::load_codewords(t, cbg, blk, r.cw);
+}
+
+__device__ __forceinline__ void load_item(const DecodeArgs &a, const int b, const int kv, const int split,
+                                          const int n_eff, const int k, const int t, ItemRegs &r) {
+  load_item_rows(a, b, kv, split, n_eff, k, t, r);
+  load_item_cw(a, kv, split, n_eff, k, t, r);
+}
+
+// Team meetings of the encode: two per item (its x in LDS, then the wave
+// partials) and one after the last item, before the key blocks' head sums.
+__device__ __forceinline__ int team_phases(const int split, const int n_eff) {
+  return 2 * items_of_split(split, n_eff) + 1;
+}
+
 // Called by the team's threads only (t = tid - 512); r holds item 0's loads.
+// Items alternate between two scratch areas, so no meeting guards their
+// reuse.  The next item's rows are requested when an item starts, its
+// codewords (needed two meetings into it) when it starts itself.  The
+// thread that found a group's codeword records its per-group result: a key
+// block's partial logits of the 8 groups per head (table entries of the
+// stored codes, res[32 k + 4 gg + h]), a value block's coordinates
+// (res[32 k + 4 gg + i]).  After the last item thread h < G of the team sums
+// each key block's head h over the groups in order, into res[32 k + h].
 __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                              const int split, const int n_eff, const size_t tokoff, const int t,
                                              ItemRegs &r) {
-  encblk::Scratch<kD> *sc = reinterpret_cast<encblk::Scratch<kD> *>(smem + kAppendScratch);
+  encblk::Scratch<kD> *sc = reinterpret_cast<encblk::Scratch<kD> *>(smem + kAppendScratch);  // [2]
   float *res = reinterpret_cast<float *>(smem + kItemRes);
+  uint64_t *xn = a.xnew + static_cast<size_t>(b * a.num_kv_heads + kv) * 8 * 32;
   const int G = a.gqa;
   const int nmine = items_of_split(split, n_eff);
   int phase = 0;
-  for (int k = 0; k < nmine; ++k) {
+  auto encode_one = [&](const int k, const ItemRegs &ri) {
     const int item = split + k * n_eff;
     const int side = item >> 2, blk = item & 3;
-    if (k > 0) load_item(a, b, kv, split, n_eff, k, t, r);
-    if (t < kD) sc->xs[t] = r.x;
+    encblk::Scratch<kD> &s = sc[k & 1];
+    if (t < kD) s.xs[t] = ri.x;
     team_sync(smem, ++phase);
-    encblk::partial_block<kD>(t, *sc, r.trow);
+    encblk::partial_block<kD>(t, s, ri.trow);
     team_sync(smem, ++phase);
-    encblk::sum_block<kD>(t, *sc);
-    team_sync(smem, ++phase);
-    const int code = encblk::search_block<kD>(t, *sc, r.cw);
-    if ((t & 31) == 0)
-      (side == 0 ? a.k_codes_w : a.v_codes_w)[tokoff + encblk::kGroups * blk + (t >> 5)] = static_cast<uint8_t>(code);
-    team_sync(smem, ++phase);
-    if (t < 32) {
-      float v = 0.f;
+    const int code = encblk::search_block<kD>(t, s, ri.cw);
+    const int gl = t >> 5, lr = t & 31;
+    const int g = encblk::kGroups * blk + gl;
+    if (lr == 0) (side == 0 ? a.k_codes_w : a.v_codes_w)[tokoff + g] = static_cast<uint8_t>(code);
+    if (lr < 4) {
+      float v;
       if (side == 0) {
-        if (t < G) {
-#pragma unroll
-          for (int gg = 0; gg < encblk::kGroups; ++gg) {
-            const int g = encblk::kGroups * blk + gg, c = sc->codes[gg];
-            v += static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + c * 256 + g * 8 + 2 * t));
-          }
-        }
+        v = lr < G ? static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + code * 256 + g * 8 + 2 * lr)) : 0.f;
       } else {
-        const int g = encblk::kGroups * blk + (t >> 2), c = sc->codes[t >> 2];
-        v = static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + kVBase + (g & 7) * 8192 + 32 * c +
-                                                                   8 * (g >> 3) + 2 * (t & 3)));
+        v = static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + kVBase + (g & 7) * 8192 + 32 * code +
+                                                                   8 * (g >> 3) + 2 * lr));
+        if (a.n_split > 1) put_word(xn + item * 32 + 4 * gl + lr, v);
       }
-      res[item * 32 + t] = v;
-      if (a.n_split > 1 && (side == 1 || t < G)) put_word(a.xnew + static_cast<size_t>(b * a.num_kv_heads + kv) * 8 * 32 + item * 32 + t, v);
+      res[item * 32 + 4 * gl + lr] = v;
     }
-    team_sync(smem, ++phase);  // the scratch is reused by the next item
+  };
+#ifdef ITEM_PREFETCH
+  ItemRegs r2;
+  for (int k = 0; k < nmine; k += 2) {
+    if (k + 1 < nmine) load_item_rows(a, b, kv, split, n_eff, k + 1, t, r2);
+    encode_one(k, r);
+    if (k + 1 >= nmine) break;
+    load_item_cw(a, kv, split, n_eff, k + 1, t, r2);
+    if (k + 2 < nmine) load_item_rows(a, b, kv, split, n_eff, k + 2, t, r);
+    encode_one(k + 1, r2);
+    if (k + 2 < nmine) load_item_cw(a, kv, split, n_eff, k + 2, t, r);
+  }
+#else
+  for (int k = 0; k < nmine; ++k) {
+    if (k > 0) load_item(a, b, kv, split, n_eff, k, t, r);
+    encode_one(k, r);
+  }
+#endif
+  team_sync(smem, ++phase);
+  if (t < G) {
+    for (int item = split; item < 4; item += n_eff) {
+      float v = 0.f;
+#pragma unroll
+      for (int gg = 0; gg < encblk::kGroups; ++gg) v += res[item * 32 + 4 * gg + t];
+      res[item * 32 + t] = v;
+      if (a.n_split > 1) put_word(xn + item * 32 + t, v);
+    }
   }
 }
 
@@ -625,7 +672,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   if constexpr (APPEND) {
     // the merge region holds the encoder team's scratch until its last item
     if (n_eff > 0 && wave < 8) {
-      const int done = 4 * 5 * items_of_split(split, n_eff);  // five team_sync phases per item
+      const int done = 4 * team_phases(split, n_eff);
       int *ctr = reinterpret_cast<int *>(smem + kTeamCtr);
       while (__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < done)
         __builtin_amdgcn_s_sleep(1);
@@ -947,10 +994,15 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
       }
     }
     if constexpr (APPEND) {
+      // the same team threads as in encode_items: value words by the thread
+      // that found the group, key words by head thread t < G
       const int t = tid - 512;
-      if (items && t >= 0 && t < 32) {
-        for (int item = split; item < 8; item += n_eff)
-          if (item >= 4 || t < G) clear_word(a.xnew + static_cast<size_t>(bk) * 8 * 32 + item * 32 + t);
+      if (items && t >= 0) {
+        uint64_t *xn = a.xnew + static_cast<size_t>(bk) * 8 * 32;
+        for (int item = split; item < 8; item += n_eff) {
+          if (item >= 4 && (t & 31) < 4) clear_word(xn + item * 32 + 4 * (t >> 5) + (t & 31));
+          if (item < 4 && t < G) clear_word(xn + item * 32 + t);
+        }
       }
     }
   }

@@ -49,8 +49,6 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   __syncthreads();
   encblk::partial_block<D>(tid, sc, trow);
   __syncthreads();
-  encblk::sum_block<D>(tid, sc);
-  __syncthreads();
   const int code = encblk::search_block<D>(tid, sc, cw);
   if ((tid & 31) == 0) {
     const int pos = a.start_pos[b] + a.start_offset + t;

@@ -14,7 +14,8 @@
 // (gl, r) = (t >> 5, t & 31) scans codewords r + 32 k of group gl.
 // Column sums are fixed in order: an fp64 fma chain over a thread's rows,
 // then a butterfly over the 8 row groups of a wave (lanes 8, 16, 32 apart,
-// the value of lane c4 kept), then the 4 waves' partials added in order.
+// the value of lane c4 kept), then the 4 waves' partials added in order by
+// each searching thread.
 #pragma once
 
 #include "nova_kv_internal.h"
@@ -27,31 +28,35 @@ constexpr int kGroups = 8;                        // groups per block
 constexpr int kCols = kGroups * kGroupDim;        // 32 coordinates
 constexpr int kPer = kCodebookSize / 32;          // codewords per search lane
 
-// LDS of one team: x [D] doubles, wave partials [4][32] doubles, sums [32]
-// doubles, the 8 codes of the block.
+// LDS of one team: x [D] doubles, wave partials [4][32] doubles.
 template <int D>
 struct Scratch {
   double xs[D];
   double wpart[4][kCols];
-  double us[kCols];
-  int codes[kGroups];
 };
 
 // Phase 1 (issue only): the block's transform columns and codewords.
 //   tm  = side transform of the KV head ([D][D] fp32, row-major)
 //   cbg = side codebooks of the KV head ([L][256][4] fp16)
 template <int D>
-__device__ __forceinline__ void load_block(const int t, const float *tm, const uint16_t *cbg, const int blk,
-                                           float4 (&trow)[D / 32], uint2 (&cw)[kPer]) {
+__device__ __forceinline__ void load_rows(const int t, const float *tm, const int blk, float4 (&trow)[D / 32]) {
   constexpr int RPT = D / 32;
   const int rg = t >> 3, c4 = t & 7;
   const float *col = tm + kCols * blk + 4 * c4;
 #pragma unroll
   for (int j = 0; j < RPT; ++j) trow[j] = *reinterpret_cast<const float4 *>(col + (RPT * rg + j) * D);
+}
+__device__ __forceinline__ void load_codewords(const int t, const uint16_t *cbg, const int blk, uint2 (&cw)[kPer]) {
   const int gl = t >> 5, r = t & 31;
   const uint2 *row = reinterpret_cast<const uint2 *>(cbg) + (kGroups * blk + gl) * kCodebookSize;
 #pragma unroll
   for (int k = 0; k < kPer; ++k) cw[k] = row[r + 32 * k];
+}
+template <int D>
+__device__ __forceinline__ void load_block(const int t, const float *tm, const uint16_t *cbg, const int blk,
+                                           float4 (&trow)[D / 32], uint2 (&cw)[kPer]) {
+  load_rows<D>(t, tm, blk, trow);
+  load_codewords(t, cbg, blk, cw);
 }
 
 // Phase 2 (after x is in LDS): this wave's share of the 32 coefficients.
@@ -82,18 +87,19 @@ __device__ __forceinline__ void partial_block(const int t, Scratch<D> &s, const 
   }
 }
 
-// Phase 3 (after the partials are in LDS): coefficient sums.
+// Phase 3 (after the partials are in LDS): nearest codeword of group t >> 5,
+// returned in all 32 lanes of the group.  The group's four coefficients are
+// the sums of the 4 waves' partials, added in wave order.
 template <int D>
-__device__ __forceinline__ void sum_block(const int t, Scratch<D> &s) {
-  if (t < kCols) s.us[t] = ((s.wpart[0][t] + s.wpart[1][t]) + s.wpart[2][t]) + s.wpart[3][t];
-}
-
-// Phase 4 (after the sums are in LDS): nearest codeword of group t >> 5; the
-// result is valid in lane (t & 31) == 0 and is also left in s.codes.
-template <int D>
-__device__ __forceinline__ int search_block(const int t, Scratch<D> &s, const uint2 (&cw)[kPer]) {
+__device__ __forceinline__ int search_block(const int t, const Scratch<D> &s, const uint2 (&cw)[kPer]) {
   const int gl = t >> 5, r = t & 31;
-  const double u0 = s.us[gl * 4 + 0], u1 = s.us[gl * 4 + 1], u2 = s.us[gl * 4 + 2], u3 = s.us[gl * 4 + 3];
+  double uu[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = gl * 4 + i;
+    uu[i] = ((s.wpart[0][c] + s.wpart[1][c]) + s.wpart[2][c]) + s.wpart[3][c];
+  }
+  const double u0 = uu[0], u1 = uu[1], u2 = uu[2], u3 = uu[3];
   double best = INFINITY;
   int arg = 0;
 #pragma unroll
@@ -123,7 +129,6 @@ __device__ __forceinline__ int search_block(const int t, Scratch<D> &s, const ui
       arg = oa;
     }
   }
-  if (r == 0) s.codes[gl] = arg;
   return arg;
 }
 
