@@ -15,6 +15,11 @@ With stored t_k_inv_t = R_K^{-T}, R_K^{-1} = t_k_inv_t^T.
 Readings: the window W attends to the last W cached tokens [S - W, S); a
 sequence with no attended token and no sink yields a zero output.
 
+Key-scale format (Algorithm 2's normalization, the read path's per-token
+scale): the reconstructed key is k_hat = rho * Q(r/rho) R_K^{-1} + k_bar with
+the stored (bf16) rho, so the logit of a token is rho times the logit of its
+normalized code.
+
 Fast form -- for self-consistency only (Algorithm 1 inference step; Sec.
 "Decoding kernel and read path"; sinks appendix): q' = q R_K^{-T} * scale,
 logit = q' . r_hat (k_bar dropped, Lemma S1), sink shifted by -(q . k_bar) * scale,
@@ -37,9 +42,12 @@ def attended_range(seq_len: int, window: int):
 
 
 def reconstruct_keys(codes_k: np.ndarray, cb_k: np.ndarray, t_k_inv_t: np.ndarray,
-                     kbar: np.ndarray) -> np.ndarray:
-    """k_hat = Q(r) R_K^{-1} + k_bar for every row of codes (n, L)."""
+                     kbar: np.ndarray, scales: Optional[np.ndarray] = None) -> np.ndarray:
+    """k_hat = Q(r) R_K^{-1} + k_bar for every row of codes (n, L); with per-token
+    scales (n,) (key-scale format) k_hat = rho * Q(r/rho) R_K^{-1} + k_bar."""
     r_hat = lookup(codes_k, cb_k)
+    if scales is not None:
+        r_hat = r_hat * np.asarray(scales, dtype=np.float64)[:, None]
     return r_hat @ np.asarray(t_k_inv_t, dtype=np.float64).T + np.asarray(kbar, dtype=np.float64)
 
 
@@ -66,22 +74,25 @@ def softmax_attention(q: np.ndarray, keys: np.ndarray, values: np.ndarray, scale
 
 
 def decode_row(q: np.ndarray, codes_k: np.ndarray, codes_v: np.ndarray, params_head: dict,
-               scale: float, window: int = 0, sink: Optional[float] = None) -> np.ndarray:
-    """Plain-form output of one query head over one sequence's cached codes (S, L)."""
+               scale: float, window: int = 0, sink: Optional[float] = None,
+               scales_k: Optional[np.ndarray] = None) -> np.ndarray:
+    """Plain-form output of one query head over one sequence's cached codes (S, L);
+    scales_k (S,) are the stored per-token key scales of the key-scale format."""
     lo, hi = attended_range(codes_k.shape[0], window)
     k_hat = reconstruct_keys(codes_k[lo:hi], params_head["cb_k"], params_head["t_k_inv_t"],
-                             params_head["kbar"])
+                             params_head["kbar"], None if scales_k is None else scales_k[lo:hi])
     v_hat = reconstruct_values(codes_v[lo:hi], params_head["cb_v"], params_head["t_v"])
     return softmax_attention(q, k_hat, v_hat, scale, sink)
 
 
 def decode_rows(q_heads: np.ndarray, codes_k: np.ndarray, codes_v: np.ndarray,
                 params_head: dict, scale: float, window: int = 0,
-                sinks: Optional[Sequence[float]] = None) -> np.ndarray:
+                sinks: Optional[Sequence[float]] = None,
+                scales_k: Optional[np.ndarray] = None) -> np.ndarray:
     """Plain-form outputs of the G query heads sharing one KV head: q_heads (G, D) -> (G, D)."""
     lo, hi = attended_range(codes_k.shape[0], window)
     k_hat = reconstruct_keys(codes_k[lo:hi], params_head["cb_k"], params_head["t_k_inv_t"],
-                             params_head["kbar"])
+                             params_head["kbar"], None if scales_k is None else scales_k[lo:hi])
     v_hat = reconstruct_values(codes_v[lo:hi], params_head["cb_v"], params_head["t_v"])
     out = np.empty((q_heads.shape[0], v_hat.shape[1]))
     for h in range(q_heads.shape[0]):
@@ -92,7 +103,7 @@ def decode_rows(q_heads: np.ndarray, codes_k: np.ndarray, codes_v: np.ndarray,
 
 def decode_row_fast(q: np.ndarray, codes_k: np.ndarray, codes_v: np.ndarray, params_head: dict,
                     scale: float, window: int = 0, sink: Optional[float] = None,
-                    n_split: int = 1) -> np.ndarray:
+                    n_split: int = 1, scales_k: Optional[np.ndarray] = None) -> np.ndarray:
     """Fast (transform-domain, split-context) form of ``decode_row``; equal up to rounding."""
     lo, hi = attended_range(codes_k.shape[0], window)
     t_k_inv_t = np.asarray(params_head["t_k_inv_t"], dtype=np.float64)
@@ -101,6 +112,8 @@ def decode_row_fast(q: np.ndarray, codes_k: np.ndarray, codes_v: np.ndarray, par
     r_hat = lookup(codes_k[lo:hi], params_head["cb_k"])
     s_hat = lookup(codes_v[lo:hi], params_head["cb_v"])
     z = r_hat @ qp
+    if scales_k is not None:  # the read path's one multiply per token
+        z = z * np.asarray(scales_k[lo:hi], dtype=np.float64)
     d = s_hat.shape[1]
     parts = []
     bounds = np.linspace(0, z.size, n_split + 1).astype(int)

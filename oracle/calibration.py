@@ -28,6 +28,7 @@ from __future__ import annotations
 
 import numpy as np
 
+from .codec import normalized_key_coefficients
 from .vq import train_codebooks
 
 EIG_FLOOR = 1e-30
@@ -150,8 +151,11 @@ def fold_columns(mat_by_rank: np.ndarray, g: int) -> np.ndarray:
 
 def calibrate_head(k_cal: np.ndarray, v_cal: np.ndarray, q_cal: np.ndarray, *,
                    group_dim: int = 4, codebook_size: int = 256, mo_stride: int = 16,
-                   kmeans_iters: int = 25, seed=0):
+                   kmeans_iters: int = 25, seed=0, key_scale: bool = False):
     """Full per-(layer, KV head) calibration: Algorithms 2 and 3, Corollary 1.
+
+    With key_scale the key codebooks are trained on the normalized coefficients
+    r_j / rho_j, rho_j = ||r_j|| / sqrt(d) (Algorithm 2), for the key-scale format.
 
     Inputs: calibration keys (M, D), values (M, D) and the G sharing query heads'
     queries (G, M, D).  Returns a dict of stored parameters (t_k, t_k_inv_t,
@@ -183,6 +187,8 @@ def calibrate_head(k_cal: np.ndarray, v_cal: np.ndarray, q_cal: np.ndarray, *,
     seed_k, seed_v = ss.spawn(2)
     r_cal = (k_cal - stored["kbar"].astype(np.float64)) @ stored["t_k"].astype(np.float64)
     s_cal_stored = v_cal @ stored["t_v"].astype(np.float64)
+    if key_scale:
+        r_cal = normalized_key_coefficients(r_cal)[0]
     stored["cb_k"] = train_codebooks(r_cal, g, codebook_size, seed_k, kmeans_iters)
     stored["cb_v"] = train_codebooks(s_cal_stored, g, codebook_size, seed_v, kmeans_iters)
     diag = {"m_q": mq, "s_k": sk, "m_o": mo, "lambda_k": lam_k, "lambda_v": lam_v,

@@ -7,6 +7,15 @@ transformed, r = (k - k_bar) R_K, and each group of g coefficients is replaced
 by the index of its nearest codeword; values are transformed by R_V
 (Corollary 1, s = v R_V) and encoded the same way.  All arithmetic in fp64 on
 the stored fp32 transforms and mean and the stored fp16 codebooks.
+
+Key-scale format (Algorithm 2's normalization; Sec. "Bit rate": a BF16 scale
+per token; Sec. "Decoding kernel and read path": the read path multiplies the
+partial logit by it): rho = ||r||_2 / sqrt(d) and the codes quantize r / rho
+against codebooks trained on normalized coefficients.  Readings fixed here:
+||r||^2 is summed in coordinate order with each square rounded; rho =
+sqrt(||r||^2) / sqrt(d); the stored scale is rho rounded to fp32 and then to
+bf16 (both to nearest even), and the decode uses the stored value; a key with
+r = 0 gets rho = 0 and the codes of the zero vector.
 """
 
 from __future__ import annotations
@@ -25,6 +34,46 @@ def key_coefficients(k: np.ndarray, kbar: np.ndarray, t_k: np.ndarray) -> np.nda
 def value_coefficients(v: np.ndarray, t_v: np.ndarray) -> np.ndarray:
     """s = v t_v for every row of v (n, D)."""
     return np.asarray(v, dtype=np.float64) @ np.asarray(t_v, dtype=np.float64)
+
+
+def key_scale(r: np.ndarray) -> np.ndarray:
+    """rho = ||r||_2 / sqrt(d) per row of r (n, d), in fp64 (Algorithm 2)."""
+    r = np.asarray(r, dtype=np.float64)
+    ss = np.cumsum(r * r, axis=-1)[..., -1]  # sequential sum of the rounded squares
+    return np.sqrt(ss) / np.sqrt(float(r.shape[-1]))
+
+
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Stored bf16 bit patterns of fp64 values: to fp32, then to bf16, each to nearest even."""
+    f = np.asarray(x, dtype=np.float64).astype(np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def bf16_value(bits: np.ndarray) -> np.ndarray:
+    """fp64 value of bf16 bit patterns."""
+    return (np.asarray(bits, dtype=np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def normalized_key_coefficients(r: np.ndarray):
+    """(r / rho, rho) with rows of r = 0 mapped to (0, 0)."""
+    rho = key_scale(r)
+    safe = np.where(rho > 0.0, rho, 1.0)
+    rn = np.where(rho[:, None] > 0.0, np.asarray(r, dtype=np.float64) / safe[:, None], 0.0)
+    return rn, rho
+
+
+def encode_tokens_scaled(k: np.ndarray, v: np.ndarray, params_head: dict):
+    """Key-scale format: codes and near-tie gaps of n keys and values (n, D) and the keys' stored scales.
+
+    Returns (codes_k, gap_k, scale_bits, codes_v, gap_v, rho) where scale_bits
+    are the stored bf16 patterns (n,) and rho the fp64 scales before storage.
+    """
+    r = key_coefficients(k, params_head["kbar"], params_head["t_k"])
+    rn, rho = normalized_key_coefficients(r)
+    ck, gk = encode(rn, params_head["cb_k"])
+    cv, gv = encode(value_coefficients(v, params_head["t_v"]), params_head["cb_v"])
+    return ck, gk, bf16_bits(rho), cv, gv, rho
 
 
 def encode_tokens(k: np.ndarray, v: np.ndarray, params_head: dict):

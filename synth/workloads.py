@@ -31,8 +31,8 @@ __all__ = [
     "Workload", "WORKLOADS", "get_workload", "ROLE",
     "rng_for", "haar_orthogonal", "power_spectrum", "round_to_bf16", "to_storage",
     "head_bases", "calibration_set", "cache_tokens", "decode_queries",
-    "sink_logits", "random_codes", "shuffled_block_table", "uniform_seq_lens",
-    "bench_params",
+    "sink_logits", "random_codes", "random_key_scales", "shuffled_block_table",
+    "uniform_seq_lens", "bench_params",
 ]
 
 ROLE = {
@@ -40,7 +40,7 @@ ROLE = {
     "calib_k": 3, "calib_v": 4, "calib_q": 5,
     "cache_k": 6, "cache_v": 7, "query": 8, "sink": 9,
     "codes_k": 10, "codes_v": 11, "block_table": 12, "seq_lens": 13,
-    "bench": 14, "new_k": 15, "new_v": 16,
+    "bench": 14, "new_k": 15, "new_v": 16, "scales_k": 17,
 }
 
 
@@ -247,6 +247,13 @@ def random_codes(wl: Workload, layer: int, side: str, shape) -> np.ndarray:
     role = "codes_k" if side == "k" else "codes_v"
     return rng_for(wl.config_id, layer, 0, role).integers(0, wl.codebook_size, size=shape,
                                                           dtype=np.uint8)
+
+
+def random_key_scales(wl: Workload, layer: int, shape, sigma: float = 0.5) -> np.ndarray:
+    """bf16 bit patterns (uint16) of log-normal positive values exp(N(0, sigma^2)):
+    a stand-in pool of per-token key scales for a cache of random codes."""
+    x = np.exp(sigma * rng_for(wl.config_id, layer, 0, "scales_k").standard_normal(shape))
+    return (round_to_bf16(x).view(np.uint32) >> 16).astype(np.uint16)
 
 
 def shuffled_block_table(wl: Workload, capacity_tokens: Optional[int] = None) -> np.ndarray:

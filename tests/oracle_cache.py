@@ -23,29 +23,35 @@ KEYS = ("kbar", "t_k", "t_k_inv_t", "t_v", "cb_k", "cb_v")
 VERSION = 1
 
 
-def _key(wl: synth.Workload, layer: int, tokens: int, iters: int, mo_stride: int) -> str:
-    desc = json.dumps([VERSION, wl.seed_config, wl.num_q_heads, wl.num_kv_heads, wl.head_dim,
-                       wl.kv_alpha, wl.q_alpha, wl.q_basis_aligned, wl.dtype, layer, tokens,
-                       iters, mo_stride])
+def _key(wl: synth.Workload, layer: int, tokens: int, iters: int, mo_stride: int,
+         key_scale: bool = False) -> str:
+    fields = [VERSION, wl.seed_config, wl.num_q_heads, wl.num_kv_heads, wl.head_dim,
+              wl.kv_alpha, wl.q_alpha, wl.q_basis_aligned, wl.dtype, layer, tokens,
+              iters, mo_stride]
+    if key_scale:
+        fields.append("key_scale")
+    desc = json.dumps(fields)
     return hashlib.sha1(desc.encode()).hexdigest()[:16]
 
 
 def calibrated_params(wl: synth.Workload, layer: int = 0, tokens: int = None, iters: int = 25,
-                      mo_stride: int = 16, heads=None):
-    """Stacked [Hkv][...] stored parameters of one layer (oracle calibration per KV head)."""
+                      mo_stride: int = 16, heads=None, key_scale: bool = False):
+    """Stacked [Hkv][...] stored parameters of one layer (oracle calibration per KV head).
+
+    key_scale: key codebooks trained on normalized coefficients (key-scale format)."""
     tokens = wl.calib_tokens if tokens is None else tokens
     heads = range(wl.num_kv_heads) if heads is None else heads
     os.makedirs(CACHE, exist_ok=True)
     per_head = []
     for kv in heads:
-        path = os.path.join(CACHE, f"{wl.name}_L{layer}_kv{kv}_{_key(wl, layer, tokens, iters, mo_stride)}.npz")
+        path = os.path.join(CACHE, f"{wl.name}_L{layer}_kv{kv}_{_key(wl, layer, tokens, iters, mo_stride, key_scale)}.npz")
         if os.path.exists(path):
             with np.load(path, allow_pickle=False) as z:
                 per_head.append({k: z[k] for k in KEYS})
             continue
         k, v, q = synth.calibration_set(wl, layer, kv, tokens)
         stored, _ = calibration.calibrate_head(k, v, q, mo_stride=mo_stride, kmeans_iters=iters,
-                                               seed=[wl.seed_config, layer, kv])
+                                               seed=[wl.seed_config, layer, kv], key_scale=key_scale)
         np.savez(path + ".tmp.npz", **stored)
         os.replace(path + ".tmp.npz", path)
         per_head.append(stored)
