@@ -133,16 +133,18 @@ def cpu_baseline(wl, budget_s: float):
 def other_workloads(nk, torch, dev, calls: int):
     """Decode-kernel time of every other workload shape (one line each).
 
-    Pools hold uniformly random codes; shapes too small to exceed the 256 MB
-    last-level cache are measured as they would run (cache-resident)."""
+    Pools hold uniformly random codes (and, in the key-scale format, random
+    bf16 scales); shapes too small to exceed the 256 MB last-level cache are
+    measured as they would run (cache-resident)."""
     import synth
     res = []
-    cases = [("single_head", 0), ("sweep_b64_s32k", 0), ("sweep_b1_s128k", 0),
-             ("gptoss_pair", 0), ("gptoss_pair", 1), ("append_paged", 0)]
-    for name, layer in cases:
+    cases = [("single_head", 0, False), ("sweep_b64_s32k", 0, False), ("sweep_b1_s128k", 0, False),
+             ("gptoss_pair", 0, False), ("gptoss_pair", 1, False), ("append_paged", 0, False),
+             ("qwen3_8b", 0, True), ("gptoss_pair", 1, True)]
+    for name, layer, key_scale in cases:
         wl = synth.get_workload(name)
         B, S, H, Hq, D, L = wl.batch, wl.seq_len, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.groups
-        P = nk.NovaKVParams.from_arrays(synth.bench_params(wl, layer), device=dev)
+        P = nk.NovaKVParams.from_arrays(synth.bench_params(wl, layer), device=dev, key_scale=key_scale)
         gen = torch.Generator(device=dev)
         gen.manual_seed(7)
         if wl.block_size:
@@ -152,10 +154,13 @@ def other_workloads(nk, torch, dev, calls: int):
         else:
             layout = nk.CacheLayout.contiguous(S)
             shape = (B, H, S, L)
-        pool_bytes = 2 * int(np.prod(shape))
+        scale_bytes = 2 * int(np.prod(shape[:3])) if key_scale else 0
+        pool_bytes = 2 * int(np.prod(shape)) + scale_bytes
         copies = int(min(6, max(1, -(-(600 << 20) // pool_bytes)))) if pool_bytes > (64 << 20) else 1
         pools = [(torch.randint(0, 256, shape, dtype=torch.uint8, device=dev, generator=gen),
-                  torch.randint(0, 256, shape, dtype=torch.uint8, device=dev, generator=gen))
+                  torch.randint(0, 256, shape, dtype=torch.uint8, device=dev, generator=gen),
+                  (torch.rand(shape[:3], generator=gen, device=dev) + 0.5).to(torch.bfloat16)
+                  if key_scale else None)
                  for _ in range(copies)]
         q = torch.randn((B, Hq, D), generator=gen, device=dev).to(torch.bfloat16)
         seq = torch.full((B,), S, dtype=torch.int32, device=dev)
@@ -163,8 +168,9 @@ def other_workloads(nk, torch, dev, calls: int):
         out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
         ws = torch.zeros(nk.decode_workspace_bytes(P, B, Hq, S), dtype=torch.uint8, device=dev)
         window = wl.windows[layer]
-        calls_ = [nk.prepare_decode(P, layout, q, pk, pv, seq, S, out, ws, window=window, sinks=sinks)
-                  for pk, pv in pools]
+        calls_ = [nk.prepare_decode(P, layout, q, pk, pv, seq, S, out, ws, window=window, sinks=sinks,
+                                    k_scales=ps)
+                  for pk, pv, ps in pools]
         for i in range(5):
             calls_[i % copies]()
         torch.cuda.synchronize()
@@ -177,11 +183,15 @@ def other_workloads(nk, torch, dev, calls: int):
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) * 1e3 / calls
         cb = wl.code_bytes_per_step(layer)
-        res.append({"workload": f"{name}" + (f" layer {layer} (window {window})" if wl.num_layers > 1 else ""),
+        # the key scales of the attended tokens: 2 bytes per token and KV head
+        sb = cb // L if key_scale else 0
+        res.append({"workload": f"{name}" + (f" layer {layer} (window {window})" if wl.num_layers > 1 else "")
+                    + (" key-scale format" if key_scale else ""),
                     "batch": B, "seq_len": S, "q_heads": Hq, "kv_heads": H, "head_dim": D,
-                    "paged_block": wl.block_size or None, "code_bytes": cb, "pool_copies": copies,
-                    "decode_us": round(us, 2), "GB_per_s": round(cb / (us * 1e-6) / 1e9, 1),
-                    "frac_of_hbm_peak": round(cb / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
+                    "paged_block": wl.block_size or None, "code_bytes": cb, "scale_bytes": sb,
+                    "pool_copies": copies,
+                    "decode_us": round(us, 2), "GB_per_s": round((cb + sb) / (us * 1e-6) / 1e9, 1),
+                    "frac_of_hbm_peak": round((cb + sb) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
         del pools, calls_, ws
         torch.cuda.empty_cache()
     return res

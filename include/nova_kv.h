@@ -73,9 +73,19 @@ typedef enum {
  *   cb_v      [Hkv][L][K][g] fp16 bit patterns: value codebook of each group
  *
  * Group l covers transform coordinates [l*g, (l+1)*g).  Supported: g = 4,
- * K = 256, D in {64, 128}; flags must be 0 (reserved).  Every array must be
- * 16-byte aligned (NOVA_KV_ERR_INVALID_ARG otherwise).
+ * K = 256, D in {64, 128}.  Every array must be 16-byte aligned
+ * (NOVA_KV_ERR_INVALID_ARG otherwise).
+ *
+ *   flags     0, or NOVA_KV_KEY_SCALE: the key-scale format (paper: Algorithm
+ *             2 normalizes r_j by rho_j = ||r_j||_2 / sqrt(D) before the
+ *             codebooks are trained; Sec. "Bit rate": a BF16 scale per token;
+ *             Sec. "Decoding kernel and read path": the read path multiplies
+ *             the partial logit by it).  cb_k must then hold codebooks of
+ *             normalized coefficients, and every call takes a k_scales pool.
+ *             Other bits are reserved (NOVA_KV_ERR_UNSUPPORTED).
  */
+#define NOVA_KV_KEY_SCALE 1u
+
 typedef struct {
     int32_t num_kv_heads;
     int32_t head_dim;
@@ -125,16 +135,24 @@ typedef struct {
  *              blocks_per_seq.
  *   k_codes, v_codes  code pools (see nova_kv_layout), written at positions
  *              start_pos[b] .. start_pos[b] + n_new - 1; nothing else is touched.
+ *   k_scales   key-scale format only (else ignored, may be NULL): the scale
+ *              pool, uint16 bf16 bit patterns [num_blocks][Hkv][block_size]
+ *              addressed like the code pools (one scale per token-head),
+ *              2-byte aligned, written at the same positions.
  *
  * For every (b, token, KV head, group l) the stored byte is the smallest index
  * c minimising sum_i (u_i - cb[l][c][i])^2, u the group's coefficients; the
- * transform and the distances are evaluated in fp64.
+ * transform and the distances are evaluated in fp64.  In the key-scale format
+ * the key side quantizes u / rho with rho = sqrt(sum of the D squared
+ * coefficients, added in coordinate order) / sqrt(D) (u = 0 when rho = 0), and
+ * stores rho rounded to fp32 and then to bf16 (each to nearest even).
  * batch == 0 or n_new == 0 is a valid no-op.
  */
 nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *layout,
                               const void *k, const void *v, nova_kv_dtype in_dtype,
                               int32_t batch, int32_t n_new, const int32_t *start_pos,
-                              uint8_t *k_codes, uint8_t *v_codes, void *hip_stream);
+                              uint8_t *k_codes, uint8_t *v_codes, uint16_t *k_scales,
+                              void *hip_stream);
 
 /*
  * Bytes of device workspace nova_kv_decode_attn needs for this shape (split
@@ -155,6 +173,8 @@ size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch,
  *
  *   q          [B][Hq][D] device, dtype q_dtype (F32 or BF16); query head h
  *              reads KV head h / (Hq / Hkv).
+ *   k_scales   key-scale format only (else ignored, may be NULL): the scale
+ *              pool of nova_kv_encode, read at the attended positions.
  *   seq_lens   [B] int32 device: cached tokens of each sequence (the current
  *              token already appended); precondition 0 <= seq_lens[b] <= max_seq_len.
  *   max_seq_len  host upper bound of seq_lens; must not exceed the layout's
@@ -166,7 +186,9 @@ size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch,
  *   out        [B][Hq][D] fp32 device:
  *                out = sum_t p_t v_hat_t,  p = softmax({z_t} U {sink}),
  *                z_t = q . k_hat_t * scale,  k_hat_t = r_hat_t t_k_inv_t^T + k_bar,
- *                v_hat_t = s_hat_t t_v^T.
+ *                v_hat_t = s_hat_t t_v^T;
+ *              in the key-scale format r_hat_t is rho_t times the codewords,
+ *              rho_t the stored bf16 scale.
  *              A row with no attended token and no sink is written as zeros.
  *   workspace  device scratch of at least nova_kv_decode_workspace_bytes(...)
  *              bytes, 256-byte aligned.  It must be zero-filled before its
@@ -179,6 +201,7 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
                                    const void *q, nova_kv_dtype q_dtype,
                                    int32_t batch, int32_t num_q_heads,
                                    const uint8_t *k_codes, const uint8_t *v_codes,
+                                   const uint16_t *k_scales,
                                    const int32_t *seq_lens, int32_t max_seq_len,
                                    int32_t window, const float *sinks, float softmax_scale,
                                    float *out, void *workspace, size_t workspace_bytes,
@@ -196,24 +219,26 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
  *   k_new, v_new  [B][Hkv][D] device, dtype new_dtype (F32 or BF16): the token
  *              at position seq_lens[b] - 1 of each sequence (the newest cached
  *              token); precondition seq_lens[b] >= 1.
- *   k_codes, v_codes  the code pools, written at position seq_lens[b] - 1
- *              exactly as nova_kv_encode(n_new = 1, start_pos = seq_lens - 1)
- *              writes them (same bytes); nothing else is touched.
+ *   k_codes, v_codes (and k_scales in the key-scale format)  the pools,
+ *              written at position seq_lens[b] - 1 exactly as
+ *              nova_kv_encode(n_new = 1, start_pos = seq_lens - 1) writes them
+ *              (same bytes); nothing else is touched.
  *   all other arguments as in nova_kv_decode_attn (params also need t_k).
  *
  * out equals the output of nova_kv_decode_attn over the pools after that
  * append, up to fp32 rounding (the new token's term is added after the
  * split combine instead of inside a split).  With head_dim 128 on 16-aligned
- * blocks the step is a single kernel launch, in which the workgroups that
- * read the pools also encode the new token; other shapes run the one-token
- * encode and the decode one after the other on the stream.
+ * blocks (and not the key-scale format) the step is a single kernel launch,
+ * in which the workgroups that read the pools also encode the new token;
+ * otherwise the one-token encode and the decode run one after the other on
+ * the stream.
  * batch == 0 is a valid no-op.
  */
 nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
                                           const void *k_new, const void *v_new, nova_kv_dtype new_dtype,
                                           const void *q, nova_kv_dtype q_dtype,
                                           int32_t batch, int32_t num_q_heads,
-                                          uint8_t *k_codes, uint8_t *v_codes,
+                                          uint8_t *k_codes, uint8_t *v_codes, uint16_t *k_scales,
                                           const int32_t *seq_lens, int32_t max_seq_len,
                                           int32_t window, const float *sinks, float softmax_scale,
                                           float *out, void *workspace, size_t workspace_bytes,

@@ -21,6 +21,8 @@ NOVA_KV_ERR_HIP = 4
 NOVA_KV_F32 = 0
 NOVA_KV_BF16 = 1
 
+NOVA_KV_KEY_SCALE = 1  # nova_kv_params.flags: the key-scale format
+
 EXPORTED = (
     "nova_kv_encode",
     "nova_kv_decode_workspace_bytes",
@@ -76,14 +78,14 @@ def lib() -> ctypes.CDLL:
         L.nova_kv_encode.restype = ctypes.c_int
         L.nova_kv_encode.argtypes = [P(Params), P(Layout), ctypes.c_void_p, ctypes.c_void_p,
                                      ctypes.c_int, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
         L.nova_kv_decode_workspace_bytes.restype = ctypes.c_size_t
         L.nova_kv_decode_workspace_bytes.argtypes = [P(Params), ctypes.c_int32, ctypes.c_int32,
                                                      ctypes.c_int32]
         L.nova_kv_decode_attn.restype = ctypes.c_int
         L.nova_kv_decode_attn.argtypes = [P(Params), P(Layout), ctypes.c_void_p, ctypes.c_int,
                                           ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                           ctypes.c_int32, ctypes.c_void_p, ctypes.c_float,
                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                           ctypes.c_void_p]
@@ -91,7 +93,7 @@ def lib() -> ctypes.CDLL:
         L.nova_kv_append_decode_attn.argtypes = [P(Params), P(Layout), ctypes.c_void_p, ctypes.c_void_p,
                                                  ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
                                                  ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
                                                  ctypes.c_int32, ctypes.c_void_p, ctypes.c_float,
                                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                                  ctypes.c_void_p]

@@ -14,8 +14,9 @@ import torch
 
 from . import _native as nat
 
-__all__ = ["NovaKVParams", "CacheLayout", "encode", "decode_attn", "decode_workspace_bytes",
-           "code_pool_shape", "prepare_encode", "prepare_decode"]
+__all__ = ["NovaKVParams", "CacheLayout", "encode", "decode_attn", "append_decode_attn",
+           "decode_workspace_bytes", "code_pool_shape", "scale_pool_shape", "prepare_encode",
+           "prepare_decode", "prepare_append_decode"]
 
 
 def _stream_ptr(stream: Optional[torch.cuda.Stream]) -> int:
@@ -37,10 +38,15 @@ def _require(t: torch.Tensor, name: str, dtypes, numel: Optional[int] = None) ->
 
 
 class NovaKVParams:
-    """Per-layer calibration outputs resident on the device (see nova_kv_params)."""
+    """Per-layer calibration outputs resident on the device (see nova_kv_params).
+
+    ``key_scale`` selects the key-scale format (one bf16 scale per cached key;
+    the key codebooks are then trained on normalized coefficients), and every
+    call then takes a ``k_scales`` pool of shape ``scale_pool_shape``.
+    """
 
     def __init__(self, kbar, t_k, t_k_inv_t, t_v, cb_k, cb_v, group_dim: int = 4,
-                 codebook_size: int = 256):
+                 codebook_size: int = 256, key_scale: bool = False):
         hkv, d = kbar.shape
         L = d // group_dim
         _require(kbar, "kbar", (torch.float32,), hkv * d)
@@ -52,7 +58,9 @@ class NovaKVParams:
         self.group_dim, self.codebook_size = group_dim, codebook_size
         self.kbar, self.t_k, self.t_k_inv_t, self.t_v = kbar, t_k, t_k_inv_t, t_v
         self.cb_k, self.cb_v = cb_k, cb_v
-        self._c = nat.Params(hkv, d, group_dim, codebook_size, 0, kbar.data_ptr(), t_k.data_ptr(),
+        self.key_scale = bool(key_scale)
+        flags = nat.NOVA_KV_KEY_SCALE if self.key_scale else 0
+        self._c = nat.Params(hkv, d, group_dim, codebook_size, flags, kbar.data_ptr(), t_k.data_ptr(),
                              t_k_inv_t.data_ptr(), t_v.data_ptr(), cb_k.data_ptr(),
                              cb_v.data_ptr())
 
@@ -61,13 +69,13 @@ class NovaKVParams:
         return self.head_dim // self.group_dim
 
     @classmethod
-    def from_arrays(cls, arrays: dict, device="cuda") -> "NovaKVParams":
+    def from_arrays(cls, arrays: dict, device="cuda", key_scale: bool = False) -> "NovaKVParams":
         """From host arrays: kbar/t_k/t_k_inv_t/t_v float32, cb_k/cb_v float16 ([Hkv][...])."""
         f32 = {k: torch.as_tensor(arrays[k]).to(torch.float32).contiguous().to(device)
                for k in ("kbar", "t_k", "t_k_inv_t", "t_v")}
         f16 = {k: torch.as_tensor(arrays[k]).to(torch.float16).contiguous().to(device)
                for k in ("cb_k", "cb_v")}
-        return cls(**f32, **f16)
+        return cls(**f32, **f16, key_scale=key_scale)
 
     @property
     def c(self) -> nat.Params:
@@ -104,6 +112,24 @@ def code_pool_shape(params: NovaKVParams, layout: CacheLayout, batch: int, num_b
     return (nb, params.num_kv_heads, layout.block_size, params.groups)
 
 
+def scale_pool_shape(params: NovaKVParams, layout: CacheLayout, batch: int, num_blocks=None):
+    """Shape of the key-scale pool: [num_blocks][Hkv][block_size] (bf16 bit patterns)."""
+    return code_pool_shape(params, layout, batch, num_blocks)[:3]
+
+
+_SCALE_DTYPES = (torch.bfloat16, torch.int16, torch.uint16)
+
+
+def _scales_ptr(params: NovaKVParams, k_scales: Optional[torch.Tensor], k_codes: torch.Tensor):
+    """Device pointer of the key-scale pool (None outside the key-scale format)."""
+    if not params.key_scale:
+        return None
+    if k_scales is None:
+        raise ValueError("the key-scale format needs a k_scales pool")
+    _require(k_scales, "k_scales", _SCALE_DTYPES, k_codes.numel() // params.groups)
+    return k_scales.data_ptr()
+
+
 def _dtype_code(t: torch.Tensor) -> int:
     if t.dtype == torch.float32:
         return nat.NOVA_KV_F32
@@ -114,7 +140,7 @@ def _dtype_code(t: torch.Tensor) -> int:
 
 def encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v: torch.Tensor,
            start_pos: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
-           stream: Optional[torch.cuda.Stream] = None) -> None:
+           stream: Optional[torch.cuda.Stream] = None, k_scales: Optional[torch.Tensor] = None) -> None:
     """nova_kv_encode: k, v [B][n_new][Hkv][D] (fp32 or bf16), start_pos int32 [B]."""
     if k.dim() != 4:
         raise ValueError("k must be [B][n_new][Hkv][D]")
@@ -126,9 +152,10 @@ def encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v: torch.
     _require(start_pos, "start_pos", (torch.int32,), b)
     _require(k_codes, "k_codes", (torch.uint8,))
     _require(v_codes, "v_codes", (torch.uint8,), k_codes.numel())
+    ks = _scales_ptr(params, k_scales, k_codes)
     nat.check(nat.lib().nova_kv_encode(
         ctypes.byref(params.c), ctypes.byref(layout.c), k.data_ptr(), v.data_ptr(), _dtype_code(k),
-        b, n_new, start_pos.data_ptr(), k_codes.data_ptr(), v_codes.data_ptr(),
+        b, n_new, start_pos.data_ptr(), k_codes.data_ptr(), v_codes.data_ptr(), ks,
         _stream_ptr(stream)))
 
 
@@ -143,7 +170,8 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
                 max_seq_len: int, window: int = 0, sinks: Optional[torch.Tensor] = None,
                 softmax_scale: float = 0.0, out: Optional[torch.Tensor] = None,
                 workspace: Optional[torch.Tensor] = None,
-                stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+                stream: Optional[torch.cuda.Stream] = None,
+                k_scales: Optional[torch.Tensor] = None) -> torch.Tensor:
     """nova_kv_decode_attn: q [B][Hq][D] (fp32 or bf16) -> out [B][Hq][D] fp32.
 
     A caller-provided workspace must be zero-filled before its first use; each
@@ -165,16 +193,17 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
     if workspace is None:
         workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=q.device)
     _require(workspace, "workspace", (torch.uint8,))
+    ks = _scales_ptr(params, k_scales, k_codes)
     nat.check(nat.lib().nova_kv_decode_attn(
         ctypes.byref(params.c), ctypes.byref(layout.c), q.data_ptr(), _dtype_code(q), b, hq,
-        k_codes.data_ptr(), v_codes.data_ptr(), seq_lens.data_ptr(), max_seq_len, window,
+        k_codes.data_ptr(), v_codes.data_ptr(), ks, seq_lens.data_ptr(), max_seq_len, window,
         sinks.data_ptr() if sinks is not None else None, float(softmax_scale), out.data_ptr(),
         workspace.data_ptr(), workspace.numel(), _stream_ptr(stream)))
     return out
 
 
 def _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
-                        workspace, window, sinks, softmax_scale, stream):
+                        workspace, window, sinks, softmax_scale, stream, k_scales):
     if q.dim() != 3 or q.shape[2] != params.head_dim:
         raise ValueError("q must be [B][Hq][D]")
     b, hq, d = q.shape
@@ -190,11 +219,12 @@ def _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_l
         _require(sinks, "sinks", (torch.float32,), hq)
     _require(out, "out", (torch.float32,), b * hq * d)
     _require(workspace, "workspace", (torch.uint8,))
+    ks = _scales_ptr(params, k_scales, k_codes)
     vp = ctypes.c_void_p
     return (ctypes.byref(params.c), ctypes.byref(layout.c), vp(k_new.data_ptr()), vp(v_new.data_ptr()),
             ctypes.c_int(_dtype_code(k_new)), vp(q.data_ptr()), ctypes.c_int(_dtype_code(q)),
             ctypes.c_int32(b), ctypes.c_int32(hq), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()),
-            vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len), ctypes.c_int32(window),
+            vp(ks), vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len), ctypes.c_int32(window),
             vp(sinks.data_ptr() if sinks is not None else None), ctypes.c_float(softmax_scale),
             vp(out.data_ptr()), vp(workspace.data_ptr()), ctypes.c_size_t(workspace.numel()),
             vp(_stream_ptr(stream)))
@@ -205,7 +235,8 @@ def append_decode_attn(params: NovaKVParams, layout: CacheLayout, k_new: torch.T
                        seq_lens: torch.Tensor, max_seq_len: int, window: int = 0,
                        sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
                        out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
-                       stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+                       stream: Optional[torch.cuda.Stream] = None,
+                       k_scales: Optional[torch.Tensor] = None) -> torch.Tensor:
     """nova_kv_append_decode_attn: store the step's k_new, v_new [B][Hkv][D] at
     position seq_lens[b] - 1 of the pools, then decode q [B][Hq][D] over the
     cache including them -> out [B][Hq][D] fp32.  Workspace as in decode_attn."""
@@ -216,7 +247,7 @@ def append_decode_attn(params: NovaKVParams, layout: CacheLayout, k_new: torch.T
     if workspace is None:
         workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=q.device)
     args = _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
-                               workspace, window, sinks, softmax_scale, stream)
+                               workspace, window, sinks, softmax_scale, stream, k_scales)
     nat.check(nat.lib().nova_kv_append_decode_attn(*args))
     return out
 
@@ -235,7 +266,8 @@ class PreparedCall:
 
 def prepare_encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v: torch.Tensor,
                    start_pos: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
-                   stream: Optional[torch.cuda.Stream] = None) -> PreparedCall:
+                   stream: Optional[torch.cuda.Stream] = None,
+                   k_scales: Optional[torch.Tensor] = None) -> PreparedCall:
     """nova_kv_encode with the arguments of encode(), marshalled once."""
     if k.dim() != 4:
         raise ValueError("k must be [B][n_new][Hkv][D]")
@@ -247,19 +279,22 @@ def prepare_encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v
     _require(start_pos, "start_pos", (torch.int32,), b)
     _require(k_codes, "k_codes", (torch.uint8,))
     _require(v_codes, "v_codes", (torch.uint8,), k_codes.numel())
+    ks = _scales_ptr(params, k_scales, k_codes)
     vp = ctypes.c_void_p
     args = (ctypes.byref(params.c), ctypes.byref(layout.c), vp(k.data_ptr()), vp(v.data_ptr()),
             ctypes.c_int(_dtype_code(k)), ctypes.c_int32(b), ctypes.c_int32(n_new),
-            vp(start_pos.data_ptr()), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()),
+            vp(start_pos.data_ptr()), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()), vp(ks),
             vp(_stream_ptr(stream)))
-    return PreparedCall(nat.lib().nova_kv_encode, args, (params, layout, k, v, start_pos, k_codes, v_codes))
+    return PreparedCall(nat.lib().nova_kv_encode, args,
+                        (params, layout, k, v, start_pos, k_codes, v_codes, k_scales))
 
 
 def prepare_decode(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
                    k_codes: torch.Tensor, v_codes: torch.Tensor, seq_lens: torch.Tensor,
                    max_seq_len: int, out: torch.Tensor, workspace: torch.Tensor, window: int = 0,
                    sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
-                   stream: Optional[torch.cuda.Stream] = None) -> PreparedCall:
+                   stream: Optional[torch.cuda.Stream] = None,
+                   k_scales: Optional[torch.Tensor] = None) -> PreparedCall:
     """nova_kv_decode_attn with the arguments of decode_attn(), marshalled once
     (out and a zero-filled workspace are required here)."""
     if q.dim() != 3 or q.shape[2] != params.head_dim:
@@ -273,25 +308,28 @@ def prepare_decode(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
         _require(sinks, "sinks", (torch.float32,), hq)
     _require(out, "out", (torch.float32,), b * hq * d)
     _require(workspace, "workspace", (torch.uint8,))
+    ks = _scales_ptr(params, k_scales, k_codes)
     vp = ctypes.c_void_p
     args = (ctypes.byref(params.c), ctypes.byref(layout.c), vp(q.data_ptr()), ctypes.c_int(_dtype_code(q)),
             ctypes.c_int32(b), ctypes.c_int32(hq), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()),
-            vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len), ctypes.c_int32(window),
+            vp(ks), vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len), ctypes.c_int32(window),
             vp(sinks.data_ptr() if sinks is not None else None), ctypes.c_float(softmax_scale),
             vp(out.data_ptr()), vp(workspace.data_ptr()), ctypes.c_size_t(workspace.numel()),
             vp(_stream_ptr(stream)))
     return PreparedCall(nat.lib().nova_kv_decode_attn, args,
-                        (params, layout, q, k_codes, v_codes, seq_lens, sinks, out, workspace))
+                        (params, layout, q, k_codes, v_codes, seq_lens, sinks, out, workspace, k_scales))
 
 
 def prepare_append_decode(params: NovaKVParams, layout: CacheLayout, k_new: torch.Tensor, v_new: torch.Tensor,
                           q: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
                           seq_lens: torch.Tensor, max_seq_len: int, out: torch.Tensor, workspace: torch.Tensor,
                           window: int = 0, sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
-                          stream: Optional[torch.cuda.Stream] = None) -> PreparedCall:
+                          stream: Optional[torch.cuda.Stream] = None,
+                          k_scales: Optional[torch.Tensor] = None) -> PreparedCall:
     """nova_kv_append_decode_attn with the arguments of append_decode_attn(),
     marshalled once (out and a zero-filled workspace are required here)."""
     args = _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
-                               workspace, window, sinks, softmax_scale, stream)
+                               workspace, window, sinks, softmax_scale, stream, k_scales)
     return PreparedCall(nat.lib().nova_kv_append_decode_attn, args,
-                        (params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, sinks, out, workspace))
+                        (params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, sinks, out, workspace,
+                         k_scales))

@@ -46,7 +46,8 @@ nova_kv_status check_params(const nova_kv_params *p, bool need_encode, bool need
     return fail(NOVA_KV_ERR_UNSUPPORTED, "codebook_size %d unsupported (only 256)", p->codebook_size);
   if (p->head_dim != 64 && p->head_dim != 128)
     return fail(NOVA_KV_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", p->head_dim);
-  if (p->flags != 0) return fail(NOVA_KV_ERR_UNSUPPORTED, "flags 0x%x unsupported (must be 0)", p->flags);
+  if ((p->flags & ~NOVA_KV_KEY_SCALE) != 0)
+    return fail(NOVA_KV_ERR_UNSUPPORTED, "flags 0x%x unsupported (0 or NOVA_KV_KEY_SCALE)", p->flags);
   if (!p->kbar || !p->cb_k || !p->cb_v) return fail(NOVA_KV_ERR_INVALID_ARG, "kbar/cb_k/cb_v is NULL");
   if (!aligned(p->cb_k, 16) || !aligned(p->cb_v, 16))
     return fail(NOVA_KV_ERR_INVALID_ARG, "codebooks must be 16-byte aligned");
@@ -65,6 +66,14 @@ nova_kv_status check_layout(const nova_kv_layout *lay) {
     return fail(NOVA_KV_ERR_INVALID_ARG, "block_size and blocks_per_seq must be > 0");
   if (static_cast<long long>(lay->block_size) * lay->blocks_per_seq > (1LL << 30))
     return fail(NOVA_KV_ERR_INVALID_ARG, "per-sequence capacity too large");
+  return NOVA_KV_OK;
+}
+
+// The scale pool of the key-scale format (ignored otherwise).
+nova_kv_status check_scales(const nova_kv_params *p, const void *k_scales) {
+  if (!(p->flags & NOVA_KV_KEY_SCALE)) return NOVA_KV_OK;
+  if (!k_scales) return fail(NOVA_KV_ERR_INVALID_ARG, "k_scales is NULL in the key-scale format");
+  if (!aligned(k_scales, 2)) return fail(NOVA_KV_ERR_INVALID_ARG, "k_scales must be 2-byte aligned");
   return NOVA_KV_OK;
 }
 
@@ -92,7 +101,7 @@ const char *nova_kv_last_error(void) { return g_last_error.c_str(); }
 nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *layout,
                               const void *k, const void *v, nova_kv_dtype in_dtype,
                               int32_t batch, int32_t n_new, const int32_t *start_pos,
-                              uint8_t *k_codes, uint8_t *v_codes, void *hip_stream) {
+                              uint8_t *k_codes, uint8_t *v_codes, uint16_t *k_scales, void *hip_stream) {
   nova_kv_status st = check_params(p, true, false);
   if (st != NOVA_KV_OK) return st;
   if ((st = check_layout(layout)) != NOVA_KV_OK) return st;
@@ -103,6 +112,7 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
   if (static_cast<long long>(n_new) > static_cast<long long>(layout->block_size) * layout->blocks_per_seq)
     return fail(NOVA_KV_ERR_INVALID_ARG, "n_new exceeds the per-sequence capacity");
   if (batch == 0 || n_new == 0) return ok();
+  if ((st = check_scales(p, k_scales)) != NOVA_KV_OK) return st;
   if (!k || !v || !start_pos || !k_codes || !v_codes)
     return fail(NOVA_KV_ERR_INVALID_ARG, "k, v, start_pos, k_codes or v_codes is NULL");
 
@@ -123,6 +133,7 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
   a.start_pos = start_pos;
   a.k_codes = k_codes;
   a.v_codes = v_codes;
+  a.k_scales = (p->flags & NOVA_KV_KEY_SCALE) ? k_scales : nullptr;
   hipError_t e = novakv::launch_encode(a, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "encode launch: %s", hipGetErrorString(e));
   return ok();
@@ -141,7 +152,8 @@ namespace {
 // Host checks and argument set-up shared by the decode entry points.
 nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *layout, const void *q,
                               nova_kv_dtype q_dtype, int32_t batch, int32_t num_q_heads, const uint8_t *k_codes,
-                              const uint8_t *v_codes, const int32_t *seq_lens, int32_t max_seq_len,
+                              const uint8_t *v_codes, const uint16_t *k_scales, const int32_t *seq_lens,
+                              int32_t max_seq_len,
                               int32_t window, const float *sinks, float softmax_scale, float *out,
                               void *workspace, size_t workspace_bytes, bool need_encode,
                               novakv::DecodeArgs &a, novakv::DecodePlan &plan) {
@@ -163,6 +175,7 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
     return fail(NOVA_KV_ERR_INVALID_ARG, "q_dtype must be NOVA_KV_F32 or NOVA_KV_BF16");
   if (!(softmax_scale >= 0.f)) return fail(NOVA_KV_ERR_INVALID_ARG, "softmax_scale must be >= 0");
   if (batch == 0) return NOVA_KV_OK;
+  if ((st = check_scales(p, k_scales)) != NOVA_KV_OK) return st;
   if (!q || !k_codes || !v_codes || !seq_lens || !out)
     return fail(NOVA_KV_ERR_INVALID_ARG, "q, k_codes, v_codes, seq_lens or out is NULL");
   if (!aligned(k_codes, 16) || !aligned(v_codes, 16))
@@ -190,6 +203,7 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   a.q_bf16 = q_dtype == NOVA_KV_BF16;
   a.k_codes = k_codes;
   a.v_codes = v_codes;
+  a.k_scales = (p->flags & NOVA_KV_KEY_SCALE) ? k_scales : nullptr;
   a.seq_lens = seq_lens;
   a.max_seq_len = max_seq_len;
   a.window = window;
@@ -217,13 +231,13 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
 nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
                                    const void *q, nova_kv_dtype q_dtype, int32_t batch,
                                    int32_t num_q_heads, const uint8_t *k_codes,
-                                   const uint8_t *v_codes, const int32_t *seq_lens,
+                                   const uint8_t *v_codes, const uint16_t *k_scales, const int32_t *seq_lens,
                                    int32_t max_seq_len, int32_t window, const float *sinks,
                                    float softmax_scale, float *out, void *workspace,
                                    size_t workspace_bytes, void *hip_stream) {
   novakv::DecodeArgs a;
   novakv::DecodePlan plan;
-  nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, seq_lens,
+  nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales, seq_lens,
                                      max_seq_len, window, sinks, softmax_scale, out, workspace, workspace_bytes,
                                      false, a, plan);
   if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
@@ -236,21 +250,22 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
                                           const void *k_new, const void *v_new, nova_kv_dtype new_dtype,
                                           const void *q, nova_kv_dtype q_dtype, int32_t batch,
                                           int32_t num_q_heads, uint8_t *k_codes, uint8_t *v_codes,
-                                          const int32_t *seq_lens, int32_t max_seq_len, int32_t window,
+                                          uint16_t *k_scales, const int32_t *seq_lens, int32_t max_seq_len,
+                                          int32_t window,
                                           const float *sinks, float softmax_scale, float *out,
                                           void *workspace, size_t workspace_bytes, void *hip_stream) {
   if (new_dtype != NOVA_KV_F32 && new_dtype != NOVA_KV_BF16)
     return fail(NOVA_KV_ERR_INVALID_ARG, "new_dtype must be NOVA_KV_F32 or NOVA_KV_BF16");
   novakv::DecodeArgs a;
   novakv::DecodePlan plan;
-  nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, seq_lens,
-                                     max_seq_len, window, sinks, softmax_scale, out, workspace, workspace_bytes,
-                                     true, a, plan);
+  nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales,
+                                     seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace,
+                                     workspace_bytes, true, a, plan);
   if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
   if (!k_new || !v_new) return fail(NOVA_KV_ERR_INVALID_ARG, "k_new or v_new is NULL");
   const hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   hipError_t e;
-  if (plan.use_lut && p->head_dim == 128) {
+  if (plan.use_lut && p->head_dim == 128 && !(p->flags & NOVA_KV_KEY_SCALE)) {
     // one launch: the table kernel encodes the new token and attends to it
     a.append = 1;
     a.k_new = k_new;
@@ -280,6 +295,7 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
     ea.start_offset = -1;
     ea.k_codes = k_codes;
     ea.v_codes = v_codes;
+    ea.k_scales = (p->flags & NOVA_KV_KEY_SCALE) ? k_scales : nullptr;
     e = novakv::launch_encode(ea, stream);
     if (e == hipSuccess) e = novakv::launch_decode(a, plan.use_lut, stream);
   }

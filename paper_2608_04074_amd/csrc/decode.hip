@@ -155,6 +155,11 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
           }
         }
       }
+      if (a.k_scales) {  // key-scale format: the read path's per-token multiply
+        const float rho = __uint_as_float(static_cast<uint32_t>(a.k_scales[off / L]) << 16);
+#pragma unroll
+        for (int h = 0; h < kMaxGqa; ++h) z[h] *= rho;
+      }
     }
     // tile max per head
 #pragma unroll

@@ -267,7 +267,7 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
   }
 }
 
-template <int WAVES, bool APPEND>
+template <int WAVES, bool APPEND, bool KS>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int split, const int t0, const int t1, const size_t row0,
                                            const int rot, const int n_eff, const int S, float4 (&tv)[8]) {
@@ -311,7 +311,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   const int bs_shift = (bsz & (bsz - 1)) == 0 ? __builtin_ctz(bsz) : -1;
   const uint32_t koff = (4 * beta + v) * kL + 8 * u;  // lane offsets inside a 16-token sub-tile
   const uint32_t voff = 4 * u * kL + 8 * v;
-  auto load_round = [&](int R, uint2 *kw, uint2 *vw) {
+  // Key-scale format: lane (beta, j) also loads the stored scale of token
+  // j of sub-tile beta, issued after the code bytes.
+  auto load_round = [&](int R, uint2 *kw, uint2 *vw, uint32_t &ks) {
     size_t sub[4];  // uniform: byte offsets of the round's four sub-tiles
 #pragma unroll
     for (int r = 0; r < 4; ++r)
@@ -325,6 +327,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     const uint8_t *vb = vpool + subb;
 #pragma unroll
     for (int s = 0; s < 4; ++s) vw[s] = *reinterpret_cast<const uint2 *>(vb + voff + s * kL);
+    if constexpr (KS) ks = a.k_scales[subb / kL + (lane & 15)];
   };
   // Two named buffers of code bytes alternate through the token loop (unrolled
   // by two), so no in-flight load destination is ever copied: round rd+W is in
@@ -334,6 +337,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   // processing the current one, so waves that the issue arbiter serves less
   // often simply take fewer rounds and all waves end together.
   uint2 kwb[2][4], vwb[2][4];
+  uint32_t ksb[2] = {0u, 0u};
   int *rctr = reinterpret_cast<int *>(smem + kAuxCtl) + 1;
   if (tid == 0) *rctr = WAVES;  // rounds 0 .. WAVES-1 are taken; visible after the setup's barriers
   if constexpr (APPEND) {
@@ -408,7 +412,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     const float2 kb2 = *reinterpret_cast<const float2 *>(a.kbar + static_cast<size_t>(kv) * kD + 2 * lane);
     // a wave without a round of its own (nrounds >= 1 in an active split)
     // re-reads the last round and never processes it
-    load_round(max(0, R0 + 64 * min(wave, nrounds - 1)), kwb[0], vwb[0]);
+    load_round(max(0, R0 + 64 * min(wave, nrounds - 1)), kwb[0], vwb[0], ksb[0]);
     float *qs = reinterpret_cast<float *>(smem + kAuxQ);       // [4][128] query
     // partial q': [8 parts][32 groups][4 heads][4 coordinates], so that a table
     // lane's float4 (its group, its head) sits next to its neighbours'
@@ -533,7 +537,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     asel[r] = half8_t{one, one, one, one, one, one, one, one};
   }
 
-  auto process_round = [&](const int R, const uint2 *kw, const uint2 *vw) {
+  auto process_round = [&](const int R, const uint2 *kw, const uint2 *vw, const uint32_t ks) {
     // K: partial logits gathered from the table by transposing reads; each
     // read hands lane (beta,u,v) four partials of (token R+16r+4beta+u, head v)
     // and serves as the B operand of a 16x16x32 MFMA (two steps per MFMA)
@@ -563,6 +567,12 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       for (int r = 0; r < 4; ++r) kacc = __builtin_amdgcn_mfma_f32_16x16x32_f16(asel[r], e[r], kacc, 0, 0, 0);
     }
     float z[4] = {kacc[0], kacc[1], kacc[2], kacc[3]};
+    if constexpr (KS) {
+      // the read path's per-token multiply: token R + 16 beta + 4 i + u's
+      // scale is held by lane 16 beta + 4 i + u
+#pragma unroll
+      for (int i = 0; i < 4; ++i) z[i] *= __uint_as_float(static_cast<uint32_t>(__shfl(static_cast<int>(ks), 16 * beta + 4 * i + u)) << 16);
+    }
     if (R < t0 || R + 64 > t1) {  // ragged first or last round of the split
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -632,12 +642,12 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   int cur = wave;
   while (cur < nrounds) {
     const int nxt = claim();
-    if (nxt < nrounds) load_round(R0 + 64 * nxt, kwb[1], vwb[1]);
-    process_round(R0 + 64 * cur, kwb[0], vwb[0]);
+    if (nxt < nrounds) load_round(R0 + 64 * nxt, kwb[1], vwb[1], ksb[1]);
+    process_round(R0 + 64 * cur, kwb[0], vwb[0], ksb[0]);
     if (nxt >= nrounds) break;
     const int nxt2 = claim();
-    if (nxt2 < nrounds) load_round(R0 + 64 * nxt2, kwb[0], vwb[0]);
-    process_round(R0 + 64 * nxt, kwb[1], vwb[1]);
+    if (nxt2 < nrounds) load_round(R0 + 64 * nxt2, kwb[0], vwb[0], ksb[0]);
+    process_round(R0 + 64 * nxt, kwb[1], vwb[1], ksb[1]);
     cur = nxt2;
   }
 
@@ -947,8 +957,9 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
 // partial to the exchange and counts its arrival; the last one combines.
 // The arrival counters live in the workspace and the last split resets its
 // counter to 0, so a decode step is a single launch.
-template <int WAVES, bool APPEND>
+template <int WAVES, bool APPEND, bool KS>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
+  static_assert(!(APPEND && KS), "the fused step serves the plain format only");
   static_assert(WAVES == 12, "the exchange roles assume 12 waves");
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES, APPEND>()];
   const int tid = threadIdx.x;
@@ -979,7 +990,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   }
 
   float4 tv[8];
-  split_pass<WAVES, APPEND>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
+  split_pass<WAVES, APPEND, KS>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
   int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
   __syncthreads();  // the split's partial and its blocks of the new token are in LDS; the count is known
   if (a.n_split > 1) {
@@ -1046,10 +1057,13 @@ int plan_b_chunk(int batch, int num_kv_heads, int n_split) {
 hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream) {
   constexpr int W = 12;
   const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
+  if (a.append && a.k_scales) return hipErrorInvalidValue;
   if (a.append)
-    decode_lut_d128<W, true><<<grid, dim3(W * 64), 0, stream>>>(a);
+    decode_lut_d128<W, true, false><<<grid, dim3(W * 64), 0, stream>>>(a);
+  else if (a.k_scales)
+    decode_lut_d128<W, false, true><<<grid, dim3(W * 64), 0, stream>>>(a);
   else
-    decode_lut_d128<W, false><<<grid, dim3(W * 64), 0, stream>>>(a);
+    decode_lut_d128<W, false, false><<<grid, dim3(W * 64), 0, stream>>>(a);
   return hipGetLastError();
 }
 

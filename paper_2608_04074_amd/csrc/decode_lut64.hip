@@ -81,7 +81,7 @@ __device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, 
   }
 }
 
-template <int WAVES>
+template <int WAVES, bool KS>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int t0, const int t1, const size_t row0, float4 (&tv)[4]) {
   const uint32_t sbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8_ptr)smem));
@@ -123,11 +123,16 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   // Code bytes of one round, per half h: K dwords kw[4h + r] (bytes 4jj..4jj+3
   // of tokens R + 32h + 8r + 2rho + tq) and V dwords vw[2h + s] (bytes
   // 4a2..4a2+3 of tokens R + 32h + 8rho + 2jj + s).
-  auto load_round = [&](int R, uint32_t *kw, uint32_t *vw) {
+  // Key-scale format: lane l also loads the stored scale of token R + l,
+  // issued after the code bytes.
+  auto load_round = [&](int R, uint32_t *kw, uint32_t *vw, uint32_t &ks) {
+    size_t sub[4];  // uniform: byte offsets of the round's four sub-tiles
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const size_t s0 = subtile_offset(a, b, kv, min(R + 32 * h, last16), bs_shift);
       const size_t s1 = subtile_offset(a, b, kv, min(R + 32 * h + 16, last16), bs_shift);
+      sub[2 * h] = s0;
+      sub[2 * h + 1] = s1;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const uint8_t *kb = kpool + (r < 2 ? s0 : s1);
@@ -137,11 +142,16 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
       for (int s = 0; s < 2; ++s) vw[2 * h + s] = *reinterpret_cast<const uint32_t *>(vb + voff + 16 * s);
     }
+    if constexpr (KS) {
+      const int st = lane >> 4;
+      const size_t sl = st == 0 ? sub[0] : (st == 1 ? sub[1] : (st == 2 ? sub[2] : sub[3]));
+      ks = a.k_scales[sl / kL + (lane & 15)];
+    }
   };
-  uint32_t kwb[kBuf][8], vwb[kBuf][4];
+  uint32_t kwb[kBuf][8], vwb[kBuf][4], ksb[kBuf] = {};
 #pragma unroll
   for (int k = 0; k < kBuf - 1; ++k)
-    if (wave + k * WAVES < nrounds) load_round(R0 + kRound * (wave + k * WAVES), kwb[k], vwb[k]);
+    if (wave + k * WAVES < nrounds) load_round(R0 + kRound * (wave + k * WAVES), kwb[k], vwb[k], ksb[k]);
 
   // ---- setup: query transform, sink shifts, value codebook into LDS, table via MFMA
   {
@@ -294,7 +304,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     asel[r] = half8_t{one, one, one, one, one, one, one, one};
   }
 
-  auto process_round = [&](const int R, const uint32_t *kw, const uint32_t *vw) {
+  auto process_round = [&](const int R, const uint32_t *kw, const uint32_t *vw, const uint32_t ks) {
     // K: both halves, four steps per token, pairs of steps per 16x16x32 MFMA
     uint32_t wr[8];
 #pragma unroll
@@ -319,6 +329,14 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     }
     // lane (tau, set, head): half h register i = token R + 32h + 8 tau + 2 i + set
     float z[8] = {kacc[0][0], kacc[0][1], kacc[0][2], kacc[0][3], kacc[1][0], kacc[1][1], kacc[1][2], kacc[1][3]};
+    if constexpr (KS) {
+      // the read path's per-token multiply: token R + l's scale is held by lane l
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int src = 32 * (i >> 2) + 8 * rho + 2 * (i & 3) + set;
+        z[i] *= __uint_as_float(static_cast<uint32_t>(__shfl(static_cast<int>(ks), src)) << 16);
+      }
+    }
     if (R < t0 || R + kRound > t1) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
@@ -368,8 +386,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       const int cur = rd + k * WAVES;
       if (cur >= nrounds) break;
       const int nxt = cur + (kBuf - 1) * WAVES;
-      if (nxt < nrounds) load_round(R0 + kRound * nxt, kwb[(k + kBuf - 1) % kBuf], vwb[(k + kBuf - 1) % kBuf]);
-      process_round(R0 + kRound * cur, kwb[k], vwb[k]);
+      if (nxt < nrounds)
+        load_round(R0 + kRound * nxt, kwb[(k + kBuf - 1) % kBuf], vwb[(k + kBuf - 1) % kBuf], ksb[(k + kBuf - 1) % kBuf]);
+      process_round(R0 + kRound * cur, kwb[k], vwb[k], ksb[k]);
     }
   }
   load_tv_rows(a, kv, tv);
@@ -532,7 +551,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
 // One workgroup per (sequence, KV head, split); the arrival protocol is the
 // one of the head_dim-128 kernel (relaxed agent-scope partials and counters,
 // the last split combines, a split finding all others arrived does not publish).
-template <int WAVES>
+template <int WAVES, bool KS>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
   const int tid = threadIdx.x;
@@ -551,7 +570,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
 
   float4 tv[4];
   if (active) {
-    split_pass<WAVES>(a, smem, b, kv, t0, t1, row0, tv);
+    split_pass<WAVES, KS>(a, smem, b, kv, t0, t1, row0, tv);
   } else {
     load_tv_rows(a, kv, tv);
   }
@@ -598,7 +617,10 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
 hipError_t launch_decode_lut64(const DecodeArgs &a, hipStream_t stream) {
   constexpr int W = 16;  // 4 waves per SIMD: the kernel fits in 128 VGPRs
   const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
-  decode_lut_d64<W><<<grid, dim3(W * 64), 0, stream>>>(a);
+  if (a.k_scales)
+    decode_lut_d64<W, true><<<grid, dim3(W * 64), 0, stream>>>(a);
+  else
+    decode_lut_d64<W, false><<<grid, dim3(W * 64), 0, stream>>>(a);
   return hipGetLastError();
 }
 

@@ -47,14 +47,42 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
     sc.xs[tid] = x;
   }
   __syncthreads();
-  encblk::partial_block<D>(tid, sc, trow);
-  __syncthreads();
-  const int code = encblk::search_block<D>(tid, sc, cw);
-  if ((tid & 31) == 0) {
-    const int pos = a.start_pos[b] + a.start_offset + t;
-    pool[code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos) + encblk::kGroups * blk + (tid >> 5)] =
-        static_cast<uint8_t>(code);
+  const int pos = a.start_pos[b] + a.start_offset + t;
+  const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos);
+  int code;
+  if (side == 0 && a.k_scales) {
+    // Key-scale format: rho needs every coefficient of the key, so the
+    // workgroup forms all NB blocks' coefficients (the same computation as
+    // the block's own), keeps them in LDS, and searches its block with the
+    // coefficients divided by rho; block 0's workgroup stores rho.
+    __shared__ double us[D];
+    __shared__ double srho;
+#pragma unroll 1
+    for (int bb = 0; bb < NB; ++bb) {
+      float4 tb[D / 32];
+      encblk::load_rows<D>(tid, tm, bb, tb);
+      encblk::partial_block<D>(tid, sc, tb);
+      __syncthreads();
+      if (tid < encblk::kCols) us[encblk::kCols * bb + tid] = encblk::coefficient<D>(sc, tid);
+      __syncthreads();
+    }
+    if (tid == 0) srho = encblk::key_scale<D>(us);
+    __syncthreads();
+    const double rho = srho;
+    double uu[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const double u = us[encblk::kCols * blk + 4 * (tid >> 5) + i];
+      uu[i] = rho > 0.0 ? u / rho : 0.0;
+    }
+    code = encblk::search_codes(tid, uu, cw);
+    if (blk == 0 && tid == 0) a.k_scales[off / L] = encblk::bf16_of(rho);
+  } else {
+    encblk::partial_block<D>(tid, sc, trow);
+    __syncthreads();
+    code = encblk::search_block<D>(tid, sc, cw);
   }
+  if ((tid & 31) == 0) pool[off + encblk::kGroups * blk + (tid >> 5)] = static_cast<uint8_t>(code);
 }
 
 // Bulk append: one workgroup (4 waves) per (32-token tile, KV head, sequence,
@@ -136,6 +164,28 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) xs[(16 * tt + 4 * i + q) * RS + 16 * (wave * OPW + j) + m] = acc[tt][j][i];
   __syncthreads();
+
+  if (side == 0 && a.k_scales) {
+    // Key-scale format: rho of each key from its D coefficients, stored as
+    // bf16, then the coefficients divided by it (0 when rho = 0).
+    __shared__ double rhos[TT];
+    if (tid < TT) {
+      const double rho = encblk::key_scale<D>(&xs[tid * RS]);
+      rhos[tid] = rho;
+      if (tid < nt) {
+        const size_t off =
+            code_row_offset(a.layout, a.num_kv_heads, L, b, kv, a.start_pos[b] + a.start_offset + n0 + tid);
+        a.k_scales[off / L] = encblk::bf16_of(rho);
+      }
+    }
+    __syncthreads();
+    for (int i = tid; i < TT * D; i += 256) {
+      const int t = i / D, d = i % D;
+      const double rho = rhos[t];
+      xs[t * RS + d] = rho > 0.0 ? xs[t * RS + d] / rho : 0.0;
+    }
+    __syncthreads();
+  }
 
   // ---- nearest codeword: wave w takes groups w, w+4, ...
   for (int g = wave; g < L; g += 4) {

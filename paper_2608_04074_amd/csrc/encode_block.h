@@ -87,19 +87,11 @@ __device__ __forceinline__ void partial_block(const int t, Scratch<D> &s, const 
   }
 }
 
-// Phase 3 (after the partials are in LDS): nearest codeword of group t >> 5,
-// returned in all 32 lanes of the group.  The group's four coefficients are
-// the sums of the 4 waves' partials, added in wave order.
-template <int D>
-__device__ __forceinline__ int search_block(const int t, const Scratch<D> &s, const uint2 (&cw)[kPer]) {
-  const int gl = t >> 5, r = t & 31;
-  double uu[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = gl * 4 + i;
-    uu[i] = ((s.wpart[0][c] + s.wpart[1][c]) + s.wpart[2][c]) + s.wpart[3][c];
-  }
-  const double u0 = uu[0], u1 = uu[1], u2 = uu[2], u3 = uu[3];
+// Nearest codeword of group t >> 5 to the coefficients u, returned in all 32
+// lanes of the group: fp64 distances, the smallest index among equal ones.
+__device__ __forceinline__ int search_codes(const int t, const double (&u)[4], const uint2 (&cw)[kPer]) {
+  const int r = t & 31;
+  const double u0 = u[0], u1 = u[1], u2 = u[2], u3 = u[3];
   double best = INFINITY;
   int arg = 0;
 #pragma unroll
@@ -130,6 +122,41 @@ __device__ __forceinline__ int search_block(const int t, const Scratch<D> &s, co
     }
   }
   return arg;
+}
+
+// Column c of the block: the 4 waves' partials added in wave order.
+template <int D>
+__device__ __forceinline__ double coefficient(const Scratch<D> &s, const int c) {
+  return ((s.wpart[0][c] + s.wpart[1][c]) + s.wpart[2][c]) + s.wpart[3][c];
+}
+
+// Phase 3 (after the partials are in LDS): nearest codeword of group t >> 5,
+// returned in all 32 lanes of the group.
+template <int D>
+__device__ __forceinline__ int search_block(const int t, const Scratch<D> &s, const uint2 (&cw)[kPer]) {
+  const int gl = t >> 5;
+  double uu[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) uu[i] = coefficient<D>(s, gl * 4 + i);
+  return search_codes(t, uu, cw);
+}
+
+// Key-scale format: rho = sqrt(sum of the squared coefficients, added in
+// coordinate order) / sqrt(D), each square rounded before it is added.
+template <int D>
+__device__ __forceinline__ double key_scale(const double *u) {
+  double s = 0.0;
+  for (int i = 0; i < D; ++i) {
+#pragma clang fp contract(off)
+    s = s + u[i] * u[i];
+  }
+  return sqrt(s) / sqrt(static_cast<double>(D));
+}
+
+// bf16 bit pattern of rho: rounded to fp32, then to bf16, each to nearest even.
+__device__ __forceinline__ uint16_t bf16_of(const double x) {
+  const uint32_t f = __float_as_uint(static_cast<float>(x));
+  return static_cast<uint16_t>((f + 0x7fffu + ((f >> 16) & 1u)) >> 16);
 }
 
 }  // namespace encblk

@@ -36,6 +36,7 @@ struct DecodeArgs {
   const void *q;
   int q_bf16;
   const uint8_t *k_codes, *v_codes;
+  const uint16_t *k_scales;  // key-scale format: bf16 per-token key scales (pool layout), else nullptr
   const int32_t *seq_lens;
   int max_seq_len, window;
   const float *sinks;
@@ -81,6 +82,7 @@ struct EncodeArgs {
   const int32_t *start_pos;
   int start_offset;  // the first new token of sequence b goes to start_pos[b] + start_offset
   uint8_t *k_codes, *v_codes;
+  uint16_t *k_scales;  // key-scale format: bf16 per-token key scales (pool layout), else nullptr
 };
 
 // Split plan and workspace carve-out of the decode path.

@@ -51,22 +51,22 @@ def _layout(**kw):
 
 def _decode(p, lay, **kw):
     a = dict(q=0x7000, q_dtype=nat.NOVA_KV_BF16, batch=2, hq=32, k=0x8000, v=0x9000, seq=0xA000,
-             max_seq=4096, window=0, sinks=None, scale=0.0, out=0xB000, ws=None, ws_bytes=0)
+             max_seq=4096, window=0, sinks=None, scale=0.0, out=0xB000, ws=None, ws_bytes=0, ks=None)
     a.update(kw)
     return nat.lib().nova_kv_decode_attn(
         ctypes.byref(p) if p is not None else None, ctypes.byref(lay) if lay is not None else None,
-        a["q"], a["q_dtype"], a["batch"], a["hq"], a["k"], a["v"], a["seq"], a["max_seq"],
+        a["q"], a["q_dtype"], a["batch"], a["hq"], a["k"], a["v"], a["ks"], a["seq"], a["max_seq"],
         a["window"], a["sinks"], a["scale"], a["out"], a["ws"], a["ws_bytes"], None)
 
 
 def _encode(p, lay, **kw):
     a = dict(k=0x7000, v=0x7800, dtype=nat.NOVA_KV_BF16, batch=2, n_new=16, start=0xA000,
-             kc=0x8000, vc=0x9000)
+             kc=0x8000, vc=0x9000, ks=None)
     a.update(kw)
     return nat.lib().nova_kv_encode(ctypes.byref(p) if p is not None else None,
                                     ctypes.byref(lay) if lay is not None else None,
                                     a["k"], a["v"], a["dtype"], a["batch"], a["n_new"], a["start"],
-                                    a["kc"], a["vc"], None)
+                                    a["kc"], a["vc"], a["ks"], None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -74,7 +74,8 @@ def _encode(p, lay, **kw):
     (dict(codebook_size=16), nat.NOVA_KV_ERR_UNSUPPORTED),
     (dict(head_dim=96), nat.NOVA_KV_ERR_UNSUPPORTED),
     (dict(head_dim=130), nat.NOVA_KV_ERR_INVALID_ARG),
-    (dict(flags=1), nat.NOVA_KV_ERR_UNSUPPORTED),
+    (dict(flags=2), nat.NOVA_KV_ERR_UNSUPPORTED),
+    (dict(flags=3), nat.NOVA_KV_ERR_UNSUPPORTED),
     (dict(num_kv_heads=0), nat.NOVA_KV_ERR_INVALID_ARG),
     (dict(cb_k=None), nat.NOVA_KV_ERR_INVALID_ARG),
     (dict(cb_v=0x6001), nat.NOVA_KV_ERR_INVALID_ARG),
@@ -145,3 +146,37 @@ def test_encode_needs_forward_transforms_and_noops():
     assert _encode(_params(t_k=None), _layout()) == nat.NOVA_KV_ERR_INVALID_ARG
     assert _encode(_params(), _layout(), n_new=0, k=None) == nat.NOVA_KV_OK
     assert _encode(_params(), _layout(), batch=0, k=None) == nat.NOVA_KV_OK
+
+
+def _append(p, lay, **kw):
+    a = dict(kn=0x7000, vn=0x7800, new_dtype=nat.NOVA_KV_BF16, q=0x7400, q_dtype=nat.NOVA_KV_BF16,
+             batch=2, hq=32, k=0x8000, v=0x9000, ks=None, seq=0xA000, max_seq=4096, window=0,
+             sinks=None, scale=0.0, out=0xB000, ws=None, ws_bytes=0)
+    a.update(kw)
+    return nat.lib().nova_kv_append_decode_attn(
+        ctypes.byref(p), ctypes.byref(lay), a["kn"], a["vn"], a["new_dtype"], a["q"], a["q_dtype"],
+        a["batch"], a["hq"], a["k"], a["v"], a["ks"], a["seq"], a["max_seq"], a["window"], a["sinks"],
+        a["scale"], a["out"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("call", [_decode, _encode, _append])
+def test_key_scale_format_needs_an_aligned_scale_pool(call):
+    p = _params(flags=nat.NOVA_KV_KEY_SCALE)
+    assert call(p, _layout()) == nat.NOVA_KV_ERR_INVALID_ARG
+    assert b"k_scales" in nat.lib().nova_kv_last_error()
+    assert call(p, _layout(), ks=0xC001) == nat.NOVA_KV_ERR_INVALID_ARG
+    # with a scale pool the checks go on to the next argument (no workspace;
+    # for the encode a NULL input, so that nothing is launched)
+    if call is _encode:
+        assert call(p, _layout(), ks=0xC000, k=None) == nat.NOVA_KV_ERR_INVALID_ARG
+        assert b"k_scales" not in nat.lib().nova_kv_last_error()
+    else:
+        assert call(p, _layout(), ks=0xC000) == nat.NOVA_KV_ERR_WORKSPACE
+        # the plain format ignores the pointer
+        assert call(_params(), _layout(), ks=0xC001) == nat.NOVA_KV_ERR_WORKSPACE
+    # batch 0 stays a no-op
+    assert call(p, _layout(), batch=0, q=None, out=None) == nat.NOVA_KV_OK
+
+
+def test_append_rejects_bad_new_dtype():
+    assert _append(_params(), _layout(), new_dtype=9) == nat.NOVA_KV_ERR_INVALID_ARG
