@@ -20,6 +20,15 @@ scale): the reconstructed key is k_hat = rho * Q(r/rho) R_K^{-1} + k_bar with
 the stored (bf16) rho, so the logit of a token is rho times the logit of its
 normalized code.
 
+Sink-plus-recent band (Sec. "Sink-plus-recent band"; Fig. "Cache layout at
+decoding position t"): the first n_sink and the most recent n_rec cached
+positions are held exactly (BF16) instead of quantized; the attention runs
+over all attended positions at once, band positions with their BF16 keys and
+values, the others reconstructed from codes.  Readings: "most recent" is
+positions [S - n_rec, S) of a sequence of S cached tokens; the band applies
+inside the attended range (a window may cut it); band keys enter the logit as
+they are (no k_bar shift in the plain form, which holds no shift at all).
+
 Fast form -- for self-consistency only (Algorithm 1 inference step; Sec.
 "Decoding kernel and read path"; sinks appendix): q' = q R_K^{-T} * scale,
 logit = q' . r_hat (k_bar dropped, Lemma S1), sink shifted by -(q . k_bar) * scale,
@@ -39,6 +48,25 @@ from .vq import lookup
 def attended_range(seq_len: int, window: int):
     lo = max(0, seq_len - window) if window > 0 else 0
     return lo, seq_len
+
+
+def band_mask(seq_len: int, n_sink: int, n_rec: int) -> np.ndarray:
+    """Positions of a sequence of seq_len tokens held exactly: t < n_sink or t >= seq_len - n_rec."""
+    t = np.arange(seq_len)
+    return (t < n_sink) | (t >= seq_len - n_rec)
+
+
+def _with_band(k_hat, v_hat, lo, hi, band):
+    """Replace the band positions of the attended rows [lo, hi) by their exact rows."""
+    if band is None:
+        return k_hat, v_hat
+    n_sink, n_rec, k_exact, v_exact = band
+    m = band_mask(hi, n_sink, n_rec)[lo:hi]
+    k_hat = k_hat.copy()
+    v_hat = v_hat.copy()
+    k_hat[m] = np.asarray(k_exact, dtype=np.float64)[lo:hi][m]
+    v_hat[m] = np.asarray(v_exact, dtype=np.float64)[lo:hi][m]
+    return k_hat, v_hat
 
 
 def reconstruct_keys(codes_k: np.ndarray, cb_k: np.ndarray, t_k_inv_t: np.ndarray,
@@ -75,25 +103,30 @@ def softmax_attention(q: np.ndarray, keys: np.ndarray, values: np.ndarray, scale
 
 def decode_row(q: np.ndarray, codes_k: np.ndarray, codes_v: np.ndarray, params_head: dict,
                scale: float, window: int = 0, sink: Optional[float] = None,
-               scales_k: Optional[np.ndarray] = None) -> np.ndarray:
+               scales_k: Optional[np.ndarray] = None, band=None) -> np.ndarray:
     """Plain-form output of one query head over one sequence's cached codes (S, L);
-    scales_k (S,) are the stored per-token key scales of the key-scale format."""
+    scales_k (S,) are the stored per-token key scales of the key-scale format;
+    band = (n_sink, n_rec, k_exact (S, D), v_exact (S, D)) holds the exact
+    rows of the sink-plus-recent band (rows outside it are not read)."""
     lo, hi = attended_range(codes_k.shape[0], window)
     k_hat = reconstruct_keys(codes_k[lo:hi], params_head["cb_k"], params_head["t_k_inv_t"],
                              params_head["kbar"], None if scales_k is None else scales_k[lo:hi])
     v_hat = reconstruct_values(codes_v[lo:hi], params_head["cb_v"], params_head["t_v"])
+    k_hat, v_hat = _with_band(k_hat, v_hat, lo, hi, band)
     return softmax_attention(q, k_hat, v_hat, scale, sink)
 
 
 def decode_rows(q_heads: np.ndarray, codes_k: np.ndarray, codes_v: np.ndarray,
                 params_head: dict, scale: float, window: int = 0,
                 sinks: Optional[Sequence[float]] = None,
-                scales_k: Optional[np.ndarray] = None) -> np.ndarray:
-    """Plain-form outputs of the G query heads sharing one KV head: q_heads (G, D) -> (G, D)."""
+                scales_k: Optional[np.ndarray] = None, band=None) -> np.ndarray:
+    """Plain-form outputs of the G query heads sharing one KV head: q_heads (G, D) -> (G, D).
+    band as in decode_row."""
     lo, hi = attended_range(codes_k.shape[0], window)
     k_hat = reconstruct_keys(codes_k[lo:hi], params_head["cb_k"], params_head["t_k_inv_t"],
                              params_head["kbar"], None if scales_k is None else scales_k[lo:hi])
     v_hat = reconstruct_values(codes_v[lo:hi], params_head["cb_v"], params_head["t_v"])
+    k_hat, v_hat = _with_band(k_hat, v_hat, lo, hi, band)
     out = np.empty((q_heads.shape[0], v_hat.shape[1]))
     for h in range(q_heads.shape[0]):
         out[h] = softmax_attention(q_heads[h], k_hat, v_hat, scale,

@@ -55,6 +55,11 @@ def bf16_value(bits: np.ndarray) -> np.ndarray:
     return (np.asarray(bits, dtype=np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
+def band_values(x: np.ndarray) -> np.ndarray:
+    """Exact rows of the sink-plus-recent band: the inputs as stored in BF16 (fp64 values)."""
+    return bf16_value(bf16_bits(x))
+
+
 def normalized_key_coefficients(r: np.ndarray):
     """(r / rho, rho) with rows of r = 0 mapped to (0, 0)."""
     rho = key_scale(r)
