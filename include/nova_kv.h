@@ -123,6 +123,36 @@ typedef struct {
 } nova_kv_layout;
 
 /*
+ * Sink-plus-recent band (paper: Sec. "Sink-plus-recent band" and the figure
+ * of the cache layout at decoding position t): the first n_sink and the most
+ * recent n_rec positions of every sequence are held in BF16 and attended with
+ * their exact keys and values; the positions in between are read from the
+ * code pools.  With S cached tokens the band is positions [0, n_sink) and
+ * [max(n_sink, S - n_rec), S) (inside the attended range).
+ *
+ *   n_sink, n_rec  >= 0, n_sink + n_rec in [1, NOVA_KV_MAX_BAND]
+ *   k, v      uint16 bf16 bit patterns [B][Hkv][n_sink + n_rec][D], device,
+ *             16-byte aligned; b is the sequence index of the call.  Position
+ *             p sits in slot p when p < n_sink, else in slot
+ *             n_sink + (p mod n_rec) (a ring holding the last n_rec positions).
+ *
+ * Calls take a `const nova_kv_band *` (NULL = no band).  nova_kv_encode writes
+ * the band rows of the new tokens that are in the band once the append is
+ * done (p < n_sink, or p >= start_pos[b] + n_new - n_rec) and, as without a
+ * band, the codes of every new token, so a position that leaves the recent
+ * band is read from codes written when it was appended.  Inputs in fp32 are
+ * rounded to bf16 (to nearest even) for the band.
+ */
+#define NOVA_KV_MAX_BAND 1024
+
+typedef struct {
+    int32_t n_sink;
+    int32_t n_rec;
+    uint16_t *k;
+    uint16_t *v;
+} nova_kv_band;
+
+/*
  * nova_kv_encode -- append n_new tokens per sequence to the code pools.
  *
  * Paper: Algorithm 1 ("Write": cache Q+((k_j - k_bar) R_K)); Theorem 1
@@ -139,6 +169,8 @@ typedef struct {
  *              pool, uint16 bf16 bit patterns [num_blocks][Hkv][block_size]
  *              addressed like the code pools (one scale per token-head),
  *              2-byte aligned, written at the same positions.
+ *   band       NULL, or the sink-plus-recent band: the new tokens that are in
+ *              it after the append are also written there (bf16).
  *
  * For every (b, token, KV head, group l) the stored byte is the smallest index
  * c minimising sum_i (u_i - cb[l][c][i])^2, u the group's coefficients; the
@@ -152,7 +184,7 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
                               const void *k, const void *v, nova_kv_dtype in_dtype,
                               int32_t batch, int32_t n_new, const int32_t *start_pos,
                               uint8_t *k_codes, uint8_t *v_codes, uint16_t *k_scales,
-                              void *hip_stream);
+                              const nova_kv_band *band, void *hip_stream);
 
 /*
  * Bytes of device workspace nova_kv_decode_attn needs for this shape (split
@@ -175,6 +207,9 @@ size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch,
  *              reads KV head h / (Hq / Hkv).
  *   k_scales   key-scale format only (else ignored, may be NULL): the scale
  *              pool of nova_kv_encode, read at the attended positions.
+ *   band       NULL, or the sink-plus-recent band: its attended positions
+ *              are read from it (exact bf16 keys and values, key scales
+ *              unused), the other attended positions from the pools.
  *   seq_lens   [B] int32 device: cached tokens of each sequence (the current
  *              token already appended); precondition 0 <= seq_lens[b] <= max_seq_len.
  *   max_seq_len  host upper bound of seq_lens; must not exceed the layout's
@@ -201,7 +236,7 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
                                    const void *q, nova_kv_dtype q_dtype,
                                    int32_t batch, int32_t num_q_heads,
                                    const uint8_t *k_codes, const uint8_t *v_codes,
-                                   const uint16_t *k_scales,
+                                   const uint16_t *k_scales, const nova_kv_band *band,
                                    const int32_t *seq_lens, int32_t max_seq_len,
                                    int32_t window, const float *sinks, float softmax_scale,
                                    float *out, void *workspace, size_t workspace_bytes,
@@ -219,8 +254,8 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
  *   k_new, v_new  [B][Hkv][D] device, dtype new_dtype (F32 or BF16): the token
  *              at position seq_lens[b] - 1 of each sequence (the newest cached
  *              token); precondition seq_lens[b] >= 1.
- *   k_codes, v_codes (and k_scales in the key-scale format)  the pools,
- *              written at position seq_lens[b] - 1 exactly as
+ *   k_codes, v_codes (and k_scales in the key-scale format, band when
+ *              given)  written at position seq_lens[b] - 1 exactly as
  *              nova_kv_encode(n_new = 1, start_pos = seq_lens - 1) writes them
  *              (same bytes); nothing else is touched.
  *   all other arguments as in nova_kv_decode_attn (params also need t_k).
@@ -228,7 +263,7 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
  * out equals the output of nova_kv_decode_attn over the pools after that
  * append, up to fp32 rounding (the new token's term is added after the
  * split combine instead of inside a split).  With head_dim 128 on 16-aligned
- * blocks (and not the key-scale format) the step is a single kernel launch,
+ * blocks (not the key-scale format, no band) the step is a single kernel launch,
  * in which the workgroups that read the pools also encode the new token;
  * otherwise the one-token encode and the decode run one after the other on
  * the stream.
@@ -239,6 +274,7 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
                                           const void *q, nova_kv_dtype q_dtype,
                                           int32_t batch, int32_t num_q_heads,
                                           uint8_t *k_codes, uint8_t *v_codes, uint16_t *k_scales,
+                                          const nova_kv_band *band,
                                           const int32_t *seq_lens, int32_t max_seq_len,
                                           int32_t window, const float *sinks, float softmax_scale,
                                           float *out, void *workspace, size_t workspace_bytes,

@@ -57,6 +57,18 @@ class Layout(ctypes.Structure):
     ]
 
 
+class Band(ctypes.Structure):
+    _fields_ = [
+        ("n_sink", ctypes.c_int32),
+        ("n_rec", ctypes.c_int32),
+        ("k", ctypes.c_void_p),
+        ("v", ctypes.c_void_p),
+    ]
+
+
+NOVA_KV_MAX_BAND = 1024
+
+
 class NovaKVError(RuntimeError):
     def __init__(self, status: int, detail: str):
         super().__init__(f"nova_kv status {status}: {detail}")
@@ -75,28 +87,27 @@ def lib() -> ctypes.CDLL:
                                "paper_2608_04074_amd.build` (or __graft_entry__.build())")
         L = ctypes.CDLL(LIB_PATH)
         P = ctypes.POINTER
+        vp, i32 = ctypes.c_void_p, ctypes.c_int32
         L.nova_kv_encode.restype = ctypes.c_int
-        L.nova_kv_encode.argtypes = [P(Params), P(Layout), ctypes.c_void_p, ctypes.c_void_p,
-                                     ctypes.c_int, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        # (params, layout, k, v, in_dtype, batch, n_new, start_pos, k_codes, v_codes,
+        #  k_scales, band, stream)
+        L.nova_kv_encode.argtypes = [P(Params), P(Layout), vp, vp, ctypes.c_int, i32, i32, vp,
+                                     vp, vp, vp, P(Band), vp]
         L.nova_kv_decode_workspace_bytes.restype = ctypes.c_size_t
-        L.nova_kv_decode_workspace_bytes.argtypes = [P(Params), ctypes.c_int32, ctypes.c_int32,
-                                                     ctypes.c_int32]
+        L.nova_kv_decode_workspace_bytes.argtypes = [P(Params), i32, i32, i32]
         L.nova_kv_decode_attn.restype = ctypes.c_int
-        L.nova_kv_decode_attn.argtypes = [P(Params), P(Layout), ctypes.c_void_p, ctypes.c_int,
-                                          ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
-                                          ctypes.c_int32, ctypes.c_void_p, ctypes.c_float,
-                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
-                                          ctypes.c_void_p]
+        # (params, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales, band,
+        #  seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace, bytes, stream)
+        L.nova_kv_decode_attn.argtypes = [P(Params), P(Layout), vp, ctypes.c_int, i32, i32, vp, vp, vp,
+                                          P(Band), vp, i32, i32, vp, ctypes.c_float, vp, vp,
+                                          ctypes.c_size_t, vp]
         L.nova_kv_append_decode_attn.restype = ctypes.c_int
-        L.nova_kv_append_decode_attn.argtypes = [P(Params), P(Layout), ctypes.c_void_p, ctypes.c_void_p,
-                                                 ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
-                                                 ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
-                                                 ctypes.c_int32, ctypes.c_void_p, ctypes.c_float,
-                                                 ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
-                                                 ctypes.c_void_p]
+        # (params, layout, k_new, v_new, new_dtype, q, q_dtype, batch, num_q_heads, k_codes,
+        #  v_codes, k_scales, band, seq_lens, max_seq_len, window, sinks, softmax_scale, out,
+        #  workspace, bytes, stream)
+        L.nova_kv_append_decode_attn.argtypes = [P(Params), P(Layout), vp, vp, ctypes.c_int, vp,
+                                                 ctypes.c_int, i32, i32, vp, vp, vp, P(Band), vp, i32,
+                                                 i32, vp, ctypes.c_float, vp, vp, ctypes.c_size_t, vp]
         L.nova_kv_status_string.restype = ctypes.c_char_p
         L.nova_kv_status_string.argtypes = [ctypes.c_int]
         L.nova_kv_last_error.restype = ctypes.c_char_p

@@ -14,7 +14,7 @@ import torch
 
 from . import _native as nat
 
-__all__ = ["NovaKVParams", "CacheLayout", "encode", "decode_attn", "append_decode_attn",
+__all__ = ["NovaKVParams", "CacheLayout", "Band", "band_shape", "encode", "decode_attn", "append_decode_attn",
            "decode_workspace_bytes", "code_pool_shape", "scale_pool_shape", "prepare_encode",
            "prepare_decode", "prepare_append_decode"]
 
@@ -130,6 +130,44 @@ def _scales_ptr(params: NovaKVParams, k_scales: Optional[torch.Tensor], k_codes:
     return k_scales.data_ptr()
 
 
+def band_shape(params: NovaKVParams, batch: int, n_sink: int, n_rec: int):
+    """Shape of each sink-plus-recent band buffer: [B][Hkv][n_sink + n_rec][D]."""
+    return (batch, params.num_kv_heads, n_sink + n_rec, params.head_dim)
+
+
+class Band:
+    """Sink-plus-recent band (see nova_kv_band): the first n_sink and the last
+    n_rec positions of every sequence held in bf16 in ``k`` and ``v``
+    ([B][Hkv][n_sink + n_rec][D], bfloat16 or 16-bit integer bit patterns);
+    position p sits in slot p < n_sink, else n_sink + p % n_rec."""
+
+    def __init__(self, n_sink: int, n_rec: int, k: torch.Tensor, v: torch.Tensor):
+        if n_sink < 0 or n_rec < 0 or not 1 <= n_sink + n_rec <= nat.NOVA_KV_MAX_BAND:
+            raise ValueError(f"band sizes ({n_sink}, {n_rec}) outside 1 .. {nat.NOVA_KV_MAX_BAND} positions")
+        _require(k, "band k", _SCALE_DTYPES)
+        _require(v, "band v", (k.dtype,), k.numel())
+        if k.dim() != 4 or k.shape[2] != n_sink + n_rec:
+            raise ValueError("band buffers must be [B][Hkv][n_sink + n_rec][D]")
+        self.n_sink, self.n_rec, self.k, self.v = n_sink, n_rec, k, v
+        self._c = nat.Band(n_sink, n_rec, k.data_ptr(), v.data_ptr())
+
+    def check(self, params: NovaKVParams, batch: int) -> None:
+        if tuple(self.k.shape) != band_shape(params, batch, self.n_sink, self.n_rec):
+            raise ValueError(f"band buffers of shape {tuple(self.k.shape)}, expected "
+                             f"{band_shape(params, batch, self.n_sink, self.n_rec)}")
+
+    @property
+    def c(self) -> nat.Band:
+        return self._c
+
+
+def _band_ref(band: Optional[Band], params: NovaKVParams, batch: int):
+    if band is None:
+        return None
+    band.check(params, batch)
+    return ctypes.byref(band.c)
+
+
 def _dtype_code(t: torch.Tensor) -> int:
     if t.dtype == torch.float32:
         return nat.NOVA_KV_F32
@@ -140,7 +178,8 @@ def _dtype_code(t: torch.Tensor) -> int:
 
 def encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v: torch.Tensor,
            start_pos: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
-           stream: Optional[torch.cuda.Stream] = None, k_scales: Optional[torch.Tensor] = None) -> None:
+           stream: Optional[torch.cuda.Stream] = None, k_scales: Optional[torch.Tensor] = None,
+           band: Optional[Band] = None) -> None:
     """nova_kv_encode: k, v [B][n_new][Hkv][D] (fp32 or bf16), start_pos int32 [B]."""
     if k.dim() != 4:
         raise ValueError("k must be [B][n_new][Hkv][D]")
@@ -156,7 +195,7 @@ def encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v: torch.
     nat.check(nat.lib().nova_kv_encode(
         ctypes.byref(params.c), ctypes.byref(layout.c), k.data_ptr(), v.data_ptr(), _dtype_code(k),
         b, n_new, start_pos.data_ptr(), k_codes.data_ptr(), v_codes.data_ptr(), ks,
-        _stream_ptr(stream)))
+        _band_ref(band, params, b), _stream_ptr(stream)))
 
 
 def decode_workspace_bytes(params: NovaKVParams, batch: int, num_q_heads: int,
@@ -171,7 +210,7 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
                 softmax_scale: float = 0.0, out: Optional[torch.Tensor] = None,
                 workspace: Optional[torch.Tensor] = None,
                 stream: Optional[torch.cuda.Stream] = None,
-                k_scales: Optional[torch.Tensor] = None) -> torch.Tensor:
+                k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None) -> torch.Tensor:
     """nova_kv_decode_attn: q [B][Hq][D] (fp32 or bf16) -> out [B][Hq][D] fp32.
 
     A caller-provided workspace must be zero-filled before its first use; each
@@ -196,14 +235,15 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
     ks = _scales_ptr(params, k_scales, k_codes)
     nat.check(nat.lib().nova_kv_decode_attn(
         ctypes.byref(params.c), ctypes.byref(layout.c), q.data_ptr(), _dtype_code(q), b, hq,
-        k_codes.data_ptr(), v_codes.data_ptr(), ks, seq_lens.data_ptr(), max_seq_len, window,
+        k_codes.data_ptr(), v_codes.data_ptr(), ks, _band_ref(band, params, b), seq_lens.data_ptr(),
+        max_seq_len, window,
         sinks.data_ptr() if sinks is not None else None, float(softmax_scale), out.data_ptr(),
         workspace.data_ptr(), workspace.numel(), _stream_ptr(stream)))
     return out
 
 
 def _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
-                        workspace, window, sinks, softmax_scale, stream, k_scales):
+                        workspace, window, sinks, softmax_scale, stream, k_scales, band):
     if q.dim() != 3 or q.shape[2] != params.head_dim:
         raise ValueError("q must be [B][Hq][D]")
     b, hq, d = q.shape
@@ -224,7 +264,8 @@ def _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_l
     return (ctypes.byref(params.c), ctypes.byref(layout.c), vp(k_new.data_ptr()), vp(v_new.data_ptr()),
             ctypes.c_int(_dtype_code(k_new)), vp(q.data_ptr()), ctypes.c_int(_dtype_code(q)),
             ctypes.c_int32(b), ctypes.c_int32(hq), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()),
-            vp(ks), vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len), ctypes.c_int32(window),
+            vp(ks), _band_ref(band, params, b), vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len),
+            ctypes.c_int32(window),
             vp(sinks.data_ptr() if sinks is not None else None), ctypes.c_float(softmax_scale),
             vp(out.data_ptr()), vp(workspace.data_ptr()), ctypes.c_size_t(workspace.numel()),
             vp(_stream_ptr(stream)))
@@ -236,7 +277,7 @@ def append_decode_attn(params: NovaKVParams, layout: CacheLayout, k_new: torch.T
                        sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
                        out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
                        stream: Optional[torch.cuda.Stream] = None,
-                       k_scales: Optional[torch.Tensor] = None) -> torch.Tensor:
+                       k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None) -> torch.Tensor:
     """nova_kv_append_decode_attn: store the step's k_new, v_new [B][Hkv][D] at
     position seq_lens[b] - 1 of the pools, then decode q [B][Hq][D] over the
     cache including them -> out [B][Hq][D] fp32.  Workspace as in decode_attn."""
@@ -247,7 +288,7 @@ def append_decode_attn(params: NovaKVParams, layout: CacheLayout, k_new: torch.T
     if workspace is None:
         workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=q.device)
     args = _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
-                               workspace, window, sinks, softmax_scale, stream, k_scales)
+                               workspace, window, sinks, softmax_scale, stream, k_scales, band)
     nat.check(nat.lib().nova_kv_append_decode_attn(*args))
     return out
 
@@ -267,7 +308,7 @@ class PreparedCall:
 def prepare_encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v: torch.Tensor,
                    start_pos: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
                    stream: Optional[torch.cuda.Stream] = None,
-                   k_scales: Optional[torch.Tensor] = None) -> PreparedCall:
+                   k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None) -> PreparedCall:
     """nova_kv_encode with the arguments of encode(), marshalled once."""
     if k.dim() != 4:
         raise ValueError("k must be [B][n_new][Hkv][D]")
@@ -284,9 +325,9 @@ def prepare_encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v
     args = (ctypes.byref(params.c), ctypes.byref(layout.c), vp(k.data_ptr()), vp(v.data_ptr()),
             ctypes.c_int(_dtype_code(k)), ctypes.c_int32(b), ctypes.c_int32(n_new),
             vp(start_pos.data_ptr()), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()), vp(ks),
-            vp(_stream_ptr(stream)))
+            _band_ref(band, params, b), vp(_stream_ptr(stream)))
     return PreparedCall(nat.lib().nova_kv_encode, args,
-                        (params, layout, k, v, start_pos, k_codes, v_codes, k_scales))
+                        (params, layout, k, v, start_pos, k_codes, v_codes, k_scales, band))
 
 
 def prepare_decode(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
@@ -294,7 +335,7 @@ def prepare_decode(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
                    max_seq_len: int, out: torch.Tensor, workspace: torch.Tensor, window: int = 0,
                    sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
                    stream: Optional[torch.cuda.Stream] = None,
-                   k_scales: Optional[torch.Tensor] = None) -> PreparedCall:
+                   k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None) -> PreparedCall:
     """nova_kv_decode_attn with the arguments of decode_attn(), marshalled once
     (out and a zero-filled workspace are required here)."""
     if q.dim() != 3 or q.shape[2] != params.head_dim:
@@ -312,12 +353,13 @@ def prepare_decode(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
     vp = ctypes.c_void_p
     args = (ctypes.byref(params.c), ctypes.byref(layout.c), vp(q.data_ptr()), ctypes.c_int(_dtype_code(q)),
             ctypes.c_int32(b), ctypes.c_int32(hq), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()),
-            vp(ks), vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len), ctypes.c_int32(window),
+            vp(ks), _band_ref(band, params, b), vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len),
+            ctypes.c_int32(window),
             vp(sinks.data_ptr() if sinks is not None else None), ctypes.c_float(softmax_scale),
             vp(out.data_ptr()), vp(workspace.data_ptr()), ctypes.c_size_t(workspace.numel()),
             vp(_stream_ptr(stream)))
     return PreparedCall(nat.lib().nova_kv_decode_attn, args,
-                        (params, layout, q, k_codes, v_codes, seq_lens, sinks, out, workspace, k_scales))
+                        (params, layout, q, k_codes, v_codes, seq_lens, sinks, out, workspace, k_scales, band))
 
 
 def prepare_append_decode(params: NovaKVParams, layout: CacheLayout, k_new: torch.Tensor, v_new: torch.Tensor,
@@ -325,11 +367,11 @@ def prepare_append_decode(params: NovaKVParams, layout: CacheLayout, k_new: torc
                           seq_lens: torch.Tensor, max_seq_len: int, out: torch.Tensor, workspace: torch.Tensor,
                           window: int = 0, sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
                           stream: Optional[torch.cuda.Stream] = None,
-                          k_scales: Optional[torch.Tensor] = None) -> PreparedCall:
+                          k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None) -> PreparedCall:
     """nova_kv_append_decode_attn with the arguments of append_decode_attn(),
     marshalled once (out and a zero-filled workspace are required here)."""
     args = _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
-                               workspace, window, sinks, softmax_scale, stream, k_scales)
+                               workspace, window, sinks, softmax_scale, stream, k_scales, band)
     return PreparedCall(nat.lib().nova_kv_append_decode_attn, args,
                         (params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, sinks, out, workspace,
-                         k_scales))
+                         k_scales, band))

@@ -77,6 +77,19 @@ nova_kv_status check_scales(const nova_kv_params *p, const void *k_scales) {
   return NOVA_KV_OK;
 }
 
+// The sink-plus-recent band (NULL: none).
+nova_kv_status check_band(const nova_kv_band *band) {
+  if (!band) return NOVA_KV_OK;
+  if (band->n_sink < 0 || band->n_rec < 0) return fail(NOVA_KV_ERR_INVALID_ARG, "band sizes must be >= 0");
+  const long long nb = static_cast<long long>(band->n_sink) + band->n_rec;
+  if (nb < 1 || nb > NOVA_KV_MAX_BAND)
+    return fail(NOVA_KV_ERR_INVALID_ARG, "band of %lld positions (1 .. %d)", nb, NOVA_KV_MAX_BAND);
+  if (!band->k || !band->v) return fail(NOVA_KV_ERR_INVALID_ARG, "band k or v is NULL");
+  if (!aligned(band->k, 16) || !aligned(band->v, 16))
+    return fail(NOVA_KV_ERR_INVALID_ARG, "band buffers must be 16-byte aligned");
+  return NOVA_KV_OK;
+}
+
 novakv::CacheLayout to_layout(const nova_kv_layout *lay) {
   return novakv::CacheLayout{lay->block_size, lay->blocks_per_seq, lay->block_table};
 }
@@ -101,7 +114,8 @@ const char *nova_kv_last_error(void) { return g_last_error.c_str(); }
 nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *layout,
                               const void *k, const void *v, nova_kv_dtype in_dtype,
                               int32_t batch, int32_t n_new, const int32_t *start_pos,
-                              uint8_t *k_codes, uint8_t *v_codes, uint16_t *k_scales, void *hip_stream) {
+                              uint8_t *k_codes, uint8_t *v_codes, uint16_t *k_scales,
+                              const nova_kv_band *band, void *hip_stream) {
   nova_kv_status st = check_params(p, true, false);
   if (st != NOVA_KV_OK) return st;
   if ((st = check_layout(layout)) != NOVA_KV_OK) return st;
@@ -113,6 +127,7 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
     return fail(NOVA_KV_ERR_INVALID_ARG, "n_new exceeds the per-sequence capacity");
   if (batch == 0 || n_new == 0) return ok();
   if ((st = check_scales(p, k_scales)) != NOVA_KV_OK) return st;
+  if ((st = check_band(band)) != NOVA_KV_OK) return st;
   if (!k || !v || !start_pos || !k_codes || !v_codes)
     return fail(NOVA_KV_ERR_INVALID_ARG, "k, v, start_pos, k_codes or v_codes is NULL");
 
@@ -134,6 +149,12 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
   a.k_codes = k_codes;
   a.v_codes = v_codes;
   a.k_scales = (p->flags & NOVA_KV_KEY_SCALE) ? k_scales : nullptr;
+  if (band) {
+    a.n_sink = band->n_sink;
+    a.n_rec = band->n_rec;
+    a.band_k = band->k;
+    a.band_v = band->v;
+  }
   hipError_t e = novakv::launch_encode(a, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "encode launch: %s", hipGetErrorString(e));
   return ok();
@@ -152,8 +173,8 @@ namespace {
 // Host checks and argument set-up shared by the decode entry points.
 nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *layout, const void *q,
                               nova_kv_dtype q_dtype, int32_t batch, int32_t num_q_heads, const uint8_t *k_codes,
-                              const uint8_t *v_codes, const uint16_t *k_scales, const int32_t *seq_lens,
-                              int32_t max_seq_len,
+                              const uint8_t *v_codes, const uint16_t *k_scales, const nova_kv_band *band,
+                              const int32_t *seq_lens, int32_t max_seq_len,
                               int32_t window, const float *sinks, float softmax_scale, float *out,
                               void *workspace, size_t workspace_bytes, bool need_encode,
                               novakv::DecodeArgs &a, novakv::DecodePlan &plan) {
@@ -176,6 +197,7 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   if (!(softmax_scale >= 0.f)) return fail(NOVA_KV_ERR_INVALID_ARG, "softmax_scale must be >= 0");
   if (batch == 0) return NOVA_KV_OK;
   if ((st = check_scales(p, k_scales)) != NOVA_KV_OK) return st;
+  if ((st = check_band(band)) != NOVA_KV_OK) return st;
   if (!q || !k_codes || !v_codes || !seq_lens || !out)
     return fail(NOVA_KV_ERR_INVALID_ARG, "q, k_codes, v_codes, seq_lens or out is NULL");
   if (!aligned(k_codes, 16) || !aligned(v_codes, 16))
@@ -204,6 +226,12 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   a.k_codes = k_codes;
   a.v_codes = v_codes;
   a.k_scales = (p->flags & NOVA_KV_KEY_SCALE) ? k_scales : nullptr;
+  if (band) {
+    a.n_sink = band->n_sink;
+    a.n_rec = band->n_rec;
+    a.band_k = band->k;
+    a.band_v = band->v;
+  }
   a.seq_lens = seq_lens;
   a.max_seq_len = max_seq_len;
   a.window = window;
@@ -231,14 +259,14 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
 nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
                                    const void *q, nova_kv_dtype q_dtype, int32_t batch,
                                    int32_t num_q_heads, const uint8_t *k_codes,
-                                   const uint8_t *v_codes, const uint16_t *k_scales, const int32_t *seq_lens,
-                                   int32_t max_seq_len, int32_t window, const float *sinks,
+                                   const uint8_t *v_codes, const uint16_t *k_scales, const nova_kv_band *band,
+                                   const int32_t *seq_lens, int32_t max_seq_len, int32_t window, const float *sinks,
                                    float softmax_scale, float *out, void *workspace,
                                    size_t workspace_bytes, void *hip_stream) {
   novakv::DecodeArgs a;
   novakv::DecodePlan plan;
-  nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales, seq_lens,
-                                     max_seq_len, window, sinks, softmax_scale, out, workspace, workspace_bytes,
+  nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales, band,
+                                     seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace, workspace_bytes,
                                      false, a, plan);
   if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
   hipError_t e = novakv::launch_decode(a, plan.use_lut, static_cast<hipStream_t>(hip_stream));
@@ -250,7 +278,8 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
                                           const void *k_new, const void *v_new, nova_kv_dtype new_dtype,
                                           const void *q, nova_kv_dtype q_dtype, int32_t batch,
                                           int32_t num_q_heads, uint8_t *k_codes, uint8_t *v_codes,
-                                          uint16_t *k_scales, const int32_t *seq_lens, int32_t max_seq_len,
+                                          uint16_t *k_scales, const nova_kv_band *band, const int32_t *seq_lens,
+                                          int32_t max_seq_len,
                                           int32_t window,
                                           const float *sinks, float softmax_scale, float *out,
                                           void *workspace, size_t workspace_bytes, void *hip_stream) {
@@ -259,13 +288,13 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
   novakv::DecodeArgs a;
   novakv::DecodePlan plan;
   nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales,
-                                     seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace,
+                                     band, seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace,
                                      workspace_bytes, true, a, plan);
   if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
   if (!k_new || !v_new) return fail(NOVA_KV_ERR_INVALID_ARG, "k_new or v_new is NULL");
   const hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   hipError_t e;
-  if (plan.use_lut && p->head_dim == 128 && !(p->flags & NOVA_KV_KEY_SCALE)) {
+  if (plan.use_lut && p->head_dim == 128 && !(p->flags & NOVA_KV_KEY_SCALE) && !band) {
     // one launch: the table kernel encodes the new token and attends to it
     a.append = 1;
     a.k_new = k_new;
@@ -296,6 +325,12 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
     ea.k_codes = k_codes;
     ea.v_codes = v_codes;
     ea.k_scales = (p->flags & NOVA_KV_KEY_SCALE) ? k_scales : nullptr;
+    if (band) {
+      ea.n_sink = band->n_sink;
+      ea.n_rec = band->n_rec;
+      ea.band_k = band->k;
+      ea.band_v = band->v;
+    }
     e = novakv::launch_encode(ea, stream);
     if (e == hipSuccess) e = novakv::launch_decode(a, plan.use_lut, stream);
   }

@@ -77,10 +77,12 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
   const int tid = threadIdx.x;
   const int G = a.gqa;
 
-  {  // a split beyond the attended span publishes an empty partial and stops
-    const int S = a.seq_lens[b];
-    const int lo = a.window > 0 ? max(0, S - a.window) : 0;
-    if (lo + split * a.chunk >= S) {
+  // the pools are read for [lo, tend): the attended span without the band
+  const int S = a.seq_lens[b];
+  const AttendedSpans spn = attended_spans(a.window > 0 ? max(0, S - a.window) : 0, S, a.n_sink, a.n_rec);
+  const int lo = spn.code_lo, tend = spn.code_hi;
+  {  // a split beyond that span publishes an empty partial and stops
+    if (lo + split * a.chunk >= tend) {
       const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
       for (int i = tid; i < G * D; i += kThreads) {
         const size_t r = (row0 + i / D) * a.n_split + split;
@@ -108,10 +110,8 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
           a.qp[(static_cast<size_t>(b) * a.num_q_heads + kv * G + i / D) * D + (i % D)];
   }
 
-  const int S = a.seq_lens[b];
-  const int lo = a.window > 0 ? max(0, S - a.window) : 0;
-  const int t0 = lo + split * a.chunk;  // splits tile the attended span [lo, S)
-  const int t1 = min(S, lo + (split + 1) * a.chunk);
+  const int t0 = lo + split * a.chunk;  // splits tile the span [lo, tend)
+  const int t1 = min(tend, lo + (split + 1) * a.chunk);
 
   float m[kMaxGqa], l[kMaxGqa], acc[kMaxGqa];
 #pragma unroll
@@ -227,8 +227,14 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
 }
 
 // Stage 2, one workgroup per (sequence, KV head): log-sum-exp merge of the
-// splits, sink once, divide, then v = s t_v^T for the KV head's query heads
-// (t_v read once per workgroup, rows as 16-byte vectors).
+// splits, sink once, the sink-plus-recent band (when there is one) as one
+// more partial, divide, then v = s t_v^T for the KV head's query heads (t_v
+// read once per workgroup, rows as 16-byte vectors) plus the band's value
+// term, which is in the original domain.
+//
+// Band (paper: Sec. "Sink-plus-recent band"): positions [lo, sink_end) and
+// [code_hi, S) with their bf16 keys and values; logits
+// z = (q . k - q . k_bar) * scale, the shift of the codes' logits (Lemma S1).
 template <int D>
 __global__ void __launch_bounds__(256) decode_combine(DecodeArgs a) {
   const int b = blockIdx.x / a.num_kv_heads;
@@ -236,6 +242,97 @@ __global__ void __launch_bounds__(256) decode_combine(DecodeArgs a) {
   const int G = a.gqa;
   const int tid = threadIdx.x;
   __shared__ float sh[kMaxGqa][D];
+  __shared__ float bq[kMaxGqa][D];           // band: query, later the value sums
+  __shared__ float bz[kMaxBand][kMaxGqa];    // band logits, then probabilities
+  __shared__ float bpart[256 / D][kMaxGqa][D];
+  __shared__ float bst[3][kMaxGqa];          // q . k_bar, max, sum
+  __shared__ float bout[kMaxGqa][D];
+  const int S = a.seq_lens[b];
+  const int att_lo = a.window > 0 ? max(0, S - a.window) : 0;
+  const AttendedSpans spn = attended_spans(att_lo, S, a.n_sink, a.n_rec);
+  const int ns = max(0, spn.sink_end - att_lo);
+  const int nband = a.band_k ? ns + (S - spn.code_hi) : 0;
+  if (nband > 0) {
+    const size_t hb = (static_cast<size_t>(b) * a.num_kv_heads + kv) * (a.n_sink + a.n_rec);
+    auto row_of = [&](const int i) -> size_t {
+      const int p = i < ns ? att_lo + i : spn.code_hi + (i - ns);
+      return (hb + band_slot(p, a.n_sink, a.n_rec)) * D;
+    };
+    for (int i = tid; i < G * D; i += 256) {
+      const size_t qi = (static_cast<size_t>(b) * a.num_q_heads + kv * G) * D + i;
+      bq[i / D][i % D] = a.q_bf16 ? bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi])
+                                  : static_cast<const float *>(a.q)[qi];
+    }
+    __syncthreads();
+    if (tid < G) {
+      float x = 0.f;
+      for (int d = 0; d < D; ++d) x = fmaf(bq[tid][d], a.kbar[kv * D + d], x);
+      bst[0][tid] = x;
+    }
+    __syncthreads();
+    for (int i = tid; i < nband; i += 256) {  // one band row per thread
+      const uint4 *kr = reinterpret_cast<const uint4 *>(a.band_k + row_of(i));
+      float z[kMaxGqa];
+#pragma unroll
+      for (int h = 0; h < kMaxGqa; ++h) z[h] = 0.f;
+      for (int c = 0; c < D / 8; ++c) {
+        const uint4 w = kr[c];
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float kx = __uint_as_float((e & 1) ? (ws[e >> 1] & 0xffff0000u) : (ws[e >> 1] << 16));
+#pragma unroll
+          for (int h = 0; h < kMaxGqa; ++h)
+            if (h < G) z[h] = fmaf(bq[h][8 * c + e], kx, z[h]);
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < kMaxGqa; ++h)
+        if (h < G) bz[i][h] = (z[h] - bst[0][h]) * a.scale;
+    }
+    __syncthreads();
+    for (int h = tid >> 6; h < G; h += 4) {  // one wave per head
+      const int lane = tid & 63;
+      float mx = -INFINITY;
+      for (int i = lane; i < nband; i += 64) mx = fmaxf(mx, bz[i][h]);
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+      float l = 0.f;
+      for (int i = lane; i < nband; i += 64) {
+        const float p = __expf(bz[i][h] - mx);
+        bz[i][h] = p;
+        l += p;
+      }
+      l = wave_sum(l);
+      if (lane == 0) {
+        bst[1][h] = mx;
+        bst[2][h] = l;
+      }
+    }
+    __syncthreads();
+    {  // values: thread (part, d) takes rows i = part mod 256 / D
+      constexpr int PARTS = 256 / D;
+      const int d = tid % D, part = tid / D;
+      float acc[kMaxGqa];
+#pragma unroll
+      for (int h = 0; h < kMaxGqa; ++h) acc[h] = 0.f;
+      for (int i = part; i < nband; i += PARTS) {
+        const float v = bf16_bits_to_float(a.band_v[row_of(i) + d]);
+#pragma unroll
+        for (int h = 0; h < kMaxGqa; ++h)
+          if (h < G) acc[h] = fmaf(bz[i][h], v, acc[h]);
+      }
+#pragma unroll
+      for (int h = 0; h < kMaxGqa; ++h) bpart[part][h][d] = acc[h];
+    }
+    __syncthreads();
+    for (int i = tid; i < G * D; i += 256) {
+      float x = 0.f;
+      for (int p = 0; p < 256 / D; ++p) x += bpart[p][i / D][i % D];
+      bq[i / D][i % D] = x;
+    }
+    __syncthreads();
+  }
   for (int i = tid; i < G * D; i += 256) {
     const int h = i / D, d = i - h * D;
     const size_t bh = static_cast<size_t>(b) * a.num_q_heads + kv * G + h;
@@ -254,7 +351,21 @@ __global__ void __launch_bounds__(256) decode_combine(DecodeArgs a) {
       }
       if (sink != -INFINITY) den += __expf(sink - big);
     }
+    float bo = 0.f;
+    if (nband > 0) {  // the band after the splits and the sink
+      const float mb = bst[1][h];
+      if (mb > big) {
+        const float f = big == -INFINITY ? 0.f : __expf(big - mb);
+        num *= f;
+        den *= f;
+        big = mb;
+      }
+      const float wb = __expf(mb - big);
+      den = fmaf(wb, bst[2][h], den);
+      bo = wb * bq[h][d];
+    }
     sh[h][d] = (den > 0.f) ? num / den : 0.f;
+    bout[h][d] = (den > 0.f) ? bo / den : 0.f;
   }
   __syncthreads();
   // thread -> (output coordinate d, half of the heads)
@@ -281,7 +392,7 @@ __global__ void __launch_bounds__(256) decode_combine(DecodeArgs a) {
 #pragma unroll
   for (int h = 0; h < kMaxGqa; ++h)
     if (h % HALVES == part && h < G)
-      a.out[(static_cast<size_t>(b) * a.num_q_heads + kv * G + h) * D + d] = o[h];
+      a.out[(static_cast<size_t>(b) * a.num_q_heads + kv * G + h) * D + d] = nband > 0 ? o[h] + bout[h][d] : o[h];
 }
 
 template <int D>

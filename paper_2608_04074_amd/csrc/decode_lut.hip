@@ -26,6 +26,7 @@
 // splits, so the cache read covers positions before it only.
 #include <math.h>
 
+#include "band_attention.h"
 #include "encode_block.h"
 #include "lut_common.h"
 #include "nova_kv_internal.h"
@@ -765,11 +766,19 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 // word's tag checked, the words emptied once read); splits that attend to no
 // token published no partial and are skipped.
 template <int WAVES, bool APPEND>
-__device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int kv, const int bk,
-                                             const size_t row0, const int own_split, const int S, const int lo,
-                                             const int tend, const int n_eff, const float4 (&tv)[8]) {
+__device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
+                                             const int bk, const size_t row0, const int own_split, const int S,
+                                             const int lo, const int tend, const int n_eff, const int band_lo,
+                                             const int sink_end, const float4 (&tv)[8]) {
   const int tid = threadIdx.x;
   const int G = a.gqa;
+  // Sink-plus-recent band: positions [band_lo, sink_end) and [tend, S) (the
+  // splits read [lo, tend) from the pools), attended here, in the table's
+  // LDS region, and taken after the splits as one more partial.
+  using BL = BandLds<kD, 4, WAVES>;
+  const int nband = a.band_k ? max(0, sink_end - band_lo) + (S - tend) : 0;
+  if (nband > 0) band_attention<kD, 4, WAVES, WAVES>(a, smem, b, kv, row0, band_lo, sink_end, tend, S);
+  float *bout = reinterpret_cast<float *>(smem + BL::kPart);  // [4][128] band term of the output
   float *shat = reinterpret_cast<float *>(smem + kAuxQ);    // [4][128]
   float *outp = reinterpret_cast<float *>(smem + kAuxOut);  // [part][head][128]
   float *ctlf = reinterpret_cast<float *>(smem + kAuxCtl);
@@ -889,8 +898,23 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
         take((((zp[0] + zp[1]) + zp[2]) + zp[3]) * kLn2, 1.f, vp);
       }
     }
+    float bo = 0.f;
+    if (nband > 0) {  // the band, after the splits (and the new token)
+      const float *bst = reinterpret_cast<const float *>(smem + BL::kStat);
+      const float mb = bst[h], lb = bst[4 + h];
+      if (mb > big) {
+        const float f = big == -INFINITY ? 0.f : __expf(big - mb);
+        num *= f;
+        den *= f;
+        big = mb;
+      }
+      const float wb = __expf(mb - big);
+      den = fmaf(wb, lb, den);
+      bo = wb * reinterpret_cast<const float *>(smem + BL::kZ)[h * kD + d];
+    }
     // a word that never arrived (not expected) leaves this row NaN
     shat[tid] = !ok ? __builtin_nanf("") : (den > 0.f ? num / den : 0.f);
+    bout[tid] = den > 0.f ? bo / den : 0.f;
   } else if (tid < 4 * kD) {
     shat[tid] = 0.f;
   }
@@ -919,8 +943,9 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
   __syncthreads();
   if (tid < G * kD) {
     const int h = tid >> 7;
-    a.out[(row0 + h) * kD + d] =
+    const float o =
         (outp[h * kD + d] + outp[(4 + h) * kD + d]) + (outp[(8 + h) * kD + d] + outp[(12 + h) * kD + d]);
+    a.out[(row0 + h) * kD + d] = nband > 0 ? o + bout[tid] : o;
   }
   // Every word read above has been seen with its tag by every thread that
   // reads it (there were barriers since): empty the other splits' words for
@@ -971,11 +996,14 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   const int G = a.gqa;
 
   const int S = a.seq_lens[b];
-  const int lo = a.window > 0 ? max(0, S - a.window) : 0;
-  // A fused step reads the pools for [lo, S - 1); its newest token comes from
-  // the step's own key and value.
-  const int tend = APPEND ? max(S - 1, lo) : S;
-  const int t0 = lo + split * a.chunk;  // splits tile the attended span
+  const int att_lo = a.window > 0 ? max(0, S - a.window) : 0;
+  // The pools are read for [lo, tend): the attended span without the band
+  // (a fused step has none: its newest token comes from the step's own key
+  // and value, so the pools are read for [att_lo, S - 1)).
+  const AttendedSpans spn = attended_spans(att_lo, S, a.n_sink, a.n_rec);
+  const int lo = APPEND ? att_lo : spn.code_lo;
+  const int tend = APPEND ? max(S - 1, att_lo) : spn.code_hi;
+  const int t0 = lo + split * a.chunk;  // splits tile the span read from the pools
   const int t1 = min(tend, lo + (split + 1) * a.chunk);
   const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
   const bool active = t0 < t1;
@@ -1017,7 +1045,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
       }
     }
   }
-  combine_unit<WAVES, APPEND>(a, smem, kv, bk, row0, split, S, lo, tend, n_eff, tv);
+  combine_unit<WAVES, APPEND>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv);
 }
 
 }  // namespace
@@ -1057,7 +1085,7 @@ int plan_b_chunk(int batch, int num_kv_heads, int n_split) {
 hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream) {
   constexpr int W = 12;
   const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
-  if (a.append && a.k_scales) return hipErrorInvalidValue;
+  if (a.append && (a.k_scales || a.band_k)) return hipErrorInvalidValue;
   if (a.append)
     decode_lut_d128<W, true, false><<<grid, dim3(W * 64), 0, stream>>>(a);
   else if (a.k_scales)

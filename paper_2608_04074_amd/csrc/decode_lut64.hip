@@ -22,6 +22,7 @@
 //  * Values: two token sets per half, 4 coordinate tiles of 16.
 #include <math.h>
 
+#include "band_attention.h"
 #include "lut_common.h"
 #include "nova_kv_internal.h"
 
@@ -454,13 +455,22 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 // Last split of a (sequence, KV head): log-sum-exp merge of the splits in
 // index order, the sink once (shifted, Lemma S1), division, and out = s_hat t_v^T.
 template <int WAVES>
-__device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int kv, const size_t row0,
-                                             const int own_split, const bool own_active, const int S, const int lo,
-                                             const float4 (&tv)[4]) {
+__device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
+                                             const size_t row0, const int own_split, const bool own_active,
+                                             const int S, const int lo, const int tend, const int band_lo,
+                                             const int sink_end, const float4 (&tv)[4]) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = a.gqa;
+  // Sink-plus-recent band: positions [band_lo, sink_end) and [tend, S) (the
+  // splits read [lo, tend) from the pools), attended here, in the table's
+  // LDS region, and taken after the splits as one more partial.
+  constexpr int kVW = 8;  // waves that sum the band's values
+  using BL = BandLds<kD, kH, kVW>;
+  const int nband = a.band_k ? max(0, sink_end - band_lo) + (S - tend) : 0;
+  if (nband > 0) band_attention<kD, kH, WAVES, kVW>(a, smem, b, kv, row0, band_lo, sink_end, tend, S);
+  float *bout = reinterpret_cast<float *>(smem + BL::kPart);  // [8][64] band term of the output
   float *shat = reinterpret_cast<float *>(smem + kAuxQ);    // [8][64]
   float *outp = reinterpret_cast<float *>(smem + kAuxOut);  // [4 parts][8 heads][64]
   float *ctlf = reinterpret_cast<float *>(smem + kAuxCtl);
@@ -501,7 +511,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
         ms[i] = -INFINITY;
         ls[i] = 0.f;
         as[i] = 0.f;
-        const bool nonempty = lo + sp * a.chunk < S;
+        const bool nonempty = lo + sp * a.chunk < tend;
         if (sp == own_split) {
           if (own_active) {
             ms[i] = ctlf[16 + 2 * h];
@@ -517,7 +527,22 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
 #pragma unroll
       for (int i = 0; i < 8; ++i) take(ms[i], ls[i], as[i]);
     }
+    float bo = 0.f;
+    if (nband > 0) {  // the band, after the splits
+      const float *bst = reinterpret_cast<const float *>(smem + BL::kStat);
+      const float mb = bst[h], lb = bst[kH + h];
+      if (mb > big) {
+        const float f = big == -INFINITY ? 0.f : __expf(big - mb);
+        num *= f;
+        den *= f;
+        big = mb;
+      }
+      const float wb = __expf(mb - big);
+      den = fmaf(wb, lb, den);
+      bo = wb * reinterpret_cast<const float *>(smem + BL::kZ)[h * kD + d];
+    }
     shat[tid] = den > 0.f ? num / den : 0.f;
+    bout[tid] = den > 0.f ? bo / den : 0.f;
   } else if (tid < kH * kD) {
     shat[tid] = 0.f;
   }
@@ -543,8 +568,9 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
   __syncthreads();
   if (tid < G * kD) {
     const int h = tid >> 6;
-    a.out[(row0 + h) * kD + d] = (outp[h * kD + d] + outp[(kH + h) * kD + d]) +
-                                 (outp[(2 * kH + h) * kD + d] + outp[(3 * kH + h) * kD + d]);
+    const float o = (outp[h * kD + d] + outp[(kH + h) * kD + d]) +
+                    (outp[(2 * kH + h) * kD + d] + outp[(3 * kH + h) * kD + d]);
+    a.out[(row0 + h) * kD + d] = nband > 0 ? o + bout[tid] : o;
   }
 }
 
@@ -562,9 +588,12 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
   const int G = a.gqa;
 
   const int S = a.seq_lens[b];
-  const int lo = a.window > 0 ? max(0, S - a.window) : 0;
-  const int t0 = lo + split * a.chunk;  // splits tile the attended span [lo, S)
-  const int t1 = min(S, lo + (split + 1) * a.chunk);
+  const int att_lo = a.window > 0 ? max(0, S - a.window) : 0;
+  // the pools are read for [lo, tend): the attended span without the band
+  const AttendedSpans spn = attended_spans(att_lo, S, a.n_sink, a.n_rec);
+  const int lo = spn.code_lo, tend = spn.code_hi;
+  const int t0 = lo + split * a.chunk;  // splits tile the span read from the pools
+  const int t1 = min(tend, lo + (split + 1) * a.chunk);
   const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
   const bool active = t0 < t1;
 
@@ -609,7 +638,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
     __syncthreads();
     if (ctl[0] == 0) return;
   }
-  combine_unit<WAVES>(a, smem, kv, row0, split, active, S, lo, tv);
+  combine_unit<WAVES>(a, smem, b, kv, row0, split, active, S, lo, tend, att_lo, spn.sink_end, tv);
 }
 
 }  // namespace

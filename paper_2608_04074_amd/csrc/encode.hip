@@ -15,6 +15,27 @@ namespace novakv {
 
 namespace {
 
+// Sink-plus-recent band: a new token's element (bf16 bits) goes to the band
+// when its position is there once the append is done (the sequence then ends
+// at `end`): a sink slot, or the ring slot of the last n_rec positions.
+__device__ __forceinline__ void store_band(const EncodeArgs &a, const int side, const int b, const int kv,
+                                           const int pos, const int end, const int d, const uint16_t bits) {
+  uint16_t *band = side == 0 ? a.band_k : a.band_v;
+  if (!band) return;
+  if (!(pos < a.n_sink || (a.n_rec > 0 && pos >= end - a.n_rec))) return;
+  const int nb = a.n_sink + a.n_rec;
+  band[((static_cast<size_t>(b) * a.num_kv_heads + kv) * nb + band_slot(pos, a.n_sink, a.n_rec)) * a.head_dim + d] =
+      bits;
+}
+
+// bf16 bits of an input element: as stored, or an fp32 value rounded to
+// nearest even.
+__device__ __forceinline__ uint16_t input_bf16_bits(const EncodeArgs &a, const void *src, const size_t idx) {
+  if (a.in_bf16) return static_cast<const uint16_t *>(src)[idx];
+  const uint32_t f = __float_as_uint(static_cast<const float *>(src)[idx]);
+  return static_cast<uint16_t>((f + 0x7fffu + ((f >> 16) & 1u)) >> 16);
+}
+
 // Few new tokens per sequence (a decode step): one workgroup per (token,
 // sequence, KV head, side, block of 8 groups).  A block needs 32 transform
 // columns (D x 32 fp32) and its 8 codebooks (16 KB), so each workgroup
@@ -45,6 +66,10 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
                          : static_cast<double>(static_cast<const float *>(src)[idx]);
     if (side == 0) x -= static_cast<double>(a.kbar[kv * D + tid]);
     sc.xs[tid] = x;
+    if (blk == 0 && a.band_k) {
+      const int p0 = a.start_pos[b] + a.start_offset;
+      store_band(a, side, b, kv, p0 + t, p0 + a.n_new, tid, input_bf16_bits(a, src, idx));
+    }
   }
   __syncthreads();
   const int pos = a.start_pos[b] + a.start_offset + t;
@@ -131,6 +156,10 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
       x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
                     : static_cast<double>(static_cast<const float *>(src)[idx]);
       if (side == 0) x -= static_cast<double>(a.kbar[kv * D + d]);
+      if (a.band_k) {
+        const int p0 = a.start_pos[b] + a.start_offset;
+        store_band(a, side, b, kv, p0 + n0 + t, p0 + a.n_new, d, input_bf16_bits(a, src, idx));
+      }
     }
     xs[t * RS + d] = x;
   }

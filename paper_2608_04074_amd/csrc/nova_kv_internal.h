@@ -37,6 +37,11 @@ struct DecodeArgs {
   int q_bf16;
   const uint8_t *k_codes, *v_codes;
   const uint16_t *k_scales;  // key-scale format: bf16 per-token key scales (pool layout), else nullptr
+  // Sink-plus-recent band: [B][Hkv][n_sink + n_rec][D] bf16 keys and values
+  // of the positions [0, n_sink) and the last n_rec (ring slots), or nullptr
+  // (then n_sink = n_rec = 0).
+  int n_sink, n_rec;
+  const uint16_t *band_k, *band_v;
   const int32_t *seq_lens;
   int max_seq_len, window;
   const float *sinks;
@@ -83,7 +88,32 @@ struct EncodeArgs {
   int start_offset;  // the first new token of sequence b goes to start_pos[b] + start_offset
   uint8_t *k_codes, *v_codes;
   uint16_t *k_scales;  // key-scale format: bf16 per-token key scales (pool layout), else nullptr
+  int n_sink, n_rec;   // sink-plus-recent band (0, 0 without one)
+  uint16_t *band_k, *band_v;
 };
+
+constexpr int kMaxBand = 1024;
+
+// Slot of band position p: the sink slots, then a ring of the last n_rec positions.
+__host__ __device__ __forceinline__ int band_slot(int p, int n_sink, int n_rec) {
+  return p < n_sink ? p : n_sink + p % n_rec;
+}
+
+// The attended positions of a sequence of S cached tokens whose range starts
+// at lo: sink band [lo, sink_end), codes [code_lo, code_hi), recent band
+// [code_hi, S).  Without a band (n_sink = n_rec = 0) everything is codes.
+struct AttendedSpans {
+  int sink_end, code_lo, code_hi;
+};
+__host__ __device__ __forceinline__ AttendedSpans attended_spans(int lo, int S, int n_sink, int n_rec) {
+  AttendedSpans sp;
+  sp.sink_end = lo < n_sink ? (S < n_sink ? S : n_sink) : lo;
+  sp.code_lo = lo > n_sink ? lo : n_sink;
+  const int r = S - n_rec;
+  sp.code_hi = r > sp.code_lo ? r : sp.code_lo;
+  if (sp.code_lo > S) sp.code_lo = sp.code_hi = S;
+  return sp;
+}
 
 // Split plan and workspace carve-out of the decode path.
 struct DecodePlan {

@@ -36,6 +36,11 @@ def test_status_strings():
     assert lib.nova_kv_status_string(99) == b"unknown status"
 
 
+def _band(b):
+    """(n_sink, n_rec, k, v) -> a pointer to a nova_kv_band, or NULL."""
+    return None if b is None else ctypes.byref(nat.Band(*b))
+
+
 def _params(**kw):
     base = dict(num_kv_heads=8, head_dim=128, group_dim=4, codebook_size=256, flags=0,
                 kbar=0x1000, t_k=0x2000, t_k_inv_t=0x3000, t_v=0x4000, cb_k=0x5000, cb_v=0x6000)
@@ -51,22 +56,24 @@ def _layout(**kw):
 
 def _decode(p, lay, **kw):
     a = dict(q=0x7000, q_dtype=nat.NOVA_KV_BF16, batch=2, hq=32, k=0x8000, v=0x9000, seq=0xA000,
-             max_seq=4096, window=0, sinks=None, scale=0.0, out=0xB000, ws=None, ws_bytes=0, ks=None)
+             max_seq=4096, window=0, sinks=None, scale=0.0, out=0xB000, ws=None, ws_bytes=0, ks=None,
+             band=None)
     a.update(kw)
     return nat.lib().nova_kv_decode_attn(
         ctypes.byref(p) if p is not None else None, ctypes.byref(lay) if lay is not None else None,
-        a["q"], a["q_dtype"], a["batch"], a["hq"], a["k"], a["v"], a["ks"], a["seq"], a["max_seq"],
+        a["q"], a["q_dtype"], a["batch"], a["hq"], a["k"], a["v"], a["ks"], _band(a["band"]), a["seq"],
+        a["max_seq"],
         a["window"], a["sinks"], a["scale"], a["out"], a["ws"], a["ws_bytes"], None)
 
 
 def _encode(p, lay, **kw):
     a = dict(k=0x7000, v=0x7800, dtype=nat.NOVA_KV_BF16, batch=2, n_new=16, start=0xA000,
-             kc=0x8000, vc=0x9000, ks=None)
+             kc=0x8000, vc=0x9000, ks=None, band=None)
     a.update(kw)
     return nat.lib().nova_kv_encode(ctypes.byref(p) if p is not None else None,
                                     ctypes.byref(lay) if lay is not None else None,
                                     a["k"], a["v"], a["dtype"], a["batch"], a["n_new"], a["start"],
-                                    a["kc"], a["vc"], a["ks"], None)
+                                    a["kc"], a["vc"], a["ks"], _band(a["band"]), None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -150,12 +157,13 @@ def test_encode_needs_forward_transforms_and_noops():
 
 def _append(p, lay, **kw):
     a = dict(kn=0x7000, vn=0x7800, new_dtype=nat.NOVA_KV_BF16, q=0x7400, q_dtype=nat.NOVA_KV_BF16,
-             batch=2, hq=32, k=0x8000, v=0x9000, ks=None, seq=0xA000, max_seq=4096, window=0,
+             batch=2, hq=32, k=0x8000, v=0x9000, ks=None, band=None, seq=0xA000, max_seq=4096, window=0,
              sinks=None, scale=0.0, out=0xB000, ws=None, ws_bytes=0)
     a.update(kw)
     return nat.lib().nova_kv_append_decode_attn(
         ctypes.byref(p), ctypes.byref(lay), a["kn"], a["vn"], a["new_dtype"], a["q"], a["q_dtype"],
-        a["batch"], a["hq"], a["k"], a["v"], a["ks"], a["seq"], a["max_seq"], a["window"], a["sinks"],
+        a["batch"], a["hq"], a["k"], a["v"], a["ks"], _band(a["band"]), a["seq"], a["max_seq"], a["window"],
+        a["sinks"],
         a["scale"], a["out"], a["ws"], a["ws_bytes"], None)
 
 
@@ -180,3 +188,20 @@ def test_key_scale_format_needs_an_aligned_scale_pool(call):
 
 def test_append_rejects_bad_new_dtype():
     assert _append(_params(), _layout(), new_dtype=9) == nat.NOVA_KV_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("call", [_decode, _encode, _append])
+@pytest.mark.parametrize("band", [(0, 0, 0xC000, 0xD000), (-1, 8, 0xC000, 0xD000), (64, 961, 0xC000, 0xD000),
+                                  (64, 256, None, 0xD000), (64, 256, 0xC000, None), (64, 256, 0xC008, 0xD000)])
+def test_bad_band_is_rejected(call, band):
+    assert call(_params(), _layout(), band=band) == nat.NOVA_KV_ERR_INVALID_ARG
+    assert b"band" in nat.lib().nova_kv_last_error()
+
+
+@pytest.mark.parametrize("call", [_decode, _append])
+def test_good_band_passes_the_checks(call):
+    # the checks go on to the next argument: no workspace
+    assert call(_params(), _layout(), band=(64, 256, 0xC000, 0xD000)) == nat.NOVA_KV_ERR_WORKSPACE
+    assert call(_params(), _layout(), band=(0, 1024, 0xC000, 0xD000)) == nat.NOVA_KV_ERR_WORKSPACE
+    # batch 0 stays a no-op whatever the band
+    assert call(_params(), _layout(), band=(0, 0, None, None), batch=0, q=None, out=None) == nat.NOVA_KV_OK
