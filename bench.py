@@ -138,10 +138,13 @@ def other_workloads(nk, torch, dev, calls: int):
     measured as they would run (cache-resident)."""
     import synth
     res = []
-    cases = [("single_head", 0, False), ("sweep_b64_s32k", 0, False), ("sweep_b1_s128k", 0, False),
-             ("gptoss_pair", 0, False), ("gptoss_pair", 1, False), ("append_paged", 0, False),
-             ("qwen3_8b", 0, True), ("gptoss_pair", 1, True)]
-    for name, layer, key_scale in cases:
+    # (workload, layer, key-scale format, sink-plus-recent band (n_sink, n_rec) or None)
+    cases = [("single_head", 0, False, None), ("sweep_b64_s32k", 0, False, None),
+             ("sweep_b1_s128k", 0, False, None), ("gptoss_pair", 0, False, None),
+             ("gptoss_pair", 1, False, None), ("append_paged", 0, False, None),
+             ("qwen3_8b", 0, True, None), ("gptoss_pair", 1, True, None),
+             ("qwen3_8b", 0, False, (64, 256)), ("gptoss_pair", 1, False, (64, 256))]
+    for name, layer, key_scale, band_sizes in cases:
         wl = synth.get_workload(name)
         B, S, H, Hq, D, L = wl.batch, wl.seq_len, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.groups
         P = nk.NovaKVParams.from_arrays(synth.bench_params(wl, layer), device=dev, key_scale=key_scale)
@@ -168,8 +171,13 @@ def other_workloads(nk, torch, dev, calls: int):
         out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
         ws = torch.zeros(nk.decode_workspace_bytes(P, B, Hq, S), dtype=torch.uint8, device=dev)
         window = wl.windows[layer]
+        band = None
+        if band_sizes:
+            bshape = nk.band_shape(P, B, *band_sizes)
+            band = nk.Band(*band_sizes, torch.randn(bshape, generator=gen, device=dev).to(torch.bfloat16),
+                           torch.randn(bshape, generator=gen, device=dev).to(torch.bfloat16))
         calls_ = [nk.prepare_decode(P, layout, q, pk, pv, seq, S, out, ws, window=window, sinks=sinks,
-                                    k_scales=ps)
+                                    k_scales=ps, band=band)
                   for pk, pv, ps in pools]
         for i in range(5):
             calls_[i % copies]()
@@ -183,16 +191,22 @@ def other_workloads(nk, torch, dev, calls: int):
         torch.cuda.synchronize()
         us = e0.elapsed_time(e1) * 1e3 / calls
         cb = wl.code_bytes_per_step(layer)
-        # the key scales of the attended tokens: 2 bytes per token and KV head
+        bb = 0
+        if band_sizes:  # the band's tokens are read as bf16 rows instead of codes
+            nband = min(sum(band_sizes), S)
+            cb -= 2 * B * H * nband * L
+            bb = 2 * B * H * nband * D * 2
+        # the key scales of the tokens read from codes: 2 bytes per token and KV head
         sb = cb // L if key_scale else 0
         res.append({"workload": f"{name}" + (f" layer {layer} (window {window})" if wl.num_layers > 1 else "")
-                    + (" key-scale format" if key_scale else ""),
+                    + (" key-scale format" if key_scale else "")
+                    + (f" band {band_sizes[0]}+{band_sizes[1]}" if band_sizes else ""),
                     "batch": B, "seq_len": S, "q_heads": Hq, "kv_heads": H, "head_dim": D,
                     "paged_block": wl.block_size or None, "code_bytes": cb, "scale_bytes": sb,
-                    "pool_copies": copies,
-                    "decode_us": round(us, 2), "GB_per_s": round((cb + sb) / (us * 1e-6) / 1e9, 1),
-                    "frac_of_hbm_peak": round((cb + sb) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
-        del pools, calls_, ws
+                    "band_bytes": bb, "pool_copies": copies,
+                    "decode_us": round(us, 2), "GB_per_s": round((cb + sb + bb) / (us * 1e-6) / 1e9, 1),
+                    "frac_of_hbm_peak": round((cb + sb + bb) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
+        del pools, calls_, ws, band
         torch.cuda.empty_cache()
     return res
 
