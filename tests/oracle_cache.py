@@ -17,6 +17,7 @@ import numpy as np
 
 import synth
 from oracle import calibration
+from oracle import fp8 as oracle_fp8
 
 CACHE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "_cache")
 KEYS = ("kbar", "t_k", "t_k_inv_t", "t_v", "cb_k", "cb_v")
@@ -35,10 +36,11 @@ def _key(wl: synth.Workload, layer: int, tokens: int, iters: int, mo_stride: int
 
 
 def calibrated_params(wl: synth.Workload, layer: int = 0, tokens: int = None, iters: int = 25,
-                      mo_stride: int = 16, heads=None, key_scale: bool = False):
+                      mo_stride: int = 16, heads=None, key_scale: bool = False, fp8: bool = False):
     """Stacked [Hkv][...] stored parameters of one layer (oracle calibration per KV head).
 
-    key_scale: key codebooks trained on normalized coefficients (key-scale format)."""
+    key_scale: key codebooks trained on normalized coefficients (key-scale format).
+    fp8: the fp16 codebooks snapped to fp8 E4M3 (still held as fp16 values)."""
     tokens = wl.calib_tokens if tokens is None else tokens
     heads = range(wl.num_kv_heads) if heads is None else heads
     os.makedirs(CACHE, exist_ok=True)
@@ -55,7 +57,10 @@ def calibrated_params(wl: synth.Workload, layer: int = 0, tokens: int = None, it
         np.savez(path + ".tmp.npz", **stored)
         os.replace(path + ".tmp.npz", path)
         per_head.append(stored)
-    return calibration.stack_params(per_head)
+    out = calibration.stack_params(per_head)
+    if fp8:
+        out = dict(out, cb_k=oracle_fp8.snap_codebooks(out["cb_k"]), cb_v=oracle_fp8.snap_codebooks(out["cb_v"]))
+    return out
 
 
 if __name__ == "__main__":
