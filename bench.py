@@ -138,18 +138,24 @@ def other_workloads(nk, torch, dev, calls: int):
     measured as they would run (cache-resident)."""
     import synth
     res = []
-    # (workload, layer, key-scale format, sink-plus-recent band (n_sink, n_rec) or None)
-    cases = [("single_head", 0, False, None), ("sweep_b64_s32k", 0, False, None),
-             ("sweep_b1_s128k", 0, False, None), ("gptoss_pair", 0, False, None),
-             ("gptoss_pair", 1, False, None), ("append_paged", 0, False, None),
-             ("qwen3_8b", 0, True, None), ("gptoss_pair", 1, True, None),
-             ("qwen3_8b", 0, False, (64, 256)), ("gptoss_pair", 1, False, (64, 256))]
-    for name, layer, key_scale, band_sizes in cases:
+    # (workload, layer, key-scale format, sink-plus-recent band (n_sink, n_rec) or None,
+    #  fp8 codebooks)
+    cases = [("single_head", 0, False, None, False), ("sweep_b64_s32k", 0, False, None, False),
+             ("sweep_b1_s128k", 0, False, None, False), ("gptoss_pair", 0, False, None, False),
+             ("gptoss_pair", 1, False, None, False), ("append_paged", 0, False, None, False),
+             ("qwen3_8b", 0, True, None, False), ("gptoss_pair", 1, True, None, False),
+             ("qwen3_8b", 0, False, (64, 256), False), ("gptoss_pair", 1, False, (64, 256), False),
+             ("qwen3_8b", 0, False, None, True), ("gptoss_pair", 1, False, None, True)]
+    for name, layer, key_scale, band_sizes, fp8 in cases:
         wl = synth.get_workload(name)
         B, S, H, Hq, D, L = wl.batch, wl.seq_len, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.groups
-        P = nk.NovaKVParams.from_arrays(synth.bench_params(wl, layer), device=dev, key_scale=key_scale)
         gen = torch.Generator(device=dev)
         gen.manual_seed(7)
+        arrays = synth.bench_params(wl, layer)
+        if fp8:  # the same codebooks rounded to fp8 E4M3 (torch's conversion), as bytes
+            for k in ("cb_k", "cb_v"):
+                arrays[k] = torch.as_tensor(arrays[k]).to(torch.float32).to(torch.float8_e4m3fn).view(torch.uint8)
+        P = nk.NovaKVParams.from_arrays(arrays, device=dev, key_scale=key_scale)
         if wl.block_size:
             bps = S // wl.block_size
             layout = nk.CacheLayout(wl.block_size, bps, torch.as_tensor(synth.shuffled_block_table(wl)).to(dev))
@@ -200,7 +206,8 @@ def other_workloads(nk, torch, dev, calls: int):
         sb = cb // L if key_scale else 0
         res.append({"workload": f"{name}" + (f" layer {layer} (window {window})" if wl.num_layers > 1 else "")
                     + (" key-scale format" if key_scale else "")
-                    + (f" band {band_sizes[0]}+{band_sizes[1]}" if band_sizes else ""),
+                    + (f" band {band_sizes[0]}+{band_sizes[1]}" if band_sizes else "")
+                    + (" fp8 codebooks" if fp8 else ""),
                     "batch": B, "seq_len": S, "q_heads": Hq, "kv_heads": H, "head_dim": D,
                     "paged_block": wl.block_size or None, "code_bytes": cb, "scale_bytes": sb,
                     "band_bytes": bb, "pool_copies": copies,

@@ -69,8 +69,9 @@ typedef enum {
  *   t_k_inv_t [Hkv][D][D]   fp32  R_K^{-T} (same column order): q' = q @ t_k_inv_t
  *   t_v       [Hkv][D][D]   fp32  value transform R_V (orthogonal, columns
  *                                 grouped):  s = v @ t_v,  v_hat = s_hat @ t_v^T
- *   cb_k      [Hkv][L][K][g] fp16 bit patterns: key codebook of each group
- *   cb_v      [Hkv][L][K][g] fp16 bit patterns: value codebook of each group
+ *   cb_k      [Hkv][L][K][g] fp16 bit patterns (uint16), or fp8 E4M3 bytes
+ *                           with NOVA_KV_FP8_CODEBOOKS: key codebook of each group
+ *   cb_v      [Hkv][L][K][g] the same for the value codebooks
  *
  * Group l covers transform coordinates [l*g, (l+1)*g).  Supported: g = 4,
  * K = 256, D in {64, 128}.  Every array must be 16-byte aligned
@@ -82,9 +83,15 @@ typedef enum {
  *             Sec. "Decoding kernel and read path": the read path multiplies
  *             the partial logit by it).  cb_k must then hold codebooks of
  *             normalized coefficients, and every call takes a k_scales pool.
+ *             NOVA_KV_FP8_CODEBOOKS (may be combined with the above): the
+ *             codebooks are stored as fp8 E4M3 bytes (OCP format: bias 7, no
+ *             infinities; paper: Sec. "Calibration", codebooks kept in fp16
+ *             and snapped to fp8 offline), 4 bytes per codeword; every value
+ *             is used exactly (E4M3 values are exact in fp16).
  *             Other bits are reserved (NOVA_KV_ERR_UNSUPPORTED).
  */
 #define NOVA_KV_KEY_SCALE 1u
+#define NOVA_KV_FP8_CODEBOOKS 2u
 
 typedef struct {
     int32_t num_kv_heads;
@@ -96,8 +103,8 @@ typedef struct {
     const float *t_k;
     const float *t_k_inv_t;
     const float *t_v;
-    const uint16_t *cb_k;
-    const uint16_t *cb_v;
+    const void *cb_k;
+    const void *cb_v;
 } nova_kv_params;
 
 /*

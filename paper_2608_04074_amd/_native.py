@@ -22,6 +22,7 @@ NOVA_KV_F32 = 0
 NOVA_KV_BF16 = 1
 
 NOVA_KV_KEY_SCALE = 1  # nova_kv_params.flags: the key-scale format
+NOVA_KV_FP8_CODEBOOKS = 2  # nova_kv_params.flags: codebooks stored as fp8 E4M3 bytes
 
 EXPORTED = (
     "nova_kv_encode",

@@ -43,6 +43,8 @@ class NovaKVParams:
     ``key_scale`` selects the key-scale format (one bf16 scale per cached key;
     the key codebooks are then trained on normalized coefficients), and every
     call then takes a ``k_scales`` pool of shape ``scale_pool_shape``.
+    Codebooks are fp16, or fp8 E4M3 bytes given as uint8 tensors (both sides
+    in the same format).
     """
 
     def __init__(self, kbar, t_k, t_k_inv_t, t_v, cb_k, cb_v, group_dim: int = 4,
@@ -53,13 +55,17 @@ class NovaKVParams:
         for name, t in (("t_k", t_k), ("t_k_inv_t", t_k_inv_t), ("t_v", t_v)):
             _require(t, name, (torch.float32,), hkv * d * d)
         for name, t in (("cb_k", cb_k), ("cb_v", cb_v)):
-            _require(t, name, (torch.float16,), hkv * L * codebook_size * group_dim)
+            _require(t, name, (torch.float16, torch.uint8), hkv * L * codebook_size * group_dim)
+        if cb_k.dtype != cb_v.dtype:
+            raise TypeError("cb_k and cb_v must have the same format (fp16, or fp8 E4M3 as uint8)")
+        self.fp8_codebooks = cb_k.dtype == torch.uint8
         self.num_kv_heads, self.head_dim = hkv, d
         self.group_dim, self.codebook_size = group_dim, codebook_size
         self.kbar, self.t_k, self.t_k_inv_t, self.t_v = kbar, t_k, t_k_inv_t, t_v
         self.cb_k, self.cb_v = cb_k, cb_v
         self.key_scale = bool(key_scale)
-        flags = nat.NOVA_KV_KEY_SCALE if self.key_scale else 0
+        flags = (nat.NOVA_KV_KEY_SCALE if self.key_scale else 0) | \
+            (nat.NOVA_KV_FP8_CODEBOOKS if self.fp8_codebooks else 0)
         self._c = nat.Params(hkv, d, group_dim, codebook_size, flags, kbar.data_ptr(), t_k.data_ptr(),
                              t_k_inv_t.data_ptr(), t_v.data_ptr(), cb_k.data_ptr(),
                              cb_v.data_ptr())
@@ -70,11 +76,14 @@ class NovaKVParams:
 
     @classmethod
     def from_arrays(cls, arrays: dict, device="cuda", key_scale: bool = False) -> "NovaKVParams":
-        """From host arrays: kbar/t_k/t_k_inv_t/t_v float32, cb_k/cb_v float16 ([Hkv][...])."""
+        """From host arrays: kbar/t_k/t_k_inv_t/t_v float32, cb_k/cb_v float16, or uint8
+        fp8 E4M3 codes ([Hkv][...])."""
         f32 = {k: torch.as_tensor(arrays[k]).to(torch.float32).contiguous().to(device)
                for k in ("kbar", "t_k", "t_k_inv_t", "t_v")}
-        f16 = {k: torch.as_tensor(arrays[k]).to(torch.float16).contiguous().to(device)
-               for k in ("cb_k", "cb_v")}
+        f16 = {}
+        for k in ("cb_k", "cb_v"):
+            t = torch.as_tensor(arrays[k])
+            f16[k] = (t if t.dtype == torch.uint8 else t.to(torch.float16)).contiguous().to(device)
         return cls(**f32, **f16, key_scale=key_scale)
 
     @property

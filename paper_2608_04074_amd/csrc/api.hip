@@ -46,8 +46,9 @@ nova_kv_status check_params(const nova_kv_params *p, bool need_encode, bool need
     return fail(NOVA_KV_ERR_UNSUPPORTED, "codebook_size %d unsupported (only 256)", p->codebook_size);
   if (p->head_dim != 64 && p->head_dim != 128)
     return fail(NOVA_KV_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", p->head_dim);
-  if ((p->flags & ~NOVA_KV_KEY_SCALE) != 0)
-    return fail(NOVA_KV_ERR_UNSUPPORTED, "flags 0x%x unsupported (0 or NOVA_KV_KEY_SCALE)", p->flags);
+  if ((p->flags & ~(NOVA_KV_KEY_SCALE | NOVA_KV_FP8_CODEBOOKS)) != 0)
+    return fail(NOVA_KV_ERR_UNSUPPORTED, "flags 0x%x unsupported (NOVA_KV_KEY_SCALE, NOVA_KV_FP8_CODEBOOKS)",
+                p->flags);
   if (!p->kbar || !p->cb_k || !p->cb_v) return fail(NOVA_KV_ERR_INVALID_ARG, "kbar/cb_k/cb_v is NULL");
   if (!aligned(p->cb_k, 16) || !aligned(p->cb_v, 16))
     return fail(NOVA_KV_ERR_INVALID_ARG, "codebooks must be 16-byte aligned");
@@ -141,6 +142,7 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
   a.t_v = p->t_v;
   a.cb_k = p->cb_k;
   a.cb_v = p->cb_v;
+  a.cb_fp8 = (p->flags & NOVA_KV_FP8_CODEBOOKS) ? 1 : 0;
   a.layout = to_layout(layout);
   a.k = k;
   a.v = v;
@@ -220,6 +222,7 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   a.t_v = p->t_v;
   a.cb_k = p->cb_k;
   a.cb_v = p->cb_v;
+  a.cb_fp8 = (p->flags & NOVA_KV_FP8_CODEBOOKS) ? 1 : 0;
   a.layout = to_layout(layout);
   a.q = q;
   a.q_bf16 = q_dtype == NOVA_KV_BF16;
@@ -316,6 +319,7 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
     ea.t_v = p->t_v;
     ea.cb_k = p->cb_k;
     ea.cb_v = p->cb_v;
+    ea.cb_fp8 = (p->flags & NOVA_KV_FP8_CODEBOOKS) ? 1 : 0;
     ea.layout = to_layout(layout);
     ea.k = k_new;
     ea.v = v_new;

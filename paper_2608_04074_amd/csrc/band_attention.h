@@ -16,7 +16,9 @@
 //    query split into a bf16 high part and a bf16 low part (rows h and GM + h
 //    of the A operand), so the products carry the query to 2^-17;
 //  * per head max and sum of exp(z - max), one wave per head;
-//  * values on the VALU in fp32: a lane holds two coordinates of one row.
+//  * values on the VALU in fp32: a lane holds two coordinates of one row;
+//  * the rows of a pass (the whole band at the usual sizes) are requested
+//    before anything waits for them.
 #pragma once
 
 #include "lut_common.h"
@@ -78,6 +80,38 @@ __device__ __forceinline__ void band_attention(const DecodeArgs &a, uint8_t *scr
     return (hb + band_slot(p, a.n_sink, a.n_rec)) * D;
   };
 
+  // Loads are issued a pass at a time, all before their first use: a pass
+  // covers 16 KT rows per wave for the keys and TPI VR rows per value wave.
+  // The first pass of both is requested before anything else, so the whole
+  // band of a usual size (up to 16 KT WAVES rows) costs one memory latency.
+  constexpr int KT = 2;
+  constexpr int HALF = D / 2, TPI = 64 / HALF;  // value rows per load instruction
+  constexpr int VR = 32;
+  const int m = lane & 15, kg = lane >> 4;
+  const int dp = lane % HALF, ts = lane / HALF;
+  const int ntile = (nb + 15) >> 4;
+  uint32_t vv[VR];
+  auto load_values = [&](const int base) {
+#pragma unroll
+    for (int j = 0; j < VR; ++j) {
+      const int i = base + TPI * (wave + VW * j) + ts;
+      vv[j] = (wave < VW && i < nb) ? *reinterpret_cast<const uint32_t *>(a.band_v + row_of(i) + 2 * dp) : 0u;
+    }
+  };
+  bf16x8_t kb[KT][D / 32];
+  auto load_keys = [&](const int tbase) {
+#pragma unroll
+    for (int u = 0; u < KT; ++u) {
+      // B column m = band row 16 tile + m (the last row repeats past nb)
+      const int i = min(16 * (tbase + wave + WAVES * u) + m, nb - 1);
+      const uint16_t *kr = a.band_k + row_of(i);
+#pragma unroll
+      for (int s = 0; s < D / 32; ++s) kb[u][s] = *reinterpret_cast<const bf16x8_t *>(kr + 32 * s + 8 * kg);
+    }
+  };
+  load_values(0);
+  load_keys(0);
+
   // ---- query in fp32
   for (int i = tid; i < GM * D; i += WAVES * 64) {
     const int h = i / D;
@@ -100,7 +134,6 @@ __device__ __forceinline__ void band_attention(const DecodeArgs &a, uint8_t *scr
     for (int j = 0; j < D / 64; ++j) x = fmaf(qf[h * D + lane + 64 * j], a.kbar[static_cast<size_t>(kv) * D + lane + 64 * j], x);
     qk[h] = wave_sum(x);
   }
-  const int m = lane & 15, kg = lane >> 4;
   bf16x8_t aq[D / 32];
 #pragma unroll
   for (int s = 0; s < D / 32; ++s) {
@@ -112,29 +145,28 @@ __device__ __forceinline__ void band_attention(const DecodeArgs &a, uint8_t *scr
       aq[s][e] = __builtin_bit_cast(__bf16, bits);
     }
   }
-  const int ntile = (nb + 15) >> 4;
-  for (int tt = wave; tt < ntile; tt += WAVES) {
-    const int i = min(16 * tt + m, nb - 1);  // B column m = band row 16 tt + m (the last row repeats past nb)
-    const uint16_t *kr = a.band_k + row_of(i);
-    bf16x8_t kb[D / 32];
+  for (int tbase = 0; tbase < ntile; tbase += KT * WAVES) {
+    if (tbase > 0) load_keys(tbase);
 #pragma unroll
-    for (int s = 0; s < D / 32; ++s) kb[s] = *reinterpret_cast<const bf16x8_t *>(kr + 32 * s + 8 * kg);
-    float4_t c = {0.f, 0.f, 0.f, 0.f};
+    for (int u = 0; u < KT; ++u) {
+      const int tt = tbase + wave + WAVES * u;
+      float4_t c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < D / 32; ++s) c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq[s], kb[s], c, 0, 0, 0);
-    // accumulator row r of lane group g = lane >> 4 is head 4g + r (high
-    // parts); the low parts sit 4 * GM lanes further
-    float zz[4];
+      for (int s = 0; s < D / 32; ++s) c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aq[s], kb[u][s], c, 0, 0, 0);
+      // accumulator row r of lane group kg is head 4 kg + r (high parts); the
+      // low parts sit 4 GM lanes further
+      float zz[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) zz[r] = c[r] + __shfl_down(c[r], 4 * GM, 64);
-    const int tok = 16 * tt + m;
-    if (lane < 4 * GM && tok < nb) {
+      for (int r = 0; r < 4; ++r) zz[r] = c[r] + __shfl_down(c[r], 4 * GM, 64);
+      const int tok = 16 * tt + m;
+      if (tt < ntile && lane < 4 * GM && tok < nb) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int h = 4 * kg + r;
-        float qkh = qk[r];
-        if constexpr (GM == 8) qkh = kg == 0 ? qk[r] : qk[4 + r];
-        zb[tok * GM + h] = h < G ? (zz[r] - qkh) * a.scale : 0.f;  // heads past G: never read
+        for (int r = 0; r < 4; ++r) {
+          const int h = 4 * kg + r;
+          float qkh = qk[r];
+          if constexpr (GM == 8) qkh = kg == 0 ? qk[r] : qk[4 + r];
+          zb[tok * GM + h] = h < G ? (zz[r] - qkh) * a.scale : 0.f;  // heads past G: never read
+        }
       }
     }
   }
@@ -159,24 +191,17 @@ __device__ __forceinline__ void band_attention(const DecodeArgs &a, uint8_t *scr
   }
   __syncthreads();
 
-  // ---- values: lane (ts, dp) takes coordinates 2dp, 2dp + 1 of rows
-  // i = TPI (wave + VW j) + ts, eight rows' loads in flight
-  constexpr int HALF = D / 2, TPI = 64 / HALF;
-  const int dp = lane % HALF, ts = lane / HALF;
+  // ---- values: lane (ts, dp) of value wave w takes coordinates 2dp, 2dp + 1
+  // of rows base + TPI (w + VW j) + ts
   if (wave < VW) {
     float acc[GM][2];
 #pragma unroll
     for (int h = 0; h < GM; ++h) acc[h][0] = acc[h][1] = 0.f;
-    for (int i0 = TPI * wave + ts; i0 < nb; i0 += 8 * VW * TPI) {
-      uint32_t vv[8];
+    for (int base = 0; base < nb; base += TPI * VW * VR) {
+      if (base > 0) load_values(base);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int i = i0 + j * VW * TPI;
-        vv[j] = i < nb ? *reinterpret_cast<const uint32_t *>(a.band_v + row_of(i) + 2 * dp) : 0u;
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int i = i0 + j * VW * TPI;
+      for (int j = 0; j < VR; ++j) {
+        const int i = base + TPI * (wave + VW * j) + ts;
         if (i < nb) {
           const float v0 = __uint_as_float(vv[j] << 16), v1 = __uint_as_float(vv[j] & 0xffff0000u);
 #pragma unroll

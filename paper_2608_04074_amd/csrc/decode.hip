@@ -97,13 +97,13 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
   }
 
   {
-    const uint4 *sk = reinterpret_cast<const uint4 *>(a.cb_k + static_cast<size_t>(kv) * CB);
-    const uint4 *sv = reinterpret_cast<const uint4 *>(a.cb_v + static_cast<size_t>(kv) * CB);
-    uint4 *dk = reinterpret_cast<uint4 *>(cbk);
-    uint4 *dv = reinterpret_cast<uint4 *>(cbv);
-    for (int i = tid; i < CB * 2 / 16; i += kThreads) {
-      dk[i] = sk[i];
-      dv[i] = sv[i];
+    // both codebooks into LDS as fp16 (fp8 codewords converted on the way)
+    const size_t cw0 = static_cast<size_t>(kv) * L * kCodebookSize;
+    uint2 *dk = reinterpret_cast<uint2 *>(cbk);
+    uint2 *dv = reinterpret_cast<uint2 *>(cbv);
+    for (int i = tid; i < L * kCodebookSize; i += kThreads) {
+      dk[i] = codeword(a.cb_k, a.cb_fp8, cw0 + i);
+      dv[i] = codeword(a.cb_v, a.cb_fp8, cw0 + i);
     }
     for (int i = tid; i < G * D; i += kThreads)
       qs[i / D][i % D] =

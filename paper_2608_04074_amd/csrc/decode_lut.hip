@@ -177,18 +177,18 @@ __device__ __forceinline__ void load_item_rows(const DecodeArgs &a, const int b,
 }
 
 // The codewords of the item's 8 groups.
+// (fp8: the codebook format, a compile-time constant at every call)
 __device__ __forceinline__ void load_item_cw(const DecodeArgs &a, const int kv, const int split, const int n_eff,
-                                             const int k, const int t, ItemRegs &r) {
+                                             const int k, const int t, ItemRegs &r, const bool fp8) {
   const int item = split + k * n_eff;
   const int side = item >> 2, blk = item & 3;
-  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * kL * 256 * 4;
-  encblk::load_codewords(t, cbg, blk, r.cw);
+  encblk::load_codewords(t, side == 0 ? a.cb_k : a.cb_v, fp8, static_cast<size_t>(kv) * kL * 256, blk, r.cw);
 }
 
 __device__ __forceinline__ void load_item(const DecodeArgs &a, const int b, const int kv, const int split,
-                                          const int n_eff, const int k, const int t, ItemRegs &r) {
+                                          const int n_eff, const int k, const int t, ItemRegs &r, const bool fp8) {
   load_item_rows(a, b, kv, split, n_eff, k, t, r);
-  load_item_cw(a, kv, split, n_eff, k, t, r);
+  load_item_cw(a, kv, split, n_eff, k, t, r, fp8);
 }
 
 // Team meetings of the encode: two per item (its x in LDS, then the wave
@@ -208,7 +208,7 @@ __device__ __forceinline__ int team_phases(const int split, const int n_eff) {
 // each key block's head h over the groups in order, into res[32 k + h].
 __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                              const int split, const int n_eff, const size_t tokoff, const int t,
-                                             ItemRegs &r) {
+                                             ItemRegs &r, const bool fp8) {
   encblk::Scratch<kD> *sc = reinterpret_cast<encblk::Scratch<kD> *>(smem + kAppendScratch);  // [2]
   float *res = reinterpret_cast<float *>(smem + kItemRes);
   uint64_t *xn = a.xnew + static_cast<size_t>(b * a.num_kv_heads + kv) * 8 * 32;
@@ -223,7 +223,7 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
     team_sync(smem, ++phase);
     encblk::partial_block<kD>(t, s, ri.trow);
     team_sync(smem, ++phase);
-    const int code = encblk::search_block<kD>(t, s, ri.cw);
+    const int code = encblk::search_block<kD>(t, s, ri.cw, fp8);
     const int gl = t >> 5, lr = t & 31;
     const int g = encblk::kGroups * blk + gl;
     if (lr == 0) (side == 0 ? a.k_codes_w : a.v_codes_w)[tokoff + g] = static_cast<uint8_t>(code);
@@ -252,7 +252,7 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
   }
 #else
   for (int k = 0; k < nmine; ++k) {
-    if (k > 0) load_item(a, b, kv, split, n_eff, k, t, r);
+    if (k > 0) load_item(a, b, kv, split, n_eff, k, t, r, fp8);
     encode_one(k, r);
   }
 #endif
@@ -268,7 +268,7 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
   }
 }
 
-template <int WAVES, bool APPEND, bool KS>
+template <int WAVES, bool APPEND, bool KS, bool FP8>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int split, const int t0, const int t1, const size_t row0,
                                            const int rot, const int n_eff, const int S, float4 (&tv)[8]) {
@@ -383,14 +383,16 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     const int lg = 16 * (wave & 1) + (lane >> 2);  // this lane's group
     const int lj = lane & 3;                       // head (A operand) / code in a quad (B, D)
     const int cbase = 64 * (wave >> 1);
-    const uint2 *cbk = reinterpret_cast<const uint2 *>(a.cb_k + static_cast<size_t>(kv) * kL * 256 * 4);
+    // codewords as raw words (fp16, or fp8 bytes converted where they are used)
+    constexpr bool fp8 = FP8;
+    const void *cbk = codebook_from(a.cb_k, fp8, static_cast<size_t>(kv) * kL * 256);
+    const void *cbv = codebook_from(a.cb_v, fp8, static_cast<size_t>(kv) * kL * 256);
     uint2 kst[16];
     if (lut_wave) {
 #pragma unroll
-      for (int t = 0; t < 16; ++t) kst[t] = cbk[lg * 256 + cbase + 4 * ((t + rot) & 15) + lj];
+      for (int t = 0; t < 16; ++t) kst[t] = codeword_raw(cbk, fp8, lg * 256 + cbase + 4 * ((t + rot) & 15) + lj);
     }
     constexpr int VPER = (kL * 256 + NT - 1) / NT;
-    const uint2 *vsrc = reinterpret_cast<const uint2 *>(a.cb_v + static_cast<size_t>(kv) * kL * 256 * 4);
     auto vmap = [](int e, int &g, int &c) {
       const int r = e >> 5;
       g = 8 * ((e >> 3) & 3) + (r & 7);
@@ -406,7 +408,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     for (int k = 0; k < VPER; ++k) {
       int g, c;
       vmap((tid + k * NT + vrot) & (kL * 256 - 1), g, c);
-      vst[k] = vsrc[g * 256 + c];
+      vst[k] = codeword_raw(cbv, fp8, g * 256 + c);
     }
     // waves 8 .. 8+G-1 form the shifted sink logit of head wave-8 (Lemma S1)
     const int sh = wave - 8;
@@ -426,7 +428,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     for (int k = 0; k < VPER; ++k) {
       int g, c;
       vmap((tid + k * NT + vrot) & (kL * 256 - 1), g, c);
-      *reinterpret_cast<uint2 *>(smem + kVBase + (g & 7) * 8192 + (c << 5) + 8 * (g >> 3)) = vst[k];
+      *reinterpret_cast<uint2 *>(smem + kVBase + (g & 7) * 8192 + (c << 5) + 8 * (g >> 3)) = codeword_f16(vst[k], fp8);
     }
     __syncthreads();
     if (sh >= 0 && sh < G) {
@@ -461,7 +463,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       }
     } else if constexpr (APPEND) {
       // the encoder team requests its first item; the table build covers the latency
-      if (n_eff > 0) load_item(a, b, kv, split, n_eff, 0, tid - 512, ir);
+      if (n_eff > 0) load_item(a, b, kv, split, n_eff, 0, tid - 512, ir, FP8);
     }
     __syncthreads();
     if (lut_wave) {
@@ -497,7 +499,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
         uint2 o[2];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
-          const half4_t bv = __builtin_bit_cast(half4_t, kst[t + u]);
+          const half4_t bv = __builtin_bit_cast(half4_t, codeword_f16(kst[t + u], fp8));
           float4_t c = {0.f, 0.f, 0.f, 0.f};
           c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_hi, bv, c, 0, 0, 0);
           c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_lo, bv, c, 0, 0, 0);
@@ -525,7 +527,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     if (n_eff > 0 && wave >= 8) {
       const int p = S - 1;
       const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
-      encode_items(a, smem, b, kv, split, n_eff, tokoff, tid - 512, ir);
+      encode_items(a, smem, b, kv, split, n_eff, tokoff, tid - 512, ir, FP8);
     }
   }
 
@@ -982,7 +984,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
 // partial to the exchange and counts its arrival; the last one combines.
 // The arrival counters live in the workspace and the last split resets its
 // counter to 0, so a decode step is a single launch.
-template <int WAVES, bool APPEND, bool KS>
+template <int WAVES, bool APPEND, bool KS, bool FP8>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   static_assert(!(APPEND && KS), "the fused step serves the plain format only");
   static_assert(WAVES == 12, "the exchange roles assume 12 waves");
@@ -1018,7 +1020,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   }
 
   float4 tv[8];
-  split_pass<WAVES, APPEND, KS>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
+  split_pass<WAVES, APPEND, KS, FP8>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
   int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
   __syncthreads();  // the split's partial and its blocks of the new token are in LDS; the count is known
   if (a.n_split > 1) {
@@ -1086,12 +1088,22 @@ hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream) {
   constexpr int W = 12;
   const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
   if (a.append && (a.k_scales || a.band_k)) return hipErrorInvalidValue;
-  if (a.append)
-    decode_lut_d128<W, true, false><<<grid, dim3(W * 64), 0, stream>>>(a);
-  else if (a.k_scales)
-    decode_lut_d128<W, false, true><<<grid, dim3(W * 64), 0, stream>>>(a);
-  else
-    decode_lut_d128<W, false, false><<<grid, dim3(W * 64), 0, stream>>>(a);
+  const dim3 block(W * 64);
+  if (a.cb_fp8) {
+    if (a.append)
+      decode_lut_d128<W, true, false, true><<<grid, block, 0, stream>>>(a);
+    else if (a.k_scales)
+      decode_lut_d128<W, false, true, true><<<grid, block, 0, stream>>>(a);
+    else
+      decode_lut_d128<W, false, false, true><<<grid, block, 0, stream>>>(a);
+  } else {
+    if (a.append)
+      decode_lut_d128<W, true, false, false><<<grid, block, 0, stream>>>(a);
+    else if (a.k_scales)
+      decode_lut_d128<W, false, true, false><<<grid, block, 0, stream>>>(a);
+    else
+      decode_lut_d128<W, false, false, false><<<grid, block, 0, stream>>>(a);
+  }
   return hipGetLastError();
 }
 

@@ -82,7 +82,7 @@ __device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, 
   }
 }
 
-template <int WAVES, bool KS>
+template <int WAVES, bool KS, bool FP8>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int t0, const int t1, const size_t row0, float4 (&tv)[4]) {
   const uint32_t sbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8_ptr)smem));
@@ -175,7 +175,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       for (int r = 0; r < 4; ++r) trow[r] = tk[r * (kD / 4)];
     }
     constexpr int VPER = (kL * 256 + NT - 1) / NT;
-    const uint2 *vsrc = reinterpret_cast<const uint2 *>(a.cb_v + static_cast<size_t>(kv) * kL * 256 * 4);
+    // codewords as raw words (fp16, or fp8 bytes converted where they are used)
+    constexpr bool fp8 = FP8;
+    const void *cbk = codebook_from(a.cb_k, fp8, static_cast<size_t>(kv) * kL * 256);
+    const void *cbv = codebook_from(a.cb_v, fp8, static_cast<size_t>(kv) * kL * 256);
     // element e -> (g, c) so that each half-wave writes 32 distinct bank pairs
     auto vmap = [](int e, int &g, int &c) {
       const int r = e >> 5;
@@ -189,7 +192,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       if (e < kL * 256) {
         int g, c;
         vmap(e, g, c);
-        vst[k] = vsrc[g * 256 + c];
+        vst[k] = codeword_raw(cbv, fp8, g * 256 + c);
       }
     }
     // table waves: groups 8*(wave & 1) .. +7, codes 64*(wave >> 1) .. +63; 4-lane
@@ -200,11 +203,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     const int lh = blk & 1;
     const int lj = lane & 3;
     const int cbase = 64 * (wave >> 1);
-    const uint2 *cbk = reinterpret_cast<const uint2 *>(a.cb_k + static_cast<size_t>(kv) * kL * 256 * 4);
     uint2 kst[16];
     if (lut_wave) {
 #pragma unroll
-      for (int t = 0; t < 16; ++t) kst[t] = cbk[lg * 256 + cbase + 4 * t + lj];
+      for (int t = 0; t < 16; ++t) kst[t] = codeword_raw(cbk, fp8, lg * 256 + cbase + 4 * t + lj);
     }
     // waves 8..11 form the shifted sink logits of heads 2(wave-8), 2(wave-8)+1
     const int sh = 2 * (wave - 8);
@@ -219,7 +221,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       if (e < kL * 256) {
         int g, c;
         vmap(e, g, c);
-        *reinterpret_cast<uint2 *>(smem + kVBase + (g & 3) * 8192 + (c << 5) + 8 * (g >> 2)) = vst[k];
+        *reinterpret_cast<uint2 *>(smem + kVBase + (g & 3) * 8192 + (c << 5) + 8 * (g >> 2)) = codeword_f16(vst[k], fp8);
       }
     }
     __syncthreads();
@@ -280,7 +282,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       }
 #pragma unroll
       for (int t = 0; t < 16; ++t) {
-        const half4_t bv = __builtin_bit_cast(half4_t, kst[t]);
+        const half4_t bv = __builtin_bit_cast(half4_t, codeword_f16(kst[t], fp8));
         float4_t c = {0.f, 0.f, 0.f, 0.f};
         c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_hi, bv, c, 0, 0, 0);
         c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_lo, bv, c, 0, 0, 0);
@@ -577,7 +579,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
 // One workgroup per (sequence, KV head, split); the arrival protocol is the
 // one of the head_dim-128 kernel (relaxed agent-scope partials and counters,
 // the last split combines, a split finding all others arrived does not publish).
-template <int WAVES, bool KS>
+template <int WAVES, bool KS, bool FP8>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
   const int tid = threadIdx.x;
@@ -599,7 +601,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
 
   float4 tv[4];
   if (active) {
-    split_pass<WAVES, KS>(a, smem, b, kv, t0, t1, row0, tv);
+    split_pass<WAVES, KS, FP8>(a, smem, b, kv, t0, t1, row0, tv);
   } else {
     load_tv_rows(a, kv, tv);
   }
@@ -646,10 +648,13 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
 hipError_t launch_decode_lut64(const DecodeArgs &a, hipStream_t stream) {
   constexpr int W = 16;  // 4 waves per SIMD: the kernel fits in 128 VGPRs
   const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
+  const dim3 block(W * 64);
   if (a.k_scales)
-    decode_lut_d64<W, true><<<grid, dim3(W * 64), 0, stream>>>(a);
+    a.cb_fp8 ? decode_lut_d64<W, true, true><<<grid, block, 0, stream>>>(a)
+             : decode_lut_d64<W, true, false><<<grid, block, 0, stream>>>(a);
   else
-    decode_lut_d64<W, false><<<grid, dim3(W * 64), 0, stream>>>(a);
+    a.cb_fp8 ? decode_lut_d64<W, false, true><<<grid, block, 0, stream>>>(a)
+             : decode_lut_d64<W, false, false><<<grid, block, 0, stream>>>(a);
   return hipGetLastError();
 }
 

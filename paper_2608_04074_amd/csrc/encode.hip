@@ -42,7 +42,7 @@ __device__ __forceinline__ uint16_t input_bf16_bits(const EncodeArgs &a, const v
 // fetches a quarter (D=128) or half (D=64) of the parameters, all loads
 // coalesced and issued before the first use; the launch costs about one
 // memory latency.  The block itself is encode_block.h's team computation.
-template <int D>
+template <int D, bool FP8>
 __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   constexpr int L = D / kGroupDim;
   constexpr int NB = L / encblk::kGroups;  // group blocks per token
@@ -53,13 +53,14 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   const int kv = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
   const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D;
-  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * L * kCodebookSize * kGroupDim;
+  const void *cb = side == 0 ? a.cb_k : a.cb_v;
+  const size_t cw0 = static_cast<size_t>(kv) * L * kCodebookSize;
   const void *src = side == 0 ? a.k : a.v;
   uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
 
   float4 trow[D / 32];
   uint2 cw[encblk::kPer];
-  encblk::load_block<D>(tid, tm, cbg, blk, trow, cw);
+  encblk::load_block<D>(tid, tm, cb, FP8, cw0, blk, trow, cw);
   if (tid < D) {
     const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + tid;
     double x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
@@ -100,12 +101,12 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
       const double u = us[encblk::kCols * blk + 4 * (tid >> 5) + i];
       uu[i] = rho > 0.0 ? u / rho : 0.0;
     }
-    code = encblk::search_codes(tid, uu, cw);
+    code = encblk::search_codes(tid, uu, cw, FP8);
     if (blk == 0 && tid == 0) a.k_scales[off / L] = encblk::bf16_of(rho);
   } else {
     encblk::partial_block<D>(tid, sc, trow);
     __syncthreads();
-    code = encblk::search_block<D>(tid, sc, cw);
+    code = encblk::search_block<D>(tid, sc, cw, FP8);
   }
   if ((tid & 31) == 0) pool[off + encblk::kGroups * blk + (tid >> 5)] = static_cast<uint8_t>(code);
 }
@@ -125,7 +126,7 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
 // LDS rows are padded by two doubles so the operand reads hit distinct banks.
 // Operand layout of v_mfma_f64_16x16x4f64 (measured): A[m][k] in lane 16k + m,
 // B[k][n] in lane 16k + n, D[m][n] in lane 16 (m mod 4) + n, register m / 4.
-template <int D>
+template <int D, bool FP8>
 __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   constexpr int L = D / kGroupDim;
   constexpr int TT = 32;                 // tokens per workgroup
@@ -144,7 +145,9 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   const int n0 = tile * TT;
   const int nt = min(TT, a.n_new - n0);
   const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D;
-  const uint16_t *cbg = (side == 0 ? a.cb_k : a.cb_v) + static_cast<size_t>(kv) * L * kCodebookSize * kGroupDim;
+  const void *cb = side == 0 ? a.cb_k : a.cb_v;
+  const size_t cw0 = static_cast<size_t>(kv) * L * kCodebookSize;
+  constexpr bool fp8 = FP8;
   const void *src = side == 0 ? a.k : a.v;
   uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
 
@@ -218,12 +221,15 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
 
   // ---- nearest codeword: wave w takes groups w, w+4, ...
   for (int g = wave; g < L; g += 4) {
-    const uint2 *cw = reinterpret_cast<const uint2 *>(cbg) + static_cast<size_t>(g) * kCodebookSize;
+    const size_t gcw = cw0 + static_cast<size_t>(g) * kCodebookSize;
     // A operands: coordinate q of codewords 16t + m
     double ac[16];
 #pragma unroll
-    for (int t = 0; t < 16; ++t)
-      ac[t] = static_cast<double>(half_bits_to_float(cbg[(static_cast<size_t>(g) * kCodebookSize + 16 * t + m) * 4 + q]));
+    for (int t = 0; t < 16; ++t) {
+      const uint2 w = codeword(cb, fp8, gcw + 16 * t + m);
+      const uint32_t h2 = q < 2 ? w.x : w.y;
+      ac[t] = static_cast<double>(half_bits_to_float(static_cast<uint16_t>((q & 1) ? (h2 >> 16) : (h2 & 0xffffu))));
+    }
     // offset: the largest |u_g|^2 of the tile (uniform)
     double un = 0.0;
     if (lane < TT) {
@@ -241,7 +247,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int c = 4 * lane + j;
-      const uint2 w = cw[c];
+      const uint2 w = codeword(cb, fp8, gcw + c);
       const double c0 = half_bits_to_float(static_cast<uint16_t>(w.x & 0xffff));
       const double c1 = half_bits_to_float(static_cast<uint16_t>(w.x >> 16));
       const double c2 = half_bits_to_float(static_cast<uint16_t>(w.y & 0xffff));
@@ -289,10 +295,16 @@ template <int D>
 hipError_t launch_encode_d(const EncodeArgs &a, hipStream_t stream) {
   if (a.n_new <= 4) {
     const dim3 grid(2 * a.n_new * (D / kGroupDim / 8), a.num_kv_heads, a.batch);
-    encode_small<D><<<grid, dim3(256), 0, stream>>>(a);
+    if (a.cb_fp8)
+      encode_small<D, true><<<grid, dim3(256), 0, stream>>>(a);
+    else
+      encode_small<D, false><<<grid, dim3(256), 0, stream>>>(a);
   } else {
     const dim3 grid((a.n_new + 31) / 32, a.num_kv_heads, 2 * a.batch);
-    encode_bulk<D><<<grid, dim3(256), 0, stream>>>(a);
+    if (a.cb_fp8)
+      encode_bulk<D, true><<<grid, dim3(256), 0, stream>>>(a);
+    else
+      encode_bulk<D, false><<<grid, dim3(256), 0, stream>>>(a);
   }
   return hipGetLastError();
 }

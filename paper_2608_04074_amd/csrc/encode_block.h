@@ -37,7 +37,9 @@ struct Scratch {
 
 // Phase 1 (issue only): the block's transform columns and codewords.
 //   tm  = side transform of the KV head ([D][D] fp32, row-major)
-//   cbg = side codebooks of the KV head ([L][256][4] fp16)
+//   cb, fp8, cw0 = side codebooks ([Hkv][L][256] codewords, fp16 or fp8) and
+//         the index of the KV head's first codeword; the raw words are kept
+//         and converted where they are used
 template <int D>
 __device__ __forceinline__ void load_rows(const int t, const float *tm, const int blk, float4 (&trow)[D / 32]) {
   constexpr int RPT = D / 32;
@@ -46,17 +48,19 @@ __device__ __forceinline__ void load_rows(const int t, const float *tm, const in
 #pragma unroll
   for (int j = 0; j < RPT; ++j) trow[j] = *reinterpret_cast<const float4 *>(col + (RPT * rg + j) * D);
 }
-__device__ __forceinline__ void load_codewords(const int t, const uint16_t *cbg, const int blk, uint2 (&cw)[kPer]) {
+__device__ __forceinline__ void load_codewords(const int t, const void *cb, const bool fp8, const size_t cw0,
+                                               const int blk, uint2 (&cw)[kPer]) {
   const int gl = t >> 5, r = t & 31;
-  const uint2 *row = reinterpret_cast<const uint2 *>(cbg) + (kGroups * blk + gl) * kCodebookSize;
+  const size_t row = cw0 + static_cast<size_t>(kGroups * blk + gl) * kCodebookSize;
 #pragma unroll
-  for (int k = 0; k < kPer; ++k) cw[k] = row[r + 32 * k];
+  for (int k = 0; k < kPer; ++k) cw[k] = codeword_raw(cb, fp8, row + r + 32 * k);
 }
 template <int D>
-__device__ __forceinline__ void load_block(const int t, const float *tm, const uint16_t *cbg, const int blk,
-                                           float4 (&trow)[D / 32], uint2 (&cw)[kPer]) {
+__device__ __forceinline__ void load_block(const int t, const float *tm, const void *cb, const bool fp8,
+                                           const size_t cw0, const int blk, float4 (&trow)[D / 32],
+                                           uint2 (&cw)[kPer]) {
   load_rows<D>(t, tm, blk, trow);
-  load_codewords(t, cbg, blk, cw);
+  load_codewords(t, cb, fp8, cw0, blk, cw);
 }
 
 // Phase 2 (after x is in LDS): this wave's share of the 32 coefficients.
@@ -89,7 +93,8 @@ __device__ __forceinline__ void partial_block(const int t, Scratch<D> &s, const 
 
 // Nearest codeword of group t >> 5 to the coefficients u, returned in all 32
 // lanes of the group: fp64 distances, the smallest index among equal ones.
-__device__ __forceinline__ int search_codes(const int t, const double (&u)[4], const uint2 (&cw)[kPer]) {
+__device__ __forceinline__ int search_codes(const int t, const double (&u)[4], const uint2 (&cw)[kPer],
+                                            const bool fp8) {
   const int r = t & 31;
   const double u0 = u[0], u1 = u[1], u2 = u[2], u3 = u[3];
   double best = INFINITY;
@@ -98,7 +103,7 @@ __device__ __forceinline__ int search_codes(const int t, const double (&u)[4], c
   for (int k = 0; k < kPer; ++k) {
 #pragma clang fp contract(off)
     const int c = r + 32 * k;
-    const uint2 w = cw[k];
+    const uint2 w = codeword_f16(cw[k], fp8);
     const double e0 = u0 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.x & 0xffff)));
     const double e1 = u1 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.x >> 16)));
     const double e2 = u2 - static_cast<double>(half_bits_to_float(static_cast<uint16_t>(w.y & 0xffff)));
@@ -133,12 +138,13 @@ __device__ __forceinline__ double coefficient(const Scratch<D> &s, const int c) 
 // Phase 3 (after the partials are in LDS): nearest codeword of group t >> 5,
 // returned in all 32 lanes of the group.
 template <int D>
-__device__ __forceinline__ int search_block(const int t, const Scratch<D> &s, const uint2 (&cw)[kPer]) {
+__device__ __forceinline__ int search_block(const int t, const Scratch<D> &s, const uint2 (&cw)[kPer],
+                                            const bool fp8) {
   const int gl = t >> 5;
   double uu[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) uu[i] = coefficient<D>(s, gl * 4 + i);
-  return search_codes(t, uu, cw);
+  return search_codes(t, uu, cw, fp8);
 }
 
 // Key-scale format: rho = sqrt(sum of the squared coefficients, added in

@@ -31,7 +31,8 @@ __device__ __forceinline__ size_t code_row_offset(const CacheLayout &lay, int nu
 struct DecodeArgs {
   int batch, num_q_heads, num_kv_heads, head_dim, gqa;
   const float *kbar, *t_k_inv_t, *t_v;
-  const uint16_t *cb_k, *cb_v;
+  const void *cb_k, *cb_v;  // [Hkv][L][256] codewords: 4 fp16, or 4 fp8 E4M3 when cb_fp8
+  int cb_fp8;
   CacheLayout layout;
   const void *q;
   int q_bf16;
@@ -80,7 +81,8 @@ constexpr int kXchSlotWords = 16 + 512;
 struct EncodeArgs {
   int batch, n_new, num_kv_heads, head_dim;
   const float *kbar, *t_k, *t_v;
-  const uint16_t *cb_k, *cb_v;
+  const void *cb_k, *cb_v;  // [Hkv][L][256] codewords: 4 fp16, or 4 fp8 E4M3 when cb_fp8
+  int cb_fp8;
   CacheLayout layout;
   const void *k, *v;
   int in_bf16;
@@ -147,6 +149,32 @@ __device__ __forceinline__ float half_bits_to_float(uint16_t h) {
 
 __device__ __forceinline__ float bf16_bits_to_float(uint16_t h) {
   return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// Raw words of codeword `idx` (an index over [Hkv][L][256]): both words of 4
+// fp16, or the 4 fp8 bytes in .x.  One load either way.
+__device__ __forceinline__ uint2 codeword_raw(const void *cb, const int fp8, const size_t idx) {
+  if (fp8) return make_uint2(static_cast<const uint32_t *>(cb)[idx], 0u);
+  return static_cast<const uint2 *>(cb)[idx];
+}
+// The 4 fp16 coordinates (bit patterns, two per word) of a raw codeword.
+// fp8 bytes are OCP E4M3 (sign, 4 exponent bits with bias 7, 3 mantissa
+// bits, no infinities); every such value is exact in fp16, and the
+// gfx950 conversion with scale 1 gives it exactly, two bytes per instruction.
+__device__ __forceinline__ uint2 codeword_f16(const uint2 raw, const int fp8) {
+  if (!fp8) return raw;
+  typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+  const f16x2_t lo = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(raw.x, 1.0f, false);
+  const f16x2_t hi = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(raw.x, 1.0f, true);
+  return make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+}
+__device__ __forceinline__ uint2 codeword(const void *cb, const int fp8, const size_t idx) {
+  return codeword_f16(codeword_raw(cb, fp8, idx), fp8);
+}
+// The codebook from codeword idx on (so that later indices stay small).
+__device__ __forceinline__ const void *codebook_from(const void *cb, const int fp8, const size_t idx) {
+  return fp8 ? static_cast<const void *>(static_cast<const uint32_t *>(cb) + idx)
+             : static_cast<const void *>(static_cast<const uint2 *>(cb) + idx);
 }
 
 }  // namespace novakv
