@@ -38,7 +38,8 @@ DECODE_KERNEL = "decode_lut_d128"
 # The step kernel's source and the headers it includes: a change to any of
 # them invalidates the committed counter summary.
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_04074_amd", "csrc", f)
-                  for f in ("decode_lut.hip", "encode_block.h", "lut_common.h", "nova_kv_internal.h")]
+                  for f in ("decode_lut.hip", "band_attention.h", "encode_block.h", "lut_common.h",
+                            "nova_kv_internal.h")]
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_lut_d128_qwen3_8b_traffic.md")
 COPY_CALIB_BYTES = 256 << 20
 
@@ -297,6 +298,17 @@ def main():
     dec_mean_us = float(np.mean(dec_runs))
     dec_med_us = float(np.median(dec_runs))
     enc_us = np.array(enc_runs)
+    # the same step with the codebooks in the paper's stored format: rounded to
+    # fp8 E4M3 (torch's conversion) and passed as bytes
+    p8 = dict(params)
+    for k in ("cb_k", "cb_v"):
+        p8[k] = torch.as_tensor(params[k]).to(torch.float32).to(torch.float8_e4m3fn).view(torch.uint8)
+    P8 = nk.NovaKVParams.from_arrays(p8, device=dev)
+    step8_calls = [nk.prepare_append_decode(P8, layout, k_new[:, 0], v_new[:, 0], q, pk, pv, seq_lens, S, out, ws)
+                   for pk, pv in pools]
+    for i in range(200):
+        step8_calls[i % COPIES]()
+    step8_runs = [timed(lambda i: step8_calls[i % COPIES](), args.steps) for _ in range(n_runs)]
 
     value = code_bytes / (ms_step * 1e-3) / 1e9
     step_mean_us = float(np.mean(step_runs))
@@ -371,6 +383,8 @@ def main():
                            "min_of_runs": round(float(np.min(step_runs)), 2),
                            "max_of_runs": round(float(np.max(step_runs)), 2),
                            "runs": len(step_runs), "calls_per_run": args.steps},
+        "step_fp8_codebooks_us": {"mean": round(float(np.mean(step8_runs)), 2),
+                                  "median_of_runs": round(float(np.median(step8_runs)), 2)},
         "two_call_step_us": round(two_call_us, 2),
         "decode_kernel_us": {"mean": round(dec_mean_us, 2), "median_of_runs": round(dec_med_us, 2),
                              "min_of_runs": round(float(np.min(dec_runs)), 2),
@@ -379,7 +393,7 @@ def main():
         "append_kernel_us": {"mean": round(float(np.mean(enc_us)), 2),
                              "median_of_runs": round(float(np.median(enc_us)), 2)},
         "roofline": {
-            "kernel": f"{DECODE_KERNEL}<12, true, false> (the step's one launch: encode of the new token, query "
+            "kernel": f"{DECODE_KERNEL}<12, true, false, false> (the step's one launch: encode of the new token, query "
                       "transform, split pass, combine)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
