@@ -29,6 +29,10 @@ positions [S - n_rec, S) of a sequence of S cached tokens; the band applies
 inside the attended range (a window may cut it); band keys enter the logit as
 they are (no k_bar shift in the plain form, which holds no shift at all).
 
+Scalar value arm (Sec. "Bit rate"; implementation table: per-token affine
+INT2 values): v_hat = (offset + scale * q) t_v^T with the stored bf16 offset
+and scale of the token (oracle/codec.py holds the encoder).
+
 Fast form -- for self-consistency only (Algorithm 1 inference step; Sec.
 "Decoding kernel and read path"; sinks appendix): q' = q R_K^{-T} * scale,
 logit = q' . r_hat (k_bar dropped, Lemma S1), sink shifted by -(q . k_bar) * scale,
@@ -42,6 +46,7 @@ from typing import Optional, Sequence
 
 import numpy as np
 
+from .codec import sq_reconstruct
 from .vq import lookup
 
 
@@ -79,9 +84,14 @@ def reconstruct_keys(codes_k: np.ndarray, cb_k: np.ndarray, t_k_inv_t: np.ndarra
     return r_hat @ np.asarray(t_k_inv_t, dtype=np.float64).T + np.asarray(kbar, dtype=np.float64)
 
 
-def reconstruct_values(codes_v: np.ndarray, cb_v: np.ndarray, t_v: np.ndarray) -> np.ndarray:
-    """v_hat = Q(s) R_V^T for every row of codes (n, L)."""
-    s_hat = lookup(codes_v, cb_v)
+def reconstruct_values(codes_v: np.ndarray, cb_v: np.ndarray, t_v: np.ndarray, sq=None) -> np.ndarray:
+    """v_hat = Q(s) R_V^T for every row of codes (n, L).  With sq = (scale bits
+    (n,), offset bits (n,)) the codes are the scalar value arm's packed INT2
+    and Q(s) = offset + scale * q (cb_v unused)."""
+    if sq is not None:
+        s_hat = sq_reconstruct(codes_v, sq[0], sq[1])
+    else:
+        s_hat = lookup(codes_v, cb_v)
     return s_hat @ np.asarray(t_v, dtype=np.float64).T
 
 
@@ -119,13 +129,15 @@ def decode_row(q: np.ndarray, codes_k: np.ndarray, codes_v: np.ndarray, params_h
 def decode_rows(q_heads: np.ndarray, codes_k: np.ndarray, codes_v: np.ndarray,
                 params_head: dict, scale: float, window: int = 0,
                 sinks: Optional[Sequence[float]] = None,
-                scales_k: Optional[np.ndarray] = None, band=None) -> np.ndarray:
+                scales_k: Optional[np.ndarray] = None, band=None, sq_v=None) -> np.ndarray:
     """Plain-form outputs of the G query heads sharing one KV head: q_heads (G, D) -> (G, D).
-    band as in decode_row."""
+    band as in decode_row; sq_v = (scale bits (S,), offset bits (S,)) for the
+    scalar value arm (codes_v then holds packed INT2, (S, D/4))."""
     lo, hi = attended_range(codes_k.shape[0], window)
     k_hat = reconstruct_keys(codes_k[lo:hi], params_head["cb_k"], params_head["t_k_inv_t"],
                              params_head["kbar"], None if scales_k is None else scales_k[lo:hi])
-    v_hat = reconstruct_values(codes_v[lo:hi], params_head["cb_v"], params_head["t_v"])
+    v_hat = reconstruct_values(codes_v[lo:hi], params_head.get("cb_v"), params_head["t_v"],
+                               None if sq_v is None else (sq_v[0][lo:hi], sq_v[1][lo:hi]))
     k_hat, v_hat = _with_band(k_hat, v_hat, lo, hi, band)
     out = np.empty((q_heads.shape[0], v_hat.shape[1]))
     for h in range(q_heads.shape[0]):

@@ -81,6 +81,50 @@ def encode_tokens_scaled(k: np.ndarray, v: np.ndarray, params_head: dict):
     return ck, gk, bf16_bits(rho), cv, gv, rho
 
 
+# ---------------------------------------------------------------------------
+# Scalar value arm (paper: Sec. "Bit rate": INT2 values with a BF16 scale and
+# offset per token; the implementation table: per-token affine INT2; Sec.
+# "Decoding kernel and read path": dequantized in the rotation basis whose
+# inverse is applied after the attention sum).  The rotation is the stored
+# value transform t_v (any orthogonal matrix: R_V, or a Hadamard rotation).
+# Readings fixed here: min-max affine grid over the D coordinates of a token,
+# offset = bf16(min), scale = bf16((max - min) / 3) (fp64 arithmetic, each
+# rounded to fp32 then to bf16, to nearest even); the codes use the stored
+# offset and scale: q_i = clamp(round_half_even((s_i - offset) / scale), 0, 3),
+# all codes 0 when the stored scale is 0; coordinate 4g + j of a token is
+# stored in bits 2j, 2j + 1 of its byte g.
+# ---------------------------------------------------------------------------
+
+def sq_encode_values(v: np.ndarray, t_v: np.ndarray):
+    """Per-token affine INT2 of s = v t_v: (packed bytes (n, D/4) uint8, scale bits (n,), offset bits (n,))."""
+    s = value_coefficients(v, t_v)
+    mn = s.min(axis=1)
+    mx = s.max(axis=1)
+    zero_bits = bf16_bits(mn)
+    scale_bits = bf16_bits((mx - mn) / 3.0)
+    zero = bf16_value(zero_bits)[:, None]
+    scale = bf16_value(scale_bits)[:, None]
+    safe = np.where(scale > 0, scale, 1.0)
+    q = np.where(scale > 0, np.clip(np.rint((s - zero) / safe), 0, 3), 0).astype(np.uint8)
+    n, d = q.shape
+    qg = q.reshape(n, d // 4, 4)
+    packed = (qg[..., 0] | (qg[..., 1] << 2) | (qg[..., 2] << 4) | (qg[..., 3] << 6)).astype(np.uint8)
+    return packed, scale_bits, zero_bits
+
+
+def sq_unpack(packed: np.ndarray) -> np.ndarray:
+    """INT2 codes (n, D) of packed bytes (n, D/4)."""
+    p = np.asarray(packed, dtype=np.uint8)
+    q = np.stack([(p >> (2 * j)) & 3 for j in range(4)], axis=-1)
+    return q.reshape(p.shape[0], -1)
+
+
+def sq_reconstruct(packed: np.ndarray, scale_bits: np.ndarray, zero_bits: np.ndarray) -> np.ndarray:
+    """s_hat = offset + scale * q per token (rotation basis), fp64."""
+    q = sq_unpack(packed).astype(np.float64)
+    return bf16_value(zero_bits)[:, None] + bf16_value(scale_bits)[:, None] * q
+
+
 def encode_tokens(k: np.ndarray, v: np.ndarray, params_head: dict):
     """Codes and near-tie gaps of n keys and values (n, D) of one KV head.
 
