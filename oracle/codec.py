@@ -116,7 +116,7 @@ def sq_unpack(packed: np.ndarray) -> np.ndarray:
     """INT2 codes (n, D) of packed bytes (n, D/4)."""
     p = np.asarray(packed, dtype=np.uint8)
     q = np.stack([(p >> (2 * j)) & 3 for j in range(4)], axis=-1)
-    return q.reshape(p.shape[0], -1)
+    return q.reshape(p.shape[0], 4 * p.shape[1])
 
 
 def sq_reconstruct(packed: np.ndarray, scale_bits: np.ndarray, zero_bits: np.ndarray) -> np.ndarray:

@@ -82,3 +82,7 @@ def test_decode_is_attention_over_the_dequantized_values():
         ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, scale=0.3).reshape(-1).numpy()
         assert np.allclose(out[h], ref, rtol=1e-12, atol=1e-12)
         assert np.allclose(out[h], v_hat.mean(axis=0), rtol=1e-12, atol=1e-12)
+
+
+def test_empty_rows():
+    assert codec.sq_unpack(np.zeros((0, 8), dtype=np.uint8)).shape == (0, 32)
