@@ -140,14 +140,15 @@ def other_workloads(nk, torch, dev, calls: int):
     import synth
     res = []
     # (workload, layer, key-scale format, sink-plus-recent band (n_sink, n_rec) or None,
-    #  fp8 codebooks)
-    cases = [("single_head", 0, False, None, False), ("sweep_b64_s32k", 0, False, None, False),
-             ("sweep_b1_s128k", 0, False, None, False), ("gptoss_pair", 0, False, None, False),
-             ("gptoss_pair", 1, False, None, False), ("append_paged", 0, False, None, False),
-             ("qwen3_8b", 0, True, None, False), ("gptoss_pair", 1, True, None, False),
-             ("qwen3_8b", 0, False, (64, 256), False), ("gptoss_pair", 1, False, (64, 256), False),
-             ("qwen3_8b", 0, False, None, True), ("gptoss_pair", 1, False, None, True)]
-    for name, layer, key_scale, band_sizes, fp8 in cases:
+    #  fp8 codebooks, scalar value arm)
+    cases = [("single_head", 0, False, None, False, False), ("sweep_b64_s32k", 0, False, None, False, False),
+             ("sweep_b1_s128k", 0, False, None, False, False), ("gptoss_pair", 0, False, None, False, False),
+             ("gptoss_pair", 1, False, None, False, False), ("append_paged", 0, False, None, False, False),
+             ("qwen3_8b", 0, True, None, False, False), ("gptoss_pair", 1, True, None, False, False),
+             ("qwen3_8b", 0, False, (64, 256), False, False), ("gptoss_pair", 1, False, (64, 256), False, False),
+             ("qwen3_8b", 0, False, None, True, False), ("gptoss_pair", 1, False, None, True, False),
+             ("qwen3_8b", 0, False, None, False, True)]
+    for name, layer, key_scale, band_sizes, fp8, sq in cases:
         wl = synth.get_workload(name)
         B, S, H, Hq, D, L = wl.batch, wl.seq_len, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.groups
         gen = torch.Generator(device=dev)
@@ -156,7 +157,7 @@ def other_workloads(nk, torch, dev, calls: int):
         if fp8:  # the same codebooks rounded to fp8 E4M3 (torch's conversion), as bytes
             for k in ("cb_k", "cb_v"):
                 arrays[k] = torch.as_tensor(arrays[k]).to(torch.float32).to(torch.float8_e4m3fn).view(torch.uint8)
-        P = nk.NovaKVParams.from_arrays(arrays, device=dev, key_scale=key_scale)
+        P = nk.NovaKVParams.from_arrays(arrays, device=dev, key_scale=key_scale, sq_values=sq)
         if wl.block_size:
             bps = S // wl.block_size
             layout = nk.CacheLayout(wl.block_size, bps, torch.as_tensor(synth.shuffled_block_table(wl)).to(dev))
@@ -170,7 +171,8 @@ def other_workloads(nk, torch, dev, calls: int):
         pools = [(torch.randint(0, 256, shape, dtype=torch.uint8, device=dev, generator=gen),
                   torch.randint(0, 256, shape, dtype=torch.uint8, device=dev, generator=gen),
                   (torch.rand(shape[:3], generator=gen, device=dev) + 0.5).to(torch.bfloat16)
-                  if key_scale else None)
+                  if key_scale else None,
+                  torch.randn(shape[:3] + (2,), generator=gen, device=dev).to(torch.bfloat16) if sq else None)
                  for _ in range(copies)]
         q = torch.randn((B, Hq, D), generator=gen, device=dev).to(torch.bfloat16)
         seq = torch.full((B,), S, dtype=torch.int32, device=dev)
@@ -184,8 +186,8 @@ def other_workloads(nk, torch, dev, calls: int):
             band = nk.Band(*band_sizes, torch.randn(bshape, generator=gen, device=dev).to(torch.bfloat16),
                            torch.randn(bshape, generator=gen, device=dev).to(torch.bfloat16))
         calls_ = [nk.prepare_decode(P, layout, q, pk, pv, seq, S, out, ws, window=window, sinks=sinks,
-                                    k_scales=ps, band=band)
-                  for pk, pv, ps in pools]
+                                    k_scales=ps, band=band, v_sq=pq)
+                  for pk, pv, ps, pq in pools]
         for i in range(5):
             calls_[i % copies]()
         torch.cuda.synchronize()
@@ -203,12 +205,14 @@ def other_workloads(nk, torch, dev, calls: int):
             nband = min(sum(band_sizes), S)
             cb -= 2 * B * H * nband * L
             bb = 2 * B * H * nband * D * 2
-        # the key scales of the tokens read from codes: 2 bytes per token and KV head
-        sb = cb // L if key_scale else 0
+        # the key scales of the tokens read from codes: 2 bytes per token and KV
+        # head; the value scale and offset: 4 more
+        sb = (cb // L if key_scale else 0) + (2 * cb // L if sq else 0)
         res.append({"workload": f"{name}" + (f" layer {layer} (window {window})" if wl.num_layers > 1 else "")
                     + (" key-scale format" if key_scale else "")
                     + (f" band {band_sizes[0]}+{band_sizes[1]}" if band_sizes else "")
-                    + (" fp8 codebooks" if fp8 else ""),
+                    + (" fp8 codebooks" if fp8 else "")
+                    + (" scalar value arm (split-K kernels)" if sq else ""),
                     "batch": B, "seq_len": S, "q_heads": Hq, "kv_heads": H, "head_dim": D,
                     "paged_block": wl.block_size or None, "code_bytes": cb, "scale_bytes": sb,
                     "band_bytes": bb, "pool_copies": copies,

@@ -88,10 +88,22 @@ typedef enum {
  *             infinities; paper: Sec. "Calibration", codebooks kept in fp16
  *             and snapped to fp8 offline), 4 bytes per codeword; every value
  *             is used exactly (E4M3 values are exact in fp16).
+ *             NOVA_KV_SQ_VALUES: the scalar value arm (paper: Sec. "Bit rate"
+ *             and the implementation table: per-token affine INT2 values with
+ *             a BF16 scale and offset).  A token's values are rotated by t_v
+ *             (any orthogonal matrix), s = v @ t_v, and every coordinate is
+ *             stored as a 2-bit code q of the grid offset + scale * q, with
+ *             offset = bf16(min_i s_i), scale = bf16((max_i s_i - min_i s_i) / 3)
+ *             and q_i = clamp(round_half_even((s_i - offset) / scale), 0, 3)
+ *             (q = 0 when the stored scale is 0); coordinate 4g + j sits in
+ *             bits 2j, 2j+1 of byte g of the token's value code row.  cb_v is
+ *             then unused (may be NULL) and every call takes a v_sq pool.
+ *             The decode uses the split-K kernels in this format.
  *             Other bits are reserved (NOVA_KV_ERR_UNSUPPORTED).
  */
 #define NOVA_KV_KEY_SCALE 1u
 #define NOVA_KV_FP8_CODEBOOKS 2u
+#define NOVA_KV_SQ_VALUES 4u
 
 typedef struct {
     int32_t num_kv_heads;
@@ -176,6 +188,10 @@ typedef struct {
  *              pool, uint16 bf16 bit patterns [num_blocks][Hkv][block_size]
  *              addressed like the code pools (one scale per token-head),
  *              2-byte aligned, written at the same positions.
+ *   v_sq       scalar value arm only (else ignored, may be NULL): uint16 bf16
+ *              bit patterns [num_blocks][Hkv][block_size][2] (scale, offset)
+ *              addressed like the code pools, 4-byte aligned, written at the
+ *              new positions.
  *   band       NULL, or the sink-plus-recent band: the new tokens that are in
  *              it after the append are also written there (bf16).
  *
@@ -191,7 +207,7 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
                               const void *k, const void *v, nova_kv_dtype in_dtype,
                               int32_t batch, int32_t n_new, const int32_t *start_pos,
                               uint8_t *k_codes, uint8_t *v_codes, uint16_t *k_scales,
-                              const nova_kv_band *band, void *hip_stream);
+                              uint16_t *v_sq, const nova_kv_band *band, void *hip_stream);
 
 /*
  * Bytes of device workspace nova_kv_decode_attn needs for this shape (split
@@ -214,6 +230,8 @@ size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch,
  *              reads KV head h / (Hq / Hkv).
  *   k_scales   key-scale format only (else ignored, may be NULL): the scale
  *              pool of nova_kv_encode, read at the attended positions.
+ *   v_sq       scalar value arm only (else ignored, may be NULL): the
+ *              (scale, offset) pool of nova_kv_encode.
  *   band       NULL, or the sink-plus-recent band: its attended positions
  *              are read from it (exact bf16 keys and values, key scales
  *              unused), the other attended positions from the pools.
@@ -243,7 +261,8 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
                                    const void *q, nova_kv_dtype q_dtype,
                                    int32_t batch, int32_t num_q_heads,
                                    const uint8_t *k_codes, const uint8_t *v_codes,
-                                   const uint16_t *k_scales, const nova_kv_band *band,
+                                   const uint16_t *k_scales, const uint16_t *v_sq,
+                                   const nova_kv_band *band,
                                    const int32_t *seq_lens, int32_t max_seq_len,
                                    int32_t window, const float *sinks, float softmax_scale,
                                    float *out, void *workspace, size_t workspace_bytes,
@@ -261,7 +280,7 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
  *   k_new, v_new  [B][Hkv][D] device, dtype new_dtype (F32 or BF16): the token
  *              at position seq_lens[b] - 1 of each sequence (the newest cached
  *              token); precondition seq_lens[b] >= 1.
- *   k_codes, v_codes (and k_scales in the key-scale format, band when
+ *   k_codes, v_codes (and k_scales, v_sq in their formats, band when
  *              given)  written at position seq_lens[b] - 1 exactly as
  *              nova_kv_encode(n_new = 1, start_pos = seq_lens - 1) writes them
  *              (same bytes); nothing else is touched.
@@ -270,7 +289,7 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
  * out equals the output of nova_kv_decode_attn over the pools after that
  * append, up to fp32 rounding (the new token's term is added after the
  * split combine instead of inside a split).  With head_dim 128 on 16-aligned
- * blocks (not the key-scale format, no band) the step is a single kernel launch,
+ * blocks (plain or fp8 codebooks, no band) the step is a single kernel launch,
  * in which the workgroups that read the pools also encode the new token;
  * otherwise the one-token encode and the decode run one after the other on
  * the stream.
@@ -281,7 +300,7 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
                                           const void *q, nova_kv_dtype q_dtype,
                                           int32_t batch, int32_t num_q_heads,
                                           uint8_t *k_codes, uint8_t *v_codes, uint16_t *k_scales,
-                                          const nova_kv_band *band,
+                                          uint16_t *v_sq, const nova_kv_band *band,
                                           const int32_t *seq_lens, int32_t max_seq_len,
                                           int32_t window, const float *sinks, float softmax_scale,
                                           float *out, void *workspace, size_t workspace_bytes,

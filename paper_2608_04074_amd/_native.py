@@ -23,6 +23,7 @@ NOVA_KV_BF16 = 1
 
 NOVA_KV_KEY_SCALE = 1  # nova_kv_params.flags: the key-scale format
 NOVA_KV_FP8_CODEBOOKS = 2  # nova_kv_params.flags: codebooks stored as fp8 E4M3 bytes
+NOVA_KV_SQ_VALUES = 4  # nova_kv_params.flags: the scalar (per-token affine INT2) value arm
 
 EXPORTED = (
     "nova_kv_encode",
@@ -91,24 +92,24 @@ def lib() -> ctypes.CDLL:
         vp, i32 = ctypes.c_void_p, ctypes.c_int32
         L.nova_kv_encode.restype = ctypes.c_int
         # (params, layout, k, v, in_dtype, batch, n_new, start_pos, k_codes, v_codes,
-        #  k_scales, band, stream)
+        #  k_scales, v_sq, band, stream)
         L.nova_kv_encode.argtypes = [P(Params), P(Layout), vp, vp, ctypes.c_int, i32, i32, vp,
-                                     vp, vp, vp, P(Band), vp]
+                                     vp, vp, vp, vp, P(Band), vp]
         L.nova_kv_decode_workspace_bytes.restype = ctypes.c_size_t
         L.nova_kv_decode_workspace_bytes.argtypes = [P(Params), i32, i32, i32]
         L.nova_kv_decode_attn.restype = ctypes.c_int
-        # (params, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales, band,
-        #  seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace, bytes, stream)
+        # (params, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales, v_sq,
+        #  band, seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace, bytes, stream)
         L.nova_kv_decode_attn.argtypes = [P(Params), P(Layout), vp, ctypes.c_int, i32, i32, vp, vp, vp,
-                                          P(Band), vp, i32, i32, vp, ctypes.c_float, vp, vp,
+                                          vp, P(Band), vp, i32, i32, vp, ctypes.c_float, vp, vp,
                                           ctypes.c_size_t, vp]
         L.nova_kv_append_decode_attn.restype = ctypes.c_int
         # (params, layout, k_new, v_new, new_dtype, q, q_dtype, batch, num_q_heads, k_codes,
-        #  v_codes, k_scales, band, seq_lens, max_seq_len, window, sinks, softmax_scale, out,
-        #  workspace, bytes, stream)
+        #  v_codes, k_scales, v_sq, band, seq_lens, max_seq_len, window, sinks, softmax_scale,
+        #  out, workspace, bytes, stream)
         L.nova_kv_append_decode_attn.argtypes = [P(Params), P(Layout), vp, vp, ctypes.c_int, vp,
-                                                 ctypes.c_int, i32, i32, vp, vp, vp, P(Band), vp, i32,
-                                                 i32, vp, ctypes.c_float, vp, vp, ctypes.c_size_t, vp]
+                                                 ctypes.c_int, i32, i32, vp, vp, vp, vp, P(Band), vp,
+                                                 i32, i32, vp, ctypes.c_float, vp, vp, ctypes.c_size_t, vp]
         L.nova_kv_status_string.restype = ctypes.c_char_p
         L.nova_kv_status_string.argtypes = [ctypes.c_int]
         L.nova_kv_last_error.restype = ctypes.c_char_p

@@ -44,16 +44,21 @@ class NovaKVParams:
     the key codebooks are then trained on normalized coefficients), and every
     call then takes a ``k_scales`` pool of shape ``scale_pool_shape``.
     Codebooks are fp16, or fp8 E4M3 bytes given as uint8 tensors (both sides
-    in the same format).
+    in the same format).  ``sq_values`` selects the scalar value arm (values
+    as per-token affine INT2 in the rotation t_v; cb_v unused, may be None),
+    and every call then takes a ``v_sq`` pool of shape ``sq_pool_shape``.
     """
 
     def __init__(self, kbar, t_k, t_k_inv_t, t_v, cb_k, cb_v, group_dim: int = 4,
-                 codebook_size: int = 256, key_scale: bool = False):
+                 codebook_size: int = 256, key_scale: bool = False, sq_values: bool = False):
         hkv, d = kbar.shape
         L = d // group_dim
         _require(kbar, "kbar", (torch.float32,), hkv * d)
         for name, t in (("t_k", t_k), ("t_k_inv_t", t_k_inv_t), ("t_v", t_v)):
             _require(t, name, (torch.float32,), hkv * d * d)
+        self.sq_values = bool(sq_values)
+        if self.sq_values and cb_v is None:
+            cb_v = cb_k  # unused by the scalar value arm
         for name, t in (("cb_k", cb_k), ("cb_v", cb_v)):
             _require(t, name, (torch.float16, torch.uint8), hkv * L * codebook_size * group_dim)
         if cb_k.dtype != cb_v.dtype:
@@ -65,7 +70,8 @@ class NovaKVParams:
         self.cb_k, self.cb_v = cb_k, cb_v
         self.key_scale = bool(key_scale)
         flags = (nat.NOVA_KV_KEY_SCALE if self.key_scale else 0) | \
-            (nat.NOVA_KV_FP8_CODEBOOKS if self.fp8_codebooks else 0)
+            (nat.NOVA_KV_FP8_CODEBOOKS if self.fp8_codebooks else 0) | \
+            (nat.NOVA_KV_SQ_VALUES if self.sq_values else 0)
         self._c = nat.Params(hkv, d, group_dim, codebook_size, flags, kbar.data_ptr(), t_k.data_ptr(),
                              t_k_inv_t.data_ptr(), t_v.data_ptr(), cb_k.data_ptr(),
                              cb_v.data_ptr())
@@ -75,16 +81,19 @@ class NovaKVParams:
         return self.head_dim // self.group_dim
 
     @classmethod
-    def from_arrays(cls, arrays: dict, device="cuda", key_scale: bool = False) -> "NovaKVParams":
+    def from_arrays(cls, arrays: dict, device="cuda", key_scale: bool = False,
+                    sq_values: bool = False) -> "NovaKVParams":
         """From host arrays: kbar/t_k/t_k_inv_t/t_v float32, cb_k/cb_v float16, or uint8
         fp8 E4M3 codes ([Hkv][...])."""
         f32 = {k: torch.as_tensor(arrays[k]).to(torch.float32).contiguous().to(device)
                for k in ("kbar", "t_k", "t_k_inv_t", "t_v")}
-        f16 = {}
+        f16 = {"cb_v": None}
         for k in ("cb_k", "cb_v"):
+            if arrays.get(k) is None:
+                continue
             t = torch.as_tensor(arrays[k])
             f16[k] = (t if t.dtype == torch.uint8 else t.to(torch.float16)).contiguous().to(device)
-        return cls(**f32, **f16, key_scale=key_scale)
+        return cls(**f32, **f16, key_scale=key_scale, sq_values=sq_values)
 
     @property
     def c(self) -> nat.Params:
@@ -139,6 +148,21 @@ def _scales_ptr(params: NovaKVParams, k_scales: Optional[torch.Tensor], k_codes:
     return k_scales.data_ptr()
 
 
+def sq_pool_shape(params: NovaKVParams, layout: CacheLayout, batch: int, num_blocks=None):
+    """Shape of the scalar value arm's pool: [num_blocks][Hkv][block_size][2] (scale, offset bf16 bits)."""
+    return code_pool_shape(params, layout, batch, num_blocks)[:3] + (2,)
+
+
+def _sq_ptr(params: NovaKVParams, v_sq: Optional[torch.Tensor], k_codes: torch.Tensor):
+    """Device pointer of the (scale, offset) pool (None outside the scalar value arm)."""
+    if not params.sq_values:
+        return None
+    if v_sq is None:
+        raise ValueError("the scalar value arm needs a v_sq pool")
+    _require(v_sq, "v_sq", _SCALE_DTYPES, 2 * (k_codes.numel() // params.groups))
+    return v_sq.data_ptr()
+
+
 def band_shape(params: NovaKVParams, batch: int, n_sink: int, n_rec: int):
     """Shape of each sink-plus-recent band buffer: [B][Hkv][n_sink + n_rec][D]."""
     return (batch, params.num_kv_heads, n_sink + n_rec, params.head_dim)
@@ -188,7 +212,7 @@ def _dtype_code(t: torch.Tensor) -> int:
 def encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v: torch.Tensor,
            start_pos: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
            stream: Optional[torch.cuda.Stream] = None, k_scales: Optional[torch.Tensor] = None,
-           band: Optional[Band] = None) -> None:
+           band: Optional[Band] = None, v_sq: Optional[torch.Tensor] = None) -> None:
     """nova_kv_encode: k, v [B][n_new][Hkv][D] (fp32 or bf16), start_pos int32 [B]."""
     if k.dim() != 4:
         raise ValueError("k must be [B][n_new][Hkv][D]")
@@ -204,7 +228,7 @@ def encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v: torch.
     nat.check(nat.lib().nova_kv_encode(
         ctypes.byref(params.c), ctypes.byref(layout.c), k.data_ptr(), v.data_ptr(), _dtype_code(k),
         b, n_new, start_pos.data_ptr(), k_codes.data_ptr(), v_codes.data_ptr(), ks,
-        _band_ref(band, params, b), _stream_ptr(stream)))
+        _sq_ptr(params, v_sq, k_codes), _band_ref(band, params, b), _stream_ptr(stream)))
 
 
 def decode_workspace_bytes(params: NovaKVParams, batch: int, num_q_heads: int,
@@ -219,7 +243,8 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
                 softmax_scale: float = 0.0, out: Optional[torch.Tensor] = None,
                 workspace: Optional[torch.Tensor] = None,
                 stream: Optional[torch.cuda.Stream] = None,
-                k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None) -> torch.Tensor:
+                k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None,
+                v_sq: Optional[torch.Tensor] = None) -> torch.Tensor:
     """nova_kv_decode_attn: q [B][Hq][D] (fp32 or bf16) -> out [B][Hq][D] fp32.
 
     A caller-provided workspace must be zero-filled before its first use; each
@@ -244,7 +269,8 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
     ks = _scales_ptr(params, k_scales, k_codes)
     nat.check(nat.lib().nova_kv_decode_attn(
         ctypes.byref(params.c), ctypes.byref(layout.c), q.data_ptr(), _dtype_code(q), b, hq,
-        k_codes.data_ptr(), v_codes.data_ptr(), ks, _band_ref(band, params, b), seq_lens.data_ptr(),
+        k_codes.data_ptr(), v_codes.data_ptr(), ks, _sq_ptr(params, v_sq, k_codes), _band_ref(band, params, b),
+        seq_lens.data_ptr(),
         max_seq_len, window,
         sinks.data_ptr() if sinks is not None else None, float(softmax_scale), out.data_ptr(),
         workspace.data_ptr(), workspace.numel(), _stream_ptr(stream)))
@@ -252,7 +278,7 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
 
 
 def _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
-                        workspace, window, sinks, softmax_scale, stream, k_scales, band):
+                        workspace, window, sinks, softmax_scale, stream, k_scales, band, v_sq=None):
     if q.dim() != 3 or q.shape[2] != params.head_dim:
         raise ValueError("q must be [B][Hq][D]")
     b, hq, d = q.shape
@@ -273,7 +299,8 @@ def _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_l
     return (ctypes.byref(params.c), ctypes.byref(layout.c), vp(k_new.data_ptr()), vp(v_new.data_ptr()),
             ctypes.c_int(_dtype_code(k_new)), vp(q.data_ptr()), ctypes.c_int(_dtype_code(q)),
             ctypes.c_int32(b), ctypes.c_int32(hq), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()),
-            vp(ks), _band_ref(band, params, b), vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len),
+            vp(ks), vp(_sq_ptr(params, v_sq, k_codes)), _band_ref(band, params, b), vp(seq_lens.data_ptr()),
+            ctypes.c_int32(max_seq_len),
             ctypes.c_int32(window),
             vp(sinks.data_ptr() if sinks is not None else None), ctypes.c_float(softmax_scale),
             vp(out.data_ptr()), vp(workspace.data_ptr()), ctypes.c_size_t(workspace.numel()),
@@ -286,7 +313,8 @@ def append_decode_attn(params: NovaKVParams, layout: CacheLayout, k_new: torch.T
                        sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
                        out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
                        stream: Optional[torch.cuda.Stream] = None,
-                       k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None) -> torch.Tensor:
+                       k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None,
+                       v_sq: Optional[torch.Tensor] = None) -> torch.Tensor:
     """nova_kv_append_decode_attn: store the step's k_new, v_new [B][Hkv][D] at
     position seq_lens[b] - 1 of the pools, then decode q [B][Hq][D] over the
     cache including them -> out [B][Hq][D] fp32.  Workspace as in decode_attn."""
@@ -297,7 +325,7 @@ def append_decode_attn(params: NovaKVParams, layout: CacheLayout, k_new: torch.T
     if workspace is None:
         workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=q.device)
     args = _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
-                               workspace, window, sinks, softmax_scale, stream, k_scales, band)
+                               workspace, window, sinks, softmax_scale, stream, k_scales, band, v_sq)
     nat.check(nat.lib().nova_kv_append_decode_attn(*args))
     return out
 
@@ -317,7 +345,8 @@ class PreparedCall:
 def prepare_encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v: torch.Tensor,
                    start_pos: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
                    stream: Optional[torch.cuda.Stream] = None,
-                   k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None) -> PreparedCall:
+                   k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None,
+                   v_sq: Optional[torch.Tensor] = None) -> PreparedCall:
     """nova_kv_encode with the arguments of encode(), marshalled once."""
     if k.dim() != 4:
         raise ValueError("k must be [B][n_new][Hkv][D]")
@@ -334,9 +363,9 @@ def prepare_encode(params: NovaKVParams, layout: CacheLayout, k: torch.Tensor, v
     args = (ctypes.byref(params.c), ctypes.byref(layout.c), vp(k.data_ptr()), vp(v.data_ptr()),
             ctypes.c_int(_dtype_code(k)), ctypes.c_int32(b), ctypes.c_int32(n_new),
             vp(start_pos.data_ptr()), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()), vp(ks),
-            _band_ref(band, params, b), vp(_stream_ptr(stream)))
+            vp(_sq_ptr(params, v_sq, k_codes)), _band_ref(band, params, b), vp(_stream_ptr(stream)))
     return PreparedCall(nat.lib().nova_kv_encode, args,
-                        (params, layout, k, v, start_pos, k_codes, v_codes, k_scales, band))
+                        (params, layout, k, v, start_pos, k_codes, v_codes, k_scales, band, v_sq))
 
 
 def prepare_decode(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
@@ -344,7 +373,8 @@ def prepare_decode(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
                    max_seq_len: int, out: torch.Tensor, workspace: torch.Tensor, window: int = 0,
                    sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
                    stream: Optional[torch.cuda.Stream] = None,
-                   k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None) -> PreparedCall:
+                   k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None,
+                   v_sq: Optional[torch.Tensor] = None) -> PreparedCall:
     """nova_kv_decode_attn with the arguments of decode_attn(), marshalled once
     (out and a zero-filled workspace are required here)."""
     if q.dim() != 3 or q.shape[2] != params.head_dim:
@@ -362,13 +392,15 @@ def prepare_decode(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
     vp = ctypes.c_void_p
     args = (ctypes.byref(params.c), ctypes.byref(layout.c), vp(q.data_ptr()), ctypes.c_int(_dtype_code(q)),
             ctypes.c_int32(b), ctypes.c_int32(hq), vp(k_codes.data_ptr()), vp(v_codes.data_ptr()),
-            vp(ks), _band_ref(band, params, b), vp(seq_lens.data_ptr()), ctypes.c_int32(max_seq_len),
+            vp(ks), vp(_sq_ptr(params, v_sq, k_codes)), _band_ref(band, params, b), vp(seq_lens.data_ptr()),
+            ctypes.c_int32(max_seq_len),
             ctypes.c_int32(window),
             vp(sinks.data_ptr() if sinks is not None else None), ctypes.c_float(softmax_scale),
             vp(out.data_ptr()), vp(workspace.data_ptr()), ctypes.c_size_t(workspace.numel()),
             vp(_stream_ptr(stream)))
     return PreparedCall(nat.lib().nova_kv_decode_attn, args,
-                        (params, layout, q, k_codes, v_codes, seq_lens, sinks, out, workspace, k_scales, band))
+                        (params, layout, q, k_codes, v_codes, seq_lens, sinks, out, workspace, k_scales, band,
+                         v_sq))
 
 
 def prepare_append_decode(params: NovaKVParams, layout: CacheLayout, k_new: torch.Tensor, v_new: torch.Tensor,
@@ -376,11 +408,12 @@ def prepare_append_decode(params: NovaKVParams, layout: CacheLayout, k_new: torc
                           seq_lens: torch.Tensor, max_seq_len: int, out: torch.Tensor, workspace: torch.Tensor,
                           window: int = 0, sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
                           stream: Optional[torch.cuda.Stream] = None,
-                          k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None) -> PreparedCall:
+                          k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None,
+                          v_sq: Optional[torch.Tensor] = None) -> PreparedCall:
     """nova_kv_append_decode_attn with the arguments of append_decode_attn(),
     marshalled once (out and a zero-filled workspace are required here)."""
     args = _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
-                               workspace, window, sinks, softmax_scale, stream, k_scales, band)
+                               workspace, window, sinks, softmax_scale, stream, k_scales, band, v_sq)
     return PreparedCall(nat.lib().nova_kv_append_decode_attn, args,
                         (params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, sinks, out, workspace,
-                         k_scales, band))
+                         k_scales, band, v_sq))

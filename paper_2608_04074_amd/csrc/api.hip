@@ -46,11 +46,12 @@ nova_kv_status check_params(const nova_kv_params *p, bool need_encode, bool need
     return fail(NOVA_KV_ERR_UNSUPPORTED, "codebook_size %d unsupported (only 256)", p->codebook_size);
   if (p->head_dim != 64 && p->head_dim != 128)
     return fail(NOVA_KV_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", p->head_dim);
-  if ((p->flags & ~(NOVA_KV_KEY_SCALE | NOVA_KV_FP8_CODEBOOKS)) != 0)
-    return fail(NOVA_KV_ERR_UNSUPPORTED, "flags 0x%x unsupported (NOVA_KV_KEY_SCALE, NOVA_KV_FP8_CODEBOOKS)",
-                p->flags);
-  if (!p->kbar || !p->cb_k || !p->cb_v) return fail(NOVA_KV_ERR_INVALID_ARG, "kbar/cb_k/cb_v is NULL");
-  if (!aligned(p->cb_k, 16) || !aligned(p->cb_v, 16))
+  if ((p->flags & ~(NOVA_KV_KEY_SCALE | NOVA_KV_FP8_CODEBOOKS | NOVA_KV_SQ_VALUES)) != 0)
+    return fail(NOVA_KV_ERR_UNSUPPORTED,
+                "flags 0x%x unsupported (NOVA_KV_KEY_SCALE, NOVA_KV_FP8_CODEBOOKS, NOVA_KV_SQ_VALUES)", p->flags);
+  const bool sq = (p->flags & NOVA_KV_SQ_VALUES) != 0;  // cb_v unused
+  if (!p->kbar || !p->cb_k || (!sq && !p->cb_v)) return fail(NOVA_KV_ERR_INVALID_ARG, "kbar/cb_k/cb_v is NULL");
+  if (!aligned(p->cb_k, 16) || (!sq && !aligned(p->cb_v, 16)))
     return fail(NOVA_KV_ERR_INVALID_ARG, "codebooks must be 16-byte aligned");
   if (need_encode && (!p->t_k || !p->t_v)) return fail(NOVA_KV_ERR_INVALID_ARG, "t_k/t_v is NULL");
   if (need_decode && (!p->t_k_inv_t || !p->t_v))
@@ -91,6 +92,14 @@ nova_kv_status check_band(const nova_kv_band *band) {
   return NOVA_KV_OK;
 }
 
+// The (scale, offset) pool of the scalar value arm (ignored otherwise).
+nova_kv_status check_sq(const nova_kv_params *p, const void *v_sq) {
+  if (!(p->flags & NOVA_KV_SQ_VALUES)) return NOVA_KV_OK;
+  if (!v_sq) return fail(NOVA_KV_ERR_INVALID_ARG, "v_sq is NULL in the scalar value format");
+  if (!aligned(v_sq, 4)) return fail(NOVA_KV_ERR_INVALID_ARG, "v_sq must be 4-byte aligned");
+  return NOVA_KV_OK;
+}
+
 novakv::CacheLayout to_layout(const nova_kv_layout *lay) {
   return novakv::CacheLayout{lay->block_size, lay->blocks_per_seq, lay->block_table};
 }
@@ -116,7 +125,7 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
                               const void *k, const void *v, nova_kv_dtype in_dtype,
                               int32_t batch, int32_t n_new, const int32_t *start_pos,
                               uint8_t *k_codes, uint8_t *v_codes, uint16_t *k_scales,
-                              const nova_kv_band *band, void *hip_stream) {
+                              uint16_t *v_sq, const nova_kv_band *band, void *hip_stream) {
   nova_kv_status st = check_params(p, true, false);
   if (st != NOVA_KV_OK) return st;
   if ((st = check_layout(layout)) != NOVA_KV_OK) return st;
@@ -128,6 +137,7 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
     return fail(NOVA_KV_ERR_INVALID_ARG, "n_new exceeds the per-sequence capacity");
   if (batch == 0 || n_new == 0) return ok();
   if ((st = check_scales(p, k_scales)) != NOVA_KV_OK) return st;
+  if ((st = check_sq(p, v_sq)) != NOVA_KV_OK) return st;
   if ((st = check_band(band)) != NOVA_KV_OK) return st;
   if (!k || !v || !start_pos || !k_codes || !v_codes)
     return fail(NOVA_KV_ERR_INVALID_ARG, "k, v, start_pos, k_codes or v_codes is NULL");
@@ -151,6 +161,7 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
   a.k_codes = k_codes;
   a.v_codes = v_codes;
   a.k_scales = (p->flags & NOVA_KV_KEY_SCALE) ? k_scales : nullptr;
+  a.v_sq = (p->flags & NOVA_KV_SQ_VALUES) ? v_sq : nullptr;
   if (band) {
     a.n_sink = band->n_sink;
     a.n_rec = band->n_rec;
@@ -175,8 +186,8 @@ namespace {
 // Host checks and argument set-up shared by the decode entry points.
 nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *layout, const void *q,
                               nova_kv_dtype q_dtype, int32_t batch, int32_t num_q_heads, const uint8_t *k_codes,
-                              const uint8_t *v_codes, const uint16_t *k_scales, const nova_kv_band *band,
-                              const int32_t *seq_lens, int32_t max_seq_len,
+                              const uint8_t *v_codes, const uint16_t *k_scales, const uint16_t *v_sq,
+                              const nova_kv_band *band, const int32_t *seq_lens, int32_t max_seq_len,
                               int32_t window, const float *sinks, float softmax_scale, float *out,
                               void *workspace, size_t workspace_bytes, bool need_encode,
                               novakv::DecodeArgs &a, novakv::DecodePlan &plan) {
@@ -199,13 +210,16 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   if (!(softmax_scale >= 0.f)) return fail(NOVA_KV_ERR_INVALID_ARG, "softmax_scale must be >= 0");
   if (batch == 0) return NOVA_KV_OK;
   if ((st = check_scales(p, k_scales)) != NOVA_KV_OK) return st;
+  if ((st = check_sq(p, v_sq)) != NOVA_KV_OK) return st;
   if ((st = check_band(band)) != NOVA_KV_OK) return st;
   if (!q || !k_codes || !v_codes || !seq_lens || !out)
     return fail(NOVA_KV_ERR_INVALID_ARG, "q, k_codes, v_codes, seq_lens or out is NULL");
   if (!aligned(k_codes, 16) || !aligned(v_codes, 16))
     return fail(NOVA_KV_ERR_INVALID_ARG, "code pools must be 16-byte aligned");
+  // the scalar value arm runs on the split-K kernels (block size 0 asks for them)
+  const bool sq = (p->flags & NOVA_KV_SQ_VALUES) != 0;
   plan = novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len, layout->block_size,
-                             window);
+                             window, sq);
   if (!workspace || workspace_bytes < plan.total)
     return fail(NOVA_KV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
                 workspace ? workspace_bytes : static_cast<size_t>(0));
@@ -229,6 +243,7 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   a.k_codes = k_codes;
   a.v_codes = v_codes;
   a.k_scales = (p->flags & NOVA_KV_KEY_SCALE) ? k_scales : nullptr;
+  a.v_sq = sq ? v_sq : nullptr;
   if (band) {
     a.n_sink = band->n_sink;
     a.n_rec = band->n_rec;
@@ -262,14 +277,15 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
 nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
                                    const void *q, nova_kv_dtype q_dtype, int32_t batch,
                                    int32_t num_q_heads, const uint8_t *k_codes,
-                                   const uint8_t *v_codes, const uint16_t *k_scales, const nova_kv_band *band,
-                                   const int32_t *seq_lens, int32_t max_seq_len, int32_t window, const float *sinks,
+                                   const uint8_t *v_codes, const uint16_t *k_scales, const uint16_t *v_sq,
+                                   const nova_kv_band *band, const int32_t *seq_lens, int32_t max_seq_len,
+                                   int32_t window, const float *sinks,
                                    float softmax_scale, float *out, void *workspace,
                                    size_t workspace_bytes, void *hip_stream) {
   novakv::DecodeArgs a;
   novakv::DecodePlan plan;
-  nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales, band,
-                                     seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace, workspace_bytes,
+  nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales, v_sq,
+                                     band, seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace, workspace_bytes,
                                      false, a, plan);
   if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
   hipError_t e = novakv::launch_decode(a, plan.use_lut, static_cast<hipStream_t>(hip_stream));
@@ -281,8 +297,8 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
                                           const void *k_new, const void *v_new, nova_kv_dtype new_dtype,
                                           const void *q, nova_kv_dtype q_dtype, int32_t batch,
                                           int32_t num_q_heads, uint8_t *k_codes, uint8_t *v_codes,
-                                          uint16_t *k_scales, const nova_kv_band *band, const int32_t *seq_lens,
-                                          int32_t max_seq_len,
+                                          uint16_t *k_scales, uint16_t *v_sq, const nova_kv_band *band,
+                                          const int32_t *seq_lens, int32_t max_seq_len,
                                           int32_t window,
                                           const float *sinks, float softmax_scale, float *out,
                                           void *workspace, size_t workspace_bytes, void *hip_stream) {
@@ -291,7 +307,7 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
   novakv::DecodeArgs a;
   novakv::DecodePlan plan;
   nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales,
-                                     band, seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace,
+                                     v_sq, band, seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace,
                                      workspace_bytes, true, a, plan);
   if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
   if (!k_new || !v_new) return fail(NOVA_KV_ERR_INVALID_ARG, "k_new or v_new is NULL");
@@ -329,6 +345,7 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
     ea.k_codes = k_codes;
     ea.v_codes = v_codes;
     ea.k_scales = (p->flags & NOVA_KV_KEY_SCALE) ? k_scales : nullptr;
+    ea.v_sq = (p->flags & NOVA_KV_SQ_VALUES) ? v_sq : nullptr;
     if (band) {
       ea.n_sink = band->n_sink;
       ea.n_rec = band->n_rec;

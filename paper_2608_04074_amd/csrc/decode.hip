@@ -71,6 +71,7 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
   __shared__ float qs[kMaxGqa][D];
   __shared__ float ps[kThreads][kMaxGqa];
   __shared__ __attribute__((aligned(16))) uint8_t vcodes[kThreads][L];
+  __shared__ float vsq[kThreads][2];  // scalar value arm: scale, offset of each token
   __shared__ float red[kWaves][kMaxGqa];
 
   const int split = blockIdx.x, kv = blockIdx.y, b = blockIdx.z;
@@ -103,7 +104,7 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
     uint2 *dv = reinterpret_cast<uint2 *>(cbv);
     for (int i = tid; i < L * kCodebookSize; i += kThreads) {
       dk[i] = codeword(a.cb_k, a.cb_fp8, cw0 + i);
-      dv[i] = codeword(a.cb_v, a.cb_fp8, cw0 + i);
+      if (!a.v_sq) dv[i] = codeword(a.cb_v, a.cb_fp8, cw0 + i);
     }
     for (int i = tid; i < G * D; i += kThreads)
       qs[i / D][i % D] =
@@ -133,6 +134,10 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
       const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, t);
       const uint8_t *kc = a.k_codes + off;
       const uint8_t *vc = a.v_codes + off;
+      if (a.v_sq) {
+        vsq[tid][0] = bf16_bits_to_float(a.v_sq[(off / L) * 2]);
+        vsq[tid][1] = bf16_bits_to_float(a.v_sq[(off / L) * 2 + 1]);
+      }
       for (int g0 = 0; g0 < L; g0 += 16) {
         uint4 w = *reinterpret_cast<const uint4 *>(kc + g0);
         *reinterpret_cast<uint4 *>(&vcodes[tid][g0]) = *reinterpret_cast<const uint4 *>(vc + g0);
@@ -196,7 +201,9 @@ __global__ void __launch_bounds__(kThreads) decode_stage1_v0(DecodeArgs a) {
       for (int h = 0; h < kMaxGqa; ++h) acc[h] *= (h < G) ? alpha[h] : 0.f;
       for (int j = 0; j < n; ++j) {
         const int c = vcodes[j][ell];
-        const float f = half_bits_to_float(cbv[(ell * kCodebookSize + c) * kGroupDim + i]);
+        // a codeword coordinate, or the scalar arm's offset + scale * q
+        const float f = a.v_sq ? fmaf(vsq[j][0], static_cast<float>((c >> (2 * i)) & 3), vsq[j][1])
+                               : half_bits_to_float(cbv[(ell * kCodebookSize + c) * kGroupDim + i]);
 #pragma unroll
         for (int h = 0; h < kMaxGqa; ++h)
           if (h < G) acc[h] = fmaf(ps[j][h], f, acc[h]);
@@ -420,7 +427,7 @@ void plan_generic(int batch, int num_kv_heads, int max_seq_len, int *n_split, in
 }  // namespace
 
 DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_dim,
-                       int max_seq_len, int block_size, int window) {
+                       int max_seq_len, int block_size, int window, bool split_k_only) {
   DecodePlan p{};
   const int gqa = num_q_heads / num_kv_heads;
   // Splits tile the attended span: the last `window` tokens, or all of them.
@@ -437,7 +444,7 @@ DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_di
   const int lut_bound = static_cast<int>((256 + units - 1) / units);
   int max_split = ns_full > lut_bound ? ns_full : lut_bound;
   if (block_size > 0) {
-    p.use_lut = lut_path_eligible(head_dim, gqa, block_size) ? 1 : 0;
+    p.use_lut = !split_k_only && lut_path_eligible(head_dim, gqa, block_size) ? 1 : 0;
     p.n_split = p.use_lut ? ns_l : ns_g;
     p.chunk = p.use_lut ? ch_l : ch_g;
   } else {

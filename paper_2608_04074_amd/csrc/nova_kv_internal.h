@@ -38,6 +38,7 @@ struct DecodeArgs {
   int q_bf16;
   const uint8_t *k_codes, *v_codes;
   const uint16_t *k_scales;  // key-scale format: bf16 per-token key scales (pool layout), else nullptr
+  const uint16_t *v_sq;      // scalar value arm: bf16 (scale, offset) per token (pool layout), else nullptr
   // Sink-plus-recent band: [B][Hkv][n_sink + n_rec][D] bf16 keys and values
   // of the positions [0, n_sink) and the last n_rec (ring slots), or nullptr
   // (then n_sink = n_rec = 0).
@@ -90,6 +91,7 @@ struct EncodeArgs {
   int start_offset;  // the first new token of sequence b goes to start_pos[b] + start_offset
   uint8_t *k_codes, *v_codes;
   uint16_t *k_scales;  // key-scale format: bf16 per-token key scales (pool layout), else nullptr
+  uint16_t *v_sq;      // scalar value arm: bf16 (scale, offset) per token (pool layout), else nullptr
   int n_sink, n_rec;   // sink-plus-recent band (0, 0 without one)
   uint16_t *band_k, *band_v;
 };
@@ -129,7 +131,7 @@ struct DecodePlan {
 // paths, so it depends only on (batch, heads, head_dim, max_seq_len);
 // block_size <= 0 asks for that size alone.
 DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_dim,
-                       int max_seq_len, int block_size, int window);
+                       int max_seq_len, int block_size, int window, bool split_k_only = false);
 
 hipError_t launch_decode(const DecodeArgs &a, int use_lut, hipStream_t stream);
 int plan_b_chunk(int batch, int num_kv_heads, int n_split);

@@ -57,23 +57,23 @@ def _layout(**kw):
 def _decode(p, lay, **kw):
     a = dict(q=0x7000, q_dtype=nat.NOVA_KV_BF16, batch=2, hq=32, k=0x8000, v=0x9000, seq=0xA000,
              max_seq=4096, window=0, sinks=None, scale=0.0, out=0xB000, ws=None, ws_bytes=0, ks=None,
-             band=None)
+             vsq=None, band=None)
     a.update(kw)
     return nat.lib().nova_kv_decode_attn(
         ctypes.byref(p) if p is not None else None, ctypes.byref(lay) if lay is not None else None,
-        a["q"], a["q_dtype"], a["batch"], a["hq"], a["k"], a["v"], a["ks"], _band(a["band"]), a["seq"],
+        a["q"], a["q_dtype"], a["batch"], a["hq"], a["k"], a["v"], a["ks"], a["vsq"], _band(a["band"]), a["seq"],
         a["max_seq"],
         a["window"], a["sinks"], a["scale"], a["out"], a["ws"], a["ws_bytes"], None)
 
 
 def _encode(p, lay, **kw):
     a = dict(k=0x7000, v=0x7800, dtype=nat.NOVA_KV_BF16, batch=2, n_new=16, start=0xA000,
-             kc=0x8000, vc=0x9000, ks=None, band=None)
+             kc=0x8000, vc=0x9000, ks=None, vsq=None, band=None)
     a.update(kw)
     return nat.lib().nova_kv_encode(ctypes.byref(p) if p is not None else None,
                                     ctypes.byref(lay) if lay is not None else None,
                                     a["k"], a["v"], a["dtype"], a["batch"], a["n_new"], a["start"],
-                                    a["kc"], a["vc"], a["ks"], _band(a["band"]), None)
+                                    a["kc"], a["vc"], a["ks"], a["vsq"], _band(a["band"]), None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -81,8 +81,8 @@ def _encode(p, lay, **kw):
     (dict(codebook_size=16), nat.NOVA_KV_ERR_UNSUPPORTED),
     (dict(head_dim=96), nat.NOVA_KV_ERR_UNSUPPORTED),
     (dict(head_dim=130), nat.NOVA_KV_ERR_INVALID_ARG),
-    (dict(flags=4), nat.NOVA_KV_ERR_UNSUPPORTED),
-    (dict(flags=7), nat.NOVA_KV_ERR_UNSUPPORTED),
+    (dict(flags=8), nat.NOVA_KV_ERR_UNSUPPORTED),
+    (dict(flags=15), nat.NOVA_KV_ERR_UNSUPPORTED),
     (dict(num_kv_heads=0), nat.NOVA_KV_ERR_INVALID_ARG),
     (dict(cb_k=None), nat.NOVA_KV_ERR_INVALID_ARG),
     (dict(cb_v=0x6001), nat.NOVA_KV_ERR_INVALID_ARG),
@@ -157,12 +157,14 @@ def test_encode_needs_forward_transforms_and_noops():
 
 def _append(p, lay, **kw):
     a = dict(kn=0x7000, vn=0x7800, new_dtype=nat.NOVA_KV_BF16, q=0x7400, q_dtype=nat.NOVA_KV_BF16,
-             batch=2, hq=32, k=0x8000, v=0x9000, ks=None, band=None, seq=0xA000, max_seq=4096, window=0,
+             batch=2, hq=32, k=0x8000, v=0x9000, ks=None, vsq=None, band=None, seq=0xA000, max_seq=4096,
+             window=0,
              sinks=None, scale=0.0, out=0xB000, ws=None, ws_bytes=0)
     a.update(kw)
     return nat.lib().nova_kv_append_decode_attn(
         ctypes.byref(p), ctypes.byref(lay), a["kn"], a["vn"], a["new_dtype"], a["q"], a["q_dtype"],
-        a["batch"], a["hq"], a["k"], a["v"], a["ks"], _band(a["band"]), a["seq"], a["max_seq"], a["window"],
+        a["batch"], a["hq"], a["k"], a["v"], a["ks"], a["vsq"], _band(a["band"]), a["seq"], a["max_seq"],
+        a["window"],
         a["sinks"],
         a["scale"], a["out"], a["ws"], a["ws_bytes"], None)
 
@@ -205,3 +207,18 @@ def test_good_band_passes_the_checks(call):
     assert call(_params(), _layout(), band=(0, 1024, 0xC000, 0xD000)) == nat.NOVA_KV_ERR_WORKSPACE
     # batch 0 stays a no-op whatever the band
     assert call(_params(), _layout(), band=(0, 0, None, None), batch=0, q=None, out=None) == nat.NOVA_KV_OK
+
+
+@pytest.mark.parametrize("call", [_decode, _encode, _append])
+def test_scalar_value_arm_needs_its_pool(call):
+    p = _params(flags=nat.NOVA_KV_SQ_VALUES, cb_v=None)   # cb_v unused in this format
+    assert call(p, _layout()) == nat.NOVA_KV_ERR_INVALID_ARG
+    assert b"v_sq" in nat.lib().nova_kv_last_error()
+    assert call(p, _layout(), vsq=0xC002) == nat.NOVA_KV_ERR_INVALID_ARG    # not 4-byte aligned
+    if call is _encode:
+        assert call(p, _layout(), vsq=0xC000, k=None) == nat.NOVA_KV_ERR_INVALID_ARG
+        assert b"v_sq" not in nat.lib().nova_kv_last_error()
+    else:
+        assert call(p, _layout(), vsq=0xC000) == nat.NOVA_KV_ERR_WORKSPACE
+    # the plain format still needs cb_v
+    assert call(_params(cb_v=None), _layout()) == nat.NOVA_KV_ERR_INVALID_ARG
