@@ -212,7 +212,7 @@ def other_workloads(nk, torch, dev, calls: int):
                     + (" key-scale format" if key_scale else "")
                     + (f" band {band_sizes[0]}+{band_sizes[1]}" if band_sizes else "")
                     + (" fp8 codebooks" if fp8 else "")
-                    + (" scalar value arm (split-K kernels)" if sq else ""),
+                    + (" scalar value arm" if sq else ""),
                     "batch": B, "seq_len": S, "q_heads": Hq, "kv_heads": H, "head_dim": D,
                     "paged_block": wl.block_size or None, "code_bytes": cb, "scale_bytes": sb,
                     "band_bytes": bb, "pool_copies": copies,

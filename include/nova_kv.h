@@ -98,7 +98,7 @@ typedef enum {
  *             (q = 0 when the stored scale is 0); coordinate 4g + j sits in
  *             bits 2j, 2j+1 of byte g of the token's value code row.  cb_v is
  *             then unused (may be NULL) and every call takes a v_sq pool.
- *             The decode uses the split-K kernels in this format.
+ *             At head_dim 64 the decode uses the split-K kernels in this format.
  *             Other bits are reserved (NOVA_KV_ERR_UNSUPPORTED).
  */
 #define NOVA_KV_KEY_SCALE 1u

@@ -216,10 +216,10 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
     return fail(NOVA_KV_ERR_INVALID_ARG, "q, k_codes, v_codes, seq_lens or out is NULL");
   if (!aligned(k_codes, 16) || !aligned(v_codes, 16))
     return fail(NOVA_KV_ERR_INVALID_ARG, "code pools must be 16-byte aligned");
-  // the scalar value arm runs on the split-K kernels (block size 0 asks for them)
+  // the scalar value arm runs on the head_dim-128 table kernel, else on the split-K kernels
   const bool sq = (p->flags & NOVA_KV_SQ_VALUES) != 0;
   plan = novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len, layout->block_size,
-                             window, sq);
+                             window, sq && p->head_dim != 128);
   if (!workspace || workspace_bytes < plan.total)
     return fail(NOVA_KV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
                 workspace ? workspace_bytes : static_cast<size_t>(0));
@@ -313,7 +313,7 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
   if (!k_new || !v_new) return fail(NOVA_KV_ERR_INVALID_ARG, "k_new or v_new is NULL");
   const hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   hipError_t e;
-  if (plan.use_lut && p->head_dim == 128 && !(p->flags & NOVA_KV_KEY_SCALE) && !band) {
+  if (plan.use_lut && p->head_dim == 128 && !(p->flags & (NOVA_KV_KEY_SCALE | NOVA_KV_SQ_VALUES)) && !band) {
     // one launch: the table kernel encodes the new token and attends to it
     a.append = 1;
     a.k_new = k_new;

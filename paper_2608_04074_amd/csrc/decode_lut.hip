@@ -268,7 +268,7 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
   }
 }
 
-template <int WAVES, bool APPEND, bool KS, bool FP8>
+template <int WAVES, bool APPEND, bool KS, bool FP8, bool SQ>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int split, const int t0, const int t1, const size_t row0,
                                            const int rot, const int n_eff, const int S, float4 (&tv)[8]) {
@@ -292,6 +292,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   const uint32_t vbase = sbase + kVBase + 8 * v;
 
   float m_run = -INFINITY, l_run = 0.f;
+  float z_run = 0.f;  // scalar value arm: sum of p * offset of the column's tokens
   float4_t acc[8];
 #pragma unroll
   for (int X = 0; X < 8; ++X) acc[X] = float4_t{0.f, 0.f, 0.f, 0.f};
@@ -313,8 +314,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   const uint32_t koff = (4 * beta + v) * kL + 8 * u;  // lane offsets inside a 16-token sub-tile
   const uint32_t voff = 4 * u * kL + 8 * v;
   // Key-scale format: lane (beta, j) also loads the stored scale of token
-  // j of sub-tile beta, issued after the code bytes.
-  auto load_round = [&](int R, uint2 *kw, uint2 *vw, uint32_t &ks) {
+  // j of sub-tile beta, issued after the code bytes; the scalar value arm
+  // loads that token's (scale, offset) word the same way.
+  auto load_round = [&](int R, uint2 *kw, uint2 *vw, uint32_t &ks, uint32_t &vq) {
     size_t sub[4];  // uniform: byte offsets of the round's four sub-tiles
 #pragma unroll
     for (int r = 0; r < 4; ++r)
@@ -329,6 +331,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
     for (int s = 0; s < 4; ++s) vw[s] = *reinterpret_cast<const uint2 *>(vb + voff + s * kL);
     if constexpr (KS) ks = a.k_scales[subb / kL + (lane & 15)];
+    if constexpr (SQ) vq = reinterpret_cast<const uint32_t *>(a.v_sq)[subb / kL + (lane & 15)];
   };
   // Two named buffers of code bytes alternate through the token loop (unrolled
   // by two), so no in-flight load destination is ever copied: round rd+W is in
@@ -338,7 +341,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   // processing the current one, so waves that the issue arbiter serves less
   // often simply take fewer rounds and all waves end together.
   uint2 kwb[2][4], vwb[2][4];
-  uint32_t ksb[2] = {0u, 0u};
+  uint32_t ksb[2] = {0u, 0u}, vqb[2] = {0u, 0u};
   int *rctr = reinterpret_cast<int *>(smem + kAuxCtl) + 1;
   if (tid == 0) *rctr = WAVES;  // rounds 0 .. WAVES-1 are taken; visible after the setup's barriers
   if constexpr (APPEND) {
@@ -404,18 +407,20 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     // elements past the codebook wrap onto entries that other threads also
     // stage: the same value is written twice
     uint2 vst[VPER];
+    if constexpr (!SQ) {
 #pragma unroll
-    for (int k = 0; k < VPER; ++k) {
-      int g, c;
-      vmap((tid + k * NT + vrot) & (kL * 256 - 1), g, c);
-      vst[k] = codeword_raw(cbv, fp8, g * 256 + c);
+      for (int k = 0; k < VPER; ++k) {
+        int g, c;
+        vmap((tid + k * NT + vrot) & (kL * 256 - 1), g, c);
+        vst[k] = codeword_raw(cbv, fp8, g * 256 + c);
+      }
     }
     // waves 8 .. 8+G-1 form the shifted sink logit of head wave-8 (Lemma S1)
     const int sh = wave - 8;
     const float2 kb2 = *reinterpret_cast<const float2 *>(a.kbar + static_cast<size_t>(kv) * kD + 2 * lane);
     // a wave without a round of its own (nrounds >= 1 in an active split)
     // re-reads the last round and never processes it
-    load_round(max(0, R0 + 64 * min(wave, nrounds - 1)), kwb[0], vwb[0], ksb[0]);
+    load_round(max(0, R0 + 64 * min(wave, nrounds - 1)), kwb[0], vwb[0], ksb[0], vqb[0]);
     float *qs = reinterpret_cast<float *>(smem + kAuxQ);       // [4][128] query
     // partial q': [8 parts][32 groups][4 heads][4 coordinates], so that a table
     // lane's float4 (its group, its head) sits next to its neighbours'
@@ -428,7 +433,11 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     for (int k = 0; k < VPER; ++k) {
       int g, c;
       vmap((tid + k * NT + vrot) & (kL * 256 - 1), g, c);
-      *reinterpret_cast<uint2 *>(smem + kVBase + (g & 7) * 8192 + (c << 5) + 8 * (g >> 3)) = codeword_f16(vst[k], fp8);
+      // scalar value arm: every group's table maps a code byte to its four
+      // 2-bit codes q (0..3, exact in fp16), so the value MFMA sums
+      // p * scale * q; the offsets are summed apart
+      const uint2 e = SQ ? sq_unpack_f16(c) : codeword_f16(vst[k], fp8);
+      *reinterpret_cast<uint2 *>(smem + kVBase + (g & 7) * 8192 + (c << 5) + 8 * (g >> 3)) = e;
     }
     __syncthreads();
     if (sh >= 0 && sh < G) {
@@ -540,7 +549,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     asel[r] = half8_t{one, one, one, one, one, one, one, one};
   }
 
-  auto process_round = [&](const int R, const uint2 *kw, const uint2 *vw, const uint32_t ks) {
+  auto process_round = [&](const int R, const uint2 *kw, const uint2 *vw, const uint32_t ks, const uint32_t vq) {
     // K: partial logits gathered from the table by transposing reads; each
     // read hands lane (beta,u,v) four partials of (token R+16r+4beta+u, head v)
     // and serves as the B operand of a 16x16x32 MFMA (two steps per MFMA)
@@ -576,11 +585,24 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
       for (int i = 0; i < 4; ++i) z[i] *= __uint_as_float(static_cast<uint32_t>(__shfl(static_cast<int>(ks), 16 * beta + 4 * i + u)) << 16);
     }
+    // scalar value arm: (scale, offset) of token R + 16 beta + 4 i + u
+    float vsc[4] = {0.f, 0.f, 0.f, 0.f}, vzr[4] = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (SQ) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t w = static_cast<uint32_t>(__shfl(static_cast<int>(vq), 16 * beta + 4 * i + u));
+        vsc[i] = __uint_as_float(w << 16) * 0x1p-8f;  // the value MFMA's B operand stays below 2^8 * scale
+        vzr[i] = __uint_as_float(w & 0xffff0000u);
+      }
+    }
     if (R < t0 || R + 64 > t1) {  // ragged first or last round of the split
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int tok = R + 16 * beta + 4 * i + u;
-        if (tok < t0 || tok >= t1) z[i] = -INFINITY;
+        if (tok < t0 || tok >= t1) {
+          z[i] = -INFINITY;
+          vsc[i] = vzr[i] = 0.f;  // rows past the tokens may hold anything
+        }
       }
     }
 
@@ -604,13 +626,20 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
     for (int i = 0; i < 4; ++i) p[i] = __builtin_amdgcn_exp2f(z[i] - base);
     l_run = l_run * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
+    if constexpr (SQ) z_run = z_run * alpha + ((p[0] * vzr[0] + p[1] * vzr[1]) + (p[2] * vzr[2] + p[3] * vzr[3]));
     if (__any(bump && m_run != -INFINITY)) {  // accumulators of -inf columns are zero
 #pragma unroll
       for (int X = 0; X < 8; ++X) acc[X] *= alpha;
     }
     m_run = ref;
-    const half4_t pb = {static_cast<_Float16>(p[0]), static_cast<_Float16>(p[1]),
-                        static_cast<_Float16>(p[2]), static_cast<_Float16>(p[3])};
+    half4_t pb;
+    if constexpr (SQ) {
+      pb = half4_t{static_cast<_Float16>(p[0] * vsc[0]), static_cast<_Float16>(p[1] * vsc[1]),
+                   static_cast<_Float16>(p[2] * vsc[2]), static_cast<_Float16>(p[3] * vsc[3])};
+    } else {
+      pb = half4_t{static_cast<_Float16>(p[0]), static_cast<_Float16>(p[1]), static_cast<_Float16>(p[2]),
+                   static_cast<_Float16>(p[3])};
+    }
     const half4_t zero4 = {0, 0, 0, 0};
 
     // V: token sets s (tokens R + 16 beta + 4 i + s) in pairs; the A operand of
@@ -645,12 +674,12 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   int cur = wave;
   while (cur < nrounds) {
     const int nxt = claim();
-    if (nxt < nrounds) load_round(R0 + 64 * nxt, kwb[1], vwb[1], ksb[1]);
-    process_round(R0 + 64 * cur, kwb[0], vwb[0], ksb[0]);
+    if (nxt < nrounds) load_round(R0 + 64 * nxt, kwb[1], vwb[1], ksb[1], vqb[1]);
+    process_round(R0 + 64 * cur, kwb[0], vwb[0], ksb[0], vqb[0]);
     if (nxt >= nrounds) break;
     const int nxt2 = claim();
-    if (nxt2 < nrounds) load_round(R0 + 64 * nxt2, kwb[0], vwb[0], ksb[0]);
-    process_round(R0 + 64 * nxt, kwb[1], vwb[1], ksb[1]);
+    if (nxt2 < nrounds) load_round(R0 + 64 * nxt2, kwb[0], vwb[0], ksb[0], vqb[0]);
+    process_round(R0 + 64 * nxt, kwb[1], vwb[1], ksb[1], vqb[1]);
     cur = nxt2;
   }
 
@@ -665,6 +694,12 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   l_tot *= wcol;
   l_tot += row_ror<4>(l_tot);
   l_tot += row_ror<8>(l_tot);
+  float z_tot = 0.f;  // scalar value arm: the offsets' term of every coordinate of head v
+  if constexpr (SQ) {
+    z_tot = add_rows32(add_rows16(z_run)) * wcol;
+    z_tot += row_ror<4>(z_tot);
+    z_tot += row_ror<8>(z_tot);
+  }
 #pragma unroll
   for (int X = 0; X < 8; ++X) {
 #pragma unroll
@@ -701,7 +736,8 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
     for (int X = 0; X < 8; ++X)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) mw[8 + v * kMergeHead + kMergeBlk * beta + 4 * X + i] = acc[X][i];
+      for (int i = 0; i < 4; ++i)
+        mw[8 + v * kMergeHead + kMergeBlk * beta + 4 * X + i] = SQ ? fmaf(acc[X][i], 256.f, z_tot) : acc[X][i];
   }
   __syncthreads();
 
@@ -984,8 +1020,9 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
 // partial to the exchange and counts its arrival; the last one combines.
 // The arrival counters live in the workspace and the last split resets its
 // counter to 0, so a decode step is a single launch.
-template <int WAVES, bool APPEND, bool KS, bool FP8>
+template <int WAVES, bool APPEND, bool KS, bool FP8, bool SQ>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
+  static_assert(!(APPEND && SQ), "the fused step serves the codebook value format only");
   static_assert(!(APPEND && KS), "the fused step serves the plain format only");
   static_assert(WAVES == 12, "the exchange roles assume 12 waves");
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES, APPEND>()];
@@ -1020,7 +1057,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   }
 
   float4 tv[8];
-  split_pass<WAVES, APPEND, KS, FP8>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
+  split_pass<WAVES, APPEND, KS, FP8, SQ>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
   int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
   __syncthreads();  // the split's partial and its blocks of the new token are in LDS; the count is known
   if (a.n_split > 1) {
@@ -1087,22 +1124,29 @@ int plan_b_chunk(int batch, int num_kv_heads, int n_split) {
 hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream) {
   constexpr int W = 12;
   const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
-  if (a.append && (a.k_scales || a.band_k)) return hipErrorInvalidValue;
+  if (a.append && (a.k_scales || a.band_k || a.v_sq)) return hipErrorInvalidValue;
   const dim3 block(W * 64);
-  if (a.cb_fp8) {
-    if (a.append)
-      decode_lut_d128<W, true, false, true><<<grid, block, 0, stream>>>(a);
-    else if (a.k_scales)
-      decode_lut_d128<W, false, true, true><<<grid, block, 0, stream>>>(a);
+  if (a.v_sq) {  // the scalar value arm (keys in either codebook format)
+    if (a.k_scales)
+      a.cb_fp8 ? decode_lut_d128<W, false, true, true, true><<<grid, block, 0, stream>>>(a)
+               : decode_lut_d128<W, false, true, false, true><<<grid, block, 0, stream>>>(a);
     else
-      decode_lut_d128<W, false, false, true><<<grid, block, 0, stream>>>(a);
+      a.cb_fp8 ? decode_lut_d128<W, false, false, true, true><<<grid, block, 0, stream>>>(a)
+               : decode_lut_d128<W, false, false, false, true><<<grid, block, 0, stream>>>(a);
+  } else if (a.cb_fp8) {
+    if (a.append)
+      decode_lut_d128<W, true, false, true, false><<<grid, block, 0, stream>>>(a);
+    else if (a.k_scales)
+      decode_lut_d128<W, false, true, true, false><<<grid, block, 0, stream>>>(a);
+    else
+      decode_lut_d128<W, false, false, true, false><<<grid, block, 0, stream>>>(a);
   } else {
     if (a.append)
-      decode_lut_d128<W, true, false, false><<<grid, block, 0, stream>>>(a);
+      decode_lut_d128<W, true, false, false, false><<<grid, block, 0, stream>>>(a);
     else if (a.k_scales)
-      decode_lut_d128<W, false, true, false><<<grid, block, 0, stream>>>(a);
+      decode_lut_d128<W, false, true, false, false><<<grid, block, 0, stream>>>(a);
     else
-      decode_lut_d128<W, false, false, false><<<grid, block, 0, stream>>>(a);
+      decode_lut_d128<W, false, false, false, false><<<grid, block, 0, stream>>>(a);
   }
   return hipGetLastError();
 }

@@ -173,6 +173,13 @@ __device__ __forceinline__ uint2 codeword_f16(const uint2 raw, const int fp8) {
 __device__ __forceinline__ uint2 codeword(const void *cb, const int fp8, const size_t idx) {
   return codeword_f16(codeword_raw(cb, fp8, idx), fp8);
 }
+// Scalar value arm: a code byte's four 2-bit codes (coordinate j in bits
+// 2j, 2j+1) as fp16 values 0..3, two per word.
+__device__ __forceinline__ uint2 sq_unpack_f16(const uint32_t c) {
+  auto h = [](uint32_t q) -> uint32_t { return __builtin_bit_cast(uint16_t, static_cast<_Float16>(q & 3u)); };
+  return make_uint2(h(c) | (h(c >> 2) << 16), h(c >> 4) | (h(c >> 6) << 16));
+}
+
 // The codebook from codeword idx on (so that later indices stay small).
 __device__ __forceinline__ const void *codebook_from(const void *cb, const int fp8, const size_t idx) {
   return fp8 ? static_cast<const void *>(static_cast<const uint32_t *>(cb) + idx)
