@@ -397,7 +397,7 @@ def main():
         "append_kernel_us": {"mean": round(float(np.mean(enc_us)), 2),
                              "median_of_runs": round(float(np.median(enc_us)), 2)},
         "roofline": {
-            "kernel": f"{DECODE_KERNEL}<12, true, false, false> (the step's one launch: encode of the new token, query "
+            "kernel": f"{DECODE_KERNEL}<12, true, false, false, false> (the step's one launch: encode of the new token, query "
                       "transform, split pass, combine)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
