@@ -50,32 +50,35 @@ __device__ __forceinline__ uint16_t bf16_rne(const float x) {
   return static_cast<uint16_t>((f + 0x7fffu + ((f >> 16) & 1u)) >> 16);
 }
 
-// Attends the G query heads of unit (b, kv) to its band positions
-// [lo, sink_end) and [rec_lo, S) (at least one row in all).  On return, after
+// Attends the G query heads of unit (b, kv) to rows first .. first+count-1
+// (count >= 1) of its band positions [lo, sink_end) then [rec_lo, S).  On return, after
 // a barrier, the f32 words at kStat hold per head h < G the max of the band
 // logits (word h) and the sum of exp(z - max) (word GM + h), and kZ holds the
 // value sums acc[h][d] = sum_t exp(z_t - max) v_t[d].  Every thread of the
 // workgroup calls it; GM >= G heads, WAVES waves, the first VW of them take
-// the values.
+// the values.  q_lds / qk_lds: the query ([GM][D] f32, rows past G unused)
+// and q . k_bar per head already in LDS, or nullptr to read q and k_bar here.
 template <int D, int GM, int WAVES, int VW>
 __device__ __forceinline__ void band_attention(const DecodeArgs &a, uint8_t *scr, const int b, const int kv,
                                                const size_t row0, const int lo, const int sink_end,
-                                               const int rec_lo, const int S) {
+                                               const int rec_lo, const int S, const int first, const int count,
+                                               const float *q_lds = nullptr, const float *qk_lds = nullptr) {
   using Lay = BandLds<D, GM, VW>;
   static_assert(2 * GM <= 16 && GM % 4 == 0, "the A operand holds the high and low parts of GM heads");
   static_assert(VW <= WAVES && Lay::kBytes <= 65536, "band scratch");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = a.gqa;
-  float *qf = reinterpret_cast<float *>(scr + Lay::kQ);
+  const float *qf = q_lds ? q_lds : reinterpret_cast<const float *>(scr + Lay::kQ);
   float *st = reinterpret_cast<float *>(scr + Lay::kStat);
   float *zb = reinterpret_cast<float *>(scr + Lay::kZ);
   float *part = reinterpret_cast<float *>(scr + Lay::kPart);
   const int ns = sink_end > lo ? sink_end - lo : 0;
-  const int nb = ns + (S - rec_lo);
+  const int nb = count;
   const int nbr = a.n_sink + a.n_rec;
   const size_t hb = (static_cast<size_t>(b) * a.num_kv_heads + kv) * nbr;
-  auto row_of = [&](const int i) -> size_t {
+  auto row_of = [&](const int i0) -> size_t {
+    const int i = first + i0;
     const int p = i < ns ? lo + i : rec_lo + (i - ns);
     return (hb + band_slot(p, a.n_sink, a.n_rec)) * D;
   };
@@ -113,26 +116,35 @@ __device__ __forceinline__ void band_attention(const DecodeArgs &a, uint8_t *scr
   load_keys(0);
 
   // ---- query in fp32
-  for (int i = tid; i < GM * D; i += WAVES * 64) {
-    const int h = i / D;
-    float x = 0.f;
-    if (h < G) {
-      const size_t qi = (row0 + h) * D + (i % D);
-      x = a.q_bf16 ? bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi]) : static_cast<const float *>(a.q)[qi];
+  if (!q_lds) {
+    float *qw = reinterpret_cast<float *>(scr + Lay::kQ);
+    for (int i = tid; i < GM * D; i += WAVES * 64) {
+      const int h = i / D;
+      float x = 0.f;
+      if (h < G) {
+        const size_t qi = (row0 + h) * D + (i % D);
+        x = a.q_bf16 ? bf16_bits_to_float(static_cast<const uint16_t *>(a.q)[qi])
+                     : static_cast<const float *>(a.q)[qi];
+      }
+      qw[i] = x;
     }
-    qf[i] = x;
+    __syncthreads();
   }
-  __syncthreads();
 
   // ---- logits.  Every wave forms q . k_bar of all heads (uniform values) and
   // the A operands: lane (m, kg) holds row m, coordinates 32s + 8kg .. +7.
   float qk[GM];
 #pragma unroll
   for (int h = 0; h < GM; ++h) {
-    float x = 0.f;
+    if (qk_lds) {
+      qk[h] = qk_lds[h];
+    } else {
+      float x = 0.f;
 #pragma unroll
-    for (int j = 0; j < D / 64; ++j) x = fmaf(qf[h * D + lane + 64 * j], a.kbar[static_cast<size_t>(kv) * D + lane + 64 * j], x);
-    qk[h] = wave_sum(x);
+      for (int j = 0; j < D / 64; ++j)
+        x = fmaf(qf[h * D + lane + 64 * j], a.kbar[static_cast<size_t>(kv) * D + lane + 64 * j], x);
+      qk[h] = wave_sum(x);
+    }
   }
   bf16x8_t aq[D / 32];
 #pragma unroll

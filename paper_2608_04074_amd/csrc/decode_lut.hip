@@ -442,8 +442,12 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     __syncthreads();
     if (sh >= 0 && sh < G) {
       const float dot = wave_sum(fmaf(qs[sh * kD + 2 * lane], kb2.x, qs[sh * kD + 2 * lane + 1] * kb2.y));
-      if (lane == 0)
+      if (lane == 0) {
         reinterpret_cast<float *>(smem + kAuxCtl)[4 + sh] = a.sinks ? a.sinks[kv * G + sh] - a.scale * dot : -INFINITY;
+        // q . k_bar itself for the band's logits (the fused step, which has no
+        // band, keeps its encoder results in this region)
+        if constexpr (!APPEND) reinterpret_cast<float *>(smem + kItemRes)[sh] = dot;
+      }
     }
     if (tid < 512) {
       float4 acc[4];
@@ -803,6 +807,15 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 // new token are read from LDS, the other splits' from the exchange (every
 // word's tag checked, the words emptied once read); splits that attend to no
 // token published no partial and are skipped.
+// Rows of the band attended by split `split` of n_split: consecutive shares
+// in split order.
+__device__ __forceinline__ void band_share(const int nband, const int n_split, const int split, int &first,
+                                           int &count) {
+  const int per = (nband + n_split - 1) / n_split;
+  first = min(nband, split * per);
+  count = min(nband, first + per) - first;
+}
+
 template <int WAVES, bool APPEND>
 __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                              const int bk, const size_t row0, const int own_split, const int S,
@@ -811,11 +824,13 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
   const int tid = threadIdx.x;
   const int G = a.gqa;
   // Sink-plus-recent band: positions [band_lo, sink_end) and [tend, S) (the
-  // splits read [lo, tend) from the pools), attended here, in the table's
-  // LDS region, and taken after the splits as one more partial.
+  // splits read [lo, tend) from the pools).  Every split attended its share
+  // of the band rows (its partial is in LDS for this split, in the exchange
+  // for the others); the shares are merged in split order and taken after
+  // the splits as one more partial, whose value term is in the original
+  // domain.
   using BL = BandLds<kD, 4, WAVES>;
   const int nband = a.band_k ? max(0, sink_end - band_lo) + (S - tend) : 0;
-  if (nband > 0) band_attention<kD, 4, WAVES, WAVES>(a, smem, b, kv, row0, band_lo, sink_end, tend, S);
   float *bout = reinterpret_cast<float *>(smem + BL::kPart);  // [4][128] band term of the output
   float *shat = reinterpret_cast<float *>(smem + kAuxQ);    // [4][128]
   float *outp = reinterpret_cast<float *>(smem + kAuxOut);  // [part][head][128]
@@ -938,17 +953,53 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
     }
     float bo = 0.f;
     if (nband > 0) {  // the band, after the splits (and the new token)
-      const float *bst = reinterpret_cast<const float *>(smem + BL::kStat);
-      const float mb = bst[h], lb = bst[4 + h];
+      float mb = -INFINITY, lb = 0.f, ab = 0.f;
+      for (int sp = 0; sp < a.n_split; ++sp) {
+        int first, count;
+        band_share(nband, a.n_split, sp, first, count);
+        if (count == 0) continue;
+        float ms, ls, as;
+        if (sp == own_split) {
+          const float *bst = reinterpret_cast<const float *>(smem + BL::kStat);
+          ms = bst[h];
+          ls = bst[4 + h];
+          as = reinterpret_cast<const float *>(smem + BL::kZ)[h * kD + d];
+        } else {
+          const uint64_t *bw = a.xch + (static_cast<size_t>(bk) * a.n_split + sp) * kXchSlotWords + kXchBandWords;
+          uint64_t wm = get_word(bw + 2 * h), wl = get_word(bw + 2 * h + 1), wa = get_word(bw + 2 * G + tid);
+          for (int n = 0; !(word_ready(wm) && word_ready(wl) && word_ready(wa)); ++n) {
+            if (n == kSpinLimit) {
+              ok = false;
+              break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+            wm = get_word(bw + 2 * h);
+            wl = get_word(bw + 2 * h + 1);
+            wa = get_word(bw + 2 * G + tid);
+          }
+          ms = word_value(wm);
+          ls = word_value(wl);
+          as = word_value(wa);
+        }
+        if (ms > mb) {
+          const float f = mb == -INFINITY ? 0.f : __expf(mb - ms);
+          lb *= f;
+          ab *= f;
+          mb = ms;
+        }
+        const float w = __expf(ms - mb);
+        lb = fmaf(w, ls, lb);
+        ab = fmaf(w, as, ab);
+      }
       if (mb > big) {
         const float f = big == -INFINITY ? 0.f : __expf(big - mb);
         num *= f;
         den *= f;
         big = mb;
       }
-      const float wb = __expf(mb - big);
+      const float wb = mb == -INFINITY ? 0.f : __expf(mb - big);
       den = fmaf(wb, lb, den);
-      bo = wb * reinterpret_cast<const float *>(smem + BL::kZ)[h * kD + d];
+      bo = wb * ab;
     }
     // a word that never arrived (not expected) leaves this row NaN
     shat[tid] = !ok ? __builtin_nanf("") : (den > 0.f ? num / den : 0.f);
@@ -993,12 +1044,22 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
     const int h = tid >> 7;
     uint64_t *xs = a.xch + static_cast<size_t>(bk) * a.n_split * kXchSlotWords;
     for (int sp = 0; sp < a.n_split; ++sp) {
-      if (sp != own_split && lo + sp * a.chunk < tend) {
-        uint64_t *slot = xs + static_cast<size_t>(sp) * kXchSlotWords;
+      if (sp == own_split) continue;
+      uint64_t *slot = xs + static_cast<size_t>(sp) * kXchSlotWords;
+      if (lo + sp * a.chunk < tend) {
         clear_word(slot + 2 * G + tid);
         if (d == 0) {
           clear_word(slot + 2 * h);
           clear_word(slot + 2 * h + 1);
+        }
+      }
+      int first, count;
+      band_share(nband, a.n_split, sp, first, count);
+      if (count > 0) {
+        clear_word(slot + kXchBandWords + 2 * G + tid);
+        if (d == 0) {
+          clear_word(slot + kXchBandWords + 2 * h);
+          clear_word(slot + kXchBandWords + 2 * h + 1);
         }
       }
     }
@@ -1058,6 +1119,30 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
 
   float4 tv[8];
   split_pass<WAVES, APPEND, KS, FP8, SQ>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
+  // Sink-plus-recent band: this split's share of the band rows, attended in
+  // the table's LDS region (free after the split pass) and published beside
+  // the split's partial; one CU would read the whole band at a fraction of
+  // the HBM rate, so the shares spread it over the unit's workgroups.
+  const int nband = a.band_k ? max(0, spn.sink_end - att_lo) + (S - tend) : 0;
+  int bfirst = 0, bcount = 0;
+  if (nband > 0) {
+    band_share(nband, a.n_split, split, bfirst, bcount);
+    if (bcount > 0) {
+      using BL = BandLds<kD, 4, WAVES>;
+      band_attention<kD, 4, WAVES, WAVES>(a, smem, b, kv, row0, att_lo, spn.sink_end, tend, S, bfirst, bcount,
+                                          reinterpret_cast<const float *>(smem + kAuxQ),
+                                          reinterpret_cast<const float *>(smem + kItemRes));
+      if (a.n_split > 1 && tid < G * kD) {
+        const int h = tid >> 7;
+        uint64_t *bw = a.xch + (static_cast<size_t>(bk) * a.n_split + split) * kXchSlotWords + kXchBandWords;
+        put_word(bw + 2 * G + tid, reinterpret_cast<const float *>(smem + BL::kZ)[tid]);
+        if ((tid & (kD - 1)) == 0) {
+          put_word(bw + 2 * h, reinterpret_cast<const float *>(smem + BL::kStat)[h]);
+          put_word(bw + 2 * h + 1, reinterpret_cast<const float *>(smem + BL::kStat)[4 + h]);
+        }
+      }
+    }
+  }
   int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
   __syncthreads();  // the split's partial and its blocks of the new token are in LDS; the count is known
   if (a.n_split > 1) {
@@ -1069,6 +1154,14 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
       if ((tid & (kD - 1)) == 0) {
         clear_word(slot + 2 * (tid >> 7));
         clear_word(slot + 2 * (tid >> 7) + 1);
+      }
+    }
+    if (bcount > 0 && tid < G * kD) {
+      uint64_t *bw = a.xch + (static_cast<size_t>(bk) * a.n_split + split) * kXchSlotWords + kXchBandWords;
+      clear_word(bw + 2 * G + tid);
+      if ((tid & (kD - 1)) == 0) {
+        clear_word(bw + 2 * (tid >> 7));
+        clear_word(bw + 2 * (tid >> 7) + 1);
       }
     }
     if constexpr (APPEND) {

@@ -471,7 +471,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
   constexpr int kVW = 8;  // waves that sum the band's values
   using BL = BandLds<kD, kH, kVW>;
   const int nband = a.band_k ? max(0, sink_end - band_lo) + (S - tend) : 0;
-  if (nband > 0) band_attention<kD, kH, WAVES, kVW>(a, smem, b, kv, row0, band_lo, sink_end, tend, S);
+  if (nband > 0) band_attention<kD, kH, WAVES, kVW>(a, smem, b, kv, row0, band_lo, sink_end, tend, S, 0, nband);
   float *bout = reinterpret_cast<float *>(smem + BL::kPart);  // [8][64] band term of the output
   float *shat = reinterpret_cast<float *>(smem + kAuxQ);    // [8][64]
   float *outp = reinterpret_cast<float *>(smem + kAuxOut);  // [4 parts][8 heads][64]

@@ -77,7 +77,10 @@ struct DecodeArgs {
 
 // Words of one split's slot in the tagged exchange: (m, l) of up to 8 query
 // heads, then their accumulators (8 x 64 or 4 x 128 coordinates).
-constexpr int kXchSlotWords = 16 + 512;
+// A second block of the same size holds the split's share of the
+// sink-plus-recent band (its own (m, l) and original-domain accumulators).
+constexpr int kXchBandWords = 16 + 512;
+constexpr int kXchSlotWords = 2 * kXchBandWords;
 
 struct EncodeArgs {
   int batch, n_new, num_kv_heads, head_dim;
