@@ -12,10 +12,14 @@ Contents (each function cites the passage of the paper it follows):
                transform, volume-equalizing grouping fold, codebooks
   vq           exhaustive nearest-codeword encoder (plain C helper
                ``vq_ref.c``), Lloyd k-means, codeword lookup
-  codec        append-time encode of keys and values
+  codec        append-time encode of keys and values; the key-scale format
+               (per-token bf16 scale), the scalar value arm (per-token
+               affine INT2 in a rotation basis), bf16 storage of band rows
   attention    plain-form decode attention (reconstruct, then textbook
-               softmax attention with an optional sink); a fast split form
-               used only to check the plain one
+               softmax attention with an optional sink), with the key scale,
+               the sink-plus-recent band and the scalar value arm; a fast
+               split form used only to check the plain one
+  fp8          fp8 E4M3 snapping of the codebooks
   grouping     Theorem 2 volumes, rate allocation and distortions
   accounting   cache byte and parameter counts
 
@@ -25,4 +29,4 @@ except Lloyd training beyond its invariants (monotone distortion, lossless on
 codebook values, which are inputs to the GPU path, not outputs it must match.
 """
 
-from . import accounting, attention, calibration, codec, grouping, vq  # noqa: F401
+from . import accounting, attention, calibration, codec, fp8, grouping, vq  # noqa: F401
