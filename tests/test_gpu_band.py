@@ -344,3 +344,13 @@ def test_append_decode(nk, qwen, gptoss, shape):
                                              None if sinks is None else sinks[heads],
                                              band=(n_sink, n_rec, kb, vb))
     assert_outputs_close(out.reshape(-1, D), ref.reshape(-1, D), what=f"band step {shape}")
+
+
+def test_many_splits_share_the_band(nk, qwen):
+    """One sequence of 16384 tokens: 32 splits, each attending about ten band
+    rows, with the band cut by a window and a sink."""
+    wl, params, P = qwen
+    sinks = np.random.default_rng(12).standard_normal(wl.num_q_heads).astype(np.float32)
+    _band_case(nk, wl, params, P, [16384], 16384, 64, 256, what="qwen B=1 S=16384 (32 splits)")
+    _band_case(nk, wl, params, P, [16384], 16384, 64, 256, window=16300, sinks=sinks,
+               what="qwen B=1 S=16384 window 16300")
