@@ -5,8 +5,9 @@ rotation t_v, with bf16 scale and offset).
   offsets equal to the oracle's except at rounding boundaries (an unrounded
   code within 1e-9 of a half-integer, a scale or offset within 1e-12
   relative of a bf16 rounding boundary);
-* decode (the split-K kernels): max-abs error within 2e-3 of each output
-  row's L2 norm, with windows, sinks, the key-scale format and the band.
+* decode (the head_dim-128 table kernel, the split-K kernels at head_dim 64):
+  max-abs error within 2e-3 of each output row's L2 norm, with windows,
+  sinks, the key-scale format, fp8 key codebooks and the band.
 """
 
 import numpy as np
@@ -255,3 +256,16 @@ def test_append_decode(nk):
             ref[b, heads] = oatt.decode_rows(q[b, heads], hk[b, kv, :p + 1], hv[b, kv, :p + 1], hp, scale,
                                              sq_v=(hs[b, kv, :p + 1, 0], hs[b, kv, :p + 1, 1]))
     assert_outputs_close(out.reshape(-1, D), ref.reshape(-1, D), what="sq step")
+
+
+def test_all_formats_together(nk):
+    """Key scale, fp8 key codebooks, the band and the scalar value arm in one decode."""
+    from oracle import fp8 as ofp8
+    wl = synth.get_workload("qwen3_8b")
+    params = calibrated_params(wl, 0, key_scale=True, fp8=True)
+    b8 = dict(params, cb_k=ofp8.e4m3_bits(params["cb_k"].astype(np.float64)), cb_v=None)
+    P = nk.NovaKVParams.from_arrays(b8, key_scale=True, sq_values=True)
+    assert P.fp8_codebooks and P.key_scale and P.sq_values
+    sinks = np.random.default_rng(4).standard_normal(wl.num_q_heads).astype(np.float32)
+    _sq_decode_case(nk, wl, params, P, [2304, 1500, 300, 1], 2304, window=1000, sinks=sinks, key_scale=True,
+                    band=(64, 256), what="qwen all formats")
