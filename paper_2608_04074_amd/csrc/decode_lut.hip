@@ -239,23 +239,10 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
       res[item * 32 + 4 * gl + lr] = v;
     }
   };
-#ifdef ITEM_PREFETCH
-  ItemRegs r2;
-  for (int k = 0; k < nmine; k += 2) {
-    if (k + 1 < nmine) load_item_rows(a, b, kv, split, n_eff, k + 1, t, r2);
-    encode_one(k, r);
-    if (k + 1 >= nmine) break;
-    load_item_cw(a, kv, split, n_eff, k + 1, t, r2);
-    if (k + 2 < nmine) load_item_rows(a, b, kv, split, n_eff, k + 2, t, r);
-    encode_one(k + 1, r2);
-    if (k + 2 < nmine) load_item_cw(a, kv, split, n_eff, k + 2, t, r);
-  }
-#else
   for (int k = 0; k < nmine; ++k) {
     if (k > 0) load_item(a, b, kv, split, n_eff, k, t, r, fp8);
     encode_one(k, r);
   }
-#endif
   team_sync(smem, ++phase);
   if (t < G) {
     for (int item = split; item < 4; item += n_eff) {
