@@ -77,13 +77,14 @@ typedef enum {
  * K = 256, D in {64, 128}.  Every array must be 16-byte aligned
  * (NOVA_KV_ERR_INVALID_ARG otherwise).
  *
- *   flags     0, or NOVA_KV_KEY_SCALE: the key-scale format (paper: Algorithm
+ *   flags     0 or any combination of the three formats below.
+ *             NOVA_KV_KEY_SCALE: the key-scale format (paper: Algorithm
  *             2 normalizes r_j by rho_j = ||r_j||_2 / sqrt(D) before the
  *             codebooks are trained; Sec. "Bit rate": a BF16 scale per token;
  *             Sec. "Decoding kernel and read path": the read path multiplies
  *             the partial logit by it).  cb_k must then hold codebooks of
  *             normalized coefficients, and every call takes a k_scales pool.
- *             NOVA_KV_FP8_CODEBOOKS (may be combined with the above): the
+ *             NOVA_KV_FP8_CODEBOOKS: the
  *             codebooks are stored as fp8 E4M3 bytes (OCP format: bias 7, no
  *             infinities; paper: Sec. "Calibration", codebooks kept in fp16
  *             and snapped to fp8 offline), 4 bytes per codeword; every value
