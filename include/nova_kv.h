@@ -182,7 +182,9 @@ typedef struct {
  *   k, v       [B][n_new][Hkv][D] device, dtype in_dtype (F32 or BF16)
  *   start_pos  [B] int32 device: position of the first new token of each
  *              sequence; precondition start_pos[b] + n_new <= block_size *
- *              blocks_per_seq.
+ *              blocks_per_seq.  A token whose position falls outside
+ *              [0, block_size * blocks_per_seq) is not stored (nothing of it is
+ *              written: codes, scales or band rows).
  *   k_codes, v_codes  code pools (see nova_kv_layout), written at positions
  *              start_pos[b] .. start_pos[b] + n_new - 1; nothing else is touched.
  *   k_scales   key-scale format only (else ignored, may be NULL): the scale
@@ -280,7 +282,8 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
  *
  *   k_new, v_new  [B][Hkv][D] device, dtype new_dtype (F32 or BF16): the token
  *              at position seq_lens[b] - 1 of each sequence (the newest cached
- *              token); precondition seq_lens[b] >= 1.
+ *              token).  A sequence with seq_lens[b] == 0 stores nothing and
+ *              attends to nothing: its output rows are zeros.
  *   k_codes, v_codes (and k_scales, v_sq in their formats, band when
  *              given)  written at position seq_lens[b] - 1 exactly as
  *              nova_kv_encode(n_new = 1, start_pos = seq_lens - 1) writes them

@@ -23,10 +23,15 @@ Contents (each function cites the passage of the paper it follows):
   grouping     Theorem 2 volumes, rate allocation and distortions
   accounting   cache byte and parameter counts
 
-Parity status: every function is pinned by tests in ``tests/test_oracle_*.py``
-except Lloyd training beyond its invariants (monotone distortion, lossless on
-<= k distinct points, determinism) -- "parity unpinned" for the exact
-codebook values, which are inputs to the GPU path, not outputs it must match.
+Parity status: every function is pinned by tests in ``tests/test_oracle_*.py``.
+Lloyd training is pinned by its invariants (monotone distortion, lossless on
+<= k distinct points, determinism), by scikit-learn's Lloyd from the same
+start when no cluster empties, by a start that must be k distinct training
+points, and by a hand-built case whose empty clusters must be refilled from
+the worst-fit points, farthest first.  The value grouping is pinned by a
+distribution on which the variance order, its reverse, the eigenvalue order
+of M_o and the raw-coordinate order all differ.  The pins of these steps are
+also run against planted mistakes, which they must catch.
 """
 
 from . import accounting, attention, calibration, codec, fp8, grouping, vq  # noqa: F401

@@ -128,6 +128,19 @@ def value_transform(mo: np.ndarray):
     return e, lam
 
 
+def value_grouping_order(v_cal: np.ndarray, r_v: np.ndarray) -> np.ndarray:
+    """Columns of R_V ranked for the grouping: decreasing empirical variance of v R_V.
+
+    Paper, Sec. "KV cache vector quantization" (the equalizing grouping deals
+    coordinates sorted by decreasing variance) and Algorithm 2 (the same fold
+    for the values).  The sort key for the values is the variance of the
+    rotated calibration values (reading: for the keys it coincides with the
+    eigenvalue order); ties keep the eigenvalue order.
+    """
+    var_v = (v_cal @ r_v).var(axis=0)
+    return np.argsort(-var_v, kind="stable")
+
+
 def equalizing_columns(d: int, g: int) -> np.ndarray:
     """Column position of each variance rank under the volume-equalizing partition.
 
@@ -172,10 +185,7 @@ def calibrate_head(k_cal: np.ndarray, v_cal: np.ndarray, q_cal: np.ndarray, *,
 
     mo = output_second_moment(q_cal, k_cal, v_cal, mo_stride, scale)
     r_v, lam_v = value_transform(mo)
-    s_cal = v_cal @ r_v
-    var_v = s_cal.var(axis=0)
-    order_v = np.argsort(-var_v, kind="stable")
-    t_v = fold_columns(r_v[:, order_v], g)
+    t_v = fold_columns(r_v[:, value_grouping_order(v_cal, r_v)], g)
 
     stored = {
         "kbar": kbar.astype(np.float32),

@@ -48,12 +48,28 @@ def nearest_codeword(u: np.ndarray, codebook: np.ndarray):
     return codes, best, second
 
 
+def initial_indices(rng: np.random.Generator, n: int, k: int) -> np.ndarray:
+    """Training points that start Lloyd: k distinct indices, uniformly without replacement."""
+    return rng.choice(n, size=k, replace=False)
+
+
+def reseed_indices(best: np.ndarray, n_empty: int) -> np.ndarray:
+    """Training points that refill empty clusters: the worst-fit points first.
+
+    ``best`` holds each point's squared distance to the centroid it was
+    assigned to; the n_empty points with the largest such distance are taken
+    in decreasing order of it (equal distances in index order), so the i-th
+    empty cluster gets the i-th worst-fit point (Sec. "Calibration").
+    """
+    return np.argsort(-best, kind="stable")[:n_empty]
+
+
 def lloyd(points: np.ndarray, k: int, seed, max_iter: int = 25, return_history: bool = False):
     """k-means (Lloyd) codebook for one group, in fp64.
 
-    Paper, Algorithm 3 and Sec. "Calibration": k-means with random
-    initialisation, at most 25 iterations, empty clusters reseeded each
-    iteration from the points farthest from their centroid.
+    Paper, Algorithm 3 and Sec. "Calibration": k-means from a random start,
+    no more than 25 iterations, and every iteration refills empty clusters
+    from the worst-fit training points.
 
     Readings where the paper is silent:
       * initialisation: k distinct training points drawn uniformly without
@@ -73,7 +89,7 @@ def lloyd(points: np.ndarray, k: int, seed, max_iter: int = 25, return_history: 
     rng = np.random.default_rng(seed)
     if n < k:
         raise ValueError("need at least k training points")
-    cent = x[rng.choice(n, size=k, replace=False)].copy()
+    cent = x[initial_indices(rng, n, k)].copy()
     prev = None
     history = []
     for _ in range(max_iter):
@@ -89,8 +105,7 @@ def lloyd(points: np.ndarray, k: int, seed, max_iter: int = 25, return_history: 
         cent[nonempty] = sums[nonempty] / counts[nonempty, None]
         empty = np.flatnonzero(~nonempty)
         if empty.size:
-            far = np.argsort(-best, kind="stable")[:empty.size]
-            cent[empty] = x[far]
+            cent[empty] = x[reseed_indices(best, empty.size)]
     else:
         assign, best, _ = nearest_codeword(x, cent)
         history.append(float(best.sum()))

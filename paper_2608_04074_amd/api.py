@@ -7,6 +7,7 @@ current HIP stream, and raises on a non-OK status.
 
 from __future__ import annotations
 
+import contextlib
 import ctypes
 from typing import Optional
 
@@ -22,6 +23,16 @@ __all__ = ["NovaKVParams", "CacheLayout", "Band", "band_shape", "encode", "decod
 def _stream_ptr(stream: Optional[torch.cuda.Stream]) -> int:
     s = stream if stream is not None else torch.cuda.current_stream()
     return int(s.cuda_stream)
+
+
+def _on_stream(stream: Optional[torch.cuda.Stream]):
+    """Context in which temporaries of a call are created: the call's stream.
+
+    The output and the zero-filled workspace that a call allocates for itself
+    are then created and filled on the stream the kernels run on, so the
+    fill is ordered before the launch, and the caching allocator only hands
+    their memory to later work of that same stream once they are freed."""
+    return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
 
 
 def _require(t: torch.Tensor, name: str, dtypes, numel: Optional[int] = None) -> None:
@@ -259,12 +270,13 @@ def decode_attn(params: NovaKVParams, layout: CacheLayout, q: torch.Tensor,
     _require(seq_lens, "seq_lens", (torch.int32,), b)
     if sinks is not None:
         _require(sinks, "sinks", (torch.float32,), hq)
-    if out is None:
-        out = torch.empty((b, hq, d), dtype=torch.float32, device=q.device)
-    _require(out, "out", (torch.float32,), b * hq * d)
     need = decode_workspace_bytes(params, b, hq, max_seq_len) if b > 0 else 0
-    if workspace is None:
-        workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=q.device)
+    with _on_stream(stream):
+        if out is None:
+            out = torch.empty((b, hq, d), dtype=torch.float32, device=q.device)
+        if workspace is None:
+            workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=q.device)
+    _require(out, "out", (torch.float32,), b * hq * d)
     _require(workspace, "workspace", (torch.uint8,))
     ks = _scales_ptr(params, k_scales, k_codes)
     nat.check(nat.lib().nova_kv_decode_attn(
@@ -319,11 +331,12 @@ def append_decode_attn(params: NovaKVParams, layout: CacheLayout, k_new: torch.T
     position seq_lens[b] - 1 of the pools, then decode q [B][Hq][D] over the
     cache including them -> out [B][Hq][D] fp32.  Workspace as in decode_attn."""
     b, hq, d = q.shape
-    if out is None:
-        out = torch.empty((b, hq, d), dtype=torch.float32, device=q.device)
     need = decode_workspace_bytes(params, b, hq, max_seq_len) if b > 0 else 0
-    if workspace is None:
-        workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=q.device)
+    with _on_stream(stream):
+        if out is None:
+            out = torch.empty((b, hq, d), dtype=torch.float32, device=q.device)
+        if workspace is None:
+            workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=q.device)
     args = _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
                                workspace, window, sinks, softmax_scale, stream, k_scales, band, v_sq)
     nat.check(nat.lib().nova_kv_append_decode_attn(*args))

@@ -21,7 +21,7 @@ namespace {
 __device__ __forceinline__ void store_band(const EncodeArgs &a, const int side, const int b, const int kv,
                                            const int pos, const int end, const int d, const uint16_t bits) {
   uint16_t *band = side == 0 ? a.band_k : a.band_v;
-  if (!band) return;
+  if (!band || !position_in_pool(a.layout, pos)) return;
   if (!(pos < a.n_sink || (a.n_rec > 0 && pos >= end - a.n_rec))) return;
   const int nb = a.n_sink + a.n_rec;
   band[((static_cast<size_t>(b) * a.num_kv_heads + kv) * nb + band_slot(pos, a.n_sink, a.n_rec)) * a.head_dim + d] =
@@ -58,6 +58,8 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   const size_t cw0 = static_cast<size_t>(kv) * L * kCodebookSize;
   const void *src = side == 0 ? a.k : a.v;
   uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
+  const int pos = a.start_pos[b] + a.start_offset + t;
+  if (!position_in_pool(a.layout, pos)) return;  // uniform: the workgroup stores nothing
 
   float4 trow[D / 32];
   uint2 cw[encblk::kPer];
@@ -74,7 +76,6 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
     }
   }
   __syncthreads();
-  const int pos = a.start_pos[b] + a.start_offset + t;
   const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos);
   int code;
   if (side == 0 && a.k_scales) {
@@ -206,9 +207,9 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
     if (tid < TT) {
       const double rho = encblk::key_scale<D>(&xs[tid * RS]);
       rhos[tid] = rho;
-      if (tid < nt) {
-        const size_t off =
-            code_row_offset(a.layout, a.num_kv_heads, L, b, kv, a.start_pos[b] + a.start_offset + n0 + tid);
+      const int pos = a.start_pos[b] + a.start_offset + n0 + tid;
+      if (tid < nt && position_in_pool(a.layout, pos)) {
+        const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos);
         a.k_scales[off / L] = encblk::bf16_of(rho);
       }
     }
@@ -288,7 +289,9 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   __syncthreads();
   for (int i = tid; i < nt * L; i += 256) {
     const int t = i / L, ell = i % L;
-    const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, a.start_pos[b] + a.start_offset + n0 + t);
+    const int pos = a.start_pos[b] + a.start_offset + n0 + t;
+    if (!position_in_pool(a.layout, pos)) continue;
+    const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos);
     pool[off + ell] = codes[t][ell];
   }
 }
@@ -309,10 +312,11 @@ __global__ void __launch_bounds__(D) encode_sq_values(EncodeArgs a) {
   __shared__ double red[2][D / 64];
   __shared__ uint8_t qs[D];
   const int t = blockIdx.x, kv = blockIdx.y, b = blockIdx.z, i = threadIdx.x;
+  const int p0 = a.start_pos[b] + a.start_offset;
+  if (!position_in_pool(a.layout, p0 + t)) return;  // uniform: the workgroup stores nothing
   const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + i;
   xs[i] = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(a.v)[idx]))
                     : static_cast<double>(static_cast<const float *>(a.v)[idx]);
-  const int p0 = a.start_pos[b] + a.start_offset;
   if (a.band_v) store_band(a, 1, b, kv, p0 + t, p0 + a.n_new, i, input_bf16_bits(a, a.v, idx));
   __syncthreads();
   const float *tv = a.t_v + static_cast<size_t>(kv) * D * D;

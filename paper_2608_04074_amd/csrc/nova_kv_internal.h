@@ -17,6 +17,13 @@ struct CacheLayout {
   const int32_t *block_table;  // device [B][blocks_per_seq] or nullptr
 };
 
+// Whether position t lies in a sequence's rows of the pools, [0, capacity).
+// The encoders store nothing for a position outside it (a step call on an
+// empty sequence asks for position -1), as the fused step skips S = 0.
+__device__ __forceinline__ bool position_in_pool(const CacheLayout &lay, int t) {
+  return t >= 0 && static_cast<long long>(t) < static_cast<long long>(lay.block_size) * lay.blocks_per_seq;
+}
+
 // Byte offset of the L code bytes of (sequence b, KV head kv, token t).
 __device__ __forceinline__ size_t code_row_offset(const CacheLayout &lay, int num_kv_heads,
                                                   int groups, int b, int kv, int t) {

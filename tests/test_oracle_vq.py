@@ -3,6 +3,7 @@
 import itertools
 
 import numpy as np
+import pytest
 from scipy.spatial import cKDTree
 
 from oracle import vq
@@ -88,3 +89,58 @@ def test_encode_and_lookup_roundtrip():
     assert np.array_equal(codes[~dup], codes_true[~dup])
     assert np.array_equal(vq.lookup(codes, books), x)
     assert np.all(gap >= 0)
+
+
+# ---- Lloyd's start and its refill of empty clusters (Sec. "Calibration"; Algorithm 3)
+
+def _two_far_points():
+    """1000 copies of the origin and two outliers, at squared distances 100 and 400."""
+    x = np.zeros((1002, 4))
+    x[1000, 0] = 10.0   # F1
+    x[1001, 0] = 20.0   # F2
+    return x
+
+
+def check_refill(lloyd_fn):
+    """Three clusters started on copies of the origin: two are empty after the
+    first assignment (equal centroids, ties to the lowest index) and must be
+    refilled from the worst-fit points, the farthest first.  Seed 3 starts on
+    three origin copies (distortion 100 + 400 at the first assignment).
+    Afterwards cluster 0 sits at the origin, cluster 1 at the farther outlier,
+    cluster 2 at the nearer one, and the training distortion is zero."""
+    x = _two_far_points()
+    cent, hist = lloyd_fn(x, 3, seed=3, max_iter=25, return_history=True)
+    assert hist[0] == 500.0, "the start was not three copies of the origin"
+    return (np.array_equal(cent[0], x[0]) and np.array_equal(cent[1], x[1001])
+            and np.array_equal(cent[2], x[1000]) and hist[-1] == 0.0)
+
+
+def test_lloyd_refills_empty_clusters_from_the_worst_fit_points():
+    assert check_refill(vq.lloyd)
+
+
+@pytest.mark.parametrize("mistake", ["nearest", "increasing"])
+def test_lloyd_refill_pin_catches_planted_mistakes(monkeypatch, mistake):
+    """The refill pin fails when the refill takes the best-fit points, or the
+    worst-fit points in increasing order of their distance."""
+    fn = {"nearest": lambda best, n: np.argsort(best, kind="stable")[:n],
+          "increasing": lambda best, n: np.argsort(-best, kind="stable")[:n][::-1]}[mistake]
+    monkeypatch.setattr(vq, "reseed_indices", fn)
+    assert not check_refill(vq.lloyd)
+
+
+def test_lloyd_starts_on_distinct_training_points():
+    """k distinct points and n = k: a start on k distinct indices is already the
+    lossless codebook (zero distortion at the first assignment)."""
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((256, 4))
+    _, hist = vq.lloyd(x, 256, seed=5, return_history=True)
+    assert hist[0] == 0.0 and len(hist) == 2      # nothing moves: stop after the second assignment
+
+
+def test_lloyd_start_pin_catches_draws_with_replacement(monkeypatch):
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((256, 4))
+    monkeypatch.setattr(vq, "initial_indices", lambda r, n, k: r.choice(n, size=k, replace=True))
+    _, hist = vq.lloyd(x, 256, seed=5, return_history=True)
+    assert hist[0] > 0.0
