@@ -11,8 +11,8 @@
  *                        values, pick the nearest codeword of every group, and
  *                        store the code bytes (paper: Algorithm 1, "Write";
  *                        Theorem 1 and Corollary 1 for the transforms; Sec.
- *                        "Calibration": exact Euclidean nearest-neighbour
- *                        search in the transform domain).
+ *                        "Calibration": the codeword at the smallest squared
+ *                        distance, searched over the whole codebook).
  *   nova_kv_decode_attn  single-token decode attention read straight from the
  *                        codes (paper: Algorithm 1, "Attention"; Sec. "Decoding
  *                        kernel and read path"; Appendix "Attention sinks in the
@@ -86,8 +86,8 @@ typedef enum {
  *             normalized coefficients, and every call takes a k_scales pool.
  *             NOVA_KV_FP8_CODEBOOKS: the
  *             codebooks are stored as fp8 E4M3 bytes (OCP format: bias 7, no
- *             infinities; paper: Sec. "Calibration", codebooks kept in fp16
- *             and snapped to fp8 offline), 4 bytes per codeword; every value
+ *             infinities; paper: Sec. "Calibration", the fp16 codebooks are
+ *             rounded to fp8 ahead of use), 4 bytes per codeword; every value
  *             is used exactly (E4M3 values are exact in fp16).
  *             NOVA_KV_SQ_VALUES: the scalar value arm (paper: Sec. "Bit rate"
  *             and the implementation table: per-token affine INT2 values with

@@ -2,8 +2,8 @@
 
 Test infrastructure only (see ``oracle/__init__.py``).
 
-Paper, Sec. "Calibration" and the implementation table: one codebook per group
-and (layer, KV head), kept in float16 and snapped to fp8 offline.  The fp8
+Paper, Sec. "Calibration" and the implementation table: each group's codebook
+(per layer and KV head) is stored in fp16 and rounded to fp8 ahead of use.  The fp8
 format is taken to be OCP E4M3 ("e4m3fn"): sign bit, 4 exponent bits with
 bias 7, 3 mantissa bits, no infinities, the code with all exponent and
 mantissa bits set is NaN; normals (-1)^s 2^(e-7) (1 + m/8), subnormals

@@ -6,9 +6,9 @@
  * does.  It shares no code with the GPU library.
  *
  * A vector quantizer's encoder maps a subvector to the index of its nearest
- * codeword (paper, Sec. "Transform coding", quantization paragraph); the
- * encoding in the transform domain is an exact nearest-neighbour search in the
- * Euclidean metric (paper, Sec. "Calibration").  This file is that definition
+ * codeword (paper, Sec. "Transform coding", quantization paragraph); in the
+ * transform domain that codeword is the one at the smallest squared Euclidean
+ * distance, found exhaustively (paper, Sec. "Calibration").  This file is that definition
  * written out: the squared distance sum_i (u_i - c_i)^2 accumulated over i in
  * order, in fp64, and the smallest index among equal minima.
  *

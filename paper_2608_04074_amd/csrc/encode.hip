@@ -2,8 +2,8 @@
 // codeword index of every group.
 //
 // Paper: Algorithm 1 (write step, Q+((k - k_bar) R_K)), Theorem 1 (key
-// transform), Corollary 1 (s = v R_V), Sec. "Calibration" (exact
-// nearest-neighbour search in the Euclidean metric of the transform domain).
+// transform), Corollary 1 (s = v R_V), Sec. "Calibration" (each group gets
+// the codeword at the smallest squared distance in the transform domain).
 // The transform and the distances are evaluated in fp64 so that the stored
 // index is the exact argmin (smallest index among equal distances).
 #include <math.h>
