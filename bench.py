@@ -7,13 +7,15 @@ step's new key/value (one token per sequence, stored at position S-1) and
 runs decode attention of one query per head over all S cached tokens.  The
 same step as two calls (nova_kv_encode, then nova_kv_decode_attn) is timed
 beside it, and each of those kernels alone.
-Inputs are resident in HBM before timing; the code pools rotate over six
-copies (6 x 64 MiB) so the 256 MB last-level cache cannot serve them.
+Inputs are resident in HBM before timing.  Every code pool of 16 MiB or more
+rotates over enough copies (at least 600 MiB in all) that the 256 MB
+last-level cache cannot serve it.
 
 Printed metric: effective compressed-KV bandwidth = K+V code bytes attended
 per step / time per step, with microseconds per step and the fraction of the
 8 TB/s HBM peak beside it.  A CPU baseline (the fp64 oracle on host cores, a
-bounded sample of the same workload) is reported next to it.
+bounded sample of the same workload, one process per core) is reported next
+to it.
 """
 
 from __future__ import annotations
@@ -32,8 +34,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+FP64_MFMA_PEAK_TFLOPS = 78.6
 WORKLOAD = "qwen3_8b"
-COPIES = 6
+ROTATE_MIN_BYTES = 16 << 20       # pools this large rotate over copies ...
+ROTATE_TOTAL_BYTES = 600 << 20    # ... until the copies hold at least this much
 DECODE_KERNEL = "decode_lut_d128"
 # The step kernel's source and the headers it includes: a change to any of
 # them invalidates the committed counter summary.
@@ -42,6 +46,20 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_04074_amd", "csrc", f)
                             "nova_kv_internal.h")]
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_lut_d128_qwen3_8b_traffic.md")
 COPY_CALIB_BYTES = 256 << 20
+# Algorithmic work of the append encoder per token-head (D = 128, two sides):
+# the transform (2 D^2 flops per side) and the exhaustive distances
+# (2 * 256 * D flops per side: one multiply-add per codeword coordinate).
+ENCODE_FLOPS_PER_TOKEN_HEAD = 2 * (2 * 128 * 128) + 2 * (2 * 256 * 128)
+
+# Other workload lines: (name, layer, key-scale format, band (n_sink, n_rec) or
+# None, fp8 codebooks, scalar value arm).
+OTHER_CASES = [("single_head", 0, False, None, False, False), ("sweep_b64_s32k", 0, False, None, False, False),
+               ("sweep_b1_s128k", 0, False, None, False, False), ("gptoss_pair", 0, False, None, False, False),
+               ("gptoss_pair", 1, False, None, False, False), ("append_paged", 0, False, None, False, False),
+               ("qwen3_8b", 0, True, None, False, False), ("gptoss_pair", 1, True, None, False, False),
+               ("qwen3_8b", 0, False, (64, 256), False, False), ("gptoss_pair", 1, False, (64, 256), False, False),
+               ("qwen3_8b", 0, False, None, True, False), ("gptoss_pair", 1, False, None, True, False),
+               ("qwen3_8b", 0, False, None, False, True)]
 
 
 def parse():
@@ -51,10 +69,14 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1000)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
-                    help="approximate CPU time budget of the oracle baseline sample")
+                    help="approximate wall time of the oracle baseline sample")
     ap.add_argument("--skip-append", action="store_true")
     ap.add_argument("--skip-others", action="store_true",
                     help="do not time the decode of the other workload shapes")
+    ap.add_argument("--only", default=None,
+                    help="time one line only and skip the headline: an other-workload label prefix "
+                         "(e.g. 'sweep_b1_s128k', 'gptoss_pair layer 1'), or 'append_encode'")
+    ap.add_argument("--calls", type=int, default=200, help="timed calls per other-workload line")
     ap.add_argument("--copy-calib", action="store_true",
                     help=f"finish with one plain device copy of {COPY_CALIB_BYTES >> 20} MiB, the known-size "
                          "reference for scaling FETCH_SIZE / WRITE_SIZE counter runs")
@@ -83,144 +105,237 @@ def measured_traffic():
     return int(val.group(1))
 
 
-def cpu_baseline(wl, budget_s: float):
-    """Time the fp64 oracle (plain-form decode + encode of the new token) on sampled units."""
+def rotation_copies(pool_bytes: int, at_least: int = 1) -> int:
+    """Copies of a pool so that a rotation over them defeats the last-level cache."""
+    if pool_bytes < ROTATE_MIN_BYTES:
+        return at_least
+    return max(at_least, -(-ROTATE_TOTAL_BYTES // pool_bytes))
+
+
+# ------------------------------------------------------------------ CPU baseline
+
+def _cpu_unit(task):
+    """One (sequence, KV head) unit of the step in the oracle: encode the new
+    token, then the plain-form fp64 decode of the G heads over S tokens.
+    Runs in a worker process with one BLAS/OpenMP thread."""
+    b, kv = task
     from oracle import attention as oatt
     from oracle import codec as ocodec
     import synth
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        threads = 1
-    params = synth.bench_params(wl)
-    S, L, G, D = wl.seq_len, wl.groups, wl.gqa, wl.head_dim
-    q = synth.decode_queries(wl, 0)
-    scale = 1.0 / np.sqrt(D)
-    rng = np.random.default_rng(0)
-    units = [(b, kv) for b in range(wl.batch) for kv in range(wl.num_kv_heads)]
-    done = 0
+    wl = synth.get_workload(WORKLOAD)
+    params = _cpu_unit.params
+    S, L, G = wl.seq_len, wl.groups, wl.gqa
+    rng = np.random.default_rng([b, kv])
+    ck = rng.integers(0, 256, (S, L), dtype=np.uint8)
+    cv = rng.integers(0, 256, (S, L), dtype=np.uint8)
+    kn, vn = synth.cache_tokens(wl, 0, kv, b, 1, start=S - 1)
+    hp = oatt.head_params(params, kv)
+    q = _cpu_unit.q
     t0 = time.perf_counter()
-    elapsed = 0.0
-    while done < len(units) and (elapsed < budget_s or done == 0):
-        b, kv = units[done]
-        hp = oatt.head_params(params, kv)
-        ck = rng.integers(0, 256, (S, L), dtype=np.uint8)
-        cv = rng.integers(0, 256, (S, L), dtype=np.uint8)
-        kn, vn = synth.cache_tokens(wl, 0, kv, b, 1, start=S - 1)
+    nk_, _, nv_, _ = ocodec.encode_tokens(kn, vn, hp)
+    ck[-1], cv[-1] = nk_[0], nv_[0]
+    oatt.decode_rows(q[b, kv * G:(kv + 1) * G], ck, cv, hp, 1.0 / np.sqrt(wl.head_dim))
+    return time.perf_counter() - t0
+
+
+def _cpu_worker_init():
+    import synth
+    wl = synth.get_workload(WORKLOAD)
+    _cpu_unit.params = synth.bench_params(wl)
+    _cpu_unit.q = synth.decode_queries(wl, 0)
+
+
+def cpu_baseline(budget_s: float):
+    """The oracle on the host cores: one worker process per core, each with one
+    BLAS/OpenMP thread, over a bounded sample of the step's (sequence, KV head)
+    units; the step time is the sample's wall time scaled to all units."""
+    import multiprocessing as mp
+    import synth
+    wl = synth.get_workload(WORKLOAD)
+    units = [(b, kv) for b in range(wl.batch) for kv in range(wl.num_kv_heads)]
+    workers = max(1, min(len(units), os.cpu_count() or 1, 16))
+    for var in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS", "BLIS_NUM_THREADS"):
+        os.environ[var] = "1"
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(workers, initializer=_cpu_worker_init) as pool:
+        # one round of one unit per worker sizes the sample to the budget
+        t0 = time.perf_counter()
+        first = pool.map(_cpu_unit, units[:workers], chunksize=1)
+        round_s = time.perf_counter() - t0
+        rounds = int(max(0, min(len(units) // workers - 1, budget_s / max(round_s, 1e-3) - 1)))
+        rest = units[workers:workers * (1 + rounds)]
         t1 = time.perf_counter()
-        nk_, _, nv_, _ = ocodec.encode_tokens(kn, vn, hp)
-        ck[-1], cv[-1] = nk_[0], nv_[0]
-        oatt.decode_rows(q[b, kv * G:(kv + 1) * G], ck, cv, hp, scale)
-        elapsed += time.perf_counter() - t1
-        done += 1
-    per_unit = elapsed / done
-    step_s = per_unit * len(units)
+        more = pool.map(_cpu_unit, rest, chunksize=1) if rest else []
+        wall = time.perf_counter() - t1
+    done = len(first) + len(more)
+    # steady-state rate from the rounds after the first (which includes worker start-up)
+    if more:
+        rate = len(more) / wall
+    else:
+        rate = len(first) / round_s
+    step_s = len(units) / rate
     code_bytes = wl.code_bytes_per_step()
     return {
         "value": round(code_bytes / step_s / 1e9, 4),
         "unit": "GB/s",
         "us_per_step": round(step_s * 1e6, 1),
-        "cores": int(threads),
+        "cores": workers,
         "host_cpus": os.cpu_count(),
         "kind": "oracle",
-        "sample": f"{done} of {len(units)} (sequence, KV head) units: encode 1 token + plain-form "
-                  f"fp64 decode of {G} heads over {S} tokens each; step time = mean unit time x "
-                  f"{len(units)}",
-        "wall_s": round(time.perf_counter() - t0, 2),
+        "sample": f"{done} of {len(units)} (sequence, KV head) units of the step, {workers} worker processes "
+                  f"with one BLAS/OpenMP thread each: encode of the new token + plain-form fp64 decode of "
+                  f"{wl.gqa} heads over {wl.seq_len} tokens per unit; step time = all {len(units)} units at "
+                  f"the sample's unit rate",
+        "unit_compute_s_mean": round(float(np.mean(first + more)), 4),
     }
 
 
-def other_workloads(nk, torch, dev, calls: int):
-    """Decode-kernel time of every other workload shape (one line each).
+# ------------------------------------------------------------------ GPU timing
 
-    Pools hold uniformly random codes (and, in the key-scale format, random
-    bf16 scales); shapes too small to exceed the 256 MB last-level cache are
-    measured as they would run (cache-resident)."""
+def timed_calls(torch, fn, n: int):
+    """Per-call GPU times (us) of n calls: an event before each call and one after
+    the last, on the stream the calls launch on (torch's current stream)."""
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+    torch.cuda.synchronize()
+    for i in range(n):
+        ev[i].record()
+        fn(i)
+    ev[n].record()
+    torch.cuda.synchronize()
+    return np.array([ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(n)])
+
+
+def back_to_back_us(torch, fn, n: int) -> float:
+    """Mean GPU time per call of n back-to-back calls (events around all of them)."""
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for i in range(n):
+        fn(i)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / n
+
+
+def pct(x):
+    return {"p10": round(float(np.percentile(x, 10)), 2), "p50": round(float(np.percentile(x, 50)), 2),
+            "p90": round(float(np.percentile(x, 90)), 2), "calls": int(len(x))}
+
+
+def case_label(name, layer, key_scale, band_sizes, fp8, sq, wl):
+    return (f"{name}" + (f" layer {layer} (window {wl.windows[layer]})" if wl.num_layers > 1 else "")
+            + (" key-scale format" if key_scale else "")
+            + (f" band {band_sizes[0]}+{band_sizes[1]}" if band_sizes else "")
+            + (" fp8 codebooks" if fp8 else "")
+            + (" scalar value arm" if sq else ""))
+
+
+def other_workload(nk, torch, dev, case, calls: int):
+    """Decode-kernel time of one workload shape (uniformly random codes; in the
+    key-scale format random bf16 scales), pools rotated over copies."""
     import synth
-    res = []
-    # (workload, layer, key-scale format, sink-plus-recent band (n_sink, n_rec) or None,
-    #  fp8 codebooks, scalar value arm)
-    cases = [("single_head", 0, False, None, False, False), ("sweep_b64_s32k", 0, False, None, False, False),
-             ("sweep_b1_s128k", 0, False, None, False, False), ("gptoss_pair", 0, False, None, False, False),
-             ("gptoss_pair", 1, False, None, False, False), ("append_paged", 0, False, None, False, False),
-             ("qwen3_8b", 0, True, None, False, False), ("gptoss_pair", 1, True, None, False, False),
-             ("qwen3_8b", 0, False, (64, 256), False, False), ("gptoss_pair", 1, False, (64, 256), False, False),
-             ("qwen3_8b", 0, False, None, True, False), ("gptoss_pair", 1, False, None, True, False),
-             ("qwen3_8b", 0, False, None, False, True)]
-    for name, layer, key_scale, band_sizes, fp8, sq in cases:
-        wl = synth.get_workload(name)
-        B, S, H, Hq, D, L = wl.batch, wl.seq_len, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.groups
-        gen = torch.Generator(device=dev)
-        gen.manual_seed(7)
-        arrays = synth.bench_params(wl, layer)
-        if fp8:  # the same codebooks rounded to fp8 E4M3 (torch's conversion), as bytes
-            for k in ("cb_k", "cb_v"):
-                arrays[k] = torch.as_tensor(arrays[k]).to(torch.float32).to(torch.float8_e4m3fn).view(torch.uint8)
-        P = nk.NovaKVParams.from_arrays(arrays, device=dev, key_scale=key_scale, sq_values=sq)
-        if wl.block_size:
-            bps = S // wl.block_size
-            layout = nk.CacheLayout(wl.block_size, bps, torch.as_tensor(synth.shuffled_block_table(wl)).to(dev))
-            shape = (B * bps, H, wl.block_size, L)
-        else:
-            layout = nk.CacheLayout.contiguous(S)
-            shape = (B, H, S, L)
-        scale_bytes = 2 * int(np.prod(shape[:3])) if key_scale else 0
-        pool_bytes = 2 * int(np.prod(shape)) + scale_bytes
-        copies = int(min(6, max(1, -(-(600 << 20) // pool_bytes)))) if pool_bytes > (64 << 20) else 1
-        pools = [(torch.randint(0, 256, shape, dtype=torch.uint8, device=dev, generator=gen),
-                  torch.randint(0, 256, shape, dtype=torch.uint8, device=dev, generator=gen),
-                  (torch.rand(shape[:3], generator=gen, device=dev) + 0.5).to(torch.bfloat16)
-                  if key_scale else None,
-                  torch.randn(shape[:3] + (2,), generator=gen, device=dev).to(torch.bfloat16) if sq else None)
-                 for _ in range(copies)]
-        q = torch.randn((B, Hq, D), generator=gen, device=dev).to(torch.bfloat16)
-        seq = torch.full((B,), S, dtype=torch.int32, device=dev)
-        sinks = torch.as_tensor(synth.sink_logits(wl, layer), dtype=torch.float32).to(dev) if wl.sinks else None
-        out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
-        ws = torch.zeros(nk.decode_workspace_bytes(P, B, Hq, S), dtype=torch.uint8, device=dev)
-        window = wl.windows[layer]
-        band = None
-        if band_sizes:
-            bshape = nk.band_shape(P, B, *band_sizes)
-            band = nk.Band(*band_sizes, torch.randn(bshape, generator=gen, device=dev).to(torch.bfloat16),
-                           torch.randn(bshape, generator=gen, device=dev).to(torch.bfloat16))
-        calls_ = [nk.prepare_decode(P, layout, q, pk, pv, seq, S, out, ws, window=window, sinks=sinks,
-                                    k_scales=ps, band=band, v_sq=pq)
-                  for pk, pv, ps, pq in pools]
-        for i in range(5):
-            calls_[i % copies]()
-        torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for i in range(calls):
-            calls_[i % copies]()
-        e1.record()
-        torch.cuda.synchronize()
-        us = e0.elapsed_time(e1) * 1e3 / calls
-        cb = wl.code_bytes_per_step(layer)
-        bb = 0
-        if band_sizes:  # the band's tokens are read as bf16 rows instead of codes
-            nband = min(sum(band_sizes), S)
-            cb -= 2 * B * H * nband * L
-            bb = 2 * B * H * nband * D * 2
-        # the key scales of the tokens read from codes: 2 bytes per token and KV
-        # head; the value scale and offset: 4 more
-        sb = (cb // L if key_scale else 0) + (2 * cb // L if sq else 0)
-        res.append({"workload": f"{name}" + (f" layer {layer} (window {window})" if wl.num_layers > 1 else "")
-                    + (" key-scale format" if key_scale else "")
-                    + (f" band {band_sizes[0]}+{band_sizes[1]}" if band_sizes else "")
-                    + (" fp8 codebooks" if fp8 else "")
-                    + (" scalar value arm" if sq else ""),
-                    "batch": B, "seq_len": S, "q_heads": Hq, "kv_heads": H, "head_dim": D,
-                    "paged_block": wl.block_size or None, "code_bytes": cb, "scale_bytes": sb,
-                    "band_bytes": bb, "pool_copies": copies,
-                    "decode_us": round(us, 2), "GB_per_s": round((cb + sb + bb) / (us * 1e-6) / 1e9, 1),
-                    "frac_of_hbm_peak": round((cb + sb + bb) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)})
-        del pools, calls_, ws, band
-        torch.cuda.empty_cache()
+    name, layer, key_scale, band_sizes, fp8, sq = case
+    wl = synth.get_workload(name)
+    B, S, H, Hq, D, L = wl.batch, wl.seq_len, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.groups
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(7)
+    arrays = synth.bench_params(wl, layer)
+    if fp8:  # the same codebooks rounded to fp8 E4M3 (torch's conversion), as bytes
+        for k in ("cb_k", "cb_v"):
+            arrays[k] = torch.as_tensor(arrays[k]).to(torch.float32).to(torch.float8_e4m3fn).view(torch.uint8)
+    P = nk.NovaKVParams.from_arrays(arrays, device=dev, key_scale=key_scale, sq_values=sq)
+    if wl.block_size:
+        bps = S // wl.block_size
+        layout = nk.CacheLayout(wl.block_size, bps, torch.as_tensor(synth.shuffled_block_table(wl)).to(dev))
+        shape = (B * bps, H, wl.block_size, L)
+    else:
+        layout = nk.CacheLayout.contiguous(S)
+        shape = (B, H, S, L)
+    scale_bytes = 2 * int(np.prod(shape[:3])) if key_scale else 0
+    sq_bytes = 4 * int(np.prod(shape[:3])) if sq else 0
+    pool_bytes = 2 * int(np.prod(shape)) + scale_bytes + sq_bytes
+    copies = rotation_copies(pool_bytes)
+    pools = [(torch.randint(0, 256, shape, dtype=torch.uint8, device=dev, generator=gen),
+              torch.randint(0, 256, shape, dtype=torch.uint8, device=dev, generator=gen),
+              (torch.rand(shape[:3], generator=gen, device=dev) + 0.5).to(torch.bfloat16)
+              if key_scale else None,
+              torch.randn(shape[:3] + (2,), generator=gen, device=dev).to(torch.bfloat16) if sq else None)
+             for _ in range(copies)]
+    q = torch.randn((B, Hq, D), generator=gen, device=dev).to(torch.bfloat16)
+    seq = torch.full((B,), S, dtype=torch.int32, device=dev)
+    sinks = torch.as_tensor(synth.sink_logits(wl, layer), dtype=torch.float32).to(dev) if wl.sinks else None
+    out = torch.empty((B, Hq, D), dtype=torch.float32, device=dev)
+    ws = torch.zeros(nk.decode_workspace_bytes(P, B, Hq, S), dtype=torch.uint8, device=dev)
+    window = wl.windows[layer]
+    band, band_copies = None, 1
+    bands = [None]
+    if band_sizes:
+        bshape = nk.band_shape(P, B, *band_sizes)
+        band_bytes_all = 2 * 2 * int(np.prod(bshape))
+        band_copies = max(1, min(copies, rotation_copies(band_bytes_all)))
+        bands = [nk.Band(*band_sizes, torch.randn(bshape, generator=gen, device=dev).to(torch.bfloat16),
+                         torch.randn(bshape, generator=gen, device=dev).to(torch.bfloat16))
+                 for _ in range(band_copies)]
+    calls_ = [nk.prepare_decode(P, layout, q, pk, pv, seq, S, out, ws, window=window, sinks=sinks,
+                                k_scales=ps, band=bands[i % len(bands)], v_sq=pq)
+              for i, (pk, pv, ps, pq) in enumerate(pools)]
+    fn = lambda i: calls_[i % copies]()  # noqa: E731
+    for i in range(20):
+        fn(i)
+    us = back_to_back_us(torch, fn, calls)
+    per_call = timed_calls(torch, fn, calls)
+    cb = wl.code_bytes_per_step(layer)
+    bb = 0
+    if band_sizes:  # the band's tokens are read as bf16 rows instead of codes
+        nband = min(sum(band_sizes), S)
+        cb -= 2 * B * H * nband * L
+        bb = 2 * B * H * nband * D * 2
+    # the key scales of the tokens read from codes: 2 bytes per token and KV
+    # head; the value scale and offset: 4 more
+    sb = (cb // L if key_scale else 0) + (2 * cb // L if sq else 0)
+    res = {"workload": case_label(name, layer, key_scale, band_sizes, fp8, sq, wl),
+           "batch": B, "seq_len": S, "q_heads": Hq, "kv_heads": H, "head_dim": D,
+           "paged_block": wl.block_size or None, "code_bytes": cb, "scale_bytes": sb,
+           "band_bytes": bb, "pool_copies": copies, "pool_bytes_rotated": pool_bytes * copies,
+           "band_copies": band_copies if band_sizes else None,
+           "decode_us": round(us, 2), "per_call_us": pct(per_call),
+           "GB_per_s": round((cb + sb + bb) / (us * 1e-6) / 1e9, 1),
+           "frac_of_hbm_peak": round((cb + sb + bb) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    del pools, calls_, ws, bands
+    torch.cuda.empty_cache()
     return res
+
+
+def append_encode(nk, torch, dev, P, gen):
+    """Prefill-encode of 4096 new tokens x 32 sequences x 8 KV heads into a paged
+    cache of 16-token blocks with a shuffled block table."""
+    import synth
+    awl = synth.get_workload("append_paged")
+    H, D, L = awl.num_kv_heads, awl.head_dim, awl.groups
+    kk = torch.randn((awl.batch, awl.n_new, H, D), generator=gen, device=dev).to(torch.bfloat16)
+    vv = torch.randn((awl.batch, awl.n_new, H, D), generator=gen, device=dev).to(torch.bfloat16)
+    bps = awl.seq_len // awl.block_size
+    table = torch.as_tensor(synth.shuffled_block_table(awl)).to(dev)
+    alay = nk.CacheLayout(awl.block_size, bps, table)
+    apk = torch.zeros((awl.batch * bps, H, awl.block_size, L), dtype=torch.uint8, device=dev)
+    apv = torch.zeros_like(apk)
+    sp = torch.full((awl.batch,), awl.seq_len - awl.n_new, dtype=torch.int32, device=dev)
+    call = nk.prepare_encode(P, alay, kk, vv, sp, apk, apv)
+    call()
+    per_call = timed_calls(torch, lambda i: call(), 10)
+    a_ms = float(np.median(per_call)) * 1e-3
+    th = awl.batch * awl.n_new * H
+    flops = th * ENCODE_FLOPS_PER_TOKEN_HEAD
+    tflops = flops / (a_ms * 1e-3) / 1e12
+    return {"workload": "append 4096 tokens x 32 sequences, 8 KV heads, D=128, paged 16-token blocks",
+            "ms": round(a_ms, 3), "per_call_us": pct(per_call),
+            "token_heads_per_s": round(th / (a_ms * 1e-3), 1),
+            "roofline": {"bound": "mfma", "dtype": "f64", "achieved": round(tflops, 2),
+                         "peak": FP64_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tflops / FP64_MFMA_PEAK_TFLOPS, 4),
+                         "algorithmic_flops": flops,
+                         "flops_per_token_head": ENCODE_FLOPS_PER_TOKEN_HEAD}}
 
 
 def main():
@@ -232,6 +347,13 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    # the oracle on the host cores first, before anything touches the GPU
+    cpu = None
+    if not args.no_cpu_baseline and args.only is None:
+        cpu = cpu_baseline(args.cpu_seconds)
+        print(f"[bench] cpu baseline done: {cpu['us_per_step']} us per step on {cpu['cores']} cores",
+              file=sys.stderr, flush=True)
+
     import torch
 
     import paper_2608_04074_amd as nk
@@ -242,17 +364,42 @@ def main():
     torch.cuda.set_device(dev)
     B, S, H, Hq, D, L = wl.batch, wl.seq_len, wl.num_kv_heads, wl.num_q_heads, wl.head_dim, wl.groups
     code_bytes = wl.code_bytes_per_step()
-
-    params = synth.bench_params(wl)
-    P = nk.NovaKVParams.from_arrays(params, device=dev)
-    layout = nk.CacheLayout.contiguous(S)
     gen = torch.Generator(device=dev)
     gen.manual_seed(1234)
-    pools = []
-    for _ in range(COPIES):
-        pk = torch.randint(0, 256, (B, H, S, L), dtype=torch.uint8, device=dev, generator=gen)
-        pv = torch.randint(0, 256, (B, H, S, L), dtype=torch.uint8, device=dev, generator=gen)
-        pools.append((pk, pv))
+    params = synth.bench_params(wl)
+    P = nk.NovaKVParams.from_arrays(params, device=dev)
+
+    if args.only is not None:
+        if args.only == "append_encode":
+            line = append_encode(nk, torch, dev, P, gen)
+        else:
+            import synth as _s
+            case = next((c for c in OTHER_CASES
+                         if case_label(*c, _s.get_workload(c[0])).startswith(args.only)), None)
+            if case is None:
+                print(f"no workload line starts with {args.only!r}", file=sys.stderr)
+                sys.exit(2)
+            line = other_workload(nk, torch, dev, case, args.calls)
+        if args.copy_calib:
+            copy_calibration(torch, dev)
+        print(json.dumps({"only": args.only, "line": line}), flush=True)
+        return
+
+    # the other workload shapes and the append encoder (reported beside the headline)
+    others = None
+    if not args.skip_others:
+        others = []
+        for case in OTHER_CASES:
+            others.append(other_workload(nk, torch, dev, case, args.calls))
+            print(f"[bench] {others[-1]['workload']}: {others[-1]['decode_us']} us", file=sys.stderr, flush=True)
+    append = None if args.skip_append else append_encode(nk, torch, dev, P, gen)
+
+    # ---- the headline step
+    layout = nk.CacheLayout.contiguous(S)
+    copies = rotation_copies(2 * B * H * S * L, at_least=6)
+    pools = [(torch.randint(0, 256, (B, H, S, L), dtype=torch.uint8, device=dev, generator=gen),
+              torch.randint(0, 256, (B, H, S, L), dtype=torch.uint8, device=dev, generator=gen))
+             for _ in range(copies)]
     q = torch.as_tensor(synth.decode_queries(wl, 0)).to(torch.bfloat16).to(dev)
     k_new = torch.randn((B, 1, H, D), generator=gen, device=dev).to(torch.bfloat16)
     v_new = torch.randn((B, 1, H, D), generator=gen, device=dev).to(torch.bfloat16)
@@ -268,40 +415,34 @@ def main():
                   for pk, pv in pools]
 
     def step(i):
-        step_calls[i % COPIES]()
+        step_calls[i % copies]()
 
     def two_call_step(i):
-        enc_calls[i % COPIES]()
-        dec_calls[i % COPIES]()
+        enc_calls[i % copies]()
+        dec_calls[i % copies]()
 
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
+    # the timed region: exactly `steps` steps, synchronized on both sides
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record()
+    for i in range(args.steps):
+        step(i)
+    e1.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_step = e0.elapsed_time(e1) / args.steps
 
-    def timed(fn, n):
-        """Mean GPU time per call of n back-to-back calls, events on the current
-        stream (the stream the calls launch on)."""
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        e0.record()
-        for i in range(n):
-            fn(i)
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / n
-
-    # whole step (append the new token and decode attention, one launch): the headline
-    ms_step = timed(step, args.steps) * 1e-3
-    step_runs = [timed(step, args.steps) for _ in range(5)]
-    two_call_us = timed(two_call_step, args.steps)
-    # each kernel alone, back to back, for the roofline of the dominant kernel
-    n_runs = 5
-    dec_runs = [timed(lambda i: dec_calls[i % COPIES](), args.steps) for _ in range(n_runs)]
-    enc_runs = [timed(lambda i: enc_calls[i % COPIES](), args.steps) for _ in range(n_runs)]
-    dec_mean_us = float(np.mean(dec_runs))
-    dec_med_us = float(np.median(dec_runs))
-    enc_us = np.array(enc_runs)
+    # beside the timed region: per-call distributions and the parts of the step
+    n_pc = max(200, args.steps)
+    step_pc = timed_calls(torch, step, n_pc)
+    two_call_us = back_to_back_us(torch, two_call_step, n_pc)
+    dec_us = back_to_back_us(torch, lambda i: dec_calls[i % copies](), n_pc)
+    dec_pc = timed_calls(torch, lambda i: dec_calls[i % copies](), n_pc)
+    enc_us = back_to_back_us(torch, lambda i: enc_calls[i % copies](), n_pc)
     # the same step with the codebooks in the paper's stored format: rounded to
     # fp8 E4M3 (torch's conversion) and passed as bytes
     p8 = dict(params)
@@ -310,56 +451,15 @@ def main():
     P8 = nk.NovaKVParams.from_arrays(p8, device=dev)
     step8_calls = [nk.prepare_append_decode(P8, layout, k_new[:, 0], v_new[:, 0], q, pk, pv, seq_lens, S, out, ws)
                    for pk, pv in pools]
-    for i in range(200):
-        step8_calls[i % COPIES]()
-    step8_runs = [timed(lambda i: step8_calls[i % COPIES](), args.steps) for _ in range(n_runs)]
-
-    value = code_bytes / (ms_step * 1e-3) / 1e9
-    step_mean_us = float(np.mean(step_runs))
-    achieved = code_bytes / (step_mean_us * 1e-6) / 1e9
-
-    # Append throughput (prefill-encode of 4096 tokens x 32 sequences x 8 KV heads), reported aside.
-    append = None
-    if not args.skip_append:
-        awl = synth.get_workload("append_paged")
-        kk = torch.randn((awl.batch, awl.n_new, H, D), generator=gen, device=dev).to(torch.bfloat16)
-        vv = torch.randn((awl.batch, awl.n_new, H, D), generator=gen, device=dev).to(torch.bfloat16)
-        bps = awl.seq_len // awl.block_size
-        table = torch.as_tensor(synth.shuffled_block_table(awl)).to(dev)
-        alay = nk.CacheLayout(awl.block_size, bps, table)
-        apk = torch.zeros((awl.batch * bps, H, awl.block_size, L), dtype=torch.uint8, device=dev)
-        apv = torch.zeros_like(apk)
-        sp = torch.full((awl.batch,), awl.seq_len - awl.n_new, dtype=torch.int32, device=dev)
-        nk.encode(P, alay, kk, vv, sp, apk, apv)
-        torch.cuda.synchronize()
-        reps = 3
-        a0 = torch.cuda.Event(enable_timing=True)
-        a1 = torch.cuda.Event(enable_timing=True)
-        a0.record()
-        for _ in range(reps):
-            nk.encode(P, alay, kk, vv, sp, apk, apv)
-        a1.record()
-        torch.cuda.synchronize()
-        a_ms = a0.elapsed_time(a1) / reps
-        th = awl.batch * awl.n_new * H
-        append = {"workload": "append 4096 tokens x 32 sequences, 8 KV heads, D=128, paged 16-token blocks",
-                  "ms": round(a_ms, 3), "token_heads_per_s": round(th / (a_ms * 1e-3), 1)}
-
-    others = None if args.skip_others else other_workloads(nk, torch, dev, 50)
+    for i in range(50):
+        step8_calls[i % copies]()
+    step8_us = back_to_back_us(torch, lambda i: step8_calls[i % copies](), n_pc)
 
     if args.copy_calib:  # plain copy of known size, last dispatch of the run
-        src = torch.empty(COPY_CALIB_BYTES, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        src.fill_(1)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
+        copy_calibration(torch, dev)
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(wl, args.cpu_seconds)
+    value = code_bytes / (ms_step * 1e-3) / 1e9
     traffic = measured_traffic()
-
     rec = {
         "metric": "VQ-KV decode attention effective compressed-KV bandwidth (K+V code bytes / step time), S=16K",
         "value": round(value, 2),
@@ -373,45 +473,49 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f16-mfma-f32acc",
         "data": "synthetic",
         "config": {
             "workload": "qwen3_8b-shaped GQA decode layer over a 2-bit VQ K/V cache: encode 1 new token "
                         "per sequence + decode attention, one launch",
             "batch": B, "seq_len": S, "q_heads": Hq, "kv_heads": H, "head_dim": D,
-            "code_bytes_per_step": code_bytes, "pool_copies": COPIES,
+            "code_bytes_per_step": code_bytes, "pool_copies": copies,
             "params": "random orthogonal transforms, fp16 N(0,1) codebooks, uniform random codes",
+            "arithmetic": "fp16 table entries and probabilities on MFMA with fp32 accumulation; fp32 softmax, "
+                          "query transform and combine; fp64 encoder",
         },
-        "step_kernel_us": {"mean": round(step_mean_us, 2),
-                           "median_of_runs": round(float(np.median(step_runs)), 2),
-                           "min_of_runs": round(float(np.min(step_runs)), 2),
-                           "max_of_runs": round(float(np.max(step_runs)), 2),
-                           "runs": len(step_runs), "calls_per_run": args.steps},
-        "step_fp8_codebooks_us": {"mean": round(float(np.mean(step8_runs)), 2),
-                                  "median_of_runs": round(float(np.median(step8_runs)), 2)},
+        "timed_region_wall_s": round(t_wall, 4),
+        "step_per_call_us": pct(step_pc),
+        "step_fp8_codebooks_us": round(step8_us, 2),
         "two_call_step_us": round(two_call_us, 2),
-        "decode_kernel_us": {"mean": round(dec_mean_us, 2), "median_of_runs": round(dec_med_us, 2),
-                             "min_of_runs": round(float(np.min(dec_runs)), 2),
-                             "max_of_runs": round(float(np.max(dec_runs)), 2),
-                             "runs": n_runs, "calls_per_run": args.steps},
-        "append_kernel_us": {"mean": round(float(np.mean(enc_us)), 2),
-                             "median_of_runs": round(float(np.median(enc_us)), 2)},
+        "decode_kernel_us": {"mean": round(dec_us, 2), **pct(dec_pc)},
+        "append_kernel_us": round(enc_us, 2),
         "roofline": {
             "kernel": f"{DECODE_KERNEL}<12, true, false, false, false> (the step's one launch: encode of the new token, query "
                       "transform, split pass, combine)",
             "bound": "hbm",
-            "achieved": round(achieved, 1),
+            "achieved": round(value, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "frac": round(value / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "algorithmic_bytes_per_launch": code_bytes,
+            "algorithmic_bytes_per_token_head": 2 * L,
         },
         "append_encode": append,
         "other_workloads_decode": others,
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
+
+
+def copy_calibration(torch, dev):
+    src = torch.empty(COPY_CALIB_BYTES, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
 
 
 if __name__ == "__main__":

@@ -32,7 +32,7 @@ __all__ = [
     "rng_for", "haar_orthogonal", "power_spectrum", "round_to_bf16", "to_storage",
     "head_bases", "calibration_set", "cache_tokens", "decode_queries",
     "sink_logits", "random_codes", "random_key_scales", "shuffled_block_table",
-    "uniform_seq_lens", "bench_params",
+    "uniform_seq_lens", "bench_params", "device_cache_tokens",
 ]
 
 ROLE = {
@@ -41,6 +41,7 @@ ROLE = {
     "cache_k": 6, "cache_v": 7, "query": 8, "sink": 9,
     "codes_k": 10, "codes_v": 11, "block_table": 12, "seq_lens": 13,
     "bench": 14, "new_k": 15, "new_v": 16, "scales_k": 17,
+    "device_cache": 18,
 }
 
 
@@ -218,6 +219,39 @@ def cache_tokens(wl: Workload, layer: int, kv_head: int, seq: int, n: int, start
         out_v[t - start:t - start + (b - a)] = vv[a:b]
         t = lo + b
     return to_storage(out_k, wl.dtype), to_storage(out_v, wl.dtype)
+
+
+def device_cache_tokens(wl: Workload, layer: int, seq: int, n: int, start: int, device):
+    """Keys and values of positions [start, start+n) of sequence ``seq`` for
+    every KV head, drawn on the device: two bf16 tensors [n][Hkv][D].
+
+    The same statistical model as ``cache_tokens`` (the unit's Haar basis and
+    power spectrum), with the Gaussian draws taken from torch's Philox
+    generator on ``device`` instead of NumPy, so that long histories of many
+    sequences are produced without host work.  The generator is seeded from
+    (config, layer, seq, start) only, so a call is reproducible; it is not
+    value-identical to ``cache_tokens``.  Draws and products are fp32, then
+    rounded once to bf16 (nearest even).
+    """
+    import torch
+
+    if wl.dtype != "bf16":
+        raise ValueError("device_cache_tokens stores bf16")
+    d, h = wl.head_dim, wl.num_kv_heads
+    seed = int(np.random.SeedSequence([wl.config_id, layer, seq, start, ROLE["device_cache"]])
+               .generate_state(1, dtype=np.uint64)[0] & 0x7FFFFFFFFFFFFFFF)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    outs = []
+    for side in (0, 1):
+        # scaled basis per head: x = z diag(sqrt(lam)) U^T, as one [H][D][D] fp32 operand
+        mats = np.stack([(np.sqrt(power_spectrum(d, wl.kv_alpha))[:, None] * head_bases(wl, layer, kv)[side].T)
+                         for kv in range(h)])
+        m = torch.as_tensor(mats, dtype=torch.float32).contiguous().to(device)
+        z = torch.randn((h, n, d), generator=gen, device=device, dtype=torch.float32)
+        x = torch.bmm(z, m)                                   # [H][n][D] fp32
+        outs.append(x.transpose(0, 1).contiguous().to(torch.bfloat16))
+    return outs[0], outs[1]
 
 
 def decode_queries(wl: Workload, layer: int, batch: Optional[int] = None) -> np.ndarray:

@@ -7,6 +7,16 @@ import numpy as np
 TOL = 2e-3          # max-abs error relative to the output row's L2 norm
 NEAR_TIE = 1e-6     # squared-distance gap under which a code mismatch is a near-tie
 
+# Parity report of the session: one entry per comparison, written by
+# conftest.py at the end of the session (codes compared, mismatches, near-ties,
+# near-tie mismatches; output rows compared and the worst row error).
+REPORT = []
+CURRENT_TEST = {"id": ""}
+
+
+def _record(kind, what, **fields):
+    REPORT.append({"test": CURRENT_TEST["id"], "kind": kind, "what": what, **fields})
+
 
 def pool_offsets(b, kv, t, *, hkv, groups, block_size, blocks_per_seq, table=None):
     """Byte offsets of the code rows of tokens t (array) of sequence b, KV head kv."""
@@ -42,6 +52,7 @@ def assert_outputs_close(gpu, ref, tol=TOL, what=""):
     err = row_errors(np.asarray(gpu, dtype=np.float64), np.asarray(ref, dtype=np.float64))
     worst = float(err.max()) if err.size else 0.0
     print(f"[parity] {what} rows={err.size} worst_rel_err={worst:.3e} tol={tol}", flush=True)
+    _record("output", what, rows=int(err.size), worst_rel_err=worst, tol=tol, ok=bool(worst <= tol))
     assert worst <= tol, f"{what}: worst relative row error {worst:.3e} > {tol}"
     return worst
 
@@ -55,5 +66,7 @@ def compare_codes(gpu_codes, ref_codes, ref_gap, what=""):
     n_near = int(near.sum())
     print(f"[parity] {what} codes={gpu_codes.size} mismatches={int(mism.sum())} "
           f"near_ties={n_near} near_tie_mismatches={int((mism & near).sum())}", flush=True)
+    _record("codes", what, codes=int(gpu_codes.size), mismatches=int(mism.sum()), near_ties=n_near,
+            near_tie_mismatches=int((mism & near).sum()), ok=not bool(bad.any()))
     assert not bad.any(), f"{what}: {int(bad.sum())} code mismatches outside near-ties"
     return int(mism.sum()), n_near

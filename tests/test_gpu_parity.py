@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import synth
-from helpers import assert_outputs_close, compare_codes, read_rows, write_rows
+from helpers import assert_outputs_close, compare_codes, pool_offsets, read_rows, write_rows
 from oracle import attention as oatt
 from oracle import codec as ocodec
 from oracle_cache import calibrated_params
@@ -559,36 +559,126 @@ def test_gptoss_pair_decode(nk, layer):
                  window=wl.windows[layer])
 
 
-def test_qwen3_8b_full_encode_sampled(nk):
-    """Full-size GPU encode of B=8 x 8 KV heads x 16384 tokens; oracle re-encodes sampled units."""
+def _device_tokens(wl, batch, n, start):
+    """Seeded device-side keys and values [B][n][Hkv][D] (bf16) of every sequence."""
+    kk = torch.empty((batch, n, wl.num_kv_heads, wl.head_dim), dtype=torch.bfloat16, device="cuda")
+    vv = torch.empty_like(kk)
+    for b in range(batch):
+        kk[b], vv[b] = synth.device_cache_tokens(wl, 0, b, n, start, "cuda")
+    return kk, vv
+
+
+def _pool_rows(pool_host, b_list, kv, start, n, *, hkv, groups, block_size, blocks_per_seq, table=None):
+    """Code rows of positions [start, start+n) of sequences b_list, KV head kv, stacked."""
+    offs = np.concatenate([pool_offsets(b, kv, np.arange(start, start + n), hkv=hkv, groups=groups,
+                                        block_size=block_size, blocks_per_seq=blocks_per_seq, table=table)
+                           for b in b_list])
+    return pool_host[offs[:, None] + np.arange(groups)[None, :]]
+
+
+def _check_all_codes(params, kk, vv, pk_host, pv_host, start, lay, what):
+    """Every code of the tokens kk, vv [B][n][Hkv][D] against the oracle, one KV head at a time.
+
+    Returns the oracle's codes {kv: (ck [B*n][L], cv)} (sequence-major rows)."""
+    B, n, H, D = kk.shape
+    L = D // 4
+    kh = kk.float().cpu().numpy()
+    vh = vv.float().cpu().numpy()
+    codes = {}
+    for kv in range(H):
+        K = kh[:, :, kv].reshape(-1, D).astype(np.float64)
+        V = vh[:, :, kv].reshape(-1, D).astype(np.float64)
+        ck, gk, cv, gv = ocodec.encode_tokens(K, V, oatt.head_params(params, kv))
+        compare_codes(_pool_rows(pk_host, range(B), kv, start, n, groups=L, **lay), ck, gk,
+                      f"{what} kv{kv} K ({B} sequences x {n})")
+        compare_codes(_pool_rows(pv_host, range(B), kv, start, n, groups=L, **lay), cv, gv,
+                      f"{what} kv{kv} V ({B} sequences x {n})")
+        codes[kv] = (ck, cv)
+    return codes
+
+
+def test_qwen3_8b_full_encode(nk):
+    """Full-size GPU encode of B=8 x 8 KV heads x 16384 tokens (one bulk call); every code against the oracle."""
     wl = synth.get_workload("qwen3_8b")
     params = calibrated_params(wl, 0)
     P = upload_params(nk, params)
-    B, S, H, L, D = wl.batch, wl.seq_len, wl.num_kv_heads, wl.groups, wl.head_dim
+    B, S, H, L = wl.batch, wl.seq_len, wl.num_kv_heads, wl.groups
+    kk, vv = _device_tokens(wl, B, S, 0)
     pk = torch.zeros((B, H, S, L), dtype=torch.uint8, device="cuda")
     pv = torch.zeros_like(pk)
-    sample = [(0, 0), (5, 3), (7, 7)]
-    kept = {}
-    for b in range(B):
-        kk = np.empty((S, H, D))
-        vv = np.empty_like(kk)
-        for kv in range(H):
-            kk[:, kv], vv[:, kv] = synth.cache_tokens(wl, 0, kv, b, S)
-            if (b, kv) in sample:
-                kept[(b, kv)] = (kk[:, kv].copy(), vv[:, kv].copy())
-        # one sequence at a time: start_pos is per sequence, so encode the row's slice of the pool
-        say(f"qwen3_8b encode sequence {b}")
-        nk.encode(P, nk.CacheLayout.contiguous(S), dev(kk[None], torch.bfloat16),
-                  dev(vv[None], torch.bfloat16), dev([0], torch.int32), pk[b:b + 1], pv[b:b + 1])
+    say("qwen3_8b full encode")
+    nk.encode(P, nk.CacheLayout.contiguous(S), kk, vv, torch.zeros(B, dtype=torch.int32, device="cuda"), pk, pv)
     torch.cuda.synchronize()
-    for (b, kv), (kk, vv) in kept.items():
-        ck, gk, cv, gv = ocodec.encode_tokens(kk, vv, oatt.head_params(params, kv))
-        compare_codes(pk[b, kv].cpu().numpy(), ck, gk, f"qwen3_8b b{b} kv{kv} K")
-        compare_codes(pv[b, kv].cpu().numpy(), cv, gv, f"qwen3_8b b{b} kv{kv} V")
+    _check_all_codes(params, kk, vv, pk.cpu().numpy().reshape(-1), pv.cpu().numpy().reshape(-1), 0,
+                     lay_kwargs(H, S, 1), "qwen3_8b encode")
 
 
+@pytest.mark.parametrize("lens", ["full", "ragged"])
+def test_step_at_qwen3_8b_bench_shape(nk, lens):
+    """The benchmarked call at its shape: nova_kv_append_decode_attn at B=8, S=16384,
+    32 q / 8 KV heads (one launch, four splits per (sequence, KV head), the new
+    token's encode shared by them).  The appended codes of all 64 units are
+    checked bit-exact, every other row of the pools unchanged, and 8 sampled
+    (sequence, KV head) units' outputs against the oracle over the history
+    codes and the oracle's own codes of the new token.  "ragged" gives the
+    sequences lengths from 16384 down to 1 at the same max_seq_len, so the
+    new token's items fall to 1..4 splits."""
+    wl = synth.get_workload("qwen3_8b")
+    params = calibrated_params(wl, 0)
+    P = upload_params(nk, params)
+    B, S, H, L, G, D = wl.batch, wl.seq_len, wl.num_kv_heads, wl.groups, wl.gqa, wl.head_dim
+    seq = np.full(B, S, dtype=np.int32) if lens == "full" else \
+        np.array([16384, 16000, 12289, 8193, 4097, 4096, 100, 1], dtype=np.int32)
+    ck, cv, kn, vn = _step_inputs(wl, B, S, seq)
+    q = synth.decode_queries(wl, 0)
+    pk, pv = dev(ck, torch.uint8), dev(cv, torch.uint8)
+    before_k, before_v = pk.clone(), pv.clone()
+    say(f"bench-shape step lens={lens}")
+    out = nk.append_decode_attn(P, nk.CacheLayout.contiguous(S), dev(kn, torch.bfloat16), dev(vn, torch.bfloat16),
+                                dev(q, torch.bfloat16), pk, pv, dev(seq, torch.int32), S)
+    torch.cuda.synchronize()
+    # every row but the new token's unchanged
+    mask = torch.ones((B, 1, S, 1), dtype=torch.bool, device="cuda")
+    for b in range(B):
+        mask[b, 0, seq[b] - 1] = False
+    assert torch.equal(pk.masked_select(mask.expand_as(pk)), before_k.masked_select(mask.expand_as(pk)))
+    assert torch.equal(pv.masked_select(mask.expand_as(pv)), before_v.masked_select(mask.expand_as(pv)))
+    hk, hv = pk.cpu().numpy(), pv.cpu().numpy()
+    ref_k, ref_v = ck.copy(), cv.copy()
+    new_k, new_v, gap_k, gap_v = [], [], [], []
+    for b in range(B):
+        p = int(seq[b]) - 1
+        for kv in range(H):
+            okk, ogk, ovv, ogv = ocodec.encode_tokens(kn[b, kv][None], vn[b, kv][None], oatt.head_params(params, kv))
+            new_k.append((hk[b, kv, p], okk[0], ogk[0]))
+            new_v.append((hv[b, kv, p], ovv[0], ogv[0]))
+            ref_k[b, kv, p], ref_v[b, kv, p] = okk[0], ovv[0]
+    for side, rows in (("K", new_k), ("V", new_v)):
+        compare_codes(np.stack([r[0] for r in rows]), np.stack([r[1] for r in rows]), np.stack([r[2] for r in rows]),
+                      f"bench-shape step lens={lens} new token {side} (64 units)")
+    out = out.cpu().numpy()
+    scale = 1 / np.sqrt(D)
+    units = [(0, 0), (1, 3), (2, 6), (3, 1), (4, 4), (5, 7), (6, 2), (7, 5)]
+    gots, refs = [], []
+    for b, kv in units:
+        hp = oatt.head_params(params, kv)
+        n = int(seq[b])
+        refs.append(oatt.decode_rows(q[b, kv * G:(kv + 1) * G], ref_k[b, kv, :n], ref_v[b, kv, :n], hp, scale))
+        gots.append(out[b, kv * G:(kv + 1) * G])
+    assert_outputs_close(np.concatenate(gots), np.concatenate(refs), what=f"bench-shape step lens={lens}")
+    assert np.isfinite(out).all()
+
+
+@pytest.mark.timeout(900)
 def test_append_paged_then_decode(nk):
-    """32 sequences append 4096 tokens into a shuffled 16-token-block pool, then decode at 32768."""
+    """The append workload as specified: 32 sequences of a paged cache (16-token
+    blocks, shuffled block table) hold a 28,672-token history encoded by the
+    same GPU encoder (untimed set-up), then 4096 new tokens per sequence are
+    appended in one call and one decode step reads all 32,768 positions.
+    Every appended code of all 256 (sequence, KV head) units is checked
+    bit-exact; for sampled units the history codes are checked too and the
+    decode output is compared with the oracle's decode over its own codes.
+    Inputs come from the seeded device-side generator."""
     wl = synth.get_workload("append_paged")
     params = calibrated_params(synth.get_workload("qwen3_8b"), 0)
     P = upload_params(nk, params)
@@ -598,49 +688,38 @@ def test_append_paged_then_decode(nk):
     start = S - wl.n_new
     table = synth.shuffled_block_table(wl)
     lk = lay_kwargs(H, bs, bps, table)
-    # history: stand-in codes written through the block table
-    hist_k, hist_v = _random_pools(wl, 0, B, start, H, L)
-    flat_k = np.zeros(B * bps * H * bs * L, dtype=np.uint8)
-    flat_v = np.zeros_like(flat_k)
-    for b in range(B):
-        for kv in range(H):
-            write_rows(flat_k, hist_k[b, kv], b, kv, 0, **lk)
-            write_rows(flat_v, hist_v[b, kv], b, kv, 0, **lk)
-    pk = dev(flat_k, torch.uint8)
-    pv = dev(flat_v, torch.uint8)
     lay = nk.CacheLayout(bs, bps, dev(table, torch.int32))
-    kk = np.empty((B, wl.n_new, H, D))
-    vv = np.empty_like(kk)
-    for b in range(B):
-        for kv in range(H):
-            kk[b, :, kv], vv[b, :, kv] = synth.cache_tokens(wl, 0, kv, b, wl.n_new, start=start)
-    say("append_paged encode")
-    nk.encode(P, lay, dev(kk, torch.bfloat16), dev(vv, torch.bfloat16), dev([start] * B, torch.int32),
-              pk, pv)
+    pk = torch.zeros((B * bps, H, bs, L), dtype=torch.uint8, device="cuda")
+    pv = torch.zeros_like(pk)
+    say("append_paged: history encode (28672 tokens x 32 sequences)")
+    hk, hv = _device_tokens(wl, B, start, 0)
+    nk.encode(P, lay, hk, hv, torch.zeros(B, dtype=torch.int32, device="cuda"), pk, pv)
+    say("append_paged: append 4096 tokens x 32 sequences")
+    kk, vv = _device_tokens(wl, B, wl.n_new, start)
+    nk.encode(P, lay, kk, vv, torch.full((B,), start, dtype=torch.int32, device="cuda"), pk, pv)
     torch.cuda.synchronize()
-    gk_pool = pk.cpu().numpy()
-    gv_pool = pv.cpu().numpy()
-    # history untouched
-    assert np.array_equal(read_rows(gk_pool, 3, 2, 0, start, groups=L, **lk), hist_k[3, 2])
-    units = [(0, 0), (13, 4), (31, 7)]
-    oracle_codes = {}
-    for b, kv in units:
-        ck, gk, cv, gv = ocodec.encode_tokens(kk[b, :, kv], vv[b, :, kv], oatt.head_params(params, kv))
-        compare_codes(read_rows(gk_pool, b, kv, start, wl.n_new, groups=L, **lk), ck, gk,
-                      f"append b{b} kv{kv} K")
-        compare_codes(read_rows(gv_pool, b, kv, start, wl.n_new, groups=L, **lk), cv, gv,
-                      f"append b{b} kv{kv} V")
-        oracle_codes[(b, kv)] = (ck, cv)
-    # decode over the paged pool; the oracle uses its own codes for the appended tokens
+    say("append_paged: oracle check of every appended code")
+    gk_pool, gv_pool = pk.cpu().numpy().reshape(-1), pv.cpu().numpy().reshape(-1)
+    new_codes = _check_all_codes(params, kk, vv, gk_pool, gv_pool, start, lk, "append")
+    del kk, vv
+    say("append_paged: decode at 32768")
     q = synth.decode_queries(wl, 0)
-    say("append_paged decode")
-    out = nk.decode_attn(P, lay, dev(q, torch.bfloat16), pk, pv, dev([S] * B, torch.int32), S)
+    out = nk.decode_attn(P, lay, dev(q, torch.bfloat16), pk, pv, torch.full((B,), S, dtype=torch.int32,
+                                                                            device="cuda"), S)
     out = out.cpu().numpy()
     scale = 1 / np.sqrt(D)
     gots, refs = [], []
-    for b, kv in units:
-        ck = np.concatenate([hist_k[b, kv], oracle_codes[(b, kv)][0]])
-        cv = np.concatenate([hist_v[b, kv], oracle_codes[(b, kv)][1]])
-        refs.append(oatt.decode_rows(q[b, kv * G:(kv + 1) * G], ck, cv, oatt.head_params(params, kv), scale))
+    for b, kv in [(0, 0), (13, 4), (31, 7)]:
+        hp = oatt.head_params(params, kv)
+        xk = hk[b, :, kv].float().cpu().numpy().astype(np.float64)
+        xv = hv[b, :, kv].float().cpu().numpy().astype(np.float64)
+        ck, gk, cv, gv = ocodec.encode_tokens(xk, xv, hp)
+        compare_codes(_pool_rows(gk_pool, [b], kv, 0, start, groups=L, **lk), ck, gk, f"append history b{b} kv{kv} K")
+        compare_codes(_pool_rows(gv_pool, [b], kv, 0, start, groups=L, **lk), cv, gv, f"append history b{b} kv{kv} V")
+        nck, ncv = new_codes[kv]
+        rows = slice(b * wl.n_new, (b + 1) * wl.n_new)
+        refs.append(oatt.decode_rows(q[b, kv * G:(kv + 1) * G], np.concatenate([ck, nck[rows]]),
+                                     np.concatenate([cv, ncv[rows]]), hp, scale))
         gots.append(out[b, kv * G:(kv + 1) * G])
     assert_outputs_close(np.concatenate(gots), np.concatenate(refs), what="append_paged decode")
+    assert np.isfinite(out).all()

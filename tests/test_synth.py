@@ -40,3 +40,22 @@ def test_block_table_is_a_permutation():
     bt = synth.shuffled_block_table(wl)
     assert bt.shape == (32, 2048)
     assert np.array_equal(np.sort(bt.ravel()), np.arange(32 * 2048))
+
+
+def test_device_cache_tokens_are_seeded_and_follow_the_model():
+    """The device-side generator (run here on the CPU device) is reproducible,
+    depends on the sequence and start, and draws each KV head's tokens with
+    that head's basis and spectrum."""
+    wl = synth.get_workload("append_paged")
+    k, v = synth.device_cache_tokens(wl, 0, 3, 8192, 1024, "cpu")
+    k2, v2 = synth.device_cache_tokens(wl, 0, 3, 8192, 1024, "cpu")
+    assert k.dtype == torch.bfloat16 and tuple(k.shape) == (8192, 8, 128)
+    assert torch.equal(k, k2) and torch.equal(v, v2)
+    assert not torch.equal(k, synth.device_cache_tokens(wl, 0, 4, 8192, 1024, "cpu")[0])
+    lam = synth.power_spectrum(128, 1.0)
+    for kv in (0, 5):
+        u_k, u_v, _ = synth.head_bases(wl, 0, kv)
+        for x, u in ((k[:, kv], u_k), (v[:, kv], u_v)):
+            var = (x.double().numpy() @ u).var(axis=0)
+            # 8192 draws: relative standard error of a variance ~ sqrt(2 / 8192) = 1.6%
+            assert np.all(np.abs(var / lam - 1) < 0.08)
