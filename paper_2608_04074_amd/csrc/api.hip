@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
 #include <string>
 
 #include "../../include/nova_kv.h"
@@ -32,6 +33,16 @@ nova_kv_status ok() {
 }
 
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Tag of the split exchange of the next decode call: every call gets a new
+// nonzero number (the workspace's words of one call are never taken for
+// another's; zero marks a never-written word).
+uint32_t next_epoch() {
+  static std::atomic<uint32_t> counter{0};
+  uint32_t e = counter.fetch_add(1, std::memory_order_relaxed) + 1;
+  while (e == 0) e = counter.fetch_add(1, std::memory_order_relaxed) + 1;
+  return e;
+}
 
 nova_kv_status check_params(const nova_kv_params *p, bool need_encode, bool need_decode) {
   if (!p) return fail(NOVA_KV_ERR_INVALID_ARG, "params is NULL");
@@ -269,6 +280,7 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   a.n_split = plan.n_split;
   a.chunk = plan.chunk;
   a.b_chunk = novakv::plan_b_chunk(batch, p->num_kv_heads, plan.n_split);
+  a.epoch = next_epoch();
   return NOVA_KV_OK;
 }
 

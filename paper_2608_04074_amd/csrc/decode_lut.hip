@@ -117,8 +117,8 @@ __device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, 
 // other memory operation of that wave delays its reply (a wave's memory
 // operations complete in issue order), counts the split in while the waves
 // merge.  The split that brings the count to n_split combines: it checks the
-// tag of every word it reads, so no order between the stores and the count
-// is needed.
+// tag of every word it reads (the call's epoch), so no order between the
+// stores and the count is needed, and no word is emptied after use.
 //   split slot: (m, l) of head h at words 2h, 2h+1, coordinate d of head h
 //               at 2G + h*128 + d;
 //   new token:  item k (side * 4 + block), lane j at word 32k + j, key
@@ -234,7 +234,7 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
       } else {
         v = static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + kVBase + (g & 7) * 8192 + 32 * code +
                                                                    8 * (g >> 3) + 2 * lr));
-        if (a.n_split > 1) put_word(xn + item * 32 + 4 * gl + lr, v);
+        if (a.n_split > 1) put_word(a.epoch, xn + item * 32 + 4 * gl + lr, v);
       }
       res[item * 32 + 4 * gl + lr] = v;
     }
@@ -250,7 +250,7 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
 #pragma unroll
       for (int gg = 0; gg < encblk::kGroups; ++gg) v += res[item * 32 + 4 * gg + t];
       res[item * 32 + t] = v;
-      if (a.n_split > 1) put_word(xn + item * 32 + t, v);
+      if (a.n_split > 1) put_word(a.epoch, xn + item * 32 + t, v);
     }
   }
 }
@@ -777,10 +777,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       ownml[2 * h + 1] = den;
     }
     if (pub) {
-      put_word(slot + 2 * G + i, num);
+      put_word(a.epoch, slot + 2 * G + i, num);
       if (d == 0) {
-        put_word(slot + 2 * h, mlog);
-        put_word(slot + 2 * h + 1, den);
+        put_word(a.epoch, slot + 2 * h, mlog);
+        put_word(a.epoch, slot + 2 * h + 1, den);
       }
     }
   }
@@ -792,7 +792,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 // division by the denominator, and the inverse value transform
 // out = s_hat t_v^T (Corollary 1).  The split's own partial and blocks of the
 // new token are read from LDS, the other splits' from the exchange (every
-// word's tag checked, the words emptied once read); splits that attend to no
+// word's tag checked against the call's epoch); splits that attend to no
 // token published no partial and are skipped.
 // Rows of the band attended by split `split` of n_split: consecutive shares
 // in split order.
@@ -883,7 +883,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
       for (int i = 0; i < 4; ++i) {
         if (want[i]) {
           const uint64_t *slot = xs + static_cast<size_t>(spk[i]) * kXchSlotWords;
-          for (int n = 0; !(word_ready(wm[i]) && word_ready(wl[i]) && word_ready(wa[i])); ++n) {
+          for (int n = 0; !(word_ready(a.epoch, wm[i]) && word_ready(a.epoch, wl[i]) && word_ready(a.epoch, wa[i])); ++n) {
             if (n == kSpinLimit) {
               ok = false;
               break;
@@ -911,7 +911,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
           if (k % n_eff == own_split) {
             zp[k] = res[k * 32 + h];
           } else {
-            for (int n = 0; !word_ready(wz[k]); ++n) {
+            for (int n = 0; !word_ready(a.epoch, wz[k]); ++n) {
               if (n == kSpinLimit) {
                 ok = false;
                 break;
@@ -925,7 +925,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
         if ((4 + (d >> 5)) % n_eff == own_split) {
           vp = res[vj];
         } else {
-          for (int n = 0; !word_ready(wv); ++n) {
+          for (int n = 0; !word_ready(a.epoch, wv); ++n) {
             if (n == kSpinLimit) {
               ok = false;
               break;
@@ -954,7 +954,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
         } else {
           const uint64_t *bw = a.xch + (static_cast<size_t>(bk) * a.n_split + sp) * kXchSlotWords + kXchBandWords;
           uint64_t wm = get_word(bw + 2 * h), wl = get_word(bw + 2 * h + 1), wa = get_word(bw + 2 * G + tid);
-          for (int n = 0; !(word_ready(wm) && word_ready(wl) && word_ready(wa)); ++n) {
+          for (int n = 0; !(word_ready(a.epoch, wm) && word_ready(a.epoch, wl) && word_ready(a.epoch, wa)); ++n) {
             if (n == kSpinLimit) {
               ok = false;
               break;
@@ -1023,45 +1023,6 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
         (outp[h * kD + d] + outp[(4 + h) * kD + d]) + (outp[(8 + h) * kD + d] + outp[(12 + h) * kD + d]);
     a.out[(row0 + h) * kD + d] = nband > 0 ? o + bout[tid] : o;
   }
-  // Every word read above has been seen with its tag by every thread that
-  // reads it (there were barriers since): empty the other splits' words for
-  // the next call, a word read by several threads by one of them.  These
-  // stores go out last, behind the output's.
-  if (tid < G * kD) {
-    const int h = tid >> 7;
-    uint64_t *xs = a.xch + static_cast<size_t>(bk) * a.n_split * kXchSlotWords;
-    for (int sp = 0; sp < a.n_split; ++sp) {
-      if (sp == own_split) continue;
-      uint64_t *slot = xs + static_cast<size_t>(sp) * kXchSlotWords;
-      if (lo + sp * a.chunk < tend) {
-        clear_word(slot + 2 * G + tid);
-        if (d == 0) {
-          clear_word(slot + 2 * h);
-          clear_word(slot + 2 * h + 1);
-        }
-      }
-      int first, count;
-      band_share(nband, a.n_split, sp, first, count);
-      if (count > 0) {
-        clear_word(slot + kXchBandWords + 2 * G + tid);
-        if (d == 0) {
-          clear_word(slot + kXchBandWords + 2 * h);
-          clear_word(slot + kXchBandWords + 2 * h + 1);
-        }
-      }
-    }
-    if constexpr (APPEND) {
-      if (S > 0) {
-        uint64_t *xn = a.xnew + static_cast<size_t>(bk) * 8 * 32;
-        if (d == 0) {
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-            if (k % n_eff != own_split) clear_word(xn + k * 32 + h);
-        }
-        if (h == 0 && (4 + (d >> 5)) % n_eff != own_split) clear_word(xn + (4 + (d >> 5)) * 32 + (d & 31));
-      }
-    }
-  }
 }
 
 // One workgroup per (sequence, KV head, split).  Every split publishes its
@@ -1122,10 +1083,10 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
       if (a.n_split > 1 && tid < G * kD) {
         const int h = tid >> 7;
         uint64_t *bw = a.xch + (static_cast<size_t>(bk) * a.n_split + split) * kXchSlotWords + kXchBandWords;
-        put_word(bw + 2 * G + tid, reinterpret_cast<const float *>(smem + BL::kZ)[tid]);
+        put_word(a.epoch, bw + 2 * G + tid, reinterpret_cast<const float *>(smem + BL::kZ)[tid]);
         if ((tid & (kD - 1)) == 0) {
-          put_word(bw + 2 * h, reinterpret_cast<const float *>(smem + BL::kStat)[h]);
-          put_word(bw + 2 * h + 1, reinterpret_cast<const float *>(smem + BL::kStat)[4 + h]);
+          put_word(a.epoch, bw + 2 * h, reinterpret_cast<const float *>(smem + BL::kStat)[h]);
+          put_word(a.epoch, bw + 2 * h + 1, reinterpret_cast<const float *>(smem + BL::kStat)[4 + h]);
         }
       }
     }
@@ -1134,35 +1095,6 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   __syncthreads();  // the split's partial and its blocks of the new token are in LDS; the count is known
   if (a.n_split > 1) {
     if (ctl[0] == 0) return;
-    // the combining split's own words are emptied by the threads that wrote them
-    if (active && tid < G * kD) {
-      uint64_t *slot = a.xch + (static_cast<size_t>(bk) * a.n_split + split) * kXchSlotWords;
-      clear_word(slot + 2 * G + tid);
-      if ((tid & (kD - 1)) == 0) {
-        clear_word(slot + 2 * (tid >> 7));
-        clear_word(slot + 2 * (tid >> 7) + 1);
-      }
-    }
-    if (bcount > 0 && tid < G * kD) {
-      uint64_t *bw = a.xch + (static_cast<size_t>(bk) * a.n_split + split) * kXchSlotWords + kXchBandWords;
-      clear_word(bw + 2 * G + tid);
-      if ((tid & (kD - 1)) == 0) {
-        clear_word(bw + 2 * (tid >> 7));
-        clear_word(bw + 2 * (tid >> 7) + 1);
-      }
-    }
-    if constexpr (APPEND) {
-      // the same team threads as in encode_items: value words by the thread
-      // that found the group, key words by head thread t < G
-      const int t = tid - 512;
-      if (items && t >= 0) {
-        uint64_t *xn = a.xnew + static_cast<size_t>(bk) * 8 * 32;
-        for (int item = split; item < 8; item += n_eff) {
-          if (item >= 4 && (t & 31) < 4) clear_word(xn + item * 32 + 4 * (t >> 5) + (t & 31));
-          if (item < 4 && t < G) clear_word(xn + item * 32 + t);
-        }
-      }
-    }
   }
   combine_unit<WAVES, APPEND>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv);
 }

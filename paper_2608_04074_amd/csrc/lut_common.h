@@ -93,23 +93,25 @@ __device__ __forceinline__ float load_dev(const float *p) {
   return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Tagged exchange words.  A published value travels with a nonzero tag in the
-// high half of one 64-bit word, written and read as a single relaxed
-// agent-scope atomic; 0 marks an empty slot.  A reader that finds a tag knows
-// that the value beside it is the published one, whatever order other stores
-// arrived in, so a writer never waits for its stores to complete.  The
-// reader that consumes a slot empties it again for the next call.
-__device__ __forceinline__ void put_word(uint64_t *p, float v) {
-  const uint64_t w = (static_cast<uint64_t>(1) << 32) | __builtin_bit_cast(uint32_t, v);
+// Tagged exchange words.  A published value travels with a tag in the high
+// half of one 64-bit word, written and read as a single relaxed agent-scope
+// atomic.  The tag is the call's epoch, a nonzero number the host gives
+// every decode call: a reader that finds its call's epoch knows that the
+// value beside it is the one published in this call, whatever order other
+// stores arrived in, so a writer never waits for its stores to complete, and
+// a word left by an earlier call (another epoch) is never taken for a new
+// one.  Words are therefore never emptied; a zero-filled workspace holds
+// tag 0, which no call uses.
+__device__ __forceinline__ void put_word(const uint32_t epoch, uint64_t *p, float v) {
+  const uint64_t w = (static_cast<uint64_t>(epoch) << 32) | __builtin_bit_cast(uint32_t, v);
   __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void clear_word(uint64_t *p) {
-  __hip_atomic_store(p, static_cast<uint64_t>(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ uint64_t get_word(const uint64_t *p) {
   return __hip_atomic_load(const_cast<uint64_t *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ bool word_ready(const uint64_t w) { return (w >> 32) != 0; }
+__device__ __forceinline__ bool word_ready(const uint32_t epoch, const uint64_t w) {
+  return static_cast<uint32_t>(w >> 32) == epoch;
+}
 __device__ __forceinline__ float word_value(const uint64_t w) {
   return __builtin_bit_cast(float, static_cast<uint32_t>(w));
 }

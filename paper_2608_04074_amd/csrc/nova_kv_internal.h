@@ -75,11 +75,12 @@ struct DecodeArgs {
   const float *t_k;
   uint8_t *k_codes_w, *v_codes_w;  // the pools k_codes / v_codes, written at the new position
   float *newp;      // [B][Hkv][8 items][32] per-block results for the new token
-  // Tagged exchange of the head_dim-128 table kernel (64-bit words, 0 = empty):
-  // split partials [B*Hkv][n_split][kXchSlotWords] and the new token's
-  // per-block results [B*Hkv][8 items][32].
+  // Tagged exchange of the head_dim-128 table kernel (64-bit words, the tag
+  // in the high half): split partials [B*Hkv][n_split][kXchSlotWords] and
+  // the new token's per-block results [B*Hkv][8 items][32].
   uint64_t *xch;
   uint64_t *xnew;
+  uint32_t epoch;   // this call's tag of the exchanged words (nonzero, new for every call)
 };
 
 // Words of one split's slot in the tagged exchange: (m, l) of up to 8 query
