@@ -1105,13 +1105,23 @@ bool lut_path_eligible(int head_dim, int gqa, int block_size) {
   return block_size % 16 == 0 && ((head_dim == 128 && gqa <= 4) || (head_dim == 64 && gqa <= 8));
 }
 
+// Splits per (sequence, KV head): enough for about 256 workgroups, one per
+// CU, but never fewer than kMinChunk tokens per split.  Every split pays the
+// whole setup (parameters, query transform, tables) and adds a partial to the
+// combine, so a short span is not worth many CUs: a split of kMinChunk tokens
+// streams its codes in less time than one more partial costs the combine.
+#ifndef NOVA_KV_MIN_CHUNK
+#define NOVA_KV_MIN_CHUNK 512
+#endif
+constexpr int kMinChunk = NOVA_KV_MIN_CHUNK;
+
 void plan_lut(int batch, int num_kv_heads, int max_seq_len, int *n_split, int *chunk) {
   const long long units = static_cast<long long>(batch) * num_kv_heads;
   int ns = static_cast<int>((256 + units - 1) / units);
   if (ns < 1) ns = 1;
   int ch = (max_seq_len + ns - 1) / ns;
   ch = (ch + 63) & ~63;
-  if (ch < 64) ch = 64;
+  if (ch < kMinChunk) ch = kMinChunk;
   *chunk = ch;
   *n_split = (max_seq_len + ch - 1) / ch;
 }
