@@ -281,7 +281,7 @@ def other_workload(nk, torch, dev, case, calls: int):
                                 k_scales=ps, band=bands[i % len(bands)], v_sq=pq)
               for i, (pk, pv, ps, pq) in enumerate(pools)]
     fn = lambda i: calls_[i % copies]()  # noqa: E731
-    for i in range(20):
+    for i in range(200):
         fn(i)
     us = back_to_back_us(torch, fn, calls)
     per_call = timed_calls(torch, fn, calls)

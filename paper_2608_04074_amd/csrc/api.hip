@@ -280,6 +280,13 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   a.n_split = plan.n_split;
   a.chunk = plan.chunk;
   a.b_chunk = novakv::plan_b_chunk(batch, p->num_kv_heads, plan.n_split);
+  a.xgrp = reinterpret_cast<uint64_t *>(ws + plan.off_xgrp);
+  a.group_size = plan.n_split;
+  a.n_group = 1;
+  if (plan.use_lut && p->head_dim == 128) {
+    a.group_size = novakv::plan_group_size(plan.n_split);
+    a.n_group = (plan.n_split + a.group_size - 1) / a.group_size;
+  }
   a.epoch = next_epoch();
   return NOVA_KV_OK;
 }

@@ -455,15 +455,22 @@ DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_di
   if (p.n_split > max_split) max_split = p.n_split;
   auto align = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
   const size_t rows = static_cast<size_t>(batch) * num_q_heads;
+  // groups of the two-level combine, at most, over every split count up to the bound
+  int max_group = 1;
+  for (int n = 1; n <= max_split; ++n) {
+    const int gs = plan_group_size(n), ng = (n + gs - 1) / gs;
+    if (ng > max_group) max_group = ng;
+  }
   p.off_cnt = 0;
-  p.off_qp = align(static_cast<size_t>(batch) * num_kv_heads * sizeof(int));
+  p.off_qp = align(static_cast<size_t>(units) * (1 + max_group) * sizeof(int));
   p.off_sinkp = align(p.off_qp + rows * head_dim * sizeof(float));
   p.off_ml = align(p.off_sinkp + rows * sizeof(float));
   p.off_acc = align(p.off_ml + rows * max_split * 2 * sizeof(float));
   p.off_new = align(p.off_acc + rows * max_split * head_dim * sizeof(float));
   p.off_xch = align(p.off_new + static_cast<size_t>(batch) * num_kv_heads * 8 * 32 * sizeof(float));
   p.off_xnew = align(p.off_xch + units * max_split * kXchSlotWords * sizeof(uint64_t));
-  p.total = align(p.off_xnew + static_cast<size_t>(units) * 8 * 32 * sizeof(uint64_t));
+  p.off_xgrp = align(p.off_xnew + static_cast<size_t>(units) * 8 * 32 * sizeof(uint64_t));
+  p.total = align(p.off_xgrp + units * max_group * kXchSlotWords * sizeof(uint64_t));
   return p;
 }
 

@@ -118,9 +118,12 @@ __device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, 
 // operations complete in issue order), counts the split in while the waves
 // merge.  The split that brings the count to n_split combines: it checks the
 // tag of every word it reads (the call's epoch), so no order between the
-// stores and the count is needed, and no word is emptied after use.
-//   split slot: (m, l) of head h at words 2h, 2h+1, coordinate d of head h
-//               at 2G + h*128 + d;
+// stores and the count is needed, and no word is emptied after use.  With
+// many splits the count runs per group of splits, and the group's last split
+// merges the group first (two levels, below).
+//   split slot: log-sum-exp m + ln l of head h at word 2h (natural log),
+//               normalised coordinate d of head h (acc / l) at 2G + h*128 + d;
+//               a split without tokens publishes nothing;
 //   new token:  item k (side * 4 + block), lane j at word 32k + j, key
 //               blocks for lanes j < G (the heads), value blocks for all 32.
 constexpr int kCtl = 512;
@@ -735,10 +738,13 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   // ---- arrival (see the exchange below): counted now, while the waves merge
   const int bk = b * a.num_kv_heads + kv;
   if (a.n_split > 1 && tid == kCtl) {
+    // the split's group (all splits when there is one group)
     int *ctl = reinterpret_cast<int *>(smem + kAuxCtl);
-    const int last = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-                     a.n_split - 1;
-    if (last) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int gi = split / a.group_size;
+    const int gsz = min(a.group_size, a.n_split - gi * a.group_size);
+    int *cnt = a.counters + bk * (1 + a.n_group) + 1 + gi;
+    const int last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == gsz - 1;
+    if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     ctl[0] = last;
   }
 
@@ -770,18 +776,18 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
         den = fmaf(wt, lv[w], den);
       }
     }
-    own[i] = num;
-    const float mlog = big == -INFINITY ? -INFINITY : big * kLn2;
+    // kept and published as (log-sum-exp, 1, normalised partial), so that the
+    // combining split takes its own partial with the bits the others read
+    const float lse = den > 0.f ? big * kLn2 + __logf(den) : -INFINITY;
+    const float o = den > 0.f ? num / den : 0.f;
+    own[i] = o;
     if (d == 0) {
-      ownml[2 * h] = mlog;
-      ownml[2 * h + 1] = den;
+      ownml[2 * h] = lse;
+      ownml[2 * h + 1] = 1.f;
     }
     if (pub) {
-      put_word(a.epoch, slot + 2 * G + i, num);
-      if (d == 0) {
-        put_word(a.epoch, slot + 2 * h, mlog);
-        put_word(a.epoch, slot + 2 * h + 1, den);
-      }
+      put_word(a.epoch, slot + 2 * G + i, o);
+      if (d == 0) put_word(a.epoch, slot + 2 * h, lse);
     }
   }
 }
@@ -803,11 +809,82 @@ __device__ __forceinline__ void band_share(const int nband, const int n_split, c
   count = min(nband, first + per) - first;
 }
 
+// Exchange slots whose words one combine requests before it waits.  The
+// combine runs once per (sequence, KV head) from a cold instruction cache, so
+// its code is kept short: four slots per batch, and many splits are merged in
+// groups (two levels) rather than read in long batches by one workgroup.
+#ifndef NOVA_KV_XCH_BATCH
+#define NOVA_KV_XCH_BATCH 4
+#endif
+constexpr int kXchBatch = NOVA_KV_XCH_BATCH;
+static_assert(kXchBatch <= 48, "a batch's requests stay within the wave's outstanding-load count");
+
+__device__ __forceinline__ uint64_t readlane64(const uint64_t x, const int lane) {
+  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x)), lane);
+  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(x >> 32)), lane);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Reads `count` (1..kXchBatch) exchange slots and hands each wanted one, in
+// batch order, to take(i, log-sum-exp, normalised partial) for head h,
+// coordinate `tid` (h = tid / 128).  The heads' log-sum-exp words are
+// requested one slot per lane and broadcast from that lane; each thread
+// requests its coordinate of every slot.  All requests are issued before the
+// first wait, so the batch costs one round trip; past `count` they repeat the
+// last slot.  If a word of the wave's batch does not carry the call's tag
+// yet, the wave reads the batch again slot by slot, waiting for each word.
+// Returns false if a word never arrived (not expected).
+template <class SlotOf, class Want, class Take>
+__device__ __forceinline__ bool read_slots(const uint32_t epoch, const int count, const int h, const int G,
+                                           const int tid, SlotOf slot_of, Want want, Take take) {
+  if (count <= 0) return true;
+  const int lane = tid & 63;
+  const uint64_t lw = get_word(slot_of(min(lane, count - 1)) + 2 * h);
+  uint64_t wa[kXchBatch];
+#pragma unroll
+  for (int i = 0; i < kXchBatch; ++i) wa[i] = get_word(slot_of(min(i, count - 1)) + 2 * G + tid);
+  bool ready = lane >= count || !want(lane) || word_ready(epoch, lw);
+#pragma unroll
+  for (int i = 0; i < kXchBatch; ++i)
+    if (i < count && want(i) && !word_ready(epoch, wa[i])) ready = false;
+  if (__all(ready)) {
+#pragma unroll
+    for (int i = 0; i < kXchBatch; ++i)
+      if (i < count && want(i)) take(i, word_value(readlane64(lw, i)), word_value(wa[i]));
+    return true;
+  }
+  bool ok = true;
+  for (int i = 0; i < count; ++i) {
+    if (!want(i)) continue;
+    const uint64_t *sp = slot_of(i);
+    uint64_t wm = get_word(sp + 2 * h), w = get_word(sp + 2 * G + tid);
+    for (int n = 0; !(word_ready(epoch, wm) && word_ready(epoch, w)); ++n) {
+      if (n == kSpinLimit) {
+        ok = false;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+      wm = get_word(sp + 2 * h);
+      w = get_word(sp + 2 * G + tid);
+    }
+    take(i, word_value(wm), word_value(w));
+  }
+  return ok;
+}
+
+// The partials this combine reads: the unit's split slots (one level), or
+// the slots of its split groups (two levels).
+struct Slots {
+  const uint64_t *base;  // slot 0
+  int n, own;            // number of slots, this workgroup's slot
+  bool all_valid;        // group slots: every slot holds a partial and a band block
+};
+
 template <int WAVES, bool APPEND>
 __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                              const int bk, const size_t row0, const int own_split, const int S,
                                              const int lo, const int tend, const int n_eff, const int band_lo,
-                                             const int sink_end, const float4 (&tv)[8]) {
+                                             const int sink_end, const float4 (&tv)[8], const Slots sl) {
   const int tid = threadIdx.x;
   const int G = a.gqa;
   // Sink-plus-recent band: positions [band_lo, sink_end) and [tend, S) (the
@@ -854,54 +931,27 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
       den = fmaf(w, ls, den);
       num = fmaf(w, as, num);
     };
-    // splits in index order whichever split combines, so the result does not
-    // depend on the arrival order.  The other splits' words are requested four
-    // splits at a time; past the last split the requests repeat its words, so
-    // every request is unconditional and one wait covers the four.
-    uint64_t *xs = a.xch + static_cast<size_t>(bk) * a.n_split * kXchSlotWords;
-    const int n_oth = a.n_split - 1;
+    // splits (or groups) in index order whichever split combines, so the
+    // result does not depend on the arrival order; the other slots are read
+    // kXchBatch at a time
+    const uint64_t *xs = sl.base;
+    const int n_oth = sl.n - 1;
+    const int own_slot = sl.own;
     bool own_done = false;
     auto take_own = [&]() {
       take(ctlf[8 + 2 * h], ctlf[8 + 2 * h + 1], own[tid]);
       own_done = true;
     };
-    for (int k0 = 0; k0 < n_oth; k0 += 4) {
-      uint64_t wm[4], wl[4], wa[4];
-      int spk[4];
-      bool want[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int k = min(k0 + i, n_oth - 1);
-        spk[i] = k + (k >= own_split ? 1 : 0);
-        want[i] = k0 + i < n_oth && lo + spk[i] * a.chunk < tend;
-        const uint64_t *slot = xs + static_cast<size_t>(spk[i]) * kXchSlotWords;
-        wm[i] = get_word(slot + 2 * h);
-        wl[i] = get_word(slot + 2 * h + 1);
-        wa[i] = get_word(slot + 2 * G + tid);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (want[i]) {
-          const uint64_t *slot = xs + static_cast<size_t>(spk[i]) * kXchSlotWords;
-          for (int n = 0; !(word_ready(a.epoch, wm[i]) && word_ready(a.epoch, wl[i]) && word_ready(a.epoch, wa[i])); ++n) {
-            if (n == kSpinLimit) {
-              ok = false;
-              break;
-            }
-            __builtin_amdgcn_s_sleep(2);
-            wm[i] = get_word(slot + 2 * h);
-            wl[i] = get_word(slot + 2 * h + 1);
-            wa[i] = get_word(slot + 2 * G + tid);
-          }
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (k0 + i < n_oth) {
-          if (!own_done && spk[i] > own_split) take_own();
-          if (want[i]) take(word_value(wm[i]), word_value(wl[i]), word_value(wa[i]));
-        }
-      }
+    for (int k0 = 0; k0 < n_oth; k0 += kXchBatch) {
+      auto sidx = [&](int i) { return k0 + i + (k0 + i >= own_slot ? 1 : 0); };
+      ok &= read_slots(
+          a.epoch, min(kXchBatch, n_oth - k0), h, G, tid,
+          [&](int i) { return xs + static_cast<size_t>(sidx(i)) * kXchSlotWords; },
+          [&](int i) { return sl.all_valid || lo + sidx(i) * a.chunk < tend; },
+          [&](int i, float ms, float as) {
+            if (!own_done && sidx(i) > own_slot) take_own();
+            take(ms, 1.f, as);
+          });
     }
     if (!own_done) take_own();
     if constexpr (APPEND) {
@@ -940,34 +990,10 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
     }
     float bo = 0.f;
     if (nband > 0) {  // the band, after the splits (and the new token)
+      // the splits' (or groups') shares in index order, this split's from LDS
       float mb = -INFINITY, lb = 0.f, ab = 0.f;
-      for (int sp = 0; sp < a.n_split; ++sp) {
-        int first, count;
-        band_share(nband, a.n_split, sp, first, count);
-        if (count == 0) continue;
-        float ms, ls, as;
-        if (sp == own_split) {
-          const float *bst = reinterpret_cast<const float *>(smem + BL::kStat);
-          ms = bst[h];
-          ls = bst[4 + h];
-          as = reinterpret_cast<const float *>(smem + BL::kZ)[h * kD + d];
-        } else {
-          const uint64_t *bw = a.xch + (static_cast<size_t>(bk) * a.n_split + sp) * kXchSlotWords + kXchBandWords;
-          uint64_t wm = get_word(bw + 2 * h), wl = get_word(bw + 2 * h + 1), wa = get_word(bw + 2 * G + tid);
-          for (int n = 0; !(word_ready(a.epoch, wm) && word_ready(a.epoch, wl) && word_ready(a.epoch, wa)); ++n) {
-            if (n == kSpinLimit) {
-              ok = false;
-              break;
-            }
-            __builtin_amdgcn_s_sleep(2);
-            wm = get_word(bw + 2 * h);
-            wl = get_word(bw + 2 * h + 1);
-            wa = get_word(bw + 2 * G + tid);
-          }
-          ms = word_value(wm);
-          ls = word_value(wl);
-          as = word_value(wa);
-        }
+      auto take_b = [&](float ms, float ls, float as) {
+        if (ms == -INFINITY) return;  // a group without band rows
         if (ms > mb) {
           const float f = mb == -INFINITY ? 0.f : __expf(mb - ms);
           lb *= f;
@@ -977,7 +1003,32 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
         const float w = __expf(ms - mb);
         lb = fmaf(w, ls, lb);
         ab = fmaf(w, as, ab);
+      };
+      auto has_share = [&](int sp) {
+        if (sl.all_valid) return true;
+        int first, count;
+        band_share(nband, a.n_split, sp, first, count);
+        return count > 0;
+      };
+      const float *bst = reinterpret_cast<const float *>(smem + BL::kStat);
+      const float *bzs = reinterpret_cast<const float *>(smem + BL::kZ);
+      bool own_b = false;
+      auto take_own_b = [&]() {
+        if (has_share(own_slot)) take_b(bst[h], bst[4 + h], bzs[h * kD + d]);
+        own_b = true;
+      };
+      for (int k0 = 0; k0 < n_oth; k0 += kXchBatch) {
+        auto sidx = [&](int i) { return k0 + i + (k0 + i >= own_slot ? 1 : 0); };
+        ok &= read_slots(
+            a.epoch, min(kXchBatch, n_oth - k0), h, G, tid,
+            [&](int i) { return xs + static_cast<size_t>(sidx(i)) * kXchSlotWords + kXchBandWords; },
+            [&](int i) { return has_share(sidx(i)); },
+            [&](int i, float ms, float as) {
+              if (!own_b && sidx(i) > own_slot) take_own_b();
+              take_b(ms, 1.f, as);
+            });
       }
+      if (!own_b) take_own_b();
       if (mb > big) {
         const float f = big == -INFINITY ? 0.f : __expf(big - mb);
         num *= f;
@@ -1025,6 +1076,113 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
   }
 }
 
+// Two-level combine (many splits): the last split of each group of
+// a.group_size splits merges its group's partials, in split order, into one
+// partial (its code part and its band part), keeps it in LDS in place of its
+// own and publishes it to the group's slot; the last group then combines the
+// group slots.  No sink, new token or inverse transform at this level.
+template <int WAVES>
+__device__ __forceinline__ void merge_group(const DecodeArgs &a, uint8_t *smem, const int bk, const int split,
+                                            const int S, const int lo, const int tend, const int band_lo,
+                                            const int sink_end) {
+  const int tid = threadIdx.x;
+  const int G = a.gqa;
+  using BL = BandLds<kD, 4, WAVES>;
+  const int nband = a.band_k ? max(0, sink_end - band_lo) + (S - tend) : 0;
+  const int gi = split / a.group_size;
+  const int g0 = gi * a.group_size, gsz = min(a.group_size, a.n_split - g0);
+  float *ctlf = reinterpret_cast<float *>(smem + kAuxCtl);
+  float *own = reinterpret_cast<float *>(smem + kAuxOwn);
+  float *bst = reinterpret_cast<float *>(smem + BL::kStat);
+  float *bz = reinterpret_cast<float *>(smem + BL::kZ);
+  const uint64_t *xs = a.xch + static_cast<size_t>(bk) * a.n_split * kXchSlotWords;
+  uint64_t *gslot = a.xgrp + (static_cast<size_t>(bk) * a.n_group + gi) * kXchSlotWords;
+  const bool mine = tid < G * kD;
+  const int h = tid >> 7, d = tid & (kD - 1);
+  float big = -INFINITY, den = 0.f, num = 0.f;  // the group's code partial
+  float mb = -INFINITY, lb = 0.f, ab = 0.f;     // the group's band partial
+  if (mine) {
+    bool ok = true;
+    auto lse = [](float &m, float &l, float &acc, const float ms, const float ls, const float as) {
+      if (ms == -INFINITY) return;
+      if (ms > m) {
+        const float f = m == -INFINITY ? 0.f : __expf(m - ms);
+        acc *= f;
+        l *= f;
+        m = ms;
+      }
+      const float w = __expf(ms - m);
+      l = fmaf(w, ls, l);
+      acc = fmaf(w, as, acc);
+    };
+    // the group's other splits in split order, this split's partial from LDS
+    const int own_i = split - g0;
+    auto sidx = [&](int i) { return g0 + i + (i >= own_i ? 1 : 0); };
+    bool own_done = false, own_b = false;
+    for (int k0 = 0; k0 < gsz - 1; k0 += kXchBatch)
+      ok &= read_slots(
+          a.epoch, min(kXchBatch, gsz - 1 - k0), h, G, tid,
+          [&](int i) { return xs + static_cast<size_t>(sidx(k0 + i)) * kXchSlotWords; },
+          [&](int i) { return lo + sidx(k0 + i) * a.chunk < tend; },
+          [&](int i, float ms, float as) {
+            if (!own_done && k0 + i >= own_i) {
+              lse(big, den, num, ctlf[8 + 2 * h], ctlf[8 + 2 * h + 1], own[tid]);
+              own_done = true;
+            }
+            lse(big, den, num, ms, 1.f, as);
+          });
+    if (!own_done) lse(big, den, num, ctlf[8 + 2 * h], ctlf[8 + 2 * h + 1], own[tid]);
+    // band shares of the group's splits, in split order
+    if (nband > 0) {
+      auto has_share = [&](int sp) {
+        int first, count;
+        band_share(nband, a.n_split, sp, first, count);
+        return count > 0;
+      };
+      auto take_own_b = [&]() {
+        if (has_share(split)) lse(mb, lb, ab, bst[h], bst[4 + h], bz[h * kD + d]);
+        own_b = true;
+      };
+      for (int k0 = 0; k0 < gsz - 1; k0 += kXchBatch)
+        ok &= read_slots(
+            a.epoch, min(kXchBatch, gsz - 1 - k0), h, G, tid,
+            [&](int i) { return xs + static_cast<size_t>(sidx(k0 + i)) * kXchSlotWords + kXchBandWords; },
+            [&](int i) { return has_share(sidx(k0 + i)); },
+            [&](int i, float ms, float as) {
+              if (!own_b && k0 + i >= own_i) take_own_b();
+              lse(mb, lb, ab, ms, 1.f, as);
+            });
+      if (!own_b) take_own_b();
+    }
+    if (!ok) num = __builtin_nanf("");  // a word that never arrived (not expected): the rows turn NaN
+    // published (and kept) in the splits' form: (log-sum-exp, 1, normalised partial)
+    num = den > 0.f ? num / den : num;
+    big = den > 0.f ? big + __logf(den) : -INFINITY;
+    den = 1.f;
+    ab = lb > 0.f ? ab / lb : 0.f;
+    mb = lb > 0.f ? mb + __logf(lb) : -INFINITY;
+    lb = 1.f;
+    put_word(a.epoch, gslot + 2 * G + tid, num);
+    if (d == 0) put_word(a.epoch, gslot + 2 * h, big);
+    if (nband > 0) {
+      put_word(a.epoch, gslot + kXchBandWords + 2 * G + tid, ab);
+      if (d == 0) put_word(a.epoch, gslot + kXchBandWords + 2 * h, mb);
+    }
+  }
+  __syncthreads();  // every read of this split's own partial is done
+  // the group's partial replaces this split's own
+  if (mine) {
+    own[tid] = num;
+    bz[h * kD + d] = ab;
+    if (d == 0) {
+      ctlf[8 + 2 * h] = big;
+      ctlf[8 + 2 * h + 1] = den;
+      bst[h] = mb;
+      bst[4 + h] = lb;
+    }
+  }
+}
+
 // One workgroup per (sequence, KV head, split).  Every split publishes its
 // partial to the exchange and counts its arrival; the last one combines.
 // The arrival counters live in the workspace and the last split resets its
@@ -1054,7 +1212,6 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   const int t0 = lo + split * a.chunk;  // splits tile the span read from the pools
   const int t1 = min(tend, lo + (split + 1) * a.chunk);
   const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
-  const bool active = t0 < t1;
   // Fused step: the splits with pool tokens (at least split 0) share the encode
   // of the new token; such a split runs the setup even with no token of its own.
   int n_eff = 1;
@@ -1080,13 +1237,27 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
       band_attention<kD, 4, WAVES, WAVES>(a, smem, b, kv, row0, att_lo, spn.sink_end, tend, S, bfirst, bcount,
                                           reinterpret_cast<const float *>(smem + kAuxQ),
                                           reinterpret_cast<const float *>(smem + kItemRes));
-      if (a.n_split > 1 && tid < G * kD) {
-        const int h = tid >> 7;
-        uint64_t *bw = a.xch + (static_cast<size_t>(bk) * a.n_split + split) * kXchSlotWords + kXchBandWords;
-        put_word(a.epoch, bw + 2 * G + tid, reinterpret_cast<const float *>(smem + BL::kZ)[tid]);
+      // the share is kept and published as (log-sum-exp, 1, normalised partial)
+      float *bst = reinterpret_cast<float *>(smem + BL::kStat);
+      float *bz = reinterpret_cast<float *>(smem + BL::kZ);
+      const int h = tid >> 7;
+      float lse = 0.f, o = 0.f;
+      if (tid < G * kD) {
+        const float lb = bst[4 + h];
+        lse = lb > 0.f ? bst[h] + __logf(lb) : -INFINITY;
+        o = lb > 0.f ? bz[tid] / lb : 0.f;
+      }
+      __syncthreads();
+      if (tid < G * kD) {
+        bz[tid] = o;
         if ((tid & (kD - 1)) == 0) {
-          put_word(a.epoch, bw + 2 * h, reinterpret_cast<const float *>(smem + BL::kStat)[h]);
-          put_word(a.epoch, bw + 2 * h + 1, reinterpret_cast<const float *>(smem + BL::kStat)[4 + h]);
+          bst[h] = lse;
+          bst[4 + h] = 1.f;
+        }
+        if (a.n_split > 1) {
+          uint64_t *bw = a.xch + (static_cast<size_t>(bk) * a.n_split + split) * kXchSlotWords + kXchBandWords;
+          put_word(a.epoch, bw + 2 * G + tid, o);
+          if ((tid & (kD - 1)) == 0) put_word(a.epoch, bw + 2 * h, lse);
         }
       }
     }
@@ -1096,7 +1267,26 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   if (a.n_split > 1) {
     if (ctl[0] == 0) return;
   }
-  combine_unit<WAVES, APPEND>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv);
+  const uint64_t *xs = a.xch + static_cast<size_t>(bk) * a.n_split * kXchSlotWords;
+  if (a.n_group > 1) {
+    // two levels: merge this split's group, then count the group in
+    merge_group<WAVES>(a, smem, bk, split, S, lo, tend, att_lo, spn.sink_end);
+    if (tid == kCtl) {
+      int *cnt = a.counters + bk * (1 + a.n_group);
+      const int last =
+          __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == a.n_group - 1;
+      if (last) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      ctl[0] = last;
+    }
+    __syncthreads();
+    if (ctl[0] == 0) return;
+    const Slots gs{a.xgrp + static_cast<size_t>(bk) * a.n_group * kXchSlotWords, a.n_group, split / a.group_size,
+                   true};
+    combine_unit<WAVES, APPEND>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv, gs);
+  } else {
+    combine_unit<WAVES, APPEND>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv,
+                                Slots{xs, a.n_split, split, false});
+  }
 }
 
 }  // namespace
@@ -1132,6 +1322,22 @@ void plan_lut(int batch, int num_kv_heads, int max_seq_len, int *n_split, int *c
 // two KV heads per XCD beat both one (32 CUs of one L2 request the same
 // parameter lines at once) and eight (every L2 fetches every KV head's
 // parameters).
+// One combine reads up to kXchBatch other slots in one round trip; above
+// that the splits are merged in groups of about sqrt(n_split) splits (a power
+// of two, at most 32) first.
+#ifndef NOVA_KV_ONE_LEVEL_MAX
+#define NOVA_KV_ONE_LEVEL_MAX (kXchBatch + 1)
+#endif
+#ifndef NOVA_KV_GROUP_MAX
+#define NOVA_KV_GROUP_MAX 32
+#endif
+int plan_group_size(int n_split) {
+  if (n_split <= NOVA_KV_ONE_LEVEL_MAX) return n_split > 0 ? n_split : 1;
+  int gs = 2;
+  while (gs < NOVA_KV_GROUP_MAX && gs * gs < n_split) gs *= 2;
+  return gs;
+}
+
 int plan_b_chunk(int batch, int num_kv_heads, int n_split) {
   const long long grid = static_cast<long long>(batch) * num_kv_heads * n_split;
   const long long per_xcd = grid / 8 > 0 ? grid / 8 : 1;

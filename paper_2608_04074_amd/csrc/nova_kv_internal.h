@@ -81,12 +81,19 @@ struct DecodeArgs {
   uint64_t *xch;
   uint64_t *xnew;
   uint32_t epoch;   // this call's tag of the exchanged words (nonzero, new for every call)
+  // Two-level combine of the head_dim-128 table kernel: splits in groups of
+  // group_size, n_group groups (n_group = 1: one level, group_size = n_split);
+  // group partials [B*Hkv][n_group][kXchSlotWords]; arrival counters
+  // [B*Hkv][1 + n_group] (the groups' count, then one per group).
+  int group_size, n_group;
+  uint64_t *xgrp;
 };
 
-// Words of one split's slot in the tagged exchange: (m, l) of up to 8 query
-// heads, then their accumulators (8 x 64 or 4 x 128 coordinates).
-// A second block of the same size holds the split's share of the
-// sink-plus-recent band (its own (m, l) and original-domain accumulators).
+// Words of one split's slot in the exchange: per-head statistics of up to 8
+// query heads (16 words), then their accumulators (8 x 64 or 4 x 128
+// coordinates).  A second block of the same size holds the split's share of
+// the sink-plus-recent band (its own statistics and original-domain
+// accumulators).
 constexpr int kXchBandWords = 16 + 512;
 constexpr int kXchSlotWords = 2 * kXchBandWords;
 
@@ -135,7 +142,7 @@ struct DecodePlan {
   int use_lut;      // 1: table-based stage 1 (decode_lut.hip), 0: generic stage 1
   int n_split;
   int chunk;
-  size_t off_cnt, off_qp, off_sinkp, off_ml, off_acc, off_new, off_xch, off_xnew, total;
+  size_t off_cnt, off_qp, off_sinkp, off_ml, off_acc, off_new, off_xch, off_xnew, off_xgrp, total;
 };
 // Splits tile each sequence's attended span (the last `window` tokens, or all).
 // The workspace (off_*, total) is sized for every window and both decode
@@ -146,6 +153,8 @@ DecodePlan plan_decode(int batch, int num_q_heads, int num_kv_heads, int head_di
 
 hipError_t launch_decode(const DecodeArgs &a, int use_lut, hipStream_t stream);
 int plan_b_chunk(int batch, int num_kv_heads, int n_split);
+// Group size of the two-level combine for n_split splits (n_split when one level suffices).
+int plan_group_size(int n_split);
 
 // Table-based decode (head_dim 128 with <= 4, or head_dim 64 with <= 8 query
 // heads per KV head; 16-token-aligned blocks): query transform, split pass and

@@ -354,3 +354,17 @@ def test_many_splits_share_the_band(nk, qwen):
     _band_case(nk, wl, params, P, [16384], 16384, 64, 256, what="qwen B=1 S=16384 (32 splits)")
     _band_case(nk, wl, params, P, [16384], 16384, 64, 256, window=16300, sinks=sinks,
                what="qwen B=1 S=16384 window 16300")
+
+
+def test_split_groups_share_the_band(nk, qwen):
+    """One KV head of one sequence at 65536 tokens: 128 splits, merged in
+    groups before the final combine, each group carrying its splits' band
+    shares (a window cuts the band)."""
+    wl0, params0, _ = qwen
+    wl = wl0.scaled(num_kv_heads=1, num_q_heads=wl0.gqa)
+    params = {k: v[:1] for k, v in params0.items()}
+    P = nk.NovaKVParams.from_arrays(params)
+    sinks = np.random.default_rng(14).standard_normal(wl.num_q_heads).astype(np.float32)
+    _band_case(nk, wl, params, P, [65536], 65536, 64, 256, sinks=sinks, what="one KV head S=65536 (128 splits)")
+    _band_case(nk, wl, params, P, [65536], 65536, 64, 256, window=65000,
+               what="one KV head S=65536 window 65000")

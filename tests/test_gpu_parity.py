@@ -437,6 +437,52 @@ def test_append_decode_matches_oracle(nk, qwen_small, paged, window, use_sink):
                          what=f"append+decode paged={paged} window={window} sink={use_sink}")
 
 
+@pytest.mark.parametrize("fused,window", [(False, 0), (False, 5000), (True, 0), (True, 5000)])
+@pytest.mark.parametrize("hkv", [8, 2])
+def test_many_splits(nk, qwen_small, fused, window, hkv):
+    """Two sequences at a long cap, one of them short.  Eight KV heads at
+    16384 tokens: 16 splits per KV head, one combine.  Two KV heads at 32768
+    tokens: 64 splits, combined in groups of splits first; the short
+    sequence leaves whole groups without tokens."""
+    wl0, params0, _ = qwen_small
+    wl = wl0.scaled(num_kv_heads=hkv, num_q_heads=hkv * wl0.gqa)
+    params = {k: v[:hkv] for k, v in params0.items()}
+    P = upload_params(nk, params)
+    B, cap = 2, (16384 if hkv == 8 else 32768)
+    H, L, G, D = wl.num_kv_heads, wl.groups, wl.gqa, wl.head_dim
+    lens = np.array([cap, 700], dtype=np.int32)
+    ck, cv, kn, vn = _step_inputs(wl, B, cap, lens)
+    q = synth.decode_queries(wl, 0, batch=B)
+    sinks = np.random.default_rng(21).standard_normal(wl.num_q_heads).astype(np.float32)
+    lay = nk.CacheLayout.contiguous(cap)
+    pk, pv = dev(ck, torch.uint8), dev(cv, torch.uint8)
+    args = dict(window=window, sinks=dev(sinks, torch.float32))
+    say(f"many splits hkv={hkv} fused={fused} window={window}")
+    if fused:
+        out = nk.append_decode_attn(P, lay, dev(kn, torch.bfloat16), dev(vn, torch.bfloat16),
+                                    dev(q, torch.bfloat16), pk, pv, dev(lens, torch.int32), cap, **args)
+    else:
+        out = nk.decode_attn(P, lay, dev(q, torch.bfloat16), pk, pv, dev(lens, torch.int32), cap, **args)
+    out = out.cpu().numpy()
+    ref_k, ref_v = ck.copy(), cv.copy()
+    if fused:
+        for b in range(B):
+            p = int(lens[b]) - 1
+            for kv in range(H):
+                okk, _, ovv, _ = ocodec.encode_tokens(kn[b, kv][None], vn[b, kv][None], oatt.head_params(params, kv))
+                ref_k[b, kv, p], ref_v[b, kv, p] = okk[0], ovv[0]
+    lk = lay_kwargs(H, cap, 1)
+    hk, hv = ref_k.reshape(-1), ref_v.reshape(-1)
+    scale = 1 / np.sqrt(D)
+    ref = np.zeros_like(out, dtype=np.float64)
+    for b in range(B):
+        for kv in range(H):
+            ref[b, kv * G:(kv + 1) * G] = oracle_rows(q, hk, hv, params, b, kv, int(lens[b]), scale, lk,
+                                                       window, sinks, G)
+    assert_outputs_close(out.reshape(-1, D), ref.reshape(-1, D),
+                         what=f"many splits hkv={hkv} fused={fused} window={window}")
+
+
 @pytest.mark.parametrize("shape", ["qwen3_8b", "gptoss_pair"])
 def test_append_decode_equals_encode_then_decode(nk, shape):
     """The step in one call stores the same bytes as the one-token encode and gives the decode's output."""
