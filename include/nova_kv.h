@@ -310,6 +310,35 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
                                           float *out, void *workspace, size_t workspace_bytes,
                                           void *hip_stream);
 
+/*
+ * nova_kv_append_decode_attn_noalloc -- nova_kv_append_decode_attn without a
+ * workspace argument, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  It allocates nothing: its scratch is a fixed array of
+ * NOVA_KV_NOALLOC_SCRATCH_BYTES (32 MiB) in the library's device image, one
+ * copy per GPU, held until the process ends.
+ *
+ *   Arguments, results and written bytes as in nova_kv_append_decode_attn.
+ *   A shape whose workspace (nova_kv_decode_workspace_bytes) exceeds the
+ *   array is rejected with NOVA_KV_ERR_WORKSPACE before any HIP call.
+ *   The first call on a device looks the array up for the current device and
+ *   zero-fills it with a kernel on hip_stream, ahead of the step.
+ *   Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ *   (on different streams, or from several threads without ordering) race;
+ *   order them on one stream.
+ * batch == 0 is a valid no-op.
+ */
+#define NOVA_KV_NOALLOC_SCRATCH_BYTES (32u << 20)
+nova_kv_status nova_kv_append_decode_attn_noalloc(const nova_kv_params *p, const nova_kv_layout *layout,
+                                                  const void *k_new, const void *v_new, nova_kv_dtype new_dtype,
+                                                  const void *q, nova_kv_dtype q_dtype,
+                                                  int32_t batch, int32_t num_q_heads,
+                                                  uint8_t *k_codes, uint8_t *v_codes, uint16_t *k_scales,
+                                                  uint16_t *v_sq, const nova_kv_band *band,
+                                                  const int32_t *seq_lens, int32_t max_seq_len,
+                                                  int32_t window, const float *sinks, float softmax_scale,
+                                                  float *out, void *hip_stream);
+
 /* Static description of a status code. */
 const char *nova_kv_status_string(nova_kv_status s);
 

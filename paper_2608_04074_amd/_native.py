@@ -30,6 +30,7 @@ EXPORTED = (
     "nova_kv_decode_workspace_bytes",
     "nova_kv_decode_attn",
     "nova_kv_append_decode_attn",
+    "nova_kv_append_decode_attn_noalloc",
     "nova_kv_status_string",
     "nova_kv_last_error",
 )
@@ -110,6 +111,11 @@ def lib() -> ctypes.CDLL:
         L.nova_kv_append_decode_attn.argtypes = [P(Params), P(Layout), vp, vp, ctypes.c_int, vp,
                                                  ctypes.c_int, i32, i32, vp, vp, vp, vp, P(Band), vp,
                                                  i32, i32, vp, ctypes.c_float, vp, vp, ctypes.c_size_t, vp]
+        L.nova_kv_append_decode_attn_noalloc.restype = ctypes.c_int
+        # the arguments of nova_kv_append_decode_attn without (workspace, bytes)
+        L.nova_kv_append_decode_attn_noalloc.argtypes = [P(Params), P(Layout), vp, vp, ctypes.c_int, vp,
+                                                         ctypes.c_int, i32, i32, vp, vp, vp, vp, P(Band), vp,
+                                                         i32, i32, vp, ctypes.c_float, vp, vp]
         L.nova_kv_status_string.restype = ctypes.c_char_p
         L.nova_kv_status_string.argtypes = [ctypes.c_int]
         L.nova_kv_last_error.restype = ctypes.c_char_p

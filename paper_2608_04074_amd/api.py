@@ -16,7 +16,7 @@ import torch
 from . import _native as nat
 
 __all__ = ["NovaKVParams", "CacheLayout", "Band", "band_shape", "encode", "decode_attn", "append_decode_attn",
-           "decode_workspace_bytes", "code_pool_shape", "scale_pool_shape", "prepare_encode",
+           "append_decode_attn_noalloc", "NOALLOC_SCRATCH_BYTES", "decode_workspace_bytes", "code_pool_shape", "scale_pool_shape", "prepare_encode",
            "prepare_decode", "prepare_append_decode"]
 
 
@@ -305,7 +305,8 @@ def _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_l
     if sinks is not None:
         _require(sinks, "sinks", (torch.float32,), hq)
     _require(out, "out", (torch.float32,), b * hq * d)
-    _require(workspace, "workspace", (torch.uint8,))
+    if workspace is not None:
+        _require(workspace, "workspace", (torch.uint8,))
     ks = _scales_ptr(params, k_scales, k_codes)
     vp = ctypes.c_void_p
     return (ctypes.byref(params.c), ctypes.byref(layout.c), vp(k_new.data_ptr()), vp(v_new.data_ptr()),
@@ -315,8 +316,8 @@ def _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_l
             ctypes.c_int32(max_seq_len),
             ctypes.c_int32(window),
             vp(sinks.data_ptr() if sinks is not None else None), ctypes.c_float(softmax_scale),
-            vp(out.data_ptr()), vp(workspace.data_ptr()), ctypes.c_size_t(workspace.numel()),
-            vp(_stream_ptr(stream)))
+            vp(out.data_ptr()), vp(workspace.data_ptr() if workspace is not None else None),
+            ctypes.c_size_t(workspace.numel() if workspace is not None else 0), vp(_stream_ptr(stream)))
 
 
 def append_decode_attn(params: NovaKVParams, layout: CacheLayout, k_new: torch.Tensor, v_new: torch.Tensor,
@@ -340,6 +341,27 @@ def append_decode_attn(params: NovaKVParams, layout: CacheLayout, k_new: torch.T
     args = _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
                                workspace, window, sinks, softmax_scale, stream, k_scales, band, v_sq)
     nat.check(nat.lib().nova_kv_append_decode_attn(*args))
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def append_decode_attn_noalloc(params: NovaKVParams, layout: CacheLayout, k_new: torch.Tensor,
+                               v_new: torch.Tensor, q: torch.Tensor, k_codes: torch.Tensor, v_codes: torch.Tensor,
+                               seq_lens: torch.Tensor, max_seq_len: int, out: torch.Tensor, window: int = 0,
+                               sinks: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
+                               stream: Optional[torch.cuda.Stream] = None,
+                               k_scales: Optional[torch.Tensor] = None, band: Optional[Band] = None,
+                               v_sq: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """nova_kv_append_decode_attn_noalloc: the step of append_decode_attn with
+    the library's fixed per-GPU scratch (NOALLOC_SCRATCH_BYTES) instead of a
+    workspace; out is required, nothing is allocated.  Calls that overlap on
+    one GPU race."""
+    args = _append_decode_args(params, layout, k_new, v_new, q, k_codes, v_codes, seq_lens, max_seq_len, out,
+                               None, window, sinks, softmax_scale, stream, k_scales, band, v_sq)
+    # the same arguments without (workspace, bytes)
+    nat.check(nat.lib().nova_kv_append_decode_attn_noalloc(*(args[:20] + args[22:])))
     return out
 
 

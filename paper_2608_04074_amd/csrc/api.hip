@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <atomic>
+#include <mutex>
 #include <string>
 
 #include "../../include/nova_kv.h"
@@ -117,6 +118,51 @@ novakv::CacheLayout to_layout(const nova_kv_layout *lay) {
 
 }  // namespace
 
+namespace {
+
+// ---- the allocation-free step: a fixed scratch array per GPU
+//
+// The array's name is a host-side stand-in: host code uses the device address
+// that hipGetSymbolAddress returns for the current device (each GPU holds its
+// own copy), never the name itself.
+constexpr size_t kStaticScratchBytes = NOVA_KV_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+__global__ void fill_zero(uint4 *p, size_t n) {
+  for (size_t i = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x; i < n;
+       i += static_cast<size_t>(gridDim.x) * blockDim.x)
+    p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+// Address of the current device's scratch array; on the first call on a
+// device it is looked up and zero-filled by a kernel on `stream` (ordered
+// before the caller's launches on that stream).
+nova_kv_status static_scratch(hipStream_t stream, void **out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(NOVA_KV_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(NOVA_KV_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    fill_zero<<<1024, 256, 0, stream>>>(static_cast<uint4 *>(ptr), kStaticScratchBytes / sizeof(uint4));
+    e = hipGetLastError();
+    if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "scratch clear: %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return NOVA_KV_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 const char *nova_kv_status_string(nova_kv_status s) {
@@ -201,7 +247,8 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
                               const nova_kv_band *band, const int32_t *seq_lens, int32_t max_seq_len,
                               int32_t window, const float *sinks, float softmax_scale, float *out,
                               void *workspace, size_t workspace_bytes, bool need_encode,
-                              novakv::DecodeArgs &a, novakv::DecodePlan &plan) {
+                              novakv::DecodeArgs &a, novakv::DecodePlan &plan,
+                              bool static_ws = false, hipStream_t stream = nullptr) {
   nova_kv_status st = check_params(p, need_encode, true);
   if (st != NOVA_KV_OK) return st;
   if ((st = check_layout(layout)) != NOVA_KV_OK) return st;
@@ -231,6 +278,15 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   const bool sq = (p->flags & NOVA_KV_SQ_VALUES) != 0;
   plan = novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len, layout->block_size,
                              window, sq && p->head_dim != 128);
+  if (static_ws) {  // the allocation-free step: the GPU's fixed scratch array (the last check)
+    if (plan.total > kStaticScratchBytes)
+      return fail(NOVA_KV_ERR_WORKSPACE,
+                  "this shape needs %zu bytes of scratch; the allocation-free step holds %zu "
+                  "(call nova_kv_append_decode_attn with a workspace)",
+                  plan.total, kStaticScratchBytes);
+    if ((st = static_scratch(stream, &workspace)) != NOVA_KV_OK) return st;
+    workspace_bytes = kStaticScratchBytes;
+  }
   if (!workspace || workspace_bytes < plan.total)
     return fail(NOVA_KV_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", plan.total,
                 workspace ? workspace_bytes : static_cast<size_t>(0));
@@ -312,25 +368,28 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
   return ok();
 }
 
-nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
-                                          const void *k_new, const void *v_new, nova_kv_dtype new_dtype,
-                                          const void *q, nova_kv_dtype q_dtype, int32_t batch,
-                                          int32_t num_q_heads, uint8_t *k_codes, uint8_t *v_codes,
-                                          uint16_t *k_scales, uint16_t *v_sq, const nova_kv_band *band,
-                                          const int32_t *seq_lens, int32_t max_seq_len,
-                                          int32_t window,
-                                          const float *sinks, float softmax_scale, float *out,
-                                          void *workspace, size_t workspace_bytes, void *hip_stream) {
+}  // extern "C"
+
+namespace {
+
+// The step of nova_kv_append_decode_attn, with the caller's workspace or
+// (static_ws) the GPU's fixed scratch array.
+nova_kv_status append_step(const nova_kv_params *p, const nova_kv_layout *layout, const void *k_new,
+                           const void *v_new, nova_kv_dtype new_dtype, const void *q, nova_kv_dtype q_dtype,
+                           int32_t batch, int32_t num_q_heads, uint8_t *k_codes, uint8_t *v_codes,
+                           uint16_t *k_scales, uint16_t *v_sq, const nova_kv_band *band, const int32_t *seq_lens,
+                           int32_t max_seq_len, int32_t window, const float *sinks, float softmax_scale, float *out,
+                           void *workspace, size_t workspace_bytes, bool static_ws, void *hip_stream) {
   if (new_dtype != NOVA_KV_F32 && new_dtype != NOVA_KV_BF16)
     return fail(NOVA_KV_ERR_INVALID_ARG, "new_dtype must be NOVA_KV_F32 or NOVA_KV_BF16");
+  if (batch > 0 && (!k_new || !v_new)) return fail(NOVA_KV_ERR_INVALID_ARG, "k_new or v_new is NULL");
+  const hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   novakv::DecodeArgs a;
   novakv::DecodePlan plan;
   nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales,
                                      v_sq, band, seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace,
-                                     workspace_bytes, true, a, plan);
+                                     workspace_bytes, true, a, plan, static_ws, stream);
   if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
-  if (!k_new || !v_new) return fail(NOVA_KV_ERR_INVALID_ARG, "k_new or v_new is NULL");
-  const hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   hipError_t e;
   if (plan.use_lut && p->head_dim == 128 && !(p->flags & (NOVA_KV_KEY_SCALE | NOVA_KV_SQ_VALUES)) && !band) {
     // one launch: the table kernel encodes the new token and attends to it
@@ -376,6 +435,37 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
   }
   if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "append-decode launch: %s", hipGetErrorString(e));
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,
+                                          const void *k_new, const void *v_new, nova_kv_dtype new_dtype,
+                                          const void *q, nova_kv_dtype q_dtype, int32_t batch,
+                                          int32_t num_q_heads, uint8_t *k_codes, uint8_t *v_codes,
+                                          uint16_t *k_scales, uint16_t *v_sq, const nova_kv_band *band,
+                                          const int32_t *seq_lens, int32_t max_seq_len,
+                                          int32_t window,
+                                          const float *sinks, float softmax_scale, float *out,
+                                          void *workspace, size_t workspace_bytes, void *hip_stream) {
+  return append_step(p, layout, k_new, v_new, new_dtype, q, q_dtype, batch, num_q_heads, k_codes, v_codes,
+                     k_scales, v_sq, band, seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace,
+                     workspace_bytes, false, hip_stream);
+}
+
+nova_kv_status nova_kv_append_decode_attn_noalloc(const nova_kv_params *p, const nova_kv_layout *layout,
+                                                  const void *k_new, const void *v_new, nova_kv_dtype new_dtype,
+                                                  const void *q, nova_kv_dtype q_dtype, int32_t batch,
+                                                  int32_t num_q_heads, uint8_t *k_codes, uint8_t *v_codes,
+                                                  uint16_t *k_scales, uint16_t *v_sq, const nova_kv_band *band,
+                                                  const int32_t *seq_lens, int32_t max_seq_len, int32_t window,
+                                                  const float *sinks, float softmax_scale, float *out,
+                                                  void *hip_stream) {
+  return append_step(p, layout, k_new, v_new, new_dtype, q, q_dtype, batch, num_q_heads, k_codes, v_codes,
+                     k_scales, v_sq, band, seq_lens, max_seq_len, window, sinks, softmax_scale, out, nullptr, 0,
+                     true, hip_stream);
 }
 
 }  // extern "C"

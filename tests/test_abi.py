@@ -12,6 +12,8 @@ import pytest
 
 from paper_2608_04074_amd import _native as nat
 
+NOALLOC_BYTES = 32 << 20   # the allocation-free step's fixed scratch array
+
 HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "nova_kv.h")
 
 
@@ -222,3 +224,31 @@ def test_scalar_value_arm_needs_its_pool(call):
         assert call(p, _layout(), vsq=0xC000) == nat.NOVA_KV_ERR_WORKSPACE
     # the plain format still needs cb_v
     assert call(_params(cb_v=None), _layout()) == nat.NOVA_KV_ERR_INVALID_ARG
+
+
+def _append_noalloc(p, lay, **kw):
+    a = dict(kn=0x7000, vn=0x7800, new_dtype=nat.NOVA_KV_BF16, q=0x7400, q_dtype=nat.NOVA_KV_BF16,
+             batch=2, hq=32, k=0x8000, v=0x9000, ks=None, vsq=None, band=None, seq=0xA000, max_seq=4096,
+             window=0, sinks=None, scale=0.0, out=0xB000)
+    a.update(kw)
+    return nat.lib().nova_kv_append_decode_attn_noalloc(
+        ctypes.byref(p), ctypes.byref(lay), a["kn"], a["vn"], a["new_dtype"], a["q"], a["q_dtype"],
+        a["batch"], a["hq"], a["k"], a["v"], a["ks"], a["vsq"], _band(a["band"]), a["seq"], a["max_seq"],
+        a["window"], a["sinks"], a["scale"], a["out"], None)
+
+
+def test_noalloc_step_checks_before_any_hip_call():
+    """The allocation-free step validates like the step with a workspace, and
+    rejects a shape whose scratch exceeds its fixed array, all on the host."""
+    lib = nat.lib()
+    assert _append_noalloc(_params(), _layout(), new_dtype=9) == nat.NOVA_KV_ERR_INVALID_ARG
+    assert _append_noalloc(_params(), _layout(), q=None) == nat.NOVA_KV_ERR_INVALID_ARG
+    assert _append_noalloc(_params(), _layout(), kn=None) == nat.NOVA_KV_ERR_INVALID_ARG
+    assert _append_noalloc(_params(), _layout(), batch=0, q=None, out=None) == nat.NOVA_KV_OK
+    # 64 sequences of 32768 tokens need more scratch than the array holds
+    big = _layout(block_size=32768)
+    need = lib.nova_kv_decode_workspace_bytes(ctypes.byref(_params()), 64, 32, 32768)
+    assert need > NOALLOC_BYTES
+    assert _append_noalloc(_params(), big, batch=64, max_seq=32768) == nat.NOVA_KV_ERR_WORKSPACE
+    msg = lib.nova_kv_last_error()
+    assert b"allocation-free" in msg and str(NOALLOC_BYTES).encode() in msg
