@@ -339,6 +339,44 @@ nova_kv_status nova_kv_append_decode_attn_noalloc(const nova_kv_params *p, const
                                                   int32_t window, const float *sinks, float softmax_scale,
                                                   float *out, void *hip_stream);
 
+/*
+ * nova_kv_check_metadata -- host-side check of a call's metadata, the
+ * preconditions the kernels take on trust.  All pointers are HOST arrays
+ * here (layout->block_table included).  Nothing is launched; usable without
+ * a GPU.
+ *
+ *   num_blocks  physical blocks of the pools (> 0), or <= 0 if unknown (then
+ *               block-table entries are only checked to be >= 0).
+ *   seq_lens    [batch] or NULL: sequences read positions [0, seq_lens[b]);
+ *               requires 0 <= seq_lens[b] <= max_seq_len <= capacity.
+ *   start_pos   [batch] or NULL: nova_kv_encode writes positions
+ *               [start_pos[b], start_pos[b] + n_new), all inside
+ *               [0, block_size * blocks_per_seq).  With start_pos NULL,
+ *               seq_lens given and n_new == 1, the write of
+ *               nova_kv_append_decode_attn: position seq_lens[b] - 1 (none
+ *               for an empty sequence).
+ * Every logical block holding a read or written position must map to a
+ * physical block in [0, num_blocks); no two sequences may write the same
+ * row; no sequence may read a physical block that another one writes in the
+ * same call.  Returns NOVA_KV_ERR_INVALID_ARG with the first offending entry
+ * in nova_kv_last_error(), else NOVA_KV_OK.
+ */
+nova_kv_status nova_kv_check_metadata(const nova_kv_layout *layout, int32_t num_blocks, int32_t batch,
+                                      const int32_t *seq_lens, int32_t max_seq_len, const int32_t *start_pos,
+                                      int32_t n_new);
+
+/*
+ * nova_kv_set_debug -- debug mode of the entry points (process-wide; also on
+ * from the start when the environment variable NOVA_KV_DEBUG is a nonzero
+ * number).  When on, nova_kv_encode, nova_kv_decode_attn and
+ * nova_kv_append_decode_attn (and its allocation-free variant) wait for their
+ * stream, copy seq_lens / start_pos / the block table to the host and run
+ * nova_kv_check_metadata (with num_blocks as given here, <= 0: unknown)
+ * before launching; a failing check launches nothing.  This synchronizes,
+ * so it is for debugging and not for graph capture.
+ */
+void nova_kv_set_debug(int32_t on, int32_t num_blocks);
+
 /* Static description of a status code. */
 const char *nova_kv_status_string(nova_kv_status s);
 

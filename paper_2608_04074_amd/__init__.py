@@ -5,7 +5,7 @@ The compute lives in ``libnovakv.so`` (hand-written HIP, C ABI in
 """
 
 from .api import (NOALLOC_SCRATCH_BYTES, Band, CacheLayout, NovaKVParams, append_decode_attn,  # noqa: F401
-                  append_decode_attn_noalloc, band_shape,
+                  append_decode_attn_noalloc, band_shape, check_metadata, set_debug,
                   code_pool_shape, decode_attn, decode_workspace_bytes, encode, prepare_append_decode,
                   prepare_decode, prepare_encode, scale_pool_shape)
 from ._native import NovaKVError  # noqa: F401

@@ -31,6 +31,8 @@ EXPORTED = (
     "nova_kv_decode_attn",
     "nova_kv_append_decode_attn",
     "nova_kv_append_decode_attn_noalloc",
+    "nova_kv_check_metadata",
+    "nova_kv_set_debug",
     "nova_kv_status_string",
     "nova_kv_last_error",
 )
@@ -116,6 +118,11 @@ def lib() -> ctypes.CDLL:
         L.nova_kv_append_decode_attn_noalloc.argtypes = [P(Params), P(Layout), vp, vp, ctypes.c_int, vp,
                                                          ctypes.c_int, i32, i32, vp, vp, vp, vp, P(Band), vp,
                                                          i32, i32, vp, ctypes.c_float, vp, vp]
+        L.nova_kv_check_metadata.restype = ctypes.c_int
+        # (layout with a host block table, num_blocks, batch, seq_lens, max_seq_len, start_pos, n_new)
+        L.nova_kv_check_metadata.argtypes = [P(Layout), i32, i32, vp, i32, vp, i32]
+        L.nova_kv_set_debug.restype = None
+        L.nova_kv_set_debug.argtypes = [i32, i32]
         L.nova_kv_status_string.restype = ctypes.c_char_p
         L.nova_kv_status_string.argtypes = [ctypes.c_int]
         L.nova_kv_last_error.restype = ctypes.c_char_p

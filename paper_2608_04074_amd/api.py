@@ -16,7 +16,8 @@ import torch
 from . import _native as nat
 
 __all__ = ["NovaKVParams", "CacheLayout", "Band", "band_shape", "encode", "decode_attn", "append_decode_attn",
-           "append_decode_attn_noalloc", "NOALLOC_SCRATCH_BYTES", "decode_workspace_bytes", "code_pool_shape", "scale_pool_shape", "prepare_encode",
+           "append_decode_attn_noalloc", "NOALLOC_SCRATCH_BYTES", "check_metadata", "set_debug",
+           "decode_workspace_bytes", "code_pool_shape", "scale_pool_shape", "prepare_encode",
            "prepare_decode", "prepare_append_decode"]
 
 
@@ -342,6 +343,34 @@ def append_decode_attn(params: NovaKVParams, layout: CacheLayout, k_new: torch.T
                                workspace, window, sinks, softmax_scale, stream, k_scales, band, v_sq)
     nat.check(nat.lib().nova_kv_append_decode_attn(*args))
     return out
+
+
+def check_metadata(block_size: int, blocks_per_seq: int, block_table=None, num_blocks: int = 0,
+                   seq_lens=None, max_seq_len: int = 0, start_pos=None, n_new: int = 0) -> None:
+    """nova_kv_check_metadata on host arrays (numpy or CPU tensors, int32):
+    raises NovaKVError naming the first offending entry."""
+    import numpy as np
+
+    def host(x):
+        return None if x is None else np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+
+    bt, sl, sp = host(block_table), host(seq_lens), host(start_pos)
+    batch = len(sl) if sl is not None else (len(sp) if sp is not None else 0)
+    for name, x in (("seq_lens", sl), ("start_pos", sp)):
+        if x is not None and len(x) != batch:
+            raise ValueError(f"{name} must have one entry per sequence")
+    if bt is not None and bt.size < batch * blocks_per_seq:
+        raise ValueError("block_table must be [batch][blocks_per_seq]")
+    ptr = lambda x: None if x is None else x.ctypes.data  # noqa: E731
+    lay = nat.Layout(block_size, blocks_per_seq, ptr(bt))
+    nat.check(nat.lib().nova_kv_check_metadata(ctypes.byref(lay), num_blocks, batch, ptr(sl), max_seq_len,
+                                               ptr(sp), n_new))
+
+
+def set_debug(on: bool, num_blocks: int = 0) -> None:
+    """nova_kv_set_debug: entry points check their metadata on the host before
+    launching (synchronizing; num_blocks <= 0: unknown pool size)."""
+    nat.lib().nova_kv_set_debug(1 if on else 0, num_blocks)
 
 
 NOALLOC_SCRATCH_BYTES = 32 << 20

@@ -12,7 +12,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libnovakv.so")
-SOURCES = ["api.hip", "decode.hip", "decode_lut.hip", "decode_lut64.hip", "encode.hip"]
+SOURCES = ["api.hip", "decode.hip", "decode_lut.hip", "decode_lut64.hip", "encode.hip", "host_checks.cpp"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -8,109 +8,15 @@
 #include <atomic>
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "../../include/nova_kv.h"
+#include "host_checks.h"
 #include "nova_kv_internal.h"
 
+using namespace novakv::host;
+
 namespace {
-
-thread_local std::string g_last_error;
-
-nova_kv_status fail(nova_kv_status s, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
-
-nova_kv_status fail(nova_kv_status s, const char *fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
-  va_end(ap);
-  g_last_error = buf;
-  return s;
-}
-
-nova_kv_status ok() {
-  g_last_error.clear();
-  return NOVA_KV_OK;
-}
-
-bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
-
-// Tag of the split exchange of the next decode call: every call gets a new
-// nonzero number (the workspace's words of one call are never taken for
-// another's; zero marks a never-written word).
-uint32_t next_epoch() {
-  static std::atomic<uint32_t> counter{0};
-  uint32_t e = counter.fetch_add(1, std::memory_order_relaxed) + 1;
-  while (e == 0) e = counter.fetch_add(1, std::memory_order_relaxed) + 1;
-  return e;
-}
-
-nova_kv_status check_params(const nova_kv_params *p, bool need_encode, bool need_decode) {
-  if (!p) return fail(NOVA_KV_ERR_INVALID_ARG, "params is NULL");
-  if (p->num_kv_heads <= 0) return fail(NOVA_KV_ERR_INVALID_ARG, "num_kv_heads must be > 0");
-  if (p->group_dim <= 0 || p->head_dim <= 0 || p->head_dim % p->group_dim != 0)
-    return fail(NOVA_KV_ERR_INVALID_ARG, "head_dim (%d) must be a positive multiple of group_dim (%d)",
-                p->head_dim, p->group_dim);
-  if (p->codebook_size <= 0) return fail(NOVA_KV_ERR_INVALID_ARG, "codebook_size must be > 0");
-  if (p->group_dim != novakv::kGroupDim)
-    return fail(NOVA_KV_ERR_UNSUPPORTED, "group_dim %d unsupported (only 4)", p->group_dim);
-  if (p->codebook_size != novakv::kCodebookSize)
-    return fail(NOVA_KV_ERR_UNSUPPORTED, "codebook_size %d unsupported (only 256)", p->codebook_size);
-  if (p->head_dim != 64 && p->head_dim != 128)
-    return fail(NOVA_KV_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", p->head_dim);
-  if ((p->flags & ~(NOVA_KV_KEY_SCALE | NOVA_KV_FP8_CODEBOOKS | NOVA_KV_SQ_VALUES)) != 0)
-    return fail(NOVA_KV_ERR_UNSUPPORTED,
-                "flags 0x%x unsupported (NOVA_KV_KEY_SCALE, NOVA_KV_FP8_CODEBOOKS, NOVA_KV_SQ_VALUES)", p->flags);
-  const bool sq = (p->flags & NOVA_KV_SQ_VALUES) != 0;  // cb_v unused
-  if (!p->kbar || !p->cb_k || (!sq && !p->cb_v)) return fail(NOVA_KV_ERR_INVALID_ARG, "kbar/cb_k/cb_v is NULL");
-  if (!aligned(p->cb_k, 16) || (!sq && !aligned(p->cb_v, 16)))
-    return fail(NOVA_KV_ERR_INVALID_ARG, "codebooks must be 16-byte aligned");
-  if (need_encode && (!p->t_k || !p->t_v)) return fail(NOVA_KV_ERR_INVALID_ARG, "t_k/t_v is NULL");
-  if (need_decode && (!p->t_k_inv_t || !p->t_v))
-    return fail(NOVA_KV_ERR_INVALID_ARG, "t_k_inv_t/t_v is NULL");
-  if (!aligned(p->kbar, 16) || !aligned(p->t_v, 16) || (need_encode && !aligned(p->t_k, 16)) ||
-      (need_decode && !aligned(p->t_k_inv_t, 16)))
-    return fail(NOVA_KV_ERR_INVALID_ARG, "kbar and transforms must be 16-byte aligned");
-  return NOVA_KV_OK;
-}
-
-nova_kv_status check_layout(const nova_kv_layout *lay) {
-  if (!lay) return fail(NOVA_KV_ERR_INVALID_ARG, "layout is NULL");
-  if (lay->block_size <= 0 || lay->blocks_per_seq <= 0)
-    return fail(NOVA_KV_ERR_INVALID_ARG, "block_size and blocks_per_seq must be > 0");
-  if (static_cast<long long>(lay->block_size) * lay->blocks_per_seq > (1LL << 30))
-    return fail(NOVA_KV_ERR_INVALID_ARG, "per-sequence capacity too large");
-  return NOVA_KV_OK;
-}
-
-// The scale pool of the key-scale format (ignored otherwise).
-nova_kv_status check_scales(const nova_kv_params *p, const void *k_scales) {
-  if (!(p->flags & NOVA_KV_KEY_SCALE)) return NOVA_KV_OK;
-  if (!k_scales) return fail(NOVA_KV_ERR_INVALID_ARG, "k_scales is NULL in the key-scale format");
-  if (!aligned(k_scales, 2)) return fail(NOVA_KV_ERR_INVALID_ARG, "k_scales must be 2-byte aligned");
-  return NOVA_KV_OK;
-}
-
-// The sink-plus-recent band (NULL: none).
-nova_kv_status check_band(const nova_kv_band *band) {
-  if (!band) return NOVA_KV_OK;
-  if (band->n_sink < 0 || band->n_rec < 0) return fail(NOVA_KV_ERR_INVALID_ARG, "band sizes must be >= 0");
-  const long long nb = static_cast<long long>(band->n_sink) + band->n_rec;
-  if (nb < 1 || nb > NOVA_KV_MAX_BAND)
-    return fail(NOVA_KV_ERR_INVALID_ARG, "band of %lld positions (1 .. %d)", nb, NOVA_KV_MAX_BAND);
-  if (!band->k || !band->v) return fail(NOVA_KV_ERR_INVALID_ARG, "band k or v is NULL");
-  if (!aligned(band->k, 16) || !aligned(band->v, 16))
-    return fail(NOVA_KV_ERR_INVALID_ARG, "band buffers must be 16-byte aligned");
-  return NOVA_KV_OK;
-}
-
-// The (scale, offset) pool of the scalar value arm (ignored otherwise).
-nova_kv_status check_sq(const nova_kv_params *p, const void *v_sq) {
-  if (!(p->flags & NOVA_KV_SQ_VALUES)) return NOVA_KV_OK;
-  if (!v_sq) return fail(NOVA_KV_ERR_INVALID_ARG, "v_sq is NULL in the scalar value format");
-  if (!aligned(v_sq, 4)) return fail(NOVA_KV_ERR_INVALID_ARG, "v_sq must be 4-byte aligned");
-  return NOVA_KV_OK;
-}
 
 novakv::CacheLayout to_layout(const nova_kv_layout *lay) {
   return novakv::CacheLayout{lay->block_size, lay->blocks_per_seq, lay->block_table};
@@ -119,6 +25,32 @@ novakv::CacheLayout to_layout(const nova_kv_layout *lay) {
 }  // namespace
 
 namespace {
+
+// ---- debug mode: the metadata copied to the host and checked before a launch
+nova_kv_status debug_check(const nova_kv_layout *lay, int32_t batch, const int32_t *seq_lens, int32_t max_seq_len,
+                           const int32_t *start_pos, int32_t n_new, hipStream_t stream) {
+  if (!debug_enabled() || batch <= 0) return NOVA_KV_OK;
+  hipError_t e = hipStreamSynchronize(stream);  // the metadata may be written by earlier work on the stream
+  auto to_host = [&](const int32_t *d, size_t n, std::vector<int32_t> &h) {
+    h.resize(n);
+    if (e == hipSuccess) e = hipMemcpy(h.data(), d, n * sizeof(int32_t), hipMemcpyDeviceToHost);
+  };
+  std::vector<int32_t> lens, starts, table;
+  if (seq_lens) to_host(seq_lens, batch, lens);
+  if (start_pos) to_host(start_pos, batch, starts);
+  if (lay->block_table) to_host(lay->block_table, static_cast<size_t>(batch) * lay->blocks_per_seq, table);
+  if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "debug mode: metadata copy: %s", hipGetErrorString(e));
+  nova_kv_layout hl = *lay;
+  hl.block_table = lay->block_table ? table.data() : nullptr;
+  const nova_kv_status st = check_metadata(&hl, debug_num_blocks(), batch, seq_lens ? lens.data() : nullptr,
+                                           max_seq_len, start_pos ? starts.data() : nullptr, n_new);
+  if (st != NOVA_KV_OK) {
+    std::string d = "debug mode: ";
+    d += nova_kv_last_error();
+    return fail(st, "%s", d.c_str());
+  }
+  return NOVA_KV_OK;
+}
 
 // ---- the allocation-free step: a fixed scratch array per GPU
 //
@@ -165,19 +97,6 @@ nova_kv_status static_scratch(hipStream_t stream, void **out) {
 
 extern "C" {
 
-const char *nova_kv_status_string(nova_kv_status s) {
-  switch (s) {
-    case NOVA_KV_OK: return "ok";
-    case NOVA_KV_ERR_INVALID_ARG: return "invalid argument";
-    case NOVA_KV_ERR_UNSUPPORTED: return "unsupported configuration";
-    case NOVA_KV_ERR_WORKSPACE: return "workspace missing or too small";
-    case NOVA_KV_ERR_HIP: return "HIP runtime error";
-  }
-  return "unknown status";
-}
-
-const char *nova_kv_last_error(void) { return g_last_error.c_str(); }
-
 nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *layout,
                               const void *k, const void *v, nova_kv_dtype in_dtype,
                               int32_t batch, int32_t n_new, const int32_t *start_pos,
@@ -198,6 +117,9 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
   if ((st = check_band(band)) != NOVA_KV_OK) return st;
   if (!k || !v || !start_pos || !k_codes || !v_codes)
     return fail(NOVA_KV_ERR_INVALID_ARG, "k, v, start_pos, k_codes or v_codes is NULL");
+  if ((st = debug_check(layout, batch, nullptr, 0, start_pos, n_new, static_cast<hipStream_t>(hip_stream))) !=
+      NOVA_KV_OK)
+    return st;
 
   novakv::EncodeArgs a{};
   a.batch = batch;
@@ -278,6 +200,8 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   const bool sq = (p->flags & NOVA_KV_SQ_VALUES) != 0;
   plan = novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len, layout->block_size,
                              window, sq && p->head_dim != 128);
+  if ((st = debug_check(layout, batch, seq_lens, max_seq_len, nullptr, need_encode ? 1 : 0, stream)) != NOVA_KV_OK)
+    return st;
   if (static_ws) {  // the allocation-free step: the GPU's fixed scratch array (the last check)
     if (plan.total > kStaticScratchBytes)
       return fail(NOVA_KV_ERR_WORKSPACE,
@@ -361,7 +285,7 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
   novakv::DecodePlan plan;
   nova_kv_status st = prepare_decode(p, layout, q, q_dtype, batch, num_q_heads, k_codes, v_codes, k_scales, v_sq,
                                      band, seq_lens, max_seq_len, window, sinks, softmax_scale, out, workspace, workspace_bytes,
-                                     false, a, plan);
+                                     false, a, plan, false, static_cast<hipStream_t>(hip_stream));
   if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
   hipError_t e = novakv::launch_decode(a, plan.use_lut, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return fail(NOVA_KV_ERR_HIP, "decode launch: %s", hipGetErrorString(e));

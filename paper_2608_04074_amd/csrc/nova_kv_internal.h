@@ -5,11 +5,9 @@
 #include <stddef.h>
 #include <stdint.h>
 
-namespace novakv {
+#include "host_checks.h"
 
-constexpr int kGroupDim = 4;        // g: coefficients per codebook group
-constexpr int kCodebookSize = 256;  // K: codewords per group (8-bit codes)
-constexpr int kMaxGqa = 8;          // query heads per KV head handled by the kernels
+namespace novakv {
 
 struct CacheLayout {
   int block_size;
