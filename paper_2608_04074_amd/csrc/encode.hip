@@ -154,36 +154,61 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   const void *src = side == 0 ? a.k : a.v;
   uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
 
-  for (int i = tid; i < TT * D; i += 256) {
-    const int t = i / D, d = i % D;
-    double x = 0.0;
-    if (t < nt) {
-      const size_t idx = ((static_cast<size_t>(b) * a.n_new + n0 + t) * a.num_kv_heads + kv) * D + d;
-      x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
-                    : static_cast<double>(static_cast<const float *>(src)[idx]);
-      if (side == 0) x -= static_cast<double>(a.kbar[kv * D + d]);
-      if (a.band_k) {
-        const int p0 = a.start_pos[b] + a.start_offset;
-        store_band(a, side, b, kv, p0 + n0 + t, p0 + a.n_new, d, input_bf16_bits(a, src, idx));
+  // ---- transform operands: wave w computes output tiles w*OT/4 .. of both
+  // token tiles; its B operands (rows 4ks + q, columns of its tiles, of T)
+  // are requested first, so that their latency passes while the inputs are
+  // staged
+  const int m = lane & 15, q = lane >> 4;
+  constexpr int OPW = OT / 4;
+  float tr[KS][OPW];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+    for (int j = 0; j < OPW; ++j) tr[ks][j] = tm[(4 * ks + q) * D + 16 * (wave * OPW + j) + m];
+
+  // inputs (minus k_bar for keys) to LDS in fp64: thread tid stages
+  // coordinate tid mod D of tokens tid / D + k * (256 / D)
+  static_assert(256 % D == 0, "a thread stages one coordinate");
+  {
+    constexpr int TP = 256 / D, NK = TT / TP;
+    const int d = tid % D, t0 = tid / D;
+    const double kb = side == 0 ? static_cast<double>(a.kbar[kv * D + d]) : 0.0;
+    const size_t row = static_cast<size_t>(a.num_kv_heads) * D;
+    const size_t idx0 = ((static_cast<size_t>(b) * a.n_new + n0 + t0) * a.num_kv_heads + kv) * D + d;
+    double x[NK];
+#pragma unroll
+    for (int k = 0; k < NK; ++k) {
+      const int t = t0 + k * TP;
+      const size_t idx = idx0 + static_cast<size_t>(k * TP) * row;
+      x[k] = 0.0;
+      if (t < nt)
+        x[k] = (a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
+                          : static_cast<double>(static_cast<const float *>(src)[idx])) - kb;
+    }
+#pragma unroll
+    for (int k = 0; k < NK; ++k) xs[(t0 + k * TP) * RS + d] = x[k];
+    if (a.band_k) {
+      const int p0 = a.start_pos[b] + a.start_offset;
+      for (int k = 0; k < NK; ++k) {
+        const int t = t0 + k * TP;
+        if (t < nt)
+          store_band(a, side, b, kv, p0 + n0 + t, p0 + a.n_new, d,
+                     input_bf16_bits(a, src, idx0 + static_cast<size_t>(k * TP) * row));
       }
     }
-    xs[t * RS + d] = x;
   }
   __syncthreads();
 
-  // ---- transform: wave w computes output tiles w*OT/4 .. of both token tiles
-  const int m = lane & 15, q = lane >> 4;
-  constexpr int OPW = OT / 4;
   double4_t acc[2][OPW];
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
     for (int j = 0; j < OPW; ++j) acc[tt][j] = double4_t{0.0, 0.0, 0.0, 0.0};
-#pragma unroll 4
+#pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     double bt[OPW];
 #pragma unroll
-    for (int j = 0; j < OPW; ++j) bt[j] = static_cast<double>(tm[(4 * ks + q) * D + 16 * (wave * OPW + j) + m]);
+    for (int j = 0; j < OPW; ++j) bt[j] = static_cast<double>(tr[ks][j]);
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
       const double ax = xs[(16 * tt + m) * RS + 4 * ks + q];
@@ -222,16 +247,46 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
     __syncthreads();
   }
 
-  // ---- nearest codeword: wave w takes groups w, w+4, ...
+  // ---- nearest codeword: wave w takes groups w, w+4, ...; the codewords of
+  // its next group are requested while it processes the current one
+  uint2 ra[16], rn[4];
+#pragma unroll
+  for (int t = 0; t < 16; ++t) ra[t] = codeword_raw(cb, fp8, cw0 + static_cast<size_t>(wave) * kCodebookSize + 16 * t + m);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) rn[j] = codeword_raw(cb, fp8, cw0 + static_cast<size_t>(wave) * kCodebookSize + 4 * lane + j);
+  // The low byte of a score is replaced by its codeword index with one
+  // and-or per score: the mask sits in a VGPR and the index base in an SGPR
+  // (opaque zeros, so that the index of each score is a scalar add and no
+  // 32-bit literal, which this instruction encoding cannot carry).
+  uint32_t keep, idx0;
+  asm volatile("v_mov_b32 %0, 0xffffff00" : "=v"(keep));
+  asm volatile("s_mov_b32 %0, 0" : "=s"(idx0));
   for (int g = wave; g < L; g += 4) {
-    const size_t gcw = cw0 + static_cast<size_t>(g) * kCodebookSize;
     // A operands: coordinate q of codewords 16t + m
     double ac[16];
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
-      const uint2 w = codeword(cb, fp8, gcw + 16 * t + m);
+      const uint2 w = codeword_f16(ra[t], fp8);
       const uint32_t h2 = q < 2 ? w.x : w.y;
       ac[t] = static_cast<double>(half_bits_to_float(static_cast<uint16_t>((q & 1) ? (h2 >> 16) : (h2 & 0xffffu))));
+    }
+    double nc[4], cmax = 0.0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint2 w = codeword_f16(rn[j], fp8);
+      const double c0 = half_bits_to_float(static_cast<uint16_t>(w.x & 0xffff));
+      const double c1 = half_bits_to_float(static_cast<uint16_t>(w.x >> 16));
+      const double c2 = half_bits_to_float(static_cast<uint16_t>(w.y & 0xffff));
+      const double c3 = half_bits_to_float(static_cast<uint16_t>(w.y >> 16));
+      nc[j] = (c0 * c0 + c1 * c1) + (c2 * c2 + c3 * c3);
+      cmax = fmax(cmax, nc[j]);
+    }
+    {  // the next group's codewords (the last group requests itself again)
+      const size_t ncw = cw0 + static_cast<size_t>(min(g + 4, L - 1)) * kCodebookSize;
+#pragma unroll
+      for (int t = 0; t < 16; ++t) ra[t] = codeword_raw(cb, fp8, ncw + 16 * t + m);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) rn[j] = codeword_raw(cb, fp8, ncw + 4 * lane + j);
     }
     // offset: the largest |u_g|^2 of the tile (uniform)
     double un = 0.0;
@@ -243,19 +298,15 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
       }
     }
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) un = fmax(un, __shfl_xor(un, o, 64));
-    // |c|^2 + offset for the group's codewords, 4 per lane, stored so that the
-    // accumulator rows 4i + q of tile t (codewords 16t + 4i + q) are contiguous
-    // for each lane row q: codeword c at 16 (c / 16) + 4 (c mod 4) + (c / 4) mod 4
+    for (int o = 32; o > 0; o >>= 1) {
+      un = fmax(un, __shfl_xor(un, o, 64));
+      cmax = fmax(cmax, __shfl_xor(cmax, o, 64));
+    }
+    un = un + 0x1p-40 * (un + cmax);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int c = 4 * lane + j;
-      const uint2 w = codeword(cb, fp8, gcw + c);
-      const double c0 = half_bits_to_float(static_cast<uint16_t>(w.x & 0xffff));
-      const double c1 = half_bits_to_float(static_cast<uint16_t>(w.x >> 16));
-      const double c2 = half_bits_to_float(static_cast<uint16_t>(w.y & 0xffff));
-      const double c3 = half_bits_to_float(static_cast<uint16_t>(w.y >> 16));
-      cn[wave][16 * (c >> 4) + 4 * (c & 3) + ((c >> 2) & 3)] = ((c0 * c0 + c1 * c1) + (c2 * c2 + c3 * c3)) + un;
+      cn[wave][16 * (c >> 4) + 4 * (c & 3) + ((c >> 2) & 3)] = nc[j] + un;
     }
 #pragma unroll
     for (int t = 0; t < 16; ++t) ac[t] *= -2.0;
@@ -272,9 +323,12 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
         const double4_t dd = __builtin_amdgcn_mfma_f64_16x16x4f64(ac[t], bu, cin, 0, 0, 0);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {  // register i = codeword 16t + 4i + q
-          unsigned long long bits = static_cast<unsigned long long>(__double_as_longlong(fmax(dd[i], 0.0)));
-          bits = (bits & ~0xffull) | static_cast<unsigned long long>(16 * t + 4 * i);
-          best = fmin(best, __longlong_as_double(static_cast<long long>(bits)));
+          const double x = dd[i];
+          const unsigned long long bits = static_cast<unsigned long long>(__double_as_longlong(x));
+          const uint32_t idx = idx0 + static_cast<uint32_t>(16 * t + 4 * i);
+          const unsigned long long packed =
+              (bits & 0xffffffff00000000ull) | ((static_cast<uint32_t>(bits) & keep) | idx);
+          best = fmin(best, __longlong_as_double(static_cast<long long>(packed)));
         }
       }
       // full codeword index 16t + 4i + q into the low byte, then the minimum over q
