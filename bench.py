@@ -59,7 +59,9 @@ OTHER_CASES = [("single_head", 0, False, None, False, False), ("sweep_b64_s32k",
                ("qwen3_8b", 0, True, None, False, False), ("gptoss_pair", 1, True, None, False, False),
                ("qwen3_8b", 0, False, (64, 256), False, False), ("gptoss_pair", 1, False, (64, 256), False, False),
                ("qwen3_8b", 0, False, None, True, False), ("gptoss_pair", 1, False, None, True, False),
-               ("qwen3_8b", 0, False, None, False, True)]
+               ("qwen3_8b", 0, False, None, False, True),
+               # the deployed format: key scale, INT2 values, a 64+256 band
+               ("qwen3_8b", 0, True, (64, 256), False, True), ("gptoss_pair", 1, True, (64, 256), False, True)]
 
 
 def parse():

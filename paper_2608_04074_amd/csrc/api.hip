@@ -196,10 +196,10 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
     return fail(NOVA_KV_ERR_INVALID_ARG, "q, k_codes, v_codes, seq_lens or out is NULL");
   if (!aligned(k_codes, 16) || !aligned(v_codes, 16))
     return fail(NOVA_KV_ERR_INVALID_ARG, "code pools must be 16-byte aligned");
-  // the scalar value arm runs on the head_dim-128 table kernel, else on the split-K kernels
+  // every value format runs on the table kernels where their layout applies
   const bool sq = (p->flags & NOVA_KV_SQ_VALUES) != 0;
   plan = novakv::plan_decode(batch, num_q_heads, p->num_kv_heads, p->head_dim, max_seq_len, layout->block_size,
-                             window, sq && p->head_dim != 128);
+                             window, false);
   if ((st = debug_check(layout, batch, seq_lens, max_seq_len, nullptr, need_encode ? 1 : 0, stream)) != NOVA_KV_OK)
     return st;
   if (static_ws) {  // the allocation-free step: the GPU's fixed scratch array (the last check)

@@ -82,7 +82,7 @@ __device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, 
   }
 }
 
-template <int WAVES, bool KS, bool FP8>
+template <int WAVES, bool KS, bool FP8, bool SQ>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int t0, const int t1, const size_t row0, float4 (&tv)[4]) {
   const uint32_t sbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8_ptr)smem));
@@ -107,6 +107,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   const uint32_t vbase = sbase + kVBase + 8 * a2;
 
   float m_run = -INFINITY, l_run = 0.f;
+  float z_run = 0.f;  // scalar value arm: sum of p * offset of the lane's tokens
   float4_t acc[4];
 #pragma unroll
   for (int X = 0; X < 4; ++X) acc[X] = float4_t{0.f, 0.f, 0.f, 0.f};
@@ -125,8 +126,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   // of tokens R + 32h + 8r + 2rho + tq) and V dwords vw[2h + s] (bytes
   // 4a2..4a2+3 of tokens R + 32h + 8rho + 2jj + s).
   // Key-scale format: lane l also loads the stored scale of token R + l,
-  // issued after the code bytes.
-  auto load_round = [&](int R, uint32_t *kw, uint32_t *vw, uint32_t &ks) {
+  // issued after the code bytes; the scalar value arm loads that token's
+  // (scale, offset) word the same way.
+  auto load_round = [&](int R, uint32_t *kw, uint32_t *vw, uint32_t &ks, uint32_t &vq) {
     size_t sub[4];  // uniform: byte offsets of the round's four sub-tiles
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -143,16 +145,17 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
       for (int s = 0; s < 2; ++s) vw[2 * h + s] = *reinterpret_cast<const uint32_t *>(vb + voff + 16 * s);
     }
-    if constexpr (KS) {
+    if constexpr (KS || SQ) {
       const int st = lane >> 4;
       const size_t sl = st == 0 ? sub[0] : (st == 1 ? sub[1] : (st == 2 ? sub[2] : sub[3]));
-      ks = a.k_scales[sl / kL + (lane & 15)];
+      if constexpr (KS) ks = a.k_scales[sl / kL + (lane & 15)];
+      if constexpr (SQ) vq = reinterpret_cast<const uint32_t *>(a.v_sq)[sl / kL + (lane & 15)];
     }
   };
-  uint32_t kwb[kBuf][8], vwb[kBuf][4], ksb[kBuf] = {};
+  uint32_t kwb[kBuf][8], vwb[kBuf][4], ksb[kBuf] = {}, vqb[kBuf] = {};
 #pragma unroll
   for (int k = 0; k < kBuf - 1; ++k)
-    if (wave + k * WAVES < nrounds) load_round(R0 + kRound * (wave + k * WAVES), kwb[k], vwb[k], ksb[k]);
+    if (wave + k * WAVES < nrounds) load_round(R0 + kRound * (wave + k * WAVES), kwb[k], vwb[k], ksb[k], vqb[k]);
 
   // ---- setup: query transform, sink shifts, value codebook into LDS, table via MFMA
   {
@@ -186,13 +189,15 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       c = 8 * (r >> 2) + (e & 7);
     };
     uint2 vst[VPER];
+    if constexpr (!SQ) {
 #pragma unroll
-    for (int k = 0; k < VPER; ++k) {
-      const int e = tid + k * NT;
-      if (e < kL * 256) {
-        int g, c;
-        vmap(e, g, c);
-        vst[k] = codeword_raw(cbv, fp8, g * 256 + c);
+      for (int k = 0; k < VPER; ++k) {
+        const int e = tid + k * NT;
+        if (e < kL * 256) {
+          int g, c;
+          vmap(e, g, c);
+          vst[k] = codeword_raw(cbv, fp8, g * 256 + c);
+        }
       }
     }
     // table waves: groups 8*(wave & 1) .. +7, codes 64*(wave >> 1) .. +63; 4-lane
@@ -221,7 +226,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       if (e < kL * 256) {
         int g, c;
         vmap(e, g, c);
-        *reinterpret_cast<uint2 *>(smem + kVBase + (g & 3) * 8192 + (c << 5) + 8 * (g >> 2)) = codeword_f16(vst[k], fp8);
+        // scalar value arm: every group's table maps a code byte to its four
+        // 2-bit codes (0..3, exact in fp16); the offsets are summed apart
+        *reinterpret_cast<uint2 *>(smem + kVBase + (g & 3) * 8192 + (c << 5) + 8 * (g >> 2)) =
+            SQ ? sq_unpack_f16(c) : codeword_f16(vst[k], fp8);
       }
     }
     __syncthreads();
@@ -307,7 +315,8 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     asel[r] = half8_t{one, one, one, one, one, one, one, one};
   }
 
-  auto process_round = [&](const int R, const uint32_t *kw, const uint32_t *vw, const uint32_t ks) {
+  auto process_round = [&](const int R, const uint32_t *kw, const uint32_t *vw, const uint32_t ks,
+                           const uint32_t vq) {
     // K: both halves, four steps per token, pairs of steps per 16x16x32 MFMA
     uint32_t wr[8];
 #pragma unroll
@@ -340,11 +349,26 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
         z[i] *= __uint_as_float(static_cast<uint32_t>(__shfl(static_cast<int>(ks), src)) << 16);
       }
     }
+    // scalar value arm: (scale, offset) of the lane's tokens; the scale
+    // carries 2^-8, so that the value product's B operand stays below 2^8 times it
+    float vsc[8], vzr[8];
+    if constexpr (SQ) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int src = 32 * (i >> 2) + 8 * rho + 2 * (i & 3) + set;
+        const uint32_t w = static_cast<uint32_t>(__shfl(static_cast<int>(vq), src));
+        vsc[i] = __uint_as_float(w << 16) * 0x1p-8f;
+        vzr[i] = __uint_as_float(w & 0xffff0000u);
+      }
+    }
     if (R < t0 || R + kRound > t1) {
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int tok = R + 32 * (i >> 2) + 8 * rho + 2 * (i & 3) + set;
-        if (tok < t0 || tok >= t1) z[i] = -INFINITY;
+        if (tok < t0 || tok >= t1) {
+          z[i] = -INFINITY;
+          if constexpr (SQ) vsc[i] = vzr[i] = 0.f;  // rows past the tokens may hold anything
+        }
       }
     }
     float zmax = fmaxf(fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3])), fmaxf(fmaxf(z[4], z[5]), fmaxf(z[6], z[7])));
@@ -359,6 +383,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
     for (int i = 0; i < 8; ++i) p[i] = __builtin_amdgcn_exp2f(z[i] - base);
     l_run = l_run * alpha + (((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7])));
+    if constexpr (SQ)
+      z_run = z_run * alpha + (((p[0] * vzr[0] + p[1] * vzr[1]) + (p[2] * vzr[2] + p[3] * vzr[3])) +
+                               ((p[4] * vzr[4] + p[5] * vzr[5]) + (p[6] * vzr[6] + p[7] * vzr[7])));
     if (__any(bump && m_run != -INFINITY)) {
 #pragma unroll
       for (int X = 0; X < 4; ++X) acc[X] *= alpha;
@@ -368,8 +395,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     // V: per half, tile X = coordinates of groups 4*(0..3) + X; sets 0 and 1 in one MFMA
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const half4_t pb = {static_cast<_Float16>(p[4 * h]), static_cast<_Float16>(p[4 * h + 1]),
-                          static_cast<_Float16>(p[4 * h + 2]), static_cast<_Float16>(p[4 * h + 3])};
+      half4_t pb;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) pb[i] = static_cast<_Float16>(SQ ? p[4 * h + i] * vsc[4 * h + i] : p[4 * h + i]);
       const half8_t bpair = __builtin_shufflevector(set == 0 ? pb : zero4, set == 1 ? pb : zero4, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
       for (int X = 0; X < 4; ++X) {
@@ -390,8 +418,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       if (cur >= nrounds) break;
       const int nxt = cur + (kBuf - 1) * WAVES;
       if (nxt < nrounds)
-        load_round(R0 + kRound * nxt, kwb[(k + kBuf - 1) % kBuf], vwb[(k + kBuf - 1) % kBuf], ksb[(k + kBuf - 1) % kBuf]);
-      process_round(R0 + kRound * cur, kwb[k], vwb[k], ksb[k]);
+        load_round(R0 + kRound * nxt, kwb[(k + kBuf - 1) % kBuf], vwb[(k + kBuf - 1) % kBuf], ksb[(k + kBuf - 1) % kBuf],
+                   vqb[(k + kBuf - 1) % kBuf]);
+      process_round(R0 + kRound * cur, kwb[k], vwb[k], ksb[k], vqb[k]);
     }
   }
   load_tv_rows(a, kv, tv);
@@ -403,6 +432,11 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   const float wcol = (m_run == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - m_head);
   l_tot *= wcol;
   l_tot += row_ror<8>(l_tot);
+  float z_tot = 0.f;  // scalar value arm: the offsets' term of every coordinate of the head
+  if constexpr (SQ) {
+    z_tot = add_rows32(add_rows16(z_run)) * wcol;
+    z_tot += row_ror<8>(z_tot);
+  }
 #pragma unroll
   for (int X = 0; X < 4; ++X) {
 #pragma unroll
@@ -425,7 +459,8 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 #pragma unroll
     for (int X = 0; X < 4; ++X)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) mw[2 * kH + head * kD + 4 * (4 * rho + X) + i] = acc[X][i];
+      for (int i = 0; i < 4; ++i)
+        mw[2 * kH + head * kD + 4 * (4 * rho + X) + i] = SQ ? fmaf(acc[X][i], 256.f, z_tot) : acc[X][i];
   }
   __syncthreads();
 
@@ -579,7 +614,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
 // One workgroup per (sequence, KV head, split); the arrival protocol is the
 // one of the head_dim-128 kernel (relaxed agent-scope partials and counters,
 // the last split combines, a split finding all others arrived does not publish).
-template <int WAVES, bool KS, bool FP8>
+template <int WAVES, bool KS, bool FP8, bool SQ>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
   const int tid = threadIdx.x;
@@ -601,7 +636,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
 
   float4 tv[4];
   if (active) {
-    split_pass<WAVES, KS, FP8>(a, smem, b, kv, t0, t1, row0, tv);
+    split_pass<WAVES, KS, FP8, SQ>(a, smem, b, kv, t0, t1, row0, tv);
   } else {
     load_tv_rows(a, kv, tv);
   }
@@ -649,12 +684,20 @@ hipError_t launch_decode_lut64(const DecodeArgs &a, hipStream_t stream) {
   constexpr int W = 16;  // 4 waves per SIMD: the kernel fits in 128 VGPRs
   const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
   const dim3 block(W * 64);
-  if (a.k_scales)
-    a.cb_fp8 ? decode_lut_d64<W, true, true><<<grid, block, 0, stream>>>(a)
-             : decode_lut_d64<W, true, false><<<grid, block, 0, stream>>>(a);
-  else
-    a.cb_fp8 ? decode_lut_d64<W, false, true><<<grid, block, 0, stream>>>(a)
-             : decode_lut_d64<W, false, false><<<grid, block, 0, stream>>>(a);
+  if (a.v_sq) {  // the scalar value arm (keys in either codebook format)
+    if (a.k_scales)
+      a.cb_fp8 ? decode_lut_d64<W, true, true, true><<<grid, block, 0, stream>>>(a)
+               : decode_lut_d64<W, true, false, true><<<grid, block, 0, stream>>>(a);
+    else
+      a.cb_fp8 ? decode_lut_d64<W, false, true, true><<<grid, block, 0, stream>>>(a)
+               : decode_lut_d64<W, false, false, true><<<grid, block, 0, stream>>>(a);
+  } else if (a.k_scales) {
+    a.cb_fp8 ? decode_lut_d64<W, true, true, false><<<grid, block, 0, stream>>>(a)
+             : decode_lut_d64<W, true, false, false><<<grid, block, 0, stream>>>(a);
+  } else {
+    a.cb_fp8 ? decode_lut_d64<W, false, true, false><<<grid, block, 0, stream>>>(a)
+             : decode_lut_d64<W, false, false, false><<<grid, block, 0, stream>>>(a);
+  }
   return hipGetLastError();
 }
 

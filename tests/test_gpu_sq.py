@@ -269,3 +269,15 @@ def test_all_formats_together(nk):
     sinks = np.random.default_rng(4).standard_normal(wl.num_q_heads).astype(np.float32)
     _sq_decode_case(nk, wl, params, P, [2304, 1500, 300, 1], 2304, window=1000, sinks=sinks, key_scale=True,
                     band=(64, 256), what="qwen all formats")
+
+
+@pytest.mark.parametrize("window", [0, 128])
+def test_gptoss_deployed_format(nk, window):
+    """The deployed format at the GPT-OSS shape (D = 64, eight query heads per
+    KV head) on its table kernel: keys with a per-token scale, INT2 values,
+    a 64 + 256 band and sinks; ragged lengths that leave splits empty."""
+    wl = synth.get_workload("gptoss_pair")
+    params, P = sq_params(nk, wl, key_scale=True)
+    _sq_decode_case(nk, wl, params, P, [4096, 2500, 400, 257, 1], 4096, window=window,
+                    sinks=synth.sink_logits(wl, 0), key_scale=True, band=(64, 256),
+                    what=f"gptoss deployed format window={window}")
