@@ -45,6 +45,7 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_04074_amd", "csrc", f)
                   for f in ("decode_lut.hip", "band_attention.h", "encode_block.h", "lut_common.h",
                             "nova_kv_internal.h")]
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_lut_d128_qwen3_8b_traffic.md")
+COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "decode_lut_d128_qwen3_8b_counters.md")
 COPY_CALIB_BYTES = 256 << 20
 # Algorithmic work of the append encoder per token-head (D = 128, two sides):
 # the transform (2 D^2 flops per side) and the exhaustive distances
@@ -91,6 +92,24 @@ def kernel_source_sha256() -> str:
         with open(path, "rb") as f:
             h.update(os.path.basename(path).encode() + b"\0" + f.read())
     return h.hexdigest()
+
+
+def measured_counters():
+    """The step kernel's SQ counter ratios from the committed summary (VALU issue
+    and LDS issue per wave time, MFMA busy per SIMD time, LDS bank-conflict cycles
+    per CU time), or None when it is missing or was taken on a different source."""
+    try:
+        text = open(COUNTER_SUMMARY).read()
+    except OSError:
+        return None
+    sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
+    row = re.search(r"\| `" + re.escape(DECODE_KERNEL) + r"<12, true, false, false, false>` \| (\d+) \| ([0-9.]+) \| "
+                    r"([0-9.]+) \| ([0-9.]+) \| ([0-9.]+) \| ([0-9.]+) \|", text)
+    if not sha or not row or sha.group(1) != kernel_source_sha256():
+        return None
+    return {"source": os.path.relpath(COUNTER_SUMMARY, ROOT), "valu_issue_frac": float(row.group(3)),
+            "mfma_busy_frac": float(row.group(4)), "lds_issue_frac": float(row.group(5)),
+            "lds_bank_conflict_frac": float(row.group(6))}
 
 
 def measured_traffic():
@@ -501,6 +520,7 @@ def main():
             "unit": "GB/s",
             "frac": round(value / HBM_PEAK_GBS, 4),
             "traffic": traffic,
+            "counters": measured_counters(),
             "algorithmic_bytes_per_launch": code_bytes,
             "algorithmic_bytes_per_token_head": 2 * L,
         },
