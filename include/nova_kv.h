@@ -257,6 +257,9 @@ size_t nova_kv_decode_workspace_bytes(const nova_kv_params *p, int32_t batch,
  *              bytes, 256-byte aligned.  It must be zero-filled before its
  *              first use (e.g. hipMemset once after allocation); every call
  *              leaves it ready for the next one, so it is never cleared again.
+ *              This holds for replays of a call captured in a HIP graph too
+ *              (they repeat the captured arguments): the words the splits
+ *              exchange are emptied by their reader within the call.
  *              Calls that share a workspace must be ordered on one stream.
  * batch == 0 is a valid no-op.
  */
@@ -325,7 +328,9 @@ nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv
  *   zero-fills it with a kernel on hip_stream, ahead of the step.
  *   Every call on a GPU shares that GPU's array: calls that overlap on one GPU
  *   (on different streams, or from several threads without ordering) race;
- *   order them on one stream.
+ *   order them on one stream.  A call may be captured in a HIP graph and
+ *   replayed; make one call outside the capture first, so that the array is
+ *   looked up and cleared before the graph runs.
  * batch == 0 is a valid no-op.
  */
 #define NOVA_KV_NOALLOC_SCRATCH_BYTES (32u << 20)

@@ -170,7 +170,7 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
                               int32_t window, const float *sinks, float softmax_scale, float *out,
                               void *workspace, size_t workspace_bytes, bool need_encode,
                               novakv::DecodeArgs &a, novakv::DecodePlan &plan,
-                              bool static_ws = false, hipStream_t stream = nullptr) {
+                              bool static_ws, hipStream_t stream) {
   nova_kv_status st = check_params(p, need_encode, true);
   if (st != NOVA_KV_OK) return st;
   if ((st = check_layout(layout)) != NOVA_KV_OK) return st;
@@ -267,7 +267,15 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
     a.group_size = novakv::plan_group_size(plan.n_split);
     a.n_group = (plan.n_split + a.group_size - 1) / a.group_size;
   }
-  a.epoch = next_epoch();
+  // A call captured in a graph is replayed with these arguments, its epoch
+  // included, so its readers empty the exchange words they read.
+  hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &capture) != hipSuccess) {
+    (void)hipGetLastError();
+    capture = hipStreamCaptureStatusNone;
+  }
+  a.clear_xch = capture == hipStreamCaptureStatusActive ? 1 : 0;
+  a.epoch = next_epoch(a.clear_xch != 0);
   return NOVA_KV_OK;
 }
 

@@ -118,9 +118,11 @@ __device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, 
 // operations complete in issue order), counts the split in while the waves
 // merge.  The split that brings the count to n_split combines: it checks the
 // tag of every word it reads (the call's epoch), so no order between the
-// stores and the count is needed, and no word is emptied after use.  With
-// many splits the count runs per group of splits, and the group's last split
-// merges the group first (two levels, below).
+// stores and the count is needed.  In a call captured in a graph, whose
+// replays repeat its epoch, it then empties every word of the unit's slots
+// and new-token blocks, its own included, so each replay leaves the exchange
+// all zero.  With many splits the count runs per group of splits, and the
+// group's last split merges the group first (two levels, below).
 //   split slot: log-sum-exp m + ln l of head h at word 2h (natural log),
 //               normalised coordinate d of head h (acc / l) at 2G + h*128 + d;
 //               a split without tokens publishes nothing;
@@ -875,10 +877,28 @@ __device__ __forceinline__ bool read_slots(const uint32_t epoch, const int count
 // The partials this combine reads: the unit's split slots (one level), or
 // the slots of its split groups (two levels).
 struct Slots {
-  const uint64_t *base;  // slot 0
+  uint64_t *base;        // slot 0
   int n, own;            // number of slots, this workgroup's slot
   bool all_valid;        // group slots: every slot holds a partial and a band block
 };
+
+// Empties n slots from base on (heads 0..G-1; the band blocks too when the
+// call has a band).  Called once every read of the slots in this workgroup
+// is done (after a barrier); the words of the other workgroups were read, so
+// their stores precede these.
+__device__ __forceinline__ void clear_slots(uint64_t *base, const int n, const int G, const int tid,
+                                            const bool band) {
+  if (tid >= G * kD) return;
+  for (int j = 0; j < n; ++j) {
+    uint64_t *sp = base + static_cast<size_t>(j) * kXchSlotWords;
+    clear_word(sp + 2 * G + tid);
+    if (tid < 2 * G) clear_word(sp + tid);
+    if (band) {
+      clear_word(sp + kXchBandWords + 2 * G + tid);
+      if (tid < 2 * G) clear_word(sp + kXchBandWords + tid);
+    }
+  }
+}
 
 template <int WAVES, bool APPEND>
 __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
@@ -934,7 +954,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
     // splits (or groups) in index order whichever split combines, so the
     // result does not depend on the arrival order; the other slots are read
     // kXchBatch at a time
-    const uint64_t *xs = sl.base;
+    uint64_t *xs = sl.base;
     const int n_oth = sl.n - 1;
     const int own_slot = sl.own;
     bool own_done = false;
@@ -1046,6 +1066,10 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
     shat[tid] = 0.f;
   }
   __syncthreads();
+  if (a.clear_xch && a.n_split > 1) {  // captured call: empty the unit's exchange words, all read
+    clear_slots(sl.base, sl.n, G, tid, nband > 0);
+    if (APPEND && tid < 8 * 32) clear_word(a.xnew + static_cast<size_t>(bk) * 8 * 32 + tid);
+  }
   if (tid < 512) {
     // all eight values of a head are requested before they are used
     float o[4];
@@ -1095,7 +1119,7 @@ __device__ __forceinline__ void merge_group(const DecodeArgs &a, uint8_t *smem, 
   float *own = reinterpret_cast<float *>(smem + kAuxOwn);
   float *bst = reinterpret_cast<float *>(smem + BL::kStat);
   float *bz = reinterpret_cast<float *>(smem + BL::kZ);
-  const uint64_t *xs = a.xch + static_cast<size_t>(bk) * a.n_split * kXchSlotWords;
+  uint64_t *xs = a.xch + static_cast<size_t>(bk) * a.n_split * kXchSlotWords;
   uint64_t *gslot = a.xgrp + (static_cast<size_t>(bk) * a.n_group + gi) * kXchSlotWords;
   const bool mine = tid < G * kD;
   const int h = tid >> 7, d = tid & (kD - 1);
@@ -1169,7 +1193,8 @@ __device__ __forceinline__ void merge_group(const DecodeArgs &a, uint8_t *smem, 
       if (d == 0) put_word(a.epoch, gslot + kXchBandWords + 2 * h, mb);
     }
   }
-  __syncthreads();  // every read of this split's own partial is done
+  __syncthreads();  // every read of this split's own partial and of the group's slots is done
+  if (a.clear_xch) clear_slots(xs + static_cast<size_t>(g0) * kXchSlotWords, gsz, G, tid, nband > 0);
   // the group's partial replaces this split's own
   if (mine) {
     own[tid] = num;
@@ -1267,7 +1292,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   if (a.n_split > 1) {
     if (ctl[0] == 0) return;
   }
-  const uint64_t *xs = a.xch + static_cast<size_t>(bk) * a.n_split * kXchSlotWords;
+  uint64_t *xs = a.xch + static_cast<size_t>(bk) * a.n_split * kXchSlotWords;
   if (a.n_group > 1) {
     // two levels: merge this split's group, then count the group in
     merge_group<WAVES>(a, smem, bk, split, S, lo, tend, att_lo, spn.sink_end);

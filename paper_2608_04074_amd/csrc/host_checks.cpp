@@ -36,11 +36,16 @@ bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 // Tag of the split exchange of the next decode call: every call gets a new
 // nonzero number (the workspace's words of one call are never taken for
-// another's; zero marks a never-written word).
-uint32_t next_epoch() {
+// another's; zero marks a never-written word).  A captured call's replays
+// all carry its epoch and empty what they exchange; its epoch is even, so no
+// directly launched call (odd epochs, whose words stay) ever shares it.
+uint32_t next_epoch(bool captured) {
   static std::atomic<uint32_t> counter{0};
-  uint32_t e = counter.fetch_add(1, std::memory_order_relaxed) + 1;
-  while (e == 0) e = counter.fetch_add(1, std::memory_order_relaxed) + 1;
+  uint32_t e;
+  do {
+    const uint32_t c = counter.fetch_add(1, std::memory_order_relaxed);
+    e = captured ? (c + 1) << 1 : (c << 1) | 1u;
+  } while (e == 0);
   return e;
 }
 

@@ -22,8 +22,9 @@ nova_kv_status fail(nova_kv_status s, const char *fmt, ...) __attribute__((forma
 // Clears the detail and returns NOVA_KV_OK.
 nova_kv_status ok();
 bool aligned(const void *p, size_t a);
-// Tag of the split exchange of the next decode call: nonzero, new for every call.
-uint32_t next_epoch();
+// Tag of the split exchange of the next decode call: nonzero, new for every
+// call; odd for a call launched directly, even for a call captured in a graph.
+uint32_t next_epoch(bool captured);
 
 nova_kv_status check_params(const nova_kv_params *p, bool need_encode, bool need_decode);
 nova_kv_status check_layout(const nova_kv_layout *lay);

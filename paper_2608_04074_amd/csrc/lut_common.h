@@ -98,13 +98,19 @@ __device__ __forceinline__ float load_dev(const float *p) {
 // atomic.  The tag is the call's epoch, a nonzero number the host gives
 // every decode call: a reader that finds its call's epoch knows that the
 // value beside it is the one published in this call, whatever order other
-// stores arrived in, so a writer never waits for its stores to complete, and
-// a word left by an earlier call (another epoch) is never taken for a new
-// one.  Words are therefore never emptied; a zero-filled workspace holds
-// tag 0, which no call uses.
+// stores arrived in, so a writer never waits for its stores to complete.
+// Words are left in place after use.  A call captured in a graph is
+// replayed with its epoch, so there the reader of a slot empties it (zero
+// words, tag 0, which no call uses) once its reads are done: each replay
+// leaves the exchange all zero and meets no word of the replay before.  The
+// host draws odd epochs for direct calls and even ones for captured calls,
+// so a replay never takes a word left by a direct call either.
 __device__ __forceinline__ void put_word(const uint32_t epoch, uint64_t *p, float v) {
   const uint64_t w = (static_cast<uint64_t>(epoch) << 32) | __builtin_bit_cast(uint32_t, v);
   __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void clear_word(uint64_t *p) {
+  __hip_atomic_store(p, static_cast<uint64_t>(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ uint64_t get_word(const uint64_t *p) {
   return __hip_atomic_load(const_cast<uint64_t *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -79,6 +79,7 @@ struct DecodeArgs {
   uint64_t *xch;
   uint64_t *xnew;
   uint32_t epoch;   // this call's tag of the exchanged words (nonzero, new for every call)
+  int clear_xch;    // captured in a graph: readers empty the words they read (replays repeat the epoch)
   // Two-level combine of the head_dim-128 table kernel: splits in groups of
   // group_size, n_group groups (n_group = 1: one level, group_size = n_split);
   // group partials [B*Hkv][n_group][kXchSlotWords]; arrival counters

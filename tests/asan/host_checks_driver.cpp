@@ -60,9 +60,11 @@ static int fixed_cases() {
   // a long error detail is cut, not overrun
   std::vector<int32_t> lens(3, 1 << 30);
   bad += expect("huge length", check_metadata(&lay, 0, 3, lens.data(), 64, nullptr, 0), NOVA_KV_ERR_INVALID_ARG);
-  uint32_t e0 = next_epoch(), e1 = next_epoch();
-  if (e0 == 0 || e1 == 0 || e0 == e1) {
-    fprintf(stderr, "epochs %u %u\n", e0, e1);
+  // epochs: nonzero, distinct, odd for direct calls and even for captured ones
+  uint32_t e0 = next_epoch(false), e1 = next_epoch(true), e2 = next_epoch(false), e3 = next_epoch(true);
+  if (e0 == 0 || e1 == 0 || e2 == 0 || e3 == 0 || e0 == e2 || e1 == e3 || (e0 & 1) != 1 || (e2 & 1) != 1 ||
+      (e1 & 1) != 0 || (e3 & 1) != 0) {
+    fprintf(stderr, "epochs %u %u %u %u\n", e0, e1, e2, e3);
     ++bad;
   }
   return bad;
