@@ -315,6 +315,23 @@ def other_workload(nk, torch, dev, case, calls: int):
     # the key scales of the tokens read from codes: 2 bytes per token and KV
     # head; the value scale and offset: 4 more
     sb = (cb // L if key_scale else 0) + (2 * cb // L if sq else 0)
+    step = {}
+    if band_sizes:
+        # the whole step on the same pools: append a token at seq_len - 1, then
+        # attend.  One launch on the head_dim-128 table kernel (the new token is
+        # the band's last row); the encode, then the decode, at head_dim 64.
+        kn = torch.randn((B, H, D), generator=gen, device=dev).to(torch.bfloat16)
+        vn = torch.randn((B, H, D), generator=gen, device=dev).to(torch.bfloat16)
+        steps_ = [nk.prepare_append_decode(P, layout, kn, vn, q, pk, pv, seq, S, out, ws, window=window,
+                                           sinks=sinks, k_scales=ps, band=bands[i % len(bands)], v_sq=pq)
+                  for i, (pk, pv, ps, pq) in enumerate(pools)]
+        sfn = lambda i: steps_[i % copies]()  # noqa: E731
+        for i in range(200):
+            sfn(i)
+        step = {"step_us": round(back_to_back_us(torch, sfn, calls), 2),
+                "step_per_call_us": pct(timed_calls(torch, sfn, calls)),
+                "step_launches": 1 if D == 128 and band_sizes[1] >= 1 else (3 if sq else 2)}
+        del steps_
     res = {"workload": case_label(name, layer, key_scale, band_sizes, fp8, sq, wl),
            "batch": B, "seq_len": S, "q_heads": Hq, "kv_heads": H, "head_dim": D,
            "paged_block": wl.block_size or None, "code_bytes": cb, "scale_bytes": sb,
@@ -322,7 +339,7 @@ def other_workload(nk, torch, dev, case, calls: int):
            "band_copies": band_copies if band_sizes else None,
            "decode_us": round(us, 2), "per_call_us": pct(per_call),
            "GB_per_s": round((cb + sb + bb) / (us * 1e-6) / 1e9, 1),
-           "frac_of_hbm_peak": round((cb + sb + bb) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+           "frac_of_hbm_peak": round((cb + sb + bb) / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4), **step}
     del pools, calls_, ws, bands
     torch.cuda.empty_cache()
     return res

@@ -323,8 +323,12 @@ nova_kv_status append_step(const nova_kv_params *p, const nova_kv_layout *layout
                                      workspace_bytes, true, a, plan, static_ws, stream);
   if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
   hipError_t e;
-  if (plan.use_lut && p->head_dim == 128 && !(p->flags & (NOVA_KV_KEY_SCALE | NOVA_KV_SQ_VALUES)) && !band) {
-    // one launch: the table kernel encodes the new token and attends to it
+  // One launch on the head_dim-128 table kernel: in the plain and fp8
+  // formats the new token is attended from its codes; with a band whose
+  // recent part holds it, in any format, it is the band's last row.
+  const bool scaled_format = (p->flags & (NOVA_KV_KEY_SCALE | NOVA_KV_SQ_VALUES)) != 0;
+  const bool fused = plan.use_lut && p->head_dim == 128 && (band ? band->n_rec >= 1 : !scaled_format);
+  if (fused) {
     a.append = 1;
     a.k_new = k_new;
     a.v_new = v_new;
@@ -332,6 +336,12 @@ nova_kv_status append_step(const nova_kv_params *p, const nova_kv_layout *layout
     a.t_k = p->t_k;
     a.k_codes_w = k_codes;
     a.v_codes_w = v_codes;
+    a.k_scales_w = (p->flags & NOVA_KV_KEY_SCALE) ? k_scales : nullptr;
+    a.v_sq_w = (p->flags & NOVA_KV_SQ_VALUES) ? v_sq : nullptr;
+    if (band) {
+      a.band_k_w = static_cast<uint16_t *>(band->k);
+      a.band_v_w = static_cast<uint16_t *>(band->v);
+    }
     e = novakv::launch_decode(a, plan.use_lut, stream);
   } else {
     // the one-token encode at position seq_lens[b] - 1, then the decode

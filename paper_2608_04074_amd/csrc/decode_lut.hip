@@ -69,7 +69,13 @@ constexpr uint32_t kLdsBytes = kMergeBase + 12 * kMergeFloats * 4;
 // outputs.
 constexpr uint32_t kAuxOwn = kVBase;
 constexpr uint32_t kAuxOut = kVBase + 4 * kD * 4;
-static_assert(32 * kD * 4 <= 12 * kMergeFloats * 4 && 2 * sizeof(encblk::Scratch<kD>) <= 12 * kMergeFloats * 4,
+// Fused step with a band: the team's whole-token coefficients [2][128] f64,
+// its min/max words [2][4] f64 and its scalar-arm levels [2][128] bytes,
+// after the two block scratch areas.
+constexpr uint32_t kBandU = kAppendScratch + 2 * sizeof(encblk::Scratch<kD>);
+constexpr uint32_t kBandRed = kBandU + 2 * kD * 8;
+constexpr uint32_t kBandQ = kBandRed + 2 * 4 * 8;
+static_assert(32 * kD * 4 <= 12 * kMergeFloats * 4 && kBandQ + 2 * kD <= kMergeBase + 12 * kMergeFloats * 4,
               "the q' partial sums and the encoder scratch fit in the merge region");
 static_assert(kLdsBytes <= 160 * 1024, "LDS budget of a workgroup");
 constexpr float kLn2 = 0.693147180559945309f;
@@ -260,7 +266,138 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
   }
 }
 
-template <int WAVES, bool APPEND, bool KS, bool FP8, bool SQ>
+// Fused step with a sink-plus-recent band (n_rec >= 1): the new token is the
+// band's last row and is attended exactly, so the team only stores its
+// codes, and its scale (key-scale format) or its levels and (scale, offset)
+// (scalar value arm).  Tasks: the key side as 4 block items, or with the key
+// scale one task (all 128 coefficients, rho, then the 4 blocks' codes); the
+// value side as 4 block items, or in the scalar arm one task.  Task j of the
+// list (keys, then values) goes to split j mod n_eff.  Each task does the
+// one-token encoder's arithmetic (encode_block.h), so both store the same
+// bytes.
+template <bool KS, bool SQ>
+struct BandTasks {
+  static constexpr int kBlocks = kL / encblk::kGroups;
+  static constexpr int kKey = KS ? 1 : kBlocks;
+  static constexpr int kAll = kKey + (SQ ? 1 : kBlocks);
+  // team meetings of task j: its x, then two per block of coefficients and
+  // one for rho (key scale) or two for the levels (scalar arm); a block item
+  // meets twice
+  __device__ static int phases(const int j) {
+    if (j < kKey) return KS ? 2 + 2 * kBlocks : 2;
+    return SQ ? 3 + 2 * kBlocks : 2;
+  }
+  // all of a split's meetings, with the last one after its last task: the
+  // waves waiting for the team to free the merge region count them all
+  __device__ static int phases_of_split(const int split, const int n_eff) {
+    int n = 1;
+    for (int j = split; j < kAll; j += n_eff) n += phases(j);
+    return n;
+  }
+};
+
+// Called by the team's threads only (t = tid - 512).  Tasks alternate between
+// two sets of scratch, so no meeting guards their reuse.
+template <bool KS, bool SQ>
+__device__ __forceinline__ void encode_token_band(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
+                                                  const int split, const int n_eff, const size_t tokoff,
+                                                  const int t, const bool fp8) {
+  using BT = BandTasks<KS, SQ>;
+  encblk::Scratch<kD> *sc = reinterpret_cast<encblk::Scratch<kD> *>(smem + kAppendScratch);  // [2]
+  int phase = 0;
+  auto sync = [&] { team_sync(smem, ++phase); };
+  const size_t elem = (static_cast<size_t>(b) * a.num_kv_heads + kv) * kD + (t & (kD - 1));
+  auto element = [&](const bool key) {  // element t of the token minus k_bar (keys) or of the token (values)
+    const void *src = key ? a.k_new : a.v_new;
+    double x = a.new_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[elem]))
+                          : static_cast<double>(static_cast<const float *>(src)[elem]);
+    if (key) x -= static_cast<double>(a.kbar[kv * kD + t]);
+    return x;
+  };
+  const size_t cw0 = static_cast<size_t>(kv) * kL * kCodebookSize;
+  int k = 0;
+  for (int j = split; j < BT::kAll; j += n_eff, ++k) {
+    encblk::Scratch<kD> &s = sc[k & 1];
+    double *u = reinterpret_cast<double *>(smem + kBandU) + (k & 1) * kD;
+    const bool key = j < BT::kKey;
+    const float *tm = (key ? a.t_k : a.t_v) + static_cast<size_t>(kv) * kD * kD;
+    const void *cb = key ? a.cb_k : a.cb_v;
+    float4 rows[kD / 32];
+    uint2 cw[encblk::kPer];
+    if ((key && KS) || (!key && SQ)) {
+      encblk::load_rows<kD>(t, tm, 0, rows);
+      if (key) encblk::load_codewords(t, cb, fp8, cw0, 0, cw);
+      if (t < kD) s.xs[t] = element(key);
+      sync();
+      encblk::token_coefficients<kD>(t, s, tm, rows, u, sync);
+      if (key) {
+        // rho, then the blocks' codes of the coefficients divided by it (the
+        // next block's codewords requested while one block is searched)
+        if (t == 0) s.wpart[0][0] = encblk::key_scale<kD>(u);
+        sync();
+        const double rho = s.wpart[0][0];
+#pragma unroll
+        for (int bb = 0; bb < BT::kBlocks; ++bb) {
+          uint2 nx[encblk::kPer];
+          if (bb + 1 < BT::kBlocks) encblk::load_codewords(t, cb, fp8, cw0, bb + 1, nx);
+          double uu[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const double v = u[encblk::kCols * bb + 4 * (t >> 5) + i];
+            uu[i] = rho > 0.0 ? v / rho : 0.0;
+          }
+          const int code = encblk::search_codes(t, uu, cw, fp8);
+          if ((t & 31) == 0) a.k_codes_w[tokoff + encblk::kGroups * bb + (t >> 5)] = static_cast<uint8_t>(code);
+          if (bb + 1 < BT::kBlocks) {
+#pragma unroll
+            for (int i = 0; i < encblk::kPer; ++i) cw[i] = nx[i];
+          }
+        }
+        if (t == 0) a.k_scales_w[tokoff / kL] = encblk::bf16_of(rho);
+      } else {
+        double *red = reinterpret_cast<double *>(smem + kBandRed) + (k & 1) * 4;
+        uint8_t *q = smem + kBandQ + (k & 1) * kD;
+        uint16_t sbits, zbits;
+        encblk::sq_levels<kD>(t, u, red, q, sync, sbits, zbits);
+        if (t < kL) a.v_codes_w[tokoff + t] = encblk::sq_byte(q, t);
+        if (t == 0) {
+          a.v_sq_w[(tokoff / kL) * 2] = sbits;
+          a.v_sq_w[(tokoff / kL) * 2 + 1] = zbits;
+        }
+      }
+    } else {
+      const int blk = key ? j : j - BT::kKey;
+      encblk::load_block<kD>(t, tm, cb, fp8, cw0, blk, rows, cw);
+      if (t < kD) s.xs[t] = element(key);
+      sync();
+      encblk::partial_block<kD>(t, s, rows);
+      sync();
+      const int code = encblk::search_block<kD>(t, s, cw, fp8);
+      if ((t & 31) == 0)
+        (key ? a.k_codes_w : a.v_codes_w)[tokoff + encblk::kGroups * blk + (t >> 5)] = static_cast<uint8_t>(code);
+    }
+  }
+  sync();  // every read of the scratch is done: the merge region is free
+}
+
+// Fused step with a band: the new token's key and value rows (bf16: as given,
+// or an fp32 element rounded to nearest even) into its band slot.
+__device__ __forceinline__ void store_new_band_rows(const DecodeArgs &a, const int b, const int kv, const int pos) {
+  const int tid = threadIdx.x;
+  if (tid >= 2 * kD) return;
+  const int side = tid / kD, d = tid % kD;
+  const void *src = side ? a.v_new : a.k_new;
+  const size_t idx = (static_cast<size_t>(b) * a.num_kv_heads + kv) * kD + d;
+  const uint16_t bits = a.new_bf16 ? static_cast<const uint16_t *>(src)[idx]
+                                   : bf16_rne(static_cast<const float *>(src)[idx]);
+  const int nb = a.n_sink + a.n_rec;
+  (side ? a.band_v_w : a.band_k_w)[((static_cast<size_t>(b) * a.num_kv_heads + kv) * nb +
+                                    band_slot(pos, a.n_sink, a.n_rec)) * kD + d] = bits;
+}
+
+// BSTEP: a fused step with a band (APPEND too): the new token is the band's
+// last row, and the team runs encode_token_band.
+template <int WAVES, bool APPEND, bool KS, bool FP8, bool SQ, bool BSTEP>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int split, const int t0, const int t1, const size_t row0,
                                            const int rot, const int n_eff, const int S, float4 (&tv)[8]) {
@@ -436,9 +573,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       const float dot = wave_sum(fmaf(qs[sh * kD + 2 * lane], kb2.x, qs[sh * kD + 2 * lane + 1] * kb2.y));
       if (lane == 0) {
         reinterpret_cast<float *>(smem + kAuxCtl)[4 + sh] = a.sinks ? a.sinks[kv * G + sh] - a.scale * dot : -INFINITY;
-        // q . k_bar itself for the band's logits (the fused step, which has no
-        // band, keeps its encoder results in this region)
-        if constexpr (!APPEND) reinterpret_cast<float *>(smem + kItemRes)[sh] = dot;
+        // q . k_bar itself for the band's logits (a fused step without a band
+        // keeps its encoder results in this region)
+        if constexpr (!APPEND || BSTEP) reinterpret_cast<float *>(smem + kItemRes)[sh] = dot;
       }
     }
     if (tid < 512) {
@@ -468,7 +605,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       }
     } else if constexpr (APPEND) {
       // the encoder team requests its first item; the table build covers the latency
-      if (n_eff > 0) load_item(a, b, kv, split, n_eff, 0, tid - 512, ir, FP8);
+      if (!BSTEP && n_eff > 0) load_item(a, b, kv, split, n_eff, 0, tid - 512, ir, FP8);
     }
     __syncthreads();
     if (lut_wave) {
@@ -532,7 +669,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     if (n_eff > 0 && wave >= 8) {
       const int p = S - 1;
       const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
-      encode_items(a, smem, b, kv, split, n_eff, tokoff, tid - 512, ir, FP8);
+      if constexpr (BSTEP)
+        encode_token_band<KS, SQ>(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8);
+      else
+        encode_items(a, smem, b, kv, split, n_eff, tokoff, tid - 512, ir, FP8);
     }
   }
 
@@ -716,7 +856,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   if constexpr (APPEND) {
     // the merge region holds the encoder team's scratch until its last item
     if (n_eff > 0 && wave < 8) {
-      const int done = 4 * team_phases(split, n_eff);
+      const int done = 4 * (BSTEP ? BandTasks<KS, SQ>::phases_of_split(split, n_eff) : team_phases(split, n_eff));
       int *ctr = reinterpret_cast<int *>(smem + kTeamCtr);
       while (__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < done)
         __builtin_amdgcn_s_sleep(1);
@@ -900,7 +1040,7 @@ __device__ __forceinline__ void clear_slots(uint64_t *base, const int n, const i
   }
 }
 
-template <int WAVES, bool APPEND>
+template <int WAVES, bool APPEND, bool BSTEP>
 __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                              const int bk, const size_t row0, const int own_split, const int S,
                                              const int lo, const int tend, const int n_eff, const int band_lo,
@@ -932,7 +1072,8 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
     uint64_t *xn = a.xnew + static_cast<size_t>(bk) * 8 * 32;
     const int vj = (4 + (d >> 5)) * 32 + (d & 31);
     uint64_t wz[4], wv;
-    if constexpr (APPEND) {
+    constexpr bool new_term = APPEND && !BSTEP;  // with a band the new token is a band row
+    if constexpr (new_term) {
 #pragma unroll
       for (int k = 0; k < 4; ++k) wz[k] = get_word(xn + k * 32 + h);
       wv = get_word(xn + vj);
@@ -974,7 +1115,7 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
           });
     }
     if (!own_done) take_own();
-    if constexpr (APPEND) {
+    if constexpr (new_term) {
       if (S > 0) {  // the new token, after the splits
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -1212,10 +1353,10 @@ __device__ __forceinline__ void merge_group(const DecodeArgs &a, uint8_t *smem, 
 // partial to the exchange and counts its arrival; the last one combines.
 // The arrival counters live in the workspace and the last split resets its
 // counter to 0, so a decode step is a single launch.
-template <int WAVES, bool APPEND, bool KS, bool FP8, bool SQ>
+template <int WAVES, bool APPEND, bool KS, bool FP8, bool SQ, bool BSTEP>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
-  static_assert(!(APPEND && SQ), "the fused step serves the codebook value format only");
-  static_assert(!(APPEND && KS), "the fused step serves the plain format only");
+  static_assert(!BSTEP || APPEND, "a band step is a fused step");
+  static_assert(!APPEND || BSTEP || !(KS || SQ), "without a band the fused step serves the plain and fp8 formats");
   static_assert(WAVES == 12, "the exchange roles assume 12 waves");
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES, APPEND>()];
   const int tid = threadIdx.x;
@@ -1228,12 +1369,14 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
 
   const int S = a.seq_lens[b];
   const int att_lo = a.window > 0 ? max(0, S - a.window) : 0;
-  // The pools are read for [lo, tend): the attended span without the band
-  // (a fused step has none: its newest token comes from the step's own key
-  // and value, so the pools are read for [att_lo, S - 1)).
+  // The pools are read for [lo, tend): the attended span without the band.
+  // A fused step without a band attends its newest token from the step's own
+  // codes, so the pools are read for [att_lo, S - 1); with a band that token
+  // is the band's last row.
   const AttendedSpans spn = attended_spans(att_lo, S, a.n_sink, a.n_rec);
-  const int lo = APPEND ? att_lo : spn.code_lo;
-  const int tend = APPEND ? max(S - 1, att_lo) : spn.code_hi;
+  constexpr bool new_from_codes = APPEND && !BSTEP;
+  const int lo = new_from_codes ? att_lo : spn.code_lo;
+  const int tend = new_from_codes ? max(S - 1, att_lo) : spn.code_hi;
   const int t0 = lo + split * a.chunk;  // splits tile the span read from the pools
   const int t1 = min(tend, lo + (split + 1) * a.chunk);
   const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
@@ -1248,7 +1391,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   }
 
   float4 tv[8];
-  split_pass<WAVES, APPEND, KS, FP8, SQ>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
+  split_pass<WAVES, APPEND, KS, FP8, SQ, BSTEP>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
   // Sink-plus-recent band: this split's share of the band rows, attended in
   // the table's LDS region (free after the split pass) and published beside
   // the split's partial; one CU would read the whole band at a fraction of
@@ -1259,6 +1402,14 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
     band_share(nband, a.n_split, split, bfirst, bcount);
     if (bcount > 0) {
       using BL = BandLds<kD, 4, WAVES>;
+      if constexpr (BSTEP) {
+        // a fused step's new token is the band's last row: the split that
+        // attends it stores it, and reads it back after the barrier
+        if (bfirst + bcount == nband) {
+          store_new_band_rows(a, b, kv, S - 1);
+          __syncthreads();
+        }
+      }
       band_attention<kD, 4, WAVES, WAVES>(a, smem, b, kv, row0, att_lo, spn.sink_end, tend, S, bfirst, bcount,
                                           reinterpret_cast<const float *>(smem + kAuxQ),
                                           reinterpret_cast<const float *>(smem + kItemRes));
@@ -1307,9 +1458,9 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
     if (ctl[0] == 0) return;
     const Slots gs{a.xgrp + static_cast<size_t>(bk) * a.n_group * kXchSlotWords, a.n_group, split / a.group_size,
                    true};
-    combine_unit<WAVES, APPEND>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv, gs);
+    combine_unit<WAVES, APPEND, BSTEP>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv, gs);
   } else {
-    combine_unit<WAVES, APPEND>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv,
+    combine_unit<WAVES, APPEND, BSTEP>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv,
                                 Slots{xs, a.n_split, split, false});
   }
 }
@@ -1374,33 +1525,37 @@ int plan_b_chunk(int batch, int num_kv_heads, int n_split) {
   return bc;
 }
 
-hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream) {
+template <bool APPEND, bool KS, bool BSTEP>
+void launch_d128(const DecodeArgs &a, const dim3 grid, const dim3 block, hipStream_t stream) {
   constexpr int W = 12;
-  const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
-  if (a.append && (a.k_scales || a.band_k || a.v_sq)) return hipErrorInvalidValue;
-  const dim3 block(W * 64);
-  if (a.v_sq) {  // the scalar value arm (keys in either codebook format)
-    if (a.k_scales)
-      a.cb_fp8 ? decode_lut_d128<W, false, true, true, true><<<grid, block, 0, stream>>>(a)
-               : decode_lut_d128<W, false, true, false, true><<<grid, block, 0, stream>>>(a);
+  if (a.v_sq) {
+    if (a.cb_fp8)
+      decode_lut_d128<W, APPEND, KS, true, true, BSTEP><<<grid, block, 0, stream>>>(a);
     else
-      a.cb_fp8 ? decode_lut_d128<W, false, false, true, true><<<grid, block, 0, stream>>>(a)
-               : decode_lut_d128<W, false, false, false, true><<<grid, block, 0, stream>>>(a);
-  } else if (a.cb_fp8) {
-    if (a.append)
-      decode_lut_d128<W, true, false, true, false><<<grid, block, 0, stream>>>(a);
-    else if (a.k_scales)
-      decode_lut_d128<W, false, true, true, false><<<grid, block, 0, stream>>>(a);
-    else
-      decode_lut_d128<W, false, false, true, false><<<grid, block, 0, stream>>>(a);
+      decode_lut_d128<W, APPEND, KS, false, true, BSTEP><<<grid, block, 0, stream>>>(a);
   } else {
-    if (a.append)
-      decode_lut_d128<W, true, false, false, false><<<grid, block, 0, stream>>>(a);
-    else if (a.k_scales)
-      decode_lut_d128<W, false, true, false, false><<<grid, block, 0, stream>>>(a);
+    if (a.cb_fp8)
+      decode_lut_d128<W, APPEND, KS, true, false, BSTEP><<<grid, block, 0, stream>>>(a);
     else
-      decode_lut_d128<W, false, false, false, false><<<grid, block, 0, stream>>>(a);
+      decode_lut_d128<W, APPEND, KS, false, false, BSTEP><<<grid, block, 0, stream>>>(a);
   }
+}
+
+hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream) {
+  // A fused step in the key-scale or scalar value format, or with a band,
+  // attends its new token as the band's last row: it needs a recent band.
+  if (a.append && (a.k_scales || a.v_sq || a.band_k) && !(a.band_k && a.n_rec >= 1)) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
+  const dim3 block(12 * 64);
+  if (a.append && a.band_k)
+    a.k_scales ? launch_d128<true, true, true>(a, grid, block, stream)
+               : launch_d128<true, false, true>(a, grid, block, stream);
+  else if (a.append)  // plain or fp8 codebooks (checked above)
+    a.cb_fp8 ? decode_lut_d128<12, true, false, true, false, false><<<grid, block, 0, stream>>>(a)
+             : decode_lut_d128<12, true, false, false, false, false><<<grid, block, 0, stream>>>(a);
+  else
+    a.k_scales ? launch_d128<false, true, false>(a, grid, block, stream)
+               : launch_d128<false, false, false>(a, grid, block, stream);
   return hipGetLastError();
 }
 

@@ -85,15 +85,9 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
     // coefficients divided by rho; block 0's workgroup stores rho.
     __shared__ double us[D];
     __shared__ double srho;
-#pragma unroll 1
-    for (int bb = 0; bb < NB; ++bb) {
-      float4 tb[D / 32];
-      encblk::load_rows<D>(tid, tm, bb, tb);
-      encblk::partial_block<D>(tid, sc, tb);
-      __syncthreads();
-      if (tid < encblk::kCols) us[encblk::kCols * bb + tid] = encblk::coefficient<D>(sc, tid);
-      __syncthreads();
-    }
+    float4 tb[D / 32];
+    encblk::load_rows<D>(tid, tm, 0, tb);
+    encblk::token_coefficients<D>(tid, sc, tm, tb, us, [] { __syncthreads(); });
     if (tid == 0) srho = encblk::key_scale<D>(us);
     __syncthreads();
     const double rho = srho;
@@ -352,56 +346,36 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
 
 // Scalar value arm (paper: Sec. "Bit rate" and the implementation table:
 // per-token affine INT2 values with a BF16 scale and offset): one workgroup
-// of D threads per (new token, KV head, sequence).  s = v t_v in fp64 (thread
-// i sums its coordinate in row order), the min and max over the D
-// coordinates, offset = bf16(min), scale = bf16((max - min) / 3), and
-// q_i = clamp(round_half_even((s_i - offset) / scale), 0, 3) with the stored
-// values (0 when the stored scale is 0); coordinate 4g + j goes to bits
-// 2j, 2j+1 of byte g.  The token's value row also goes to the band when it
-// is in it.
+// (the 256-thread team of encode_block.h) per (new token, KV head,
+// sequence).  s = v t_v in fp64 with the block encoder's arithmetic, then
+// encode_block.h's levels; coordinate 4g + j goes to bits 2j, 2j + 1 of
+// byte g.  The token's value row also goes to the band when it is in it.
 template <int D>
-__global__ void __launch_bounds__(D) encode_sq_values(EncodeArgs a) {
+__global__ void __launch_bounds__(256) encode_sq_values(EncodeArgs a) {
   constexpr int L = D / kGroupDim;
-  __shared__ double xs[D];
-  __shared__ double red[2][D / 64];
+  __shared__ encblk::Scratch<D> sc;
+  __shared__ double us[D];
+  __shared__ double red[2 * D / 64];
   __shared__ uint8_t qs[D];
   const int t = blockIdx.x, kv = blockIdx.y, b = blockIdx.z, i = threadIdx.x;
   const int p0 = a.start_pos[b] + a.start_offset;
   if (!position_in_pool(a.layout, p0 + t)) return;  // uniform: the workgroup stores nothing
-  const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + i;
-  xs[i] = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(a.v)[idx]))
-                    : static_cast<double>(static_cast<const float *>(a.v)[idx]);
-  if (a.band_v) store_band(a, 1, b, kv, p0 + t, p0 + a.n_new, i, input_bf16_bits(a, a.v, idx));
-  __syncthreads();
   const float *tv = a.t_v + static_cast<size_t>(kv) * D * D;
-  double s = 0.0;
-#pragma unroll 8
-  for (int d = 0; d < D; ++d) s = fma(xs[d], static_cast<double>(tv[d * D + i]), s);
-  double mn = s, mx = s;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    mn = fmin(mn, __shfl_xor(mn, o, 64));
-    mx = fmax(mx, __shfl_xor(mx, o, 64));
-  }
-  if ((i & 63) == 0) {
-    red[0][i >> 6] = mn;
-    red[1][i >> 6] = mx;
+  float4 rows[D / 32];
+  encblk::load_rows<D>(i, tv, 0, rows);
+  if (i < D) {
+    const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + i;
+    sc.xs[i] = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(a.v)[idx]))
+                         : static_cast<double>(static_cast<const float *>(a.v)[idx]);
+    if (a.band_v) store_band(a, 1, b, kv, p0 + t, p0 + a.n_new, i, input_bf16_bits(a, a.v, idx));
   }
   __syncthreads();
-  mn = red[0][0];
-  mx = red[1][0];
-#pragma unroll
-  for (int w = 1; w < D / 64; ++w) {
-    mn = fmin(mn, red[0][w]);
-    mx = fmax(mx, red[1][w]);
-  }
-  const uint16_t zb = encblk::bf16_of(mn), sb = encblk::bf16_of((mx - mn) / 3.0);
-  const double zero = bf16_bits_to_float(zb), scale = bf16_bits_to_float(sb);
-  qs[i] = scale > 0.0 ? static_cast<uint8_t>(fmin(fmax(rint((s - zero) / scale), 0.0), 3.0)) : 0;
-  __syncthreads();
+  auto sync = [] { __syncthreads(); };
+  encblk::token_coefficients<D>(i, sc, tv, rows, us, sync);
+  uint16_t sb, zb;
+  encblk::sq_levels<D>(i, us, red, qs, sync, sb, zb);
   const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, p0 + t);
-  if (i < L)
-    a.v_codes[off + i] = static_cast<uint8_t>(qs[4 * i] | (qs[4 * i + 1] << 2) | (qs[4 * i + 2] << 4) | (qs[4 * i + 3] << 6));
+  if (i < L) a.v_codes[off + i] = encblk::sq_byte(qs, i);
   if (i == 0) {
     a.v_sq[(off / L) * 2] = sb;
     a.v_sq[(off / L) * 2 + 1] = zb;
@@ -410,7 +384,7 @@ __global__ void __launch_bounds__(D) encode_sq_values(EncodeArgs a) {
 
 template <int D>
 hipError_t launch_encode_d(const EncodeArgs &a, hipStream_t stream) {
-  if (a.v_sq) encode_sq_values<D><<<dim3(a.n_new, a.num_kv_heads, a.batch), dim3(D), 0, stream>>>(a);
+  if (a.v_sq) encode_sq_values<D><<<dim3(a.n_new, a.num_kv_heads, a.batch), dim3(256), 0, stream>>>(a);
   if (a.n_new <= 4) {
     const dim3 grid(2 * a.n_new * (D / kGroupDim / 8), a.num_kv_heads, a.batch);
     if (a.cb_fp8)

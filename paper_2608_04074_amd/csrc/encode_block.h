@@ -147,6 +147,79 @@ __device__ __forceinline__ int search_block(const int t, const Scratch<D> &s, co
   return search_codes(t, uu, cw, fp8);
 }
 
+// bf16 bit pattern of an fp64 value: rounded to fp32, then to bf16, each to
+// nearest even.
+__device__ __forceinline__ uint16_t bf16_of(const double x) {
+  const uint32_t f = __float_as_uint(static_cast<float>(x));
+  return static_cast<uint16_t>((f + 0x7fffu + ((f >> 16) & 1u)) >> 16);
+}
+
+// All D coefficients of one token (x in s.xs) into u[D]: block after block,
+// each with the block's own arithmetic (partial_block, then coefficient), the
+// next block's transform rows requested while the current one is summed.
+// `first` holds block 0's rows (load_rows) on entry.  Two meetings of the
+// team (sync) per block.
+template <int D, class Sync>
+__device__ __forceinline__ void token_coefficients(const int t, Scratch<D> &s, const float *tm,
+                                                   float4 (&first)[D / 32], double *u, Sync sync) {
+  constexpr int NB = D / kCols;
+  float4 next[D / 32];
+#pragma unroll
+  for (int bb = 0; bb < NB; ++bb) {
+    if (bb + 1 < NB) load_rows<D>(t, tm, bb + 1, next);
+    partial_block<D>(t, s, first);
+    sync();
+    if (t < kCols) u[kCols * bb + t] = coefficient<D>(s, t);
+    sync();
+    if (bb + 1 < NB) {
+#pragma unroll
+      for (int j = 0; j < D / 32; ++j) first[j] = next[j];
+    }
+  }
+}
+
+// Scalar value arm of one token (paper: Sec. "Bit rate" and the
+// implementation table: per-token affine INT2 values with a BF16 scale and
+// offset) from its D coefficients u: offset = bf16(min), scale =
+// bf16((max - min) / 3), and level_i = clamp(round_half_even((u_i - offset)
+// / scale), 0, 3) with the stored values (0 when the stored scale is 0),
+// into q[i].  Thread t < D takes coordinate t; D is a multiple of 64, so
+// the waves that hold coordinates are whole.  red: 2 D / 64 doubles of LDS.
+// Two meetings of the team (sync).
+template <int D, class Sync>
+__device__ __forceinline__ void sq_levels(const int t, const double *u, double *red, uint8_t *q, Sync sync,
+                                          uint16_t &scale_bits, uint16_t &offset_bits) {
+  static_assert(D % 64 == 0, "whole waves hold the coordinates");
+  double mn = t < D ? u[t] : 0.0, mx = mn;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    mn = fmin(mn, __shfl_xor(mn, o, 64));
+    mx = fmax(mx, __shfl_xor(mx, o, 64));
+  }
+  if (t < D && (t & 63) == 0) {
+    red[t >> 6] = mn;
+    red[D / 64 + (t >> 6)] = mx;
+  }
+  sync();
+  mn = red[0];
+  mx = red[D / 64];
+#pragma unroll
+  for (int w = 1; w < D / 64; ++w) {
+    mn = fmin(mn, red[w]);
+    mx = fmax(mx, red[D / 64 + w]);
+  }
+  offset_bits = bf16_of(mn);
+  scale_bits = bf16_of((mx - mn) / 3.0);
+  const double zero = bf16_bits_to_float(offset_bits), scale = bf16_bits_to_float(scale_bits);
+  if (t < D) q[t] = scale > 0.0 ? static_cast<uint8_t>(fmin(fmax(rint((u[t] - zero) / scale), 0.0), 3.0)) : 0;
+  sync();
+}
+
+// Byte g of a token's scalar-arm codes: levels 4g + j at bits 2j, 2j + 1.
+__device__ __forceinline__ uint8_t sq_byte(const uint8_t *q, const int g) {
+  return static_cast<uint8_t>(q[4 * g] | (q[4 * g + 1] << 2) | (q[4 * g + 2] << 4) | (q[4 * g + 3] << 6));
+}
+
 // Key-scale format: rho = sqrt(sum of the squared coefficients, added in
 // coordinate order) / sqrt(D), each square rounded before it is added.
 template <int D>
@@ -159,11 +232,6 @@ __device__ __forceinline__ double key_scale(const double *u) {
   return sqrt(s) / sqrt(static_cast<double>(D));
 }
 
-// bf16 bit pattern of rho: rounded to fp32, then to bf16, each to nearest even.
-__device__ __forceinline__ uint16_t bf16_of(const double x) {
-  const uint32_t f = __float_as_uint(static_cast<float>(x));
-  return static_cast<uint16_t>((f + 0x7fffu + ((f >> 16) & 1u)) >> 16);
-}
 
 }  // namespace encblk
 }  // namespace novakv

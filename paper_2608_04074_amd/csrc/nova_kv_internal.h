@@ -65,13 +65,17 @@ struct DecodeArgs {
   int chunk;        // tokens per split
   int b_chunk;      // table kernels: sequences per block of the workgroup order (divides batch)
   // Fused step (nova_kv_append_decode_attn): the step's key and value of every
-  // sequence are encoded in the launch, stored at position seq_lens[b] - 1 and
-  // attended from their codes; the pool tokens read are [lo, seq_lens[b] - 1).
+  // sequence are encoded in the launch and stored at position seq_lens[b] - 1.
+  // Without a band they are attended from their codes (the pool tokens read
+  // are [lo, seq_lens[b] - 1)); with one (n_rec >= 1) the new token is the
+  // band's last row, stored there in the launch and attended exactly.
   int append;
   const void *k_new, *v_new;  // [B][Hkv][D]
   int new_bf16;
   const float *t_k;
   uint8_t *k_codes_w, *v_codes_w;  // the pools k_codes / v_codes, written at the new position
+  uint16_t *k_scales_w, *v_sq_w;   // the key-scale and scalar-arm pools, written there (else nullptr)
+  uint16_t *band_k_w, *band_v_w;   // the band buffers, written at the new token's slot (else nullptr)
   float *newp;      // [B][Hkv][8 items][32] per-block results for the new token
   // Tagged exchange of the head_dim-128 table kernel (64-bit words, the tag
   // in the high half): split partials [B*Hkv][n_split][kXchSlotWords] and
