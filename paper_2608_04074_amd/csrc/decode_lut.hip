@@ -208,10 +208,12 @@ __device__ __forceinline__ int team_phases(const int split, const int n_eff) {
   return 2 * items_of_split(split, n_eff) + 1;
 }
 
-// Called by the team's threads only (t = tid - 512); r holds item 0's loads.
+// Called by the team's threads only (t = tid - 512), once the tables are
+// built.  Each item requests its loads when it starts.  (Requesting the
+// first item's during the setup kept 34 registers live across the table
+// build: the fp8 step spilled, and both steps ran 0.4-1 us slower.)
 // Items alternate between two scratch areas, so no meeting guards their
-// reuse.  The next item's rows are requested when an item starts, its
-// codewords (needed two meetings into it) when it starts itself.  The
+// reuse.  The
 // thread that found a group's codeword records its per-group result: a key
 // block's partial logits of the 8 groups per head (table entries of the
 // stored codes, res[32 k + 4 gg + h]), a value block's coordinates
@@ -219,7 +221,7 @@ __device__ __forceinline__ int team_phases(const int split, const int n_eff) {
 // each key block's head h over the groups in order, into res[32 k + h].
 __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                              const int split, const int n_eff, const size_t tokoff, const int t,
-                                             ItemRegs &r, const bool fp8) {
+                                             const bool fp8) {
   encblk::Scratch<kD> *sc = reinterpret_cast<encblk::Scratch<kD> *>(smem + kAppendScratch);  // [2]
   float *res = reinterpret_cast<float *>(smem + kItemRes);
   uint64_t *xn = a.xnew + static_cast<size_t>(b * a.num_kv_heads + kv) * 8 * 32;
@@ -251,7 +253,8 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
     }
   };
   for (int k = 0; k < nmine; ++k) {
-    if (k > 0) load_item(a, b, kv, split, n_eff, k, t, r, fp8);
+    ItemRegs r;
+    load_item(a, b, kv, split, n_eff, k, t, r, fp8);
     encode_one(k, r);
   }
   team_sync(smem, ++phase);
@@ -477,7 +480,6 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     if (tid == 0) *reinterpret_cast<int *>(smem + kTeamCtr) = 0;
   }
 
-  ItemRegs ir;  // fused step: the encoder team's first item, loaded during the setup
   // ---- setup: value codebook into LDS, table of partial logits via MFMA.
   // All global loads of the setup are issued before any of them is used, in
   // the order query, t_k_inv_t rows, key codebook, value codebook, k_bar,
@@ -603,9 +605,6 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
         acc[hh].w = add_rows32(acc[hh].w);
         if (lane < 32) *reinterpret_cast<float4 *>(qsum + wave * 512 + e4 * 16 + hh * 4) = acc[hh];
       }
-    } else if constexpr (APPEND) {
-      // the encoder team requests its first item; the table build covers the latency
-      if (!BSTEP && n_eff > 0) load_item(a, b, kv, split, n_eff, 0, tid - 512, ir, FP8);
     }
     __syncthreads();
     if (lut_wave) {
@@ -672,7 +671,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       if constexpr (BSTEP)
         encode_token_band<KS, SQ>(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8);
       else
-        encode_items(a, smem, b, kv, split, n_eff, tokoff, tid - 512, ir, FP8);
+        encode_items(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8);
     }
   }
 
