@@ -89,27 +89,41 @@ def history(wl, B, cap, n_sink, n_rec, seed):
     return ck, cv, ks, np.stack([sb, zb], axis=-1), band
 
 
-def run_both(nk, wl, P, fmt, lens, cap, *, window=0, sinks=None, n_sink=64, n_rec=256, seed=3):
+def run_both(nk, wl, P, fmt, lens, cap, *, window=0, sinks=None, n_sink=64, n_rec=256, seed=3, paged_bs=None,
+             new_dtype=torch.bfloat16):
+    """paged_bs: a paged cache of blocks of that many tokens (seeded shuffled
+    block table; the history is then a random pool); new_dtype: the step's
+    key and value (fp32 ones are rounded to bf16 for the band)."""
     ks, _, sq = FORMATS[fmt]
     B, H, D = len(lens), wl.num_kv_heads, wl.head_dim
     ck, cv, hks, hsq, hband = history(wl, B, cap, n_sink, n_rec, seed)
     rng = np.random.default_rng(seed + 1)
-    kn = dev(rng.standard_normal((B, H, D)), torch.bfloat16)
-    vn = dev(rng.standard_normal((B, H, D)), torch.bfloat16)
+    kn = dev(rng.standard_normal((B, H, D)), new_dtype)
+    vn = dev(rng.standard_normal((B, H, D)), new_dtype)
     q = dev(synth.decode_queries(wl, 0, batch=B), torch.bfloat16)
     lens_d = dev(np.asarray(lens, np.int32), torch.int32)
     sk = dev(sinks, torch.float32) if sinks is not None else None
     lay = nk.CacheLayout.contiguous(cap)
+    if paged_bs:
+        # the same bytes read as a pool of B * cap / paged_bs blocks of [Hkv][paged_bs] rows
+        bps = cap // paged_bs
+        table = np.random.default_rng(seed + 2).permutation(B * bps).astype(np.int32).reshape(B, bps)
+        lay = nk.CacheLayout(paged_bs, bps, dev(table, torch.int32))
+        ck = ck.reshape(B * bps, H, paged_bs, -1)
+        cv = cv.reshape(B * bps, H, paged_bs, -1)
+        hks = hks.reshape(B * bps, H, paged_bs)
+        hsq = hsq.reshape(B * bps, H, paged_bs, 2)
 
     def state():
         return dict(k=dev(ck, torch.uint8), v=dev(cv, torch.uint8), ks=dev_bits(hks) if ks else None,
                     sq=dev_bits(hsq) if sq else None, bk=dev_bits(hband[0]), bv=dev_bits(hband[1]))
 
     one, two = state(), state()
-    say(f"deployed step {fmt} B={B} cap={cap} window={window}: one launch")
+    what = f"{fmt} B={B} cap={cap} window={window} band={n_sink}+{n_rec}" + (f" paged {paged_bs}" if paged_bs else "")
+    say(f"deployed step {what}: one launch")
     out1 = nk.append_decode_attn(P, lay, kn, vn, q, one["k"], one["v"], lens_d, cap, window=window, sinks=sk,
                                  k_scales=one["ks"], v_sq=one["sq"], band=nk.Band(n_sink, n_rec, one["bk"], one["bv"]))
-    say(f"deployed step {fmt} B={B} cap={cap} window={window}: encode, then decode")
+    say(f"deployed step {what}: encode, then decode")
     band2 = nk.Band(n_sink, n_rec, two["bk"], two["bv"])
     nk.encode(P, lay, kn[:, None], vn[:, None], lens_d - 1, two["k"], two["v"], k_scales=two["ks"], band=band2,
               v_sq=two["sq"])
@@ -122,8 +136,7 @@ def run_both(nk, wl, P, fmt, lens, cap, *, window=0, sinks=None, n_sink=64, n_re
     o1, o2 = out1.cpu().numpy(), out2.cpu().numpy()
     assert np.isfinite(o1).all()
     err = row_errors(o1.reshape(-1, D), o2.reshape(-1, D).astype(np.float64))
-    print(f"[parity] deployed step {fmt} B={B} cap={cap} window={window} vs two calls "
-          f"worst_rel_diff={float(err.max()):.3e}", flush=True)
+    print(f"[parity] deployed step {what} vs two calls worst_rel_diff={float(err.max()):.3e}", flush=True)
     assert float(err.max()) <= SAME_TOL
     return one, o1
 
@@ -137,6 +150,23 @@ def test_step_matches_encode_then_decode(nk, fmt):
     # one inside the sinks, one just past the band, long ones
     run_both(nk, wl, P, fmt, [1, 40, 330, 2048], 2048, sinks=sinks)
     run_both(nk, wl, P, fmt, [1500, 2048, 700, 321], 2048, window=500, seed=5)
+
+
+@pytest.mark.parametrize("fmt", ["band", "deployed", "deployed_fp8"])
+def test_step_paged_fp32_inputs(nk, fmt):
+    """A paged cache of 16-token blocks (shuffled table) and fp32 step inputs."""
+    wl = synth.get_workload("qwen3_8b")
+    _, P = format_params(nk, wl, fmt)
+    run_both(nk, wl, P, fmt, [1, 333, 2048, 1000], 2048, window=700, paged_bs=16, new_dtype=torch.float32, seed=8)
+
+
+@pytest.mark.parametrize("fmt", ["band", "deployed"])
+def test_step_with_sinks_only(nk, fmt):
+    """A band of sink positions only (n_rec = 0): the new token is read from
+    codes, so the step runs as the encode and then the decode."""
+    wl = synth.get_workload("qwen3_8b")
+    _, P = format_params(nk, wl, fmt)
+    run_both(nk, wl, P, fmt, [1, 40, 64, 65, 2048], 2048, n_sink=64, n_rec=0, seed=9)
 
 
 @pytest.mark.parametrize("fmt", ["band", "deployed"])
