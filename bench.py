@@ -318,8 +318,8 @@ def other_workload(nk, torch, dev, case, calls: int):
     step = {}
     if band_sizes:
         # the whole step on the same pools: append a token at seq_len - 1, then
-        # attend.  One launch on the head_dim-128 table kernel (the new token is
-        # the band's last row); the encode, then the decode, at head_dim 64.
+        # attend; one launch on the table kernels when the band's recent part
+        # holds the new token (it is then the band's last row)
         kn = torch.randn((B, H, D), generator=gen, device=dev).to(torch.bfloat16)
         vn = torch.randn((B, H, D), generator=gen, device=dev).to(torch.bfloat16)
         steps_ = [nk.prepare_append_decode(P, layout, kn, vn, q, pk, pv, seq, S, out, ws, window=window,
@@ -330,7 +330,7 @@ def other_workload(nk, torch, dev, case, calls: int):
             sfn(i)
         step = {"step_us": round(back_to_back_us(torch, sfn, calls), 2),
                 "step_per_call_us": pct(timed_calls(torch, sfn, calls)),
-                "step_launches": 1 if D == 128 and band_sizes[1] >= 1 else (3 if sq else 2)}
+                "step_launches": 1 if band_sizes[1] >= 1 else (3 if sq else 2)}
         del steps_
     res = {"workload": case_label(name, layer, key_scale, band_sizes, fp8, sq, wl),
            "batch": B, "seq_len": S, "q_heads": Hq, "kv_heads": H, "head_dim": D,

@@ -294,18 +294,18 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
  *   all other arguments as in nova_kv_decode_attn (params also need t_k).
  *
  * out equals the output of nova_kv_decode_attn over the pools after that
- * append, up to fp32 rounding.  With head_dim 128 on 16-aligned blocks the
- * step is a single kernel launch, in which the workgroups that read the pools
- * also encode the new token and store what nova_kv_encode would:
- *   - plain or fp8 codebooks without a band: the new token is attended from
- *     its codes (its term is added after the split combine instead of inside
- *     a split);
+ * append, up to fp32 rounding.  On 16-aligned blocks the step is a single
+ * kernel launch, in which the workgroups that read the pools also encode the
+ * new token and store what nova_kv_encode would:
  *   - any format (key scale, scalar value arm, fp8) with a band whose n_rec
- *     >= 1: the new token is the band's last row, stored in the launch and
- *     attended exactly from it, as the decode after the encode would.
- * Otherwise (head_dim 64; the key-scale or scalar value format without such a
- * band) the one-token encode and the decode run one after the other on the
- * stream.
+ *     >= 1, at head_dim 128 or 64: the new token is the band's last row,
+ *     stored in the launch and attended exactly from it, as the decode after
+ *     the encode would;
+ *   - head_dim 128, plain or fp8 codebooks, no band: the new token is
+ *     attended from its codes (its term is added after the split combine
+ *     instead of inside a split).
+ * Otherwise the one-token encode and the decode run one after the other on
+ * the stream.
  * batch == 0 is a valid no-op.
  */
 nova_kv_status nova_kv_append_decode_attn(const nova_kv_params *p, const nova_kv_layout *layout,

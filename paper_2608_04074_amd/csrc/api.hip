@@ -323,11 +323,12 @@ nova_kv_status append_step(const nova_kv_params *p, const nova_kv_layout *layout
                                      workspace_bytes, true, a, plan, static_ws, stream);
   if (st != NOVA_KV_OK || batch == 0) return st == NOVA_KV_OK ? ok() : st;
   hipError_t e;
-  // One launch on the head_dim-128 table kernel: in the plain and fp8
-  // formats the new token is attended from its codes; with a band whose
-  // recent part holds it, in any format, it is the band's last row.
+  // One launch on a table kernel.  With a band whose recent part holds the
+  // new token, in any format and at either head_dim, that token is the band's
+  // last row; otherwise (head_dim 128, plain or fp8 codebooks) it is attended
+  // from its codes.
   const bool scaled_format = (p->flags & (NOVA_KV_KEY_SCALE | NOVA_KV_SQ_VALUES)) != 0;
-  const bool fused = plan.use_lut && p->head_dim == 128 && (band ? band->n_rec >= 1 : !scaled_format);
+  const bool fused = plan.use_lut && (band ? band->n_rec >= 1 : p->head_dim == 128 && !scaled_format);
   if (fused) {
     a.append = 1;
     a.k_new = k_new;

@@ -30,6 +30,7 @@
 #include "encode_block.h"
 #include "lut_common.h"
 #include "nova_kv_internal.h"
+#include "step_encode.h"
 
 namespace novakv {
 
@@ -69,14 +70,8 @@ constexpr uint32_t kLdsBytes = kMergeBase + 12 * kMergeFloats * 4;
 // outputs.
 constexpr uint32_t kAuxOwn = kVBase;
 constexpr uint32_t kAuxOut = kVBase + 4 * kD * 4;
-// Fused step with a band: the team's whole-token coefficients [2][128] f64,
-// its min/max words [2][4] f64 and its scalar-arm levels [2][128] bytes,
-// after the two block scratch areas.
-constexpr uint32_t kBandU = kAppendScratch + 2 * sizeof(encblk::Scratch<kD>);
-constexpr uint32_t kBandRed = kBandU + 2 * kD * 8;
-constexpr uint32_t kBandQ = kBandRed + 2 * 4 * 8;
-static_assert(32 * kD * 4 <= 12 * kMergeFloats * 4 && kBandQ + 2 * kD <= kMergeBase + 12 * kMergeFloats * 4,
-              "the q' partial sums and the encoder scratch fit in the merge region");
+static_assert(32 * kD * 4 <= 12 * kMergeFloats * 4 && sizeof(step::Scratch<kD>) <= 12 * kMergeFloats * 4,
+              "the q' partial sums and the encoder team's scratch fit in the merge region");
 static_assert(kLdsBytes <= 160 * 1024, "LDS budget of a workgroup");
 constexpr float kLn2 = 0.693147180559945309f;
 
@@ -157,10 +152,7 @@ __device__ __forceinline__ int items_of_split(const int split, const int n_eff) 
 // All four waves of the team arrive, then each continues once the counter
 // has reached 4 * phase: LDS writes before the call are visible after it.
 __device__ __forceinline__ void team_sync(uint8_t *smem, const int phase) {
-  int *ctr = reinterpret_cast<int *>(smem + kTeamCtr);
-  if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-  while (__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 4 * phase)
-    __builtin_amdgcn_s_sleep(1);
+  step::team_meet(reinterpret_cast<int *>(smem + kTeamCtr), phase);
 }
 
 // The loads of the team's k-th item (thread t = tid - 512 of the team).
@@ -269,137 +261,9 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
   }
 }
 
-// Fused step with a sink-plus-recent band (n_rec >= 1): the new token is the
-// band's last row and is attended exactly, so the team only stores its
-// codes, and its scale (key-scale format) or its levels and (scale, offset)
-// (scalar value arm).  Tasks: the key side as 4 block items, or with the key
-// scale one task (all 128 coefficients, rho, then the 4 blocks' codes); the
-// value side as 4 block items, or in the scalar arm one task.  Task j of the
-// list (keys, then values) goes to split j mod n_eff.  Each task does the
-// one-token encoder's arithmetic (encode_block.h), so both store the same
-// bytes.
-template <bool KS, bool SQ>
-struct BandTasks {
-  static constexpr int kBlocks = kL / encblk::kGroups;
-  static constexpr int kKey = KS ? 1 : kBlocks;
-  static constexpr int kAll = kKey + (SQ ? 1 : kBlocks);
-  // team meetings of task j: its x, then two per block of coefficients and
-  // one for rho (key scale) or two for the levels (scalar arm); a block item
-  // meets twice
-  __device__ static int phases(const int j) {
-    if (j < kKey) return KS ? 2 + 2 * kBlocks : 2;
-    return SQ ? 3 + 2 * kBlocks : 2;
-  }
-  // all of a split's meetings, with the last one after its last task: the
-  // waves waiting for the team to free the merge region count them all
-  __device__ static int phases_of_split(const int split, const int n_eff) {
-    int n = 1;
-    for (int j = split; j < kAll; j += n_eff) n += phases(j);
-    return n;
-  }
-};
-
-// Called by the team's threads only (t = tid - 512).  Tasks alternate between
-// two sets of scratch, so no meeting guards their reuse.
-template <bool KS, bool SQ>
-__device__ __forceinline__ void encode_token_band(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
-                                                  const int split, const int n_eff, const size_t tokoff,
-                                                  const int t, const bool fp8) {
-  using BT = BandTasks<KS, SQ>;
-  encblk::Scratch<kD> *sc = reinterpret_cast<encblk::Scratch<kD> *>(smem + kAppendScratch);  // [2]
-  int phase = 0;
-  auto sync = [&] { team_sync(smem, ++phase); };
-  const size_t elem = (static_cast<size_t>(b) * a.num_kv_heads + kv) * kD + (t & (kD - 1));
-  auto element = [&](const bool key) {  // element t of the token minus k_bar (keys) or of the token (values)
-    const void *src = key ? a.k_new : a.v_new;
-    double x = a.new_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[elem]))
-                          : static_cast<double>(static_cast<const float *>(src)[elem]);
-    if (key) x -= static_cast<double>(a.kbar[kv * kD + t]);
-    return x;
-  };
-  const size_t cw0 = static_cast<size_t>(kv) * kL * kCodebookSize;
-  int k = 0;
-  for (int j = split; j < BT::kAll; j += n_eff, ++k) {
-    encblk::Scratch<kD> &s = sc[k & 1];
-    double *u = reinterpret_cast<double *>(smem + kBandU) + (k & 1) * kD;
-    const bool key = j < BT::kKey;
-    const float *tm = (key ? a.t_k : a.t_v) + static_cast<size_t>(kv) * kD * kD;
-    const void *cb = key ? a.cb_k : a.cb_v;
-    float4 rows[kD / 32];
-    uint2 cw[encblk::kPer];
-    if ((key && KS) || (!key && SQ)) {
-      encblk::load_rows<kD>(t, tm, 0, rows);
-      if (key) encblk::load_codewords(t, cb, fp8, cw0, 0, cw);
-      if (t < kD) s.xs[t] = element(key);
-      sync();
-      encblk::token_coefficients<kD>(t, s, tm, rows, u, sync);
-      if (key) {
-        // rho, then the blocks' codes of the coefficients divided by it (the
-        // next block's codewords requested while one block is searched)
-        if (t == 0) s.wpart[0][0] = encblk::key_scale<kD>(u);
-        sync();
-        const double rho = s.wpart[0][0];
-#pragma unroll
-        for (int bb = 0; bb < BT::kBlocks; ++bb) {
-          uint2 nx[encblk::kPer];
-          if (bb + 1 < BT::kBlocks) encblk::load_codewords(t, cb, fp8, cw0, bb + 1, nx);
-          double uu[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const double v = u[encblk::kCols * bb + 4 * (t >> 5) + i];
-            uu[i] = rho > 0.0 ? v / rho : 0.0;
-          }
-          const int code = encblk::search_codes(t, uu, cw, fp8);
-          if ((t & 31) == 0) a.k_codes_w[tokoff + encblk::kGroups * bb + (t >> 5)] = static_cast<uint8_t>(code);
-          if (bb + 1 < BT::kBlocks) {
-#pragma unroll
-            for (int i = 0; i < encblk::kPer; ++i) cw[i] = nx[i];
-          }
-        }
-        if (t == 0) a.k_scales_w[tokoff / kL] = encblk::bf16_of(rho);
-      } else {
-        double *red = reinterpret_cast<double *>(smem + kBandRed) + (k & 1) * 4;
-        uint8_t *q = smem + kBandQ + (k & 1) * kD;
-        uint16_t sbits, zbits;
-        encblk::sq_levels<kD>(t, u, red, q, sync, sbits, zbits);
-        if (t < kL) a.v_codes_w[tokoff + t] = encblk::sq_byte(q, t);
-        if (t == 0) {
-          a.v_sq_w[(tokoff / kL) * 2] = sbits;
-          a.v_sq_w[(tokoff / kL) * 2 + 1] = zbits;
-        }
-      }
-    } else {
-      const int blk = key ? j : j - BT::kKey;
-      encblk::load_block<kD>(t, tm, cb, fp8, cw0, blk, rows, cw);
-      if (t < kD) s.xs[t] = element(key);
-      sync();
-      encblk::partial_block<kD>(t, s, rows);
-      sync();
-      const int code = encblk::search_block<kD>(t, s, cw, fp8);
-      if ((t & 31) == 0)
-        (key ? a.k_codes_w : a.v_codes_w)[tokoff + encblk::kGroups * blk + (t >> 5)] = static_cast<uint8_t>(code);
-    }
-  }
-  sync();  // every read of the scratch is done: the merge region is free
-}
-
-// Fused step with a band: the new token's key and value rows (bf16: as given,
-// or an fp32 element rounded to nearest even) into its band slot.
-__device__ __forceinline__ void store_new_band_rows(const DecodeArgs &a, const int b, const int kv, const int pos) {
-  const int tid = threadIdx.x;
-  if (tid >= 2 * kD) return;
-  const int side = tid / kD, d = tid % kD;
-  const void *src = side ? a.v_new : a.k_new;
-  const size_t idx = (static_cast<size_t>(b) * a.num_kv_heads + kv) * kD + d;
-  const uint16_t bits = a.new_bf16 ? static_cast<const uint16_t *>(src)[idx]
-                                   : bf16_rne(static_cast<const float *>(src)[idx]);
-  const int nb = a.n_sink + a.n_rec;
-  (side ? a.band_v_w : a.band_k_w)[((static_cast<size_t>(b) * a.num_kv_heads + kv) * nb +
-                                    band_slot(pos, a.n_sink, a.n_rec)) * kD + d] = bits;
-}
-
 // BSTEP: a fused step with a band (APPEND too): the new token is the band's
-// last row, and the team runs encode_token_band.
+// last row, and the team runs step::encode_token (step_encode.h): task j of
+// the new token's encode goes to split j mod n_eff.
 template <int WAVES, bool APPEND, bool KS, bool FP8, bool SQ, bool BSTEP>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int split, const int t0, const int t1, const size_t row0,
@@ -668,9 +532,12 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     if (n_eff > 0 && wave >= 8) {
       const int p = S - 1;
       const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
-      if constexpr (BSTEP)
-        encode_token_band<KS, SQ>(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8);
-      else
+      if constexpr (BSTEP) {
+        int phase = 0;  // shared by every copy of the meeting
+        auto meet = [&] { team_sync(smem, ++phase); };
+        step::encode_token<kD, KS, SQ>(a, *reinterpret_cast<step::Scratch<kD> *>(smem + kAppendScratch), b, kv,
+                                       split, n_eff, tokoff, tid - 512, FP8, meet);
+      } else
         encode_items(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8);
     }
   }
@@ -855,7 +722,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   if constexpr (APPEND) {
     // the merge region holds the encoder team's scratch until its last item
     if (n_eff > 0 && wave < 8) {
-      const int done = 4 * (BSTEP ? BandTasks<KS, SQ>::phases_of_split(split, n_eff) : team_phases(split, n_eff));
+      const int done = 4 * (BSTEP ? step::Tasks<kD, KS, SQ>::phases_of(split, n_eff) : team_phases(split, n_eff));
       int *ctr = reinterpret_cast<int *>(smem + kTeamCtr);
       while (__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < done)
         __builtin_amdgcn_s_sleep(1);
@@ -1405,7 +1272,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
         // a fused step's new token is the band's last row: the split that
         // attends it stores it, and reads it back after the barrier
         if (bfirst + bcount == nband) {
-          store_new_band_rows(a, b, kv, S - 1);
+          step::store_band_rows<kD>(a, b, kv, S - 1);
           __syncthreads();
         }
       }

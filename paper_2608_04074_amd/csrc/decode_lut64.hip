@@ -25,6 +25,7 @@
 #include "band_attention.h"
 #include "lut_common.h"
 #include "nova_kv_internal.h"
+#include "step_encode.h"
 
 namespace novakv {
 
@@ -49,8 +50,14 @@ constexpr uint32_t kAuxPart = kAuxQ + kH * kD * 4;  // 10 KB
 constexpr uint32_t kAuxOwn = kAuxPart;
 constexpr uint32_t kAuxOut = kAuxPart + kH * kD * 4;
 constexpr uint32_t kAuxCtl = kAuxPart + 10240;
-// control words (32-bit): [0] arrival state, [8..16) shifted sink logits, [16..32) own (m, l)
+// control words (32-bit): [0] arrival state, [1] first arrival, [8..16) shifted
+// sink logits, [16..32) own (m, l)
 constexpr uint32_t kLdsBytes = kAuxCtl + 128;
+// One-launch step with a band: the first split to count in encodes the new
+// token with four teams of four waves, in the table region (free once the
+// split's partial is published): the teams' scratch, then their counters.
+constexpr uint32_t kStepCtr = 4 * sizeof(step::Scratch<kD>);
+static_assert(kStepCtr + 16 <= kLutBytes, "the step teams' scratch fits in the table region");
 
 template <int WAVES>
 constexpr uint32_t lds_bytes() {
@@ -82,7 +89,9 @@ __device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, 
   }
 }
 
-template <int WAVES, bool KS, bool FP8, bool SQ>
+// (BSTEP: the kernel's own instantiation, so that each kernel inlines a
+// split pass of its own and the plain kernels compile as without the step)
+template <int WAVES, bool KS, bool FP8, bool SQ, bool BSTEP>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int t0, const int t1, const size_t row0, float4 (&tv)[4]) {
   const uint32_t sbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8_ptr)smem));
@@ -491,7 +500,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 
 // Last split of a (sequence, KV head): log-sum-exp merge of the splits in
 // index order, the sink once (shifted, Lemma S1), division, and out = s_hat t_v^T.
-template <int WAVES>
+template <int WAVES, bool BSTEP>
 __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                              const size_t row0, const int own_split, const bool own_active,
                                              const int S, const int lo, const int tend, const int band_lo,
@@ -506,6 +515,14 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
   constexpr int kVW = 8;  // waves that sum the band's values
   using BL = BandLds<kD, kH, kVW>;
   const int nband = a.band_k ? max(0, sink_end - band_lo) + (S - tend) : 0;
+  if constexpr (BSTEP) {
+    // one-launch step: the new token is the band's last row, stored here and
+    // read back after the barrier
+    if (S > 0) {
+      step::store_band_rows<kD>(a, b, kv, S - 1);
+      __syncthreads();
+    }
+  }
   if (nband > 0) band_attention<kD, kH, WAVES, kVW>(a, smem, b, kv, row0, band_lo, sink_end, tend, S, 0, nband);
   float *bout = reinterpret_cast<float *>(smem + BL::kPart);  // [8][64] band term of the output
   float *shat = reinterpret_cast<float *>(smem + kAuxQ);    // [8][64]
@@ -614,7 +631,10 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
 // One workgroup per (sequence, KV head, split); the arrival protocol is the
 // one of the head_dim-128 kernel (relaxed agent-scope partials and counters,
 // the last split combines, a split finding all others arrived does not publish).
-template <int WAVES, bool KS, bool FP8, bool SQ>
+// BSTEP: the one-launch step with a band (nova_kv_append_decode_attn): the new
+// token is the band's last row, stored by the combining split; the first
+// split to count in stores its codes (step_encode.h).
+template <int WAVES, bool KS, bool FP8, bool SQ, bool BSTEP>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
   const int tid = threadIdx.x;
@@ -636,7 +656,7 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
 
   float4 tv[4];
   if (active) {
-    split_pass<WAVES, KS, FP8, SQ>(a, smem, b, kv, t0, t1, row0, tv);
+    split_pass<WAVES, KS, FP8, SQ, BSTEP>(a, smem, b, kv, t0, t1, row0, tv);
   } else {
     load_tv_rows(a, kv, tv);
   }
@@ -667,37 +687,74 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
     }
     __syncthreads();
     if (tid == kCtl) {
-      const int last = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
-                       a.n_split - 1;
-      if (last) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      ctl[0] = last;
+      if constexpr (BSTEP) {
+        const int old = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (old == a.n_split - 1) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ctl[0] = old == a.n_split - 1;
+        ctl[1] = old == 0;
+      } else {
+        const int last = __hip_atomic_fetch_add(a.counters + bk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                         a.n_split - 1;
+        if (last) __hip_atomic_store(a.counters + bk, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ctl[0] = last;
+      }
     }
     __syncthreads();
-    if (ctl[0] == 0) return;
+    if constexpr (!BSTEP) {
+      if (ctl[0] == 0) return;
+    }
   }
-  combine_unit<WAVES>(a, smem, b, kv, row0, split, active, S, lo, tend, att_lo, spn.sink_end, tv);
+  if constexpr (BSTEP) {
+    // the first split to count in (the only one without splits) encodes the
+    // new token while the others finish: team tid / 256 takes tasks team,
+    // team + 4, ...
+    if ((a.n_split == 1 || ctl[1] != 0) && S > 0) {
+      int *ctr = reinterpret_cast<int *>(smem + kStepCtr);
+      if (tid < 4) ctr[tid] = 0;
+      __syncthreads();
+      const int team = tid >> 8, p = S - 1;
+      const int bsz = a.layout.block_size;
+      const int bs_shift = (bsz & (bsz - 1)) == 0 ? __builtin_ctz(bsz) : -1;
+      const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
+      int phase = 0;  // shared by every copy of the meeting
+      auto meet = [&] { step::team_meet(ctr + team, ++phase); };
+      step::encode_token<kD, KS, SQ>(a, reinterpret_cast<step::Scratch<kD> *>(smem)[team], b, kv, team, 4, tokoff,
+                                     tid & 255, FP8, meet);
+      __syncthreads();  // the table region is free again
+    }
+    if (a.n_split > 1 && ctl[0] == 0) return;
+  }
+  combine_unit<WAVES, BSTEP>(a, smem, b, kv, row0, split, active, S, lo, tend, att_lo, spn.sink_end, tv);
 }
 
 }  // namespace
 
-hipError_t launch_decode_lut64(const DecodeArgs &a, hipStream_t stream) {
-  constexpr int W = 16;  // 4 waves per SIMD: the kernel fits in 128 VGPRs
-  const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
-  const dim3 block(W * 64);
+template <bool BSTEP>
+void launch_d64(const DecodeArgs &a, const dim3 grid, const dim3 block, hipStream_t stream) {
+  constexpr int W = 16;
   if (a.v_sq) {  // the scalar value arm (keys in either codebook format)
     if (a.k_scales)
-      a.cb_fp8 ? decode_lut_d64<W, true, true, true><<<grid, block, 0, stream>>>(a)
-               : decode_lut_d64<W, true, false, true><<<grid, block, 0, stream>>>(a);
+      a.cb_fp8 ? decode_lut_d64<W, true, true, true, BSTEP><<<grid, block, 0, stream>>>(a)
+               : decode_lut_d64<W, true, false, true, BSTEP><<<grid, block, 0, stream>>>(a);
     else
-      a.cb_fp8 ? decode_lut_d64<W, false, true, true><<<grid, block, 0, stream>>>(a)
-               : decode_lut_d64<W, false, false, true><<<grid, block, 0, stream>>>(a);
+      a.cb_fp8 ? decode_lut_d64<W, false, true, true, BSTEP><<<grid, block, 0, stream>>>(a)
+               : decode_lut_d64<W, false, false, true, BSTEP><<<grid, block, 0, stream>>>(a);
   } else if (a.k_scales) {
-    a.cb_fp8 ? decode_lut_d64<W, true, true, false><<<grid, block, 0, stream>>>(a)
-             : decode_lut_d64<W, true, false, false><<<grid, block, 0, stream>>>(a);
+    a.cb_fp8 ? decode_lut_d64<W, true, true, false, BSTEP><<<grid, block, 0, stream>>>(a)
+             : decode_lut_d64<W, true, false, false, BSTEP><<<grid, block, 0, stream>>>(a);
   } else {
-    a.cb_fp8 ? decode_lut_d64<W, false, true, false><<<grid, block, 0, stream>>>(a)
-             : decode_lut_d64<W, false, false, false><<<grid, block, 0, stream>>>(a);
+    a.cb_fp8 ? decode_lut_d64<W, false, true, false, BSTEP><<<grid, block, 0, stream>>>(a)
+             : decode_lut_d64<W, false, false, false, BSTEP><<<grid, block, 0, stream>>>(a);
   }
+}
+
+hipError_t launch_decode_lut64(const DecodeArgs &a, hipStream_t stream) {
+  // 16 waves, 4 per SIMD: the kernel fits in 128 VGPRs.  A step (append) runs
+  // here only with a band whose recent part holds the new token.
+  if (a.append && !(a.band_k && a.n_rec >= 1)) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
+  const dim3 block(16 * 64);
+  a.append ? launch_d64<true>(a, grid, block, stream) : launch_d64<false>(a, grid, block, stream);
   return hipGetLastError();
 }
 

@@ -1,9 +1,9 @@
 """The one-launch step with a sink-plus-recent band, in every format.
 
 With a band whose recent part holds the new token, nova_kv_append_decode_attn
-runs as one launch of the head_dim-128 table kernel in the plain, fp8,
-key-scale and scalar-value formats and their combinations: the encoder team
-stores the new token's codes (and scale, levels, (scale, offset)), the split
+runs as one launch of a table kernel (head_dim 128 or 64) in the plain, fp8,
+key-scale and scalar-value formats and their combinations: encoder teams
+store the new token's codes (and scale, levels, (scale, offset)), the split
 that attends the band's last row stores that row, and the token is attended
 exactly from it.
 
@@ -169,6 +169,20 @@ def test_step_with_sinks_only(nk, fmt):
     run_both(nk, wl, P, fmt, [1, 40, 64, 65, 2048], 2048, n_sink=64, n_rec=0, seed=9)
 
 
+@pytest.mark.parametrize("fmt", ["band", "key_scale", "sq_values", "deployed", "deployed_fp8"])
+def test_head_dim_64_step(nk, fmt):
+    """The GPT-OSS shape (head_dim 64, eight query heads per KV head, learned
+    sinks) on its table kernel: the first split to count in encodes the new
+    token, the combining split stores and attends its band row.  Ragged
+    lengths, a window of 128, many splits per KV head."""
+    wl = synth.get_workload("gptoss_pair")
+    _, P = format_params(nk, wl, fmt)
+    sinks = synth.sink_logits(wl, 0)
+    run_both(nk, wl, P, fmt, [1, 40, 330, 2048], 2048, sinks=sinks)
+    run_both(nk, wl, P, fmt, [2048, 1500, 700, 321], 2048, window=128, sinks=sinks, seed=5)
+    run_both(nk, wl, P, fmt, [32768, 30000], 32768, sinks=sinks, seed=6)
+
+
 @pytest.mark.parametrize("fmt", ["band", "deployed"])
 @pytest.mark.parametrize("B,S", [(8, 16384), (1, 16384)], ids=["bench_shape", "one_sequence"])
 def test_step_matches_at_many_splits(nk, fmt, B, S):
@@ -180,8 +194,9 @@ def test_step_matches_at_many_splits(nk, fmt, B, S):
     run_both(nk, wl, P, fmt, [S - 7 * i for i in range(B)], S, sinks=sinks)
 
 
-def test_deployed_step_against_the_oracle(nk):
-    wl = synth.get_workload("qwen3_8b")
+@pytest.mark.parametrize("shape", ["qwen3_8b", "gptoss_pair"])
+def test_deployed_step_against_the_oracle(nk, shape):
+    wl = synth.get_workload(shape)
     params, P = format_params(nk, wl, "deployed")
     n_sink, n_rec = 64, 256
     B, cap = 4, 2304
@@ -206,7 +221,7 @@ def test_deployed_step_against_the_oracle(nk):
     sinks = np.random.default_rng(4).standard_normal(wl.num_q_heads).astype(np.float32)  # learned-sink logits
     pk, pv, pks, psq = dev(ck, torch.uint8), dev(cv, torch.uint8), dev_bits(hks), dev_bits(hsq)
     bk, bv = dev_bits(band_k), dev_bits(band_v)
-    say("deployed step against the oracle")
+    say(f"deployed step against the oracle {shape}")
     out = nk.append_decode_attn(P, nk.CacheLayout.contiguous(cap), dev(kn, torch.bfloat16), dev(vn, torch.bfloat16),
                                 dev(q, torch.bfloat16), pk, pv, dev(lens, torch.int32), cap,
                                 sinks=dev(sinks, torch.float32), k_scales=pks, v_sq=psq,
@@ -229,13 +244,13 @@ def test_deployed_step_against_the_oracle(nk):
             assert np.array_equal(hbk[b, kv, sl], ocodec.bf16_bits(kb[p])), f"b{b} kv{kv}: band key row"
             assert np.array_equal(hbv[b, kv, sl], ocodec.bf16_bits(vb[p])), f"b{b} kv{kv}: band value row"
             okk, ogk, _, _, _, rho = ocodec.encode_tokens_scaled(kb[p][None], vb[p][None], hp)
-            compare_codes(hk[b, kv, p:p + 1], okk, ogk, f"deployed step b{b} kv{kv} K")
+            compare_codes(hk[b, kv, p:p + 1], okk, ogk, f"deployed step {shape} b{b} kv{kv} K")
             assert near_bits(hs[b, kv, p:p + 1], rho).all(), f"b{b} kv{kv}: key scale"
             compare_sq(hv[b, kv, p:p + 1], hq[b, kv, p:p + 1, 0], hq[b, kv, p:p + 1, 1], vb[p][None], hp["t_v"],
-                       f"deployed step b{b} kv{kv} V")
+                       f"deployed step {shape} b{b} kv{kv} V")
             heads = slice(kv * G, (kv + 1) * G)
             ref[b, heads] = oatt.decode_rows(q[b, heads], hk[b, kv, :S], hv[b, kv, :S], hp, scale, 0, sinks[heads],
                                              scales_k=ocodec.bf16_value(hs[b, kv, :S]),
                                              band=(n_sink, n_rec, kb[:S], vb[:S]),
                                              sq_v=(hq[b, kv, :S, 0], hq[b, kv, :S, 1]))
-    assert_outputs_close(out.reshape(-1, D), ref.reshape(-1, D), what="deployed step qwen3_8b")
+    assert_outputs_close(out.reshape(-1, D), ref.reshape(-1, D), what=f"deployed step {shape}")
