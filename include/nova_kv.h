@@ -64,10 +64,11 @@ typedef enum {
  * D = head_dim, L = D / group_dim, K = codebook_size.
  *
  *   kbar      [Hkv][D]      fp32  key mean k_bar
- *   t_k       [Hkv][D][D]   fp32  key transform R_K with the grouping folded
- *                                 into its columns:  r = (k - k_bar) @ t_k
- *   t_k_inv_t [Hkv][D][D]   fp32  R_K^{-T} (same column order): q' = q @ t_k_inv_t
- *   t_v       [Hkv][D][D]   fp32  value transform R_V (orthogonal, columns
+ *   t_k       [Hkv][D][D]   fp32 (or bf16, below)  key transform R_K with the
+ *                                 grouping folded into its columns:
+ *                                 r = (k - k_bar) @ t_k
+ *   t_k_inv_t [Hkv][D][D]   R_K^{-T} (same column order): q' = q @ t_k_inv_t
+ *   t_v       [Hkv][D][D]   value transform R_V (orthogonal, columns
  *                                 grouped):  s = v @ t_v,  v_hat = s_hat @ t_v^T
  *   cb_k      [Hkv][L][K][g] fp16 bit patterns (uint16), or fp8 E4M3 bytes
  *                           with NOVA_KV_FP8_CODEBOOKS: key codebook of each group
@@ -77,7 +78,7 @@ typedef enum {
  * K = 256, D in {64, 128}.  Every array must be 16-byte aligned
  * (NOVA_KV_ERR_INVALID_ARG otherwise).
  *
- *   flags     0 or any combination of the three formats below.
+ *   flags     0 or any combination of the four formats below.
  *             NOVA_KV_KEY_SCALE: the key-scale format (paper: Algorithm
  *             2 normalizes r_j by rho_j = ||r_j||_2 / sqrt(D) before the
  *             codebooks are trained; Sec. "Bit rate": a BF16 scale per token;
@@ -99,12 +100,16 @@ typedef enum {
  *             (q = 0 when the stored scale is 0); coordinate 4g + j sits in
  *             bits 2j, 2j+1 of byte g of the token's value code row.  cb_v is
  *             then unused (may be NULL) and every call takes a v_sq pool.
- *             At head_dim 64 the decode uses the split-K kernels in this format.
+ *             NOVA_KV_BF16_TRANSFORMS: t_k, t_k_inv_t and t_v are bf16 bit
+ *             patterns (uint16) instead of fp32 (paper: Sec. "Calibration",
+ *             the bases are cast to bfloat16 when loaded into the serving
+ *             engine); every kernel reads them as those exact values.
  *             Other bits are reserved (NOVA_KV_ERR_UNSUPPORTED).
  */
 #define NOVA_KV_KEY_SCALE 1u
 #define NOVA_KV_FP8_CODEBOOKS 2u
 #define NOVA_KV_SQ_VALUES 4u
+#define NOVA_KV_BF16_TRANSFORMS 8u
 
 typedef struct {
     int32_t num_kv_heads;
@@ -113,9 +118,9 @@ typedef struct {
     int32_t codebook_size;
     uint32_t flags;
     const float *kbar;
-    const float *t_k;
-    const float *t_k_inv_t;
-    const float *t_v;
+    const void *t_k;        /* fp32, or bf16 bit patterns with NOVA_KV_BF16_TRANSFORMS */
+    const void *t_k_inv_t;
+    const void *t_v;
     const void *cb_k;
     const void *cb_v;
 } nova_kv_params;

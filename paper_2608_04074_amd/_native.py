@@ -24,6 +24,7 @@ NOVA_KV_BF16 = 1
 NOVA_KV_KEY_SCALE = 1  # nova_kv_params.flags: the key-scale format
 NOVA_KV_FP8_CODEBOOKS = 2  # nova_kv_params.flags: codebooks stored as fp8 E4M3 bytes
 NOVA_KV_SQ_VALUES = 4  # nova_kv_params.flags: the scalar (per-token affine INT2) value arm
+NOVA_KV_BF16_TRANSFORMS = 8  # nova_kv_params.flags: t_k, t_k_inv_t and t_v stored as bf16
 
 EXPORTED = (
     "nova_kv_encode",

@@ -59,6 +59,8 @@ class NovaKVParams:
     in the same format).  ``sq_values`` selects the scalar value arm (values
     as per-token affine INT2 in the rotation t_v; cb_v unused, may be None),
     and every call then takes a ``v_sq`` pool of shape ``sq_pool_shape``.
+    The transforms t_k, t_k_inv_t and t_v are fp32, or all three bf16 (the
+    paper's serving storage of the bases), read as exactly those values.
     """
 
     def __init__(self, kbar, t_k, t_k_inv_t, t_v, cb_k, cb_v, group_dim: int = 4,
@@ -67,7 +69,10 @@ class NovaKVParams:
         L = d // group_dim
         _require(kbar, "kbar", (torch.float32,), hkv * d)
         for name, t in (("t_k", t_k), ("t_k_inv_t", t_k_inv_t), ("t_v", t_v)):
-            _require(t, name, (torch.float32,), hkv * d * d)
+            _require(t, name, (torch.float32, torch.bfloat16), hkv * d * d)
+        if not t_k.dtype == t_k_inv_t.dtype == t_v.dtype:
+            raise TypeError("t_k, t_k_inv_t and t_v must have the same storage (fp32, or bf16)")
+        self.bf16_transforms = t_k.dtype == torch.bfloat16
         self.sq_values = bool(sq_values)
         if self.sq_values and cb_v is None:
             cb_v = cb_k  # unused by the scalar value arm
@@ -83,7 +88,8 @@ class NovaKVParams:
         self.key_scale = bool(key_scale)
         flags = (nat.NOVA_KV_KEY_SCALE if self.key_scale else 0) | \
             (nat.NOVA_KV_FP8_CODEBOOKS if self.fp8_codebooks else 0) | \
-            (nat.NOVA_KV_SQ_VALUES if self.sq_values else 0)
+            (nat.NOVA_KV_SQ_VALUES if self.sq_values else 0) | \
+            (nat.NOVA_KV_BF16_TRANSFORMS if self.bf16_transforms else 0)
         self._c = nat.Params(hkv, d, group_dim, codebook_size, flags, kbar.data_ptr(), t_k.data_ptr(),
                              t_k_inv_t.data_ptr(), t_v.data_ptr(), cb_k.data_ptr(),
                              cb_v.data_ptr())
@@ -94,11 +100,13 @@ class NovaKVParams:
 
     @classmethod
     def from_arrays(cls, arrays: dict, device="cuda", key_scale: bool = False,
-                    sq_values: bool = False) -> "NovaKVParams":
+                    sq_values: bool = False, bf16_transforms: bool = False) -> "NovaKVParams":
         """From host arrays: kbar/t_k/t_k_inv_t/t_v float32, cb_k/cb_v float16, or uint8
-        fp8 E4M3 codes ([Hkv][...])."""
-        f32 = {k: torch.as_tensor(arrays[k]).to(torch.float32).contiguous().to(device)
-               for k in ("kbar", "t_k", "t_k_inv_t", "t_v")}
+        fp8 E4M3 codes ([Hkv][...]).  bf16_transforms: t_k, t_k_inv_t and t_v are
+        stored as bf16 (rounded to nearest even from fp32)."""
+        tdt = torch.bfloat16 if bf16_transforms else torch.float32
+        f32 = {k: torch.as_tensor(arrays[k]).to(torch.float32).to(torch.float32 if k == "kbar" else tdt)
+               .contiguous().to(device) for k in ("kbar", "t_k", "t_k_inv_t", "t_v")}
         f16 = {"cb_v": None}
         for k in ("cb_k", "cb_v"):
             if arrays.get(k) is None:

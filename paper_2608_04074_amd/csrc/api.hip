@@ -129,6 +129,7 @@ nova_kv_status nova_kv_encode(const nova_kv_params *p, const nova_kv_layout *lay
   a.kbar = p->kbar;
   a.t_k = p->t_k;
   a.t_v = p->t_v;
+  a.t_bf16 = (p->flags & NOVA_KV_BF16_TRANSFORMS) ? 1 : 0;
   a.cb_k = p->cb_k;
   a.cb_v = p->cb_v;
   a.cb_fp8 = (p->flags & NOVA_KV_FP8_CODEBOOKS) ? 1 : 0;
@@ -225,6 +226,7 @@ nova_kv_status prepare_decode(const nova_kv_params *p, const nova_kv_layout *lay
   a.kbar = p->kbar;
   a.t_k_inv_t = p->t_k_inv_t;
   a.t_v = p->t_v;
+  a.t_bf16 = (p->flags & NOVA_KV_BF16_TRANSFORMS) ? 1 : 0;
   a.cb_k = p->cb_k;
   a.cb_v = p->cb_v;
   a.cb_fp8 = (p->flags & NOVA_KV_FP8_CODEBOOKS) ? 1 : 0;
@@ -354,6 +356,7 @@ nova_kv_status append_step(const nova_kv_params *p, const nova_kv_layout *layout
     ea.kbar = p->kbar;
     ea.t_k = p->t_k;
     ea.t_v = p->t_v;
+    ea.t_bf16 = (p->flags & NOVA_KV_BF16_TRANSFORMS) ? 1 : 0;
     ea.cb_k = p->cb_k;
     ea.cb_v = p->cb_v;
     ea.cb_fp8 = (p->flags & NOVA_KV_FP8_CODEBOOKS) ? 1 : 0;

@@ -48,10 +48,10 @@ __global__ void __launch_bounds__(D) decode_prologue(DecodeArgs a) {
   float dotk = wave_sum(qv * a.kbar[kv * D + tid]);
   if ((tid & 63) == 0) red[tid >> 6] = dotk;
   __syncthreads();
-  const float *tk = a.t_k_inv_t + static_cast<size_t>(kv) * D * D;
+  const void *tk = transform_of(a.t_k_inv_t, kv, D, a.t_bf16);
   float acc = 0.f;
 #pragma unroll 16
-  for (int d = 0; d < D; ++d) acc = fmaf(qsh[d], tk[d * D + tid], acc);
+  for (int d = 0; d < D; ++d) acc = fmaf(qsh[d], t1_value(tk, static_cast<size_t>(d) * D + tid, a.t_bf16), acc);
   a.qp[static_cast<size_t>(bh) * D + tid] = acc * a.qscale;
   if (tid == 0) {
     float s = 0.f;
@@ -378,14 +378,13 @@ __global__ void __launch_bounds__(256) decode_combine(DecodeArgs a) {
   // thread -> (output coordinate d, half of the heads)
   constexpr int HALVES = 256 / D;
   const int d = tid % D, part = tid / D;
-  const float4 *tv = reinterpret_cast<const float4 *>(a.t_v + static_cast<size_t>(kv) * D * D +
-                                                      static_cast<size_t>(d) * D);
+  const void *tv = transform_of(a.t_v, kv, D, a.t_bf16);
   float o[kMaxGqa];
 #pragma unroll
   for (int h = 0; h < kMaxGqa; ++h) o[h] = 0.f;
 #pragma unroll 8
   for (int j4 = 0; j4 < D / 4; ++j4) {
-    const float4 w = tv[j4];
+    const float4 w = t4_value(load_t4(tv, static_cast<size_t>(d) * D + 4 * j4, a.t_bf16), a.t_bf16);
 #pragma unroll
     for (int h = 0; h < kMaxGqa; ++h) {
       if (h % HALVES == part && h < G) {

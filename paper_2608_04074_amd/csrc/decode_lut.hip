@@ -101,13 +101,13 @@ __device__ __forceinline__ size_t subtile_offset(const DecodeArgs &a, int b, int
 // the split's partials (max in natural-log units, denominator, accumulator).
 // Thread t < 512 of a workgroup holds row (t mod 128) of t_v, columns
 // 32 * (t / 128) .. +31, for the inverse value transform of the combine.
-__device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, float4 (&tv)[8]) {
+template <bool TBF>
+__device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, T4 (&tv)[8]) {
   const int tid = threadIdx.x;
   if (tid < 512) {
-    const float4 *row = reinterpret_cast<const float4 *>(a.t_v + (static_cast<size_t>(kv) * kD + (tid & (kD - 1))) * kD) +
-                        8 * (tid >> 7);
+    const size_t row = (static_cast<size_t>(kv) * kD + (tid & (kD - 1))) * kD + 32 * (tid >> 7);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) tv[i] = row[i];
+    for (int i = 0; i < 8; ++i) tv[i] = load_t4(a.t_v, row + 4 * i, TBF);
   }
 }
 
@@ -157,18 +157,18 @@ __device__ __forceinline__ void team_sync(uint8_t *smem, const int phase) {
 
 // The loads of the team's k-th item (thread t = tid - 512 of the team).
 struct ItemRegs {
-  float4 trow[kD / 32];
+  T4 trow[kD / 32];
   uint2 cw[encblk::kPer];
   double x;  // thread t < D: element t of the token minus k_bar (keys) or of the token (values)
 };
 
 // The transform columns and the token element of the item (its rows).
+template <bool TBF>
 __device__ __forceinline__ void load_item_rows(const DecodeArgs &a, const int b, const int kv, const int split,
                                                const int n_eff, const int k, const int t, ItemRegs &r) {
   const int item = split + k * n_eff;
   const int side = item >> 2, blk = item & 3;
-  const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * kD * kD;
-  encblk::load_rows<kD>(t, tm, blk, r.trow);
+  encblk::load_rows<kD>(t, transform_of(side == 0 ? a.t_k : a.t_v, kv, kD, TBF), TBF, blk, r.trow);
   if (t < kD) {
     const void *src = side == 0 ? a.k_new : a.v_new;
     const size_t idx = (static_cast<size_t>(b) * a.num_kv_heads + kv) * kD + t;
@@ -188,9 +188,10 @@ __device__ __forceinline__ void load_item_cw(const DecodeArgs &a, const int kv, 
   encblk::load_codewords(t, side == 0 ? a.cb_k : a.cb_v, fp8, static_cast<size_t>(kv) * kL * 256, blk, r.cw);
 }
 
+template <bool TBF>
 __device__ __forceinline__ void load_item(const DecodeArgs &a, const int b, const int kv, const int split,
                                           const int n_eff, const int k, const int t, ItemRegs &r, const bool fp8) {
-  load_item_rows(a, b, kv, split, n_eff, k, t, r);
+  load_item_rows<TBF>(a, b, kv, split, n_eff, k, t, r);
   load_item_cw(a, kv, split, n_eff, k, t, r, fp8);
 }
 
@@ -211,6 +212,7 @@ __device__ __forceinline__ int team_phases(const int split, const int n_eff) {
 // stored codes, res[32 k + 4 gg + h]), a value block's coordinates
 // (res[32 k + 4 gg + i]).  After the last item thread h < G of the team sums
 // each key block's head h over the groups in order, into res[32 k + h].
+template <bool TBF>
 __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                              const int split, const int n_eff, const size_t tokoff, const int t,
                                              const bool fp8) {
@@ -226,7 +228,7 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
     encblk::Scratch<kD> &s = sc[k & 1];
     if (t < kD) s.xs[t] = ri.x;
     team_sync(smem, ++phase);
-    encblk::partial_block<kD>(t, s, ri.trow);
+    encblk::partial_block<kD>(t, s, ri.trow, TBF);
     team_sync(smem, ++phase);
     const int code = encblk::search_block<kD>(t, s, ri.cw, fp8);
     const int gl = t >> 5, lr = t & 31;
@@ -246,7 +248,7 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
   };
   for (int k = 0; k < nmine; ++k) {
     ItemRegs r;
-    load_item(a, b, kv, split, n_eff, k, t, r, fp8);
+    load_item<TBF>(a, b, kv, split, n_eff, k, t, r, fp8);
     encode_one(k, r);
   }
   team_sync(smem, ++phase);
@@ -264,10 +266,10 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
 // BSTEP: a fused step with a band (APPEND too): the new token is the band's
 // last row, and the team runs step::encode_token (step_encode.h): task j of
 // the new token's encode goes to split j mod n_eff.
-template <int WAVES, bool APPEND, bool KS, bool FP8, bool SQ, bool BSTEP>
+template <int WAVES, bool APPEND, bool KS, bool FP8, bool SQ, bool BSTEP, bool TBF>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                            const int split, const int t0, const int t1, const size_t row0,
-                                           const int rot, const int n_eff, const int S, float4 (&tv)[8]) {
+                                           const int rot, const int n_eff, const int S, T4 (&tv)[8]) {
   const uint32_t sbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8_ptr)smem));
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -369,12 +371,12 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     // converted only when it is stored
     const size_t qi = (row0 + min(tid >> 7, G - 1)) * kD + (tid & (kD - 1));
     uint32_t qword = 0;
-    float4 trow[8];
+    T4 trow[8];
     if (tid < 512) {
       qword = a.q_bf16 ? reinterpret_cast<const uint32_t *>(a.q)[qi >> 1] : reinterpret_cast<const uint32_t *>(a.q)[qi];
-      const float4 *tk = reinterpret_cast<const float4 *>(a.t_k_inv_t + (static_cast<size_t>(kv) * kD + 8 * jq) * kD) + e4;
+      const size_t tk = (static_cast<size_t>(kv) * kD + 8 * jq) * kD + 4 * e4;
 #pragma unroll
-      for (int r = 0; r < 8; ++r) trow[r] = tk[r * (kD / 4)];
+      for (int r = 0; r < 8; ++r) trow[r] = load_t4(a.t_k_inv_t, tk + r * kD, TBF);
     }
     // table waves: group set (wave & 1) of 16 groups, code range 64*(wave >> 1) .. +63
     const bool lut_wave = wave < 8;
@@ -454,10 +456,11 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
         const float qq[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
-          acc[hh].x = fmaf(qq[r], trow[r].x, acc[hh].x);
-          acc[hh].y = fmaf(qq[r], trow[r].y, acc[hh].y);
-          acc[hh].z = fmaf(qq[r], trow[r].z, acc[hh].z);
-          acc[hh].w = fmaf(qq[r], trow[r].w, acc[hh].w);
+          const float4 tr = t4_value(trow[r], TBF);
+          acc[hh].x = fmaf(qq[r], tr.x, acc[hh].x);
+          acc[hh].y = fmaf(qq[r], tr.y, acc[hh].y);
+          acc[hh].z = fmaf(qq[r], tr.z, acc[hh].z);
+          acc[hh].w = fmaf(qq[r], tr.w, acc[hh].w);
         }
       }
       // lanes l and l + 32 hold rows of the same columns: fold them, one part per wave
@@ -535,10 +538,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       if constexpr (BSTEP) {
         int phase = 0;  // shared by every copy of the meeting
         auto meet = [&] { team_sync(smem, ++phase); };
-        step::encode_token<kD, KS, SQ>(a, *reinterpret_cast<step::Scratch<kD> *>(smem + kAppendScratch), b, kv,
+        step::encode_token<kD, KS, SQ, TBF>(a, *reinterpret_cast<step::Scratch<kD> *>(smem + kAppendScratch), b, kv,
                                        split, n_eff, tokoff, tid - 512, FP8, meet);
       } else
-        encode_items(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8);
+        encode_items<TBF>(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8);
     }
   }
 
@@ -718,7 +721,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   // ends, before the arrival is known: their latency hides behind the waves
   // still in the loop and the merge, and the last arrival finds them in
   // registers.
-  load_tv_rows(a, kv, tv);
+  load_tv_rows<TBF>(a, kv, tv);
   if constexpr (APPEND) {
     // the merge region holds the encoder team's scratch until its last item
     if (n_eff > 0 && wave < 8) {
@@ -906,11 +909,11 @@ __device__ __forceinline__ void clear_slots(uint64_t *base, const int n, const i
   }
 }
 
-template <int WAVES, bool APPEND, bool BSTEP>
+template <int WAVES, bool APPEND, bool BSTEP, bool TBF>
 __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                              const int bk, const size_t row0, const int own_split, const int S,
                                              const int lo, const int tend, const int n_eff, const int band_lo,
-                                             const int sink_end, const float4 (&tv)[8], const Slots sl) {
+                                             const int sink_end, const T4 (&tv)[8], const Slots sl) {
   const int tid = threadIdx.x;
   const int G = a.gqa;
   // Sink-plus-recent band: positions [band_lo, sink_end) and [tend, S) (the
@@ -1088,10 +1091,11 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
       float x = 0.f;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        x = fmaf(sv[i].x, tv[i].x, x);
-        x = fmaf(sv[i].y, tv[i].y, x);
-        x = fmaf(sv[i].z, tv[i].z, x);
-        x = fmaf(sv[i].w, tv[i].w, x);
+        const float4 t = t4_value(tv[i], TBF);
+        x = fmaf(sv[i].x, t.x, x);
+        x = fmaf(sv[i].y, t.y, x);
+        x = fmaf(sv[i].z, t.z, x);
+        x = fmaf(sv[i].w, t.w, x);
       }
       o[h] = x;
     }
@@ -1219,7 +1223,8 @@ __device__ __forceinline__ void merge_group(const DecodeArgs &a, uint8_t *smem, 
 // partial to the exchange and counts its arrival; the last one combines.
 // The arrival counters live in the workspace and the last split resets its
 // counter to 0, so a decode step is a single launch.
-template <int WAVES, bool APPEND, bool KS, bool FP8, bool SQ, bool BSTEP>
+// TBF: the transforms are stored as bf16 (NOVA_KV_BF16_TRANSFORMS).
+template <int WAVES, bool APPEND, bool KS, bool FP8, bool SQ, bool BSTEP, bool TBF>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
   static_assert(!BSTEP || APPEND, "a band step is a fused step");
   static_assert(!APPEND || BSTEP || !(KS || SQ), "without a band the fused step serves the plain and fp8 formats");
@@ -1256,8 +1261,8 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
     items = split < n_eff;
   }
 
-  float4 tv[8];
-  split_pass<WAVES, APPEND, KS, FP8, SQ, BSTEP>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
+  T4 tv[8];
+  split_pass<WAVES, APPEND, KS, FP8, SQ, BSTEP, TBF>(a, smem, b, kv, split, t0, max(t0, t1), row0, rest, items ? n_eff : 0, S, tv);
   // Sink-plus-recent band: this split's share of the band rows, attended in
   // the table's LDS region (free after the split pass) and published beside
   // the split's partial; one CU would read the whole band at a fraction of
@@ -1324,9 +1329,9 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d128(DecodeArgs a) {
     if (ctl[0] == 0) return;
     const Slots gs{a.xgrp + static_cast<size_t>(bk) * a.n_group * kXchSlotWords, a.n_group, split / a.group_size,
                    true};
-    combine_unit<WAVES, APPEND, BSTEP>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv, gs);
+    combine_unit<WAVES, APPEND, BSTEP, TBF>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv, gs);
   } else {
-    combine_unit<WAVES, APPEND, BSTEP>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv,
+    combine_unit<WAVES, APPEND, BSTEP, TBF>(a, smem, b, kv, bk, row0, split, S, lo, tend, n_eff, att_lo, spn.sink_end, tv,
                                 Slots{xs, a.n_split, split, false});
   }
 }
@@ -1391,20 +1396,33 @@ int plan_b_chunk(int batch, int num_kv_heads, int n_split) {
   return bc;
 }
 
-template <bool APPEND, bool KS, bool BSTEP>
+template <bool APPEND, bool KS, bool BSTEP, bool TBF>
 void launch_d128(const DecodeArgs &a, const dim3 grid, const dim3 block, hipStream_t stream) {
   constexpr int W = 12;
   if (a.v_sq) {
     if (a.cb_fp8)
-      decode_lut_d128<W, APPEND, KS, true, true, BSTEP><<<grid, block, 0, stream>>>(a);
+      decode_lut_d128<W, APPEND, KS, true, true, BSTEP, TBF><<<grid, block, 0, stream>>>(a);
     else
-      decode_lut_d128<W, APPEND, KS, false, true, BSTEP><<<grid, block, 0, stream>>>(a);
+      decode_lut_d128<W, APPEND, KS, false, true, BSTEP, TBF><<<grid, block, 0, stream>>>(a);
   } else {
     if (a.cb_fp8)
-      decode_lut_d128<W, APPEND, KS, true, false, BSTEP><<<grid, block, 0, stream>>>(a);
+      decode_lut_d128<W, APPEND, KS, true, false, BSTEP, TBF><<<grid, block, 0, stream>>>(a);
     else
-      decode_lut_d128<W, APPEND, KS, false, false, BSTEP><<<grid, block, 0, stream>>>(a);
+      decode_lut_d128<W, APPEND, KS, false, false, BSTEP, TBF><<<grid, block, 0, stream>>>(a);
   }
+}
+
+template <bool TBF>
+void launch_d128_storage(const DecodeArgs &a, const dim3 grid, const dim3 block, hipStream_t stream) {
+  if (a.append && a.band_k)
+    a.k_scales ? launch_d128<true, true, true, TBF>(a, grid, block, stream)
+               : launch_d128<true, false, true, TBF>(a, grid, block, stream);
+  else if (a.append)  // plain or fp8 codebooks (checked by the caller)
+    a.cb_fp8 ? decode_lut_d128<12, true, false, true, false, false, TBF><<<grid, block, 0, stream>>>(a)
+             : decode_lut_d128<12, true, false, false, false, false, TBF><<<grid, block, 0, stream>>>(a);
+  else
+    a.k_scales ? launch_d128<false, true, false, TBF>(a, grid, block, stream)
+               : launch_d128<false, false, false, TBF>(a, grid, block, stream);
 }
 
 hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream) {
@@ -1413,15 +1431,7 @@ hipError_t launch_decode_lut(const DecodeArgs &a, hipStream_t stream) {
   if (a.append && (a.k_scales || a.v_sq || a.band_k) && !(a.band_k && a.n_rec >= 1)) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
   const dim3 block(12 * 64);
-  if (a.append && a.band_k)
-    a.k_scales ? launch_d128<true, true, true>(a, grid, block, stream)
-               : launch_d128<true, false, true>(a, grid, block, stream);
-  else if (a.append)  // plain or fp8 codebooks (checked above)
-    a.cb_fp8 ? decode_lut_d128<12, true, false, true, false, false><<<grid, block, 0, stream>>>(a)
-             : decode_lut_d128<12, true, false, false, false, false><<<grid, block, 0, stream>>>(a);
-  else
-    a.k_scales ? launch_d128<false, true, false>(a, grid, block, stream)
-               : launch_d128<false, false, false>(a, grid, block, stream);
+  a.t_bf16 ? launch_d128_storage<true>(a, grid, block, stream) : launch_d128_storage<false>(a, grid, block, stream);
   return hipGetLastError();
 }
 

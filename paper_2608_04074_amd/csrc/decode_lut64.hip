@@ -79,21 +79,21 @@ __device__ __forceinline__ size_t subtile_offset(const DecodeArgs &a, int b, int
 }
 
 // Thread t < 256 holds row (t mod 64) of t_v, columns 16 * (t / 64) .. +15.
-__device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, float4 (&tv)[4]) {
+template <bool TBF>
+__device__ __forceinline__ void load_tv_rows(const DecodeArgs &a, const int kv, T4 (&tv)[4]) {
   const int tid = threadIdx.x;
   if (tid < 256) {
-    const float4 *row = reinterpret_cast<const float4 *>(a.t_v + (static_cast<size_t>(kv) * kD + (tid & (kD - 1))) * kD) +
-                        4 * (tid >> 6);
+    const size_t row = (static_cast<size_t>(kv) * kD + (tid & (kD - 1))) * kD + 16 * (tid >> 6);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) tv[i] = row[i];
+    for (int i = 0; i < 4; ++i) tv[i] = load_t4(a.t_v, row + 4 * i, TBF);
   }
 }
 
 // (BSTEP: the kernel's own instantiation, so that each kernel inlines a
 // split pass of its own and the plain kernels compile as without the step)
-template <int WAVES, bool KS, bool FP8, bool SQ, bool BSTEP>
+template <int WAVES, bool KS, bool FP8, bool SQ, bool BSTEP, bool TBF>
 __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
-                                           const int t0, const int t1, const size_t row0, float4 (&tv)[4]) {
+                                           const int t0, const int t1, const size_t row0, T4 (&tv)[4]) {
   const uint32_t sbase = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u8_ptr)smem));
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -172,7 +172,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
     // thread (jq, e4) < 256 holds rows 4jq .. 4jq+3, columns 4e4 .. 4e4+3 of t_k_inv_t
     const int e4 = tid & 15, jq = tid >> 4;
     float qval = 0.f;
-    float4 trow[4];
+    T4 trow[4];
     if (tid < kH * kD) {
       const int qh = tid >> 6;
       if (qh < G) {
@@ -182,9 +182,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       }
     }
     if (tid < 256) {
-      const float4 *tk = reinterpret_cast<const float4 *>(a.t_k_inv_t + (static_cast<size_t>(kv) * kD + 4 * jq) * kD) + e4;
+      const size_t tk = (static_cast<size_t>(kv) * kD + 4 * jq) * kD + 4 * e4;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) trow[r] = tk[r * (kD / 4)];
+      for (int r = 0; r < 4; ++r) trow[r] = load_t4(a.t_k_inv_t, tk + r * kD, TBF);
     }
     constexpr int VPER = (kL * 256 + NT - 1) / NT;
     // codewords as raw words (fp16, or fp8 bytes converted where they are used)
@@ -261,10 +261,11 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
         acc4[hq] = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          acc4[hq].x = fmaf(qq[r], trow[r].x, acc4[hq].x);
-          acc4[hq].y = fmaf(qq[r], trow[r].y, acc4[hq].y);
-          acc4[hq].z = fmaf(qq[r], trow[r].z, acc4[hq].z);
-          acc4[hq].w = fmaf(qq[r], trow[r].w, acc4[hq].w);
+          const float4 tr = t4_value(trow[r], TBF);
+          acc4[hq].x = fmaf(qq[r], tr.x, acc4[hq].x);
+          acc4[hq].y = fmaf(qq[r], tr.y, acc4[hq].y);
+          acc4[hq].z = fmaf(qq[r], tr.z, acc4[hq].z);
+          acc4[hq].w = fmaf(qq[r], tr.w, acc4[hq].w);
         }
       }
       // the 4 lane rows of a wave hold rows of the same columns: fold them, one part per wave
@@ -432,7 +433,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       process_round(R0 + kRound * cur, kwb[k], vwb[k], ksb[k], vqb[k]);
     }
   }
-  load_tv_rows(a, kv, tv);
+  load_tv_rows<TBF>(a, kv, tv);
 
   // ---- per-wave reduction: l over the rows of a column; the two set columns
   // of a head (lanes n and n + 8 of a row) are rescaled to a common max and summed
@@ -500,11 +501,11 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
 
 // Last split of a (sequence, KV head): log-sum-exp merge of the splits in
 // index order, the sink once (shifted, Lemma S1), division, and out = s_hat t_v^T.
-template <int WAVES, bool BSTEP>
+template <int WAVES, bool BSTEP, bool TBF>
 __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                              const size_t row0, const int own_split, const bool own_active,
                                              const int S, const int lo, const int tend, const int band_lo,
-                                             const int sink_end, const float4 (&tv)[4]) {
+                                             const int sink_end, const T4 (&tv)[4]) {
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -610,10 +611,11 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
 #pragma unroll
       for (int h = 0; h < kH; ++h) {
         const float4 sv = *reinterpret_cast<const float4 *>(shat + h * kD + 16 * jp + 4 * i);
-        o[h] = fmaf(sv.x, tv[i].x, o[h]);
-        o[h] = fmaf(sv.y, tv[i].y, o[h]);
-        o[h] = fmaf(sv.z, tv[i].z, o[h]);
-        o[h] = fmaf(sv.w, tv[i].w, o[h]);
+        const float4 t = t4_value(tv[i], TBF);
+        o[h] = fmaf(sv.x, t.x, o[h]);
+        o[h] = fmaf(sv.y, t.y, o[h]);
+        o[h] = fmaf(sv.z, t.z, o[h]);
+        o[h] = fmaf(sv.w, t.w, o[h]);
       }
     }
 #pragma unroll
@@ -634,7 +636,8 @@ __device__ __forceinline__ void combine_unit(const DecodeArgs &a, uint8_t *smem,
 // BSTEP: the one-launch step with a band (nova_kv_append_decode_attn): the new
 // token is the band's last row, stored by the combining split; the first
 // split to count in stores its codes (step_encode.h).
-template <int WAVES, bool KS, bool FP8, bool SQ, bool BSTEP>
+// TBF: the transforms are stored as bf16 (NOVA_KV_BF16_TRANSFORMS).
+template <int WAVES, bool KS, bool FP8, bool SQ, bool BSTEP, bool TBF>
 __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) uint8_t smem[lds_bytes<WAVES>()];
   const int tid = threadIdx.x;
@@ -654,11 +657,11 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
   const size_t row0 = static_cast<size_t>(b) * a.num_q_heads + kv * G;
   const bool active = t0 < t1;
 
-  float4 tv[4];
+  T4 tv[4];
   if (active) {
-    split_pass<WAVES, KS, FP8, SQ, BSTEP>(a, smem, b, kv, t0, t1, row0, tv);
+    split_pass<WAVES, KS, FP8, SQ, BSTEP, TBF>(a, smem, b, kv, t0, t1, row0, tv);
   } else {
-    load_tv_rows(a, kv, tv);
+    load_tv_rows<TBF>(a, kv, tv);
   }
   // Arrival: every split publishes its partial (when it has one) and counts
   // itself in; the split that brings the count to n_split combines.  The
@@ -718,33 +721,33 @@ __global__ void __launch_bounds__(WAVES * 64) decode_lut_d64(DecodeArgs a) {
       const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
       int phase = 0;  // shared by every copy of the meeting
       auto meet = [&] { step::team_meet(ctr + team, ++phase); };
-      step::encode_token<kD, KS, SQ>(a, reinterpret_cast<step::Scratch<kD> *>(smem)[team], b, kv, team, 4, tokoff,
+      step::encode_token<kD, KS, SQ, TBF>(a, reinterpret_cast<step::Scratch<kD> *>(smem)[team], b, kv, team, 4, tokoff,
                                      tid & 255, FP8, meet);
       __syncthreads();  // the table region is free again
     }
     if (a.n_split > 1 && ctl[0] == 0) return;
   }
-  combine_unit<WAVES, BSTEP>(a, smem, b, kv, row0, split, active, S, lo, tend, att_lo, spn.sink_end, tv);
+  combine_unit<WAVES, BSTEP, TBF>(a, smem, b, kv, row0, split, active, S, lo, tend, att_lo, spn.sink_end, tv);
 }
 
 }  // namespace
 
-template <bool BSTEP>
+template <bool BSTEP, bool TBF>
 void launch_d64(const DecodeArgs &a, const dim3 grid, const dim3 block, hipStream_t stream) {
   constexpr int W = 16;
   if (a.v_sq) {  // the scalar value arm (keys in either codebook format)
     if (a.k_scales)
-      a.cb_fp8 ? decode_lut_d64<W, true, true, true, BSTEP><<<grid, block, 0, stream>>>(a)
-               : decode_lut_d64<W, true, false, true, BSTEP><<<grid, block, 0, stream>>>(a);
+      a.cb_fp8 ? decode_lut_d64<W, true, true, true, BSTEP, TBF><<<grid, block, 0, stream>>>(a)
+               : decode_lut_d64<W, true, false, true, BSTEP, TBF><<<grid, block, 0, stream>>>(a);
     else
-      a.cb_fp8 ? decode_lut_d64<W, false, true, true, BSTEP><<<grid, block, 0, stream>>>(a)
-               : decode_lut_d64<W, false, false, true, BSTEP><<<grid, block, 0, stream>>>(a);
+      a.cb_fp8 ? decode_lut_d64<W, false, true, true, BSTEP, TBF><<<grid, block, 0, stream>>>(a)
+               : decode_lut_d64<W, false, false, true, BSTEP, TBF><<<grid, block, 0, stream>>>(a);
   } else if (a.k_scales) {
-    a.cb_fp8 ? decode_lut_d64<W, true, true, false, BSTEP><<<grid, block, 0, stream>>>(a)
-             : decode_lut_d64<W, true, false, false, BSTEP><<<grid, block, 0, stream>>>(a);
+    a.cb_fp8 ? decode_lut_d64<W, true, true, false, BSTEP, TBF><<<grid, block, 0, stream>>>(a)
+             : decode_lut_d64<W, true, false, false, BSTEP, TBF><<<grid, block, 0, stream>>>(a);
   } else {
-    a.cb_fp8 ? decode_lut_d64<W, false, true, false, BSTEP><<<grid, block, 0, stream>>>(a)
-             : decode_lut_d64<W, false, false, false, BSTEP><<<grid, block, 0, stream>>>(a);
+    a.cb_fp8 ? decode_lut_d64<W, false, true, false, BSTEP, TBF><<<grid, block, 0, stream>>>(a)
+             : decode_lut_d64<W, false, false, false, BSTEP, TBF><<<grid, block, 0, stream>>>(a);
   }
 }
 
@@ -754,7 +757,10 @@ hipError_t launch_decode_lut64(const DecodeArgs &a, hipStream_t stream) {
   if (a.append && !(a.band_k && a.n_rec >= 1)) return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(a.batch * a.num_kv_heads * a.n_split));
   const dim3 block(16 * 64);
-  a.append ? launch_d64<true>(a, grid, block, stream) : launch_d64<false>(a, grid, block, stream);
+  if (a.t_bf16)
+    a.append ? launch_d64<true, true>(a, grid, block, stream) : launch_d64<false, true>(a, grid, block, stream);
+  else
+    a.append ? launch_d64<true, false>(a, grid, block, stream) : launch_d64<false, false>(a, grid, block, stream);
   return hipGetLastError();
 }
 

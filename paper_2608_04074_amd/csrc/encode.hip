@@ -53,7 +53,7 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   const int t = blockIdx.x / (2 * NB);
   const int kv = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
-  const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D;
+  const void *tm = transform_of(side == 0 ? a.t_k : a.t_v, kv, D, a.t_bf16);
   const void *cb = side == 0 ? a.cb_k : a.cb_v;
   const size_t cw0 = static_cast<size_t>(kv) * L * kCodebookSize;
   const void *src = side == 0 ? a.k : a.v;
@@ -61,9 +61,9 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   const int pos = a.start_pos[b] + a.start_offset + t;
   if (!position_in_pool(a.layout, pos)) return;  // uniform: the workgroup stores nothing
 
-  float4 trow[D / 32];
+  T4 trow[D / 32];
   uint2 cw[encblk::kPer];
-  encblk::load_block<D>(tid, tm, cb, FP8, cw0, blk, trow, cw);
+  encblk::load_block<D>(tid, tm, a.t_bf16, cb, FP8, cw0, blk, trow, cw);
   if (tid < D) {
     const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + tid;
     double x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
@@ -85,9 +85,9 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
     // coefficients divided by rho; block 0's workgroup stores rho.
     __shared__ double us[D];
     __shared__ double srho;
-    float4 tb[D / 32];
-    encblk::load_rows<D>(tid, tm, 0, tb);
-    encblk::token_coefficients<D>(tid, sc, tm, tb, us, [] { __syncthreads(); });
+    T4 tb[D / 32];
+    encblk::load_rows<D>(tid, tm, a.t_bf16, 0, tb);
+    encblk::token_coefficients<D>(tid, sc, tm, a.t_bf16, tb, us, [] { __syncthreads(); });
     if (tid == 0) srho = encblk::key_scale<D>(us);
     __syncthreads();
     const double rho = srho;
@@ -100,7 +100,7 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
     code = encblk::search_codes(tid, uu, cw, FP8);
     if (blk == 0 && tid == 0) a.k_scales[off / L] = encblk::bf16_of(rho);
   } else {
-    encblk::partial_block<D>(tid, sc, trow);
+    encblk::partial_block<D>(tid, sc, trow, a.t_bf16);
     __syncthreads();
     code = encblk::search_block<D>(tid, sc, cw, FP8);
   }
@@ -141,7 +141,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n0 = tile * TT;
   const int nt = min(TT, a.n_new - n0);
-  const float *tm = (side == 0 ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D;
+  const void *tm = transform_of(side == 0 ? a.t_k : a.t_v, kv, D, a.t_bf16);
   const void *cb = side == 0 ? a.cb_k : a.cb_v;
   const size_t cw0 = static_cast<size_t>(kv) * L * kCodebookSize;
   constexpr bool fp8 = FP8;
@@ -154,11 +154,11 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   // staged
   const int m = lane & 15, q = lane >> 4;
   constexpr int OPW = OT / 4;
-  float tr[KS][OPW];
+  uint32_t tr[KS][OPW];  // as loaded (fp32 words, or zero-extended bf16)
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-    for (int j = 0; j < OPW; ++j) tr[ks][j] = tm[(4 * ks + q) * D + 16 * (wave * OPW + j) + m];
+    for (int j = 0; j < OPW; ++j) tr[ks][j] = load_t1_raw(tm, (4 * ks + q) * D + 16 * (wave * OPW + j) + m, a.t_bf16);
 
   // inputs (minus k_bar for keys) to LDS in fp64: thread tid stages
   // coordinate tid mod D of tokens tid / D + k * (256 / D)
@@ -202,7 +202,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   for (int ks = 0; ks < KS; ++ks) {
     double bt[OPW];
 #pragma unroll
-    for (int j = 0; j < OPW; ++j) bt[j] = static_cast<double>(tr[ks][j]);
+    for (int j = 0; j < OPW; ++j) bt[j] = static_cast<double>(t1_raw_value(tr[ks][j], a.t_bf16));
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
       const double ax = xs[(16 * tt + m) * RS + 4 * ks + q];
@@ -360,9 +360,9 @@ __global__ void __launch_bounds__(256) encode_sq_values(EncodeArgs a) {
   const int t = blockIdx.x, kv = blockIdx.y, b = blockIdx.z, i = threadIdx.x;
   const int p0 = a.start_pos[b] + a.start_offset;
   if (!position_in_pool(a.layout, p0 + t)) return;  // uniform: the workgroup stores nothing
-  const float *tv = a.t_v + static_cast<size_t>(kv) * D * D;
-  float4 rows[D / 32];
-  encblk::load_rows<D>(i, tv, 0, rows);
+  const void *tv = transform_of(a.t_v, kv, D, a.t_bf16);
+  T4 rows[D / 32];
+  encblk::load_rows<D>(i, tv, a.t_bf16, 0, rows);
   if (i < D) {
     const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + i;
     sc.xs[i] = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(a.v)[idx]))
@@ -371,7 +371,7 @@ __global__ void __launch_bounds__(256) encode_sq_values(EncodeArgs a) {
   }
   __syncthreads();
   auto sync = [] { __syncthreads(); };
-  encblk::token_coefficients<D>(i, sc, tv, rows, us, sync);
+  encblk::token_coefficients<D>(i, sc, tv, a.t_bf16, rows, us, sync);
   uint16_t sb, zb;
   encblk::sq_levels<D>(i, us, red, qs, sync, sb, zb);
   const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, p0 + t);

@@ -36,17 +36,19 @@ struct Scratch {
 };
 
 // Phase 1 (issue only): the block's transform columns and codewords.
-//   tm  = side transform of the KV head ([D][D] fp32, row-major)
+//   tm  = side transform of the KV head ([D][D], row-major; fp32, or bf16
+//         bit patterns when tbf, kept as loaded and converted where used)
 //   cb, fp8, cw0 = side codebooks ([Hkv][L][256] codewords, fp16 or fp8) and
 //         the index of the KV head's first codeword; the raw words are kept
 //         and converted where they are used
 template <int D>
-__device__ __forceinline__ void load_rows(const int t, const float *tm, const int blk, float4 (&trow)[D / 32]) {
+__device__ __forceinline__ void load_rows(const int t, const void *tm, const int tbf, const int blk,
+                                          T4 (&trow)[D / 32]) {
   constexpr int RPT = D / 32;
   const int rg = t >> 3, c4 = t & 7;
-  const float *col = tm + kCols * blk + 4 * c4;
+  const size_t col = kCols * blk + 4 * c4;
 #pragma unroll
-  for (int j = 0; j < RPT; ++j) trow[j] = *reinterpret_cast<const float4 *>(col + (RPT * rg + j) * D);
+  for (int j = 0; j < RPT; ++j) trow[j] = load_t4(tm, col + static_cast<size_t>(RPT * rg + j) * D, tbf);
 }
 __device__ __forceinline__ void load_codewords(const int t, const void *cb, const bool fp8, const size_t cw0,
                                                const int blk, uint2 (&cw)[kPer]) {
@@ -56,26 +58,27 @@ __device__ __forceinline__ void load_codewords(const int t, const void *cb, cons
   for (int k = 0; k < kPer; ++k) cw[k] = codeword_raw(cb, fp8, row + r + 32 * k);
 }
 template <int D>
-__device__ __forceinline__ void load_block(const int t, const float *tm, const void *cb, const bool fp8,
-                                           const size_t cw0, const int blk, float4 (&trow)[D / 32],
+__device__ __forceinline__ void load_block(const int t, const void *tm, const int tbf, const void *cb,
+                                           const bool fp8, const size_t cw0, const int blk, T4 (&trow)[D / 32],
                                            uint2 (&cw)[kPer]) {
-  load_rows<D>(t, tm, blk, trow);
+  load_rows<D>(t, tm, tbf, blk, trow);
   load_codewords(t, cb, fp8, cw0, blk, cw);
 }
 
 // Phase 2 (after x is in LDS): this wave's share of the 32 coefficients.
 template <int D>
-__device__ __forceinline__ void partial_block(const int t, Scratch<D> &s, const float4 (&trow)[D / 32]) {
+__device__ __forceinline__ void partial_block(const int t, Scratch<D> &s, const T4 (&trow)[D / 32], const int tbf) {
   constexpr int RPT = D / 32;
   const int rg = t >> 3, c4 = t & 7;
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
   for (int j = 0; j < RPT; ++j) {
     const double x = s.xs[RPT * rg + j];
-    acc[0] = fma(x, static_cast<double>(trow[j].x), acc[0]);
-    acc[1] = fma(x, static_cast<double>(trow[j].y), acc[1]);
-    acc[2] = fma(x, static_cast<double>(trow[j].z), acc[2]);
-    acc[3] = fma(x, static_cast<double>(trow[j].w), acc[3]);
+    const float4 tr = t4_value(trow[j], tbf);
+    acc[0] = fma(x, static_cast<double>(tr.x), acc[0]);
+    acc[1] = fma(x, static_cast<double>(tr.y), acc[1]);
+    acc[2] = fma(x, static_cast<double>(tr.z), acc[2]);
+    acc[3] = fma(x, static_cast<double>(tr.w), acc[3]);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -160,14 +163,14 @@ __device__ __forceinline__ uint16_t bf16_of(const double x) {
 // `first` holds block 0's rows (load_rows) on entry.  Two meetings of the
 // team (sync) per block.
 template <int D, class Sync>
-__device__ __forceinline__ void token_coefficients(const int t, Scratch<D> &s, const float *tm,
-                                                   float4 (&first)[D / 32], double *u, Sync sync) {
+__device__ __forceinline__ void token_coefficients(const int t, Scratch<D> &s, const void *tm, const int tbf,
+                                                   T4 (&first)[D / 32], double *u, Sync sync) {
   constexpr int NB = D / kCols;
-  float4 next[D / 32];
+  T4 next[D / 32];
 #pragma unroll
   for (int bb = 0; bb < NB; ++bb) {
-    if (bb + 1 < NB) load_rows<D>(t, tm, bb + 1, next);
-    partial_block<D>(t, s, first);
+    if (bb + 1 < NB) load_rows<D>(t, tm, tbf, bb + 1, next);
+    partial_block<D>(t, s, first, tbf);
     sync();
     if (t < kCols) u[kCols * bb + t] = coefficient<D>(s, t);
     sync();

@@ -62,9 +62,10 @@ nova_kv_status check_params(const nova_kv_params *p, bool need_encode, bool need
     return fail(NOVA_KV_ERR_UNSUPPORTED, "codebook_size %d unsupported (only 256)", p->codebook_size);
   if (p->head_dim != 64 && p->head_dim != 128)
     return fail(NOVA_KV_ERR_UNSUPPORTED, "head_dim %d unsupported (64 or 128)", p->head_dim);
-  if ((p->flags & ~(NOVA_KV_KEY_SCALE | NOVA_KV_FP8_CODEBOOKS | NOVA_KV_SQ_VALUES)) != 0)
+  if ((p->flags & ~(NOVA_KV_KEY_SCALE | NOVA_KV_FP8_CODEBOOKS | NOVA_KV_SQ_VALUES | NOVA_KV_BF16_TRANSFORMS)) != 0)
     return fail(NOVA_KV_ERR_UNSUPPORTED,
-                "flags 0x%x unsupported (NOVA_KV_KEY_SCALE, NOVA_KV_FP8_CODEBOOKS, NOVA_KV_SQ_VALUES)", p->flags);
+                "flags 0x%x unsupported (NOVA_KV_KEY_SCALE, NOVA_KV_FP8_CODEBOOKS, NOVA_KV_SQ_VALUES, "
+                "NOVA_KV_BF16_TRANSFORMS)", p->flags);
   const bool sq = (p->flags & NOVA_KV_SQ_VALUES) != 0;  // cb_v unused
   if (!p->kbar || !p->cb_k || (!sq && !p->cb_v)) return fail(NOVA_KV_ERR_INVALID_ARG, "kbar/cb_k/cb_v is NULL");
   if (!aligned(p->cb_k, 16) || (!sq && !aligned(p->cb_v, 16)))

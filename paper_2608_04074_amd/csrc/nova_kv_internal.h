@@ -35,7 +35,9 @@ __device__ __forceinline__ size_t code_row_offset(const CacheLayout &lay, int nu
 
 struct DecodeArgs {
   int batch, num_q_heads, num_kv_heads, head_dim, gqa;
-  const float *kbar, *t_k_inv_t, *t_v;
+  const float *kbar;
+  const void *t_k_inv_t, *t_v;  // transforms: fp32, or bf16 bit patterns when t_bf16
+  int t_bf16;
   const void *cb_k, *cb_v;  // [Hkv][L][256] codewords: 4 fp16, or 4 fp8 E4M3 when cb_fp8
   int cb_fp8;
   CacheLayout layout;
@@ -72,7 +74,7 @@ struct DecodeArgs {
   int append;
   const void *k_new, *v_new;  // [B][Hkv][D]
   int new_bf16;
-  const float *t_k;
+  const void *t_k;
   uint8_t *k_codes_w, *v_codes_w;  // the pools k_codes / v_codes, written at the new position
   uint16_t *k_scales_w, *v_sq_w;   // the key-scale and scalar-arm pools, written there (else nullptr)
   uint16_t *band_k_w, *band_v_w;   // the band buffers, written at the new token's slot (else nullptr)
@@ -102,7 +104,9 @@ constexpr int kXchSlotWords = 2 * kXchBandWords;
 
 struct EncodeArgs {
   int batch, n_new, num_kv_heads, head_dim;
-  const float *kbar, *t_k, *t_v;
+  const float *kbar;
+  const void *t_k, *t_v;  // transforms: fp32, or bf16 bit patterns when t_bf16
+  int t_bf16;
   const void *cb_k, *cb_v;  // [Hkv][L][256] codewords: 4 fp16, or 4 fp8 E4M3 when cb_fp8
   int cb_fp8;
   CacheLayout layout;
@@ -174,6 +178,44 @@ __device__ __forceinline__ float half_bits_to_float(uint16_t h) {
 
 __device__ __forceinline__ float bf16_bits_to_float(uint16_t h) {
   return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+// Four consecutive elements (i a multiple of 4) of a transform (t_k,
+// t_k_inv_t, t_v) as loaded, in one load: fp32 words, or with bf16 storage
+// two words of bf16 pairs in .x and .y.  They are converted where they are
+// used, so that a load issued early is not waited for at its issue.
+using T4 = uint4;
+__device__ __forceinline__ T4 load_t4(const void *t, const size_t i, const int bf16) {
+  if (bf16) {
+    const uint2 h = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(t) + i);
+    return make_uint4(h.x, h.y, 0u, 0u);
+  }
+  return *reinterpret_cast<const uint4 *>(static_cast<const float *>(t) + i);
+}
+__device__ __forceinline__ float4 t4_value(const T4 w, const int bf16) {
+  if (bf16)
+    return make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xffff0000u), __uint_as_float(w.y << 16),
+                       __uint_as_float(w.y & 0xffff0000u));
+  return make_float4(__uint_as_float(w.x), __uint_as_float(w.y), __uint_as_float(w.z), __uint_as_float(w.w));
+}
+// The [D][D] transform of KV head kv in a [Hkv][D][D] array.
+__host__ __device__ __forceinline__ const void *transform_of(const void *t, const int kv, const int D,
+                                                             const int bf16) {
+  const size_t off = static_cast<size_t>(kv) * D * D;
+  return bf16 ? static_cast<const void *>(static_cast<const uint16_t *>(t) + off)
+              : static_cast<const void *>(static_cast<const float *>(t) + off);
+}
+// One element of a transform as loaded (a bf16 element zero-extended), and
+// its value.
+__device__ __forceinline__ uint32_t load_t1_raw(const void *t, const size_t i, const int bf16) {
+  return bf16 ? static_cast<uint32_t>(static_cast<const uint16_t *>(t)[i]) : static_cast<const uint32_t *>(t)[i];
+}
+__device__ __forceinline__ float t1_raw_value(const uint32_t w, const int bf16) {
+  return __uint_as_float(bf16 ? w << 16 : w);
+}
+// One element of a transform.
+__device__ __forceinline__ float t1_value(const void *t, const size_t i, const int bf16) {
+  return bf16 ? bf16_bits_to_float(static_cast<const uint16_t *>(t)[i]) : static_cast<const float *>(t)[i];
 }
 
 // Raw words of codeword `idx` (an index over [Hkv][L][256]): both words of 4

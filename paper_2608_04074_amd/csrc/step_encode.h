@@ -65,7 +65,8 @@ struct Scratch {
 
 // Tasks first, first + stride, ... of the new token at code row offset tokoff
 // of the pools, by team thread t (0..255); meet() is the team's meeting.
-template <int D, bool KS, bool SQ, class Meet>
+// TBF: the transforms are stored as bf16.
+template <int D, bool KS, bool SQ, bool TBF, class Meet>
 __device__ __forceinline__ void encode_token(const DecodeArgs &a, Scratch<D> &ls, const int b, const int kv,
                                              const int first, const int stride, const size_t tokoff, const int t,
                                              const bool fp8, Meet meet) {
@@ -85,16 +86,16 @@ __device__ __forceinline__ void encode_token(const DecodeArgs &a, Scratch<D> &ls
     encblk::Scratch<D> &s = ls.sc[k & 1];
     double *u = ls.u[k & 1];
     const bool key = j < T::kKey;
-    const float *tm = (key ? a.t_k : a.t_v) + static_cast<size_t>(kv) * D * D;
+    const void *tm = transform_of(key ? a.t_k : a.t_v, kv, D, TBF);
     const void *cb = key ? a.cb_k : a.cb_v;
-    float4 rows[D / 32];
+    T4 rows[D / 32];
     uint2 cw[encblk::kPer];
     if ((key && KS) || (!key && SQ)) {
-      encblk::load_rows<D>(t, tm, 0, rows);
+      encblk::load_rows<D>(t, tm, TBF, 0, rows);
       if (key) encblk::load_codewords(t, cb, fp8, cw0, 0, cw);
       if (t < D) s.xs[t] = element(key);
       meet();
-      encblk::token_coefficients<D>(t, s, tm, rows, u, meet);
+      encblk::token_coefficients<D>(t, s, tm, TBF, rows, u, meet);
       if (key) {
         // rho, then the blocks' codes of the coefficients divided by it (the
         // next block's codewords requested while one block is searched)
@@ -130,10 +131,10 @@ __device__ __forceinline__ void encode_token(const DecodeArgs &a, Scratch<D> &ls
       }
     } else {
       const int blk = key ? j : j - T::kKey;
-      encblk::load_block<D>(t, tm, cb, fp8, cw0, blk, rows, cw);
+      encblk::load_block<D>(t, tm, TBF, cb, fp8, cw0, blk, rows, cw);
       if (t < D) s.xs[t] = element(key);
       meet();
-      encblk::partial_block<D>(t, s, rows);
+      encblk::partial_block<D>(t, s, rows, TBF);
       meet();
       const int code = encblk::search_block<D>(t, s, cw, fp8);
       if ((t & 31) == 0)

@@ -83,8 +83,8 @@ def _encode(p, lay, **kw):
     (dict(codebook_size=16), nat.NOVA_KV_ERR_UNSUPPORTED),
     (dict(head_dim=96), nat.NOVA_KV_ERR_UNSUPPORTED),
     (dict(head_dim=130), nat.NOVA_KV_ERR_INVALID_ARG),
-    (dict(flags=8), nat.NOVA_KV_ERR_UNSUPPORTED),
-    (dict(flags=15), nat.NOVA_KV_ERR_UNSUPPORTED),
+    (dict(flags=16), nat.NOVA_KV_ERR_UNSUPPORTED),
+    (dict(flags=31), nat.NOVA_KV_ERR_UNSUPPORTED),
     (dict(num_kv_heads=0), nat.NOVA_KV_ERR_INVALID_ARG),
     (dict(cb_k=None), nat.NOVA_KV_ERR_INVALID_ARG),
     (dict(cb_v=0x6001), nat.NOVA_KV_ERR_INVALID_ARG),
