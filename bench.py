@@ -103,7 +103,7 @@ def measured_counters():
     except OSError:
         return None
     sha = re.search(r"kernel_source_sha256:\s*([0-9a-f]{64})", text)
-    row = re.search(r"\| `" + re.escape(DECODE_KERNEL) + r"<12, true, false, false, false>` \| (\d+) \| ([0-9.]+) \| "
+    row = re.search(r"\| `" + re.escape(DECODE_KERNEL) + r"<12, true, false, false, false, false, false>` \| (\d+) \| ([0-9.]+) \| "
                     r"([0-9.]+) \| ([0-9.]+) \| ([0-9.]+) \| ([0-9.]+) \|", text)
     if not sha or not row or sha.group(1) != kernel_source_sha256():
         return None
@@ -538,7 +538,7 @@ def main():
         "decode_kernel_us": {"mean": round(dec_us, 2), **pct(dec_pc)},
         "append_kernel_us": round(enc_us, 2),
         "roofline": {
-            "kernel": f"{DECODE_KERNEL}<12, true, false, false, false> (the step's one launch: encode of the new token, query "
+            "kernel": f"{DECODE_KERNEL}<12, true, false, false, false, false, false> (the step's one launch: encode of the new token, query "
                       "transform, split pass, combine)",
             "bound": "hbm",
             "achieved": round(value, 1),

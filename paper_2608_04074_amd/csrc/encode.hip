@@ -42,7 +42,7 @@ __device__ __forceinline__ uint16_t input_bf16_bits(const EncodeArgs &a, const v
 // fetches a quarter (D=128) or half (D=64) of the parameters, all loads
 // coalesced and issued before the first use; the launch costs about one
 // memory latency.  The block itself is encode_block.h's team computation.
-template <int D, bool FP8>
+template <int D, bool FP8, bool TBF>
 __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   constexpr int L = D / kGroupDim;
   constexpr int NB = L / encblk::kGroups;  // group blocks per token
@@ -53,7 +53,7 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   const int t = blockIdx.x / (2 * NB);
   const int kv = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x;
-  const void *tm = transform_of(side == 0 ? a.t_k : a.t_v, kv, D, a.t_bf16);
+  const void *tm = transform_of(side == 0 ? a.t_k : a.t_v, kv, D, TBF);
   const void *cb = side == 0 ? a.cb_k : a.cb_v;
   const size_t cw0 = static_cast<size_t>(kv) * L * kCodebookSize;
   const void *src = side == 0 ? a.k : a.v;
@@ -63,7 +63,7 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
 
   T4 trow[D / 32];
   uint2 cw[encblk::kPer];
-  encblk::load_block<D>(tid, tm, a.t_bf16, cb, FP8, cw0, blk, trow, cw);
+  encblk::load_block<D>(tid, tm, TBF, cb, FP8, cw0, blk, trow, cw);
   if (tid < D) {
     const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + tid;
     double x = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(src)[idx]))
@@ -86,8 +86,8 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
     __shared__ double us[D];
     __shared__ double srho;
     T4 tb[D / 32];
-    encblk::load_rows<D>(tid, tm, a.t_bf16, 0, tb);
-    encblk::token_coefficients<D>(tid, sc, tm, a.t_bf16, tb, us, [] { __syncthreads(); });
+    encblk::load_rows<D>(tid, tm, TBF, 0, tb);
+    encblk::token_coefficients<D>(tid, sc, tm, TBF, tb, us, [] { __syncthreads(); });
     if (tid == 0) srho = encblk::key_scale<D>(us);
     __syncthreads();
     const double rho = srho;
@@ -100,7 +100,7 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
     code = encblk::search_codes(tid, uu, cw, FP8);
     if (blk == 0 && tid == 0) a.k_scales[off / L] = encblk::bf16_of(rho);
   } else {
-    encblk::partial_block<D>(tid, sc, trow, a.t_bf16);
+    encblk::partial_block<D>(tid, sc, trow, TBF);
     __syncthreads();
     code = encblk::search_block<D>(tid, sc, cw, FP8);
   }
@@ -122,7 +122,7 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
 // LDS rows are padded by two doubles so the operand reads hit distinct banks.
 // Operand layout of v_mfma_f64_16x16x4f64 (measured): A[m][k] in lane 16k + m,
 // B[k][n] in lane 16k + n, D[m][n] in lane 16 (m mod 4) + n, register m / 4.
-template <int D, bool FP8>
+template <int D, bool FP8, bool TBF>
 __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   constexpr int L = D / kGroupDim;
   constexpr int TT = 32;                 // tokens per workgroup
@@ -141,7 +141,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n0 = tile * TT;
   const int nt = min(TT, a.n_new - n0);
-  const void *tm = transform_of(side == 0 ? a.t_k : a.t_v, kv, D, a.t_bf16);
+  const void *tm = transform_of(side == 0 ? a.t_k : a.t_v, kv, D, TBF);
   const void *cb = side == 0 ? a.cb_k : a.cb_v;
   const size_t cw0 = static_cast<size_t>(kv) * L * kCodebookSize;
   constexpr bool fp8 = FP8;
@@ -158,7 +158,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-    for (int j = 0; j < OPW; ++j) tr[ks][j] = load_t1_raw(tm, (4 * ks + q) * D + 16 * (wave * OPW + j) + m, a.t_bf16);
+    for (int j = 0; j < OPW; ++j) tr[ks][j] = load_t1_raw(tm, (4 * ks + q) * D + 16 * (wave * OPW + j) + m, TBF);
 
   // inputs (minus k_bar for keys) to LDS in fp64: thread tid stages
   // coordinate tid mod D of tokens tid / D + k * (256 / D)
@@ -202,7 +202,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   for (int ks = 0; ks < KS; ++ks) {
     double bt[OPW];
 #pragma unroll
-    for (int j = 0; j < OPW; ++j) bt[j] = static_cast<double>(t1_raw_value(tr[ks][j], a.t_bf16));
+    for (int j = 0; j < OPW; ++j) bt[j] = static_cast<double>(t1_raw_value(tr[ks][j], TBF));
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
       const double ax = xs[(16 * tt + m) * RS + 4 * ks + q];
@@ -350,7 +350,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
 // sequence).  s = v t_v in fp64 with the block encoder's arithmetic, then
 // encode_block.h's levels; coordinate 4g + j goes to bits 2j, 2j + 1 of
 // byte g.  The token's value row also goes to the band when it is in it.
-template <int D>
+template <int D, bool TBF>
 __global__ void __launch_bounds__(256) encode_sq_values(EncodeArgs a) {
   constexpr int L = D / kGroupDim;
   __shared__ encblk::Scratch<D> sc;
@@ -360,9 +360,9 @@ __global__ void __launch_bounds__(256) encode_sq_values(EncodeArgs a) {
   const int t = blockIdx.x, kv = blockIdx.y, b = blockIdx.z, i = threadIdx.x;
   const int p0 = a.start_pos[b] + a.start_offset;
   if (!position_in_pool(a.layout, p0 + t)) return;  // uniform: the workgroup stores nothing
-  const void *tv = transform_of(a.t_v, kv, D, a.t_bf16);
+  const void *tv = transform_of(a.t_v, kv, D, TBF);
   T4 rows[D / 32];
-  encblk::load_rows<D>(i, tv, a.t_bf16, 0, rows);
+  encblk::load_rows<D>(i, tv, TBF, 0, rows);
   if (i < D) {
     const size_t idx = ((static_cast<size_t>(b) * a.n_new + t) * a.num_kv_heads + kv) * D + i;
     sc.xs[i] = a.in_bf16 ? static_cast<double>(bf16_bits_to_float(static_cast<const uint16_t *>(a.v)[idx]))
@@ -371,7 +371,7 @@ __global__ void __launch_bounds__(256) encode_sq_values(EncodeArgs a) {
   }
   __syncthreads();
   auto sync = [] { __syncthreads(); };
-  encblk::token_coefficients<D>(i, sc, tv, a.t_bf16, rows, us, sync);
+  encblk::token_coefficients<D>(i, sc, tv, TBF, rows, us, sync);
   uint16_t sb, zb;
   encblk::sq_levels<D>(i, us, red, qs, sync, sb, zb);
   const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, p0 + t);
@@ -382,23 +382,30 @@ __global__ void __launch_bounds__(256) encode_sq_values(EncodeArgs a) {
   }
 }
 
-template <int D>
-hipError_t launch_encode_d(const EncodeArgs &a, hipStream_t stream) {
-  if (a.v_sq) encode_sq_values<D><<<dim3(a.n_new, a.num_kv_heads, a.batch), dim3(256), 0, stream>>>(a);
+// TBF: the transforms are stored as bf16 (a compile-time choice, so that the
+// fp32 kernels carry no branch on it).
+template <int D, bool TBF>
+hipError_t launch_encode_t(const EncodeArgs &a, hipStream_t stream) {
+  if (a.v_sq) encode_sq_values<D, TBF><<<dim3(a.n_new, a.num_kv_heads, a.batch), dim3(256), 0, stream>>>(a);
   if (a.n_new <= 4) {
     const dim3 grid(2 * a.n_new * (D / kGroupDim / 8), a.num_kv_heads, a.batch);
     if (a.cb_fp8)
-      encode_small<D, true><<<grid, dim3(256), 0, stream>>>(a);
+      encode_small<D, true, TBF><<<grid, dim3(256), 0, stream>>>(a);
     else
-      encode_small<D, false><<<grid, dim3(256), 0, stream>>>(a);
+      encode_small<D, false, TBF><<<grid, dim3(256), 0, stream>>>(a);
   } else {
     const dim3 grid((a.n_new + 31) / 32, a.num_kv_heads, 2 * a.batch);
     if (a.cb_fp8)
-      encode_bulk<D, true><<<grid, dim3(256), 0, stream>>>(a);
+      encode_bulk<D, true, TBF><<<grid, dim3(256), 0, stream>>>(a);
     else
-      encode_bulk<D, false><<<grid, dim3(256), 0, stream>>>(a);
+      encode_bulk<D, false, TBF><<<grid, dim3(256), 0, stream>>>(a);
   }
   return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_encode_d(const EncodeArgs &a, hipStream_t stream) {
+  return a.t_bf16 ? launch_encode_t<D, true>(a, stream) : launch_encode_t<D, false>(a, stream);
 }
 
 }  // namespace
