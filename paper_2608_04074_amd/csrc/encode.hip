@@ -116,9 +116,14 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
 //    |u - c|^2 + (off_g - |u_g|^2) is >= 0 and ordered like the distance) and
 //    the MFMA adds -2 c . u;
 //  * argmin: the codeword index replaces the low 8 mantissa bits of the
-//    (clamped, non-negative) fp64 value, so one min per score keeps the nearest
+//    (non-negative) fp64 value, so one min per score keeps the nearest
 //    codeword and, on equal values, the smallest index.  The truncation is
 //    2^-44 relative, far below the spacing of distinct distances.
+// Each wave owns a contiguous run of groups and both token tiles: every
+// codeword tile's C operand (norms from LDS) serves two MFMAs, the codes stay
+// in registers until one store per token, and the norms of half a codebook
+// at a time are staged.  That keeps the workgroup within 37 KB of LDS and
+// 128 VGPRs, so four of them share a CU.
 // LDS rows are padded by two doubles so the operand reads hit distinct banks.
 // Operand layout of v_mfma_f64_16x16x4f64 (measured): A[m][k] in lane 16k + m,
 // B[k][n] in lane 16k + n, D[m][n] in lane 16 (m mod 4) + n, register m / 4.
@@ -131,8 +136,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   constexpr int KS = D / 4;              // k-steps of the transform
   typedef double double4_t __attribute__((ext_vector_type(4)));
   __shared__ double xs[TT * RS];         // inputs, then coefficients
-  __shared__ __attribute__((aligned(32))) double cn[4][kCodebookSize];
-  __shared__ uint8_t codes[TT][L];
+  __shared__ __attribute__((aligned(32))) double cn[4][kCodebookSize / 2];  // norms of half a codebook per wave
 
   const int tile = blockIdx.x, kv = blockIdx.y;
   const int b = blockIdx.z >> 1, side = blockIdx.z & 1;
@@ -222,7 +226,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   if (side == 0 && a.k_scales) {
     // Key-scale format: rho of each key from its D coefficients, stored as
     // bf16, then the coefficients divided by it (0 when rho = 0).
-    __shared__ double rhos[TT];
+    double *rhos = &cn[0][0];  // the norms are written only after the last read of these
     if (tid < TT) {
       const double rho = encblk::key_scale<D>(&xs[tid * RS]);
       rhos[tid] = rho;
@@ -241,29 +245,23 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
     __syncthreads();
   }
 
-  // ---- nearest codeword: wave w takes groups w, w+4, ...; the codewords of
-  // its next group are requested while it processes the current one
+  // ---- nearest codeword: wave w takes groups GPW*w .. GPW*w + GPW-1 and keeps
+  // their codes in registers; the codewords of its next group are requested
+  // tile by tile as the current group's are converted
+  constexpr int GPW = L / 4;
+  const int g0 = GPW * wave;
   uint2 ra[16], rn[4];
 #pragma unroll
-  for (int t = 0; t < 16; ++t) ra[t] = codeword_raw(cb, fp8, cw0 + static_cast<size_t>(wave) * kCodebookSize + 16 * t + m);
+  for (int t = 0; t < 16; ++t) ra[t] = codeword_raw(cb, fp8, cw0 + static_cast<size_t>(g0) * kCodebookSize + 16 * t + m);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) rn[j] = codeword_raw(cb, fp8, cw0 + static_cast<size_t>(wave) * kCodebookSize + 4 * lane + j);
-  // The low byte of a score is replaced by its codeword index with one
-  // and-or per score: the mask sits in a VGPR and the index base in an SGPR
-  // (opaque zeros, so that the index of each score is a scalar add and no
-  // 32-bit literal, which this instruction encoding cannot carry).
+  for (int j = 0; j < 4; ++j) rn[j] = codeword_raw(cb, fp8, cw0 + static_cast<size_t>(g0) * kCodebookSize + 4 * lane + j);
   uint32_t keep, idx0;
   asm volatile("v_mov_b32 %0, 0xffffff00" : "=v"(keep));
   asm volatile("s_mov_b32 %0, 0" : "=s"(idx0));
-  for (int g = wave; g < L; g += 4) {
-    // A operands: coordinate q of codewords 16t + m
-    double ac[16];
-#pragma unroll
-    for (int t = 0; t < 16; ++t) {
-      const uint2 w = codeword_f16(ra[t], fp8);
-      const uint32_t h2 = q < 2 ? w.x : w.y;
-      ac[t] = static_cast<double>(half_bits_to_float(static_cast<uint16_t>((q & 1) ? (h2 >> 16) : (h2 & 0xffffu))));
-    }
+  unsigned long long code_acc[2] = {0ull, 0ull};
+  for (int k = 0; k < GPW; ++k) {
+    const int g = g0 + k;
+    const size_t ncw = cw0 + static_cast<size_t>(min(g + 1, g0 + GPW - 1)) * kCodebookSize;
     double nc[4], cmax = 0.0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -275,14 +273,8 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
       nc[j] = (c0 * c0 + c1 * c1) + (c2 * c2 + c3 * c3);
       cmax = fmax(cmax, nc[j]);
     }
-    {  // the next group's codewords (the last group requests itself again)
-      const size_t ncw = cw0 + static_cast<size_t>(min(g + 4, L - 1)) * kCodebookSize;
 #pragma unroll
-      for (int t = 0; t < 16; ++t) ra[t] = codeword_raw(cb, fp8, ncw + 16 * t + m);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) rn[j] = codeword_raw(cb, fp8, ncw + 4 * lane + j);
-    }
-    // offset: the largest |u_g|^2 of the tile (uniform)
+    for (int j = 0; j < 4; ++j) rn[j] = codeword_raw(cb, fp8, ncw + 4 * lane + j);
     double un = 0.0;
     if (lane < TT) {
 #pragma unroll
@@ -297,50 +289,90 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
       cmax = fmax(cmax, __shfl_xor(cmax, o, 64));
     }
     un = un + 0x1p-40 * (un + cmax);
+    // B operands: -2 u (exact scaling), tokens m and 16 + m
+    double bu0 = -2.0 * xs[m * RS + 4 * g + q];
+    double bu1 = -2.0 * xs[(16 + m) * RS + 4 * g + q];
+    double best0 = __builtin_huge_val(), best1 = __builtin_huge_val();
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int c = 4 * lane + j;
-      cn[wave][16 * (c >> 4) + 4 * (c & 3) + ((c >> 2) & 3)] = nc[j] + un;
-    }
+    for (int h = 0; h < 2; ++h) {
+      // norms (+ offset) of codewords 128h .. 128h + 127, held by lanes 32h .. 32h + 31
+      asm volatile("" ::: "memory");
+      if ((lane >> 5) == h) {
 #pragma unroll
-    for (int t = 0; t < 16; ++t) ac[t] *= -2.0;
-    // LDS writes of this wave's norms are read only by this wave: a wave-level wait suffices
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-    __builtin_amdgcn_wave_barrier();
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      const double bu = xs[(16 * tt + m) * RS + 4 * g + q];  // B[k = q][n = token m]
-      double best = __builtin_huge_val();
-#pragma unroll
-      for (int t = 0; t < 16; ++t) {
-        const double4_t cin = *reinterpret_cast<const double4_t *>(&cn[wave][16 * t + 4 * q]);
-        const double4_t dd = __builtin_amdgcn_mfma_f64_16x16x4f64(ac[t], bu, cin, 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {  // register i = codeword 16t + 4i + q
-          const double x = dd[i];
-          const unsigned long long bits = static_cast<unsigned long long>(__double_as_longlong(x));
-          const uint32_t idx = idx0 + static_cast<uint32_t>(16 * t + 4 * i);
-          const unsigned long long packed =
-              (bits & 0xffffffff00000000ull) | ((static_cast<uint32_t>(bits) & keep) | idx);
-          best = fmin(best, __longlong_as_double(static_cast<long long>(packed)));
+        for (int j = 0; j < 4; ++j) {
+          const int c = 4 * (lane & 31) + j;
+          cn[wave][16 * (c >> 4) + 4 * (c & 3) + ((c >> 2) & 3)] = nc[j] + un;
         }
       }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+      __builtin_amdgcn_wave_barrier();
+      asm volatile("" ::: "memory");
+      // coordinate q of codeword 16t + m as the A operand; the register then
+      // receives the next group's codeword
+      auto conv = [&](const int t) -> double {
+        const uint2 w = codeword_f16(ra[t], fp8);
+        const uint32_t h2 = q < 2 ? w.x : w.y;
+        const double c = half_bits_to_float(static_cast<uint16_t>((q & 1) ? (h2 >> 16) : (h2 & 0xffffu)));
+        ra[t] = codeword_raw(cb, fp8, ncw + 16 * t + m);
+        return c;
+      };
+      double4_t cin = *reinterpret_cast<const double4_t *>(&cn[wave][4 * q]);
+      double ac = conv(8 * h);
+      double4_t n0 = __builtin_amdgcn_mfma_f64_16x16x4f64(ac, bu0, cin, 0, 0, 0);
+      double4_t n1 = __builtin_amdgcn_mfma_f64_16x16x4f64(ac, bu1, cin, 0, 0, 0);
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const int t = 8 * h + s;
+        const double4_t d0 = n0, d1 = n1;
+        if (s + 1 < 8) {
+          cin = *reinterpret_cast<const double4_t *>(&cn[wave][16 * (s + 1) + 4 * q]);
+          ac = conv(t + 1);
+          n0 = __builtin_amdgcn_mfma_f64_16x16x4f64(ac, bu0, cin, 0, 0, 0);
+          n1 = __builtin_amdgcn_mfma_f64_16x16x4f64(ac, bu1, cin, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {  // register i = codeword 16t + 4i + q
+          const uint32_t idx = idx0 + static_cast<uint32_t>(16 * t + 4 * i);
+          const unsigned long long b0 = static_cast<unsigned long long>(__double_as_longlong(d0[i]));
+          const unsigned long long b1 = static_cast<unsigned long long>(__double_as_longlong(d1[i]));
+          best0 = fmin(best0, __longlong_as_double(static_cast<long long>(
+                                  (b0 & 0xffffffff00000000ull) | ((static_cast<uint32_t>(b0) & keep) | idx))));
+          best1 = fmin(best1, __longlong_as_double(static_cast<long long>(
+                                  (b1 & 0xffffffff00000000ull) | ((static_cast<uint32_t>(b1) & keep) | idx))));
+        }
+        // the MFMAs of tile t + 2 wait for these minima, so at most two
+        // tiles' results are held at once
+        asm volatile("" : "+v"(bu0), "+v"(bu1) : "v"(best0), "v"(best1));
+      }
+    }
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
       // full codeword index 16t + 4i + q into the low byte, then the minimum over q
+      double best = tt ? best1 : best0;
       unsigned long long bits = static_cast<unsigned long long>(__double_as_longlong(best));
       bits = (bits & ~0xffull) | ((bits & 0xffull) + static_cast<unsigned long long>(q));
       best = __longlong_as_double(static_cast<long long>(bits));
       best = fmin(best, __shfl_xor(best, 16, 64));
       best = fmin(best, __shfl_xor(best, 32, 64));
-      if (lane < 16) codes[16 * tt + lane][g] = static_cast<uint8_t>(__double_as_longlong(best) & 0xff);
+      const unsigned long long code = static_cast<unsigned long long>(__double_as_longlong(best)) & 0xffull;
+      code_acc[tt] = (code_acc[tt] >> 8) | (code << 56);  // byte GPW - 1 - (GPW - 1 - k) after the last group
     }
   }
-  __syncthreads();
-  for (int i = tid; i < nt * L; i += 256) {
-    const int t = i / L, ell = i % L;
-    const int pos = a.start_pos[b] + a.start_offset + n0 + t;
-    if (!position_in_pool(a.layout, pos)) continue;
-    const size_t off = code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos);
-    pool[off + ell] = codes[t][ell];
+  // lanes 0..15: the GPW codes of tokens lane and 16 + lane, one store each
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt) {
+    const int t = 16 * tt + lane;
+    if (lane < 16 && t < nt) {
+      const int pos = a.start_pos[b] + a.start_offset + n0 + t;
+      if (position_in_pool(a.layout, pos)) {
+        uint8_t *row = pool + code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos) + g0;
+        if constexpr (GPW == 8)
+          *reinterpret_cast<uint2 *>(row) = make_uint2(static_cast<uint32_t>(code_acc[tt]),
+                                                       static_cast<uint32_t>(code_acc[tt] >> 32));
+        else
+          *reinterpret_cast<uint32_t *>(row) = static_cast<uint32_t>(code_acc[tt] >> 32);
+      }
+    }
   }
 }
 
