@@ -36,6 +36,74 @@ __device__ __forceinline__ uint16_t input_bf16_bits(const EncodeArgs &a, const v
   return static_cast<uint16_t>((f + 0x7fffu + ((f >> 16) & 1u)) >> 16);
 }
 
+// Coordinate q of codeword idx (an index over [Hkv][L][256]): its address,
+// the coordinate as loaded from there (the fp16 bits, or the fp8 byte,
+// zero-extended), and its value.  Codeword idx + j lies j * 4 elements on.
+__device__ __forceinline__ const uint8_t *coordinate_ptr(const void *cb, const bool fp8, const size_t idx, const int q) {
+  return static_cast<const uint8_t *>(cb) + (4 * idx + q) * (fp8 ? 1 : 2);
+}
+__device__ __forceinline__ uint32_t coordinate_raw(const uint8_t *p, const bool fp8, const int j) {
+  if (fp8) return p[4 * j];
+  return reinterpret_cast<const uint16_t *>(p)[4 * j];
+}
+__device__ __forceinline__ double coordinate_value(const uint32_t raw, const bool fp8) {
+  if (fp8) {
+    typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+    const f16x2_t h = __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(raw, 1.0f, false);
+    return static_cast<double>(static_cast<float>(h[0]));
+  }
+  return static_cast<double>(half_bits_to_float(static_cast<uint16_t>(raw)));
+}
+
+// Cross-lane steps on doubles without LDS traffic (each 32-bit half moves on
+// its own).  row_dpp: DPP within 16-lane rows (quad_perm xor 1 = 0xB1, xor 2 =
+// 0x4E, row_half_mirror = 0x141, row_mirror = 0x140).  swap_rows: the
+// v_permlane{16,32}_swap of x (first operand) and y (second): R = 16
+// exchanges the odd rows of x with the even rows of y, R = 32 the high half
+// of x with the low half of y; the results are copied out of the returned
+// vectors before any reinterpretation.
+template <int CTRL>
+__device__ __forceinline__ double row_dpp(const double x) {
+  const unsigned long long u = static_cast<unsigned long long>(__double_as_longlong(x));
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(u), CTRL, 0xf, 0xf, true));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(u >> 32), CTRL, 0xf, 0xf, true));
+  return __longlong_as_double(static_cast<long long>((static_cast<unsigned long long>(hi) << 32) | lo));
+}
+template <int R>
+__device__ __forceinline__ void swap_rows(double &x, double &y) {
+  static_assert(R == 16 || R == 32, "row distance");
+  const unsigned long long ux = static_cast<unsigned long long>(__double_as_longlong(x));
+  const unsigned long long uy = static_cast<unsigned long long>(__double_as_longlong(y));
+  const uint32_t xl = static_cast<uint32_t>(ux), xh = static_cast<uint32_t>(ux >> 32);
+  const uint32_t yl = static_cast<uint32_t>(uy), yh = static_cast<uint32_t>(uy >> 32);
+  uint32_t l0, l1, h0, h1;
+  if constexpr (R == 16) {
+    const auto sl = __builtin_amdgcn_permlane16_swap(xl, yl, false, false);
+    const auto sh = __builtin_amdgcn_permlane16_swap(xh, yh, false, false);
+    l0 = sl[0], l1 = sl[1], h0 = sh[0], h1 = sh[1];
+  } else {
+    const auto sl = __builtin_amdgcn_permlane32_swap(xl, yl, false, false);
+    const auto sh = __builtin_amdgcn_permlane32_swap(xh, yh, false, false);
+    l0 = sl[0], l1 = sl[1], h0 = sh[0], h1 = sh[1];
+  }
+  x = __longlong_as_double(static_cast<long long>((static_cast<unsigned long long>(h0) << 32) | l0));
+  y = __longlong_as_double(static_cast<long long>((static_cast<unsigned long long>(h1) << 32) | l1));
+}
+// The largest x of the wave, in every lane (swapping x with a copy of itself
+// leaves x and the value of lane l ^ R in the two results).
+__device__ __forceinline__ double wave_max(double x) {
+  x = fmax(x, row_dpp<0xB1>(x));
+  x = fmax(x, row_dpp<0x4E>(x));
+  x = fmax(x, row_dpp<0x141>(x));
+  x = fmax(x, row_dpp<0x140>(x));
+  double y = x;
+  swap_rows<16>(x, y);
+  x = fmax(x, y);
+  y = x;
+  swap_rows<32>(x, y);
+  return fmax(x, y);
+}
+
 // Few new tokens per sequence (a decode step): one workgroup per (token,
 // sequence, KV head, side, block of 8 groups).  A block needs 32 transform
 // columns (D x 32 fp32) and its 8 codebooks (16 KB), so each workgroup
@@ -107,7 +175,7 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
   if ((tid & 31) == 0) pool[off + encblk::kGroups * blk + (tid >> 5)] = static_cast<uint8_t>(code);
 }
 
-// Bulk append: one workgroup (4 waves) per (32-token tile, KV head, sequence,
+// Bulk append: one workgroup (8 waves) per (64-token tile, KV head, sequence,
 // side), everything on the fp64 matrix cores.
 //  * transform: U = (X - k_bar) T with v_mfma_f64_16x16x4f64 (A = 16 tokens x 4
 //    input coordinates from LDS, B = 4 input x 16 output coordinates of T);
@@ -119,24 +187,38 @@ __global__ void __launch_bounds__(256) encode_small(EncodeArgs a) {
 //    (non-negative) fp64 value, so one min per score keeps the nearest
 //    codeword and, on equal values, the smallest index.  The truncation is
 //    2^-44 relative, far below the spacing of distinct distances.
-// Each wave owns a contiguous run of groups and both token tiles: every
-// codeword tile's C operand (norms from LDS) serves two MFMAs, the codes stay
-// in registers until one store per token, and the norms of half a codebook
-// at a time are staged.  That keeps the workgroup within 37 KB of LDS and
-// 128 VGPRs, so four of them share a CU.
+// On this part a SIMD does not run VALU work of one wave while it runs
+// matrix instructions of another, so the time is the matrix work plus the
+// VALU work.  Each wave therefore owns a contiguous run of groups for all
+// four 16-token tiles: every codeword tile's conversion and C operand (norms
+// from LDS) serve four MFMAs, and the per-group work (norms, offset) is
+// shared by 64 tokens.  The codes stay in registers until one store per
+// token, and the norms of half a codebook at a time are staged, so the
+// workgroup needs 73 KB of LDS and at most 128 VGPRs: two workgroups (four
+// waves per SIMD) share a CU.
 // LDS rows are padded by two doubles so the operand reads hit distinct banks.
 // Operand layout of v_mfma_f64_16x16x4f64 (measured): A[m][k] in lane 16k + m,
 // B[k][n] in lane 16k + n, D[m][n] in lane 16 (m mod 4) + n, register m / 4.
+constexpr int kBulkWaves = 8;
+constexpr int kBulkTokens = 64;
+
 template <int D, bool FP8, bool TBF>
-__global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
+__global__ void __launch_bounds__(64 * kBulkWaves) encode_bulk(EncodeArgs a) {
   constexpr int L = D / kGroupDim;
-  constexpr int TT = 32;                 // tokens per workgroup
+  constexpr int NW = kBulkWaves;
+  constexpr int NT = 64 * NW;            // threads
+  constexpr int TT = kBulkTokens;        // tokens per workgroup
+  constexpr int NTT = TT / 16;           // token tiles
   constexpr int RS = D + 2;              // LDS row stride (doubles)
   constexpr int OT = D / 16;             // output tiles of the transform
   constexpr int KS = D / 4;              // k-steps of the transform
+  constexpr int WPO = NW / OT;           // waves per output tile
+  constexpr int TPW = NTT / WPO;         // token tiles per wave in the transform
+  constexpr int GPW = L / NW;            // groups per wave in the search
+  static_assert(NW % OT == 0 && NTT % WPO == 0 && L % NW == 0, "tiling");
   typedef double double4_t __attribute__((ext_vector_type(4)));
   __shared__ double xs[TT * RS];         // inputs, then coefficients
-  __shared__ __attribute__((aligned(32))) double cn[4][kCodebookSize / 2];  // norms of half a codebook per wave
+  __shared__ __attribute__((aligned(32))) double cn[NW][kCodebookSize / 2];  // norms of half a codebook per wave
 
   const int tile = blockIdx.x, kv = blockIdx.y;
   const int b = blockIdx.z >> 1, side = blockIdx.z & 1;
@@ -152,23 +234,21 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   const void *src = side == 0 ? a.k : a.v;
   uint8_t *pool = side == 0 ? a.k_codes : a.v_codes;
 
-  // ---- transform operands: wave w computes output tiles w*OT/4 .. of both
-  // token tiles; its B operands (rows 4ks + q, columns of its tiles, of T)
-  // are requested first, so that their latency passes while the inputs are
-  // staged
+  // ---- transform operands: wave w computes output tile w mod OT of token
+  // tiles tt0 .. tt0 + TPW - 1; its B operands (rows 4ks + q, columns of its
+  // tile, of T) are requested first, so that their latency passes while the
+  // inputs are staged
   const int m = lane & 15, q = lane >> 4;
-  constexpr int OPW = OT / 4;
-  uint32_t tr[KS][OPW];  // as loaded (fp32 words, or zero-extended bf16)
+  const int ot = wave % OT, tt0 = (wave / OT) * TPW;
+  uint32_t tr[KS];  // as loaded (fp32 words, or zero-extended bf16)
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-    for (int j = 0; j < OPW; ++j) tr[ks][j] = load_t1_raw(tm, (4 * ks + q) * D + 16 * (wave * OPW + j) + m, TBF);
+  for (int ks = 0; ks < KS; ++ks) tr[ks] = load_t1_raw(tm, (4 * ks + q) * D + 16 * ot + m, TBF);
 
   // inputs (minus k_bar for keys) to LDS in fp64: thread tid stages
-  // coordinate tid mod D of tokens tid / D + k * (256 / D)
-  static_assert(256 % D == 0, "a thread stages one coordinate");
+  // coordinate tid mod D of tokens tid / D + k * (NT / D)
+  static_assert(NT % D == 0, "a thread stages one coordinate");
   {
-    constexpr int TP = 256 / D, NK = TT / TP;
+    constexpr int TP = NT / D, NK = TT / TP;
     const int d = tid % D, t0 = tid / D;
     const double kb = side == 0 ? static_cast<double>(a.kbar[kv * D + d]) : 0.0;
     const size_t row = static_cast<size_t>(a.num_kv_heads) * D;
@@ -197,30 +277,25 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
   }
   __syncthreads();
 
-  double4_t acc[2][OPW];
+  {
+    double4_t acc[TPW];
 #pragma unroll
-  for (int tt = 0; tt < 2; ++tt)
+    for (int j = 0; j < TPW; ++j) acc[j] = double4_t{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
-    for (int j = 0; j < OPW; ++j) acc[tt][j] = double4_t{0.0, 0.0, 0.0, 0.0};
+    for (int ks = 0; ks < KS; ++ks) {
+      const double bt = static_cast<double>(t1_raw_value(tr[ks], TBF));
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    double bt[OPW];
-#pragma unroll
-    for (int j = 0; j < OPW; ++j) bt[j] = static_cast<double>(t1_raw_value(tr[ks][j], TBF));
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      const double ax = xs[(16 * tt + m) * RS + 4 * ks + q];
-#pragma unroll
-      for (int j = 0; j < OPW; ++j) acc[tt][j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ax, bt[j], acc[tt][j], 0, 0, 0);
+      for (int j = 0; j < TPW; ++j) {
+        const double ax = xs[(16 * (tt0 + j) + m) * RS + 4 * ks + q];
+        acc[j] = __builtin_amdgcn_mfma_f64_16x16x4f64(ax, bt, acc[j], 0, 0, 0);
+      }
     }
+    __syncthreads();  // every wave has read its inputs; the coefficients overwrite them
+#pragma unroll
+    for (int j = 0; j < TPW; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) xs[(16 * (tt0 + j) + 4 * i + q) * RS + 16 * ot + m] = acc[j][i];
   }
-  __syncthreads();  // every wave has read its inputs; the coefficients overwrite them
-#pragma unroll
-  for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-    for (int j = 0; j < OPW; ++j)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) xs[(16 * tt + 4 * i + q) * RS + 16 * (wave * OPW + j) + m] = acc[tt][j][i];
   __syncthreads();
 
   if (side == 0 && a.k_scales) {
@@ -237,7 +312,7 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
       }
     }
     __syncthreads();
-    for (int i = tid; i < TT * D; i += 256) {
+    for (int i = tid; i < TT * D; i += NT) {
       const int t = i / D, d = i % D;
       const double rho = rhos[t];
       xs[t * RS + d] = rho > 0.0 ? xs[t * RS + d] / rho : 0.0;
@@ -245,23 +320,28 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
     __syncthreads();
   }
 
-  // ---- nearest codeword: wave w takes groups GPW*w .. GPW*w + GPW-1 and keeps
-  // their codes in registers; the codewords of its next group are requested
-  // tile by tile as the current group's are converted
-  constexpr int GPW = L / 4;
+  // ---- nearest codeword: wave w takes groups GPW*w .. GPW*w + GPW-1 of all
+  // token tiles and keeps their codes in registers; the codewords of its next
+  // group are requested tile by tile as the current group's are converted
   const int g0 = GPW * wave;
-  uint2 ra[16], rn[4];
+  uint32_t ra[16];  // coordinate q of codeword 16t + m, as loaded
+  uint2 rn[4];      // codewords 4 lane .. 4 lane + 3, for their norms
+  {
+    const size_t cw = cw0 + static_cast<size_t>(g0) * kCodebookSize;
+    const uint8_t *cp = coordinate_ptr(cb, fp8, cw + m, q);
 #pragma unroll
-  for (int t = 0; t < 16; ++t) ra[t] = codeword_raw(cb, fp8, cw0 + static_cast<size_t>(g0) * kCodebookSize + 16 * t + m);
+    for (int t = 0; t < 16; ++t) ra[t] = coordinate_raw(cp, fp8, 16 * t);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) rn[j] = codeword_raw(cb, fp8, cw0 + static_cast<size_t>(g0) * kCodebookSize + 4 * lane + j);
+    for (int j = 0; j < 4; ++j) rn[j] = codeword_raw(cb, fp8, cw + 4 * lane + j);
+  }
   uint32_t keep, idx0;
   asm volatile("v_mov_b32 %0, 0xffffff00" : "=v"(keep));
   asm volatile("s_mov_b32 %0, 0" : "=s"(idx0));
-  unsigned long long code_acc[2] = {0ull, 0ull};
+  uint32_t code_acc = 0u;  // codes of token lane
   for (int k = 0; k < GPW; ++k) {
     const int g = g0 + k;
     const size_t ncw = cw0 + static_cast<size_t>(min(g + 1, g0 + GPW - 1)) * kCodebookSize;
+    const uint8_t *ncp = coordinate_ptr(cb, fp8, ncw + m, q);
     double nc[4], cmax = 0.0;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -275,24 +355,25 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) rn[j] = codeword_raw(cb, fp8, ncw + 4 * lane + j);
+    // offset off_g = M (1 + 2^-39), M the larger of the tile's largest |u_g|^2
+    // (lane = token) and the group's largest |c|^2: off_g is at least every
+    // |u_g|^2, and the margin off_g - |u_g|^2 >= 2^-39 M exceeds the rounding
+    // of a score (a few ulp of a value below 4M)
     double un = 0.0;
-    if (lane < TT) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const double u = xs[lane * RS + 4 * g + i];
-        un = fma(u, u, un);
-      }
+    for (int i = 0; i < 4; ++i) {
+      const double u = xs[lane * RS + 4 * g + i];
+      un = fma(u, u, un);
     }
+    const double big = wave_max(fmax(un, cmax));
+    un = big + 0x1p-39 * big;
+    // B operands: -2 u (exact scaling), tokens 16 tt + m
+    double bu[NTT], best[NTT];
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      un = fmax(un, __shfl_xor(un, o, 64));
-      cmax = fmax(cmax, __shfl_xor(cmax, o, 64));
+    for (int tt = 0; tt < NTT; ++tt) {
+      bu[tt] = -2.0 * xs[(16 * tt + m) * RS + 4 * g + q];
+      best[tt] = __builtin_huge_val();
     }
-    un = un + 0x1p-40 * (un + cmax);
-    // B operands: -2 u (exact scaling), tokens m and 16 + m
-    double bu0 = -2.0 * xs[m * RS + 4 * g + q];
-    double bu1 = -2.0 * xs[(16 + m) * RS + 4 * g + q];
-    double best0 = __builtin_huge_val(), best1 = __builtin_huge_val();
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       // norms (+ offset) of codewords 128h .. 128h + 127, held by lanes 32h .. 32h + 31
@@ -307,71 +388,59 @@ __global__ void __launch_bounds__(256) encode_bulk(EncodeArgs a) {
       __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
       __builtin_amdgcn_wave_barrier();
       asm volatile("" ::: "memory");
-      // coordinate q of codeword 16t + m as the A operand; the register then
-      // receives the next group's codeword
-      auto conv = [&](const int t) -> double {
-        const uint2 w = codeword_f16(ra[t], fp8);
-        const uint32_t h2 = q < 2 ? w.x : w.y;
-        const double c = half_bits_to_float(static_cast<uint16_t>((q & 1) ? (h2 >> 16) : (h2 & 0xffffu)));
-        ra[t] = codeword_raw(cb, fp8, ncw + 16 * t + m);
-        return c;
-      };
-      double4_t cin = *reinterpret_cast<const double4_t *>(&cn[wave][4 * q]);
-      double ac = conv(8 * h);
-      double4_t n0 = __builtin_amdgcn_mfma_f64_16x16x4f64(ac, bu0, cin, 0, 0, 0);
-      double4_t n1 = __builtin_amdgcn_mfma_f64_16x16x4f64(ac, bu1, cin, 0, 0, 0);
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
         const int t = 8 * h + s;
-        const double4_t d0 = n0, d1 = n1;
-        if (s + 1 < 8) {
-          cin = *reinterpret_cast<const double4_t *>(&cn[wave][16 * (s + 1) + 4 * q]);
-          ac = conv(t + 1);
-          n0 = __builtin_amdgcn_mfma_f64_16x16x4f64(ac, bu0, cin, 0, 0, 0);
-          n1 = __builtin_amdgcn_mfma_f64_16x16x4f64(ac, bu1, cin, 0, 0, 0);
-        }
+        // A operand: coordinate q of codeword 16t + m; the register then
+        // receives the next group's codeword
+        const double ac = coordinate_value(ra[t], fp8);
+        ra[t] = coordinate_raw(ncp, fp8, 16 * t);
+        const double4_t cin = *reinterpret_cast<const double4_t *>(&cn[wave][16 * s + 4 * q]);
+        double4_t dd[NTT];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {  // register i = codeword 16t + 4i + q
-          const uint32_t idx = idx0 + static_cast<uint32_t>(16 * t + 4 * i);
-          const unsigned long long b0 = static_cast<unsigned long long>(__double_as_longlong(d0[i]));
-          const unsigned long long b1 = static_cast<unsigned long long>(__double_as_longlong(d1[i]));
-          best0 = fmin(best0, __longlong_as_double(static_cast<long long>(
-                                  (b0 & 0xffffffff00000000ull) | ((static_cast<uint32_t>(b0) & keep) | idx))));
-          best1 = fmin(best1, __longlong_as_double(static_cast<long long>(
-                                  (b1 & 0xffffffff00000000ull) | ((static_cast<uint32_t>(b1) & keep) | idx))));
-        }
-        // the MFMAs of tile t + 2 wait for these minima, so at most two
-        // tiles' results are held at once
-        asm volatile("" : "+v"(bu0), "+v"(bu1) : "v"(best0), "v"(best1));
+        for (int tt = 0; tt < NTT; ++tt) dd[tt] = __builtin_amdgcn_mfma_f64_16x16x4f64(ac, bu[tt], cin, 0, 0, 0);
+#pragma unroll
+        for (int tt = 0; tt < NTT; ++tt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {  // register i = codeword 16t + 4i + q
+            const uint32_t idx = idx0 + static_cast<uint32_t>(16 * t + 4 * i);
+            const unsigned long long bits = static_cast<unsigned long long>(__double_as_longlong(dd[tt][i]));
+            best[tt] = fmin(best[tt], __longlong_as_double(static_cast<long long>(
+                                          (bits & 0xffffffff00000000ull) | ((static_cast<uint32_t>(bits) & keep) | idx))));
+          }
+        // the next tile's MFMAs wait for these minima, so one tile's results
+        // are held at a time
+#pragma unroll
+        for (int tt = 0; tt < NTT; ++tt) asm volatile("" : "+v"(bu[tt]) : "v"(best[tt]));
       }
     }
+    // full codeword index 16t + 4i + q into the low byte (q fills its two
+    // low bits), then the minimum over the rows q, transposed: rows q and
+    // q ^ 1 leave tiles 0 and 2 to the even rows and 1 and 3 to the odd ones,
+    // rows q and q ^ 2 tiles 0 and 1 to the low half and 2 and 3 to the high
+    // half, so that lane 16q + m ends with tile q's minimum for token m: the
+    // code of token lane
+    static_assert(NTT == 4, "one token per lane");
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      // full codeword index 16t + 4i + q into the low byte, then the minimum over q
-      double best = tt ? best1 : best0;
-      unsigned long long bits = static_cast<unsigned long long>(__double_as_longlong(best));
-      bits = (bits & ~0xffull) | ((bits & 0xffull) + static_cast<unsigned long long>(q));
-      best = __longlong_as_double(static_cast<long long>(bits));
-      best = fmin(best, __shfl_xor(best, 16, 64));
-      best = fmin(best, __shfl_xor(best, 32, 64));
-      const unsigned long long code = static_cast<unsigned long long>(__double_as_longlong(best)) & 0xffull;
-      code_acc[tt] = (code_acc[tt] >> 8) | (code << 56);  // byte GPW - 1 - (GPW - 1 - k) after the last group
-    }
+    for (int tt = 0; tt < NTT; ++tt)
+      best[tt] = __longlong_as_double(__double_as_longlong(best[tt]) | static_cast<long long>(q));
+    swap_rows<16>(best[0], best[1]);
+    swap_rows<16>(best[2], best[3]);
+    double lo = fmin(best[0], best[1]), hi = fmin(best[2], best[3]);
+    swap_rows<32>(lo, hi);
+    const uint32_t code = static_cast<uint32_t>(__double_as_longlong(fmin(lo, hi))) & 0xffu;
+    code_acc = (code_acc >> 8) | (code << 24);  // group g0 + k ends in byte 4 - GPW + k
   }
-  // lanes 0..15: the GPW codes of tokens lane and 16 + lane, one store each
-#pragma unroll
-  for (int tt = 0; tt < 2; ++tt) {
-    const int t = 16 * tt + lane;
-    if (lane < 16 && t < nt) {
-      const int pos = a.start_pos[b] + a.start_offset + n0 + t;
-      if (position_in_pool(a.layout, pos)) {
-        uint8_t *row = pool + code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos) + g0;
-        if constexpr (GPW == 8)
-          *reinterpret_cast<uint2 *>(row) = make_uint2(static_cast<uint32_t>(code_acc[tt]),
-                                                       static_cast<uint32_t>(code_acc[tt] >> 32));
-        else
-          *reinterpret_cast<uint32_t *>(row) = static_cast<uint32_t>(code_acc[tt] >> 32);
-      }
+  // the GPW codes of token lane, one store
+  if (lane < nt) {
+    const int pos = a.start_pos[b] + a.start_offset + n0 + lane;
+    if (position_in_pool(a.layout, pos)) {
+      uint8_t *row = pool + code_row_offset(a.layout, a.num_kv_heads, L, b, kv, pos) + g0;
+      static_assert(GPW == 4 || GPW == 2, "code store width");
+      if constexpr (GPW == 4)
+        *reinterpret_cast<uint32_t *>(row) = code_acc;
+      else
+        *reinterpret_cast<uint16_t *>(row) = static_cast<uint16_t>(code_acc >> 16);
     }
   }
 }
@@ -426,11 +495,11 @@ hipError_t launch_encode_t(const EncodeArgs &a, hipStream_t stream) {
     else
       encode_small<D, false, TBF><<<grid, dim3(256), 0, stream>>>(a);
   } else {
-    const dim3 grid((a.n_new + 31) / 32, a.num_kv_heads, 2 * a.batch);
+    const dim3 grid((a.n_new + kBulkTokens - 1) / kBulkTokens, a.num_kv_heads, 2 * a.batch);
     if (a.cb_fp8)
-      encode_bulk<D, true, TBF><<<grid, dim3(256), 0, stream>>>(a);
+      encode_bulk<D, true, TBF><<<grid, dim3(64 * kBulkWaves), 0, stream>>>(a);
     else
-      encode_bulk<D, false, TBF><<<grid, dim3(256), 0, stream>>>(a);
+      encode_bulk<D, false, TBF><<<grid, dim3(64 * kBulkWaves), 0, stream>>>(a);
   }
   return hipGetLastError();
 }
