@@ -56,6 +56,7 @@ constexpr uint32_t kAuxCtl = kAuxQ + 4 * kD * 4;
 // control words: [0] arrival state, [1] next unclaimed round, [4..8) shifted
 // sink logits, [8..16) own (m, l) per head
 constexpr uint32_t kTeamCtr = kAuxCtl + 64;        // arrivals of the encoder team's waves
+constexpr uint32_t kTableCtr = kTeamCtr + 4;       // arrivals of the table waves (two per wave when built)
 constexpr uint32_t kItemRes = kTeamCtr + 16;       // [8 items][32] f32
 // A region used in turn by the partial sums of q' (setup, [8 parts][4 heads]
 // [128] f32), the encoder team's scratch (fused step, early in the loop) and
@@ -63,15 +64,18 @@ constexpr uint32_t kItemRes = kTeamCtr + 16;       // [8 items][32] f32
 // other waves still read both tables).
 constexpr uint32_t kMergeBase = (kItemRes + 8 * 32 * 4 + 255) & ~255u;
 constexpr uint32_t kAuxPart = kMergeBase;
-constexpr uint32_t kAppendScratch = kMergeBase;
+// The encoder team's scratch sits past the q' partial sums (16 KiB), so the
+// team can encode while the table waves still read those.
+constexpr uint32_t kAppendScratch = kMergeBase + 16384;
 constexpr uint32_t kLdsBytes = kMergeBase + 12 * kMergeFloats * 4;
 // Once every wave has left the loop, the value-codebook region holds the
 // split's own merged partial ([4][128] at kAuxOwn) and the combine's partial
 // outputs.
 constexpr uint32_t kAuxOwn = kVBase;
 constexpr uint32_t kAuxOut = kVBase + 4 * kD * 4;
-static_assert(32 * kD * 4 <= 12 * kMergeFloats * 4 && sizeof(step::Scratch<kD>) <= 12 * kMergeFloats * 4,
-              "the q' partial sums and the encoder team's scratch fit in the merge region");
+static_assert(32 * kD * 4 <= 16384 && 16384 + sizeof(step::Scratch<kD>) <= 12 * kMergeFloats * 4 &&
+                  16384 + 2 * sizeof(encblk::Scratch<kD>) <= 12 * kMergeFloats * 4,
+              "the q' partial sums and, past them, the encoder team's scratch fit in the merge region");
 static_assert(kLdsBytes <= 160 * 1024, "LDS budget of a workgroup");
 constexpr float kLn2 = 0.693147180559945309f;
 
@@ -155,6 +159,14 @@ __device__ __forceinline__ void team_sync(uint8_t *smem, const int phase) {
   step::team_meet(reinterpret_cast<int *>(smem + kTeamCtr), phase);
 }
 
+// The eight table waves arrive, then each continues once all eight have
+// (8 * phase arrivals): LDS writes before the call are visible after it.
+__device__ __forceinline__ void table_meet(int *ctr, const int phase) {
+  if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(ctr, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+  while (__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 8 * phase)
+    __builtin_amdgcn_s_sleep(1);
+}
+
 // The loads of the team's k-th item (thread t = tid - 512 of the team).
 struct ItemRegs {
   T4 trow[kD / 32];
@@ -201,12 +213,10 @@ __device__ __forceinline__ int team_phases(const int split, const int n_eff) {
   return 2 * items_of_split(split, n_eff) + 1;
 }
 
-// Called by the team's threads only (t = tid - 512), once the tables are
-// built.  Each item requests its loads when it starts.  (Requesting the
-// first item's during the setup kept 34 registers live across the table
-// build: the fp8 step spilled, and both steps ran 0.4-1 us slower.)
-// Items alternate between two scratch areas, so no meeting guards their
-// reuse.  The
+// Called by the team's threads only (t = tid - 512) while the table waves
+// build the tables (the key blocks wait for them, counter tctr, before their
+// table lookups).  Each item requests its loads when it starts.  Items
+// alternate between two scratch areas, so no meeting guards their reuse.  The
 // thread that found a group's codeword records its per-group result: a key
 // block's partial logits of the 8 groups per head (table entries of the
 // stored codes, res[32 k + 4 gg + h]), a value block's coordinates
@@ -215,7 +225,7 @@ __device__ __forceinline__ int team_phases(const int split, const int n_eff) {
 template <bool TBF>
 __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem, const int b, const int kv,
                                              const int split, const int n_eff, const size_t tokoff, const int t,
-                                             const bool fp8) {
+                                             const bool fp8, int *tctr) {
   encblk::Scratch<kD> *sc = reinterpret_cast<encblk::Scratch<kD> *>(smem + kAppendScratch);  // [2]
   float *res = reinterpret_cast<float *>(smem + kItemRes);
   uint64_t *xn = a.xnew + static_cast<size_t>(b * a.num_kv_heads + kv) * 8 * 32;
@@ -237,6 +247,9 @@ __device__ __forceinline__ void encode_items(const DecodeArgs &a, uint8_t *smem,
     if (lr < 4) {
       float v;
       if (side == 0) {
+        // the key tables: built by the table waves meanwhile
+        while (__hip_atomic_load(tctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 16)
+          __builtin_amdgcn_s_sleep(1);
         v = lr < G ? static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + code * 256 + g * 8 + 2 * lr)) : 0.f;
       } else {
         v = static_cast<float>(*reinterpret_cast<const _Float16 *>(smem + kVBase + (g & 7) * 8192 + 32 * code +
@@ -341,9 +354,10 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
   uint2 kwb[2][4], vwb[2][4];
   uint32_t ksb[2] = {0u, 0u}, vqb[2] = {0u, 0u};
   int *rctr = reinterpret_cast<int *>(smem + kAuxCtl) + 1;
-  if (tid == 0) *rctr = WAVES;  // rounds 0 .. WAVES-1 are taken; visible after the setup's barriers
-  if constexpr (APPEND) {
-    if (tid == 0) *reinterpret_cast<int *>(smem + kTeamCtr) = 0;
+  if (tid == 0) {
+    *rctr = WAVES;  // rounds 0 .. WAVES-1 are taken; visible after the setup's barrier
+    *reinterpret_cast<int *>(smem + kTableCtr) = 0;
+    if constexpr (APPEND) *reinterpret_cast<int *>(smem + kTeamCtr) = 0;
   }
 
   // ---- setup: value codebook into LDS, table of partial logits via MFMA.
@@ -437,111 +451,124 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       *reinterpret_cast<uint2 *>(smem + kVBase + (g & 7) * 8192 + (c << 5) + 8 * (g >> 3)) = e;
     }
     __syncthreads();
-    if (sh >= 0 && sh < G) {
-      const float dot = wave_sum(fmaf(qs[sh * kD + 2 * lane], kb2.x, qs[sh * kD + 2 * lane + 1] * kb2.y));
-      if (lane == 0) {
-        reinterpret_cast<float *>(smem + kAuxCtl)[4 + sh] = a.sinks ? a.sinks[kv * G + sh] - a.scale * dot : -INFINITY;
-        // q . k_bar itself for the band's logits (a fused step without a band
-        // keeps its encoder results in this region)
-        if constexpr (!APPEND || BSTEP) reinterpret_cast<float *>(smem + kItemRes)[sh] = dot;
-      }
-    }
-    if (tid < 512) {
-      float4 acc[4];
-#pragma unroll
-      for (int hh = 0; hh < 4; ++hh) {
-        acc[hh] = make_float4(0.f, 0.f, 0.f, 0.f);
-        const float4 q0 = *reinterpret_cast<const float4 *>(qs + hh * kD + 8 * jq);
-        const float4 q1 = *reinterpret_cast<const float4 *>(qs + hh * kD + 8 * jq + 4);
-        const float qq[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
-#pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          const float4 tr = t4_value(trow[r], TBF);
-          acc[hh].x = fmaf(qq[r], tr.x, acc[hh].x);
-          acc[hh].y = fmaf(qq[r], tr.y, acc[hh].y);
-          acc[hh].z = fmaf(qq[r], tr.z, acc[hh].z);
-          acc[hh].w = fmaf(qq[r], tr.w, acc[hh].w);
+    // From here the encoder team (waves 8..11) and the table waves (0..7)
+    // run apart: the table waves meet through an LDS counter, not workgroup
+    // barriers, so the team's work (the sink logits; in a fused step the new
+    // token's encode, whose SIMD time then falls in the setup instead of the
+    // token loop) never holds up the tables, and the team waits for the
+    // tables only where it reads them.  Values live on one path only (the
+    // team's loads, or the rows of t_k_inv_t and the key codewords).
+    int *tctr = reinterpret_cast<int *>(smem + kTableCtr);
+    if (wave >= 8) {
+      if (sh < G) {
+        const float dot = wave_sum(fmaf(qs[sh * kD + 2 * lane], kb2.x, qs[sh * kD + 2 * lane + 1] * kb2.y));
+        if (lane == 0) {
+          reinterpret_cast<float *>(smem + kAuxCtl)[4 + sh] = a.sinks ? a.sinks[kv * G + sh] - a.scale * dot : -INFINITY;
+          // q . k_bar itself for the band's logits (a fused step without a band
+          // keeps its encoder results in this region)
+          if constexpr (!APPEND || BSTEP) reinterpret_cast<float *>(smem + kItemRes)[sh] = dot;
         }
       }
-      // lanes l and l + 32 hold rows of the same columns: fold them, one part per wave
-#pragma unroll
-      for (int hh = 0; hh < 4; ++hh) {
-        acc[hh].x = add_rows32(acc[hh].x);
-        acc[hh].y = add_rows32(acc[hh].y);
-        acc[hh].z = add_rows32(acc[hh].z);
-        acc[hh].w = add_rows32(acc[hh].w);
-        if (lane < 32) *reinterpret_cast<float4 *>(qsum + wave * 512 + e4 * 16 + hh * 4) = acc[hh];
-      }
-    }
-    __syncthreads();
-    if (lut_wave) {
-      float qv[4] = {0.f, 0.f, 0.f, 0.f};
-      if (lj < G) {
-#pragma unroll
-        for (int pp = 0; pp < 8; ++pp) {
-          const float4 x4 = *reinterpret_cast<const float4 *>(qsum + pp * 512 + lg * 16 + lj * 4);
-          qv[0] += x4.x; qv[1] += x4.y; qv[2] += x4.z; qv[3] += x4.w;
+      if constexpr (APPEND) {
+        if (n_eff > 0) {
+          const int p = S - 1;
+          const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
+          if constexpr (BSTEP) {
+            int phase = 0;  // shared by every copy of the meeting
+            auto meet = [&] { team_sync(smem, ++phase); };
+            step::encode_token<kD, KS, SQ, TBF>(a, *reinterpret_cast<step::Scratch<kD> *>(smem + kAppendScratch), b,
+                                                kv, split, n_eff, tokoff, tid - 512, FP8, meet);
+          } else {
+            encode_items<TBF>(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8, tctr);
+          }
         }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) qv[i] *= a.qscale;
       }
-      half4_t a_hi, a_lo;
+      // the token loop reads the tables
+      while (__hip_atomic_load(tctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 16) __builtin_amdgcn_s_sleep(1);
+    } else {
+      {  // tid < 512
+        float4 acc[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const _Float16 hi = static_cast<_Float16>(qv[i]);
-        a_hi[i] = hi;
-        a_lo[i] = static_cast<_Float16>(qv[i] - static_cast<float>(hi));
-      }
-      // After the MFMA of step t, lane 4b + j holds the 4 heads of (group
-      // 16*(wave&1) + b, code cbase + 4*((t + rot) & 15) + j); all 4 lanes of a
-      // block hit the bank pair of their group.  Two steps are exchanged across
-      // the wave halves first, so that each half-wave writes 16 groups x 2
-      // codes (2 lanes per bank pair instead of 4): lanes j < 2 keep groups
-      // b (< 8) in the first write and b + 8 in the second, lanes j >= 2 the
-      // reverse; the low half of the wave writes step t, the high half t + 1.
-      const int gA = 16 * (wave & 1) + ((lane >> 2) & 7), gB = gA + 8;
-      const bool lowj = lj < 2;
-      const int g1 = lowj ? gA : gB, g2 = lowj ? gB : gA;
+        for (int hh = 0; hh < 4; ++hh) {
+          acc[hh] = make_float4(0.f, 0.f, 0.f, 0.f);
+          const float4 q0 = *reinterpret_cast<const float4 *>(qs + hh * kD + 8 * jq);
+          const float4 q1 = *reinterpret_cast<const float4 *>(qs + hh * kD + 8 * jq + 4);
+          const float qq[8] = {q0.x, q0.y, q0.z, q0.w, q1.x, q1.y, q1.z, q1.w};
 #pragma unroll
-      for (int t = 0; t < 16; t += 2) {
-        uint2 o[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const half4_t bv = __builtin_bit_cast(half4_t, codeword_f16(kst[t + u], fp8));
-          float4_t c = {0.f, 0.f, 0.f, 0.f};
-          c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_hi, bv, c, 0, 0, 0);
-          c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_lo, bv, c, 0, 0, 0);
-          half4_t h;
-          h[0] = static_cast<_Float16>(c[0]);
-          h[1] = static_cast<_Float16>(c[1]);
-          h[2] = static_cast<_Float16>(c[2]);
-          h[3] = static_cast<_Float16>(c[3]);
-          o[u] = __builtin_bit_cast(uint2, h);
+          for (int r = 0; r < 8; ++r) {
+            const float4 tr = t4_value(trow[r], TBF);
+            acc[hh].x = fmaf(qq[r], tr.x, acc[hh].x);
+            acc[hh].y = fmaf(qq[r], tr.y, acc[hh].y);
+            acc[hh].z = fmaf(qq[r], tr.z, acc[hh].z);
+            acc[hh].w = fmaf(qq[r], tr.w, acc[hh].w);
+          }
         }
-        // x: group gA of this lane's step, y: group gB of it
-        const auto sx = __builtin_amdgcn_permlane32_swap(o[0].x, o[1].x, false, false);
-        const auto sy = __builtin_amdgcn_permlane32_swap(o[0].y, o[1].y, false, false);
-        const unsigned ax = sx[0], bx = sx[1], ay = sy[0], by = sy[1];
-        const uint2 wa = make_uint2(ax, ay), wb = make_uint2(bx, by);
-        const int code = cbase + 4 * ((t + (lane >> 5) + rot) & 15) + lj;
-        *reinterpret_cast<uint2 *>(smem + code * 256 + g1 * 8) = lowj ? wa : wb;
-        *reinterpret_cast<uint2 *>(smem + code * 256 + g2 * 8) = lowj ? wb : wa;
+        // lanes l and l + 32 hold rows of the same columns: fold them, one part per wave
+#pragma unroll
+        for (int hh = 0; hh < 4; ++hh) {
+          acc[hh].x = add_rows32(acc[hh].x);
+          acc[hh].y = add_rows32(acc[hh].y);
+          acc[hh].z = add_rows32(acc[hh].z);
+          acc[hh].w = add_rows32(acc[hh].w);
+          if (lane < 32) *reinterpret_cast<float4 *>(qsum + wave * 512 + e4 * 16 + hh * 4) = acc[hh];
+        }
       }
-    }
-  }
-  __syncthreads();
-  if constexpr (APPEND) {
-    static_assert(WAVES == 12, "the encoder team is waves 8..11");
-    if (n_eff > 0 && wave >= 8) {
-      const int p = S - 1;
-      const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
-      if constexpr (BSTEP) {
-        int phase = 0;  // shared by every copy of the meeting
-        auto meet = [&] { team_sync(smem, ++phase); };
-        step::encode_token<kD, KS, SQ, TBF>(a, *reinterpret_cast<step::Scratch<kD> *>(smem + kAppendScratch), b, kv,
-                                       split, n_eff, tokoff, tid - 512, FP8, meet);
-      } else
-        encode_items<TBF>(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8);
+      table_meet(tctr, 1);  // q' partial sums written
+      {  // a table wave
+        float qv[4] = {0.f, 0.f, 0.f, 0.f};
+        if (lj < G) {
+#pragma unroll
+          for (int pp = 0; pp < 8; ++pp) {
+            const float4 x4 = *reinterpret_cast<const float4 *>(qsum + pp * 512 + lg * 16 + lj * 4);
+            qv[0] += x4.x; qv[1] += x4.y; qv[2] += x4.z; qv[3] += x4.w;
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) qv[i] *= a.qscale;
+        }
+        half4_t a_hi, a_lo;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const _Float16 hi = static_cast<_Float16>(qv[i]);
+          a_hi[i] = hi;
+          a_lo[i] = static_cast<_Float16>(qv[i] - static_cast<float>(hi));
+        }
+        // After the MFMA of step t, lane 4b + j holds the 4 heads of (group
+        // 16*(wave&1) + b, code cbase + 4*((t + rot) & 15) + j); all 4 lanes of a
+        // block hit the bank pair of their group.  Two steps are exchanged across
+        // the wave halves first, so that each half-wave writes 16 groups x 2
+        // codes (2 lanes per bank pair instead of 4): lanes j < 2 keep groups
+        // b (< 8) in the first write and b + 8 in the second, lanes j >= 2 the
+        // reverse; the low half of the wave writes step t, the high half t + 1.
+        const int gA = 16 * (wave & 1) + ((lane >> 2) & 7), gB = gA + 8;
+        const bool lowj = lj < 2;
+        const int g1 = lowj ? gA : gB, g2 = lowj ? gB : gA;
+#pragma unroll
+        for (int t = 0; t < 16; t += 2) {
+          uint2 o[2];
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            const half4_t bv = __builtin_bit_cast(half4_t, codeword_f16(kst[t + u], fp8));
+            float4_t c = {0.f, 0.f, 0.f, 0.f};
+            c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_hi, bv, c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_4x4x4f16(a_lo, bv, c, 0, 0, 0);
+            half4_t h;
+            h[0] = static_cast<_Float16>(c[0]);
+            h[1] = static_cast<_Float16>(c[1]);
+            h[2] = static_cast<_Float16>(c[2]);
+            h[3] = static_cast<_Float16>(c[3]);
+            o[u] = __builtin_bit_cast(uint2, h);
+          }
+          // x: group gA of this lane's step, y: group gB of it
+          const auto sx = __builtin_amdgcn_permlane32_swap(o[0].x, o[1].x, false, false);
+          const auto sy = __builtin_amdgcn_permlane32_swap(o[0].y, o[1].y, false, false);
+          const unsigned ax = sx[0], bx = sx[1], ay = sy[0], by = sy[1];
+          const uint2 wa = make_uint2(ax, ay), wb = make_uint2(bx, by);
+          const int code = cbase + 4 * ((t + (lane >> 5) + rot) & 15) + lj;
+          *reinterpret_cast<uint2 *>(smem + code * 256 + g1 * 8) = lowj ? wa : wb;
+          *reinterpret_cast<uint2 *>(smem + code * 256 + g2 * 8) = lowj ? wb : wa;
+        }
+      }
+      table_meet(tctr, 2);  // tables built
     }
   }
 
