@@ -451,15 +451,9 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       *reinterpret_cast<uint2 *>(smem + kVBase + (g & 7) * 8192 + (c << 5) + 8 * (g >> 3)) = e;
     }
     __syncthreads();
-    // From here the encoder team (waves 8..11) and the table waves (0..7)
-    // run apart: the table waves meet through an LDS counter, not workgroup
-    // barriers, so the team's work (the sink logits; in a fused step the new
-    // token's encode, whose SIMD time then falls in the setup instead of the
-    // token loop) never holds up the tables, and the team waits for the
-    // tables only where it reads them.  Values live on one path only (the
-    // team's loads, or the rows of t_k_inv_t and the key codewords).
-    int *tctr = reinterpret_cast<int *>(smem + kTableCtr);
-    if (wave >= 8) {
+    // The sink logits (waves 8 .. 8+G-1), the partial sums of q' (waves
+    // 0..7) and the tables (waves 0..7).
+    auto sink_logits = [&] {
       if (sh < G) {
         const float dot = wave_sum(fmaf(qs[sh * kD + 2 * lane], kb2.x, qs[sh * kD + 2 * lane + 1] * kb2.y));
         if (lane == 0) {
@@ -469,23 +463,8 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
           if constexpr (!APPEND || BSTEP) reinterpret_cast<float *>(smem + kItemRes)[sh] = dot;
         }
       }
-      if constexpr (APPEND) {
-        if (n_eff > 0) {
-          const int p = S - 1;
-          const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
-          if constexpr (BSTEP) {
-            int phase = 0;  // shared by every copy of the meeting
-            auto meet = [&] { team_sync(smem, ++phase); };
-            step::encode_token<kD, KS, SQ, TBF>(a, *reinterpret_cast<step::Scratch<kD> *>(smem + kAppendScratch), b,
-                                                kv, split, n_eff, tokoff, tid - 512, FP8, meet);
-          } else {
-            encode_items<TBF>(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8, tctr);
-          }
-        }
-      }
-      // the token loop reads the tables
-      while (__hip_atomic_load(tctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 16) __builtin_amdgcn_s_sleep(1);
-    } else {
+    };
+    auto q_partials = [&] {
       {  // tid < 512
         float4 acc[4];
 #pragma unroll
@@ -513,7 +492,8 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
           if (lane < 32) *reinterpret_cast<float4 *>(qsum + wave * 512 + e4 * 16 + hh * 4) = acc[hh];
         }
       }
-      table_meet(tctr, 1);  // q' partial sums written
+    };
+    auto build_tables = [&] {
       {  // a table wave
         float qv[4] = {0.f, 0.f, 0.f, 0.f};
         if (lj < G) {
@@ -568,7 +548,52 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
           *reinterpret_cast<uint2 *>(smem + code * 256 + g2 * 8) = lowj ? wb : wa;
         }
       }
-      table_meet(tctr, 2);  // tables built
+    };
+    int *tctr = reinterpret_cast<int *>(smem + kTableCtr);
+    if constexpr (APPEND && !BSTEP) {
+      // In the fused step the encoder team (waves 8..11) and the table waves
+      // (0..7) run apart from here: the table waves meet through an LDS
+      // counter, not workgroup barriers, so the team's encode never holds up
+      // the tables, and the team waits for the tables only where it reads
+      // them.  Its fp64 arithmetic then takes SIMD time in the setup, where
+      // the SIMDs mostly wait for the parameter loads, instead of in the
+      // token loop.  Values live on one path only (the team's loads, or the
+      // rows of t_k_inv_t and the key codewords).
+      if (wave >= 8) {
+        if (sh < G) sink_logits();
+        if (n_eff > 0) {
+          const int p = S - 1;
+          const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
+          encode_items<TBF>(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8, tctr);
+        }
+        // the token loop reads the tables
+        while (__hip_atomic_load(tctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 16)
+          __builtin_amdgcn_s_sleep(1);
+      } else {
+        q_partials();
+        table_meet(tctr, 1);  // q' partial sums written
+        build_tables();
+        table_meet(tctr, 2);  // tables built
+      }
+    } else {
+      // (The plain decode keeps workgroup barriers: with the waves apart, its
+      // paged-cache decode at 32 x 32K tokens ran 26% slower.)
+      if (sh >= 0 && sh < G) sink_logits();
+      if (tid < 512) q_partials();
+      __syncthreads();
+      if (lut_wave) build_tables();
+      __syncthreads();
+    }
+  }
+  if constexpr (BSTEP) {
+    static_assert(WAVES == 12, "the encoder team is waves 8..11");
+    if (n_eff > 0 && wave >= 8) {
+      const int p = S - 1;
+      const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
+      int phase = 0;  // shared by every copy of the meeting
+      auto meet = [&] { team_sync(smem, ++phase); };
+      step::encode_token<kD, KS, SQ, TBF>(a, *reinterpret_cast<step::Scratch<kD> *>(smem + kAppendScratch), b, kv,
+                                     split, n_eff, tokoff, tid - 512, FP8, meet);
     }
   }
 
