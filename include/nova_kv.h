@@ -306,8 +306,9 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
  *     >= 1, at head_dim 128 or 64: the new token is the band's last row,
  *     stored in the launch and attended exactly from it, as the decode after
  *     the encode would;
- *   - head_dim 128, plain or fp8 codebooks, no band: the new token is
- *     attended from its codes (its term is added after the split combine
+ *   - head_dim 128, plain or fp8 codebooks, no band, when the planner splits
+ *     each (sequence, KV head) over more than one workgroup: the new token
+ *     is attended from its codes (its term is added after the split combine
  *     instead of inside a split).
  * Otherwise the one-token encode and the decode run one after the other on
  * the stream.
