@@ -141,10 +141,12 @@ constexpr int kSpinLimit = 1 << 20;
 // Fused step: this split's share of the new token's encode.  Item i =
 // side * 4 + block (blocks of 8 groups) is done by split i mod n_eff.  Waves
 // 8..11 (the encoder team, 256 threads) take this split's items one after the
-// other with the shared block encoder (encode_block.h), right after the
-// table is built, while waves 0..7 start the token loop (rounds are claimed
-// dynamically, so the team's waves simply take fewer).  The team synchronises
-// through an LDS arrival counter instead of workgroup barriers.  Each item
+// other with the shared block encoder (encode_block.h), from the end of the
+// value-codebook staging, while waves 0..7 build the tables and then start
+// the token loop (rounds are claimed dynamically, so the team's waves simply
+// take fewer).  The team synchronises through an LDS arrival counter instead
+// of workgroup barriers, and waits on the table waves' counter before it
+// reads the tables.  Each item
 // stores its codes at position p of the pools and leaves its contribution in
 // LDS: a key block the partial logits of its 8 groups for each head (table
 // entries of the stored codes, added in group order), a value block its 32
