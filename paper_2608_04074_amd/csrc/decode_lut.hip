@@ -552,7 +552,7 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       }
     };
     int *tctr = reinterpret_cast<int *>(smem + kTableCtr);
-    if constexpr (APPEND && !BSTEP) {
+    if constexpr (APPEND) {
       // In the fused step the encoder team (waves 8..11) and the table waves
       // (0..7) run apart from here: the table waves meet through an LDS
       // counter, not workgroup barriers, so the team's encode never holds up
@@ -560,13 +560,22 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       // them.  Its fp64 arithmetic then takes SIMD time in the setup, where
       // the SIMDs mostly wait for the parameter loads, instead of in the
       // token loop.  Values live on one path only (the team's loads, or the
-      // rows of t_k_inv_t and the key codewords).
+      // rows of t_k_inv_t and the key codewords).  The band step's encode
+      // reads no table (the new token's logit comes from the band), and its
+      // scratch lies past the q' partial sums.
       if (wave >= 8) {
         if (sh < G) sink_logits();
         if (n_eff > 0) {
           const int p = S - 1;
           const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
-          encode_items<TBF>(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8, tctr);
+          if constexpr (BSTEP) {
+            int phase = 0;  // shared by every copy of the meeting
+            auto meet = [&] { team_sync(smem, ++phase); };
+            step::encode_token<kD, KS, SQ, TBF>(a, *reinterpret_cast<step::Scratch<kD> *>(smem + kAppendScratch),
+                                                b, kv, split, n_eff, tokoff, tid - 512, FP8, meet);
+          } else {
+            encode_items<TBF>(a, smem, b, kv, split, n_eff, tokoff, tid - 512, FP8, tctr);
+          }
         }
         // the token loop reads the tables
         while (__hip_atomic_load(tctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 16)
@@ -585,17 +594,6 @@ __device__ __forceinline__ void split_pass(const DecodeArgs &a, uint8_t *smem, c
       __syncthreads();
       if (lut_wave) build_tables();
       __syncthreads();
-    }
-  }
-  if constexpr (BSTEP) {
-    static_assert(WAVES == 12, "the encoder team is waves 8..11");
-    if (n_eff > 0 && wave >= 8) {
-      const int p = S - 1;
-      const size_t tokoff = subtile_offset(a, b, kv, p & ~15, bs_shift) + static_cast<size_t>(p & 15) * kL;
-      int phase = 0;  // shared by every copy of the meeting
-      auto meet = [&] { team_sync(smem, ++phase); };
-      step::encode_token<kD, KS, SQ, TBF>(a, *reinterpret_cast<step::Scratch<kD> *>(smem + kAppendScratch), b, kv,
-                                     split, n_eff, tokoff, tid - 512, FP8, meet);
     }
   }
 
