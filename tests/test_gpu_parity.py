@@ -554,6 +554,49 @@ def test_shared_workspace_across_shapes(nk, qwen_small):
                 assert float(err.max()) <= 1e-4, (rep, i, fused, float(err.max()))
 
 
+def test_side_stream_temporaries(nk, qwen_small):
+    """Calls on a stream other than torch's current one, with the output and
+    the zeroed workspace left to the binding: those are created and filled on
+    the call's stream, so the kernel sees a filled workspace and the memory
+    is not handed to other streams' work while the kernel runs.  The default
+    stream meanwhile allocates and fills memory of the workspace's size; the
+    results must equal the same calls on the default stream."""
+    wl, params, P = qwen_small
+    B, cap = 4, 4096
+    lens = np.array([4096, 3001, 64, 1], dtype=np.int32)
+    ck, cv, kn, vn = _step_inputs(wl, B, cap, lens)
+    q = dev(synth.decode_queries(wl, 0, batch=B), torch.bfloat16)
+    kn_d, vn_d = dev(kn, torch.bfloat16), dev(vn, torch.bfloat16)
+    lay = nk.CacheLayout.contiguous(cap)
+    lens_d = dev(lens, torch.int32)
+    need = nk.decode_workspace_bytes(P, B, wl.num_q_heads, cap)
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    for fused in (False, True):
+        say(f"side stream fused={fused}: default-stream reference")
+        pk, pv = dev(ck, torch.uint8), dev(cv, torch.uint8)
+        if fused:
+            ref = nk.append_decode_attn(P, lay, kn_d, vn_d, q, pk, pv, lens_d, cap)
+        else:
+            ref = nk.decode_attn(P, lay, q, pk, pv, lens_d, cap)
+        torch.cuda.synchronize()
+        for rep in range(3):
+            say(f"side stream fused={fused} rep={rep}")
+            pk, pv = dev(ck, torch.uint8), dev(cv, torch.uint8)
+            side.wait_stream(main)  # the inputs were written on the default stream
+            if fused:
+                out = nk.append_decode_attn(P, lay, kn_d, vn_d, q, pk, pv, lens_d, cap, stream=side)
+            else:
+                out = nk.decode_attn(P, lay, q, pk, pv, lens_d, cap, stream=side)
+            junk = torch.full((need,), 0xFF, dtype=torch.uint8, device="cuda")  # default-stream allocation
+            main.wait_stream(side)
+            torch.cuda.synchronize()
+            del junk
+            assert torch.isfinite(out).all()
+            err = (out - ref).abs().amax(dim=-1) / ref.norm(dim=-1).clamp_min(1e-30)
+            assert float(err.max()) <= 1e-4, (fused, rep, float(err.max()))
+
+
 # ------------------------------------------------- full-size configurations
 
 def _full_decode(nk, wl, layer, params, units, window=0, batch=None, cap=None):
