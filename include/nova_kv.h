@@ -303,9 +303,10 @@ nova_kv_status nova_kv_decode_attn(const nova_kv_params *p, const nova_kv_layout
  * kernel launch, in which the workgroups that read the pools also encode the
  * new token and store what nova_kv_encode would:
  *   - any format (key scale, scalar value arm, fp8) with a band whose n_rec
- *     >= 1, at head_dim 128 or 64: the new token is the band's last row,
- *     stored in the launch and attended exactly from it, as the decode after
- *     the encode would;
+ *     >= 1, at head_dim 64, and at head_dim 128 on a contiguous cache or when
+ *     the planner splits each (sequence, KV head) over more than one
+ *     workgroup: the new token is the band's last row, stored in the launch
+ *     and attended exactly from it, as the decode after the encode would;
  *   - head_dim 128, plain or fp8 codebooks, no band, when the planner splits
  *     each (sequence, KV head) over more than one workgroup: the new token
  *     is attended from its codes (its term is added after the split combine

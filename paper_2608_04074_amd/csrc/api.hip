@@ -331,10 +331,14 @@ nova_kv_status append_step(const nova_kv_params *p, const nova_kv_layout *layout
   // from its codes, which the splits of a (sequence, KV head) encode between
   // them: with one split, one workgroup's encoder team would encode all 8
   // blocks while its token loop runs, and two launches are faster (B = 32,
-  // S = 32K: paged 133 us against 171 us in one launch).
+  // S = 32K: paged 133 us against 171 us in one launch).  The head_dim-128
+  // band step on a paged cache with one split per unit also runs as encode
+  // then decode (deployed format, B = 32, S = 32K: 166 us against 189 us in
+  // one launch; on a contiguous cache the one launch stays as fast).
   const bool scaled_format = (p->flags & (NOVA_KV_KEY_SCALE | NOVA_KV_SQ_VALUES)) != 0;
   const bool fused =
-      plan.use_lut && (band ? band->n_rec >= 1 : p->head_dim == 128 && !scaled_format && plan.n_split > 1);
+      plan.use_lut && (band ? band->n_rec >= 1 && (plan.n_split > 1 || !layout->block_table || p->head_dim != 128)
+                            : p->head_dim == 128 && !scaled_format && plan.n_split > 1);
   if (fused) {
     a.append = 1;
     a.k_new = k_new;

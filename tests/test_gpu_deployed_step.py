@@ -160,6 +160,19 @@ def test_step_paged_fp32_inputs(nk, fmt):
     run_both(nk, wl, P, fmt, [1, 333, 2048, 1000], 2048, window=700, paged_bs=16, new_dtype=torch.float32, seed=8)
 
 
+@pytest.mark.parametrize("paged_bs", [None, 16], ids=["contiguous", "paged16"])
+@pytest.mark.parametrize("fmt", ["band", "deployed"])
+def test_step_one_split_per_unit(nk, fmt, paged_bs):
+    """32 sequences x 8 KV heads fill the 256 workgroups with one split per
+    (sequence, KV head): the contiguous step stays one launch, the paged one
+    runs as encode then decode; both store the encoder's bytes and give the
+    decode's output."""
+    wl = synth.get_workload("qwen3_8b")
+    _, P = format_params(nk, wl, fmt)
+    lens = [1024, 1, 333, 1023, 700, 64, 512, 999] * 4
+    run_both(nk, wl, P, fmt, lens, 1024, paged_bs=paged_bs, seed=11)
+
+
 @pytest.mark.parametrize("fmt", ["band", "deployed"])
 def test_step_with_sinks_only(nk, fmt):
     """A band of sink positions only (n_rec = 0): the new token is read from
